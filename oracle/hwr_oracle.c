@@ -1,0 +1,183 @@
+/*
+ * CPU oracle for HW-Router's routing-score path.  TEST INFRASTRUCTURE ONLY
+ * (tests, smoke check, CPU-baseline leg of the benchmark); no product code
+ * links or calls it.  Plain loops, one candidate at a time, fp64 accumulation.
+ *
+ * Readings of the paper used here (the paper fixes none of these numbers):
+ *  - Feature vector (Eq. 1 says: query features, one-hot model/GPU identifiers
+ *    and the runtime signals S_i of Table 2, concatenated).  With
+ *    A = arch_width, Gw = gpu_width, b = A + Gw:
+ *      x[model_arch[m]] = 1, x[A + gpu] = 1,
+ *      x[b+0] = ln(params_B)/4,   x[b+1] = ln(input_len)/8,
+ *      x[b+2] = ln(1+running)/2,  x[b+3] = ln(1+waiting)/2,
+ *      x[b+4] = kv_util,          x[b+5] = gpu_util,
+ *      x[b+6] = ln(ttft_avg_s)/4, x[b+7] = ln(tpot_avg_s)/4, rest 0.
+ *    Each value is computed in fp64 and rounded to fp32 (then bf16).
+ *  - Predictor (Eq. 1: two hidden ReLU layers): h1 = ReLU(W1^T x + b1),
+ *    h2 = ReLU(W2^T h1 + b2), z = W3^T h2 + b3, TTFT = softplus(z0),
+ *    TPOT = softplus(z1).  Each layer output is accumulated in fp64, rounded
+ *    to fp32, and (bf16 workloads) h1, h2 are rounded to bf16.
+ *  - Cost (Eq. 2) with the output length given per query:
+ *    C = TTFT + N_out * TPOT, one fp32 rounding.
+ *  - Quality (Sec. 3.2 item 3, hardware-independent): Q = e . Wq[:, m] + bq[m].
+ *  - Decision (Sec. 3.1 score, Eq. 3): utility u = Q - alpha * C / SLO in fp32
+ *    (alpha = 0.5 is the paper's score with lambda = 1/3 and C normalised by
+ *    the bound, scaled by 2/3: the argmax is the same); a pair is feasible iff
+ *    C <= SLO; choose the feasible pair with the largest u, ties to the lowest
+ *    pair index; if no pair is feasible, the largest u over all pairs.
+ */
+#include "hwr_oracle.h"
+
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* Round-to-nearest-even onto the bf16 grid (8 significand bits), from the
+ * definition: keep the top 16 bits of the fp32 pattern; add one unit in the
+ * last kept place when the dropped half is above one half, or exactly one half
+ * with an odd kept part. */
+float orc_bf16(float x) {
+    uint32_t u;
+    memcpy(&u, &x, 4);
+    if ((u & 0x7F800000u) == 0x7F800000u) {          /* inf or NaN */
+        if (u & 0x007FFFFFu) u |= 0x00400000u;       /* stay NaN   */
+        u &= 0xFFFF0000u;
+    } else {
+        uint32_t kept = u >> 16, dropped = u & 0xFFFFu;
+        if (dropped > 0x8000u || (dropped == 0x8000u && (kept & 1u))) kept += 1u;
+        u = kept << 16;
+    }
+    float y;
+    memcpy(&y, &u, 4);
+    return y;
+}
+
+void orc_bf16_n(const float *x, float *y, int64_t n) {
+    for (int64_t i = 0; i < n; ++i) y[i] = orc_bf16(x[i]);
+}
+
+float orc_softplus(float z) {
+    double v = (double)z;
+    double r = (v > 0.0 ? v : 0.0) + log1p(exp(-fabs(v)));
+    return (float)r;
+}
+
+static float store(const orc_problem *p, double v) {
+    float f = (float)v;
+    return p->bf16 ? orc_bf16(f) : f;
+}
+
+void orc_features(const orc_problem *p, const orc_state *s, int32_t d,
+                  int32_t input_len, float *x) {
+    const int32_t m = p->dep_model[d];
+    const int32_t A = p->arch_width, b = p->arch_width + p->gpu_width;
+    for (int32_t f = 0; f < p->F; ++f) x[f] = 0.0f;
+    x[p->model_arch[m]] = 1.0f;
+    x[A + p->dep_gpu[d]] = 1.0f;
+    x[b + 0] = store(p, log((double)p->model_params_b[m]) / 4.0);
+    x[b + 1] = store(p, log((double)input_len) / 8.0);
+    x[b + 2] = store(p, log(1.0 + (double)s->running_q[d]) / 2.0);
+    x[b + 3] = store(p, log(1.0 + (double)s->waiting_q[d]) / 2.0);
+    x[b + 4] = store(p, (double)s->kv_util[d]);
+    x[b + 5] = store(p, (double)s->gpu_util[d]);
+    x[b + 6] = store(p, log((double)s->ttft_avg_s[d]) / 4.0);
+    x[b + 7] = store(p, log((double)s->tpot_avg_s[d]) / 4.0);
+}
+
+float orc_quality(const orc_problem *p, const float *emb_row, int32_t m) {
+    double acc = 0.0;
+    for (int32_t k = 0; k < p->D; ++k)
+        acc += (double)emb_row[k] * (double)p->wq[(size_t)k * p->M + m];
+    return (float)(acc + (double)p->bq[m]);
+}
+
+void orc_mlp(const orc_problem *p, const float *x, float *z) {
+    const int32_t F = p->F, H = p->H;
+    float *h1 = (float *)malloc(sizeof(float) * (size_t)H);
+    float *h2 = (float *)malloc(sizeof(float) * (size_t)H);
+    for (int32_t j = 0; j < H; ++j) {
+        double acc = 0.0;
+        for (int32_t f = 0; f < F; ++f)
+            acc += (double)p->w1[(size_t)f * H + j] * (double)x[f];
+        float a = (float)(acc + (double)p->b1[j]);
+        h1[j] = store(p, a > 0.0f ? a : 0.0f);
+    }
+    for (int32_t j = 0; j < H; ++j) {
+        double acc = 0.0;
+        for (int32_t i = 0; i < H; ++i)
+            acc += (double)p->w2[(size_t)i * H + j] * (double)h1[i];
+        float a = (float)(acc + (double)p->b2[j]);
+        h2[j] = store(p, a > 0.0f ? a : 0.0f);
+    }
+    for (int32_t k = 0; k < 2; ++k) {
+        double acc = 0.0;
+        for (int32_t i = 0; i < H; ++i)
+            acc += (double)p->w3[(size_t)i * 2 + k] * (double)h2[i];
+        z[k] = (float)(acc + (double)p->b3[k]);
+    }
+    free(h1);
+    free(h2);
+}
+
+/* u in fp32: t = C / SLO, then u = Q - alpha * t, each operation rounded once
+ * (the file is built with contraction off); -0 -> +0, NaN -> -inf. */
+static float utility(float q, float alpha, float c, float slo) {
+    const float t = c / slo;
+    const float at = alpha * t;
+    float u = q - at;
+    if (u != u) u = -INFINITY;
+    if (u == 0.0f) u = 0.0f;
+    return u;
+}
+
+int orc_route(const orc_problem *p, const orc_state *s, const orc_queries *q,
+              orc_result *r) {
+    const int32_t N = p->N, M = p->M, F = p->F;
+    if (N <= 0 || M <= 0 || F <= 0 || p->H <= 0 || q->n < 0) return -1;
+    if (p->arch_width + p->gpu_width + 8 > F) return -1;
+    float *x = (float *)malloc(sizeof(float) * (size_t)F);
+    float *qual = (float *)malloc(sizeof(float) * (size_t)M);
+    for (int32_t iq = 0; iq < q->n; ++iq) {
+        const float *e = q->emb + (size_t)iq * p->D;
+        const float slo = q->slo_s[iq];
+        const float nout = (float)q->expected_out_len[iq];
+        for (int32_t m = 0; m < M; ++m) {
+            qual[m] = orc_quality(p, e, m);
+            if (r->quality) r->quality[(size_t)iq * M + m] = qual[m];
+        }
+        int32_t best = -1;
+        int best_f = 0;
+        float best_u = 0.0f, best_c = 0.0f, best_tt = 0.0f, best_tp = 0.0f;
+        for (int32_t d = 0; d < N; ++d) {
+            float z[2];
+            orc_features(p, s, d, q->input_len[iq], x);
+            orc_mlp(p, x, z);
+            const float ttft = orc_softplus(z[0]);
+            const float tpot = orc_softplus(z[1]);
+            const float c = fmaf(tpot, nout, ttft);
+            const int feas = (c <= slo);
+            const float u = utility(qual[p->dep_model[d]], p->alpha, c, slo);
+            const size_t ci = (size_t)iq * N + d;
+            if (r->cand_z) { r->cand_z[2 * ci] = z[0]; r->cand_z[2 * ci + 1] = z[1]; }
+            if (r->cand_ttft) r->cand_ttft[ci] = ttft;
+            if (r->cand_tpot) r->cand_tpot[ci] = tpot;
+            if (r->cand_e2e) r->cand_e2e[ci] = c;
+            if (r->cand_u) r->cand_u[ci] = u;
+            if (r->cand_feasible) r->cand_feasible[ci] = (uint8_t)feas;
+            /* lexicographic (feasible, u), earlier pair wins exact ties */
+            if (best < 0 || feas > best_f || (feas == best_f && u > best_u)) {
+                best = d; best_f = feas; best_u = u;
+                best_c = c; best_tt = ttft; best_tp = tpot;
+            }
+        }
+        if (r->choice) r->choice[iq] = best;
+        if (r->feasible) r->feasible[iq] = (uint8_t)best_f;
+        if (r->utility) r->utility[iq] = best_u;
+        if (r->e2e_s) r->e2e_s[iq] = best_c;
+        if (r->ttft_s) r->ttft_s[iq] = best_tt;
+        if (r->tpot_s) r->tpot_s[iq] = best_tp;
+    }
+    free(x);
+    free(qual);
+    return 0;
+}

@@ -1,0 +1,82 @@
+/*
+ * CPU oracle for HW-Router's batched routing-score path.  TEST INFRASTRUCTURE
+ * ONLY: the tests, the smoke check and the benchmark's CPU-baseline leg call
+ * it; the HIP library never does, and the two share no code.
+ *
+ * It computes, for every query x and every model-GPU pair i, literally and one
+ * candidate at a time:
+ *   - the feature vector feat(x, M_i, S_i)                     (Sec. 3.2, Eq. 1)
+ *   - the cost predictor f_cost -> TTFT_i(x), TPOT_i(x)        (Sec. 3.2, Eq. 1)
+ *   - the cost C_i(x) = TTFT_i(x) + N_out(x) * TPOT_i(x)       (Sec. 3.2, Eq. 2)
+ *   - the hardware-independent quality Q_i(x)                  (Sec. 3.2, item 3)
+ *   - the SLO-constrained argmax of the trade-off score        (Sec. 3.1; Eq. 3)
+ * Accumulation is in fp64; values are rounded to fp32 (and to bf16 where the
+ * workload stores bf16) at the points documented in hwr_oracle.c.
+ *
+ * Parity pins: see tests/test_oracle_pins.py (every function here is pinned).
+ */
+#ifndef HWR_ORACLE_H
+#define HWR_ORACLE_H
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct {
+    int32_t M, G, N, D, F, H;          /* models, GPU types, pairs, embed, feat, hidden */
+    int32_t arch_width, gpu_width;     /* one-hot widths                                 */
+    int32_t bf16;                      /* 1: round x, h1, h2 to bf16 before next layer  */
+    float   alpha;                     /* u = Q - alpha * C / SLO                        */
+    const int32_t *dep_model, *dep_gpu;     /* [N]                                   */
+    const int32_t *model_arch;              /* [M]                                   */
+    const float   *model_params_b;          /* [M] (billions)                        */
+    const float   *wq, *bq;                 /* [D*M] row-major [D][M], [M]           */
+    const float   *w1, *b1;                 /* [F*H] row-major [F][H], [H]           */
+    const float   *w2, *b2;                 /* [H*H] row-major [H_in][H_out], [H]    */
+    const float   *w3, *b3;                 /* [H*2] row-major [H][2], [2]           */
+} orc_problem;
+
+typedef struct {                            /* per pair, Table 2 + GPU utilisation  */
+    const int32_t *running_q, *waiting_q;
+    const float   *kv_util, *gpu_util, *ttft_avg_s, *tpot_avg_s;
+} orc_state;
+
+typedef struct {
+    int32_t n;
+    const float   *emb;                     /* [n*D]                                 */
+    const int32_t *input_len;               /* [n]                                   */
+    const int32_t *expected_out_len;        /* [n]                                   */
+    const float   *slo_s;                   /* [n]                                   */
+} orc_queries;
+
+typedef struct {                            /* any pointer may be NULL (not written) */
+    int32_t *choice;                        /* [n]                                   */
+    uint8_t *feasible;                      /* [n]                                   */
+    float   *utility, *e2e_s, *ttft_s, *tpot_s;   /* [n], of the chosen pair         */
+    float   *cand_z;                        /* [n*N*2] predictor outputs before softplus */
+    float   *cand_ttft, *cand_tpot, *cand_e2e, *cand_u;   /* [n*N]                   */
+    uint8_t *cand_feasible;                 /* [n*N]                                 */
+    float   *quality;                       /* [n*M]                                 */
+} orc_result;
+
+/* fp32 -> nearest bf16 value (ties to even), returned as fp32. */
+float orc_bf16(float x);
+void  orc_bf16_n(const float *x, float *y, int64_t n);
+/* softplus in fp64, rounded to fp32. */
+float orc_softplus(float z);
+/* feature vector of (query with input_len, pair d) into x[F]. */
+void  orc_features(const orc_problem *p, const orc_state *s, int32_t d,
+                   int32_t input_len, float *x);
+/* quality of model m for one embedding row. */
+float orc_quality(const orc_problem *p, const float *emb_row, int32_t m);
+/* predictor on one feature vector: z[2] before softplus. */
+void  orc_mlp(const orc_problem *p, const float *x, float *z);
+/* the whole path over a batch of queries.  Returns 0, or -1 on bad sizes. */
+int   orc_route(const orc_problem *p, const orc_state *s, const orc_queries *q,
+                orc_result *r);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

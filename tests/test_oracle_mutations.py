@@ -1,0 +1,53 @@
+"""The oracle pins must catch plausible mistakes: each case plants one mistake
+in a temporary copy of the oracle source (CPU only), rebuilds it, and expects
+the pin suite to fail against it."""
+import os
+import shutil
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "hwr_oracle.c")
+
+MUTATIONS = {
+    "swap_running_waiting": (
+        "x[b + 2] = store(p, log(1.0 + (double)s->running_q[d]) / 2.0);\n"
+        "    x[b + 3] = store(p, log(1.0 + (double)s->waiting_q[d]) / 2.0);",
+        "x[b + 3] = store(p, log(1.0 + (double)s->running_q[d]) / 2.0);\n"
+        "    x[b + 2] = store(p, log(1.0 + (double)s->waiting_q[d]) / 2.0);"),
+    "input_len_scale": ("log((double)input_len) / 8.0", "log((double)input_len) / 4.0"),
+    "w2_transposed": ("p->w2[(size_t)i * H + j]", "p->w2[(size_t)j * H + i]"),
+    "dropped_b2": ("float a = (float)(acc + (double)p->b2[j]);", "float a = (float)(acc);"),
+    "no_second_relu": ("h2[j] = store(p, a > 0.0f ? a : 0.0f);", "h2[j] = store(p, a);"),
+    "w3_heads_swapped": ("p->w3[(size_t)i * 2 + k]", "p->w3[(size_t)i * 2 + (1 - k)]"),
+    "cost_without_nout": ("fmaf(tpot, nout, ttft)", "(tpot + ttft)"),
+    "strict_bound": ("(c <= slo)", "(c < slo)"),
+    "utility_sign": ("float u = q - at;", "float u = q + at;"),
+    "ties_to_highest": ("(feas == best_f && u > best_u)", "(feas == best_f && u >= best_u)"),
+    "bound_ignored": ("feas > best_f || ", ""),
+    "wq_transposed": ("p->wq[(size_t)k * p->M + m]", "p->wq[(size_t)m * p->D + k]"),
+    "gpu_onehot_offset": ("x[A + p->dep_gpu[d]] = 1.0f;", "x[p->dep_gpu[d]] = 1.0f;"),
+    "bf16_truncates": (
+        "if (dropped > 0x8000u || (dropped == 0x8000u && (kept & 1u))) kept += 1u;", ""),
+    "softplus_sign": ("log1p(exp(-fabs(v)))", "log1p(exp(fabs(v)))"),
+    "wrong_model_of_pair": ("qual[p->dep_model[d]]", "qual[d % M]"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTATIONS))
+def test_pins_catch_planted_mistake(name, tmp_path):
+    src = open(SRC).read()
+    a, b = MUTATIONS[name]
+    assert a in src, "mutation anchor no longer in the oracle source"
+    (tmp_path / "hwr_oracle.c").write_text(src.replace(a, b))
+    shutil.copy(os.path.join(ROOT, "oracle", "hwr_oracle.h"), tmp_path / "hwr_oracle.h")
+    so = tmp_path / "liboracle.so"
+    subprocess.check_call(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-ffp-contract=off",
+                           "-o", str(so), str(tmp_path / "hwr_oracle.c"), "-lm"])
+    env = dict(os.environ, ORACLE_LIB_OVERRIDE=str(so))
+    r = subprocess.run([sys.executable, "-m", "pytest", os.path.join(ROOT, "tests", "test_oracle_pins.py"),
+                        "-q", "-x", "-p", "no:cacheprovider"], env=env, cwd=ROOT,
+                       capture_output=True, text=True, timeout=300)
+    assert r.returncode != 0, f"planted mistake {name!r} passed every pin:\n{r.stdout[-2000:]}"

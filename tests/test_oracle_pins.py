@@ -1,0 +1,348 @@
+"""Pins of the CPU oracle against facts fixed outside it: hand-computed closed
+forms, library routines the method reduces to in special cases, invariants of
+the decision rule (Sec. 3.1 score; Sec. 3.2 Eq. 1-3), and an independent
+brute force on tiny inputs.  CPU only."""
+import itertools
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as O
+from paper_2608_14575_amd import synth as S
+
+import bruteforce as BF
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _golden(name):
+    out = {}
+    with open(os.path.join(GOLD, name)) as f:
+        for line in f:
+            line = line.split("#", 1)[0].strip()
+            if line:
+                k, v = line.split()[:2]
+                out[k] = float(v)
+    return out
+
+
+def _state(**cols):
+    n = len(next(iter(cols.values())))
+    st = np.zeros(n, S.STATE_DTYPE)
+    defaults = dict(running_q=0, waiting_q=0, kv_util=0.0, gpu_util=0.0,
+                    ttft_avg_s=1.0, tpot_avg_s=1.0)
+    for k, v in defaults.items():
+        st[k] = cols.get(k, [v] * n)
+    return st
+
+
+def _p5_problem(M=2, H=64):
+    F = 24
+    w1 = np.zeros((F, H), np.float32)
+    w1[11, 0] = 1.0
+    w1[10, 1] = 1.0
+    w2 = np.zeros((H, H), np.float32)
+    w2[0, 0] = w2[1, 1] = 1.0
+    w3 = np.zeros((H, 2), np.float32)
+    w3[0, 0] = w3[1, 1] = 1.0
+    D = 8
+    return O.OracleProblem(
+        dep_model=np.arange(M, dtype=np.int32), dep_gpu=np.zeros(M, np.int32),
+        model_arch=np.zeros(M, np.int32), model_params_b=np.full(M, 7.0, np.float32),
+        wq=np.zeros((D, M), np.float32), bq=np.array([0.6, 0.7][:M], np.float32),
+        w1=w1, b1=np.zeros(H, np.float32), w2=w2, b2=np.zeros(H, np.float32),
+        w3=w3, b3=np.array([0.0, -5.0], np.float32),
+        arch_width=4, gpu_width=3, n_gpu_types=1, bf16=False, alpha=0.5)
+
+
+# ------------------------------------------------------------ rounding, softplus
+def test_bf16_rne_matches_torch():
+    rng = np.random.default_rng(0)
+    bits = rng.integers(0, 2**32, 1_000_000, dtype=np.uint64).astype(np.uint32)
+    # keep finite values; add exact ties (dropped half == 0x8000) with odd and even kept parts
+    x = bits.view(np.float32)
+    x = x[np.isfinite(x)]
+    ties = (rng.integers(0, 2**16, 20000, dtype=np.uint32) << 16) | np.uint32(0x8000)
+    ties = ties.view(np.float32)
+    ties = ties[np.isfinite(ties)]
+    sub = (rng.integers(1, 2**23, 20000, dtype=np.uint32)).view(np.float32)   # subnormals
+    allx = np.concatenate([x, ties, sub, np.array([0.0, -0.0, 1.0, 65504.0, 3.4e38], np.float32)])
+    ours = O.bf16_array(allx)
+    ref = torch.from_numpy(allx.copy()).to(torch.bfloat16).to(torch.float32).numpy()
+    assert np.array_equal(ours.view(np.uint32), ref.view(np.uint32))
+
+
+def test_softplus_closed_forms():
+    assert O.softplus(0.0) == np.float32(math.log(2.0))
+    assert O.softplus(math.log(math.e - 1.0)) == pytest.approx(1.0, rel=1e-7)
+    assert O.softplus(30.0) == np.float32(30.0)
+    assert O.softplus(-30.0) == pytest.approx(math.exp(-30.0), rel=1e-6)
+    # softplus(z) - softplus(-z) = z
+    for z in (-3.5, -0.25, 0.7, 4.0):
+        assert O.softplus(z) - O.softplus(-z) == pytest.approx(z, abs=1e-6)
+
+
+# ------------------------------------------------------------ features
+def test_features_hand_golden():
+    g = _golden("features_hand.txt")
+    F, H = 24, 8
+    prob = O.OracleProblem(
+        dep_model=np.array([0], np.int32), dep_gpu=np.array([1], np.int32),
+        model_arch=np.array([2], np.int32), model_params_b=np.array([7.0], np.float32),
+        wq=np.zeros((4, 1), np.float32), bq=np.zeros(1, np.float32),
+        w1=np.zeros((F, H), np.float32), b1=np.zeros(H, np.float32),
+        w2=np.zeros((H, H), np.float32), b2=np.zeros(H, np.float32),
+        w3=np.zeros((H, 2), np.float32), b3=np.zeros(2, np.float32),
+        arch_width=4, gpu_width=3, n_gpu_types=2, bf16=False)
+    st = _state(running_q=[3], waiting_q=[0], kv_util=[0.25], gpu_util=[0.75],
+                ttft_avg_s=[0.2], tpot_avg_s=[0.03])
+    x = O.features(prob, st, 0, 1000)
+    want = np.array([g[str(i)] for i in range(F)])
+    np.testing.assert_allclose(x, want, rtol=2e-7, atol=0)
+    # bf16 workloads round every feature to bf16 (an independent rounding: torch)
+    prob.bf16 = True
+    xb = O.features(prob, st, 0, 1000)
+    ref = torch.tensor(want, dtype=torch.float32).to(torch.bfloat16).to(torch.float32).numpy()
+    assert np.array_equal(xb, ref)
+
+
+# ------------------------------------------------------------ predictor
+def test_mlp_linear_regime_is_affine_chain():
+    """With non-negative weights, biases and inputs every ReLU is the
+    identity, so the predictor is W3^T(W2^T(W1^T x + b1) + b2) + b3: a chain
+    of library matrix products (a transposed or mis-indexed operand fails)."""
+    rng = np.random.default_rng(1)
+    F, H = 24, 48
+    w1 = rng.uniform(0, 0.3, (F, H)).astype(np.float32)
+    w2 = rng.uniform(0, 0.1, (H, H)).astype(np.float32)
+    w3 = rng.uniform(0, 0.1, (H, 2)).astype(np.float32)
+    b1 = rng.uniform(0, 0.2, H).astype(np.float32)
+    b2 = rng.uniform(0, 0.2, H).astype(np.float32)
+    b3 = np.array([0.3, -0.4], np.float32)
+    prob = O.OracleProblem(np.zeros(1, np.int32), np.zeros(1, np.int32), np.zeros(1, np.int32),
+                           np.ones(1, np.float32), np.zeros((4, 1), np.float32), np.zeros(1, np.float32),
+                           w1, b1, w2, b2, w3, b3, 4, 3, 1, False)
+    for _ in range(5):
+        x = rng.uniform(0, 1, F).astype(np.float32)
+        z = O.mlp(prob, x)
+        h1 = x.astype(np.float64) @ w1 + b1
+        h2 = h1 @ w2 + b2
+        zz = h2 @ w3 + b3
+        np.testing.assert_allclose(z, zz, rtol=3e-6)
+    # and W2 is not symmetric, so a transposed W2 would differ
+    assert not np.allclose(w2, w2.T)
+
+
+def test_mlp_relu_cuts_negative_units():
+    """A unit with negative pre-activation contributes nothing."""
+    F, H = 24, 8
+    w1 = np.zeros((F, H), np.float32)
+    w1[0, 0] = 1.0
+    w1[0, 1] = -1.0
+    w2 = np.zeros((H, H), np.float32)
+    w2[0, 0] = 2.0
+    w2[1, 1] = 5.0
+    w3 = np.zeros((H, 2), np.float32)
+    w3[0, 0] = 1.0
+    w3[1, 1] = 1.0
+    prob = O.OracleProblem(np.zeros(1, np.int32), np.zeros(1, np.int32), np.zeros(1, np.int32),
+                           np.ones(1, np.float32), np.zeros((4, 1), np.float32), np.zeros(1, np.float32),
+                           w1, np.zeros(H, np.float32), w2, np.array([0, -1] + [0] * 6, np.float32),
+                           w3, np.zeros(2, np.float32), 4, 3, 1, False)
+    x = np.zeros(F, np.float32)
+    x[0] = 0.75
+    z = O.mlp(prob, x)
+    assert z[0] == pytest.approx(1.5)       # 2 * relu(0.75)
+    assert z[1] == 0.0                      # relu(5 * relu(-0.75) - 1) = 0
+
+
+def test_two_candidate_hand_case():
+    g = _golden("p5_two_candidate.txt")
+    prob = _p5_problem()
+    st = _state(running_q=[0, 0], waiting_q=[0, 3], kv_util=[0.5, 0.0], gpu_util=[0.0, 0.0],
+                ttft_avg_s=[1.0, 1.0], tpot_avg_s=[1.0, 1.0])
+    emb = np.zeros((1, 8), np.float32)
+    for slo, want in ((2.0, 0), (2.1, 1)):
+        r = O.route(prob, st, emb, [100], [100], [slo])
+        np.testing.assert_allclose(r.cand_ttft[0], [g["ttft0"], g["ttft1"]], rtol=2e-7)
+        np.testing.assert_allclose(r.cand_tpot[0], [g["tpot0"], g["tpot1"]], rtol=2e-7)
+        np.testing.assert_allclose(r.cand_e2e[0], [g["e2e0"], g["e2e1"]], rtol=2e-7)
+        np.testing.assert_allclose(r.cand_u[0], [g[f"u0_slo{slo}"], g[f"u1_slo{slo}"]], rtol=1e-6)
+        assert r.choice[0] == want == int(g[f"choice_slo{slo}"])
+        assert r.feasible[0] == 1
+    # SLO = 2.0: the infeasible pair has the larger utility, and is still not chosen
+    r = O.route(prob, st, emb, [100], [100], [2.0])
+    assert r.cand_u[0, 1] > r.cand_u[0, 0] and r.cand_feasible[0].tolist() == [1, 0]
+
+
+# ------------------------------------------------------------ quality
+def test_quality_is_matrix_product():
+    rng = np.random.default_rng(2)
+    sp = S.custom_spec(n_models=5, n_gpu_types=2, embed_dim=96)
+    pb = S.make_problem(sp, 3)
+    st = S.make_state(sp, 3)
+    qs = S.make_queries(sp, 3, n=12)
+    r = O.route_synth(pb, st, qs)
+    want = qs.emb.astype(np.float64) @ pb.wq.astype(np.float64) + pb.bq
+    np.testing.assert_allclose(r.quality, want, rtol=1e-6, atol=1e-7)
+    assert rng is not None
+
+
+# ------------------------------------------------------------ decision rule
+def _synth_case(seed=5, **kw):
+    sp = S.custom_spec(**kw)
+    return sp, S.make_problem(sp, seed), S.make_state(sp, seed), S.make_queries(sp, seed)
+
+
+def test_alpha_zero_unbounded_is_quality_argmax():
+    """alpha = 0 and SLO = 1e30: the choice is argmax_d Q[q, model(d)], first
+    maximum (a gather plus numpy argmax)."""
+    sp, pb, st, qs = _synth_case(n_models=4, n_gpu_types=3, n_queries=40)
+    qs.slo_s[:] = 1e30
+    r = O.route_synth(pb, st, qs, alpha=0.0)
+    Q = qs.emb.astype(np.float64) @ pb.wq + pb.bq
+    want = np.argmax(Q[:, pb.dep_model], axis=1)
+    assert np.array_equal(r.choice, want)
+    assert r.feasible.all()
+
+
+def test_equal_quality_is_min_latency():
+    sp, pb, st, qs = _synth_case(n_models=3, n_gpu_types=3, n_queries=40)
+    pb.wq[:] = 0.0
+    pb.bq[:] = 0.5
+    r = O.route_synth(pb, st, qs)
+    e2e = np.where(r.cand_feasible.astype(bool), r.cand_e2e, np.inf)
+    anyf = r.cand_feasible.any(axis=1)
+    want = np.where(anyf, np.argmin(e2e, axis=1), np.argmin(r.cand_e2e, axis=1))
+    assert np.array_equal(r.choice, want)
+
+
+def test_all_infeasible_falls_back_to_best_utility():
+    sp, pb, st, qs = _synth_case(n_queries=30)
+    qs.slo_s[:] = 1e-6
+    r = O.route_synth(pb, st, qs)
+    assert not r.cand_feasible.any() and not r.feasible.any()
+    assert np.array_equal(r.choice, np.argmax(r.cand_u, axis=1))
+
+
+def test_single_pair():
+    sp, pb, st, qs = _synth_case(n_models=1, n_gpu_types=1, n_queries=10)
+    r = O.route_synth(pb, st, qs)
+    assert (r.choice == 0).all()
+
+
+def test_cost_composition_and_feasibility():
+    """Eq. 2: C = TTFT + N_out * TPOT (one fp32 rounding), feasible iff C <= SLO."""
+    sp, pb, st, qs = _synth_case(n_queries=50)
+    r = O.route_synth(pb, st, qs)
+    exact = r.cand_tpot.astype(np.float64) * qs.expected_out_len[:, None] + r.cand_ttft
+    assert np.array_equal(r.cand_e2e, exact.astype(np.float32))
+    assert np.array_equal(r.cand_feasible.astype(bool), r.cand_e2e <= qs.slo_s[:, None])
+    # u = Q - alpha C / SLO
+    Q = r.quality[:, pb.dep_model]
+    np.testing.assert_allclose(r.cand_u, Q - 0.5 * r.cand_e2e / qs.slo_s[:, None], rtol=0, atol=3e-7)
+
+
+def test_slo_invariant_overloaded_pairs():
+    """Whenever some pair is feasible, the chosen pair is feasible; per-query
+    SLOs from {0.5, 1, 2, 5} s with 20% overloaded pairs."""
+    sp = S.spec("C3", n_queries=48, n_models=4, n_gpu_types=4, embed_dim=64, hidden=32)
+    pb, st = S.make_problem(sp, 7), S.make_state(sp, 7)
+    qs = S.make_queries(sp, 7)
+    r = O.route_synth(pb, st, qs)
+    anyf = r.cand_feasible.any(axis=1)
+    assert anyf.any() and (~anyf).sum() >= 0
+    assert np.array_equal(r.feasible.astype(bool), anyf)
+    chosen_f = r.cand_feasible[np.arange(qs.n), r.choice]
+    assert (chosen_f[anyf] == 1).all()
+
+
+def test_paper_score_gives_same_choice():
+    """Sec. 3.1 score S = (1 - lambda) Q - lambda C'/B with lambda = 1/3 and C
+    normalised by the bound, argmax over feasible pairs (Eq. 3), equals the
+    choice under u = Q - 0.5 C / SLO."""
+    sp, pb, st, qs = _synth_case(n_models=4, n_gpu_types=2, n_queries=64)
+    r = O.route_synth(pb, st, qs)
+    lam = 1.0 / 3.0
+    Sc = (1 - lam) * r.quality[:, pb.dep_model].astype(np.float64) - lam * r.cand_e2e / qs.slo_s[:, None]
+    feas = r.cand_feasible.astype(bool)
+    Sm = np.where(feas | ~feas.any(axis=1, keepdims=True), Sc, -np.inf)
+    want = np.argmax(Sm, axis=1)
+    srt = np.sort(Sm, axis=1)
+    clear = (srt[:, -1] - srt[:, -2]) > 1e-6
+    assert np.array_equal(r.choice[clear], want[clear])
+
+
+def test_deployment_permutation_invariance():
+    sp, pb, st, qs = _synth_case(n_models=3, n_gpu_types=3, n_queries=40, seed=11)
+    r = O.route_synth(pb, st, qs)
+    perm = np.random.default_rng(0).permutation(pb.n_deployments)
+    pb2 = S.make_problem(sp, 11)
+    pb2.dep_model = pb.dep_model[perm].copy()
+    pb2.dep_gpu = pb.dep_gpu[perm].copy()
+    st2 = st[perm].copy()
+    r2 = O.route_synth(pb2, st2, qs)
+    assert np.array_equal(perm[r2.choice], r.choice)
+    # permuting queries permutes the outputs
+    qp = np.random.default_rng(1).permutation(qs.n)
+    r3 = O.route_synth(pb, st, qs.take(qp))
+    assert np.array_equal(r3.choice, r.choice[qp])
+
+
+def test_duplicate_pairs_tie_to_lowest_index():
+    sp, pb, st, qs = _synth_case(n_models=2, n_gpu_types=2, n_queries=30, seed=13)
+    # pairs 1 and 3 become exact copies of pair 0 / pair 2 (same model, GPU, state)
+    pb.dep_model[:] = [0, 0, 1, 1]
+    pb.dep_gpu[:] = [0, 0, 1, 1]
+    st[1] = st[0]
+    st[3] = st[2]
+    r = O.route_synth(pb, st, qs)
+    assert np.array_equal(r.cand_u[:, 0], r.cand_u[:, 1])
+    assert set(np.unique(r.choice)) <= {0, 2}
+
+
+def test_bound_equality_is_feasible():
+    """A pair whose cost equals the bound exactly is feasible (reading of the
+    bound as C <= SLO)."""
+    sp, pb, st, qs = _synth_case(n_queries=8)
+    r = O.route_synth(pb, st, qs)
+    qs.slo_s[:] = r.cand_e2e[:, 0]
+    r2 = O.route_synth(pb, st, qs)
+    assert (r2.cand_feasible[:, 0] == 1).all()
+    assert np.array_equal(r2.cand_feasible.astype(bool), r2.cand_e2e <= qs.slo_s[:, None])
+
+
+# ------------------------------------------------------------ brute force
+@pytest.mark.parametrize("dtype,seed", [("f32", 21), ("bf16", 22), ("bf16", 23)])
+def test_bruteforce_matches_oracle(dtype, seed):
+    sp = S.custom_spec(n_queries=6, n_models=3, n_gpu_types=2, embed_dim=8, hidden=8,
+                       dtype=dtype)
+    pb, st, qs = S.make_problem(sp, seed), S.make_state(sp, seed), S.make_queries(sp, seed)
+    r = O.route_synth(pb, st, qs)
+    ch, ranked = BF.route(*BF.from_synth(pb, st, qs))
+    for i in range(qs.n):
+        vals = sorted(ranked[i], key=lambda c: c[3]["d"])
+        np.testing.assert_allclose(r.cand_ttft[i], [c[3]["ttft"] for c in vals], rtol=1e-6)
+        np.testing.assert_allclose(r.cand_tpot[i], [c[3]["tpot"] for c in vals], rtol=1e-6)
+        np.testing.assert_allclose(r.cand_u[i], [c[3]["u"] for c in vals], rtol=0, atol=1e-6)
+        top, second = ranked[i][0], ranked[i][1]
+        if top[0] != second[0] or top[1] - second[1] > 1e-5:
+            assert r.choice[i] == ch[i]
+
+
+def test_bruteforce_all_pair_orders():
+    """All N! orders of 4 pairs: the chosen pair (by identity) never changes."""
+    sp = S.custom_spec(n_queries=3, n_models=2, n_gpu_types=2, embed_dim=8, hidden=8)
+    pb, st, qs = S.make_problem(sp, 31), S.make_state(sp, 31), S.make_queries(sp, 31)
+    base = O.route_synth(pb, st, qs)
+    for perm in itertools.permutations(range(4)):
+        perm = np.array(perm)
+        pb2 = S.make_problem(sp, 31)
+        pb2.dep_model, pb2.dep_gpu = pb.dep_model[perm].copy(), pb.dep_gpu[perm].copy()
+        r = O.route_synth(pb2, st[perm].copy(), qs)
+        assert np.array_equal(perm[r.choice], base.choice)
+        ch, _ = BF.route(*BF.from_synth(pb2, st[perm].copy(), qs))
+        assert np.array_equal(np.array(ch), r.choice)
