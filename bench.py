@@ -1,0 +1,236 @@
+"""Benchmark: batched routing-score evaluation on one MI355X.
+
+Step = one call of hwr_route_batch over the whole throughput workload
+(1,048,576 queries x 256 model-GPU pairs, 16 chunks of 65,536 queries on one
+stream, inputs resident in HBM).  Prints one JSON line with candidates
+scored per second, the roofline position of the dominant kernel (the fused
+predictor, MFMA-bound) measured with HIP events on the launch stream, the
+single-query latency path (p50 / p99 over 10,000 sequential calls with a
+state update between calls), and the CPU oracle timed on a bounded sample.
+
+    python bench.py [--gpus 1] [--steps 10] [--warmup 2]
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes as C
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "routing candidates scored/sec (query×deployment) at 1 MI355X; p50 1-query route µs"
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def predictor_flops(F: int, H: int) -> int:
+    """Algorithmic flops of the Eq. 1 predictor per candidate: 2(FH + H^2 + 2H)."""
+    return 2 * (F * H + H * H + 2 * H)
+
+
+def throughput(args, S, hwr, torch):
+    sp = S.spec(args.workload)
+    pb, st = S.make_problem(sp, args.seed), S.make_state(sp, args.seed)
+    n, N, M, D = sp.total_queries, sp.n_deployments, sp.n_models, sp.embed_dim
+    dev = torch.device("cuda:0")
+    emb = torch.empty((n, D), dtype=torch.int16, device=dev)
+    il = torch.empty(n, dtype=torch.int32, device=dev)
+    no = torch.empty(n, dtype=torch.int32, device=dev)
+    slo = torch.empty(n, dtype=torch.float32, device=dev)
+    sample = None
+    for c in range(sp.n_chunks):
+        qs = S.make_queries(sp, args.seed, chunk=c)
+        a, b = c * sp.n_queries, (c + 1) * sp.n_queries
+        emb[a:b] = torch.from_numpy(qs.emb_bits.view(np.int16)).to(dev)
+        il[a:b] = torch.from_numpy(qs.input_len).to(dev)
+        no[a:b] = torch.from_numpy(qs.expected_out_len).to(dev)
+        slo[a:b] = torch.from_numpy(qs.slo_s).to(dev)
+        if c == 0:
+            sample = qs.slice(0, args.cpu_sample)
+        log(f"generated chunk {c + 1}/{sp.n_chunks}")
+    stream = torch.cuda.current_stream()
+    r = hwr.Router.from_problem(pb, max_chunk=sp.n_queries, pipeline=args.pipeline,
+                                stream=int(stream.cuda_stream))
+    r.update(st)
+    out = dict(choice=torch.empty(n, dtype=torch.int32, device=dev),
+               feasible=torch.empty(n, dtype=torch.uint8, device=dev),
+               utility=torch.empty(n, dtype=torch.float32, device=dev),
+               e2e_s=torch.empty(n, dtype=torch.float32, device=dev),
+               ttft_s=torch.empty(n, dtype=torch.float32, device=dev),
+               tpot_s=torch.empty(n, dtype=torch.float32, device=dev))
+
+    def step():
+        r.route(emb, il, no, slo, mem=hwr.HWR_MEM_DEVICE, **out)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"warmup done ({args.warmup} steps)")
+    r.profile(True)
+    r.profile_read(reset=True)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    kt = r.profile_read(reset=True)
+    r.profile(False)
+    gpu_ms = e0.elapsed_time(e1)
+    log(f"timed {args.steps} steps: {gpu_ms:.2f} ms (events), {wall * 1e3:.2f} ms (host)")
+    choice = out["choice"].cpu().numpy()
+    assert (choice >= 0).all() and (choice < N).all(), "choice out of range"
+    ms_step = max(gpu_ms, wall * 1e3) / args.steps
+    value = n * N / (ms_step / 1e3)
+
+    kname = "fused" if args.pipeline == "fused" else "mlp"
+    k_ms, k_n = kt[kname]
+    k_avg_ms = k_ms / max(k_n, 1)
+    chunk_cands = sp.n_queries * N
+    flops = predictor_flops(sp.feat_dim, sp.hidden) * chunk_cands
+    achieved = flops / (k_avg_ms / 1e3) / 1e12
+    q_ms, q_n = kt["quality"]
+    q_avg = q_ms / max(q_n, 1)
+    q_bytes = sp.n_queries * (D * 2 + M * 4) + D * 32 * 2
+    stages = {k: {"avg_ms": (v[0] / v[1]) if v[1] else 0.0, "launches_per_step": v[1] / args.steps}
+              for k, v in kt.items() if v[1]}
+    res = dict(
+        value=value, ms_per_step=ms_step,
+        roofline={"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                  "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                  "kernel": f"k_mlp_bf16<{sp.hidden}> ({args.pipeline})",
+                  "flop_per_launch": flops, "avg_launch_ms": k_avg_ms},
+        quality_roofline={"bound": "hbm", "achieved": q_bytes / (q_avg / 1e3) / 1e9, "peak": PEAK_HBM_GBS,
+                          "unit": "GB/s", "frac": q_bytes / (q_avg / 1e3) / 1e9 / PEAK_HBM_GBS,
+                          "bytes_per_launch": q_bytes, "avg_launch_ms": q_avg},
+        stages=stages,
+        config={"workload": f"{sp.name} throughput stress: {n} queries x {N} pairs ({M} models x "
+                            f"{sp.n_gpu_types} GPU types), embed {D} bf16, predictor "
+                            f"{sp.feat_dim}-{sp.hidden}-{sp.hidden}-2 bf16/fp32-acc, "
+                            f"{sp.n_chunks} chunks of {sp.n_queries} on one stream",
+                "queries": n, "pairs": N, "chunk": sp.n_queries, "pipeline": args.pipeline,
+                "seed": args.seed},
+    )
+    r.close()
+    return res, pb, st, sample, sp
+
+
+def single_query(args, S, hwr, torch):
+    """p50 / p99 of hwr_route_batch for one host query, with the runtime
+    signals updated (random walk) between calls; host clock around the call."""
+    sp = S.spec("C4")
+    pb = S.make_problem(sp, 4)
+    walk = S.StateWalk(sp, 4)
+    r = hwr.Router.from_problem(pb, stream=int(torch.cuda.current_stream().cuda_stream))
+    r.update(walk.state)
+    calls = args.c4_calls
+    qs = S.make_queries(sp, 4, n=calls)
+    L = hwr.load()
+    emb = np.zeros((1, sp.embed_dim), np.uint16)
+    il = np.zeros(1, np.int32)
+    no = np.zeros(1, np.int32)
+    slo = np.zeros(1, np.float32)
+    outs = [np.zeros(1, np.int32), np.zeros(1, np.uint8)] + [np.zeros(1, np.float32) for _ in range(4)]
+    b = hwr.hwr_query_batch(1, hwr.HWR_MEM_HOST, emb.ctypes.data, il.ctypes.data, no.ctypes.data,
+                            slo.ctypes.data)
+    res = hwr.hwr_route_result(*[o.ctypes.data for o in outs], 0, 0, 0)
+    bref, rref = C.byref(b), C.byref(res)
+    ctx = r.ctx
+    route_ns = np.zeros(calls, np.int64)
+    upd_ns = np.zeros(calls, np.int64)
+    for i in range(calls + 100):
+        k = i % calls
+        st = walk.step()
+        t0 = time.perf_counter_ns()
+        rc = L.hwr_update_hw_state(ctx, st.ctypes.data, st.shape[0])
+        t1 = time.perf_counter_ns()
+        assert rc == 0, hwr.hwr_last_error(ctx)
+        emb[0] = qs.emb_bits[k]
+        il[0], no[0], slo[0] = qs.input_len[k], qs.expected_out_len[k], qs.slo_s[k]
+        t2 = time.perf_counter_ns()
+        rc = L.hwr_route_batch(ctx, bref, rref)
+        t3 = time.perf_counter_ns()
+        assert rc == 0, hwr.hwr_last_error(ctx)
+        if i >= 100:                     # the first 100 calls warm up
+            route_ns[k], upd_ns[k] = t3 - t2, t1 - t0
+    r.close()
+    us = route_ns / 1e3
+    return {"calls": calls, "p50_us": float(np.percentile(us, 50)), "p99_us": float(np.percentile(us, 99)),
+            "mean_us": float(us.mean()), "update_p50_us": float(np.percentile(upd_ns / 1e3, 50)),
+            "workload": "C4: 1 query x 32 pairs (16 models x 2 GPU types), embed 768 bf16, "
+                        "predictor 24-128-128-2, graph-launched, host I/O",
+            "timing": "host clock around hwr_route_batch (ctypes call included)"}
+
+
+def cpu_baseline(pb, st, sample, sp):
+    """The CPU oracle (plain C, one thread) on a bounded sample of the same
+    workload: the first queries of chunk 0 against all pairs."""
+    from oracle import oracle as O
+    O.build(force=False)
+    t0 = time.perf_counter()
+    O.route_synth(pb, st, sample, candidates=False)
+    dt = time.perf_counter() - t0
+    cands = sample.n * sp.n_deployments
+    return {"value": cands / dt, "unit": "candidates/s", "cores": 1, "kind": "oracle",
+            "sample": f"first {sample.n} queries of chunk 0 x {sp.n_deployments} pairs "
+                      f"({cands} candidates, {dt:.1f} s, one thread)"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="C5")
+    ap.add_argument("--pipeline", default="fused", choices=["fused", "staged"])
+    ap.add_argument("--seed", type=int, default=5)
+    ap.add_argument("--c4-calls", type=int, default=10000)
+    ap.add_argument("--cpu-sample", type=int, default=1024)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-single", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(run with --gpus 1)", file=sys.stderr)
+        return 2
+    import torch
+    from paper_2608_14575_amd import hwr
+    from paper_2608_14575_amd import synth as S
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 2
+    hwr.load()
+    torch.cuda.set_device(0)
+    res, pb, st, sample, sp = throughput(args, S, hwr, torch)
+    log(f"throughput {res['value']:.3e} candidates/s, predictor {res['roofline']['achieved']:.1f} TFLOP/s")
+    single = None if args.no_single else single_query(args, S, hwr, torch)
+    if single:
+        log(f"single query p50 {single['p50_us']:.1f} us p99 {single['p99_us']:.1f} us")
+    cpu = None if args.no_cpu_baseline else cpu_baseline(pb, st, sample, sp)
+    line = {
+        "metric": METRIC, "value": res["value"], "unit": "candidates/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": res["ms_per_step"],
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded; stands in for the paper's embedded prompt sets)",
+        "config": res["config"], "roofline": res["roofline"], "cpu_baseline": cpu,
+        "single_query": single, "quality_roofline": res["quality_roofline"], "stages": res["stages"],
+    }
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,795 @@
+// Host runtime of libhwr: the C ABI of include/hwr.h on the HIP runtime.
+// Validation, weight re-layout for the MFMA kernels, state ingest, chunked
+// batch routing, the graph-launched single-query path, and event timing.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <atomic>
+#include <chrono>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "hwr_internal.hpp"
+
+using namespace hwr;
+
+namespace {
+
+thread_local std::string g_init_error;
+
+constexpr int kStateSlots = 64;     // pinned ring of state snapshots
+
+struct Pending {
+    int kind;
+    hipEvent_t a, b;
+};
+
+}  // namespace
+
+struct hwr_ctx {
+    // configuration
+    int dev = 0;
+    hipStream_t stream = nullptr;
+    int M = 0, G = 0, N = 0, A = 0, Gw = 0, D = 0, F = 0, H = 0, len_slot = 0;
+    int bf16 = 0, pipeline = 0, max_chunk = 0, flags = 0, cus = 0;
+    float alpha = 0.5f, default_slo = 1.0f, b3[2] = {0, 0};
+    // per-pair tables and state
+    int32_t *d_dep_model = nullptr, *d_dep_gpu = nullptr, *d_model_arch = nullptr;
+    float *d_params = nullptr;
+    float *d_dep_f32 = nullptr;
+    uint16_t *d_dep_bf16 = nullptr;
+    hwr_hw_state *h_ring = nullptr;
+    hipEvent_t ring_ev[kStateSlots] = {};
+    bool ring_used[kStateSlots] = {};
+    int ring_next = 0;
+    bool has_state = false;
+    // weights
+    float *d_bq = nullptr;
+    uint16_t *d_wq_pk = nullptr, *d_wqT = nullptr, *d_w1_pk = nullptr, *d_w2_pk = nullptr;
+    float *d_b1_pk = nullptr, *d_b2_pk = nullptr;
+    uint32_t *d_w3_pk = nullptr;
+    float *d_wq = nullptr, *d_w1 = nullptr, *d_w2 = nullptr, *d_w3 = nullptr, *d_b1 = nullptr,
+          *d_b2 = nullptr;
+    // work space
+    float *d_qmat = nullptr, *d_ctt = nullptr, *d_ctp = nullptr;
+    uint16_t *d_X = nullptr;
+    uint64_t *d_pkey = nullptr;
+    float *d_pval = nullptr;
+    size_t part_cap = 0;
+    // host-memory batches: device staging
+    size_t hs_cap = 0;
+    void *d_hemb = nullptr;
+    int32_t *d_hlen = nullptr, *d_hnout = nullptr, *d_hchoice = nullptr;
+    float *d_hslo = nullptr, *d_hval = nullptr, *d_hcand = nullptr, *d_hqual = nullptr;
+    uint8_t *d_hfeas = nullptr;
+    // single-query path
+    SingleIn *h_sin = nullptr;
+    SingleOut *h_sout = nullptr;
+    SingleIn *d_sin = nullptr;
+    SingleOut *d_sout = nullptr;
+    uint32_t seq = 0;
+    hipGraph_t graph = nullptr;
+    hipGraphExec_t gexec = nullptr;
+    // timing
+    bool prof = false;
+    std::vector<Pending> pending;
+    std::vector<hipEvent_t> pool;
+    double acc_ms[HWR_K_COUNT] = {};
+    int64_t acc_n[HWR_K_COUNT] = {};
+    std::string err;
+};
+
+namespace {
+
+hwr_status fail(hwr_ctx *c, hwr_status s, const std::string &msg) {
+    if (c) c->err = msg;
+    else g_init_error = msg;
+    return s;
+}
+
+hwr_status hip_fail(hwr_ctx *c, hipError_t e, const char *what) {
+    std::string m = std::string(what) + ": " + hipGetErrorName(e) + " (" + hipGetErrorString(e) + ")";
+    return fail(c, e == hipErrorOutOfMemory ? HWR_ERR_OOM : HWR_ERR_HIP, m);
+}
+
+#define HWR_HIP(ctx, call)                                           \
+    do {                                                             \
+        hipError_t e_ = (call);                                      \
+        if (e_ != hipSuccess) return hip_fail((ctx), e_, #call);     \
+    } while (0)
+
+template <class T>
+hipError_t dev_alloc(T **p, size_t count) {
+    *p = nullptr;
+    if (count == 0) count = 1;
+    return hipMalloc(reinterpret_cast<void **>(p), count * sizeof(T));
+}
+
+template <class T>
+hipError_t upload(T **p, const T *src, size_t count) {
+    hipError_t e = dev_alloc(p, count);
+    if (e != hipSuccess) return e;
+    return hipMemcpy(*p, src, count * sizeof(T), hipMemcpyHostToDevice);
+}
+
+bool finite(float v) { return std::isfinite(v); }
+
+// ---------------------------------------------------------------- weight re-layout
+// Quality GEMM B operand: for 64-wide slice s, k-block c and lane (n, h),
+// element j holds Wq[64 s + 32 h + 8 c + j][n] (zero for padded models).
+std::vector<uint16_t> pack_quality(const uint16_t *wq, int D, int M) {
+    std::vector<uint16_t> out(static_cast<size_t>(D) * kQualTile, 0);
+    for (int s = 0; s < D / 64; ++s)
+        for (int c = 0; c < 4; ++c)
+            for (int lane = 0; lane < 64; ++lane) {
+                const int n = lane & 31, h = lane >> 5;
+                for (int j = 0; j < 8; ++j) {
+                    const int k = 64 * s + 32 * h + 8 * c + j;
+                    out[((static_cast<size_t>(s) * 4 + c) * 64 + lane) * 8 + j] =
+                        n < M ? wq[static_cast<size_t>(k) * M + n] : 0;
+                }
+            }
+    return out;
+}
+
+// Predictor A operands.  Layer 1 (W1^T, 32-row tile mt, k-block kb): lane
+// (m, h) element j = W1[16 kb + 8 h + j][32 mt + m], zero past F.  Layer 2
+// (W2^T, tile mo, k-block kb = 2 t + b): the k order follows the layer-1
+// accumulator: element j of lane half h multiplies hidden unit
+// 32 t + crow(8 b + j, h).  Bias tiles hold b[32 mt + crow(r, h)] for
+// r = 0..15; head pairs hold (W3[row(2p)][o], W3[row(2p+1)][o]) as bf16x2.
+struct PackedPredictor {
+    std::vector<uint16_t> w1, w2;
+    std::vector<float> b1, b2;
+    std::vector<uint32_t> w3;
+};
+
+PackedPredictor pack_predictor(const uint16_t *w1, const uint16_t *w2, const uint16_t *w3,
+                               const float *b1, const float *b2, int F, int H) {
+    const int MT = H / 32, KB2 = H / 16;
+    PackedPredictor p;
+    p.w1.assign(static_cast<size_t>(MT) * 2 * 64 * 8, 0);
+    p.w2.assign(static_cast<size_t>(MT) * KB2 * 64 * 8, 0);
+    p.b1.assign(static_cast<size_t>(MT) * 2 * 16, 0.0f);
+    p.b2.assign(static_cast<size_t>(MT) * 2 * 16, 0.0f);
+    p.w3.assign(static_cast<size_t>(MT) * 2 * 16, 0u);
+    for (int mt = 0; mt < MT; ++mt)
+        for (int lane = 0; lane < 64; ++lane) {
+            const int m = lane & 31, h = lane >> 5;
+            for (int kb = 0; kb < 2; ++kb)
+                for (int j = 0; j < 8; ++j) {
+                    const int f = 16 * kb + 8 * h + j;
+                    p.w1[((static_cast<size_t>(mt) * 2 + kb) * 64 + lane) * 8 + j] =
+                        f < F ? w1[static_cast<size_t>(f) * H + 32 * mt + m] : 0;
+                }
+            for (int kb = 0; kb < KB2; ++kb)
+                for (int j = 0; j < 8; ++j) {
+                    const int hin = 32 * (kb >> 1) + crow(8 * (kb & 1) + j, h);
+                    p.w2[((static_cast<size_t>(mt) * KB2 + kb) * 64 + lane) * 8 + j] =
+                        w2[static_cast<size_t>(hin) * H + 32 * mt + m];
+                }
+        }
+    for (int mt = 0; mt < MT; ++mt)
+        for (int h = 0; h < 2; ++h) {
+            for (int r = 0; r < 16; ++r) {
+                p.b1[(mt * 2 + h) * 16 + r] = b1[32 * mt + crow(r, h)];
+                p.b2[(mt * 2 + h) * 16 + r] = b2[32 * mt + crow(r, h)];
+            }
+            for (int o = 0; o < 2; ++o)
+                for (int pp = 0; pp < 8; ++pp) {
+                    const uint32_t lo = w3[static_cast<size_t>(32 * mt + crow(2 * pp, h)) * 2 + o];
+                    const uint32_t hi = w3[static_cast<size_t>(32 * mt + crow(2 * pp + 1, h)) * 2 + o];
+                    p.w3[(mt * 2 + h) * 16 + o * 8 + pp] = lo | (hi << 16);
+                }
+        }
+    return p;
+}
+
+// ---------------------------------------------------------------- timing
+hipEvent_t take_event(hwr_ctx *c) {
+    if (!c->pool.empty()) {
+        hipEvent_t e = c->pool.back();
+        c->pool.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+}
+
+template <class F>
+hipError_t timed(hwr_ctx *c, int kind, F &&launch) {
+    if (!c->prof) return launch();
+    hipEvent_t a = take_event(c), b = take_event(c);
+    if (!a || !b) return hipErrorOutOfMemory;
+    hipError_t e = hipEventRecord(a, c->stream);
+    if (e != hipSuccess) return e;
+    e = launch();
+    if (e != hipSuccess) return e;
+    e = hipEventRecord(b, c->stream);
+    if (e != hipSuccess) return e;
+    c->pending.push_back({kind, a, b});
+    return hipSuccess;
+}
+
+hwr_status drain_timing(hwr_ctx *c) {
+    for (const Pending &p : c->pending) {
+        HWR_HIP(c, hipEventSynchronize(p.b));
+        float ms = 0.0f;
+        HWR_HIP(c, hipEventElapsedTime(&ms, p.a, p.b));
+        c->acc_ms[p.kind] += ms;
+        c->acc_n[p.kind] += 1;
+        c->pool.push_back(p.a);
+        c->pool.push_back(p.b);
+    }
+    c->pending.clear();
+    return HWR_OK;
+}
+
+// ---------------------------------------------------------------- validation
+hwr_status check_config(const hwr_config *cfg) {
+    auto bad = [](const char *m) { return fail(nullptr, HWR_ERR_INVALID_ARG, m); };
+    auto uns = [](const char *m) { return fail(nullptr, HWR_ERR_UNSUPPORTED, m); };
+    if (!cfg) return bad("config is NULL");
+    const int M = cfg->n_models, G = cfg->n_gpu_types, N = cfg->n_deployments;
+    if (M < 1 || G < 1 || N < 1) return bad("n_models, n_gpu_types and n_deployments must be >= 1");
+    if (cfg->arch_width < 1 || cfg->gpu_width < G) return bad("arch_width >= 1 and gpu_width >= n_gpu_types required");
+    if (cfg->arch_width + cfg->gpu_width + 8 > cfg->feat_dim) return bad("feat_dim must hold both one-hots and 8 signal slots");
+    if (cfg->feat_dim > kFeatPad) return uns("feat_dim above 32 is not supported");
+    if (M > kMaxModels) return uns("more than 32 models is not supported");
+    if (N > kMaxPairs) return uns("more than 1024 pairs is not supported");
+    if (cfg->embed_dim < 64 || cfg->embed_dim % 64 != 0 || cfg->embed_dim > 8192)
+        return uns("embed_dim must be a multiple of 64 in [64, 8192]");
+    if (cfg->emb_dtype != cfg->weight_dtype) return uns("emb_dtype must equal weight_dtype");
+    if (cfg->weight_dtype != HWR_F32 && cfg->weight_dtype != HWR_BF16) return bad("unknown dtype");
+    if (cfg->weight_dtype == HWR_BF16 && cfg->hidden != 64 && cfg->hidden != 128 && cfg->hidden != 256)
+        return uns("bf16 hidden width must be 64, 128 or 256");
+    if (cfg->weight_dtype == HWR_F32 && cfg->hidden != 64 && cfg->hidden != 128)
+        return uns("fp32 hidden width must be 64 or 128");
+    if (cfg->pipeline != HWR_PIPE_FUSED && cfg->pipeline != HWR_PIPE_STAGED) return bad("unknown pipeline");
+    if (cfg->max_chunk < 0 || cfg->max_chunk > (1 << 22)) return bad("max_chunk must be in [0, 2^22]");
+    if (!finite(cfg->cost_weight) || cfg->cost_weight < 0.0f) return bad("cost_weight must be finite and >= 0");
+    if (!finite(cfg->default_slo_s) || cfg->default_slo_s <= 0.0f) return bad("default_slo_s must be finite and > 0");
+    if (!cfg->dep_model || !cfg->dep_gpu || !cfg->model_arch || !cfg->model_params_b || !cfg->wq ||
+        !cfg->bq || !cfg->w1 || !cfg->b1 || !cfg->w2 || !cfg->b2 || !cfg->w3 || !cfg->b3)
+        return bad("a table or weight pointer is NULL");
+    for (int d = 0; d < N; ++d) {
+        if (cfg->dep_model[d] < 0 || cfg->dep_model[d] >= M) return bad("dep_model out of range");
+        if (cfg->dep_gpu[d] < 0 || cfg->dep_gpu[d] >= G) return bad("dep_gpu out of range");
+    }
+    for (int m = 0; m < M; ++m) {
+        if (cfg->model_arch[m] < 0 || cfg->model_arch[m] >= cfg->arch_width) return bad("model_arch out of range");
+        if (!finite(cfg->model_params_b[m]) || cfg->model_params_b[m] <= 0.0f) return bad("model_params_b must be > 0");
+        if (!finite(cfg->bq[m])) return bad("bq not finite");
+    }
+    for (int j = 0; j < cfg->hidden; ++j)
+        if (!finite(cfg->b1[j]) || !finite(cfg->b2[j])) return bad("b1/b2 not finite");
+    if (!finite(cfg->b3[0]) || !finite(cfg->b3[1])) return bad("b3 not finite");
+    return HWR_OK;
+}
+
+void release(hwr_ctx *c) {
+    if (!c) return;
+    hipSetDevice(c->dev);
+    hipStreamSynchronize(c->stream);
+    for (const Pending &p : c->pending) {
+        hipEventDestroy(p.a);
+        hipEventDestroy(p.b);
+    }
+    for (hipEvent_t e : c->pool) hipEventDestroy(e);
+    for (int i = 0; i < kStateSlots; ++i)
+        if (c->ring_ev[i]) hipEventDestroy(c->ring_ev[i]);
+    if (c->gexec) hipGraphExecDestroy(c->gexec);
+    if (c->graph) hipGraphDestroy(c->graph);
+    void *dev_ptrs[] = {c->d_dep_model, c->d_dep_gpu, c->d_model_arch, c->d_params, c->d_dep_f32,
+                        c->d_dep_bf16, c->d_bq, c->d_wq_pk, c->d_wqT, c->d_w1_pk, c->d_w2_pk,
+                        c->d_b1_pk, c->d_b2_pk, c->d_w3_pk, c->d_wq, c->d_w1, c->d_w2, c->d_w3,
+                        c->d_b1, c->d_b2, c->d_qmat, c->d_ctt, c->d_ctp, c->d_X, c->d_pkey,
+                        c->d_pval, c->d_hemb, c->d_hlen, c->d_hnout, c->d_hchoice, c->d_hslo,
+                        c->d_hval, c->d_hcand, c->d_hqual, c->d_hfeas};
+    for (void *p : dev_ptrs)
+        if (p) hipFree(p);
+    if (c->h_ring) hipHostFree(c->h_ring);
+    if (c->h_sin) hipHostFree(c->h_sin);
+    if (c->h_sout) hipHostFree(c->h_sout);
+    delete c;
+}
+
+hwr_status init_impl(const hwr_config *cfg, hwr_ctx **out) {
+    hwr_status st = check_config(cfg);
+    if (st != HWR_OK) return st;
+    int ndev = 0;
+    hipError_t e = hipGetDeviceCount(&ndev);
+    if (e != hipSuccess || ndev < 1) return fail(nullptr, HWR_ERR_HIP, "no HIP device available");
+    if (cfg->device < 0 || cfg->device >= ndev) return fail(nullptr, HWR_ERR_INVALID_ARG, "device ordinal out of range");
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, cfg->device) != hipSuccess)
+        return fail(nullptr, HWR_ERR_HIP, "hipGetDeviceProperties failed");
+    if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+        return fail(nullptr, HWR_ERR_UNSUPPORTED, std::string("library is built for gfx950, device is ") + prop.gcnArchName);
+
+    hwr_ctx *c = new hwr_ctx();
+    c->dev = cfg->device;
+    c->stream = static_cast<hipStream_t>(cfg->stream);
+    c->M = cfg->n_models;
+    c->G = cfg->n_gpu_types;
+    c->N = cfg->n_deployments;
+    c->A = cfg->arch_width;
+    c->Gw = cfg->gpu_width;
+    c->D = cfg->embed_dim;
+    c->F = cfg->feat_dim;
+    c->H = cfg->hidden;
+    c->len_slot = c->A + c->Gw + 1;
+    c->bf16 = cfg->weight_dtype == HWR_BF16;
+    c->pipeline = cfg->pipeline;
+    c->max_chunk = cfg->max_chunk > 0 ? cfg->max_chunk : 65536;
+    c->flags = cfg->flags;
+    c->alpha = cfg->cost_weight;
+    c->default_slo = cfg->default_slo_s;
+    c->b3[0] = cfg->b3[0];
+    c->b3[1] = cfg->b3[1];
+    c->cus = prop.multiProcessorCount;
+
+    auto bail = [&](hipError_t err, const char *what) {
+        hwr_status s = hip_fail(nullptr, err, what);
+        release(c);
+        return s;
+    };
+#define INIT_HIP(call)                                   \
+    do {                                                 \
+        hipError_t e_ = (call);                          \
+        if (e_ != hipSuccess) return bail(e_, #call);    \
+    } while (0)
+
+    INIT_HIP(hipSetDevice(c->dev));
+    const int M = c->M, N = c->N, D = c->D, F = c->F, H = c->H;
+    INIT_HIP(upload(&c->d_dep_model, cfg->dep_model, N));
+    INIT_HIP(upload(&c->d_dep_gpu, cfg->dep_gpu, N));
+    INIT_HIP(upload(&c->d_model_arch, cfg->model_arch, M));
+    INIT_HIP(upload(&c->d_params, cfg->model_params_b, M));
+    INIT_HIP(upload(&c->d_bq, cfg->bq, M));
+    INIT_HIP(dev_alloc(&c->d_dep_f32, static_cast<size_t>(N) * kFeatPad));
+    INIT_HIP(dev_alloc(&c->d_dep_bf16, static_cast<size_t>(N) * kFeatPad));
+    if (c->bf16) {
+        const uint16_t *wq = static_cast<const uint16_t *>(cfg->wq);
+        std::vector<uint16_t> wqpk = pack_quality(wq, D, M);
+        INIT_HIP(upload(&c->d_wq_pk, wqpk.data(), wqpk.size()));
+        std::vector<uint16_t> wqT(static_cast<size_t>(M) * D);
+        for (int k = 0; k < D; ++k)
+            for (int m = 0; m < M; ++m) wqT[static_cast<size_t>(m) * D + k] = wq[static_cast<size_t>(k) * M + m];
+        INIT_HIP(upload(&c->d_wqT, wqT.data(), wqT.size()));
+        PackedPredictor p = pack_predictor(static_cast<const uint16_t *>(cfg->w1),
+                                           static_cast<const uint16_t *>(cfg->w2),
+                                           static_cast<const uint16_t *>(cfg->w3), cfg->b1, cfg->b2, F, H);
+        INIT_HIP(upload(&c->d_w1_pk, p.w1.data(), p.w1.size()));
+        INIT_HIP(upload(&c->d_w2_pk, p.w2.data(), p.w2.size()));
+        INIT_HIP(upload(&c->d_b1_pk, p.b1.data(), p.b1.size()));
+        INIT_HIP(upload(&c->d_b2_pk, p.b2.data(), p.b2.size()));
+        INIT_HIP(upload(&c->d_w3_pk, p.w3.data(), p.w3.size()));
+    } else {
+        INIT_HIP(upload(&c->d_wq, static_cast<const float *>(cfg->wq), static_cast<size_t>(D) * M));
+        INIT_HIP(upload(&c->d_w1, static_cast<const float *>(cfg->w1), static_cast<size_t>(F) * H));
+        INIT_HIP(upload(&c->d_w2, static_cast<const float *>(cfg->w2), static_cast<size_t>(H) * H));
+        INIT_HIP(upload(&c->d_w3, static_cast<const float *>(cfg->w3), static_cast<size_t>(H) * 2));
+        INIT_HIP(upload(&c->d_b1, cfg->b1, H));
+        INIT_HIP(upload(&c->d_b2, cfg->b2, H));
+    }
+    const size_t chunk = static_cast<size_t>(c->max_chunk);
+    INIT_HIP(dev_alloc(&c->d_qmat, chunk * M));
+    if (!c->bf16 || c->pipeline == HWR_PIPE_STAGED) {
+        INIT_HIP(dev_alloc(&c->d_ctt, chunk * N));
+        INIT_HIP(dev_alloc(&c->d_ctp, chunk * N));
+    }
+    if (c->bf16 && c->pipeline == HWR_PIPE_STAGED) INIT_HIP(dev_alloc(&c->d_X, chunk * N * kFeatPad));
+    if (c->bf16 && c->pipeline == HWR_PIPE_FUSED) {
+        c->part_cap = static_cast<size_t>(2 * c->cus) * kQPerBlock;
+        INIT_HIP(dev_alloc(&c->d_pkey, c->part_cap));
+        INIT_HIP(dev_alloc(&c->d_pval, c->part_cap * 4));
+    }
+    INIT_HIP(hipHostMalloc(reinterpret_cast<void **>(&c->h_ring),
+                           sizeof(hwr_hw_state) * N * kStateSlots, hipHostMallocMapped));
+    for (int i = 0; i < kStateSlots; ++i) INIT_HIP(hipEventCreateWithFlags(&c->ring_ev[i], hipEventDisableTiming));
+    if (c->bf16) {
+        const size_t in_bytes = sizeof(SingleIn) + static_cast<size_t>(D) * 2;
+        INIT_HIP(hipHostMalloc(reinterpret_cast<void **>(&c->h_sin), in_bytes,
+                               hipHostMallocMapped | hipHostMallocCoherent));
+        INIT_HIP(hipHostMalloc(reinterpret_cast<void **>(&c->h_sout), sizeof(SingleOut),
+                               hipHostMallocMapped | hipHostMallocCoherent));
+        std::memset(c->h_sin, 0, in_bytes);
+        std::memset(c->h_sout, 0, sizeof(SingleOut));
+        INIT_HIP(hipHostGetDevicePointer(reinterpret_cast<void **>(&c->d_sin), c->h_sin, 0));
+        INIT_HIP(hipHostGetDevicePointer(reinterpret_cast<void **>(&c->d_sout), c->h_sout, 0));
+    }
+#undef INIT_HIP
+    *out = c;
+    return HWR_OK;
+}
+
+// ---------------------------------------------------------------- batch routing
+struct DevBatch {
+    int n;
+    const void *emb;
+    const int32_t *len, *nout;
+    const float *slo;
+    OutArgs out;
+    float *cand_ttft, *cand_tpot, *cand_quality;
+};
+
+hwr_status route_device(hwr_ctx *c, const DevBatch &b) {
+    const int M = c->M, N = c->N, D = c->D;
+    const size_t esz = c->bf16 ? 2 : 4;
+    for (int off = 0; off < b.n; off += c->max_chunk) {
+        const int cn = std::min(c->max_chunk, b.n - off);
+        QueryArgs qa;
+        qa.nq = cn;
+        qa.input_len = b.len + off;
+        qa.nout = b.nout + off;
+        qa.slo = b.slo ? b.slo + off : nullptr;
+        qa.default_slo = c->default_slo;
+        OutArgs oa = b.out;
+        oa.choice += off;
+        if (oa.feasible) oa.feasible += off;
+        if (oa.utility) oa.utility += off;
+        if (oa.e2e) oa.e2e += off;
+        if (oa.ttft) oa.ttft += off;
+        if (oa.tpot) oa.tpot += off;
+        float *qmat = b.cand_quality ? b.cand_quality + static_cast<size_t>(off) * M : c->d_qmat;
+        float *ctt = b.cand_ttft ? b.cand_ttft + static_cast<size_t>(off) * N : nullptr;
+        float *ctp = b.cand_tpot ? b.cand_tpot + static_cast<size_t>(off) * N : nullptr;
+
+        QualityArgs qu;
+        qu.nq = cn;
+        qu.D = D;
+        qu.M = M;
+        qu.emb = static_cast<const char *>(b.emb) + static_cast<size_t>(off) * D * esz;
+        qu.wq_pk = c->d_wq_pk;
+        qu.wq = c->d_wq;
+        qu.bq = c->d_bq;
+        qu.qmat = qmat;
+        HWR_HIP(c, timed(c, HWR_K_QUALITY, [&] {
+            return c->bf16 ? launch_quality_bf16(qu, c->stream) : launch_quality_f32(qu, c->stream);
+        }));
+
+        if (c->bf16) {
+            MlpArgs ma{};
+            ma.N = N;
+            ma.M = M;
+            ma.len_slot = c->len_slot;
+            ma.alpha = c->alpha;
+            ma.b3_0 = c->b3[0];
+            ma.b3_1 = c->b3[1];
+            ma.q = qa;
+            ma.dep_bf16 = c->d_dep_bf16;
+            ma.dep_model = c->d_dep_model;
+            ma.qmat = qmat;
+            ma.w1_pk = c->d_w1_pk;
+            ma.w2_pk = c->d_w2_pk;
+            ma.b1_pk = c->d_b1_pk;
+            ma.b2_pk = c->d_b2_pk;
+            ma.w3_pk = c->d_w3_pk;
+            ma.out = oa;
+            ma.nsplit = 1;
+            if (c->pipeline == HWR_PIPE_FUSED) {
+                ma.cand_ttft = ctt;
+                ma.cand_tpot = ctp;
+                const int blocks = (cn + kQPerBlock - 1) / kQPerBlock;
+                int nsplit = 1;
+                if (blocks < c->cus) nsplit = std::min(N, (c->cus + blocks - 1) / blocks);
+                while (nsplit > 1 && static_cast<size_t>(nsplit) * cn > c->part_cap) --nsplit;
+                ma.nsplit = nsplit;
+                ma.part_key = c->d_pkey;
+                ma.part_val = c->d_pval;
+                HWR_HIP(c, timed(c, HWR_K_FUSED, [&] { return launch_mlp_bf16(c->H, false, ma, c->stream); }));
+                if (nsplit > 1) {
+                    MergeArgs mg{cn, nsplit, c->d_pkey, c->d_pval, oa};
+                    HWR_HIP(c, timed(c, HWR_K_MERGE, [&] { return launch_merge(mg, c->stream); }));
+                }
+                continue;
+            }
+            GatherArgs ga{N, c->len_slot, qa, c->d_dep_bf16, c->d_X};
+            HWR_HIP(c, timed(c, HWR_K_GATHER, [&] { return launch_gather(ga, c->stream); }));
+            ma.X = c->d_X;
+            ma.cand_ttft = ctt ? ctt : c->d_ctt;
+            ma.cand_tpot = ctp ? ctp : c->d_ctp;
+            HWR_HIP(c, timed(c, HWR_K_MLP, [&] { return launch_mlp_bf16(c->H, true, ma, c->stream); }));
+        } else {
+            MlpF32Args fa{};
+            fa.N = N;
+            fa.F = c->F;
+            fa.len_slot = c->len_slot;
+            fa.b3_0 = c->b3[0];
+            fa.b3_1 = c->b3[1];
+            fa.q = qa;
+            fa.dep_f32 = c->d_dep_f32;
+            fa.w1 = c->d_w1;
+            fa.b1 = c->d_b1;
+            fa.w2 = c->d_w2;
+            fa.b2 = c->d_b2;
+            fa.w3 = c->d_w3;
+            fa.cand_ttft = ctt ? ctt : c->d_ctt;
+            fa.cand_tpot = ctp ? ctp : c->d_ctp;
+            HWR_HIP(c, timed(c, HWR_K_MLP, [&] { return launch_mlp_f32(c->H, fa, c->stream); }));
+        }
+        EpilogueArgs ea{};
+        ea.N = N;
+        ea.M = M;
+        int g = 1;
+        while (g < N && g < 64) g <<= 1;
+        ea.group = g;
+        ea.alpha = c->alpha;
+        ea.q = qa;
+        ea.dep_model = c->d_dep_model;
+        ea.qmat = qmat;
+        ea.cand_ttft = ctt ? ctt : c->d_ctt;
+        ea.cand_tpot = ctp ? ctp : c->d_ctp;
+        ea.out = oa;
+        HWR_HIP(c, timed(c, HWR_K_EPILOGUE, [&] { return launch_epilogue(ea, c->stream); }));
+    }
+    return HWR_OK;
+}
+
+hwr_status ensure_host_staging(hwr_ctx *c, size_t rows) {
+    if (rows <= c->hs_cap) return HWR_OK;
+    void *ptrs[] = {c->d_hemb, c->d_hlen, c->d_hnout, c->d_hchoice, c->d_hslo,
+                    c->d_hval, c->d_hcand, c->d_hqual, c->d_hfeas};
+    HWR_HIP(c, hipStreamSynchronize(c->stream));
+    for (void *p : ptrs)
+        if (p) hipFree(p);
+    c->hs_cap = 0;
+    const size_t esz = c->bf16 ? 2 : 4;
+    HWR_HIP(c, hipMalloc(&c->d_hemb, rows * c->D * esz));
+    HWR_HIP(c, dev_alloc(&c->d_hlen, rows));
+    HWR_HIP(c, dev_alloc(&c->d_hnout, rows));
+    HWR_HIP(c, dev_alloc(&c->d_hchoice, rows));
+    HWR_HIP(c, dev_alloc(&c->d_hslo, rows));
+    HWR_HIP(c, dev_alloc(&c->d_hval, rows * 4));
+    HWR_HIP(c, dev_alloc(&c->d_hcand, rows * c->N * 2));
+    HWR_HIP(c, dev_alloc(&c->d_hqual, rows * c->M));
+    HWR_HIP(c, dev_alloc(&c->d_hfeas, rows));
+    c->hs_cap = rows;
+    return HWR_OK;
+}
+
+hwr_status route_host(hwr_ctx *c, const hwr_query_batch *q, hwr_route_result *r) {
+    const size_t rows = static_cast<size_t>(std::min(q->n, c->max_chunk));
+    hwr_status st = ensure_host_staging(c, rows);
+    if (st != HWR_OK) return st;
+    const size_t esz = c->bf16 ? 2 : 4;
+    const int N = c->N, M = c->M, D = c->D;
+    hipStream_t s = c->stream;
+    for (int off = 0; off < q->n; off += c->max_chunk) {
+        const int cn = std::min(c->max_chunk, q->n - off);
+        HWR_HIP(c, hipMemcpyAsync(c->d_hemb, static_cast<const char *>(q->emb) + static_cast<size_t>(off) * D * esz,
+                                  static_cast<size_t>(cn) * D * esz, hipMemcpyHostToDevice, s));
+        HWR_HIP(c, hipMemcpyAsync(c->d_hlen, q->input_len + off, cn * 4, hipMemcpyHostToDevice, s));
+        HWR_HIP(c, hipMemcpyAsync(c->d_hnout, q->expected_out_len + off, cn * 4, hipMemcpyHostToDevice, s));
+        if (q->slo_s) HWR_HIP(c, hipMemcpyAsync(c->d_hslo, q->slo_s + off, cn * 4, hipMemcpyHostToDevice, s));
+        DevBatch b{};
+        b.n = cn;
+        b.emb = c->d_hemb;
+        b.len = c->d_hlen;
+        b.nout = c->d_hnout;
+        b.slo = q->slo_s ? c->d_hslo : nullptr;
+        float *v = c->d_hval;
+        b.out = OutArgs{c->d_hchoice, c->d_hfeas, v, v + rows, v + 2 * rows, v + 3 * rows};
+        b.cand_ttft = r->cand_ttft ? c->d_hcand : nullptr;
+        b.cand_tpot = r->cand_tpot ? c->d_hcand + rows * N : nullptr;
+        b.cand_quality = r->cand_quality ? c->d_hqual : nullptr;
+        hwr_status rs = route_device(c, b);
+        if (rs != HWR_OK) return rs;
+        auto d2h = [&](void *dst, const void *src, size_t bytes) {
+            return hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToHost, s);
+        };
+        HWR_HIP(c, d2h(r->choice + off, c->d_hchoice, cn * 4));
+        if (r->feasible) HWR_HIP(c, d2h(r->feasible + off, c->d_hfeas, cn));
+        if (r->utility) HWR_HIP(c, d2h(r->utility + off, v, cn * 4));
+        if (r->e2e_s) HWR_HIP(c, d2h(r->e2e_s + off, v + rows, cn * 4));
+        if (r->ttft_s) HWR_HIP(c, d2h(r->ttft_s + off, v + 2 * rows, cn * 4));
+        if (r->tpot_s) HWR_HIP(c, d2h(r->tpot_s + off, v + 3 * rows, cn * 4));
+        if (r->cand_ttft) HWR_HIP(c, d2h(r->cand_ttft + static_cast<size_t>(off) * N, c->d_hcand, static_cast<size_t>(cn) * N * 4));
+        if (r->cand_tpot) HWR_HIP(c, d2h(r->cand_tpot + static_cast<size_t>(off) * N, c->d_hcand + rows * N, static_cast<size_t>(cn) * N * 4));
+        if (r->cand_quality) HWR_HIP(c, d2h(r->cand_quality + static_cast<size_t>(off) * M, c->d_hqual, static_cast<size_t>(cn) * M * 4));
+        HWR_HIP(c, hipStreamSynchronize(s));   // staging is reused by the next chunk
+    }
+    return HWR_OK;
+}
+
+// ---------------------------------------------------------------- single query
+SingleArgs single_args(const hwr_ctx *c) {
+    SingleArgs a{};
+    a.N = c->N;
+    a.M = c->M;
+    a.D = c->D;
+    a.len_slot = c->len_slot;
+    a.alpha = c->alpha;
+    a.b3_0 = c->b3[0];
+    a.b3_1 = c->b3[1];
+    a.in = c->d_sin;
+    a.out = c->d_sout;
+    a.dep_bf16 = c->d_dep_bf16;
+    a.dep_model = c->d_dep_model;
+    a.wqT = c->d_wqT;
+    a.bq = c->d_bq;
+    a.w1_pk = c->d_w1_pk;
+    a.w2_pk = c->d_w2_pk;
+    a.b1_pk = c->d_b1_pk;
+    a.b2_pk = c->d_b2_pk;
+    a.w3_pk = c->d_w3_pk;
+    return a;
+}
+
+// Capture the single-query kernel into a graph once; replays read the query
+// record and the pair features by address, so state updates need no re-capture.
+hwr_status single_graph(hwr_ctx *c) {
+    if (c->gexec || (c->flags & HWR_FLAG_NO_GRAPH)) return HWR_OK;
+    const SingleArgs a = single_args(c);
+    hipStream_t cs = nullptr;
+    HWR_HIP(c, hipStreamCreateWithFlags(&cs, hipStreamNonBlocking));
+    hipError_t e = hipStreamBeginCapture(cs, hipStreamCaptureModeThreadLocal);
+    if (e == hipSuccess) e = launch_single(c->H, a, cs);
+    hipGraph_t g = nullptr;
+    hipError_t e2 = hipStreamEndCapture(cs, &g);
+    hipStreamDestroy(cs);
+    if (e != hipSuccess) {
+        if (g) hipGraphDestroy(g);
+        return hip_fail(c, e, "single-query graph capture");
+    }
+    if (e2 != hipSuccess) return hip_fail(c, e2, "hipStreamEndCapture");
+    c->graph = g;
+    HWR_HIP(c, hipGraphInstantiate(&c->gexec, c->graph, nullptr, nullptr, 0));
+    return HWR_OK;
+}
+
+hwr_status route_single(hwr_ctx *c, const hwr_query_batch *q, hwr_route_result *r) {
+    hwr_status st = single_graph(c);
+    if (st != HWR_OK) return st;
+    SingleIn *in = c->h_sin;
+    const uint32_t seq = ++c->seq == 0 ? ++c->seq : c->seq;
+    in->input_len = q->input_len[0];
+    in->nout = q->expected_out_len[0];
+    in->slo = q->slo_s ? q->slo_s[0] : c->default_slo;
+    std::memcpy(in + 1, q->emb, static_cast<size_t>(c->D) * 2);
+    in->seq = seq;
+    std::atomic_thread_fence(std::memory_order_release);
+    if (c->gexec) {
+        HWR_HIP(c, timed(c, HWR_K_SINGLE, [&] { return hipGraphLaunch(c->gexec, c->stream); }));
+    } else {
+        const SingleArgs a = single_args(c);
+        HWR_HIP(c, timed(c, HWR_K_SINGLE, [&] { return launch_single(c->H, a, c->stream); }));
+    }
+    // wait for the decision record (written last by the kernel, system scope)
+    volatile uint32_t *flag = &c->h_sout->seq;
+    auto t0 = std::chrono::steady_clock::now();
+    uint64_t spins = 0;
+    while (*flag != seq) {
+        if ((++spins & 0xFFFF) == 0) {
+            hipError_t qe = hipStreamQuery(c->stream);
+            if (qe != hipSuccess && qe != hipErrorNotReady) return hip_fail(c, qe, "single-query launch");
+            if (qe == hipSuccess && *flag != seq)
+                return fail(c, HWR_ERR_HIP, "single-query kernel finished without writing its result");
+            if (std::chrono::steady_clock::now() - t0 > std::chrono::seconds(10))
+                return fail(c, HWR_ERR_HIP, "single-query launch did not complete within 10 s");
+        }
+    }
+    std::atomic_thread_fence(std::memory_order_acquire);
+    const SingleOut *o = c->h_sout;
+    r->choice[0] = o->choice;
+    if (r->feasible) r->feasible[0] = static_cast<uint8_t>(o->feasible);
+    if (r->utility) r->utility[0] = o->utility;
+    if (r->e2e_s) r->e2e_s[0] = o->e2e;
+    if (r->ttft_s) r->ttft_s[0] = o->ttft;
+    if (r->tpot_s) r->tpot_s[0] = o->tpot;
+    return HWR_OK;
+}
+
+}  // namespace
+
+// ==================================================================== C ABI
+extern "C" {
+
+hwr_status hwr_init(const hwr_config *cfg, hwr_ctx **out) {
+    if (!out) return fail(nullptr, HWR_ERR_INVALID_ARG, "out is NULL");
+    *out = nullptr;
+    g_init_error.clear();
+    return init_impl(cfg, out);
+}
+
+hwr_status hwr_update_hw_state(hwr_ctx *c, const hwr_hw_state *state, int32_t n) {
+    if (!c) return fail(nullptr, HWR_ERR_INVALID_ARG, "ctx is NULL");
+    if (!state) return fail(c, HWR_ERR_INVALID_ARG, "state is NULL");
+    if (n != c->N) return fail(c, HWR_ERR_INVALID_ARG, "state count must equal n_deployments");
+    for (int d = 0; d < n; ++d) {
+        const hwr_hw_state &s = state[d];
+        if (s.running_q < 0 || s.waiting_q < 0) return fail(c, HWR_ERR_INVALID_ARG, "queue length < 0");
+        if (!finite(s.kv_util) || s.kv_util < 0.0f || s.kv_util > 1.0f)
+            return fail(c, HWR_ERR_INVALID_ARG, "kv_util outside [0, 1]");
+        if (!finite(s.gpu_util) || s.gpu_util < 0.0f || s.gpu_util > 1.0f)
+            return fail(c, HWR_ERR_INVALID_ARG, "gpu_util outside [0, 1]");
+        if (!finite(s.ttft_avg_s) || s.ttft_avg_s <= 0.0f || !finite(s.tpot_avg_s) || s.tpot_avg_s <= 0.0f)
+            return fail(c, HWR_ERR_INVALID_ARG, "ttft_avg_s / tpot_avg_s must be finite and > 0");
+    }
+    HWR_HIP(c, hipSetDevice(c->dev));
+    const int slot = c->ring_next;
+    if (c->ring_used[slot]) HWR_HIP(c, hipEventSynchronize(c->ring_ev[slot]));
+    hwr_hw_state *dst = c->h_ring + static_cast<size_t>(slot) * c->N;
+    std::memcpy(dst, state, sizeof(hwr_hw_state) * n);
+    hwr_hw_state *dsrc = nullptr;
+    HWR_HIP(c, hipHostGetDevicePointer(reinterpret_cast<void **>(&dsrc), dst, 0));
+    StateArgs a{dsrc, c->N, c->A, c->Gw, c->d_dep_model, c->d_dep_gpu, c->d_model_arch,
+                c->d_params, c->d_dep_f32, c->d_dep_bf16};
+    HWR_HIP(c, timed(c, HWR_K_STATE, [&] { return launch_state(a, c->stream); }));
+    HWR_HIP(c, hipEventRecord(c->ring_ev[slot], c->stream));
+    c->ring_used[slot] = true;
+    c->ring_next = (slot + 1) % kStateSlots;
+    c->has_state = true;
+    return HWR_OK;
+}
+
+hwr_status hwr_route_batch(hwr_ctx *c, const hwr_query_batch *q, hwr_route_result *r) {
+    if (!c) return fail(nullptr, HWR_ERR_INVALID_ARG, "ctx is NULL");
+    if (!q || !r) return fail(c, HWR_ERR_INVALID_ARG, "batch or result is NULL");
+    if (q->n < 0) return fail(c, HWR_ERR_INVALID_ARG, "n < 0");
+    if (q->mem != HWR_MEM_DEVICE && q->mem != HWR_MEM_HOST) return fail(c, HWR_ERR_INVALID_ARG, "unknown mem");
+    if (q->n == 0) return HWR_OK;
+    if (!q->emb || !q->input_len || !q->expected_out_len || !r->choice)
+        return fail(c, HWR_ERR_INVALID_ARG, "emb, input_len, expected_out_len and choice are required");
+    if (!c->has_state) return fail(c, HWR_ERR_STATE, "no hardware state yet: call hwr_update_hw_state first");
+    HWR_HIP(c, hipSetDevice(c->dev));
+    if (q->mem == HWR_MEM_DEVICE) {
+        DevBatch b{};
+        b.n = q->n;
+        b.emb = q->emb;
+        b.len = q->input_len;
+        b.nout = q->expected_out_len;
+        b.slo = q->slo_s;
+        b.out = OutArgs{r->choice, r->feasible, r->utility, r->e2e_s, r->ttft_s, r->tpot_s};
+        b.cand_ttft = r->cand_ttft;
+        b.cand_tpot = r->cand_tpot;
+        b.cand_quality = r->cand_quality;
+        return route_device(c, b);
+    }
+    for (int i = 0; i < q->n; ++i) {
+        if (q->input_len[i] < 1) return fail(c, HWR_ERR_INVALID_ARG, "input_len < 1");
+        if (q->expected_out_len[i] < 0) return fail(c, HWR_ERR_INVALID_ARG, "expected_out_len < 0");
+        if (q->slo_s && (!finite(q->slo_s[i]) || q->slo_s[i] <= 0.0f))
+            return fail(c, HWR_ERR_INVALID_ARG, "slo_s must be finite and > 0");
+    }
+    if (q->n == 1 && c->bf16 && !r->cand_ttft && !r->cand_tpot && !r->cand_quality)
+        return route_single(c, q, r);
+    return route_host(c, q, r);
+}
+
+void hwr_free(hwr_ctx *c) { release(c); }
+
+const char *hwr_last_error(const hwr_ctx *c) {
+    if (c) return c->err.c_str();
+    return g_init_error.c_str();
+}
+
+hwr_status hwr_profile_enable(hwr_ctx *c, int32_t enable) {
+    if (!c) return fail(nullptr, HWR_ERR_INVALID_ARG, "ctx is NULL");
+    c->prof = enable != 0;
+    return HWR_OK;
+}
+
+hwr_status hwr_profile_read(hwr_ctx *c, hwr_kernel_times *out, int32_t reset) {
+    if (!c || !out) return fail(c, HWR_ERR_INVALID_ARG, "ctx or out is NULL");
+    hwr_status st = drain_timing(c);
+    if (st != HWR_OK) return st;
+    for (int k = 0; k < HWR_K_COUNT; ++k) {
+        out->ms[k] = c->acc_ms[k];
+        out->launches[k] = c->acc_n[k];
+    }
+    if (reset) {
+        for (int k = 0; k < HWR_K_COUNT; ++k) {
+            c->acc_ms[k] = 0.0;
+            c->acc_n[k] = 0;
+        }
+    }
+    return HWR_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,179 @@
+// Internal definitions shared by the HIP kernels and the host runtime of
+// libhwr (gfx950 only).  Nothing here is part of the public C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+#include "hwr.h"
+
+namespace hwr {
+
+constexpr int kFeatPad = 32;     // feature slots padded to two 16-wide MFMA k-blocks
+constexpr int kQualTile = 32;    // quality GEMM: models padded to one 32-wide tile
+constexpr int kBlock = 256;      // threads per workgroup of the batch kernels
+constexpr int kQPerWave = 64;    // fused predictor: queries per wave (two 32-column tiles)
+constexpr int kQPerBlock = kQPerWave * (kBlock / 64);
+constexpr int kGatherQ = 16;     // feature gather: queries per workgroup
+constexpr int kMaxPairs = 1024;
+constexpr int kMaxModels = 32;
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef short i16x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// Row of output element r (0..15) held by a lane of half h (lane >> 5) in the
+// accumulator of a 32x32 MFMA; the column is lane & 31.
+__host__ __device__ constexpr int crow(int r, int h) { return 8 * (r >> 2) + 4 * h + (r & 3); }
+
+// Order-preserving map of an fp32 utility onto uint32 (larger u -> larger key).
+__host__ __device__ inline uint32_t ord_u32(uint32_t bits) {
+    return (bits & 0x80000000u) ? ~bits : (bits | 0x80000000u);
+}
+
+// Decision key (Eq. 3): feasibility first, then utility, then the lower pair
+// index.  Maximising it as an unsigned integer is exact and associative.
+__device__ inline uint64_t decision_key(bool feasible, float u, int d) {
+    if (u != u) u = -__builtin_huge_valf();
+    if (u == 0.0f) u = 0.0f;
+    const uint64_t o = ord_u32(__float_as_uint(u));
+    return (static_cast<uint64_t>(feasible) << 63) | (o << 31) |
+           static_cast<uint64_t>(0x7FFFFFFF - d);
+}
+__device__ inline int key_pair(uint64_t k) { return 0x7FFFFFFF - static_cast<int>(k & 0x7FFFFFFFull); }
+__device__ inline bool key_feasible(uint64_t k) { return (k >> 63) != 0; }
+
+// ---------------------------------------------------------------- arguments
+struct QueryArgs {
+    int nq;                       // queries in this chunk
+    const int32_t *input_len;     // [nq]
+    const int32_t *nout;          // [nq]
+    const float *slo;             // [nq] or nullptr
+    float default_slo;
+};
+
+struct OutArgs {                  // per query; all but choice may be null
+    int32_t *choice;
+    uint8_t *feasible;
+    float *utility, *e2e, *ttft, *tpot;
+};
+
+struct StateArgs {
+    const hwr_hw_state *src;      // [N] (pinned host slot, device-visible)
+    int N, arch_width, gpu_width;
+    const int32_t *dep_model, *dep_gpu, *model_arch;
+    const float *params_b;
+    float *dep_f32;               // [N][32]
+    uint16_t *dep_bf16;           // [N][32]
+};
+
+struct QualityArgs {
+    int nq, D, M;
+    const void *emb;              // [nq][D] (bf16 bits or fp32)
+    const uint16_t *wq_pk;        // bf16 B-operand fragments
+    const float *wq;              // fp32 [D][M]
+    const float *bq;              // [M]
+    float *qmat;                  // [nq][M]
+};
+
+struct MlpArgs {                  // bf16 predictor (fused or staged)
+    int N, M, len_slot;
+    float alpha;
+    float b3_0, b3_1;
+    QueryArgs q;
+    const uint16_t *dep_bf16;     // [N][32]
+    const int32_t *dep_model;     // [N]
+    const float *qmat;            // [nq][M]
+    const uint16_t *w1_pk, *w2_pk;
+    const float *b1_pk, *b2_pk;
+    const uint32_t *w3_pk;
+    const uint16_t *X;            // staged input [nq][N][32]
+    float *cand_ttft, *cand_tpot; // [nq][N] (staged output or debug)
+    OutArgs out;
+    int nsplit;                   // pair ranges (grid.y); >1 writes partials
+    uint64_t *part_key;           // [nsplit][nq]
+    float *part_val;              // [nsplit][nq][4]
+};
+
+struct MlpF32Args {
+    int N, F, len_slot;
+    float b3_0, b3_1;
+    QueryArgs q;
+    const float *dep_f32;         // [N][32]
+    const float *w1, *b1, *w2, *b2, *w3;   // [F][H], [H], [H][H], [H], [H][2]
+    float *cand_ttft, *cand_tpot;
+};
+
+struct GatherArgs {
+    int N, len_slot;
+    QueryArgs q;
+    const uint16_t *dep_bf16;     // [N][32]
+    uint16_t *X;                  // [nq][N][32]
+};
+
+struct EpilogueArgs {
+    int N, M, group;
+    float alpha;
+    QueryArgs q;
+    const int32_t *dep_model;
+    const float *qmat;
+    const float *cand_ttft, *cand_tpot;
+    OutArgs out;
+};
+
+struct MergeArgs {
+    int nq, nsplit;
+    const uint64_t *part_key;
+    const float *part_val;
+    OutArgs out;
+};
+
+// Single query, all pairs: input and output records in pinned host memory.
+struct SingleIn {
+    uint32_t seq;
+    int32_t input_len, nout;
+    float slo;
+    uint32_t pad[4];
+    // followed by D bf16 embedding values (16-byte aligned)
+};
+struct SingleOut {
+    uint32_t seq;
+    int32_t choice;
+    uint32_t feasible;
+    float utility, e2e, ttft, tpot;
+    uint32_t pad;
+};
+
+struct SingleArgs {
+    int N, M, D, len_slot;
+    float alpha, b3_0, b3_1;
+    const SingleIn *in;           // device-visible pinned record
+    SingleOut *out;               // device-visible pinned record
+    const uint16_t *dep_bf16;
+    const int32_t *dep_model;
+    const uint16_t *wqT;          // [M][D] bf16
+    const float *bq;
+    const uint16_t *w1_pk, *w2_pk;
+    const float *b1_pk, *b2_pk;
+    const uint32_t *w3_pk;
+};
+
+// ---------------------------------------------------------------- launchers
+// Each returns the launch error (hipSuccess on success).
+hipError_t launch_state(const StateArgs &a, hipStream_t s);
+hipError_t launch_quality_bf16(const QualityArgs &a, hipStream_t s);
+hipError_t launch_quality_f32(const QualityArgs &a, hipStream_t s);
+hipError_t launch_mlp_bf16(int H, bool staged, const MlpArgs &a, hipStream_t s);
+hipError_t launch_mlp_f32(int H, const MlpF32Args &a, hipStream_t s);
+hipError_t launch_gather(const GatherArgs &a, hipStream_t s);
+hipError_t launch_epilogue(const EpilogueArgs &a, hipStream_t s);
+hipError_t launch_merge(const MergeArgs &a, hipStream_t s);
+hipError_t launch_single(int H, const SingleArgs &a, hipStream_t s);
+
+}  // namespace hwr

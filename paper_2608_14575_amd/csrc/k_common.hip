@@ -1,0 +1,243 @@
+// State ingest, feature gather, decision epilogue, split merge and the fp32
+// predictor / quality kernels of libhwr (gfx950).
+#include "hwr_device.hpp"
+
+namespace hwr {
+
+// ------------------------------------------------------------ state ingest
+// One thread per pair: the pair's slice of the Eq. 1 feature vector (model
+// and GPU one-hots, parameter count, Table 2 signals, GPU utilisation), in
+// fp32 and bf16.  The query slot (ln(input_len)/8) is left 0 here and filled
+// per candidate.  Logs are evaluated in fp64 and rounded once to fp32.
+__global__ __launch_bounds__(256) void k_state(StateArgs a) {
+    const int d = blockIdx.x * blockDim.x + threadIdx.x;
+    if (d >= a.N) return;
+    const hwr_hw_state s = a.src[d];
+    const int m = a.dep_model[d];
+    const int ia = a.model_arch[m];
+    const int ig = a.arch_width + a.dep_gpu[d];
+    const int b = a.arch_width + a.gpu_width;
+    const float v0 = static_cast<float>(log(static_cast<double>(a.params_b[m])) * 0.25);
+    const float v2 = static_cast<float>(log(1.0 + static_cast<double>(s.running_q)) * 0.5);
+    const float v3 = static_cast<float>(log(1.0 + static_cast<double>(s.waiting_q)) * 0.5);
+    const float v6 = static_cast<float>(log(static_cast<double>(s.ttft_avg_s)) * 0.25);
+    const float v7 = static_cast<float>(log(static_cast<double>(s.tpot_avg_s)) * 0.25);
+    float *rf = a.dep_f32 + static_cast<size_t>(d) * kFeatPad;
+    uint16_t *rb = a.dep_bf16 + static_cast<size_t>(d) * kFeatPad;
+#pragma unroll
+    for (int f = 0; f < kFeatPad; ++f) {
+        float v = 0.0f;
+        if (f == ia || f == ig) v = 1.0f;
+        if (f == b + 0) v = v0;
+        if (f == b + 2) v = v2;
+        if (f == b + 3) v = v3;
+        if (f == b + 4) v = s.kv_util;
+        if (f == b + 5) v = s.gpu_util;
+        if (f == b + 6) v = v6;
+        if (f == b + 7) v = v7;
+        rf[f] = v;
+        rb[f] = bf16_bits(v);
+    }
+}
+
+hipError_t launch_state(const StateArgs &a, hipStream_t s) {
+    hipLaunchKernelGGL(k_state, dim3((a.N + 255) / 256), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------ fp32 quality
+// Hardware-independent quality (Sec. 3.2 item 3): Q[q][m] = e_q . Wq[:, m] + bq[m].
+// fp32 workloads only (small); one thread per (query, model).
+__global__ __launch_bounds__(256) void k_quality_f32(QualityArgs a) {
+    const long idx = static_cast<long>(blockIdx.x) * blockDim.x + threadIdx.x;
+    const long q = idx / a.M;
+    const int m = static_cast<int>(idx - q * a.M);
+    if (q >= a.nq) return;
+    const float *e = static_cast<const float *>(a.emb) + q * a.D;
+    float acc = 0.0f;
+    for (int k = 0; k < a.D; ++k) acc = fmaf(e[k], a.wq[static_cast<size_t>(k) * a.M + m], acc);
+    a.qmat[q * a.M + m] = acc + a.bq[m];
+}
+
+hipError_t launch_quality_f32(const QualityArgs &a, hipStream_t s) {
+    const long total = static_cast<long>(a.nq) * a.M;
+    hipLaunchKernelGGL(k_quality_f32, dim3(static_cast<unsigned>((total + 255) / 256)), dim3(256), 0,
+                       s, a);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------ fp32 predictor
+// Eq. 1 predictor in fp32, one thread per candidate (q, d): features, two
+// hidden ReLU layers, the two heads, softplus.  Weights staged in LDS; the
+// first-layer rows are zero-padded to 32 slots.
+template <int H>
+__global__ __launch_bounds__(256) void k_mlp_f32(MlpF32Args a) {
+    __shared__ float s_w1[kFeatPad * H];
+    __shared__ float s_w2[H * H];
+    __shared__ float s_w3[H * 2];
+    __shared__ float s_b1[H];
+    __shared__ float s_b2[H];
+    for (int i = threadIdx.x; i < kFeatPad * H; i += blockDim.x)
+        s_w1[i] = (i / H) < a.F ? a.w1[i] : 0.0f;
+    for (int i = threadIdx.x; i < H * H; i += blockDim.x) s_w2[i] = a.w2[i];
+    for (int i = threadIdx.x; i < H * 2; i += blockDim.x) s_w3[i] = a.w3[i];
+    for (int i = threadIdx.x; i < H; i += blockDim.x) {
+        s_b1[i] = a.b1[i];
+        s_b2[i] = a.b2[i];
+    }
+    __syncthreads();
+    const long c = static_cast<long>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (c >= static_cast<long>(a.q.nq) * a.N) return;
+    const long q = c / a.N;
+    const int d = static_cast<int>(c - q * a.N);
+    float x[kFeatPad];
+    const float xl = len_feature(a.q.input_len[q]);
+#pragma unroll
+    for (int f = 0; f < kFeatPad; ++f) {
+        const float v = a.dep_f32[static_cast<size_t>(d) * kFeatPad + f];
+        x[f] = (f == a.len_slot) ? xl : v;
+    }
+    float h1[H];
+#pragma unroll
+    for (int j = 0; j < H; ++j) h1[j] = s_b1[j];
+#pragma unroll
+    for (int f = 0; f < kFeatPad; ++f) {
+#pragma unroll
+        for (int j = 0; j < H; ++j) h1[j] = fmaf(s_w1[f * H + j], x[f], h1[j]);
+    }
+#pragma unroll
+    for (int j = 0; j < H; ++j) h1[j] = fmaxf(h1[j], 0.0f);
+    float z0 = 0.0f, z1 = 0.0f;
+    for (int j = 0; j < H; ++j) {
+        float acc = s_b2[j];
+#pragma unroll
+        for (int i = 0; i < H; ++i) acc = fmaf(s_w2[i * H + j], h1[i], acc);
+        acc = fmaxf(acc, 0.0f);
+        z0 = fmaf(s_w3[2 * j + 0], acc, z0);
+        z1 = fmaf(s_w3[2 * j + 1], acc, z1);
+    }
+    a.cand_ttft[c] = softplus_f32(z0 + a.b3_0);
+    a.cand_tpot[c] = softplus_f32(z1 + a.b3_1);
+}
+
+hipError_t launch_mlp_f32(int H, const MlpF32Args &a, hipStream_t s) {
+    const long total = static_cast<long>(a.q.nq) * a.N;
+    const dim3 grid(static_cast<unsigned>((total + 255) / 256));
+    if (H == 64) hipLaunchKernelGGL(k_mlp_f32<64>, grid, dim3(256), 0, s, a);
+    else if (H == 128) hipLaunchKernelGGL(k_mlp_f32<128>, grid, dim3(256), 0, s, a);
+    else return hipErrorInvalidValue;
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------ feature gather
+// Staged pipeline: X[q][d][0:32] (bf16) = the pair's feature row with the
+// query's input-length slot filled in.  Each workgroup stages all pair rows
+// in LDS once and broadcasts them across kGatherQ queries; every thread
+// writes one 16-byte piece, consecutive threads consecutive pieces.
+__global__ __launch_bounds__(256) void k_gather(GatherArgs a) {
+    extern __shared__ uint4 s_dep[];          // [N][4]
+    __shared__ uint32_t s_xl[kGatherQ];
+    const uint4 *g = reinterpret_cast<const uint4 *>(a.dep_bf16);
+    for (int i = threadIdx.x; i < a.N * 4; i += blockDim.x) s_dep[i] = g[i];
+    const int q0 = blockIdx.x * kGatherQ;
+    if (threadIdx.x < kGatherQ && q0 + static_cast<int>(threadIdx.x) < a.q.nq)
+        s_xl[threadIdx.x] = bf16_bits(len_feature(a.q.input_len[q0 + threadIdx.x]));
+    __syncthreads();
+    const int nqb = min(kGatherQ, a.q.nq - q0);
+    const int per_q = a.N * 4;
+    const int total = nqb * per_q;
+    const int lpart = a.len_slot >> 3, lword = (a.len_slot & 7) >> 1, lhi = a.len_slot & 1;
+    uint4 *X = reinterpret_cast<uint4 *>(a.X);
+    for (int i = threadIdx.x; i < total; i += blockDim.x) {
+        const int qi = i / per_q;
+        const int rem = i - qi * per_q;
+        const int d = rem >> 2, part = rem & 3;
+        uint4 v = s_dep[d * 4 + part];
+        if (part == lpart) {
+            const uint32_t xl = s_xl[qi];
+            const uint32_t keep = lhi ? 0x0000FFFFu : 0xFFFF0000u;
+            const uint32_t put = lhi ? (xl << 16) : xl;
+            if (lword == 0) v.x = (v.x & keep) | put;
+            if (lword == 1) v.y = (v.y & keep) | put;
+            if (lword == 2) v.z = (v.z & keep) | put;
+            if (lword == 3) v.w = (v.w & keep) | put;
+        }
+        X[(static_cast<size_t>(q0 + qi) * a.N + d) * 4 + part] = v;
+    }
+}
+
+hipError_t launch_gather(const GatherArgs &a, hipStream_t s) {
+    const unsigned grid = static_cast<unsigned>((a.q.nq + kGatherQ - 1) / kGatherQ);
+    hipLaunchKernelGGL(k_gather, dim3(grid), dim3(256), static_cast<size_t>(a.N) * 64, s, a);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------ decision epilogue
+// Per query: cost (Eq. 2), bound test and utility for every pair, then the
+// Eq. 3 argmax as a maximum of packed decision keys, reduced across the
+// `group` lanes that share the query by wavefront shuffles.
+__global__ __launch_bounds__(256) void k_epilogue(EpilogueArgs a) {
+    const int G = a.group;
+    const long gid = static_cast<long>(blockIdx.x) * blockDim.x + threadIdx.x;
+    const long q = gid / G;
+    const int g = static_cast<int>(gid & (G - 1));
+    const bool valid = q < a.q.nq;
+    const long qc = valid ? q : 0;
+    const int32_t no = a.q.nout[qc];
+    const float nout = static_cast<float>(no < 0 ? 0 : no);
+    const float slo = a.q.slo ? a.q.slo[qc] : a.q.default_slo;
+    uint64_t best = 0;
+    if (valid) {
+        for (int d = g; d < a.N; d += G) {
+            const size_t ci = static_cast<size_t>(qc) * a.N + d;
+            const float Q = a.qmat[qc * a.M + a.dep_model[d]];
+            const Decision r = decide(a.cand_ttft[ci], a.cand_tpot[ci], nout, slo, Q, a.alpha);
+            const uint64_t k = decision_key(r.feasible, r.u, d);
+            best = k > best ? k : best;
+        }
+    }
+    for (int off = G >> 1; off >= 1; off >>= 1) {
+        const uint64_t o = shfl_xor_u64(best, off);
+        best = o > best ? o : best;
+    }
+    if (valid && g == 0) {
+        const int d = key_pair(best);
+        const size_t ci = static_cast<size_t>(qc) * a.N + d;
+        const float tt = a.cand_ttft[ci], tp = a.cand_tpot[ci];
+        const Decision r = decide(tt, tp, nout, slo, a.qmat[qc * a.M + a.dep_model[d]], a.alpha);
+        write_outputs(a.out, static_cast<int>(q), best, r.u, r.e2e, tt, tp);
+    }
+}
+
+hipError_t launch_epilogue(const EpilogueArgs &a, hipStream_t s) {
+    const long threads = static_cast<long>(a.q.nq) * a.group;
+    hipLaunchKernelGGL(k_epilogue, dim3(static_cast<unsigned>((threads + 255) / 256)), dim3(256), 0,
+                       s, a);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------ split merge
+// When the pairs of a chunk are split over several workgroups, each writes
+// its best key and values; this picks the maximum key per query.
+__global__ __launch_bounds__(256) void k_merge(MergeArgs a) {
+    const int q = blockIdx.x * blockDim.x + threadIdx.x;
+    if (q >= a.nq) return;
+    uint64_t best = 0;
+    int bs = 0;
+    for (int s = 0; s < a.nsplit; ++s) {
+        const uint64_t k = a.part_key[static_cast<size_t>(s) * a.nq + q];
+        if (k > best) {
+            best = k;
+            bs = s;
+        }
+    }
+    const float *v = a.part_val + (static_cast<size_t>(bs) * a.nq + q) * 4;
+    write_outputs(a.out, q, best, v[0], v[1], v[2], v[3]);
+}
+
+hipError_t launch_merge(const MergeArgs &a, hipStream_t s) {
+    hipLaunchKernelGGL(k_merge, dim3((a.nq + 255) / 256), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace hwr

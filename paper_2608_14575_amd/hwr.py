@@ -1,0 +1,260 @@
+"""ctypes binding of libhwr (include/hwr.h): the same entry points, argument
+marshalling only.  Every step of the routing path runs in the library's HIP
+kernels; if libhwr.so is missing this module raises instead of falling back.
+
+``Router`` is a convenience wrapper that fills ``hwr_config`` from numpy
+arrays and routes numpy (host) or torch (device) batches.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import Optional
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libhwr.so")
+
+HWR_OK, HWR_ERR_INVALID_ARG, HWR_ERR_OOM, HWR_ERR_HIP, HWR_ERR_STATE, HWR_ERR_UNSUPPORTED = 0, -1, -2, -3, -4, -5
+HWR_F32, HWR_BF16 = 0, 1
+HWR_MEM_DEVICE, HWR_MEM_HOST = 0, 1
+HWR_PIPE_FUSED, HWR_PIPE_STAGED = 0, 1
+HWR_FLAG_NO_GRAPH = 1
+HWR_K_STATE, HWR_K_QUALITY, HWR_K_GATHER, HWR_K_MLP, HWR_K_EPILOGUE, HWR_K_FUSED, HWR_K_MERGE, HWR_K_SINGLE = range(8)
+HWR_K_COUNT = 8
+KERNEL_NAMES = ["state", "quality", "gather", "mlp", "epilogue", "fused", "merge", "single"]
+
+EXPORTS = ["hwr_init", "hwr_update_hw_state", "hwr_route_batch", "hwr_free", "hwr_last_error",
+           "hwr_profile_enable", "hwr_profile_read"]
+
+_STATUS = {0: "HWR_OK", -1: "HWR_ERR_INVALID_ARG", -2: "HWR_ERR_OOM", -3: "HWR_ERR_HIP",
+           -4: "HWR_ERR_STATE", -5: "HWR_ERR_UNSUPPORTED"}
+
+
+class HwrError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{_STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+_vp = C.c_void_p
+_i32p = C.POINTER(C.c_int32)
+_f32p = C.POINTER(C.c_float)
+_u8p = C.POINTER(C.c_uint8)
+
+
+class hwr_hw_state(C.Structure):
+    _fields_ = [("running_q", C.c_int32), ("waiting_q", C.c_int32), ("kv_util", C.c_float),
+                ("gpu_util", C.c_float), ("ttft_avg_s", C.c_float), ("tpot_avg_s", C.c_float)]
+
+
+class hwr_config(C.Structure):
+    _fields_ = [("n_models", C.c_int32), ("n_gpu_types", C.c_int32), ("n_deployments", C.c_int32),
+                ("arch_width", C.c_int32), ("gpu_width", C.c_int32), ("embed_dim", C.c_int32),
+                ("feat_dim", C.c_int32), ("hidden", C.c_int32), ("emb_dtype", C.c_int32),
+                ("weight_dtype", C.c_int32), ("pipeline", C.c_int32), ("max_chunk", C.c_int32),
+                ("cost_weight", C.c_float), ("default_slo_s", C.c_float), ("device", C.c_int32),
+                ("flags", C.c_int32),
+                ("dep_model", _i32p), ("dep_gpu", _i32p), ("model_arch", _i32p),
+                ("model_params_b", _f32p), ("wq", _vp), ("bq", _f32p), ("w1", _vp), ("b1", _f32p),
+                ("w2", _vp), ("b2", _f32p), ("w3", _vp), ("b3", _f32p), ("stream", _vp)]
+
+
+class hwr_query_batch(C.Structure):
+    _fields_ = [("n", C.c_int32), ("mem", C.c_int32), ("emb", _vp), ("input_len", _vp),
+                ("expected_out_len", _vp), ("slo_s", _vp)]
+
+
+class hwr_route_result(C.Structure):
+    _fields_ = [("choice", _vp), ("feasible", _vp), ("utility", _vp), ("e2e_s", _vp),
+                ("ttft_s", _vp), ("tpot_s", _vp), ("cand_ttft", _vp), ("cand_tpot", _vp),
+                ("cand_quality", _vp)]
+
+
+class hwr_kernel_times(C.Structure):
+    _fields_ = [("ms", C.c_double * HWR_K_COUNT), ("launches", C.c_int64 * HWR_K_COUNT)]
+
+
+_lib = None
+
+
+def load(path: Optional[str] = None) -> C.CDLL:
+    """Load libhwr.so (in-tree).  Raises if it has not been built."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    p = path or LIB_PATH
+    if not os.path.exists(p):
+        raise RuntimeError(f"libhwr.so not found at {p}: build it first "
+                           "(python -m paper_2608_14575_amd.build); there is no fallback")
+    L = C.CDLL(p)
+    L.hwr_init.restype = C.c_int
+    L.hwr_init.argtypes = [C.POINTER(hwr_config), C.POINTER(_vp)]
+    L.hwr_update_hw_state.restype = C.c_int
+    L.hwr_update_hw_state.argtypes = [_vp, _vp, C.c_int32]
+    L.hwr_route_batch.restype = C.c_int
+    L.hwr_route_batch.argtypes = [_vp, C.POINTER(hwr_query_batch), C.POINTER(hwr_route_result)]
+    L.hwr_free.restype = None
+    L.hwr_free.argtypes = [_vp]
+    L.hwr_last_error.restype = C.c_char_p
+    L.hwr_last_error.argtypes = [_vp]
+    L.hwr_profile_enable.restype = C.c_int
+    L.hwr_profile_enable.argtypes = [_vp, C.c_int32]
+    L.hwr_profile_read.restype = C.c_int
+    L.hwr_profile_read.argtypes = [_vp, C.POINTER(hwr_kernel_times), C.c_int32]
+    if path is None:
+        _lib = L
+    return L
+
+
+def _check(status: int, ctx) -> None:
+    if status != HWR_OK:
+        raise HwrError(status, hwr_last_error(ctx))
+
+
+# ---------------------------------------------------------------- the C ABI, 1:1
+def hwr_init(cfg: hwr_config):
+    ctx = _vp()
+    st = load().hwr_init(C.byref(cfg), C.byref(ctx))
+    _check(st, None)
+    return ctx
+
+
+def hwr_update_hw_state(ctx, state: np.ndarray) -> None:
+    state = np.ascontiguousarray(state)
+    assert state.dtype.itemsize == 24
+    _check(load().hwr_update_hw_state(ctx, state.ctypes.data, int(state.shape[0])), ctx)
+
+
+def hwr_route_batch(ctx, batch: hwr_query_batch, result: hwr_route_result) -> None:
+    _check(load().hwr_route_batch(ctx, C.byref(batch), C.byref(result)), ctx)
+
+
+def hwr_free(ctx) -> None:
+    load().hwr_free(ctx)
+
+
+def hwr_last_error(ctx) -> str:
+    m = load().hwr_last_error(ctx)
+    return m.decode() if m else ""
+
+
+def hwr_profile_enable(ctx, enable: bool) -> None:
+    _check(load().hwr_profile_enable(ctx, 1 if enable else 0), ctx)
+
+
+def hwr_profile_read(ctx, reset: bool = True) -> dict:
+    t = hwr_kernel_times()
+    _check(load().hwr_profile_read(ctx, C.byref(t), 1 if reset else 0), ctx)
+    return {KERNEL_NAMES[k]: (t.ms[k], int(t.launches[k])) for k in range(HWR_K_COUNT)}
+
+
+# ---------------------------------------------------------------- convenience
+def _ptr(a) -> int:
+    if a is None:
+        return 0
+    if isinstance(a, np.ndarray):
+        return a.ctypes.data
+    return int(a.data_ptr())   # torch tensor
+
+
+class Router:
+    """Owns one hwr context.  Arrays follow include/hwr.h: weights row-major
+    ([D][M], [F][H], [H][H], [H][2]) as uint16 bf16 bits (bf16) or float32."""
+
+    def __init__(self, *, dep_model, dep_gpu, model_arch, model_params_b, wq, bq, w1, b1, w2, b2,
+                 w3, b3, arch_width: int, gpu_width: int, n_gpu_types: int, dtype: str,
+                 cost_weight: float = 0.5, default_slo_s: float = 1.0, pipeline: str = "fused",
+                 max_chunk: int = 65536, stream: int = 0, flags: int = 0, device: int = 0):
+        wdt = np.uint16 if dtype == "bf16" else np.float32
+        keep = dict(dep_model=np.ascontiguousarray(dep_model, np.int32),
+                    dep_gpu=np.ascontiguousarray(dep_gpu, np.int32),
+                    model_arch=np.ascontiguousarray(model_arch, np.int32),
+                    model_params_b=np.ascontiguousarray(model_params_b, np.float32),
+                    wq=np.ascontiguousarray(wq, wdt), bq=np.ascontiguousarray(bq, np.float32),
+                    w1=np.ascontiguousarray(w1, wdt), b1=np.ascontiguousarray(b1, np.float32),
+                    w2=np.ascontiguousarray(w2, wdt), b2=np.ascontiguousarray(b2, np.float32),
+                    w3=np.ascontiguousarray(w3, wdt), b3=np.ascontiguousarray(b3, np.float32))
+        D, M = keep["wq"].shape
+        F, H = keep["w1"].shape
+        N = keep["dep_model"].shape[0]
+        cfg = hwr_config()
+        cfg.n_models, cfg.n_gpu_types, cfg.n_deployments = M, int(n_gpu_types), N
+        cfg.arch_width, cfg.gpu_width = int(arch_width), int(gpu_width)
+        cfg.embed_dim, cfg.feat_dim, cfg.hidden = D, F, H
+        cfg.emb_dtype = cfg.weight_dtype = HWR_BF16 if dtype == "bf16" else HWR_F32
+        cfg.pipeline = HWR_PIPE_STAGED if pipeline == "staged" else HWR_PIPE_FUSED
+        cfg.max_chunk = int(max_chunk)
+        cfg.cost_weight, cfg.default_slo_s = float(cost_weight), float(default_slo_s)
+        cfg.device, cfg.flags = int(device), int(flags)
+        for k in ("dep_model", "dep_gpu", "model_arch"):
+            setattr(cfg, k, keep[k].ctypes.data_as(_i32p))
+        for k in ("model_params_b", "bq", "b1", "b2", "b3"):
+            setattr(cfg, k, keep[k].ctypes.data_as(_f32p))
+        for k in ("wq", "w1", "w2", "w3"):
+            setattr(cfg, k, keep[k].ctypes.data)
+        cfg.stream = int(stream)
+        self.M, self.N, self.D, self.dtype = M, N, D, dtype
+        self.ctx = hwr_init(cfg)
+
+    @classmethod
+    def from_problem(cls, pb, **kw) -> "Router":
+        """Build from a generator problem (paper_2608_14575_amd.synth.Problem)."""
+        sp = pb.spec
+        kw.setdefault("cost_weight", sp.cost_weight)
+        kw.setdefault("default_slo_s", sp.slo_value)
+        return cls(dep_model=pb.dep_model, dep_gpu=pb.dep_gpu, model_arch=pb.model_arch,
+                   model_params_b=pb.model_params_b, wq=pb.wq_bits, bq=pb.bq, w1=pb.w1_bits,
+                   b1=pb.b1, w2=pb.w2_bits, b2=pb.b2, w3=pb.w3_bits, b3=pb.b3,
+                   arch_width=sp.arch_width, gpu_width=sp.gpu_width, n_gpu_types=sp.n_gpu_types,
+                   dtype=sp.dtype, **kw)
+
+    def close(self) -> None:
+        if getattr(self, "ctx", None):
+            hwr_free(self.ctx)
+            self.ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def update(self, state: np.ndarray) -> None:
+        hwr_update_hw_state(self.ctx, state)
+
+    def profile(self, enable: bool = True) -> None:
+        hwr_profile_enable(self.ctx, enable)
+
+    def profile_read(self, reset: bool = True) -> dict:
+        return hwr_profile_read(self.ctx, reset)
+
+    def route(self, emb, input_len, expected_out_len, slo_s=None, *, mem: int,
+              choice, feasible=None, utility=None, e2e_s=None, ttft_s=None, tpot_s=None,
+              cand_ttft=None, cand_tpot=None, cand_quality=None) -> None:
+        """Route into caller-owned outputs (numpy for HWR_MEM_HOST, torch
+        tensors on the device for HWR_MEM_DEVICE)."""
+        n = int(input_len.shape[0])
+        b = hwr_query_batch(n, mem, _ptr(emb), _ptr(input_len), _ptr(expected_out_len), _ptr(slo_s))
+        r = hwr_route_result(_ptr(choice), _ptr(feasible), _ptr(utility), _ptr(e2e_s), _ptr(ttft_s),
+                             _ptr(tpot_s), _ptr(cand_ttft), _ptr(cand_tpot), _ptr(cand_quality))
+        hwr_route_batch(self.ctx, b, r)
+
+    def route_host(self, emb, input_len, expected_out_len, slo_s=None, candidates: bool = False) -> dict:
+        """Route numpy inputs; returns numpy outputs (synchronous)."""
+        n = int(np.shape(input_len)[0])
+        wdt = np.uint16 if self.dtype == "bf16" else np.float32
+        emb = np.ascontiguousarray(emb, wdt)
+        il = np.ascontiguousarray(input_len, np.int32)
+        no = np.ascontiguousarray(expected_out_len, np.int32)
+        slo = None if slo_s is None else np.ascontiguousarray(slo_s, np.float32)
+        out = dict(choice=np.full(n, -1, np.int32), feasible=np.zeros(n, np.uint8),
+                   utility=np.zeros(n, np.float32), e2e_s=np.zeros(n, np.float32),
+                   ttft_s=np.zeros(n, np.float32), tpot_s=np.zeros(n, np.float32))
+        if candidates:
+            out.update(cand_ttft=np.zeros((n, self.N), np.float32),
+                       cand_tpot=np.zeros((n, self.N), np.float32),
+                       cand_quality=np.zeros((n, self.M), np.float32))
+        self.route(emb, il, no, slo, mem=HWR_MEM_HOST, **out)
+        return out

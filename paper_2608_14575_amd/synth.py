@@ -125,11 +125,13 @@ def spec(name: str, **overrides) -> Spec:
 
 # ---------------------------------------------------------------- bf16 bits
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
-    """Round fp32 values to the nearest bf16 (ties to even); return raw bits."""
+    """Round finite fp32 values to the nearest bf16 (ties to even); return raw
+    bits.  (For finite inputs the 32-bit sum below cannot overflow.)"""
     u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
-    lsb = (u >> np.uint32(16)) & np.uint32(1)
-    r = (u.astype(np.uint64) + np.uint64(0x7FFF) + lsb.astype(np.uint64)) >> np.uint64(16)
-    return r.astype(np.uint16)
+    if not np.isfinite(x).all():
+        raise ValueError("non-finite input")
+    r = u + (np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1)))
+    return (r >> np.uint32(16)).astype(np.uint16)
 
 
 def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:

@@ -1,0 +1,146 @@
+"""C-ABI contract checks that need no GPU: the library loads and exports every
+function include/hwr.h declares, the ctypes structures match the C layout,
+and argument errors come back as status codes (no device touched)."""
+import ctypes as C
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+from paper_2608_14575_amd import hwr
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "hwr.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(hwr.LIB_PATH):
+        from paper_2608_14575_amd import build
+        build.build()
+    return hwr.load()
+
+
+def _declared():
+    txt = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:hwr_status|void|const char \*)\s*(hwr_\w+)\s*\(", txt, re.M)))
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = _declared()
+    assert set(names) == set(hwr.EXPORTS), names
+    out = subprocess.run(["nm", "-D", "--defined-only", hwr.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (hwr_\w+)", out))
+    for n in names:
+        assert n in exported, n
+        assert hasattr(lib, n)
+
+
+def test_struct_layout_matches_header(tmp_path):
+    """offsetof / sizeof from the C compiler against the ctypes mirror."""
+    fields = {
+        "hwr_hw_state": [f for f, _ in hwr.hwr_hw_state._fields_],
+        "hwr_config": [f for f, _ in hwr.hwr_config._fields_],
+        "hwr_query_batch": [f for f, _ in hwr.hwr_query_batch._fields_],
+        "hwr_route_result": [f for f, _ in hwr.hwr_route_result._fields_],
+        "hwr_kernel_times": [f for f, _ in hwr.hwr_kernel_times._fields_],
+    }
+    src = ['#include <stdio.h>', '#include <stddef.h>', '#include "hwr.h"', "int main(void) {"]
+    for s, fl in fields.items():
+        src.append(f'printf("{s} sizeof %zu\\n", sizeof({s}));')
+        for f in fl:
+            src.append(f'printf("{s} {f} %zu\\n", offsetof({s}, {f}));')
+    src.append("return 0; }")
+    c = tmp_path / "layout.c"
+    c.write_text("\n".join(src))
+    exe = tmp_path / "layout"
+    subprocess.check_call(["gcc", "-std=c11", f"-I{os.path.join(ROOT, 'include')}", str(c), "-o", str(exe)])
+    got = {}
+    for line in subprocess.check_output([str(exe)], text=True).splitlines():
+        s, f, v = line.split()
+        got[(s, f)] = int(v)
+    for s, fl in fields.items():
+        cls = getattr(hwr, s)
+        assert got[(s, "sizeof")] == C.sizeof(cls), s
+        for f in fl:
+            assert got[(s, f)] == getattr(cls, f).offset, (s, f)
+    assert got[("hwr_hw_state", "sizeof")] == 24
+
+
+def _valid_cfg(keep):
+    M, G, N, D, F, H = 2, 2, 4, 64, 24, 64
+    keep.update(dep_model=np.array([0, 0, 1, 1], np.int32), dep_gpu=np.array([0, 1, 0, 1], np.int32),
+                arch=np.array([0, 1], np.int32), params=np.array([7.0, 14.0], np.float32),
+                wq=np.zeros((D, M), np.uint16), bq=np.zeros(M, np.float32),
+                w1=np.zeros((F, H), np.uint16), w2=np.zeros((H, H), np.uint16),
+                w3=np.zeros((H, 2), np.uint16), b=np.zeros(H, np.float32), b3=np.zeros(2, np.float32))
+    cfg = hwr.hwr_config()
+    cfg.n_models, cfg.n_gpu_types, cfg.n_deployments = M, G, N
+    cfg.arch_width, cfg.gpu_width, cfg.embed_dim, cfg.feat_dim, cfg.hidden = 4, 3, D, F, H
+    cfg.emb_dtype = cfg.weight_dtype = hwr.HWR_BF16
+    cfg.cost_weight, cfg.default_slo_s = 0.5, 1.5
+    i32 = C.POINTER(C.c_int32)
+    f32 = C.POINTER(C.c_float)
+    cfg.dep_model = keep["dep_model"].ctypes.data_as(i32)
+    cfg.dep_gpu = keep["dep_gpu"].ctypes.data_as(i32)
+    cfg.model_arch = keep["arch"].ctypes.data_as(i32)
+    cfg.model_params_b = keep["params"].ctypes.data_as(f32)
+    cfg.wq, cfg.w1, cfg.w2, cfg.w3 = (keep[k].ctypes.data for k in ("wq", "w1", "w2", "w3"))
+    cfg.bq = keep["bq"].ctypes.data_as(f32)
+    cfg.b1 = cfg.b2 = keep["b"].ctypes.data_as(f32)
+    cfg.b3 = keep["b3"].ctypes.data_as(f32)
+    return cfg
+
+
+@pytest.mark.parametrize("mutate,status", [
+    (lambda c, k: setattr(c, "n_deployments", 0), hwr.HWR_ERR_INVALID_ARG),
+    (lambda c, k: k["dep_model"].__setitem__(2, 5), hwr.HWR_ERR_INVALID_ARG),
+    (lambda c, k: k["dep_gpu"].__setitem__(0, -1), hwr.HWR_ERR_INVALID_ARG),
+    (lambda c, k: k["arch"].__setitem__(1, 4), hwr.HWR_ERR_INVALID_ARG),
+    (lambda c, k: k["params"].__setitem__(0, 0.0), hwr.HWR_ERR_INVALID_ARG),
+    (lambda c, k: setattr(c, "feat_dim", 14), hwr.HWR_ERR_INVALID_ARG),
+    (lambda c, k: setattr(c, "default_slo_s", float("nan")), hwr.HWR_ERR_INVALID_ARG),
+    (lambda c, k: setattr(c, "cost_weight", -1.0), hwr.HWR_ERR_INVALID_ARG),
+    (lambda c, k: setattr(c, "w2", None), hwr.HWR_ERR_INVALID_ARG),
+    (lambda c, k: setattr(c, "hidden", 96), hwr.HWR_ERR_UNSUPPORTED),
+    (lambda c, k: setattr(c, "embed_dim", 100), hwr.HWR_ERR_UNSUPPORTED),
+    (lambda c, k: setattr(c, "feat_dim", 40), hwr.HWR_ERR_UNSUPPORTED),
+    (lambda c, k: setattr(c, "emb_dtype", hwr.HWR_F32), hwr.HWR_ERR_UNSUPPORTED),
+])
+def test_config_errors_are_status_codes(lib, mutate, status):
+    keep = {}
+    cfg = _valid_cfg(keep)
+    mutate(cfg, keep)
+    ctx = C.c_void_p()
+    st = lib.hwr_init(C.byref(cfg), C.byref(ctx))
+    assert st == status
+    assert not ctx.value
+    assert lib.hwr_last_error(None)
+
+
+def test_null_arguments(lib):
+    ctx = C.c_void_p()
+    assert lib.hwr_init(None, C.byref(ctx)) == hwr.HWR_ERR_INVALID_ARG
+    assert lib.hwr_update_hw_state(None, None, 0) == hwr.HWR_ERR_INVALID_ARG
+    assert lib.hwr_route_batch(None, None, None) == hwr.HWR_ERR_INVALID_ARG
+    assert lib.hwr_profile_enable(None, 1) == hwr.HWR_ERR_INVALID_ARG
+    lib.hwr_free(None)
+
+
+def test_no_device_is_a_clean_error(lib):
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a device is present")
+    keep = {}
+    cfg = _valid_cfg(keep)
+    ctx = C.c_void_p()
+    assert lib.hwr_init(C.byref(cfg), C.byref(ctx)) == hwr.HWR_ERR_HIP
+    assert b"device" in lib.hwr_last_error(None)
+
+
+def test_binding_fails_loudly_without_library(tmp_path):
+    with pytest.raises(RuntimeError, match="no fallback"):
+        hwr.load(str(tmp_path / "missing.so"))

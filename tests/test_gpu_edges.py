@@ -1,0 +1,199 @@
+"""GPU edge cases and invariants of the C ABI: error paths, empty and ragged
+batches, chunking and workgroup-split invariance (bit-exact), fused vs
+staged, host vs device memory, degenerate decisions, maximum sizes."""
+import numpy as np
+import pytest
+
+from paper_2608_14575_amd import hwr
+from paper_2608_14575_amd import synth as S
+
+import gpu_util as G
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _device():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a device"
+    hwr.load()
+    yield
+
+
+def _same(a: dict, b: dict, keys=None):
+    for k in keys or a.keys():
+        assert np.array_equal(a[k], b[k]), k
+
+
+def _case(name="C2", seed=9, **kw):
+    sp = S.spec(name, **kw)
+    return sp, S.make_problem(sp, seed), S.make_state(sp, seed), S.make_queries(sp, seed)
+
+
+def test_route_before_state_and_bad_state():
+    sp, pb, st, qs = _case(n_queries=64)
+    r = G.make_router(pb)
+    with pytest.raises(hwr.HwrError) as e:
+        r.route_host(qs.emb_bits, qs.input_len, qs.expected_out_len, qs.slo_s)
+    assert e.value.status == hwr.HWR_ERR_STATE
+    r.update(st)
+    before = r.route_host(qs.emb_bits, qs.input_len, qs.expected_out_len, qs.slo_s)
+    for field, val in (("kv_util", 1.5), ("ttft_avg_s", np.nan), ("waiting_q", -1), ("tpot_avg_s", 0.0)):
+        bad = st.copy()
+        bad[field][3] = val
+        with pytest.raises(hwr.HwrError) as e:
+            r.update(bad)
+        assert e.value.status == hwr.HWR_ERR_INVALID_ARG
+    with pytest.raises(hwr.HwrError):
+        r.update(st[:-1])
+    after = r.route_host(qs.emb_bits, qs.input_len, qs.expected_out_len, qs.slo_s)
+    _same(before, after)
+
+
+def test_bad_host_queries_rejected():
+    sp, pb, st, qs = _case(n_queries=8)
+    r = G.make_router(pb)
+    r.update(st)
+    il = qs.input_len.copy()
+    il[2] = 0
+    with pytest.raises(hwr.HwrError):
+        r.route_host(qs.emb_bits, il, qs.expected_out_len, qs.slo_s)
+    slo = qs.slo_s.copy()
+    slo[1] = -1.0
+    with pytest.raises(hwr.HwrError):
+        r.route_host(qs.emb_bits, qs.input_len, qs.expected_out_len, slo)
+
+
+def test_empty_batch_is_noop():
+    sp, pb, st, qs = _case(n_queries=4)
+    r = G.make_router(pb)
+    r.update(st)
+    out = r.route_host(qs.emb_bits[:0], qs.input_len[:0], qs.expected_out_len[:0], qs.slo_s[:0])
+    assert out["choice"].shape == (0,)
+
+
+@pytest.mark.parametrize("pipeline", ["fused", "staged"])
+def test_chunking_is_invisible(pipeline):
+    sp, pb, st, qs = _case(n_queries=333)
+    a = G.make_router(pb, pipeline=pipeline)
+    b = G.make_router(pb, pipeline=pipeline, max_chunk=100)
+    a.update(st)
+    b.update(st)
+    _same(G.route_device(a, qs, "bf16"), G.route_device(b, qs, "bf16"))
+
+
+def test_fused_equals_staged_and_split_equals_unsplit():
+    """Same arithmetic per candidate in every mode: bit-identical outputs.
+    40 queries over 64 pairs makes the fused kernel split the pairs over
+    workgroups and merge their keys."""
+    sp, pb, st, qs = _case("C3", n_queries=40, seed=12)
+    f = G.make_router(pb, pipeline="fused")
+    s = G.make_router(pb, pipeline="staged")
+    f.update(st)
+    s.update(st)
+    of, os_ = G.route_device(f, qs, "bf16"), G.route_device(s, qs, "bf16")
+    _same(of, os_)
+    rep = G.check(pb, st, qs, of)
+    assert rep.ok, rep.failures[:5]
+
+
+def test_debug_outputs_do_not_change_decisions_and_repeat_exactly():
+    sp, pb, st, qs = _case(n_queries=500)
+    r = G.make_router(pb)
+    r.update(st)
+    with_c = G.route_device(r, qs, "bf16", candidates=True)
+    without = G.route_device(r, qs, "bf16", candidates=False)
+    again = G.route_device(r, qs, "bf16", candidates=False)
+    _same(without, {k: with_c[k] for k in without})
+    _same(without, again)
+
+
+def test_host_equals_device():
+    sp, pb, st, qs = _case(n_queries=257)
+    r = G.make_router(pb)
+    r.update(st)
+    d = G.route_device(r, qs, "bf16", candidates=True)
+    h = r.route_host(qs.emb_bits, qs.input_len, qs.expected_out_len, qs.slo_s, candidates=True)
+    _same(d, h)
+
+
+def test_default_slo_used_when_absent():
+    sp, pb, st, qs = _case(n_queries=64)
+    r = G.make_router(pb, default_slo_s=1.5)
+    r.update(st)
+    a = G.route_device(r, qs, "bf16", with_slo=False)
+    qs.slo_s[:] = 1.5
+    b = G.route_device(r, qs, "bf16")
+    _same(a, b)
+
+
+def test_all_infeasible_falls_back():
+    sp, pb, st, qs = _case(n_queries=128)
+    qs.slo_s[:] = 1e-4
+    r = G.make_router(pb)
+    r.update(st)
+    out = G.route_device(r, qs, "bf16")
+    assert not out["feasible"].any()
+    rep = G.check(pb, st, qs, out)
+    assert rep.ok, rep.failures[:5]
+
+
+def test_duplicate_pairs_go_to_lowest_index():
+    sp = S.spec("C2", n_queries=96, n_models=2, n_gpu_types=2)
+    pb, st, qs = S.make_problem(sp, 14), S.make_state(sp, 14), S.make_queries(sp, 14)
+    pb.dep_model[:] = [0, 0, 1, 1]
+    pb.dep_gpu[:] = [0, 0, 1, 1]
+    st[1] = st[0]
+    st[3] = st[2]
+    r = G.make_router(pb)
+    r.update(st)
+    out = G.route_device(r, qs, "bf16")
+    assert set(np.unique(out["choice"]).tolist()) <= {0, 2}
+    assert np.array_equal(out["cand_ttft"][:, 0], out["cand_ttft"][:, 1])
+
+
+def test_single_pair():
+    sp, pb, st, qs = _case(n_queries=50, n_models=1, n_gpu_types=1)
+    r = G.make_router(pb)
+    r.update(st)
+    assert (G.route_device(r, qs, "bf16")["choice"] == 0).all()
+
+
+def test_pair_permutation_maps_choice():
+    sp, pb, st, qs = _case(n_queries=200, seed=21)
+    r = G.make_router(pb)
+    r.update(st)
+    base = G.route_device(r, qs, "bf16")
+    perm = np.random.default_rng(3).permutation(pb.n_deployments)
+    pb2 = S.make_problem(sp, 21)
+    pb2.dep_model, pb2.dep_gpu = pb.dep_model[perm].copy(), pb.dep_gpu[perm].copy()
+    r2 = G.make_router(pb2)
+    r2.update(st[perm].copy())
+    out = G.route_device(r2, qs, "bf16")
+    # identical per-candidate arithmetic -> identical decisions up to the relabelling
+    assert np.array_equal(perm[out["choice"]], base["choice"])
+
+
+def test_maximum_shape():
+    """1024 pairs (32 models x 8 GPU types, each pair listed 4 times with its
+    own state), D = 8192, H = 256; ragged query count."""
+    sp = S.spec("C5", n_queries=37, embed_dim=8192)
+    pb = S.make_problem(sp, 31)
+    pb.dep_model = np.tile(pb.dep_model, 4)
+    pb.dep_gpu = np.tile(pb.dep_gpu, 4)
+    st = np.concatenate([S.make_state(sp, 31 + k) for k in range(4)])
+    qs = S.make_queries(sp, 31)
+    r = G.make_router(pb)
+    r.update(st)
+    out = G.route_device(r, qs, "bf16")
+    rep = G.check(pb, st, qs, out)
+    print(f"[parity] max shape: {rep.summary()}", flush=True)
+    assert rep.ok, rep.failures[:5]
+
+
+def test_unsupported_shapes_are_rejected():
+    sp = S.spec("C2", n_queries=4, hidden=96)
+    pb = S.make_problem(sp, 1)
+    with pytest.raises(hwr.HwrError) as e:
+        G.make_router(pb)
+    assert e.value.status == hwr.HWR_ERR_UNSUPPORTED

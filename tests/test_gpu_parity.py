@@ -1,0 +1,133 @@
+"""GPU parity: the HIP library (through its C ABI) against the CPU oracle on
+seeded workloads of the synthetic configurations, under the acceptance rule
+in tests/parity.py (fp32 1e-4, bf16 1e-2 relative)."""
+import numpy as np
+import pytest
+
+from paper_2608_14575_amd import hwr
+from paper_2608_14575_amd import synth as S
+
+import gpu_util as G
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _device():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a device"
+    hwr.load()
+    yield
+
+
+def _report(name, rep):
+    print(f"[parity] {name}: {rep.summary()}", flush=True)
+    assert rep.ok, rep.failures[:8]
+
+
+def test_c1_fp32_host_full():
+    sp = S.spec("C1")
+    pb, st, qs = S.make_problem(sp, 1), S.make_state(sp, 1), S.make_queries(sp, 1)
+    r = G.make_router(pb)
+    r.update(st)
+    out = r.route_host(qs.emb_bits, qs.input_len, qs.expected_out_len, qs.slo_s, candidates=True)
+    rep = G.check(pb, st, qs, out)
+    _report("C1 fp32 host", rep)
+    assert rep.max_rel_ttft < 1e-5 and rep.max_rel_tpot < 1e-5
+
+
+@pytest.mark.parametrize("pipeline", ["fused", "staged"])
+def test_c2_bf16_device_full(pipeline):
+    sp = S.spec("C2")
+    pb, st, qs = S.make_problem(sp, 2), S.make_state(sp, 2), S.make_queries(sp, 2)
+    r = G.make_router(pb, pipeline=pipeline)
+    r.update(st)
+    out = G.route_device(r, qs, sp.dtype)
+    rep = G.check(pb, st, qs, out)
+    _report(f"C2 bf16 {pipeline}", rep)
+    # the oracle rounds at the same points, so errors sit far below the bound
+    assert rep.max_rel_ttft < 2e-3 and rep.max_rel_tpot < 2e-3
+
+
+@pytest.mark.parametrize("pipeline", ["fused", "staged"])
+def test_c3_shape_ragged_tail(pipeline):
+    """H = 256, 64 pairs, 300 queries: two workgroups, the second ragged."""
+    sp = S.spec("C3", n_queries=300)
+    pb, st, qs = S.make_problem(sp, 3), S.make_state(sp, 3), S.make_queries(sp, 3)
+    r = G.make_router(pb, pipeline=pipeline)
+    r.update(st)
+    out = G.route_device(r, qs, sp.dtype)
+    _report(f"C3-shape ragged {pipeline}", G.check(pb, st, qs, out))
+
+
+def test_c3_full_size_sampled():
+    sp = S.spec("C3")
+    pb, st, qs = S.make_problem(sp, 1), S.make_state(sp, 1), S.make_queries(sp, 1)
+    r = G.make_router(pb)
+    r.update(st)
+    out = G.route_device(r, qs, sp.dtype, candidates=False)
+    idx = np.arange(0, qs.n, 256) + (np.arange(qs.n // 256) % 256)
+    sub = {k: v[idx] for k, v in out.items()}
+    _report("C3 full, sampled", G.check(pb, st, qs.take(idx), sub, query_ids=idx))
+
+
+def test_c5_full_size_sampled():
+    """1,048,576 queries x 256 pairs in 65,536-query chunks, the launch
+    configuration the benchmark times; parity on a strided sample."""
+    import torch
+    sp = S.spec("C5")
+    pb, st = S.make_problem(sp, 5), S.make_state(sp, 5)
+    r = G.make_router(pb, max_chunk=sp.n_queries)
+    r.update(st)
+    n = sp.total_queries
+    dev = torch.device("cuda")
+    emb = torch.empty((n, sp.embed_dim), dtype=torch.int16, device=dev)
+    il = torch.empty(n, dtype=torch.int32, device=dev)
+    no = torch.empty(n, dtype=torch.int32, device=dev)
+    slo = torch.empty(n, dtype=torch.float32, device=dev)
+    samples = []
+    for c in range(sp.n_chunks):
+        qs = S.make_queries(sp, 5, chunk=c)
+        a, b = c * sp.n_queries, (c + 1) * sp.n_queries
+        emb[a:b] = torch.from_numpy(qs.emb_bits.view(np.int16)).to(dev)
+        il[a:b] = torch.from_numpy(qs.input_len).to(dev)
+        no[a:b] = torch.from_numpy(qs.expected_out_len).to(dev)
+        slo[a:b] = torch.from_numpy(qs.slo_s).to(dev)
+        local = np.arange(7 * c % 4096, sp.n_queries, 4096)[:16]
+        samples.append((a + local, qs.take(local)))
+    out = G.dev_outputs(n, r.N, r.M, False)
+    r.route(emb, il, no, slo, mem=hwr.HWR_MEM_DEVICE, **out)
+    torch.cuda.synchronize()
+    out = {k: v.cpu().numpy() for k, v in out.items()}
+    idx = np.concatenate([s[0] for s in samples])
+    qsub = S.Queries(*(np.concatenate([getattr(s[1], f) for s in samples])
+                       for f in ("emb", "emb_bits", "input_len", "expected_out_len", "slo_s")))
+    sub = {k: v[idx] for k, v in out.items()}
+    _report("C5 full, sampled", G.check(pb, st, qsub, sub, query_ids=idx))
+    assert (out["choice"] >= 0).all() and (out["choice"] < r.N).all()
+
+
+@pytest.mark.parametrize("flags", [0, hwr.HWR_FLAG_NO_GRAPH])
+def test_c4_single_query_walk(flags):
+    """Sequential single-query calls with a state update between each."""
+    sp = S.spec("C4")
+    pb = S.make_problem(sp, 4)
+    walk = S.StateWalk(sp, 4)
+    r = G.make_router(pb, flags=flags)
+    qs_all = S.make_queries(sp, 4, n=200)
+    from oracle import oracle as O
+    import parity
+    exact = elig = 0
+    for i in range(200):
+        st = walk.step()
+        r.update(st)
+        qs = qs_all.slice(i, i + 1)
+        out = r.route_host(qs.emb_bits, qs.input_len, qs.expected_out_len, qs.slo_s)
+        orc = O.route_synth(pb, st, qs)
+        rep = parity.compare(out, orc, slo=qs.slo_s, alpha=sp.cost_weight, dep_model=pb.dep_model,
+                             rtol=1e-2)
+        assert rep.ok, (i, rep.failures)
+        elig += rep.eligible
+        exact += rep.exact
+    print(f"[parity] C4 single-query walk flags={flags}: eligible {elig}/200 exact {exact}", flush=True)
+    assert elig > 100
