@@ -189,6 +189,20 @@ def cpu_baseline(pb, st, sample, sp):
                       f"({cands} candidates, {dt:.1f} s, one thread)"}
 
 
+def copy_probe(torch) -> int:
+    """A plain device-to-device copy of 1 GiB, three times: the reference
+    for scaling the FETCH_SIZE / WRITE_SIZE counters to bytes."""
+    nbytes = 1 << 30
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes_read": nbytes, "copy_probe_bytes_written": nbytes,
+                      "launches": 3}), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -201,6 +215,8 @@ def main() -> int:
     ap.add_argument("--cpu-sample", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-single", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="only run a plain device copy of known size (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -212,8 +228,10 @@ def main() -> int:
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         return 2
-    hwr.load()
     torch.cuda.set_device(0)
+    if args.copy_probe:
+        return copy_probe(torch)
+    hwr.load()
     res, pb, st, sample, sp = throughput(args, S, hwr, torch)
     log(f"throughput {res['value']:.3e} candidates/s, predictor {res['roofline']['achieved']:.1f} TFLOP/s")
     single = None if args.no_single else single_query(args, S, hwr, torch)
