@@ -15,7 +15,8 @@ constexpr int kFeatPad = 32;     // feature slots padded to two 16-wide MFMA k-b
 constexpr int kQualTile = 32;    // quality GEMM: models padded to one 32-wide tile
 constexpr int kBlock = 256;      // threads per workgroup of the batch kernels
 constexpr int kQPerWave = 64;    // fused predictor: queries per wave (two 32-column tiles)
-constexpr int kQPerBlock = kQPerWave * (kBlock / 64);
+constexpr int kQPerBlock = kQPerWave * 4;   // four query sub-blocks per workgroup
+constexpr int kMlpThreads = 512;             // predictor workgroup: 8 waves, two per SIMD
 constexpr int kGatherQ = 16;     // feature gather: queries per workgroup
 constexpr int kMaxPairs = 1024;
 constexpr int kMaxModels = 32;

@@ -85,8 +85,11 @@ hipError_t launch_quality_bf16(const QualityArgs &a, hipStream_t s) {
 
 // ------------------------------------------------------------ predictor
 // Eq. 1 cost predictor on MFMA tiles, for all (query, pair) candidates of a
-// chunk.  Workgroup: 4 waves x 64 queries; each wave loops over the pairs of
-// its range, evaluating 2 x 32 candidates (one pair, 64 queries) per step:
+// chunk.  Workgroup: 8 waves, two per SIMD.  Waves w and w + 4 take the same
+// 64 queries and split the workgroup's pair range in two halves, so that one
+// wave's VALU epilogue overlaps the other's MFMAs; their decision keys merge
+// through LDS at the end.  Each wave steps through its pairs, evaluating
+// 2 x 32 candidates (one pair, 64 queries) per step:
 //   X^T  (32 features x 32 candidates, bf16)   built from the pair's feature
 //        row (L1-resident) and each query's input-length feature;
 //   h1^T = ReLU(W1^T X^T + b1)  -> bf16, registers;
@@ -94,11 +97,12 @@ hipError_t launch_quality_bf16(const QualityArgs &a, hipStream_t s) {
 //   z    = W3^T h2^T + b3 by packed bf16 dot products;
 //   TTFT = softplus(z0), TPOT = softplus(z1).
 // W1, W2 (A operands), biases (as accumulator initial values) and W3 pairs
-// live in LDS.  Fused mode then applies Eq. 2, the bound test and the
+// live in LDS.  After the heads, lane half h carries column tile h alone (one
+// query per lane).  Fused mode then applies Eq. 2, the bound test and the
 // utility and keeps a running maximum decision key per query (Eq. 3); staged
 // mode reads X from HBM and writes TTFT/TPOT per candidate instead.
 template <int H, bool STAGED>
-__global__ __launch_bounds__(256, 1) void k_mlp_bf16(MlpArgs a) {
+__global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
     constexpr int MT = H / 32;     // 32-row tiles of a hidden layer
     constexpr int KB2 = H / 16;    // k-blocks of the second layer
     constexpr int NT = 2;          // 32-candidate column tiles per wave
@@ -107,60 +111,66 @@ __global__ __launch_bounds__(256, 1) void k_mlp_bf16(MlpArgs a) {
     __shared__ f32x4 s_b1[MT * 2 * 4];
     __shared__ f32x4 s_b2[MT * 2 * 4];
     __shared__ u32x4 s_w3[MT * 2 * 4];
+    __shared__ uint64_t s_mkey[kQPerBlock];
+    __shared__ f32x4 s_mval[kQPerBlock];
     const int tid = threadIdx.x;
     {
         const uint4 *g;
         uint4 *d;
         g = reinterpret_cast<const uint4 *>(a.w1_pk);
         d = reinterpret_cast<uint4 *>(s_w1);
-        for (int i = tid; i < MT * 2 * 64; i += 256) d[i] = g[i];
+        for (int i = tid; i < MT * 2 * 64; i += kMlpThreads) d[i] = g[i];
         g = reinterpret_cast<const uint4 *>(a.w2_pk);
         d = reinterpret_cast<uint4 *>(s_w2);
-        for (int i = tid; i < MT * KB2 * 64; i += 256) d[i] = g[i];
+        for (int i = tid; i < MT * KB2 * 64; i += kMlpThreads) d[i] = g[i];
         g = reinterpret_cast<const uint4 *>(a.b1_pk);
         d = reinterpret_cast<uint4 *>(s_b1);
-        for (int i = tid; i < MT * 2 * 4; i += 256) d[i] = g[i];
+        for (int i = tid; i < MT * 2 * 4; i += kMlpThreads) d[i] = g[i];
         g = reinterpret_cast<const uint4 *>(a.b2_pk);
         d = reinterpret_cast<uint4 *>(s_b2);
-        for (int i = tid; i < MT * 2 * 4; i += 256) d[i] = g[i];
+        for (int i = tid; i < MT * 2 * 4; i += kMlpThreads) d[i] = g[i];
         g = reinterpret_cast<const uint4 *>(a.w3_pk);
         d = reinterpret_cast<uint4 *>(s_w3);
-        for (int i = tid; i < MT * 2 * 4; i += 256) d[i] = g[i];
+        for (int i = tid; i < MT * 2 * 4; i += kMlpThreads) d[i] = g[i];
     }
     __syncthreads();
 
     const int lane = tid & 63, wave = tid >> 6, n = lane & 31, h = lane >> 5;
+    const int qw = wave & 3, grp = wave >> 2;
     const int nq = a.q.nq;
-    const int qbase = blockIdx.x * kQPerBlock + wave * kQPerWave;
+    const int qbase = blockIdx.x * kQPerBlock + qw * kQPerWave;
+    // every lane builds features for both column tiles ...
     int qc[NT];
-    bool vq[NT];
     uint32_t xl[NT];
-    float nout[NT], slo[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
         const int q = qbase + 32 * t + n;
-        vq[t] = q < nq;
-        qc[t] = vq[t] ? q : 0;
+        qc[t] = q < nq ? q : 0;
         xl[t] = bf16_bits(len_feature(a.q.input_len[qc[t]]));
-        const int32_t no = a.q.nout[qc[t]];
-        nout[t] = static_cast<float>(no < 0 ? 0 : no);
-        slo[t] = a.q.slo ? a.q.slo[qc[t]] : a.q.default_slo;
+        // keep the feature in a register: otherwise the fp64 log is
+        // recomputed inside the pair loop
+        asm volatile("" : "+v"(xl[t]));
     }
+    // ... and decides for column tile h only (query qme)
+    const int qme = qbase + 32 * h + n;
+    const bool vme = qme < nq;
+    const int qmc = vme ? qme : 0;
+    const int32_t nomy = a.q.nout[qmc];
+    const float nout = static_cast<float>(nomy < 0 ? 0 : nomy);
+    const float slo = a.q.slo ? a.q.slo[qmc] : a.q.default_slo;
     // the input-length slot: k-block, lane half and element holding it
     const int ls_kb = a.len_slot >> 4, ls_h = (a.len_slot >> 3) & 1, ls_e = a.len_slot & 7;
     const bool patch = (h == ls_h);
 
-    const int split = blockIdx.y;
-    const int d0 = static_cast<int>(static_cast<long>(a.N) * split / a.nsplit);
-    const int d1 = static_cast<int>(static_cast<long>(a.N) * (split + 1) / a.nsplit);
+    const int split = STAGED ? 0 : blockIdx.y;
+    const int nsplit = STAGED ? 1 : a.nsplit;
+    const long span0 = static_cast<long>(a.N) * split / nsplit;
+    const long span1 = static_cast<long>(a.N) * (split + 1) / nsplit;
+    const int d0 = static_cast<int>(span0 + (span1 - span0) * grp / 2);
+    const int d1 = static_cast<int>(span0 + (span1 - span0) * (grp + 1) / 2);
 
-    uint64_t bkey[NT];
-    float bu[NT], be[NT], btt[NT], btp[NT];
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
-        bkey[t] = 0;
-        bu[t] = be[t] = btt[t] = btp[t] = 0.0f;
-    }
+    uint64_t bkey = 0;
+    float bu = 0.0f, be = 0.0f, btt = 0.0f, btp = 0.0f;
 
     for (int d = d0; d < d1; ++d) {
         // LDS offsets made opaque per step: the weight fragments are
@@ -236,52 +246,63 @@ __global__ __launch_bounds__(256, 1) void k_mlp_bf16(MlpArgs a) {
                 }
             }
         }
-        // ---- heads, cost, decision
-        const int m = a.dep_model[d];
-#pragma unroll
-        for (int t = 0; t < NT; ++t) {
-            const float zz0 = z0[t] + __shfl_xor(z0[t], 32);
-            const float zz1 = z1[t] + __shfl_xor(z1[t], 32);
-            const float tt = softplus_f32(zz0 + a.b3_0);
-            const float tp = softplus_f32(zz1 + a.b3_1);
-            const size_t ci = static_cast<size_t>(qc[t]) * a.N + d;
-            if constexpr (STAGED) {
-                if (h == 0 && vq[t]) {
-                    a.cand_ttft[ci] = tt;
-                    a.cand_tpot[ci] = tp;
-                }
-            } else {
-                if (a.cand_ttft && h == 0 && vq[t]) {
-                    a.cand_ttft[ci] = tt;
-                    a.cand_tpot[ci] = tp;
-                }
-                const float Q = a.qmat[static_cast<size_t>(qc[t]) * a.M + m];
-                const Decision r = decide(tt, tp, nout[t], slo[t], Q, a.alpha);
-                const uint64_t k = decision_key(r.feasible, r.u, d);
-                if (k > bkey[t]) {
-                    bkey[t] = k;
-                    bu[t] = r.u;
-                    be[t] = r.e2e;
-                    btt[t] = tt;
-                    btp[t] = tp;
-                }
+        // ---- heads: lane half h completes column tile h (its partner lane
+        // holds the other 128 hidden units of the same candidates)
+        const float give0 = h ? z0[0] : z0[1], keep0 = h ? z0[1] : z0[0];
+        const float give1 = h ? z1[0] : z1[1], keep1 = h ? z1[1] : z1[0];
+        const float tt = softplus_f32(keep0 + __shfl_xor(give0, 32) + a.b3_0);
+        const float tp = softplus_f32(keep1 + __shfl_xor(give1, 32) + a.b3_1);
+        const size_t ci = static_cast<size_t>(qmc) * a.N + d;
+        if constexpr (STAGED) {
+            if (vme) {
+                a.cand_ttft[ci] = tt;
+                a.cand_tpot[ci] = tp;
+            }
+        } else {
+            if (a.cand_ttft && vme) {
+                a.cand_ttft[ci] = tt;
+                a.cand_tpot[ci] = tp;
+            }
+            // ---- cost, bound test, utility, running argmax (Eq. 2, Eq. 3)
+            const float Q = a.qmat[static_cast<size_t>(qmc) * a.M + a.dep_model[d]];
+            const Decision r = decide(tt, tp, nout, slo, Q, a.alpha);
+            const uint64_t k = decision_key(r.feasible, r.u, d);
+            if (k > bkey) {
+                bkey = k;
+                bu = r.u;
+                be = r.e2e;
+                btt = tt;
+                btp = tp;
             }
         }
     }
     if constexpr (!STAGED) {
-#pragma unroll
-        for (int t = 0; t < NT; ++t) {
-            if (h != 0 || !vq[t]) continue;
-            const int q = qbase + 32 * t + n;
-            if (a.nsplit == 1) {
-                write_outputs(a.out, q, bkey[t], bu[t], be[t], btt[t], btp[t]);
+        // merge the two pair halves of each query through LDS
+        const int slot = qw * kQPerWave + lane;
+        if (grp == 1) {
+            s_mkey[slot] = bkey;
+            s_mval[slot] = (f32x4){bu, be, btt, btp};
+        }
+        __syncthreads();
+        if (grp == 0 && vme) {
+            const uint64_t ok = s_mkey[slot];
+            if (ok > bkey) {
+                const f32x4 v = s_mval[slot];
+                bkey = ok;
+                bu = v[0];
+                be = v[1];
+                btt = v[2];
+                btp = v[3];
+            }
+            if (nsplit == 1) {
+                write_outputs(a.out, qme, bkey, bu, be, btt, btp);
             } else {
-                const size_t pi = static_cast<size_t>(split) * nq + q;
-                a.part_key[pi] = bkey[t];
-                a.part_val[pi * 4 + 0] = bu[t];
-                a.part_val[pi * 4 + 1] = be[t];
-                a.part_val[pi * 4 + 2] = btt[t];
-                a.part_val[pi * 4 + 3] = btp[t];
+                const size_t pi = static_cast<size_t>(split) * nq + qme;
+                a.part_key[pi] = bkey;
+                a.part_val[pi * 4 + 0] = bu;
+                a.part_val[pi * 4 + 1] = be;
+                a.part_val[pi * 4 + 2] = btt;
+                a.part_val[pi * 4 + 3] = btp;
             }
         }
     }
@@ -290,8 +311,8 @@ __global__ __launch_bounds__(256, 1) void k_mlp_bf16(MlpArgs a) {
 template <int H>
 static hipError_t launch_mlp_h(bool staged, const MlpArgs &a, hipStream_t s) {
     const dim3 grid((a.q.nq + kQPerBlock - 1) / kQPerBlock, staged ? 1 : a.nsplit);
-    if (staged) hipLaunchKernelGGL((k_mlp_bf16<H, true>), grid, dim3(256), 0, s, a);
-    else hipLaunchKernelGGL((k_mlp_bf16<H, false>), grid, dim3(256), 0, s, a);
+    if (staged) hipLaunchKernelGGL((k_mlp_bf16<H, true>), grid, dim3(kMlpThreads), 0, s, a);
+    else hipLaunchKernelGGL((k_mlp_bf16<H, false>), grid, dim3(kMlpThreads), 0, s, a);
     return hipGetLastError();
 }
 
