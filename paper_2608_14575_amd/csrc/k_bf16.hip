@@ -37,6 +37,17 @@ __device__ __forceinline__ bf16x8 relu_pack8(const f32x16 &c, int base) {
     return __builtin_bit_cast(bf16x8, u);
 }
 
+// A 32-column tile's head output is split between lane l (hidden-row half 0)
+// and lane l ^ 32 (half 1).  Given each lane's partial sums for column tiles
+// 0 and 1, return in lanes 0-31 the full sum for tile 0 and in lanes 32-63
+// the full sum for tile 1: one v_permlane32_swap moves tile 0's upper-half
+// partials down and tile 1's lower-half partials up.
+__device__ __forceinline__ float half_tile_sum(float tile0, float tile1) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(tile0), __float_as_uint(tile1),
+                                                    false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // ------------------------------------------------------------ quality GEMM
 // Q[q][m] = e_q . Wq[:, m] + bq[m] (Sec. 3.2 item 3), bf16 in, fp32 out.
 // Each wave: 32 queries x 32 (padded) models.  Per 64-wide slice of the
@@ -172,7 +183,51 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
     uint64_t bkey = 0;
     float bu = 0.0f, be = 0.0f, btt = 0.0f, btp = 0.0f;
 
+    // Per-pair inputs are loaded one step ahead: the pair's feature row
+    // (fused) or the candidates' feature rows (staged), and the quality
+    // Q[query][model(pair)], whose address needs a scalar load first.
+    const bf16x8 *dep = reinterpret_cast<const bf16x8 *>(a.dep_bf16);
+    const float *qrow = a.qmat + static_cast<size_t>(qmc) * a.M;
+    const int dfirst = d0 < d1 ? d0 : 0;
+    bf16x8 nr[NT][2];
+    if constexpr (STAGED) {
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            const bf16x8 *xr = reinterpret_cast<const bf16x8 *>(
+                a.X + (static_cast<size_t>(qc[t]) * a.N + dfirst) * kFeatPad);
+            nr[t][0] = xr[h];
+            nr[t][1] = xr[2 + h];
+        }
+    } else {
+        nr[0][0] = dep[dfirst * 4 + h];
+        nr[0][1] = dep[dfirst * 4 + 2 + h];
+    }
+    float nq_val = STAGED ? 0.0f : qrow[a.dep_model[dfirst]];
+
     for (int d = d0; d < d1; ++d) {
+        bf16x8 cr[NT][2];
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            cr[t][0] = nr[t][0];
+            cr[t][1] = nr[t][1];
+        }
+        const float Qd = nq_val;
+        {
+            const int dn = d + 1 < d1 ? d + 1 : d;
+            if constexpr (STAGED) {
+#pragma unroll
+                for (int t = 0; t < NT; ++t) {
+                    const bf16x8 *xr = reinterpret_cast<const bf16x8 *>(
+                        a.X + (static_cast<size_t>(qc[t]) * a.N + dn) * kFeatPad);
+                    nr[t][0] = xr[h];
+                    nr[t][1] = xr[2 + h];
+                }
+            } else {
+                nr[0][0] = dep[dn * 4 + h];
+                nr[0][1] = dep[dn * 4 + 2 + h];
+                nq_val = qrow[a.dep_model[dn]];
+            }
+        }
         // LDS offsets made opaque per step: the weight fragments are
         // loop-invariant, and hoisting all of them out of the pair loop would
         // need far more registers than a lane has.
@@ -183,75 +238,108 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
         if constexpr (STAGED) {
 #pragma unroll
             for (int t = 0; t < NT; ++t) {
-                const uint16_t *xr = a.X + (static_cast<size_t>(qc[t]) * a.N + d) * kFeatPad + 8 * h;
-                xf[t][0] = *reinterpret_cast<const bf16x8 *>(xr);
-                xf[t][1] = *reinterpret_cast<const bf16x8 *>(xr + 16);
+                xf[t][0] = cr[t][0];
+                xf[t][1] = cr[t][1];
             }
         } else {
-            const bf16x8 *row = reinterpret_cast<const bf16x8 *>(a.dep_bf16 + static_cast<size_t>(d) * kFeatPad);
-            const bf16x8 r0 = row[h], r1 = row[2 + h];
+            const bf16x8 r0 = cr[0][0], r1 = cr[0][1];
 #pragma unroll
             for (int t = 0; t < NT; ++t) {
                 xf[t][0] = (patch && ls_kb == 0) ? put_elem(r0, ls_e, xl[t]) : r0;
                 xf[t][1] = (patch && ls_kb == 1) ? put_elem(r1, ls_e, xl[t]) : r1;
             }
         }
-        // ---- layer 1
+        // ---- layers 1 and 2, software-pipelined: the VALU epilogue of row
+        // tile i-1 (ReLU, bf16 rounding, head dot products) is issued between
+        // the first and the remaining MFMAs of row tile i, so it runs while
+        // those MFMAs occupy the matrix pipe.  The fences keep that order
+        // (the scheduler would otherwise cluster the epilogues after the
+        // MFMAs); LDS and global reads may still move across them.
+        constexpr int kFence = 0x100 | 0x020;   // DS reads, VMEM reads may cross
         bf16x8 h1[NT][KB2];
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
+        f32x16 acc[2][NT];
+        auto l1_mfma = [&](int mt, f32x16 (&c)[NT]) {
             const f32x16 bi = bias_tile(s_b1 + (mt * 2 + ho) * 4);
-            f32x16 acc[NT];
 #pragma unroll
-            for (int t = 0; t < NT; ++t) acc[t] = bi;
+            for (int t = 0; t < NT; ++t) c[t] = bi;
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb) {
                 const bf16x8 w = s_w1[(mt * 2 + kb) * 64 + lo];
 #pragma unroll
-                for (int t = 0; t < NT; ++t) acc[t] = mfma32(w, xf[t][kb], acc[t]);
+                for (int t = 0; t < NT; ++t) c[t] = mfma32(w, xf[t][kb], c[t]);
             }
+        };
+        // (the empty asm statements pin each epilogue's results at this
+        // point: otherwise IR passes sink the pure ReLU / dot-product chains
+        // to their last use, past the fences, and the registers overflow)
+        auto l1_epi = [&](int mt, const f32x16 (&c)[NT]) {
 #pragma unroll
             for (int t = 0; t < NT; ++t) {
-                h1[t][2 * mt] = relu_pack8(acc[t], 0);
-                h1[t][2 * mt + 1] = relu_pack8(acc[t], 8);
+                h1[t][2 * mt] = relu_pack8(c[t], 0);
+                h1[t][2 * mt + 1] = relu_pack8(c[t], 8);
+                asm volatile("" : "+v"(h1[t][2 * mt]), "+v"(h1[t][2 * mt + 1]));
             }
-        }
-        // ---- layer 2, folded into the output heads tile by tile
+        };
+        auto l2_mfma = [&](int mo, int kb0, int kb1, f32x16 (&c)[NT]) {
+            if (kb0 == 0) {
+                const f32x16 bi = bias_tile(s_b2 + (mo * 2 + ho) * 4);
+#pragma unroll
+                for (int t = 0; t < NT; ++t) c[t] = bi;
+            }
+#pragma unroll
+            for (int kb = kb0; kb < kb1; ++kb) {
+                const bf16x8 w = s_w2[(mo * KB2 + kb) * 64 + lo];
+#pragma unroll
+                for (int t = 0; t < NT; ++t) c[t] = mfma32(w, h1[t][kb], c[t]);
+            }
+        };
         float z0[NT], z1[NT];
 #pragma unroll
         for (int t = 0; t < NT; ++t) z0[t] = z1[t] = 0.0f;
-#pragma unroll
-        for (int mo = 0; mo < MT; ++mo) {
-            const f32x16 bi = bias_tile(s_b2 + (mo * 2 + ho) * 4);
-            f32x16 acc[NT];
-#pragma unroll
-            for (int t = 0; t < NT; ++t) acc[t] = bi;
-#pragma unroll
-            for (int kb = 0; kb < KB2; ++kb) {
-                const bf16x8 w = s_w2[(mo * KB2 + kb) * 64 + lo];
-#pragma unroll
-                for (int t = 0; t < NT; ++t) acc[t] = mfma32(w, h1[t][kb], acc[t]);
-            }
+        auto l2_epi = [&](int mo, const f32x16 (&c)[NT]) {
             const u32x4 *w3 = s_w3 + (mo * 2 + ho) * 4;
             const u32x4 wa = w3[0], wb = w3[1], wc = w3[2], wd = w3[3];
 #pragma unroll
             for (int t = 0; t < NT; ++t) {
 #pragma unroll
                 for (int p = 0; p < 8; ++p) {
-                    const bf16x2 hp = relu_bf16x2(acc[t][2 * p], acc[t][2 * p + 1]);
+                    const bf16x2 hp = relu_bf16x2(c[t][2 * p], c[t][2 * p + 1]);
                     const uint32_t w0 = p < 4 ? wa[p & 3] : wb[p & 3];
                     const uint32_t w1 = p < 4 ? wc[p & 3] : wd[p & 3];
                     z0[t] = __builtin_amdgcn_fdot2_f32_bf16(hp, __builtin_bit_cast(bf16x2, w0), z0[t], false);
                     z1[t] = __builtin_amdgcn_fdot2_f32_bf16(hp, __builtin_bit_cast(bf16x2, w1), z1[t], false);
                 }
+                asm volatile("" : "+v"(z0[t]), "+v"(z1[t]));
+            }
+        };
+        constexpr int kHead = KB2 < 4 ? KB2 : 4;   // MFMA k-steps issued before the previous epilogue
+        // layer 1: MFMAs of tile mt, then the epilogue of tile mt - 1
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+            l1_mfma(mt, acc[mt & 1]);
+            if (mt > 0) {
+                __builtin_amdgcn_sched_barrier(kFence);
+                l1_epi(mt - 1, acc[(mt - 1) & 1]);
+                __builtin_amdgcn_sched_barrier(kFence);
             }
         }
+        // layer 2: first k-steps of tile mo, epilogue of the previous tile
+        // (layer-1 tile MT-1 for mo = 0), then the remaining k-steps
+#pragma unroll
+        for (int mo = 0; mo < MT; ++mo) {
+            const int cur = (MT + mo) & 1, prev = (MT + mo - 1) & 1;
+            l2_mfma(mo, 0, kHead, acc[cur]);
+            __builtin_amdgcn_sched_barrier(kFence);
+            if (mo == 0) l1_epi(MT - 1, acc[prev]);
+            else l2_epi(mo - 1, acc[prev]);
+            __builtin_amdgcn_sched_barrier(kFence);
+            l2_mfma(mo, kHead, KB2, acc[cur]);
+        }
+        l2_epi(MT - 1, acc[(2 * MT - 1) & 1]);
         // ---- heads: lane half h completes column tile h (its partner lane
         // holds the other 128 hidden units of the same candidates)
-        const float give0 = h ? z0[0] : z0[1], keep0 = h ? z0[1] : z0[0];
-        const float give1 = h ? z1[0] : z1[1], keep1 = h ? z1[1] : z1[0];
-        const float tt = softplus_f32(keep0 + __shfl_xor(give0, 32) + a.b3_0);
-        const float tp = softplus_f32(keep1 + __shfl_xor(give1, 32) + a.b3_1);
+        const float tt = softplus_fast(half_tile_sum(z0[0], z0[1]) + a.b3_0);
+        const float tp = softplus_fast(half_tile_sum(z1[0], z1[1]) + a.b3_1);
         const size_t ci = static_cast<size_t>(qmc) * a.N + d;
         if constexpr (STAGED) {
             if (vme) {
@@ -264,8 +352,7 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
                 a.cand_tpot[ci] = tp;
             }
             // ---- cost, bound test, utility, running argmax (Eq. 2, Eq. 3)
-            const float Q = a.qmat[static_cast<size_t>(qmc) * a.M + a.dep_model[d]];
-            const Decision r = decide(tt, tp, nout, slo, Q, a.alpha);
+            const Decision r = decide(tt, tp, nout, slo, Qd, a.alpha);
             const uint64_t k = decision_key(r.feasible, r.u, d);
             if (k > bkey) {
                 bkey = k;

@@ -120,8 +120,8 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
         if (wave == 0 && h == 0 && vd) {
             const float zz0 = s_z[0][n][0] + s_z[1][n][0] + s_z[2][n][0] + s_z[3][n][0];
             const float zz1 = s_z[0][n][1] + s_z[1][n][1] + s_z[2][n][1] + s_z[3][n][1];
-            const float tt = softplus_f32(zz0 + a.b3_0);
-            const float tp = softplus_f32(zz1 + a.b3_1);
+            const float tt = softplus_fast(zz0 + a.b3_0);
+            const float tp = softplus_fast(zz1 + a.b3_1);
             const Decision r = decide(tt, tp, nout, slo, s_q[a.dep_model[d]], a.alpha);
             const uint64_t k = decision_key(r.feasible, r.u, d);
             if (k > bkey) {
