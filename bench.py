@@ -128,13 +128,14 @@ def throughput(args, S, hwr, torch):
     return res, pb, st, sample, sp
 
 
-def single_query(args, S, hwr, torch):
+def single_query(args, S, hwr, torch, flags=0):
     """p50 / p99 of hwr_route_batch for one host query, with the runtime
-    signals updated (random walk) between calls; host clock around the call."""
+    signals updated (random walk) between calls; host clock around the call.
+    flags = 0: graph launch; HWR_FLAG_NO_GRAPH: plain kernel launch."""
     sp = S.spec("C4")
     pb = S.make_problem(sp, 4)
     walk = S.StateWalk(sp, 4)
-    r = hwr.Router.from_problem(pb, stream=int(torch.cuda.current_stream().cuda_stream))
+    r = hwr.Router.from_problem(pb, stream=int(torch.cuda.current_stream().cuda_stream), flags=flags)
     r.update(walk.state)
     calls = args.c4_calls
     qs = S.make_queries(sp, 4, n=calls)
@@ -171,7 +172,8 @@ def single_query(args, S, hwr, torch):
     return {"calls": calls, "p50_us": float(np.percentile(us, 50)), "p99_us": float(np.percentile(us, 99)),
             "mean_us": float(us.mean()), "update_p50_us": float(np.percentile(upd_ns / 1e3, 50)),
             "workload": "C4: 1 query x 32 pairs (16 models x 2 GPU types), embed 768 bf16, "
-                        "predictor 24-128-128-2, graph-launched, host I/O",
+                        "predictor 24-128-128-2, host I/O, "
+                        + ("graph launch" if flags == 0 else "plain kernel launch"),
             "timing": "host clock around hwr_route_batch (ctypes call included)"}
 
 
@@ -235,8 +237,10 @@ def main() -> int:
     res, pb, st, sample, sp = throughput(args, S, hwr, torch)
     log(f"throughput {res['value']:.3e} candidates/s, predictor {res['roofline']['achieved']:.1f} TFLOP/s")
     single = None if args.no_single else single_query(args, S, hwr, torch)
+    single_plain = None if args.no_single else single_query(args, S, hwr, torch, hwr.HWR_FLAG_NO_GRAPH)
     if single:
-        log(f"single query p50 {single['p50_us']:.1f} us p99 {single['p99_us']:.1f} us")
+        log(f"single query (graph) p50 {single['p50_us']:.1f} us p99 {single['p99_us']:.1f} us; "
+            f"(plain launch) p50 {single_plain['p50_us']:.1f} us p99 {single_plain['p99_us']:.1f} us")
     cpu = None if args.no_cpu_baseline else cpu_baseline(pb, st, sample, sp)
     line = {
         "metric": METRIC, "value": res["value"], "unit": "candidates/s", "n_gpus": 1,
@@ -244,7 +248,8 @@ def main() -> int:
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic (seeded; stands in for the paper's embedded prompt sets)",
         "config": res["config"], "roofline": res["roofline"], "cpu_baseline": cpu,
-        "single_query": single, "quality_roofline": res["quality_roofline"], "stages": res["stages"],
+        "single_query": single, "single_query_plain_launch": single_plain,
+        "quality_roofline": res["quality_roofline"], "stages": res["stages"],
     }
     print(json.dumps(line), flush=True)
     return 0

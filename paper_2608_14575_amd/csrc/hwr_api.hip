@@ -45,12 +45,17 @@ struct hwr_ctx {
     hipEvent_t ring_ev[kStateSlots] = {};
     bool ring_used[kStateSlots] = {};
     int ring_next = 0;
+    int state_slot = 0;           // ring slot of the newest snapshot
+    bool state_dirty = false;     // newest snapshot not yet turned into pair rows
     bool has_state = false;
+    hwr_hw_state *h_cur = nullptr;   // pinned copy of the newest snapshot (single-query path)
+    hwr_hw_state *d_cur = nullptr;
     // weights
     float *d_bq = nullptr;
     uint16_t *d_wq_pk = nullptr, *d_wqT = nullptr, *d_w1_pk = nullptr, *d_w2_pk = nullptr;
     float *d_b1_pk = nullptr, *d_b2_pk = nullptr;
     uint32_t *d_w3_pk = nullptr;
+    uint16_t *d_w3_frag = nullptr;
     float *d_wq = nullptr, *d_w1 = nullptr, *d_w2 = nullptr, *d_w3 = nullptr, *d_b1 = nullptr,
           *d_b2 = nullptr;
     // work space
@@ -142,7 +147,7 @@ std::vector<uint16_t> pack_quality(const uint16_t *wq, int D, int M) {
 // 32 t + crow(8 b + j, h).  Bias tiles hold b[32 mt + crow(r, h)] for
 // r = 0..15; head pairs hold (W3[row(2p)][o], W3[row(2p+1)][o]) as bf16x2.
 struct PackedPredictor {
-    std::vector<uint16_t> w1, w2;
+    std::vector<uint16_t> w1, w2, w3frag;
     std::vector<float> b1, b2;
     std::vector<uint32_t> w3;
 };
@@ -156,6 +161,18 @@ PackedPredictor pack_predictor(const uint16_t *w1, const uint16_t *w2, const uin
     p.b1.assign(static_cast<size_t>(MT) * 2 * 16, 0.0f);
     p.b2.assign(static_cast<size_t>(MT) * 2 * 16, 0.0f);
     p.w3.assign(static_cast<size_t>(MT) * 2 * 16, 0u);
+    // Head layer on MFMA (z^T = W3^T h2^T): A operand rows are the two heads,
+    // k follows the layer-2 accumulator order like W2's.  Only lanes of rows
+    // 0 and 1 hold data: [k-block][row m < 2][half h][8], then one zero
+    // fragment that every other lane reads.
+    p.w3frag.assign(static_cast<size_t>(KB2) * 4 * 8 + 8, 0);
+    for (int kb = 0; kb < KB2; ++kb)
+        for (int m = 0; m < 2; ++m)
+            for (int h = 0; h < 2; ++h)
+                for (int j = 0; j < 8; ++j) {
+                    const int hin = 32 * (kb >> 1) + crow(8 * (kb & 1) + j, h);
+                    p.w3frag[((static_cast<size_t>(kb) * 2 + m) * 2 + h) * 8 + j] = w3[static_cast<size_t>(hin) * 2 + m];
+                }
     for (int mt = 0; mt < MT; ++mt)
         for (int lane = 0; lane < 64; ++lane) {
             const int m = lane & 31, h = lane >> 5;
@@ -286,13 +303,14 @@ void release(hwr_ctx *c) {
     if (c->graph) hipGraphDestroy(c->graph);
     void *dev_ptrs[] = {c->d_dep_model, c->d_dep_gpu, c->d_model_arch, c->d_params, c->d_dep_f32,
                         c->d_dep_bf16, c->d_bq, c->d_wq_pk, c->d_wqT, c->d_w1_pk, c->d_w2_pk,
-                        c->d_b1_pk, c->d_b2_pk, c->d_w3_pk, c->d_wq, c->d_w1, c->d_w2, c->d_w3,
+                        c->d_b1_pk, c->d_b2_pk, c->d_w3_pk, c->d_w3_frag, c->d_wq, c->d_w1, c->d_w2, c->d_w3,
                         c->d_b1, c->d_b2, c->d_qmat, c->d_ctt, c->d_ctp, c->d_X, c->d_pkey,
                         c->d_pval, c->d_hemb, c->d_hlen, c->d_hnout, c->d_hchoice, c->d_hslo,
                         c->d_hval, c->d_hcand, c->d_hqual, c->d_hfeas};
     for (void *p : dev_ptrs)
         if (p) hipFree(p);
     if (c->h_ring) hipHostFree(c->h_ring);
+    if (c->h_cur) hipHostFree(c->h_cur);
     if (c->h_sin) hipHostFree(c->h_sin);
     if (c->h_sout) hipHostFree(c->h_sout);
     delete c;
@@ -369,6 +387,7 @@ hwr_status init_impl(const hwr_config *cfg, hwr_ctx **out) {
         INIT_HIP(upload(&c->d_b1_pk, p.b1.data(), p.b1.size()));
         INIT_HIP(upload(&c->d_b2_pk, p.b2.data(), p.b2.size()));
         INIT_HIP(upload(&c->d_w3_pk, p.w3.data(), p.w3.size()));
+        INIT_HIP(upload(&c->d_w3_frag, p.w3frag.data(), p.w3frag.size()));
     } else {
         INIT_HIP(upload(&c->d_wq, static_cast<const float *>(cfg->wq), static_cast<size_t>(D) * M));
         INIT_HIP(upload(&c->d_w1, static_cast<const float *>(cfg->w1), static_cast<size_t>(F) * H));
@@ -392,6 +411,9 @@ hwr_status init_impl(const hwr_config *cfg, hwr_ctx **out) {
     INIT_HIP(hipHostMalloc(reinterpret_cast<void **>(&c->h_ring),
                            sizeof(hwr_hw_state) * N * kStateSlots, hipHostMallocMapped));
     for (int i = 0; i < kStateSlots; ++i) INIT_HIP(hipEventCreateWithFlags(&c->ring_ev[i], hipEventDisableTiming));
+    INIT_HIP(hipHostMalloc(reinterpret_cast<void **>(&c->h_cur), sizeof(hwr_hw_state) * N,
+                           hipHostMallocMapped | hipHostMallocCoherent));
+    INIT_HIP(hipHostGetDevicePointer(reinterpret_cast<void **>(&c->d_cur), c->h_cur, 0));
     if (c->bf16) {
         const size_t in_bytes = sizeof(SingleIn) + static_cast<size_t>(D) * 2;
         INIT_HIP(hipHostMalloc(reinterpret_cast<void **>(&c->h_sin), in_bytes,
@@ -418,7 +440,26 @@ struct DevBatch {
     float *cand_ttft, *cand_tpot, *cand_quality;
 };
 
+// Turn the newest state snapshot into the device pair rows, once, ordered on
+// the context's stream before the batch that needs them.
+hwr_status sync_state(hwr_ctx *c) {
+    if (!c->state_dirty) return HWR_OK;
+    const int slot = c->state_slot;
+    hwr_hw_state *src = c->h_ring + static_cast<size_t>(slot) * c->N;
+    hwr_hw_state *dsrc = nullptr;
+    HWR_HIP(c, hipHostGetDevicePointer(reinterpret_cast<void **>(&dsrc), src, 0));
+    StateArgs a{dsrc, c->N, c->A, c->Gw, c->d_dep_model, c->d_dep_gpu, c->d_model_arch,
+                c->d_params, c->d_dep_f32, c->d_dep_bf16};
+    HWR_HIP(c, timed(c, HWR_K_STATE, [&] { return launch_state(a, c->stream); }));
+    HWR_HIP(c, hipEventRecord(c->ring_ev[slot], c->stream));
+    c->ring_used[slot] = true;
+    c->state_dirty = false;
+    return HWR_OK;
+}
+
 hwr_status route_device(hwr_ctx *c, const DevBatch &b) {
+    hwr_status st = sync_state(c);
+    if (st != HWR_OK) return st;
     const int M = c->M, N = c->N, D = c->D;
     const size_t esz = c->bf16 ? 2 : 4;
     for (int off = 0; off < b.n; off += c->max_chunk) {
@@ -469,7 +510,7 @@ hwr_status route_device(hwr_ctx *c, const DevBatch &b) {
             ma.w2_pk = c->d_w2_pk;
             ma.b1_pk = c->d_b1_pk;
             ma.b2_pk = c->d_b2_pk;
-            ma.w3_pk = c->d_w3_pk;
+            ma.w3_frag = c->d_w3_frag;
             ma.out = oa;
             ma.nsplit = 1;
             if (c->pipeline == HWR_PIPE_FUSED) {
@@ -607,10 +648,15 @@ SingleArgs single_args(const hwr_ctx *c) {
     a.alpha = c->alpha;
     a.b3_0 = c->b3[0];
     a.b3_1 = c->b3[1];
+    a.arch_width = c->A;
+    a.gpu_width = c->Gw;
     a.in = c->d_sin;
     a.out = c->d_sout;
-    a.dep_bf16 = c->d_dep_bf16;
+    a.state = c->d_cur;
     a.dep_model = c->d_dep_model;
+    a.dep_gpu = c->d_dep_gpu;
+    a.model_arch = c->d_model_arch;
+    a.params_b = c->d_params;
     a.wqT = c->d_wqT;
     a.bq = c->d_bq;
     a.w1_pk = c->d_w1_pk;
@@ -712,17 +758,19 @@ hwr_status hwr_update_hw_state(hwr_ctx *c, const hwr_hw_state *state, int32_t n)
             return fail(c, HWR_ERR_INVALID_ARG, "ttft_avg_s / tpot_avg_s must be finite and > 0");
     }
     HWR_HIP(c, hipSetDevice(c->dev));
+    // The snapshot goes to the next slot of a pinned ring (turned into device
+    // pair rows lazily, before the next batch) and to the pinned current copy
+    // the single-query kernel reads.  A slot still awaited by an enqueued
+    // state kernel is waited for before it is overwritten.
     const int slot = c->ring_next;
-    if (c->ring_used[slot]) HWR_HIP(c, hipEventSynchronize(c->ring_ev[slot]));
-    hwr_hw_state *dst = c->h_ring + static_cast<size_t>(slot) * c->N;
-    std::memcpy(dst, state, sizeof(hwr_hw_state) * n);
-    hwr_hw_state *dsrc = nullptr;
-    HWR_HIP(c, hipHostGetDevicePointer(reinterpret_cast<void **>(&dsrc), dst, 0));
-    StateArgs a{dsrc, c->N, c->A, c->Gw, c->d_dep_model, c->d_dep_gpu, c->d_model_arch,
-                c->d_params, c->d_dep_f32, c->d_dep_bf16};
-    HWR_HIP(c, timed(c, HWR_K_STATE, [&] { return launch_state(a, c->stream); }));
-    HWR_HIP(c, hipEventRecord(c->ring_ev[slot], c->stream));
-    c->ring_used[slot] = true;
+    if (c->ring_used[slot]) {
+        HWR_HIP(c, hipEventSynchronize(c->ring_ev[slot]));
+        c->ring_used[slot] = false;
+    }
+    std::memcpy(c->h_ring + static_cast<size_t>(slot) * c->N, state, sizeof(hwr_hw_state) * n);
+    std::memcpy(c->h_cur, state, sizeof(hwr_hw_state) * n);
+    c->state_slot = slot;
+    c->state_dirty = true;
     c->ring_next = (slot + 1) % kStateSlots;
     c->has_state = true;
     return HWR_OK;

@@ -12,6 +12,39 @@ __device__ inline float len_feature(int32_t len) {
     return static_cast<float>(log(v) * 0.125);
 }
 
+// The pair's slice of the Eq. 1 feature vector: one-hot architecture id (ia)
+// and GPU type (ig), then, from slot b = A + Gw: ln(params_B)/4, the query
+// slot (0 here), ln(1+running)/2, ln(1+waiting)/2, kv_util, gpu_util,
+// ln(ttft)/4, ln(tpot)/4.  Logs in fp64, each value rounded once to fp32.
+struct PairFeatures {
+    int ia, ig, b;
+    float v[8];
+    __device__ float slot(int f) const {
+        float x = 0.0f;
+        if (f == ia || f == ig) x = 1.0f;
+#pragma unroll
+        for (int k = 0; k < 8; ++k)
+            if (f == b + k) x = v[k];
+        return x;
+    }
+};
+__device__ inline PairFeatures pair_features(const hwr_hw_state &s, float params_b, int arch,
+                                             int gpu, int arch_width, int gpu_width) {
+    PairFeatures p;
+    p.ia = arch;
+    p.ig = arch_width + gpu;
+    p.b = arch_width + gpu_width;
+    p.v[0] = static_cast<float>(log(static_cast<double>(params_b)) * 0.25);
+    p.v[1] = 0.0f;
+    p.v[2] = static_cast<float>(log(1.0 + static_cast<double>(s.running_q)) * 0.5);
+    p.v[3] = static_cast<float>(log(1.0 + static_cast<double>(s.waiting_q)) * 0.5);
+    p.v[4] = s.kv_util;
+    p.v[5] = s.gpu_util;
+    p.v[6] = static_cast<float>(log(static_cast<double>(s.ttft_avg_s)) * 0.25);
+    p.v[7] = static_cast<float>(log(static_cast<double>(s.tpot_avg_s)) * 0.25);
+    return p;
+}
+
 __device__ inline uint16_t bf16_bits(float x) {   // nearest, ties to even
     return __builtin_bit_cast(uint16_t, static_cast<__bf16>(x));
 }

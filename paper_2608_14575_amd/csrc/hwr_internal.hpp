@@ -93,7 +93,7 @@ struct MlpArgs {                  // bf16 predictor (fused or staged)
     const float *qmat;            // [nq][M]
     const uint16_t *w1_pk, *w2_pk;
     const float *b1_pk, *b2_pk;
-    const uint32_t *w3_pk;
+    const uint16_t *w3_frag;      // head layer A fragments (compact, see pack_predictor)
     const uint16_t *X;            // staged input [nq][N][32]
     float *cand_ttft, *cand_tpot; // [nq][N] (staged output or debug)
     OutArgs out;
@@ -152,12 +152,13 @@ struct SingleOut {
 };
 
 struct SingleArgs {
-    int N, M, D, len_slot;
+    int N, M, D, len_slot, arch_width, gpu_width;
     float alpha, b3_0, b3_1;
     const SingleIn *in;           // device-visible pinned record
     SingleOut *out;               // device-visible pinned record
-    const uint16_t *dep_bf16;
-    const int32_t *dep_model;
+    const hwr_hw_state *state;    // device-visible pinned copy of the current signals [N]
+    const int32_t *dep_model, *dep_gpu, *model_arch;
+    const float *params_b;
     const uint16_t *wqT;          // [M][D] bf16
     const float *bq;
     const uint16_t *w1_pk, *w2_pk;

@@ -37,15 +37,14 @@ __device__ __forceinline__ bf16x8 relu_pack8(const f32x16 &c, int base) {
     return __builtin_bit_cast(bf16x8, u);
 }
 
-// A 32-column tile's head output is split between lane l (hidden-row half 0)
-// and lane l ^ 32 (half 1).  Given each lane's partial sums for column tiles
-// 0 and 1, return in lanes 0-31 the full sum for tile 0 and in lanes 32-63
-// the full sum for tile 1: one v_permlane32_swap moves tile 0's upper-half
-// partials down and tile 1's lower-half partials up.
-__device__ __forceinline__ float half_tile_sum(float tile0, float tile1) {
-    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(tile0), __float_as_uint(tile1),
-                                                    false, false);
-    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+// Move each 32-bit element from lane i to lane i + 4 within every row of 16
+// lanes (DPP row_shr:4; lanes 0-3 of a row receive 0).
+__device__ __forceinline__ bf16x8 shift_rows4(bf16x8 v) {
+    u32x4 u = __builtin_bit_cast(u32x4, v);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+        u[i] = static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(u[i]), 0x114, 0xF, 0xF, true));
+    return __builtin_bit_cast(bf16x8, u);
 }
 
 // ------------------------------------------------------------ quality GEMM
@@ -121,7 +120,7 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
     __shared__ bf16x8 s_w2[MT * KB2 * 64];
     __shared__ f32x4 s_b1[MT * 2 * 4];
     __shared__ f32x4 s_b2[MT * 2 * 4];
-    __shared__ u32x4 s_w3[MT * 2 * 4];
+    __shared__ bf16x8 s_w3f[KB2 * 4 + 1];
     __shared__ uint64_t s_mkey[kQPerBlock];
     __shared__ f32x4 s_mval[kQPerBlock];
     const int tid = threadIdx.x;
@@ -140,9 +139,9 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
         g = reinterpret_cast<const uint4 *>(a.b2_pk);
         d = reinterpret_cast<uint4 *>(s_b2);
         for (int i = tid; i < MT * 2 * 4; i += kMlpThreads) d[i] = g[i];
-        g = reinterpret_cast<const uint4 *>(a.w3_pk);
-        d = reinterpret_cast<uint4 *>(s_w3);
-        for (int i = tid; i < MT * 2 * 4; i += kMlpThreads) d[i] = g[i];
+        g = reinterpret_cast<const uint4 *>(a.w3_frag);
+        d = reinterpret_cast<uint4 *>(s_w3f);
+        for (int i = tid; i < KB2 * 4 + 1; i += kMlpThreads) d[i] = g[i];
     }
     __syncthreads();
 
@@ -293,26 +292,35 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
                 for (int t = 0; t < NT; ++t) c[t] = mfma32(w, h1[t][kb], c[t]);
             }
         };
-        float z0[NT], z1[NT];
-#pragma unroll
-        for (int t = 0; t < NT; ++t) z0[t] = z1[t] = 0.0f;
+        // Head layer on the matrix pipe: z^T = W3^T h2^T.  Both column tiles
+        // share one accumulator: tile 0's A fragment holds the two heads in
+        // rows 0-1, tile 1's the same values in rows 4-5 (a 4-lane shift), so
+        // lanes 0-31 end with tile 0's (z0, z1) and lanes 32-63 with tile 1's,
+        // in accumulator elements 0 and 1.  (Packed bf16 dot products would
+        // stall the matrix pipe: they do not co-issue with MFMA on gfx950.)
+        f32x16 acc3 = {};
+        const int w3_lane = (lo & 31) < 2 ? (lo & 31) : -1;
         auto l2_epi = [&](int mo, const f32x16 (&c)[NT]) {
-            const u32x4 *w3 = s_w3 + (mo * 2 + ho) * 4;
-            const u32x4 wa = w3[0], wb = w3[1], wc = w3[2], wd = w3[3];
+            bf16x8 h2[NT][2];
 #pragma unroll
             for (int t = 0; t < NT; ++t) {
-#pragma unroll
-                for (int p = 0; p < 8; ++p) {
-                    const bf16x2 hp = relu_bf16x2(c[t][2 * p], c[t][2 * p + 1]);
-                    const uint32_t w0 = p < 4 ? wa[p & 3] : wb[p & 3];
-                    const uint32_t w1 = p < 4 ? wc[p & 3] : wd[p & 3];
-                    z0[t] = __builtin_amdgcn_fdot2_f32_bf16(hp, __builtin_bit_cast(bf16x2, w0), z0[t], false);
-                    z1[t] = __builtin_amdgcn_fdot2_f32_bf16(hp, __builtin_bit_cast(bf16x2, w1), z1[t], false);
-                }
-                asm volatile("" : "+v"(z0[t]), "+v"(z1[t]));
+                h2[t][0] = relu_pack8(c[t], 0);
+                h2[t][1] = relu_pack8(c[t], 8);
             }
+#pragma unroll
+            for (int b = 0; b < 2; ++b) {
+                const int kb = 2 * mo + b;
+                const bf16x8 f0 = s_w3f[w3_lane >= 0 ? (kb * 2 + w3_lane) * 2 + ho : KB2 * 4];
+                const bf16x8 f1 = shift_rows4(f0);
+                acc3 = mfma32(f0, h2[0][b], acc3);
+                acc3 = mfma32(f1, h2[1][b], acc3);
+            }
+            asm volatile("" : "+v"(acc3));
         };
-        constexpr int kHead = KB2 < 4 ? KB2 : 4;   // MFMA k-steps issued before the previous epilogue
+        // MFMA k-steps of tile mo issued before the previous epilogue.  For
+        // mo = 0 that epilogue produces layer-1 k-blocks KB2-2 and KB2-1, so
+        // the head steps must stop short of them.
+        constexpr int kHead = KB2 - 2 < 4 ? KB2 - 2 : 4;
         // layer 1: MFMAs of tile mt, then the epilogue of tile mt - 1
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
@@ -338,8 +346,8 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
         l2_epi(MT - 1, acc[(2 * MT - 1) & 1]);
         // ---- heads: lane half h completes column tile h (its partner lane
         // holds the other 128 hidden units of the same candidates)
-        const float tt = softplus_fast(half_tile_sum(z0[0], z0[1]) + a.b3_0);
-        const float tp = softplus_fast(half_tile_sum(z1[0], z1[1]) + a.b3_1);
+        const float tt = softplus_fast(acc3[0] + a.b3_0);
+        const float tp = softplus_fast(acc3[1] + a.b3_1);
         const size_t ci = static_cast<size_t>(qmc) * a.N + d;
         if constexpr (STAGED) {
             if (vme) {

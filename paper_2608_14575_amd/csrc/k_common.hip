@@ -12,29 +12,14 @@ namespace hwr {
 __global__ __launch_bounds__(256) void k_state(StateArgs a) {
     const int d = blockIdx.x * blockDim.x + threadIdx.x;
     if (d >= a.N) return;
-    const hwr_hw_state s = a.src[d];
     const int m = a.dep_model[d];
-    const int ia = a.model_arch[m];
-    const int ig = a.arch_width + a.dep_gpu[d];
-    const int b = a.arch_width + a.gpu_width;
-    const float v0 = static_cast<float>(log(static_cast<double>(a.params_b[m])) * 0.25);
-    const float v2 = static_cast<float>(log(1.0 + static_cast<double>(s.running_q)) * 0.5);
-    const float v3 = static_cast<float>(log(1.0 + static_cast<double>(s.waiting_q)) * 0.5);
-    const float v6 = static_cast<float>(log(static_cast<double>(s.ttft_avg_s)) * 0.25);
-    const float v7 = static_cast<float>(log(static_cast<double>(s.tpot_avg_s)) * 0.25);
+    const PairFeatures p = pair_features(a.src[d], a.params_b[m], a.model_arch[m], a.dep_gpu[d],
+                                         a.arch_width, a.gpu_width);
     float *rf = a.dep_f32 + static_cast<size_t>(d) * kFeatPad;
     uint16_t *rb = a.dep_bf16 + static_cast<size_t>(d) * kFeatPad;
 #pragma unroll
     for (int f = 0; f < kFeatPad; ++f) {
-        float v = 0.0f;
-        if (f == ia || f == ig) v = 1.0f;
-        if (f == b + 0) v = v0;
-        if (f == b + 2) v = v2;
-        if (f == b + 3) v = v3;
-        if (f == b + 4) v = s.kv_util;
-        if (f == b + 5) v = s.gpu_util;
-        if (f == b + 6) v = v6;
-        if (f == b + 7) v = v7;
+        const float v = p.slot(f);
         rf[f] = v;
         rb[f] = bf16_bits(v);
     }

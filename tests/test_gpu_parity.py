@@ -50,6 +50,17 @@ def test_c2_bf16_device_full(pipeline):
 
 
 @pytest.mark.parametrize("pipeline", ["fused", "staged"])
+def test_hidden_64_bf16(pipeline):
+    """H = 64 (two row tiles): the shallowest software pipeline."""
+    sp = S.spec("C2", n_queries=700, hidden=64)
+    pb, st, qs = S.make_problem(sp, 6), S.make_state(sp, 6), S.make_queries(sp, 6)
+    r = G.make_router(pb, pipeline=pipeline)
+    r.update(st)
+    out = G.route_device(r, qs, sp.dtype)
+    _report(f"H=64 bf16 {pipeline}", G.check(pb, st, qs, out))
+
+
+@pytest.mark.parametrize("pipeline", ["fused", "staged"])
 def test_c3_shape_ragged_tail(pipeline):
     """H = 256, 64 pairs, 300 queries: two workgroups, the second ragged."""
     sp = S.spec("C3", n_queries=300)
