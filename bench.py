@@ -131,7 +131,7 @@ def throughput(args, S, hwr, torch):
 def single_query(args, S, hwr, torch, flags=0):
     """p50 / p99 of hwr_route_batch for one host query, with the runtime
     signals updated (random walk) between calls; host clock around the call.
-    flags = 0: graph launch; HWR_FLAG_NO_GRAPH: plain kernel launch."""
+    flags = 0: plain kernel launch; HWR_FLAG_GRAPH: graph launch."""
     sp = S.spec("C4")
     pb = S.make_problem(sp, 4)
     walk = S.StateWalk(sp, 4)
@@ -173,7 +173,7 @@ def single_query(args, S, hwr, torch, flags=0):
             "mean_us": float(us.mean()), "update_p50_us": float(np.percentile(upd_ns / 1e3, 50)),
             "workload": "C4: 1 query x 32 pairs (16 models x 2 GPU types), embed 768 bf16, "
                         "predictor 24-128-128-2, host I/O, "
-                        + ("graph launch" if flags == 0 else "plain kernel launch"),
+                        + ("kernel launch" if flags == 0 else "graph launch"),
             "timing": "host clock around hwr_route_batch (ctypes call included)"}
 
 
@@ -237,10 +237,10 @@ def main() -> int:
     res, pb, st, sample, sp = throughput(args, S, hwr, torch)
     log(f"throughput {res['value']:.3e} candidates/s, predictor {res['roofline']['achieved']:.1f} TFLOP/s")
     single = None if args.no_single else single_query(args, S, hwr, torch)
-    single_plain = None if args.no_single else single_query(args, S, hwr, torch, hwr.HWR_FLAG_NO_GRAPH)
+    single_graph = None if args.no_single else single_query(args, S, hwr, torch, hwr.HWR_FLAG_GRAPH)
     if single:
-        log(f"single query (graph) p50 {single['p50_us']:.1f} us p99 {single['p99_us']:.1f} us; "
-            f"(plain launch) p50 {single_plain['p50_us']:.1f} us p99 {single_plain['p99_us']:.1f} us")
+        log(f"single query (kernel launch) p50 {single['p50_us']:.1f} us p99 {single['p99_us']:.1f} us; "
+            f"(graph launch) p50 {single_graph['p50_us']:.1f} us p99 {single_graph['p99_us']:.1f} us")
     cpu = None if args.no_cpu_baseline else cpu_baseline(pb, st, sample, sp)
     line = {
         "metric": METRIC, "value": res["value"], "unit": "candidates/s", "n_gpus": 1,
@@ -248,7 +248,7 @@ def main() -> int:
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic (seeded; stands in for the paper's embedded prompt sets)",
         "config": res["config"], "roofline": res["roofline"], "cpu_baseline": cpu,
-        "single_query": single, "single_query_plain_launch": single_plain,
+        "single_query": single, "single_query_graph_launch": single_graph,
         "quality_roofline": res["quality_roofline"], "stages": res["stages"],
     }
     print(json.dumps(line), flush=True)

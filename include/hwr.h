@@ -72,7 +72,7 @@ typedef enum { HWR_MEM_DEVICE = 0, HWR_MEM_HOST = 1 } hwr_mem;
 typedef enum { HWR_PIPE_FUSED = 0, HWR_PIPE_STAGED = 1 } hwr_pipeline;
 
 /* hwr_config.flags */
-#define HWR_FLAG_NO_GRAPH 1       /* single host query: plain launch, no graph */
+#define HWR_FLAG_GRAPH 1          /* single host query: launch a captured graph */
 
 /* Runtime signals of one pair (Table 2 of the paper plus GPU utilisation). */
 typedef struct {
@@ -152,8 +152,11 @@ hwr_status hwr_update_hw_state(hwr_ctx *ctx, const hwr_hw_state *state, int32_t 
 
 /* Route a batch (Eq. 3 for each query).  n == 0 is a no-op.  Batches larger
  * than max_chunk run as successive chunks on the context's stream.  A single
- * query in host memory takes a latency path (one captured graph launch, the
- * query read and the result written through pinned host memory).  Host
+ * query in host memory takes a latency path: one kernel launch (or, with
+ * HWR_FLAG_GRAPH, one launch of a graph holding that kernel, captured on the
+ * first call) on a private stream of the context, reading the query and the
+ * newest state from pinned host memory and writing the decision there; it
+ * does not wait for batches still enqueued on the context's stream.  Host
  * inputs are checked (input_len >= 1, N_out >= 0, SLO > 0 and finite); device
  * inputs are not, and out-of-range values give unspecified choices (all
  * memory accesses stay in bounds). */

@@ -39,6 +39,8 @@ struct hwr_ctx {
     // per-pair tables and state
     int32_t *d_dep_model = nullptr, *d_dep_gpu = nullptr, *d_model_arch = nullptr;
     float *d_params = nullptr;
+    int32_t *d_pair_arch = nullptr;  // model attributes gathered per pair (single-query path)
+    float *d_pair_params = nullptr;
     float *d_dep_f32 = nullptr;
     uint16_t *d_dep_bf16 = nullptr;
     hwr_hw_state *h_ring = nullptr;
@@ -76,6 +78,7 @@ struct hwr_ctx {
     SingleIn *d_sin = nullptr;
     SingleOut *d_sout = nullptr;
     uint32_t seq = 0;
+    hipStream_t sstream = nullptr;   // private stream of the single-query path
     hipGraph_t graph = nullptr;
     hipGraphExec_t gexec = nullptr;
     // timing
@@ -218,18 +221,23 @@ hipEvent_t take_event(hwr_ctx *c) {
 }
 
 template <class F>
-hipError_t timed(hwr_ctx *c, int kind, F &&launch) {
+hipError_t timed_on(hwr_ctx *c, hipStream_t s, int kind, F &&launch) {
     if (!c->prof) return launch();
     hipEvent_t a = take_event(c), b = take_event(c);
     if (!a || !b) return hipErrorOutOfMemory;
-    hipError_t e = hipEventRecord(a, c->stream);
+    hipError_t e = hipEventRecord(a, s);
     if (e != hipSuccess) return e;
     e = launch();
     if (e != hipSuccess) return e;
-    e = hipEventRecord(b, c->stream);
+    e = hipEventRecord(b, s);
     if (e != hipSuccess) return e;
     c->pending.push_back({kind, a, b});
     return hipSuccess;
+}
+
+template <class F>
+hipError_t timed(hwr_ctx *c, int kind, F &&launch) {
+    return timed_on(c, c->stream, kind, static_cast<F &&>(launch));
 }
 
 hwr_status drain_timing(hwr_ctx *c) {
@@ -299,9 +307,11 @@ void release(hwr_ctx *c) {
     for (hipEvent_t e : c->pool) hipEventDestroy(e);
     for (int i = 0; i < kStateSlots; ++i)
         if (c->ring_ev[i]) hipEventDestroy(c->ring_ev[i]);
+    if (c->sstream) hipStreamSynchronize(c->sstream);
     if (c->gexec) hipGraphExecDestroy(c->gexec);
     if (c->graph) hipGraphDestroy(c->graph);
-    void *dev_ptrs[] = {c->d_dep_model, c->d_dep_gpu, c->d_model_arch, c->d_params, c->d_dep_f32,
+    void *dev_ptrs[] = {c->d_dep_model, c->d_dep_gpu, c->d_model_arch, c->d_params, c->d_pair_arch,
+                        c->d_pair_params, c->d_dep_f32,
                         c->d_dep_bf16, c->d_bq, c->d_wq_pk, c->d_wqT, c->d_w1_pk, c->d_w2_pk,
                         c->d_b1_pk, c->d_b2_pk, c->d_w3_pk, c->d_w3_frag, c->d_wq, c->d_w1, c->d_w2, c->d_w3,
                         c->d_b1, c->d_b2, c->d_qmat, c->d_ctt, c->d_ctp, c->d_X, c->d_pkey,
@@ -311,6 +321,7 @@ void release(hwr_ctx *c) {
         if (p) hipFree(p);
     if (c->h_ring) hipHostFree(c->h_ring);
     if (c->h_cur) hipHostFree(c->h_cur);
+    if (c->sstream) hipStreamDestroy(c->sstream);
     if (c->h_sin) hipHostFree(c->h_sin);
     if (c->h_sout) hipHostFree(c->h_sout);
     delete c;
@@ -369,6 +380,16 @@ hwr_status init_impl(const hwr_config *cfg, hwr_ctx **out) {
     INIT_HIP(upload(&c->d_model_arch, cfg->model_arch, M));
     INIT_HIP(upload(&c->d_params, cfg->model_params_b, M));
     INIT_HIP(upload(&c->d_bq, cfg->bq, M));
+    {
+        std::vector<int32_t> pa(N);
+        std::vector<float> pp(N);
+        for (int d = 0; d < N; ++d) {
+            pa[d] = cfg->model_arch[cfg->dep_model[d]];
+            pp[d] = cfg->model_params_b[cfg->dep_model[d]];
+        }
+        INIT_HIP(upload(&c->d_pair_arch, pa.data(), N));
+        INIT_HIP(upload(&c->d_pair_params, pp.data(), N));
+    }
     INIT_HIP(dev_alloc(&c->d_dep_f32, static_cast<size_t>(N) * kFeatPad));
     INIT_HIP(dev_alloc(&c->d_dep_bf16, static_cast<size_t>(N) * kFeatPad));
     if (c->bf16) {
@@ -424,6 +445,7 @@ hwr_status init_impl(const hwr_config *cfg, hwr_ctx **out) {
         std::memset(c->h_sout, 0, sizeof(SingleOut));
         INIT_HIP(hipHostGetDevicePointer(reinterpret_cast<void **>(&c->d_sin), c->h_sin, 0));
         INIT_HIP(hipHostGetDevicePointer(reinterpret_cast<void **>(&c->d_sout), c->h_sout, 0));
+        INIT_HIP(hipStreamCreateWithFlags(&c->sstream, hipStreamNonBlocking));
     }
 #undef INIT_HIP
     *out = c;
@@ -448,8 +470,8 @@ hwr_status sync_state(hwr_ctx *c) {
     hwr_hw_state *src = c->h_ring + static_cast<size_t>(slot) * c->N;
     hwr_hw_state *dsrc = nullptr;
     HWR_HIP(c, hipHostGetDevicePointer(reinterpret_cast<void **>(&dsrc), src, 0));
-    StateArgs a{dsrc, c->N, c->A, c->Gw, c->d_dep_model, c->d_dep_gpu, c->d_model_arch,
-                c->d_params, c->d_dep_f32, c->d_dep_bf16};
+    StateArgs a{dsrc, c->N, c->A, c->Gw, c->d_dep_model, c->d_dep_gpu, c->d_pair_arch,
+                c->d_pair_params, c->d_dep_f32, c->d_dep_bf16};
     HWR_HIP(c, timed(c, HWR_K_STATE, [&] { return launch_state(a, c->stream); }));
     HWR_HIP(c, hipEventRecord(c->ring_ev[slot], c->stream));
     c->ring_used[slot] = true;
@@ -655,8 +677,8 @@ SingleArgs single_args(const hwr_ctx *c) {
     a.state = c->d_cur;
     a.dep_model = c->d_dep_model;
     a.dep_gpu = c->d_dep_gpu;
-    a.model_arch = c->d_model_arch;
-    a.params_b = c->d_params;
+    a.pair_arch = c->d_pair_arch;
+    a.pair_params = c->d_pair_params;
     a.wqT = c->d_wqT;
     a.bq = c->d_bq;
     a.w1_pk = c->d_w1_pk;
@@ -670,7 +692,7 @@ SingleArgs single_args(const hwr_ctx *c) {
 // Capture the single-query kernel into a graph once; replays read the query
 // record and the pair features by address, so state updates need no re-capture.
 hwr_status single_graph(hwr_ctx *c) {
-    if (c->gexec || (c->flags & HWR_FLAG_NO_GRAPH)) return HWR_OK;
+    if (c->gexec || !(c->flags & HWR_FLAG_GRAPH)) return HWR_OK;
     const SingleArgs a = single_args(c);
     hipStream_t cs = nullptr;
     HWR_HIP(c, hipStreamCreateWithFlags(&cs, hipStreamNonBlocking));
@@ -701,10 +723,10 @@ hwr_status route_single(hwr_ctx *c, const hwr_query_batch *q, hwr_route_result *
     in->seq = seq;
     std::atomic_thread_fence(std::memory_order_release);
     if (c->gexec) {
-        HWR_HIP(c, timed(c, HWR_K_SINGLE, [&] { return hipGraphLaunch(c->gexec, c->stream); }));
+        HWR_HIP(c, timed_on(c, c->sstream, HWR_K_SINGLE, [&] { return hipGraphLaunch(c->gexec, c->sstream); }));
     } else {
         const SingleArgs a = single_args(c);
-        HWR_HIP(c, timed(c, HWR_K_SINGLE, [&] { return launch_single(c->H, a, c->stream); }));
+        HWR_HIP(c, timed_on(c, c->sstream, HWR_K_SINGLE, [&] { return launch_single(c->H, a, c->sstream); }));
     }
     // wait for the decision record (written last by the kernel, system scope)
     volatile uint32_t *flag = &c->h_sout->seq;
@@ -712,7 +734,7 @@ hwr_status route_single(hwr_ctx *c, const hwr_query_batch *q, hwr_route_result *
     uint64_t spins = 0;
     while (*flag != seq) {
         if ((++spins & 0xFFFF) == 0) {
-            hipError_t qe = hipStreamQuery(c->stream);
+            hipError_t qe = hipStreamQuery(c->sstream);
             if (qe != hipSuccess && qe != hipErrorNotReady) return hip_fail(c, qe, "single-query launch");
             if (qe == hipSuccess && *flag != seq)
                 return fail(c, HWR_ERR_HIP, "single-query kernel finished without writing its result");

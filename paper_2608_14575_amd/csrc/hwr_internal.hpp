@@ -68,8 +68,9 @@ struct OutArgs {                  // per query; all but choice may be null
 struct StateArgs {
     const hwr_hw_state *src;      // [N] (pinned host slot, device-visible)
     int N, arch_width, gpu_width;
-    const int32_t *dep_model, *dep_gpu, *model_arch;
-    const float *params_b;
+    const int32_t *dep_model, *dep_gpu;
+    const int32_t *pair_arch;     // [N] architecture id of the pair's model
+    const float *pair_params;     // [N] parameter count (B) of the pair's model
     float *dep_f32;               // [N][32]
     uint16_t *dep_bf16;           // [N][32]
 };
@@ -157,8 +158,9 @@ struct SingleArgs {
     const SingleIn *in;           // device-visible pinned record
     SingleOut *out;               // device-visible pinned record
     const hwr_hw_state *state;    // device-visible pinned copy of the current signals [N]
-    const int32_t *dep_model, *dep_gpu, *model_arch;
-    const float *params_b;
+    const int32_t *dep_model, *dep_gpu;
+    const int32_t *pair_arch;     // [N] architecture id of the pair's model
+    const float *pair_params;     // [N] parameter count (B) of the pair's model
     const uint16_t *wqT;          // [M][D] bf16
     const float *bq;
     const uint16_t *w1_pk, *w2_pk;

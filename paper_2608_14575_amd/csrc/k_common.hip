@@ -12,8 +12,7 @@ namespace hwr {
 __global__ __launch_bounds__(256) void k_state(StateArgs a) {
     const int d = blockIdx.x * blockDim.x + threadIdx.x;
     if (d >= a.N) return;
-    const int m = a.dep_model[d];
-    const PairFeatures p = pair_features(a.src[d], a.params_b[m], a.model_arch[m], a.dep_gpu[d],
+    const PairFeatures p = pair_features(a.src[d], a.pair_params[d], a.pair_arch[d], a.dep_gpu[d],
                                          a.arch_width, a.gpu_width);
     float *rf = a.dep_f32 + static_cast<size_t>(d) * kFeatPad;
     uint16_t *rb = a.dep_bf16 + static_cast<size_t>(d) * kFeatPad;

@@ -20,172 +20,230 @@ __device__ __forceinline__ bf16x8 relu_pack8s(const f32x16 &c, int base) {
     return __builtin_bit_cast(bf16x8, u);
 }
 
+// Thread j (0..7) of a pair's group of eight writes feature slots j, j + 8,
+// j + 16, j + 24 of its row.  The eight signal slots b .. b + 7 meet each
+// residue mod 8 once, so the thread evaluates exactly one signal: number
+// (j - b) mod 8 (Eq. 1 layout; the query's input length is signal 1).  Logs
+// in fp64, rounded once to fp32, then to bf16 (as the state kernel does).
+__device__ __forceinline__ void pair_row(uint16_t *row, int j, int b0, int ks, int ia, int ig,
+                                         uint32_t raw, float params, int32_t len) {
+    double arg = 1.0, scale = 0.0;
+    if (ks == 0) { arg = static_cast<double>(params); scale = 0.25; }
+    if (ks == 1) { arg = static_cast<double>(len < 1 ? 1 : len); scale = 0.125; }
+    if (ks == 2 || ks == 3) { arg = 1.0 + static_cast<double>(static_cast<int32_t>(raw)); scale = 0.5; }
+    if (ks == 6 || ks == 7) { arg = static_cast<double>(__uint_as_float(raw)); scale = 0.25; }
+    float v = static_cast<float>(log(arg) * scale);
+    if (ks == 4 || ks == 5) v = __uint_as_float(raw);
+    const uint16_t sig = bf16_bits(v);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int f = j + 8 * i;
+        const uint16_t hot = (f == ia || f == ig) ? 0x3F80 : 0;
+        row[f] = (f >= b0 && f < b0 + 8) ? sig : hot;
+    }
+}
+
+// Cross-lane reductions on DPP (data-parallel primitives within a 16-lane
+// row: quad permutes, half-row and row mirrors), then one read of each row's
+// lane 0; no LDS round trips.  After the four steps every lane of a row holds
+// the row's result.
+template <int Ctrl>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t v) {
+    return static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), Ctrl, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float wave_sum(float v) {
+    v += __uint_as_float(dpp_u32<0xB1>(__float_as_uint(v)));    // quad_perm [1,0,3,2]
+    v += __uint_as_float(dpp_u32<0x4E>(__float_as_uint(v)));    // quad_perm [2,3,0,1]
+    v += __uint_as_float(dpp_u32<0x141>(__float_as_uint(v)));   // row_half_mirror
+    v += __uint_as_float(dpp_u32<0x140>(__float_as_uint(v)));   // row_mirror
+    const int b = __float_as_int(v);
+    return (__int_as_float(__builtin_amdgcn_readlane(b, 0)) + __int_as_float(__builtin_amdgcn_readlane(b, 16))) +
+           (__int_as_float(__builtin_amdgcn_readlane(b, 32)) + __int_as_float(__builtin_amdgcn_readlane(b, 48)));
+}
+template <int Ctrl>
+__device__ __forceinline__ uint64_t max_dpp(uint64_t k) {
+    const uint64_t o = (static_cast<uint64_t>(dpp_u32<Ctrl>(static_cast<uint32_t>(k >> 32))) << 32) |
+                       dpp_u32<Ctrl>(static_cast<uint32_t>(k));
+    return o > k ? o : k;
+}
+__device__ __forceinline__ uint64_t wave_max(uint64_t k) {
+    k = max_dpp<0xB1>(k);
+    k = max_dpp<0x4E>(k);
+    k = max_dpp<0x141>(k);
+    k = max_dpp<0x140>(k);
+    uint64_t best = 0;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const uint64_t o = (static_cast<uint64_t>(static_cast<uint32_t>(
+                                __builtin_amdgcn_readlane(static_cast<int>(k >> 32), 16 * r))) << 32) |
+                           static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(k), 16 * r));
+        best = o > best ? o : best;
+    }
+    return best;
+}
+
 template <int H>
 __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
     constexpr int MT = H / 32, KB2 = H / 16;
     constexpr int MO = (MT + 3) / 4;          // second-layer row tiles per wave
+    constexpr int kW1 = MT * 128 / 256;       // 16-byte pieces of w1 per thread
+    constexpr int kEmb = 4;                   // 16-byte embedding pieces per thread (D <= 8192)
+    constexpr int kHeldS = 4;                 // quality: embedding slices held (D <= 2048)
+    constexpr int kHeldM = H <= 128 ? 2 : 1;  // quality: model pairs held per wave
+    __shared__ bf16x8 s_w1[MT * 2 * 64];
+    __shared__ u32x4 s_bw[3][MT * 8];         // b1 tiles, b2 tiles, head pairs
+    __shared__ __attribute__((aligned(16))) uint16_t s_emb[8192];
+    __shared__ __attribute__((aligned(16))) uint16_t s_row[kMaxPairs][kFeatPad];   // bf16 rows
+    __shared__ int s_model[kMaxPairs];
+    __shared__ float s_bq[kMaxModels];
     __shared__ float s_q[kMaxModels];
     __shared__ float s_z[4][32][2];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, n = lane & 31, h = lane >> 5;
-    const bf16x8 *w1 = reinterpret_cast<const bf16x8 *>(a.w1_pk);
-    const bf16x8 *w2 = reinterpret_cast<const bf16x8 *>(a.w2_pk);
-    const u32x4 *w3 = reinterpret_cast<const u32x4 *>(a.w3_pk);
-    const f32x4 *b1 = reinterpret_cast<const f32x4 *>(a.b1_pk);
-    const f32x4 *b2 = reinterpret_cast<const f32x4 *>(a.b2_pk);
+    const int b0 = a.arch_width + a.gpu_width;
+    const int j8 = tid & 7, ks = (j8 - b0) & 7;
 
-    // Everything that does not depend on the query is loaded first, so that
-    // its latency overlaps the read of the query record from host memory:
-    // the first-layer fragments and bias tiles, this wave's second-layer
-    // fragments, bias tiles and head pairs, and the first tile's pair rows.
-    // (at H = 256 the first-layer bias tiles are read where they are used:
-    // holding them all would overflow the register file)
-    constexpr bool kHoldB1 = H <= 128;
-    bf16x8 fw1[MT][2];
-    f32x4 fb1[kHoldB1 ? MT : 1][4];
+    // ---- phase 1: every independent load is issued before any is waited
+    // for -- host memory first (query record, runtime signals), then the
+    // device-side weights -- so the phase costs one host round trip.
+    const u32x4 hdr = *reinterpret_cast<const u32x4 *>(a.in);   // seq, input_len, nout, slo
+    const int p0 = tid >> 3;
+    const bool has0 = p0 < a.N;
+    const int pc0 = has0 ? p0 : 0;
+    // (loads are unconditional, indices clamped into range: a load under a
+    // branch makes the compiler wait for it, and for all earlier ones, there)
+    const uint32_t raw0 = reinterpret_cast<const uint32_t *>(a.state + pc0)[ks >= 2 ? ks - 2 : 0];
+    u32x4 re[kEmb];
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb) fw1[mt][kb] = w1[(mt * 2 + kb) * 64 + lane];
-        if constexpr (kHoldB1) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) fb1[mt][i] = b1[(mt * 2 + h) * 4 + i];
-        }
+    for (int i = 0; i < kEmb; ++i) {
+        const int idx = tid + 256 * i;
+        re[i] = reinterpret_cast<const u32x4 *>(a.in + 1)[idx < a.D / 8 ? idx : 0];
     }
+    const float prm0 = a.pair_params[pc0];
+    const int ia0 = a.pair_arch[pc0], ig0 = a.arch_width + a.dep_gpu[pc0];
+    const int md0 = a.dep_model[pc0];
+    u32x4 rw1[kW1];
+#pragma unroll
+    for (int i = 0; i < kW1; ++i) rw1[i] = reinterpret_cast<const u32x4 *>(a.w1_pk)[tid + 256 * i];
+    u32x4 rbw;
+    {
+        const int tb = tid < MT * 24 ? tid : 0;
+        const int t = tb / (MT * 8), k = tb - t * (MT * 8);
+        const u32x4 *src = reinterpret_cast<const u32x4 *>(t == 0 ? static_cast<const void *>(a.b1_pk)
+                                                           : t == 1 ? static_cast<const void *>(a.b2_pk)
+                                                                    : static_cast<const void *>(a.w3_pk));
+        rbw = src[k];
+    }
+    const float rbq = a.bq[tid < a.M ? tid : 0];
     constexpr int MOH = MO == 1 ? 1 : 0;     // second-layer tiles held in registers
     bf16x8 fw2[MO][KB2];
-    f32x4 fb2[MO][4];
-    u32x4 fw3[MO][4];
+    {
+        const bf16x8 *w2 = reinterpret_cast<const bf16x8 *>(a.w2_pk);
 #pragma unroll
-    for (int i = 0; i < MOH; ++i) {
-        const int mo = wave + 4 * i < MT ? wave + 4 * i : 0;
+        for (int i = 0; i < MOH; ++i) {
+            const int mo = wave + 4 * i < MT ? wave + 4 * i : 0;
 #pragma unroll
-        for (int kb = 0; kb < KB2; ++kb) fw2[i][kb] = w2[(mo * KB2 + kb) * 64 + lane];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            fb2[i][j] = b2[(mo * 2 + h) * 4 + j];
-            fw3[i][j] = w3[(mo * 2 + h) * 4 + j];
+            for (int kb = 0; kb < KB2; ++kb) fw2[i][kb] = w2[(mo * KB2 + kb) * 64 + lane];
         }
     }
-    // the first tile's pairs: runtime signals (pinned host memory, written
-    // by the last state update) and static attributes
-    const int d0 = n < a.N ? n : 0;
-    hwr_hw_state st0 = a.state[d0];
-    int model0 = a.dep_model[d0], gpu0 = a.dep_gpu[d0];
+    bf16x8 wq0[kHeldM][kHeldS], wq1[kHeldM][kHeldS];
+#pragma unroll
+    for (int jm = 0; jm < kHeldM; ++jm) {
+        const int m0 = wave + 8 * jm < a.M ? wave + 8 * jm : 0;
+        const int m1 = wave + 8 * jm + 4 < a.M ? wave + 8 * jm + 4 : m0;
+#pragma unroll
+        for (int i = 0; i < kHeldS; ++i) {
+            const int k = (lane + 64 * i) * 8 < a.D ? (lane + 64 * i) * 8 : 0;
+            wq0[jm][i] = *reinterpret_cast<const bf16x8 *>(a.wqT + static_cast<size_t>(m0) * a.D + k);
+            wq1[jm][i] = *reinterpret_cast<const bf16x8 *>(a.wqT + static_cast<size_t>(m1) * a.D + k);
+        }
+    }
+    const uint32_t seq = hdr[0];
+    const int32_t len = static_cast<int32_t>(hdr[1]);
+    const int32_t no = static_cast<int32_t>(hdr[2]);
+    const float slo = __uint_as_float(hdr[3]);
 
-    // query record (pinned host memory): header and embedding
-    const uint32_t seq = a.in->seq;
-    const int32_t len = a.in->input_len;
-    const int32_t no = a.in->nout;
+    // ---- phase 2: LDS stores, the feature rows, one barrier
+#pragma unroll
+    for (int i = 0; i < kEmb; ++i) {
+        const int idx = tid + 256 * i;
+        if (idx < a.D / 8) reinterpret_cast<u32x4 *>(s_emb)[idx] = re[i];
+    }
+#pragma unroll
+    for (int i = 0; i < kW1; ++i) reinterpret_cast<u32x4 *>(s_w1)[tid + 256 * i] = rw1[i];
+    if (tid < MT * 24) s_bw[0][tid] = rbw;
+    if (tid < a.M) s_bq[tid] = rbq;
+    if (has0) {
+        pair_row(s_row[p0], j8, b0, ks, ia0, ig0, raw0, prm0, len);
+        if (j8 == 0) s_model[p0] = md0;
+    }
+    for (int p = p0 + 32; p < a.N; p += 32) {       // more than 32 pairs
+        const uint32_t raw = ks >= 2 ? reinterpret_cast<const uint32_t *>(a.state + p)[ks - 2] : 0u;
+        const float prm = ks == 0 ? a.pair_params[p] : 1.0f;
+        pair_row(s_row[p], j8, b0, ks, a.pair_arch[p], a.arch_width + a.dep_gpu[p], raw, prm, len);
+        if (j8 == 0) s_model[p] = a.dep_model[p];
+    }
+    __syncthreads();
+
     const float nout = static_cast<float>(no < 0 ? 0 : no);
-    const float slo = a.in->slo;
-    const uint16_t *emb = reinterpret_cast<const uint16_t *>(a.in + 1);
-
-    // quality of every model (Sec. 3.2 item 3): one wave per model, lanes
-    // split D; the embedding slices are read straight from host memory
-    for (int m0 = wave; m0 < a.M; m0 += 8) {
-        const int m1 = m0 + 4;
-        float acc0 = 0.0f, acc1 = 0.0f;
-        for (int k = lane * 8; k < a.D; k += 512) {
-            const bf16x8 e = *reinterpret_cast<const bf16x8 *>(emb + k);
-            const bf16x8 q0 = *reinterpret_cast<const bf16x8 *>(a.wqT + static_cast<size_t>(m0) * a.D + k);
-            const bf16x8 q1 = m1 < a.M ? *reinterpret_cast<const bf16x8 *>(a.wqT + static_cast<size_t>(m1) * a.D + k) : q0;
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                acc0 = fmaf(static_cast<float>(e[j]), static_cast<float>(q0[j]), acc0);
-                acc1 = fmaf(static_cast<float>(e[j]), static_cast<float>(q1[j]), acc1);
-            }
-        }
-#pragma unroll
-        for (int off = 32; off >= 1; off >>= 1) {
-            acc0 += __shfl_xor(acc0, off);
-            acc1 += __shfl_xor(acc1, off);
-        }
-        if (lane == 0) {
-            s_q[m0] = acc0 + a.bq[m0];
-            if (m1 < a.M) s_q[m1] = acc1 + a.bq[m1];
-        }
-    }
-
-    const uint32_t xl = bf16_bits(len_feature(len));
-    const int ls_kb = a.len_slot >> 4, ls_h = (a.len_slot >> 3) & 1, ls_e = a.len_slot & 7;
-
     uint64_t bkey = 0;
     float bu = 0.0f, be = 0.0f, btt = 0.0f, btp = 0.0f;
     const int ntiles = (a.N + 31) / 32;
     for (int ct = 0; ct < ntiles; ++ct) {
         const int d = ct * 32 + n;
         const bool vd = d < a.N;
-        // features of pair d (Eq. 1), zero columns past the last pair
+        const int dc = vd ? d : 0;
+        // ---- features of pair d (zero columns past the last pair)
         bf16x8 xf[2];
-        const int model = model0;
         {
-            const PairFeatures pf = pair_features(st0, a.params_b[model], a.model_arch[model], gpu0,
-                                                  a.arch_width, a.gpu_width);
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb) {
-                u32x4 u;
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const int f = 16 * kb + 8 * h + 2 * j;
-                    const f32x2 v = {vd ? pf.slot(f) : 0.0f, vd ? pf.slot(f + 1) : 0.0f};
-                    u[j] = __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
-                }
-                xf[kb] = __builtin_bit_cast(bf16x8, u);
-            }
-            if (vd && h == ls_h) {
-                if (ls_kb == 0) xf[0] = put_elem(xf[0], ls_e, xl);
-                else xf[1] = put_elem(xf[1], ls_e, xl);
-            }
+            const u32x4 *row = reinterpret_cast<const u32x4 *>(s_row[dc]);
+            const u32x4 z = {0, 0, 0, 0};
+            xf[0] = __builtin_bit_cast(bf16x8, vd ? row[h] : z);
+            xf[1] = __builtin_bit_cast(bf16x8, vd ? row[2 + h] : z);
         }
-        if (ct + 1 < ntiles) {          // next tile's pairs
-            const int dn = (ct + 1) * 32 + n < a.N ? (ct + 1) * 32 + n : 0;
-            st0 = a.state[dn];
-            model0 = a.dep_model[dn];
-            gpu0 = a.dep_gpu[dn];
-        }
-        // layer 1 (every wave, all row tiles)
+        const int model = s_model[dc];
+        // ---- layer 1 (every wave, all row tiles; weights from LDS)
         bf16x8 h1[KB2];
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
             f32x16 acc;
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const f32x4 bt = kHoldB1 ? fb1[kHoldB1 ? mt : 0][i] : b1[(mt * 2 + h) * 4 + i];
+                const f32x4 bt = __builtin_bit_cast(f32x4, s_bw[0][(mt * 2 + h) * 4 + i]);
 #pragma unroll
                 for (int j = 0; j < 4; ++j) acc[4 * i + j] = bt[j];
             }
 #pragma unroll
-            for (int kb = 0; kb < 2; ++kb) acc = mfma32s(fw1[mt][kb], xf[kb], acc);
+            for (int kb = 0; kb < 2; ++kb) acc = mfma32s(s_w1[(mt * 2 + kb) * 64 + lane], xf[kb], acc);
             h1[2 * mt] = relu_pack8s(acc, 0);
             h1[2 * mt + 1] = relu_pack8s(acc, 8);
         }
-        // layer 2 row tiles of this wave, folded into the heads
+        // ---- layer 2 row tiles of this wave, folded into the heads
         float z0 = 0.0f, z1 = 0.0f;
 #pragma unroll
         for (int i = 0; i < MO; ++i) {
             if (wave + 4 * i >= MT) break;
+            const int mo = wave + 4 * i;
             if (i >= MOH) {
-                const int mo = wave + 4 * i;
+                const bf16x8 *w2 = reinterpret_cast<const bf16x8 *>(a.w2_pk);
 #pragma unroll
                 for (int kb = 0; kb < KB2; ++kb) fw2[i][kb] = w2[(mo * KB2 + kb) * 64 + lane];
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    fb2[i][j] = b2[(mo * 2 + h) * 4 + j];
-                    fw3[i][j] = w3[(mo * 2 + h) * 4 + j];
-                }
             }
             f32x16 acc;
 #pragma unroll
-            for (int p = 0; p < 4; ++p)
+            for (int p = 0; p < 4; ++p) {
+                const f32x4 bt = __builtin_bit_cast(f32x4, s_bw[1][(mo * 2 + h) * 4 + p]);
 #pragma unroll
-                for (int j = 0; j < 4; ++j) acc[4 * p + j] = fb2[i][p][j];
+                for (int j = 0; j < 4; ++j) acc[4 * p + j] = bt[j];
+            }
 #pragma unroll
             for (int kb = 0; kb < KB2; ++kb) acc = mfma32s(fw2[i][kb], h1[kb], acc);
+            const u32x4 *w3 = &s_bw[2][(mo * 2 + h) * 4];
+            const u32x4 wa = w3[0], wb = w3[1], wc = w3[2], wd = w3[3];
 #pragma unroll
             for (int p = 0; p < 8; ++p) {
                 const bf16x2 hp = relu_bf16x2(acc[2 * p], acc[2 * p + 1]);
-                const uint32_t u0 = p < 4 ? fw3[i][0][p & 3] : fw3[i][1][p & 3];
-                const uint32_t u1 = p < 4 ? fw3[i][2][p & 3] : fw3[i][3][p & 3];
+                const uint32_t u0 = p < 4 ? wa[p & 3] : wb[p & 3];
+                const uint32_t u1 = p < 4 ? wc[p & 3] : wd[p & 3];
                 z0 = __builtin_amdgcn_fdot2_f32_bf16(hp, __builtin_bit_cast(bf16x2, u0), z0, false);
                 z1 = __builtin_amdgcn_fdot2_f32_bf16(hp, __builtin_bit_cast(bf16x2, u1), z1, false);
             }
@@ -196,7 +254,60 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
             s_z[wave][n][0] = z0;
             s_z[wave][n][1] = z1;
         }
+        // ---- quality of every model (Sec. 3.2 item 3), once: wave w takes
+        // models w, w + 4, w + 8, ...; lanes split D
+        if (ct == 0) {
+            // models wave + 8j and wave + 8j + 4; the first kHeldM pairs use the
+            // heads already in registers for the first kHeldS slices of D
+            auto finish = [&](float acc0, float acc1, int m0, int m1) {
+                acc0 = wave_sum(acc0);
+                acc1 = wave_sum(acc1);
+                if (lane == 0) {
+                    s_q[m0] = acc0 + s_bq[m0];
+                    if (m1 < a.M) s_q[m1] = acc1 + s_bq[m1];
+                }
+            };
+            auto dot8 = [](const bf16x8 &e, const bf16x8 &q, float acc) {
+#pragma unroll
+                for (int t = 0; t < 8; ++t) acc = fmaf(static_cast<float>(e[t]), static_cast<float>(q[t]), acc);
+                return acc;
+            };
+#pragma unroll
+            for (int j = 0; j < kHeldM; ++j) {
+                const int m0 = wave + 8 * j, m1 = m0 + 4;
+                if (m0 < a.M) {
+                    float acc0 = 0.0f, acc1 = 0.0f;
+#pragma unroll
+                    for (int i = 0; i < kHeldS; ++i) {
+                        const int k = (lane + 64 * i) * 8;
+                        if (k < a.D) {
+                            const bf16x8 e = *reinterpret_cast<const bf16x8 *>(s_emb + k);
+                            acc0 = dot8(e, wq0[j][i], acc0);
+                            acc1 = dot8(e, wq1[j][i], acc1);
+                        }
+                    }
+                    for (int k = (lane + 64 * kHeldS) * 8; k < a.D; k += 512) {
+                        const bf16x8 e = *reinterpret_cast<const bf16x8 *>(s_emb + k);
+                        const int mm1 = m1 < a.M ? m1 : m0;
+                        acc0 = dot8(e, *reinterpret_cast<const bf16x8 *>(a.wqT + static_cast<size_t>(m0) * a.D + k), acc0);
+                        acc1 = dot8(e, *reinterpret_cast<const bf16x8 *>(a.wqT + static_cast<size_t>(mm1) * a.D + k), acc1);
+                    }
+                    finish(acc0, acc1, m0, m1);
+                }
+            }
+            for (int j = kHeldM; wave + 8 * j < a.M; ++j) {
+                const int m0 = wave + 8 * j, m1 = m0 + 4, mm1 = m1 < a.M ? m1 : m0;
+                float acc0 = 0.0f, acc1 = 0.0f;
+                for (int k = lane * 8; k < a.D; k += 512) {
+                    const bf16x8 e = *reinterpret_cast<const bf16x8 *>(s_emb + k);
+                    acc0 = dot8(e, *reinterpret_cast<const bf16x8 *>(a.wqT + static_cast<size_t>(m0) * a.D + k), acc0);
+                    acc1 = dot8(e, *reinterpret_cast<const bf16x8 *>(a.wqT + static_cast<size_t>(mm1) * a.D + k), acc1);
+                }
+                finish(acc0, acc1, m0, m1);
+            }
+        }
         __syncthreads();
+        // ---- heads, cost, decision (Eq. 2, Eq. 3)
         if (wave == 0 && h == 0 && vd) {
             const float zz0 = s_z[0][n][0] + s_z[1][n][0] + s_z[2][n][0] + s_z[3][n][0];
             const float zz1 = s_z[0][n][1] + s_z[1][n][1] + s_z[2][n][1] + s_z[3][n][1];
@@ -212,15 +323,10 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
                 btp = tp;
             }
         }
-        __syncthreads();
+        if (ct + 1 < ntiles) __syncthreads();
     }
     if (wave == 0) {
-        uint64_t k = bkey;
-#pragma unroll
-        for (int off = 32; off >= 1; off >>= 1) {
-            const uint64_t o = shfl_xor_u64(k, off);
-            k = o > k ? o : k;
-        }
+        const uint64_t k = wave_max(bkey);
         if (bkey == k && k != 0) {
             SingleOut *o = a.out;
             o->choice = key_pair(k);

@@ -20,7 +20,7 @@ HWR_OK, HWR_ERR_INVALID_ARG, HWR_ERR_OOM, HWR_ERR_HIP, HWR_ERR_STATE, HWR_ERR_UN
 HWR_F32, HWR_BF16 = 0, 1
 HWR_MEM_DEVICE, HWR_MEM_HOST = 0, 1
 HWR_PIPE_FUSED, HWR_PIPE_STAGED = 0, 1
-HWR_FLAG_NO_GRAPH = 1
+HWR_FLAG_GRAPH = 1
 HWR_K_STATE, HWR_K_QUALITY, HWR_K_GATHER, HWR_K_MLP, HWR_K_EPILOGUE, HWR_K_FUSED, HWR_K_MERGE, HWR_K_SINGLE = range(8)
 HWR_K_COUNT = 8
 KERNEL_NAMES = ["state", "quality", "gather", "mlp", "epilogue", "fused", "merge", "single"]

@@ -118,7 +118,7 @@ def test_c5_full_size_sampled():
     assert (out["choice"] >= 0).all() and (out["choice"] < r.N).all()
 
 
-@pytest.mark.parametrize("flags", [0, hwr.HWR_FLAG_NO_GRAPH])
+@pytest.mark.parametrize("flags", [0, hwr.HWR_FLAG_GRAPH])
 def test_c4_single_query_walk(flags):
     """Sequential single-query calls with a state update between each."""
     sp = S.spec("C4")

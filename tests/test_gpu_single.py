@@ -28,7 +28,7 @@ def _device():
     ("C5", dict()),                                   # H = 256, 256 pairs (8 tiles), D = 1536, M = 32
     ("C2", dict(n_models=5, n_gpu_types=3)),          # 15 pairs, odd model count
 ])
-@pytest.mark.parametrize("flags", [0, hwr.HWR_FLAG_NO_GRAPH])
+@pytest.mark.parametrize("flags", [0, hwr.HWR_FLAG_GRAPH])
 def test_single_query_matches_oracle(name, kw, flags):
     sp = S.spec(name, n_queries=40, **kw)
     pb, st, qs = S.make_problem(sp, 17), S.make_state(sp, 17), S.make_queries(sp, 17)
