@@ -38,10 +38,12 @@ def predictor_flops(F: int, H: int) -> int:
     return 2 * (F * H + H * H + 2 * H)
 
 
-def throughput(args, S, hwr, torch):
+def prepare(args, S, torch):
+    """The throughput workload, generated chunk by chunk and made resident in
+    HBM before any timing."""
     sp = S.spec(args.workload)
     pb, st = S.make_problem(sp, args.seed), S.make_state(sp, args.seed)
-    n, N, M, D = sp.total_queries, sp.n_deployments, sp.n_models, sp.embed_dim
+    n, D = sp.total_queries, sp.embed_dim
     dev = torch.device("cuda:0")
     emb = torch.empty((n, D), dtype=torch.int16, device=dev)
     il = torch.empty(n, dtype=torch.int32, device=dev)
@@ -58,10 +60,27 @@ def throughput(args, S, hwr, torch):
         if c == 0:
             sample = qs.slice(0, args.cpu_sample)
         log(f"generated chunk {c + 1}/{sp.n_chunks}")
+    return dict(sp=sp, pb=pb, st=st, emb=emb, il=il, no=no, slo=slo, sample=sample)
+
+
+def hbm_line(nbytes: float, avg_ms: float, kernel: str) -> dict:
+    gbs = nbytes / (avg_ms / 1e3) / 1e9 if avg_ms > 0 else 0.0
+    return {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": gbs / PEAK_HBM_GBS, "bytes_per_launch": nbytes, "avg_launch_ms": avg_ms,
+            "kernel": kernel}
+
+
+def throughput(args, hwr, torch, w, pipeline, steps, warmup):
+    """Time `steps` calls of hwr_route_batch over the whole workload with one
+    pipeline; per-kernel durations from the library's HIP events on the
+    stream the kernels run on."""
+    sp = w["sp"]
+    n, N, M, D = sp.total_queries, sp.n_deployments, sp.n_models, sp.embed_dim
+    dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream()
-    r = hwr.Router.from_problem(pb, max_chunk=sp.n_queries, pipeline=args.pipeline,
+    r = hwr.Router.from_problem(w["pb"], max_chunk=sp.n_queries, pipeline=pipeline,
                                 stream=int(stream.cuda_stream))
-    r.update(st)
+    r.update(w["st"])
     out = dict(choice=torch.empty(n, dtype=torch.int32, device=dev),
                feasible=torch.empty(n, dtype=torch.uint8, device=dev),
                utility=torch.empty(n, dtype=torch.float32, device=dev),
@@ -70,19 +89,19 @@ def throughput(args, S, hwr, torch):
                tpot_s=torch.empty(n, dtype=torch.float32, device=dev))
 
     def step():
-        r.route(emb, il, no, slo, mem=hwr.HWR_MEM_DEVICE, **out)
+        r.route(w["emb"], w["il"], w["no"], w["slo"], mem=hwr.HWR_MEM_DEVICE, **out)
 
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         step()
     torch.cuda.synchronize()
-    log(f"warmup done ({args.warmup} steps)")
+    log(f"{pipeline}: warmup done ({warmup} steps)")
     r.profile(True)
     r.profile_read(reset=True)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     e0.record(stream)
-    for _ in range(args.steps):
+    for _ in range(steps):
         step()
     e1.record(stream)
     torch.cuda.synchronize()
@@ -90,42 +109,48 @@ def throughput(args, S, hwr, torch):
     kt = r.profile_read(reset=True)
     r.profile(False)
     gpu_ms = e0.elapsed_time(e1)
-    log(f"timed {args.steps} steps: {gpu_ms:.2f} ms (events), {wall * 1e3:.2f} ms (host)")
+    log(f"{pipeline}: timed {steps} steps: {gpu_ms:.2f} ms (events), {wall * 1e3:.2f} ms (host)")
     choice = out["choice"].cpu().numpy()
     assert (choice >= 0).all() and (choice < N).all(), "choice out of range"
-    ms_step = max(gpu_ms, wall * 1e3) / args.steps
+    r.close()
+    ms_step = max(gpu_ms, wall * 1e3) / steps
     value = n * N / (ms_step / 1e3)
 
-    kname = "fused" if args.pipeline == "fused" else "mlp"
-    k_ms, k_n = kt[kname]
-    k_avg_ms = k_ms / max(k_n, 1)
-    chunk_cands = sp.n_queries * N
+    def avg(k):
+        ms, cnt = kt[k]
+        return ms / cnt if cnt else 0.0
+
+    kname = "fused" if pipeline == "fused" else "mlp"
+    k_avg_ms = avg(kname)
+    nq = sp.n_queries
+    chunk_cands = nq * N
     flops = predictor_flops(sp.feat_dim, sp.hidden) * chunk_cands
     achieved = flops / (k_avg_ms / 1e3) / 1e12
-    q_ms, q_n = kt["quality"]
-    q_avg = q_ms / max(q_n, 1)
-    q_bytes = sp.n_queries * (D * 2 + M * 4) + D * 32 * 2
-    stages = {k: {"avg_ms": (v[0] / v[1]) if v[1] else 0.0, "launches_per_step": v[1] / args.steps}
+    stages = {k: {"avg_ms": (v[0] / v[1]) if v[1] else 0.0, "launches_per_step": v[1] / steps}
               for k, v in kt.items() if v[1]}
     res = dict(
-        value=value, ms_per_step=ms_step,
+        value=value, ms_per_step=ms_step, stages=stages,
         roofline={"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                   "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
-                  "kernel": f"k_mlp_bf16<{sp.hidden}> ({args.pipeline})",
+                  "kernel": f"k_mlp_bf16<{sp.hidden}> ({pipeline})",
                   "flop_per_launch": flops, "avg_launch_ms": k_avg_ms},
-        quality_roofline={"bound": "hbm", "achieved": q_bytes / (q_avg / 1e3) / 1e9, "peak": PEAK_HBM_GBS,
-                          "unit": "GB/s", "frac": q_bytes / (q_avg / 1e3) / 1e9 / PEAK_HBM_GBS,
-                          "bytes_per_launch": q_bytes, "avg_launch_ms": q_avg},
-        stages=stages,
+        # per chunk: embeddings read, Q matrix written, heads read once
+        quality_roofline=hbm_line(nq * (D * 2 + M * 4) + D * 32 * 2, avg("quality"), "k_quality_bf16"),
         config={"workload": f"{sp.name} throughput stress: {n} queries x {N} pairs ({M} models x "
                             f"{sp.n_gpu_types} GPU types), embed {D} bf16, predictor "
                             f"{sp.feat_dim}-{sp.hidden}-{sp.hidden}-2 bf16/fp32-acc, "
-                            f"{sp.n_chunks} chunks of {sp.n_queries} on one stream",
-                "queries": n, "pairs": N, "chunk": sp.n_queries, "pipeline": args.pipeline,
-                "seed": args.seed},
+                            f"{sp.n_chunks} chunks of {nq} on one stream",
+                "queries": n, "pairs": N, "chunk": nq, "pipeline": pipeline, "seed": args.seed},
     )
-    r.close()
-    return res, pb, st, sample, sp
+    if pipeline == "staged":
+        # gather: writes the feature matrix X (64 B per candidate), reads the
+        # input lengths and the pair rows; epilogue: reads TTFT and TPOT
+        # (8 B per candidate), the Q matrix, N_out and the bound, writes
+        # choice, feasible and four floats per query
+        res["gather_roofline"] = hbm_line(chunk_cands * 64 + nq * 4 + N * 64, avg("gather"), "k_gather")
+        res["epilogue_roofline"] = hbm_line(chunk_cands * 8 + nq * (M * 4 + 8 + 21), avg("epilogue"),
+                                            "k_epilogue")
+    return res
 
 
 def single_query(args, S, hwr, torch, flags=0):
@@ -213,6 +238,8 @@ def main() -> int:
     ap.add_argument("--workload", default="C5")
     ap.add_argument("--pipeline", default="fused", choices=["fused", "staged"])
     ap.add_argument("--seed", type=int, default=5)
+    ap.add_argument("--staged-steps", type=int, default=5,
+                    help="steps of the staged pipeline (gather / epilogue HBM figures); 0 skips it")
     ap.add_argument("--c4-calls", type=int, default=10000)
     ap.add_argument("--cpu-sample", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -234,14 +261,24 @@ def main() -> int:
     if args.copy_probe:
         return copy_probe(torch)
     hwr.load()
-    res, pb, st, sample, sp = throughput(args, S, hwr, torch)
+    w = prepare(args, S, torch)
+    res = throughput(args, hwr, torch, w, args.pipeline, args.steps, args.warmup)
     log(f"throughput {res['value']:.3e} candidates/s, predictor {res['roofline']['achieved']:.1f} TFLOP/s")
+    staged = None
+    if args.pipeline == "fused" and args.staged_steps > 0:
+        sr = throughput(args, hwr, torch, w, "staged", args.staged_steps, 1)
+        staged = {"value": sr["value"], "unit": "candidates/s", "ms_per_step": sr["ms_per_step"],
+                  "steps": args.staged_steps, "gather_roofline": sr["gather_roofline"],
+                  "epilogue_roofline": sr["epilogue_roofline"], "mlp_roofline": sr["roofline"],
+                  "stages": sr["stages"]}
+        log(f"staged: gather {sr['gather_roofline']['frac']:.2f} of HBM, "
+            f"epilogue {sr['epilogue_roofline']['frac']:.2f} of HBM")
     single = None if args.no_single else single_query(args, S, hwr, torch)
     single_graph = None if args.no_single else single_query(args, S, hwr, torch, hwr.HWR_FLAG_GRAPH)
     if single:
         log(f"single query (kernel launch) p50 {single['p50_us']:.1f} us p99 {single['p99_us']:.1f} us; "
             f"(graph launch) p50 {single_graph['p50_us']:.1f} us p99 {single_graph['p99_us']:.1f} us")
-    cpu = None if args.no_cpu_baseline else cpu_baseline(pb, st, sample, sp)
+    cpu = None if args.no_cpu_baseline else cpu_baseline(w["pb"], w["st"], w["sample"], w["sp"])
     line = {
         "metric": METRIC, "value": res["value"], "unit": "candidates/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": res["ms_per_step"],
@@ -250,6 +287,7 @@ def main() -> int:
         "config": res["config"], "roofline": res["roofline"], "cpu_baseline": cpu,
         "single_query": single, "single_query_graph_launch": single_graph,
         "quality_roofline": res["quality_roofline"], "stages": res["stages"],
+        "staged_pipeline": staged,
     }
     print(json.dumps(line), flush=True)
     return 0

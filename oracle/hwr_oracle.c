@@ -181,3 +181,31 @@ int orc_route(const orc_problem *p, const orc_state *s, const orc_queries *q,
     free(qual);
     return 0;
 }
+
+int orc_decide(int32_t n, int32_t N, int32_t M, const int32_t *dep_model,
+               const float *cand_ttft, const float *cand_tpot, const float *quality,
+               const int32_t *expected_out_len, const float *slo_s, float alpha,
+               int32_t *choice, uint8_t *feasible, float *utility_out, float *e2e_out) {
+    if (n < 0 || N <= 0 || M <= 0) return -1;
+    for (int32_t iq = 0; iq < n; ++iq) {
+        const float slo = slo_s[iq];
+        const float nout = (float)expected_out_len[iq];
+        int32_t best = -1;
+        int best_f = 0;
+        float best_u = 0.0f, best_c = 0.0f;
+        for (int32_t d = 0; d < N; ++d) {
+            const size_t ci = (size_t)iq * N + d;
+            const float c = fmaf(cand_tpot[ci], nout, cand_ttft[ci]);
+            const int feas = (c <= slo);
+            const float u = utility(quality[(size_t)iq * M + dep_model[d]], alpha, c, slo);
+            if (best < 0 || feas > best_f || (feas == best_f && u > best_u)) {
+                best = d; best_f = feas; best_u = u; best_c = c;
+            }
+        }
+        choice[iq] = best;
+        feasible[iq] = (uint8_t)best_f;
+        utility_out[iq] = best_u;
+        e2e_out[iq] = best_c;
+    }
+    return 0;
+}

@@ -72,6 +72,15 @@ void  orc_features(const orc_problem *p, const orc_state *s, int32_t d,
 float orc_quality(const orc_problem *p, const float *emb_row, int32_t m);
 /* predictor on one feature vector: z[2] before softplus. */
 void  orc_mlp(const orc_problem *p, const float *x, float *z);
+/* Eq. 2 and Eq. 3 alone, on given predictions: for each of n queries, the
+ * candidates' TTFT and TPOT ([n*N]) and the per-model quality ([n*M], mapped
+ * to pairs through dep_model) -> the choice and its feasibility, utility and
+ * cost, with the same arithmetic and tie rule as orc_route.  Returns 0, or -1
+ * on bad sizes. */
+int   orc_decide(int32_t n, int32_t N, int32_t M, const int32_t *dep_model,
+                 const float *cand_ttft, const float *cand_tpot, const float *quality,
+                 const int32_t *expected_out_len, const float *slo_s, float alpha,
+                 int32_t *choice, uint8_t *feasible, float *utility_out, float *e2e_out);
 /* the whole path over a batch of queries.  Returns 0, or -1 on bad sizes. */
 int   orc_route(const orc_problem *p, const orc_state *s, const orc_queries *q,
                 orc_result *r);

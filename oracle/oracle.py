@@ -87,6 +87,9 @@ def lib():
         L.orc_quality.argtypes = [C.POINTER(_Problem), _f32p, C.c_int32]
         L.orc_mlp.restype = None
         L.orc_mlp.argtypes = [C.POINTER(_Problem), _f32p, _f32p]
+        L.orc_decide.restype = C.c_int
+        L.orc_decide.argtypes = [C.c_int32, C.c_int32, C.c_int32, _i32p, _f32p, _f32p, _f32p, _i32p,
+                                 _f32p, C.c_float, _i32p, _u8p, _f32p, _f32p]
         L.orc_route.restype = C.c_int
         L.orc_route.argtypes = [C.POINTER(_Problem), C.POINTER(_State), C.POINTER(_Queries),
                                 C.POINTER(_Result)]
@@ -261,6 +264,27 @@ def route(prob: OracleProblem, state: np.ndarray, emb: np.ndarray, input_len, ex
     rc = lib().orc_route(C.byref(p), C.byref(s), C.byref(q), C.byref(r))
     if rc != 0:
         raise ValueError("oracle rejected the problem sizes")
+    return out
+
+
+def decide(dep_model, cand_ttft, cand_tpot, quality, expected_out_len, slo_s, alpha: float) -> dict:
+    """Eq. 2 and Eq. 3 on given predictions (the decision step alone, same
+    arithmetic and tie rule as ``route``): per query the choice, feasibility,
+    utility and cost.  Inputs: TTFT / TPOT [n, N], quality [n, M]."""
+    tt, tp, qual = _f32(cand_ttft), _f32(cand_tpot), _f32(quality)
+    n, N = tt.shape
+    M = qual.shape[1]
+    dm, no, slo = _i32(dep_model), _i32(expected_out_len), _f32(slo_s)
+    assert tp.shape == (n, N) and qual.shape[0] == n and dm.shape == (N,)
+    assert no.shape == (n,) and slo.shape == (n,)
+    out = {"choice": np.zeros(n, np.int32), "feasible": np.zeros(n, np.uint8),
+           "utility": np.zeros(n, np.float32), "e2e_s": np.zeros(n, np.float32)}
+    rc = lib().orc_decide(n, N, M, _ptr(dm, C.c_int32), _ptr(tt, C.c_float), _ptr(tp, C.c_float),
+                          _ptr(qual, C.c_float), _ptr(no, C.c_int32), _ptr(slo, C.c_float),
+                          float(alpha), _ptr(out["choice"], C.c_int32), _ptr(out["feasible"], C.c_uint8),
+                          _ptr(out["utility"], C.c_float), _ptr(out["e2e_s"], C.c_float))
+    if rc != 0:
+        raise ValueError("oracle rejected the sizes")
     return out
 
 

@@ -579,15 +579,21 @@ hwr_status route_device(hwr_ctx *c, const DevBatch &b) {
         EpilogueArgs ea{};
         ea.N = N;
         ea.M = M;
-        int g = 1;
-        while (g < N && g < 64) g <<= 1;
-        ea.group = g;
         ea.alpha = c->alpha;
         ea.q = qa;
         ea.dep_model = c->d_dep_model;
         ea.qmat = qmat;
         ea.cand_ttft = ctt ? ctt : c->d_ctt;
         ea.cand_tpot = ctp ? ctp : c->d_ctp;
+        ea.vec4 = N % 4 == 0 && reinterpret_cast<uintptr_t>(ea.cand_ttft) % 16 == 0 &&
+                  reinterpret_cast<uintptr_t>(ea.cand_tpot) % 16 == 0;
+        // lanes per query: a power of two from 8 (which bounds the LDS rows of
+        // the quality matrix a workgroup stages) up to 64, with up to four
+        // slices of the row per lane
+        const int units = ea.vec4 ? N / 4 : N;
+        int g = 8;
+        while (g * 4 < units && g < 64) g <<= 1;
+        ea.group = g;
         ea.out = oa;
         HWR_HIP(c, timed(c, HWR_K_EPILOGUE, [&] { return launch_epilogue(ea, c->stream); }));
     }

@@ -78,21 +78,85 @@ __device__ inline bf16x2 relu_bf16x2(float a, float b) {
     return __builtin_bit_cast(bf16x2, s);
 }
 
+// A query's latency bound with its correctly rounded reciprocal, for the
+// division C / SLO of the utility (computed once per query).
+struct Bound {
+    float slo, rcp;
+    bool fast;                    // slo in [2^-20, 2^20]: the reciprocal path applies
+};
+__device__ inline Bound make_bound(float slo) {
+    Bound b;
+    b.slo = slo;
+    b.rcp = __fdiv_rn(1.0f, slo);
+    b.fast = slo >= 0x1p-20f && slo <= 0x1p20f;
+    return b;
+}
+
+// RN(c / slo), the IEEE quotient, from y = RN(1 / slo): q0 = RN(c y), the
+// remainder r = c - q0 slo (exact with one FMA), then RN(q0 + r y).  With y
+// within half an ulp of 1 / slo and q0 within one ulp of the quotient, this
+// correction gives the correctly rounded quotient (P. Markstein, IBM J. Res.
+// Dev. 34(1), 1990; Muller et al., Handbook of Floating-Point Arithmetic,
+// division by FMA).  The ranges keep every step clear of underflow and
+// overflow; outside them the plain IEEE division is used.
+__device__ inline float div_bound(float c, const Bound &b) {
+    const float q0 = __fmul_rn(c, b.rcp);
+    const float r = __fmaf_rn(-q0, b.slo, c);
+    float t = __fmaf_rn(r, b.rcp, q0);
+    if (!(b.fast && c >= 0x1p-60f && c <= 0x1p60f)) {
+        asm volatile("");         // a real branch: keeps the division off the common path
+        t = __fdiv_rn(c, b.slo);
+    }
+    return t;
+}
+
 // Candidate decision values: cost (Eq. 2), bound test (Eq. 3) and utility,
 // each fp32 operation rounded once.
 struct Decision {
     float e2e, u;
     bool feasible;
 };
-__device__ inline Decision decide(float ttft, float tpot, float nout, float slo,
+__device__ inline Decision decide(float ttft, float tpot, float nout, const Bound &bound,
                                   float quality, float alpha) {
     Decision r;
     r.e2e = __fmaf_rn(tpot, nout, ttft);
-    r.feasible = r.e2e <= slo;
-    const float t = __fdiv_rn(r.e2e, slo);
+    r.feasible = r.e2e <= bound.slo;
+    const float t = div_bound(r.e2e, bound);
     r.u = __fsub_rn(quality, __fmul_rn(alpha, t));
     return r;
 }
+
+// Running best candidate of one lane (Eq. 3), offered candidates in
+// increasing pair order: feasibility first, then utility; a candidate
+// replaces the best only when strictly better, so ties keep the lower pair
+// index.  A NaN utility ranks as -inf and -0 as +0, exactly as in
+// decision_key (the stored utility takes the same canonical value); the key
+// is built once, for the reduction across lanes.
+struct Best {
+    float u, e2e, tt, tp;
+    int d;                        // -1: no candidate yet
+    bool f;
+};
+__device__ inline Best best_none() {
+    Best b;
+    b.u = -__builtin_huge_valf();
+    b.e2e = b.tt = b.tp = 0.0f;
+    b.d = -1;
+    b.f = false;
+    return b;
+}
+__device__ inline void offer(Best &b, const Decision &r, int d, float tt, float tp) {
+    const float u = fmaxf(r.u, -__builtin_huge_valf()) + 0.0f;   // NaN -> -inf, -0 -> +0
+    const bool better = b.d < 0 || (r.feasible && !b.f) || (r.feasible == b.f && u > b.u);
+    // selects, not a branch: one v_cndmask per field
+    b.u = better ? u : b.u;
+    b.e2e = better ? r.e2e : b.e2e;
+    b.tt = better ? tt : b.tt;
+    b.tp = better ? tp : b.tp;
+    b.d = better ? d : b.d;
+    b.f = better ? r.feasible : b.f;
+}
+__device__ inline uint64_t best_key(const Best &b) { return b.d < 0 ? 0 : decision_key(b.f, b.u, b.d); }
 
 // Put the bf16 bits xl into element `elem` (0..7) of v.
 __device__ inline bf16x8 put_elem(bf16x8 v, int elem, uint32_t xl) {
@@ -111,6 +175,33 @@ __device__ inline uint64_t shfl_xor_u64(uint64_t v, int m) {
     const uint32_t lo = __shfl_xor(static_cast<uint32_t>(v), m);
     const uint32_t hi = __shfl_xor(static_cast<uint32_t>(v >> 32), m);
     return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
+// Cross-lane steps on DPP (data-parallel primitives inside a 16-lane row):
+// quad permutes, half-row and row mirrors; no LDS round trip.
+template <int Ctrl>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t v) {
+    return static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), Ctrl, 0xF, 0xF, false));
+}
+template <int Ctrl>
+__device__ __forceinline__ uint64_t max_dpp(uint64_t k) {
+    const uint64_t o = (static_cast<uint64_t>(dpp_u32<Ctrl>(static_cast<uint32_t>(k >> 32))) << 32) |
+                       dpp_u32<Ctrl>(static_cast<uint32_t>(k));
+    return o > k ? o : k;
+}
+// Maximum of a key over aligned groups of G lanes (G a power of two <= 64,
+// the same in the whole wave); every lane of a group receives it.  Lanes
+// without a candidate hold 0.
+__device__ inline uint64_t group_max_u64(uint64_t k, int G) {
+    if (G > 1) k = max_dpp<0xB1>(k);     // quad_perm [1,0,3,2]: lane ^ 1
+    if (G > 2) k = max_dpp<0x4E>(k);     // quad_perm [2,3,0,1]: lane ^ 2
+    if (G > 4) k = max_dpp<0x141>(k);    // row_half_mirror: the other quad of 8
+    if (G > 8) k = max_dpp<0x140>(k);    // row_mirror: the other 8 of 16
+    for (int off = 16; off < G; off <<= 1) {
+        const uint64_t o = shfl_xor_u64(k, off);
+        k = o > k ? o : k;
+    }
+    return k;
 }
 
 __device__ inline void write_outputs(const OutArgs &o, int q, uint64_t key, float u,

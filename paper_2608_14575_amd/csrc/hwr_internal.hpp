@@ -120,7 +120,8 @@ struct GatherArgs {
 };
 
 struct EpilogueArgs {
-    int N, M, group;
+    int N, M, group;              // group: lanes per query (power of two <= 64)
+    int vec4;                     // 1: N % 4 == 0 and TTFT / TPOT rows 16-byte aligned
     float alpha;
     QueryArgs q;
     const int32_t *dep_model;

@@ -167,7 +167,7 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
     const int qmc = vme ? qme : 0;
     const int32_t nomy = a.q.nout[qmc];
     const float nout = static_cast<float>(nomy < 0 ? 0 : nomy);
-    const float slo = a.q.slo ? a.q.slo[qmc] : a.q.default_slo;
+    const Bound bound = make_bound(a.q.slo ? a.q.slo[qmc] : a.q.default_slo);
     // the input-length slot: k-block, lane half and element holding it
     const int ls_kb = a.len_slot >> 4, ls_h = (a.len_slot >> 3) & 1, ls_e = a.len_slot & 7;
     const bool patch = (h == ls_h);
@@ -179,8 +179,7 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
     const int d0 = static_cast<int>(span0 + (span1 - span0) * grp / 2);
     const int d1 = static_cast<int>(span0 + (span1 - span0) * (grp + 1) / 2);
 
-    uint64_t bkey = 0;
-    float bu = 0.0f, be = 0.0f, btt = 0.0f, btp = 0.0f;
+    Best best = best_none();
 
     // Per-pair inputs are loaded one step ahead: the pair's feature row
     // (fused) or the candidates' feature rows (staged), and the quality
@@ -360,18 +359,12 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
                 a.cand_tpot[ci] = tp;
             }
             // ---- cost, bound test, utility, running argmax (Eq. 2, Eq. 3)
-            const Decision r = decide(tt, tp, nout, slo, Qd, a.alpha);
-            const uint64_t k = decision_key(r.feasible, r.u, d);
-            if (k > bkey) {
-                bkey = k;
-                bu = r.u;
-                be = r.e2e;
-                btt = tt;
-                btp = tp;
-            }
+            offer(best, decide(tt, tp, nout, bound, Qd, a.alpha), d, tt, tp);
         }
     }
     if constexpr (!STAGED) {
+        uint64_t bkey = best_key(best);
+        float bu = best.u, be = best.e2e, btt = best.tt, btp = best.tp;
         // merge the two pair halves of each query through LDS
         const int slot = qw * kQPerWave + lane;
         if (grp == 1) {

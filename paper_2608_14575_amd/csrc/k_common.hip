@@ -158,45 +158,98 @@ hipError_t launch_gather(const GatherArgs &a, hipStream_t s) {
 
 // ------------------------------------------------------------ decision epilogue
 // Per query: cost (Eq. 2), bound test and utility for every pair, then the
-// Eq. 3 argmax as a maximum of packed decision keys, reduced across the
-// `group` lanes that share the query by wavefront shuffles.
+// Eq. 3 argmax as a maximum of packed decision keys over the `group` lanes
+// that share the query.  A lane takes up to kEpiSlices slices of the row
+// (4 pairs each with 16-byte loads when rows are aligned, else 1 pair); the
+// models of its pairs are the same for every query, so they are loaded
+// alongside.  Each wave stages the quality rows of its own queries in LDS
+// (no workgroup barrier).  Each lane keeps its own best candidate, so the
+// lane holding the winning key writes the outputs without reading anything
+// again.
+constexpr int kEpiSlices = 4;
+
+template <bool V4>
 __global__ __launch_bounds__(256) void k_epilogue(EpilogueArgs a) {
+    extern __shared__ float s_qm[];            // [4 waves][64 / G][M] quality rows
     const int G = a.group;
-    const long gid = static_cast<long>(blockIdx.x) * blockDim.x + threadIdx.x;
-    const long q = gid / G;
-    const int g = static_cast<int>(gid & (G - 1));
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = tid & (G - 1);
+    const int qpw = 64 / G;                    // queries per wave
+    const int qw0 = blockIdx.x * (kBlock / G) + wave * qpw;
+    const int q = qw0 + lane / G;
     const bool valid = q < a.q.nq;
-    const long qc = valid ? q : 0;
+    const int qc = valid ? q : 0;
+    const int units = V4 ? a.N / 4 : a.N;
+    const float *tt_row = a.cand_ttft + static_cast<size_t>(qc) * a.N;
+    const float *tp_row = a.cand_tpot + static_cast<size_t>(qc) * a.N;
+    auto load = [&](int u, f32x4 &tv, f32x4 &pv, int4 &mv) {
+        if (V4) {
+            tv = reinterpret_cast<const f32x4 *>(tt_row)[u];
+            pv = reinterpret_cast<const f32x4 *>(tp_row)[u];
+            mv = reinterpret_cast<const int4 *>(a.dep_model)[u];
+        } else {
+            tv[0] = tt_row[u];
+            pv[0] = tp_row[u];
+            mv.x = a.dep_model[u];
+        }
+    };
+    f32x4 t4[kEpiSlices], p4[kEpiSlices];
+    int4 m4[kEpiSlices];
+#pragma unroll
+    for (int j = 0; j < kEpiSlices; ++j) {
+        t4[j] = f32x4{0, 0, 0, 0};
+        p4[j] = f32x4{0, 0, 0, 0};
+        m4[j] = int4{0, 0, 0, 0};
+        const int u = g + j * G;
+        if (valid && u < units) load(u, t4[j], p4[j], m4[j]);
+    }
     const int32_t no = a.q.nout[qc];
     const float nout = static_cast<float>(no < 0 ? 0 : no);
-    const float slo = a.q.slo ? a.q.slo[qc] : a.q.default_slo;
-    uint64_t best = 0;
-    if (valid) {
-        for (int d = g; d < a.N; d += G) {
-            const size_t ci = static_cast<size_t>(qc) * a.N + d;
-            const float Q = a.qmat[qc * a.M + a.dep_model[d]];
-            const Decision r = decide(a.cand_ttft[ci], a.cand_tpot[ci], nout, slo, Q, a.alpha);
-            const uint64_t k = decision_key(r.feasible, r.u, d);
-            best = k > best ? k : best;
+    const Bound bound = make_bound(a.q.slo ? a.q.slo[qc] : a.q.default_slo);
+    float *s_qw = s_qm + wave * qpw * a.M;
+    const int nqw = max(0, min(qpw, a.q.nq - qw0));
+    for (int i = lane; i < nqw * a.M; i += 64) s_qw[i] = a.qmat[static_cast<size_t>(qw0) * a.M + i];
+    // the rows are read by other lanes of the same wave only: wait for this
+    // wave's LDS writes, no workgroup barrier
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+    const float *qrow = s_qw + (lane / G) * a.M;
+    Best best = best_none();
+    auto consider = [&](int d, int model, float tt, float tp) {
+        offer(best, decide(tt, tp, nout, bound, qrow[model], a.alpha), d, tt, tp);
+    };
+    auto consider_slice = [&](int u, const f32x4 &tv, const f32x4 &pv, const int4 &mv) {
+        if (V4) {
+            consider(4 * u + 0, mv.x, tv[0], pv[0]);
+            consider(4 * u + 1, mv.y, tv[1], pv[1]);
+            consider(4 * u + 2, mv.z, tv[2], pv[2]);
+            consider(4 * u + 3, mv.w, tv[3], pv[3]);
+        } else {
+            consider(u, mv.x, tv[0], pv[0]);
         }
+    };
+#pragma unroll
+    for (int j = 0; j < kEpiSlices; ++j) {
+        const int u = g + j * G;
+        if (valid && u < units) consider_slice(u, t4[j], p4[j], m4[j]);
     }
-    for (int off = G >> 1; off >= 1; off >>= 1) {
-        const uint64_t o = shfl_xor_u64(best, off);
-        best = o > best ? o : best;
+    for (int u = g + kEpiSlices * G; valid && u < units; u += G) {
+        f32x4 tv = {0, 0, 0, 0}, pv = {0, 0, 0, 0};
+        int4 mv = {0, 0, 0, 0};
+        load(u, tv, pv, mv);
+        consider_slice(u, tv, pv, mv);
     }
-    if (valid && g == 0) {
-        const int d = key_pair(best);
-        const size_t ci = static_cast<size_t>(qc) * a.N + d;
-        const float tt = a.cand_ttft[ci], tp = a.cand_tpot[ci];
-        const Decision r = decide(tt, tp, nout, slo, a.qmat[qc * a.M + a.dep_model[d]], a.alpha);
-        write_outputs(a.out, static_cast<int>(q), best, r.u, r.e2e, tt, tp);
-    }
+    const uint64_t k = best_key(best);
+    const uint64_t m = group_max_u64(k, G);
+    if (valid && k == m && k != 0) write_outputs(a.out, q, k, best.u, best.e2e, best.tt, best.tp);
 }
 
 hipError_t launch_epilogue(const EpilogueArgs &a, hipStream_t s) {
-    const long threads = static_cast<long>(a.q.nq) * a.group;
-    hipLaunchKernelGGL(k_epilogue, dim3(static_cast<unsigned>((threads + 255) / 256)), dim3(256), 0,
-                       s, a);
+    const int qpb = kBlock / a.group;
+    const unsigned grid = static_cast<unsigned>((a.q.nq + qpb - 1) / qpb);
+    const size_t lds = static_cast<size_t>(qpb) * a.M * 4;
+    if (a.vec4) hipLaunchKernelGGL(k_epilogue<true>, dim3(grid), dim3(kBlock), lds, s, a);
+    else hipLaunchKernelGGL(k_epilogue<false>, dim3(grid), dim3(kBlock), lds, s, a);
     return hipGetLastError();
 }
 

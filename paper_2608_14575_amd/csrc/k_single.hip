@@ -47,10 +47,6 @@ __device__ __forceinline__ void pair_row(uint16_t *row, int j, int b0, int ks, i
 // row: quad permutes, half-row and row mirrors), then one read of each row's
 // lane 0; no LDS round trips.  After the four steps every lane of a row holds
 // the row's result.
-template <int Ctrl>
-__device__ __forceinline__ uint32_t dpp_u32(uint32_t v) {
-    return static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), Ctrl, 0xF, 0xF, false));
-}
 __device__ __forceinline__ float wave_sum(float v) {
     v += __uint_as_float(dpp_u32<0xB1>(__float_as_uint(v)));    // quad_perm [1,0,3,2]
     v += __uint_as_float(dpp_u32<0x4E>(__float_as_uint(v)));    // quad_perm [2,3,0,1]
@@ -59,12 +55,6 @@ __device__ __forceinline__ float wave_sum(float v) {
     const int b = __float_as_int(v);
     return (__int_as_float(__builtin_amdgcn_readlane(b, 0)) + __int_as_float(__builtin_amdgcn_readlane(b, 16))) +
            (__int_as_float(__builtin_amdgcn_readlane(b, 32)) + __int_as_float(__builtin_amdgcn_readlane(b, 48)));
-}
-template <int Ctrl>
-__device__ __forceinline__ uint64_t max_dpp(uint64_t k) {
-    const uint64_t o = (static_cast<uint64_t>(dpp_u32<Ctrl>(static_cast<uint32_t>(k >> 32))) << 32) |
-                       dpp_u32<Ctrl>(static_cast<uint32_t>(k));
-    return o > k ? o : k;
 }
 __device__ __forceinline__ uint64_t wave_max(uint64_t k) {
     k = max_dpp<0xB1>(k);
@@ -160,7 +150,7 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
     const uint32_t seq = hdr[0];
     const int32_t len = static_cast<int32_t>(hdr[1]);
     const int32_t no = static_cast<int32_t>(hdr[2]);
-    const float slo = __uint_as_float(hdr[3]);
+    const Bound bound = make_bound(__uint_as_float(hdr[3]));
 
     // ---- phase 2: LDS stores, the feature rows, one barrier
 #pragma unroll
@@ -185,8 +175,7 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
     __syncthreads();
 
     const float nout = static_cast<float>(no < 0 ? 0 : no);
-    uint64_t bkey = 0;
-    float bu = 0.0f, be = 0.0f, btt = 0.0f, btp = 0.0f;
+    Best best = best_none();
     const int ntiles = (a.N + 31) / 32;
     for (int ct = 0; ct < ntiles; ++ct) {
         const int d = ct * 32 + n;
@@ -313,28 +302,21 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
             const float zz1 = s_z[0][n][1] + s_z[1][n][1] + s_z[2][n][1] + s_z[3][n][1];
             const float tt = softplus_fast(zz0 + a.b3_0);
             const float tp = softplus_fast(zz1 + a.b3_1);
-            const Decision r = decide(tt, tp, nout, slo, s_q[model], a.alpha);
-            const uint64_t k = decision_key(r.feasible, r.u, d);
-            if (k > bkey) {
-                bkey = k;
-                bu = r.u;
-                be = r.e2e;
-                btt = tt;
-                btp = tp;
-            }
+            offer(best, decide(tt, tp, nout, bound, s_q[model], a.alpha), d, tt, tp);
         }
         if (ct + 1 < ntiles) __syncthreads();
     }
     if (wave == 0) {
+        const uint64_t bkey = best_key(best);
         const uint64_t k = wave_max(bkey);
         if (bkey == k && k != 0) {
             SingleOut *o = a.out;
             o->choice = key_pair(k);
             o->feasible = key_feasible(k) ? 1u : 0u;
-            o->utility = bu;
-            o->e2e = be;
-            o->ttft = btt;
-            o->tpot = btp;
+            o->utility = best.u;
+            o->e2e = best.e2e;
+            o->ttft = best.tt;
+            o->tpot = best.tp;
             __threadfence_system();
             __hip_atomic_store(&o->seq, seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
         }

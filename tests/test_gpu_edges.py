@@ -197,3 +197,56 @@ def test_unsupported_shapes_are_rejected():
     with pytest.raises(hwr.HwrError) as e:
         G.make_router(pb)
     assert e.value.status == hwr.HWR_ERR_UNSUPPORTED
+
+
+def _wide(seed: int, n_queries: int):
+    """1024 pairs: the 32 x 8 pair grid listed four times, each copy with its
+    own runtime signals (several pair slices per epilogue lane)."""
+    sp = S.spec("C5", n_queries=n_queries)
+    pb = S.make_problem(sp, seed)
+    pb.dep_model = np.tile(pb.dep_model, 4)
+    pb.dep_gpu = np.tile(pb.dep_gpu, 4)
+    st = np.concatenate([S.make_state(sp, seed + k) for k in range(4)])
+    return sp, pb, st, S.make_queries(sp, seed)
+
+
+@pytest.mark.parametrize("shape", ["15 pairs", "1 pair", "1024 pairs"])
+def test_staged_epilogue_shapes(shape):
+    """The staged decision epilogue against the fused path (bit-exact) and the
+    oracle, for pair counts that take its scalar path (N % 4 != 0), a
+    one-lane group, and several 4-pair slices per lane."""
+    if shape == "1024 pairs":
+        sp, pb, st, qs = _wide(41, 70)
+    else:
+        kw = dict(n_models=5, n_gpu_types=3) if shape == "15 pairs" else dict(n_models=1, n_gpu_types=1)
+        sp, pb, st, qs = _case(n_queries=301, seed=40, **kw)
+    f = G.make_router(pb, pipeline="fused")
+    s = G.make_router(pb, pipeline="staged")
+    f.update(st)
+    s.update(st)
+    of, os_ = G.route_device(f, qs, "bf16"), G.route_device(s, qs, "bf16")
+    _same(of, os_, keys=["choice", "feasible", "utility", "e2e_s", "ttft_s", "tpot_s"])
+    rep = G.check(pb, st, qs, os_)
+    print(f"[parity] staged {shape}: {rep.summary()}", flush=True)
+    assert rep.ok, rep.failures[:5]
+
+
+def test_staged_epilogue_unaligned_candidate_buffers():
+    """Caller candidate buffers 4 bytes off a 16-byte boundary: the epilogue
+    must fall back to element loads and give the same decisions."""
+    import torch
+    sp, pb, st, qs = _case(n_queries=257, seed=42)
+    r = G.make_router(pb, pipeline="staged")
+    r.update(st)
+    ref = G.route_device(r, qs, "bf16")
+    emb, il, no, slo = G.to_dev_inputs(qs, "bf16")
+    out = G.dev_outputs(qs.n, r.N, r.M, False)
+    n, N = qs.n, r.N
+    tt = torch.zeros(n * N + 1, dtype=torch.float32, device="cuda")
+    tp = torch.zeros(n * N + 1, dtype=torch.float32, device="cuda")
+    assert tt[1:].data_ptr() % 16 != 0
+    r.route(emb, il, no, slo, mem=hwr.HWR_MEM_DEVICE, cand_ttft=tt[1:], cand_tpot=tp[1:], **out)
+    torch.cuda.synchronize()
+    got = {k: v.cpu().numpy() for k, v in out.items()}
+    _same(got, ref, keys=list(got))
+    assert np.array_equal(tt[1:].cpu().numpy().reshape(n, N), ref["cand_ttft"])

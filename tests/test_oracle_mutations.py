@@ -33,6 +33,8 @@ MUTATIONS = {
         "if (dropped > 0x8000u || (dropped == 0x8000u && (kept & 1u))) kept += 1u;", ""),
     "softplus_sign": ("log1p(exp(-fabs(v)))", "log1p(exp(fabs(v)))"),
     "wrong_model_of_pair": ("qual[p->dep_model[d]]", "qual[d % M]"),
+    "decide_cost_terms_swapped": ("fmaf(cand_tpot[ci], nout, cand_ttft[ci])", "fmaf(cand_ttft[ci], nout, cand_tpot[ci])"),
+    "decide_model_of_pair": ("quality[(size_t)iq * M + dep_model[d]]", "quality[(size_t)iq * M + d % M]"),
 }
 
 

@@ -346,3 +346,49 @@ def test_bruteforce_all_pair_orders():
         assert np.array_equal(perm[r.choice], base.choice)
         ch, _ = BF.route(*BF.from_synth(pb2, st[perm].copy(), qs))
         assert np.array_equal(np.array(ch), r.choice)
+
+
+# ---------------------------------------------------------------- decision step alone
+def _decide1(tt, tp, q_of_pair, nout, slo, alpha=0.5):
+    """orc_decide on one query whose N pairs each have their own model."""
+    N = len(tt)
+    out = O.decide(np.arange(N), np.array([tt], np.float32), np.array([tp], np.float32),
+                   np.array([q_of_pair], np.float32), np.array([nout]), np.array([slo], np.float32), alpha)
+    return {k: v[0] for k, v in out.items()}
+
+
+@pytest.mark.parametrize("name,kw", [("C1", {}), ("C2", dict(n_queries=300)), ("C3", dict(n_queries=200))])
+def test_decide_reproduces_route(name, kw):
+    """Eq. 2 / Eq. 3 applied to the oracle's own predictions give the oracle's
+    decisions bit for bit (the route itself is pinned by brute force)."""
+    sp = S.spec(name, **kw)
+    pb, st, qs = S.make_problem(sp, 7), S.make_state(sp, 7), S.make_queries(sp, 7)
+    r = O.route_synth(pb, st, qs)
+    d = O.decide(pb.dep_model, r.cand_ttft, r.cand_tpot, r.quality, qs.expected_out_len, qs.slo_s,
+                 sp.cost_weight)
+    assert np.array_equal(d["choice"], r.choice)
+    assert np.array_equal(d["feasible"], r.feasible)
+    assert np.array_equal(d["utility"].view(np.int32), r.utility.view(np.int32))
+    assert np.array_equal(d["e2e_s"].view(np.int32), r.e2e_s.view(np.int32))
+
+
+def test_decide_hand_cases():
+    """Values fixed by Eq. 2 / Eq. 3 and the tie rule, computed by hand."""
+    # C = 0.5 + 2 * 0.25 = 1.0 exactly, on the bound: feasible; u = 0.7 - 0.5 * 1.0 / 1.0
+    r = _decide1([0.5], [0.25], [0.7], 2, 1.0)
+    assert r["feasible"] == 1 and r["e2e_s"] == np.float32(1.0)
+    assert r["utility"] == np.float32(np.float32(0.7) - np.float32(0.5))
+    # a feasible pair beats an infeasible one with higher quality
+    r = _decide1([2.0, 0.5], [0.0, 0.0], [0.9, 0.1], 0, 1.0)
+    assert r["choice"] == 1 and r["feasible"] == 1
+    # nothing feasible: the larger utility, reported infeasible
+    r = _decide1([3.0, 2.0], [0.0, 0.0], [0.5, 0.5], 0, 1.0)
+    assert r["choice"] == 1 and r["feasible"] == 0
+    # identical candidates: the lower index
+    r = _decide1([0.2, 0.2, 0.2], [0.01, 0.01, 0.01], [0.6, 0.6, 0.6], 10, 1.5)
+    assert r["choice"] == 0
+    # utility order among feasible pairs: u = Q - 0.5 * C / SLO
+    r = _decide1([0.2, 0.1], [0.0, 0.0], [0.6, 0.55], 0, 1.0)   # 0.5 vs 0.5: tie -> 0
+    assert r["choice"] == 0
+    r = _decide1([0.2, 0.05], [0.0, 0.0], [0.6, 0.55], 0, 1.0)  # 0.5 vs 0.525
+    assert r["choice"] == 1
