@@ -14,6 +14,8 @@ from __future__ import annotations
 
 import argparse
 import ctypes as C
+import glob
+import hashlib
 import json
 import os
 import sys
@@ -27,6 +29,40 @@ sys.path.insert(0, ROOT)
 METRIC = "routing candidates scored/sec (query×deployment) at 1 MI355X; p50 1-query route µs"
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_C5_1Mx256.json")
+KERNEL_NAMES = {   # as the profiler names them
+    "fused": "void hwr::k_mlp_bf16<256, false>(hwr::MlpArgs)",
+    "mlp": "void hwr::k_mlp_bf16<256, true>(hwr::MlpArgs)",
+    "quality": "hwr::k_quality_bf16(hwr::QualityArgs)",
+    "gather": "hwr::k_gather(hwr::GatherArgs)",
+    "epilogue": "void hwr::k_epilogue<true>(hwr::EpilogueArgs)",
+}
+
+
+def source_hash() -> str:
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2608_14575_amd", "csrc")
+    for f in sorted(glob.glob(os.path.join(csrc, "*.hip")) + glob.glob(os.path.join(csrc, "*.hpp"))):
+        h.update(os.path.basename(f).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def counter_traffic(workload: str) -> dict:
+    """HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, scaled by the copy
+    calibration) from the committed counter summary of this workload -- only
+    while the kernel sources are the ones the counters were taken on."""
+    if workload != "C5" or not os.path.exists(TRAFFIC_FILE):
+        return {}
+    with open(TRAFFIC_FILE) as fh:
+        rec = json.load(fh)
+    if rec.get("source_sha256") != source_hash():
+        return {}
+    per = {k: v["fetch_bytes"] + v["write_bytes"] for k, v in rec["kernels"].items()}
+    return {short: per[name] for short, name in KERNEL_NAMES.items() if name in per}
 
 
 def log(msg: str) -> None:
@@ -63,11 +99,11 @@ def prepare(args, S, torch):
     return dict(sp=sp, pb=pb, st=st, emb=emb, il=il, no=no, slo=slo, sample=sample)
 
 
-def hbm_line(nbytes: float, avg_ms: float, kernel: str) -> dict:
+def hbm_line(nbytes: float, avg_ms: float, kernel: str, traffic=None) -> dict:
     gbs = nbytes / (avg_ms / 1e3) / 1e9 if avg_ms > 0 else 0.0
     return {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-            "frac": gbs / PEAK_HBM_GBS, "bytes_per_launch": nbytes, "avg_launch_ms": avg_ms,
-            "kernel": kernel}
+            "frac": gbs / PEAK_HBM_GBS, "traffic": traffic, "bytes_per_launch": nbytes,
+            "avg_launch_ms": avg_ms, "kernel": kernel}
 
 
 def throughput(args, hwr, torch, w, pipeline, steps, warmup):
@@ -122,6 +158,7 @@ def throughput(args, hwr, torch, w, pipeline, steps, warmup):
 
     kname = "fused" if pipeline == "fused" else "mlp"
     k_avg_ms = avg(kname)
+    traffic = counter_traffic(args.workload)
     nq = sp.n_queries
     chunk_cands = nq * N
     flops = predictor_flops(sp.feat_dim, sp.hidden) * chunk_cands
@@ -131,11 +168,12 @@ def throughput(args, hwr, torch, w, pipeline, steps, warmup):
     res = dict(
         value=value, ms_per_step=ms_step, stages=stages,
         roofline={"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                  "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                  "frac": achieved / PEAK_BF16_TFLOPS, "traffic": traffic.get(kname),
                   "kernel": f"k_mlp_bf16<{sp.hidden}> ({pipeline})",
                   "flop_per_launch": flops, "avg_launch_ms": k_avg_ms},
         # per chunk: embeddings read, Q matrix written, heads read once
-        quality_roofline=hbm_line(nq * (D * 2 + M * 4) + D * 32 * 2, avg("quality"), "k_quality_bf16"),
+        quality_roofline=hbm_line(nq * (D * 2 + M * 4) + D * 32 * 2, avg("quality"), "k_quality_bf16",
+                                  traffic.get("quality")),
         config={"workload": f"{sp.name} throughput stress: {n} queries x {N} pairs ({M} models x "
                             f"{sp.n_gpu_types} GPU types), embed {D} bf16, predictor "
                             f"{sp.feat_dim}-{sp.hidden}-{sp.hidden}-2 bf16/fp32-acc, "
@@ -147,9 +185,10 @@ def throughput(args, hwr, torch, w, pipeline, steps, warmup):
         # input lengths and the pair rows; epilogue: reads TTFT and TPOT
         # (8 B per candidate), the Q matrix, N_out and the bound, writes
         # choice, feasible and four floats per query
-        res["gather_roofline"] = hbm_line(chunk_cands * 64 + nq * 4 + N * 64, avg("gather"), "k_gather")
+        res["gather_roofline"] = hbm_line(chunk_cands * 64 + nq * 4 + N * 64, avg("gather"), "k_gather",
+                                          traffic.get("gather"))
         res["epilogue_roofline"] = hbm_line(chunk_cands * 8 + nq * (M * 4 + 8 + 21), avg("epilogue"),
-                                            "k_epilogue")
+                                            "k_epilogue", traffic.get("epilogue"))
     return res
 
 
