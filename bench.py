@@ -18,6 +18,7 @@ import glob
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -42,12 +43,17 @@ KERNEL_NAMES = {   # as the profiler names them
 
 
 def source_hash() -> str:
+    """sha256 of the library's HIP sources with comments and whitespace
+    removed: changes to code change it, changes to comments do not."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2608_14575_amd", "csrc")
     for f in sorted(glob.glob(os.path.join(csrc, "*.hip")) + glob.glob(os.path.join(csrc, "*.hpp"))):
+        with open(f) as fh:
+            text = fh.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
         h.update(os.path.basename(f).encode())
-        with open(f, "rb") as fh:
-            h.update(fh.read())
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()
 
 

@@ -103,14 +103,17 @@ hipError_t launch_quality_bf16(const QualityArgs &a, hipStream_t s) {
 //   X^T  (32 features x 32 candidates, bf16)   built from the pair's feature
 //        row (L1-resident) and each query's input-length feature;
 //   h1^T = ReLU(W1^T X^T + b1)  -> bf16, registers;
-//   h2^T = ReLU(W2^T h1^T + b2) -> bf16, per 32-row tile, folded at once into
-//   z    = W3^T h2^T + b3 by packed bf16 dot products;
+//   h2^T = ReLU(W2^T h1^T + b2) -> bf16, per 32-row tile, each tile folded at
+//   once into the head layer z = W3^T h2^T + b3, itself an MFMA chain whose A
+//   fragments carry the two heads in rows 0-1 (tile 0) and 4-5 (tile 1);
 //   TTFT = softplus(z0), TPOT = softplus(z1).
-// W1, W2 (A operands), biases (as accumulator initial values) and W3 pairs
-// live in LDS.  After the heads, lane half h carries column tile h alone (one
-// query per lane).  Fused mode then applies Eq. 2, the bound test and the
-// utility and keeps a running maximum decision key per query (Eq. 3); staged
-// mode reads X from HBM and writes TTFT/TPOT per candidate instead.
+// The layers are software-pipelined: a tile's MFMAs are issued before the
+// previous tile's VALU epilogue (bias, ReLU, bf16 packing), so the matrix
+// pipe and the vector ALU overlap.  W1, W2 and W3 (A operands) and the biases
+// (accumulator initial values) live in LDS.  After the heads, lane half h
+// carries column tile h alone (one query per lane).  Fused mode then applies
+// Eq. 2, the bound test and the utility and keeps the query's best candidate
+// (Eq. 3); staged mode reads X from HBM and writes TTFT/TPOT per candidate.
 template <int H, bool STAGED>
 __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
     constexpr int MT = H / 32;     // 32-row tiles of a hidden layer
