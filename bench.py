@@ -34,11 +34,11 @@ PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_C5_1Mx256.json")
 KERNEL_NAMES = {   # as the profiler names them
-    "fused": "void hwr::k_mlp_bf16<256, false>(hwr::MlpArgs)",
-    "mlp": "void hwr::k_mlp_bf16<256, true>(hwr::MlpArgs)",
+    "fused": "void hwr::k_mlp_bf16<256, false, 2>(hwr::MlpArgs)",
+    "mlp": "void hwr::k_mlp_bf16<256, true, 2>(hwr::MlpArgs)",
     "quality": "hwr::k_quality_bf16(hwr::QualityArgs)",
     "gather": "hwr::k_gather(hwr::GatherArgs)",
-    "epilogue": "void hwr::k_epilogue<true>(hwr::EpilogueArgs)",
+    "epilogue": "void hwr::k_epilogue<true, false>(hwr::EpilogueArgs)",
 }
 
 
@@ -217,7 +217,9 @@ def single_query(args, S, hwr, torch, flags=0):
     outs = [np.zeros(1, np.int32), np.zeros(1, np.uint8)] + [np.zeros(1, np.float32) for _ in range(4)]
     b = hwr.hwr_query_batch(1, hwr.HWR_MEM_HOST, emb.ctypes.data, il.ctypes.data, no.ctypes.data,
                             slo.ctypes.data)
-    res = hwr.hwr_route_result(*[o.ctypes.data for o in outs], 0, 0, 0)
+    res = hwr.hwr_route_result(choice=outs[0].ctypes.data, feasible=outs[1].ctypes.data,
+                               utility=outs[2].ctypes.data, e2e_s=outs[3].ctypes.data,
+                               ttft_s=outs[4].ctypes.data, tpot_s=outs[5].ctypes.data)
     bref, rref = C.byref(b), C.byref(res)
     ctx = r.ctx
     route_ns = np.zeros(calls, np.int64)

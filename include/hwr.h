@@ -9,8 +9,9 @@
  *      and the pair's runtime signals S_i (Table 2 plus GPU utilisation)
  *      -- Sec. 3.2, Eq. 1;
  *   2. runs the cost predictor f_cost, a small MLP with two hidden ReLU layers,
- *      giving TTFT and TPOT, and the cost C = TTFT + N_out * TPOT
- *      -- Sec. 3.2, Eq. 1 and Eq. 2 (N_out is given per query);
+ *      giving TTFT and TPOT -- and, with three output heads, the number of
+ *      output tokens N_out -- and the cost C = TTFT + N_out * TPOT
+ *      -- Sec. 3.2, Eq. 1 and Eq. 2 (with two heads N_out is given per query);
  *   3. estimates the hardware-independent quality Q of the pair's model from
  *      the query embedding (a linear head per model) -- Sec. 3.2, item 3;
  *   4. scores u = Q - alpha * C / SLO (the Sec. 3.1 trade-off score with the
@@ -26,11 +27,15 @@
  * meets the bound, the largest u over all pairs (reported feasible = 0);
  * exact ties go to the lowest pair index.
  *
+ * Predictor outputs: z = W3^T h2 + b3; TTFT = softplus(z0), TPOT = softplus(z1)
+ * in seconds and, with three heads, N_out = softplus(z2) in tokens.
+ *
  * Precision: with HWR_BF16 the embeddings and all weight matrices are bf16
  * (raw uint16 bit patterns); features and hidden activations are rounded to
  * bf16 (nearest, ties to even) before each matrix product; products accumulate
  * in fp32; biases, predictions, costs and utilities are fp32.  With HWR_F32
- * everything is fp32.
+ * everything is fp32.  The decision arithmetic rounds each operation once:
+ * C = fma(TPOT, N_out, TTFT), t = C / SLO, u = Q - alpha * t.
  *
  * Conventions
  *  - Every call returns an hwr_status; nothing throws across this boundary.
@@ -101,6 +106,8 @@ typedef struct {
     float   default_slo_s;        /* bound when a batch gives no per-query SLO   */
     int32_t device;               /* HIP device ordinal                          */
     int32_t flags;                /* HWR_FLAG_*                                  */
+    int32_t n_heads;              /* predictor heads: 2 (or 0): N_out given per  */
+                                  /* query; 3: N_out predicted (Eq. 1)           */
     const int32_t *dep_model;     /* [N] model of pair i, in [0, M)              */
     const int32_t *dep_gpu;       /* [N] GPU type of pair i, in [0, G)           */
     const int32_t *model_arch;    /* [M] architecture id, in [0, A)              */
@@ -111,8 +118,9 @@ typedef struct {
     const float   *b1;            /* [H]                                         */
     const void    *w2;            /* [H][H] row-major, [in][out]                 */
     const float   *b2;            /* [H]                                         */
-    const void    *w3;            /* [H][2] row-major; column 0 TTFT, 1 TPOT     */
-    const float   *b3;            /* [2]                                         */
+    const void    *w3;            /* [H][n_heads] row-major; column 0 TTFT,      */
+                                  /* 1 TPOT, 2 N_out                             */
+    const float   *b3;            /* [n_heads]                                   */
     void          *stream;        /* hipStream_t the context works on, or NULL   */
 } hwr_config;                     /* all pointers are host memory                */
 
@@ -121,7 +129,8 @@ typedef struct {
     int32_t mem;                  /* hwr_mem of every pointer here and in the result */
     const void    *emb;           /* [n][D] in emb_dtype                         */
     const int32_t *input_len;     /* [n] prompt tokens, >= 1                     */
-    const int32_t *expected_out_len; /* [n] N_out of Eq. 2, >= 0                 */
+    const int32_t *expected_out_len; /* [n] N_out of Eq. 2, >= 0; ignored (may   */
+                                     /* be NULL) with n_heads == 3               */
     const float   *slo_s;         /* [n] latency bound in s, > 0; NULL -> default_slo_s */
 } hwr_query_batch;
 
@@ -132,8 +141,12 @@ typedef struct {                  /* caller-owned, in the batch's memory space  
     float   *e2e_s;               /* [n] C of the chosen pair                    */
     float   *ttft_s;              /* [n] TTFT of the chosen pair                 */
     float   *tpot_s;              /* [n] TPOT of the chosen pair                 */
+    float   *nout;                /* [n] N_out of the chosen pair (given or      */
+                                  /* predicted)                                  */
     float   *cand_ttft;           /* [n][N] every candidate's TTFT (debug)       */
     float   *cand_tpot;           /* [n][N] every candidate's TPOT (debug)       */
+    float   *cand_nout;           /* [n][N] every candidate's predicted N_out    */
+                                  /* (debug; n_heads == 3 only)                  */
     float   *cand_quality;        /* [n][M] every (query, model) quality (debug) */
 } hwr_route_result;               /* every pointer but choice may be NULL        */
 

@@ -15,10 +15,12 @@
  *    Each value is computed in fp64 and rounded to fp32 (then bf16).
  *  - Predictor (Eq. 1: two hidden ReLU layers): h1 = ReLU(W1^T x + b1),
  *    h2 = ReLU(W2^T h1 + b2), z = W3^T h2 + b3, TTFT = softplus(z0),
- *    TPOT = softplus(z1).  Each layer output is accumulated in fp64, rounded
- *    to fp32, and (bf16 workloads) h1, h2 are rounded to bf16.
- *  - Cost (Eq. 2) with the output length given per query:
- *    C = TTFT + N_out * TPOT, one fp32 rounding.
+ *    TPOT = softplus(z1), and with three heads N_out = softplus(z2), in
+ *    tokens.  Each layer output is accumulated in fp64, rounded to fp32, and
+ *    (bf16 workloads) h1, h2 are rounded to bf16.
+ *  - Cost (Eq. 2): C = TTFT + N_out * TPOT, one fp32 rounding, with N_out the
+ *    third head's prediction for the candidate, or (two heads) the output
+ *    length given per query.
  *  - Quality (Sec. 3.2 item 3, hardware-independent): Q = e . Wq[:, m] + bq[m].
  *  - Decision (Sec. 3.1 score, Eq. 3): utility u = Q - alpha * C / SLO in fp32
  *    (alpha = 0.5 is the paper's score with lambda = 1/3 and C normalised by
@@ -109,10 +111,11 @@ void orc_mlp(const orc_problem *p, const float *x, float *z) {
         float a = (float)(acc + (double)p->b2[j]);
         h2[j] = store(p, a > 0.0f ? a : 0.0f);
     }
-    for (int32_t k = 0; k < 2; ++k) {
+    const int32_t NH = p->n_heads == 3 ? 3 : 2;
+    for (int32_t k = 0; k < NH; ++k) {
         double acc = 0.0;
         for (int32_t i = 0; i < H; ++i)
-            acc += (double)p->w3[(size_t)i * 2 + k] * (double)h2[i];
+            acc += (double)p->w3[(size_t)i * NH + k] * (double)h2[i];
         z[k] = (float)(acc + (double)p->b3[k]);
     }
     free(h1);
@@ -133,32 +136,37 @@ static float utility(float q, float alpha, float c, float slo) {
 int orc_route(const orc_problem *p, const orc_state *s, const orc_queries *q,
               orc_result *r) {
     const int32_t N = p->N, M = p->M, F = p->F;
+    const int32_t NH = p->n_heads == 3 ? 3 : 2;
     if (N <= 0 || M <= 0 || F <= 0 || p->H <= 0 || q->n < 0) return -1;
+    if (p->n_heads != 0 && p->n_heads != 2 && p->n_heads != 3) return -1;
     if (p->arch_width + p->gpu_width + 8 > F) return -1;
     float *x = (float *)malloc(sizeof(float) * (size_t)F);
     float *qual = (float *)malloc(sizeof(float) * (size_t)M);
     for (int32_t iq = 0; iq < q->n; ++iq) {
         const float *e = q->emb + (size_t)iq * p->D;
         const float slo = q->slo_s[iq];
-        const float nout = (float)q->expected_out_len[iq];
+        const float nout_given = NH == 2 ? (float)q->expected_out_len[iq] : 0.0f;
         for (int32_t m = 0; m < M; ++m) {
             qual[m] = orc_quality(p, e, m);
             if (r->quality) r->quality[(size_t)iq * M + m] = qual[m];
         }
         int32_t best = -1;
         int best_f = 0;
-        float best_u = 0.0f, best_c = 0.0f, best_tt = 0.0f, best_tp = 0.0f;
+        float best_u = 0.0f, best_c = 0.0f, best_tt = 0.0f, best_tp = 0.0f, best_n = 0.0f;
         for (int32_t d = 0; d < N; ++d) {
-            float z[2];
+            float z[3];
             orc_features(p, s, d, q->input_len[iq], x);
             orc_mlp(p, x, z);
             const float ttft = orc_softplus(z[0]);
             const float tpot = orc_softplus(z[1]);
+            const float nout = NH == 3 ? orc_softplus(z[2]) : nout_given;
             const float c = fmaf(tpot, nout, ttft);
             const int feas = (c <= slo);
             const float u = utility(qual[p->dep_model[d]], p->alpha, c, slo);
             const size_t ci = (size_t)iq * N + d;
-            if (r->cand_z) { r->cand_z[2 * ci] = z[0]; r->cand_z[2 * ci + 1] = z[1]; }
+            if (r->cand_z)
+                for (int32_t k = 0; k < NH; ++k) r->cand_z[NH * ci + k] = z[k];
+            if (r->cand_nout) r->cand_nout[ci] = nout;
             if (r->cand_ttft) r->cand_ttft[ci] = ttft;
             if (r->cand_tpot) r->cand_tpot[ci] = tpot;
             if (r->cand_e2e) r->cand_e2e[ci] = c;
@@ -167,7 +175,7 @@ int orc_route(const orc_problem *p, const orc_state *s, const orc_queries *q,
             /* lexicographic (feasible, u), earlier pair wins exact ties */
             if (best < 0 || feas > best_f || (feas == best_f && u > best_u)) {
                 best = d; best_f = feas; best_u = u;
-                best_c = c; best_tt = ttft; best_tp = tpot;
+                best_c = c; best_tt = ttft; best_tp = tpot; best_n = nout;
             }
         }
         if (r->choice) r->choice[iq] = best;
@@ -176,6 +184,7 @@ int orc_route(const orc_problem *p, const orc_state *s, const orc_queries *q,
         if (r->e2e_s) r->e2e_s[iq] = best_c;
         if (r->ttft_s) r->ttft_s[iq] = best_tt;
         if (r->tpot_s) r->tpot_s[iq] = best_tp;
+        if (r->nout) r->nout[iq] = best_n;
     }
     free(x);
     free(qual);
@@ -183,18 +192,18 @@ int orc_route(const orc_problem *p, const orc_state *s, const orc_queries *q,
 }
 
 int orc_decide(int32_t n, int32_t N, int32_t M, const int32_t *dep_model,
-               const float *cand_ttft, const float *cand_tpot, const float *quality,
-               const int32_t *expected_out_len, const float *slo_s, float alpha,
+               const float *cand_ttft, const float *cand_tpot, const float *cand_nout,
+               const float *quality, const int32_t *expected_out_len, const float *slo_s, float alpha,
                int32_t *choice, uint8_t *feasible, float *utility_out, float *e2e_out) {
     if (n < 0 || N <= 0 || M <= 0) return -1;
     for (int32_t iq = 0; iq < n; ++iq) {
         const float slo = slo_s[iq];
-        const float nout = (float)expected_out_len[iq];
         int32_t best = -1;
         int best_f = 0;
         float best_u = 0.0f, best_c = 0.0f;
         for (int32_t d = 0; d < N; ++d) {
             const size_t ci = (size_t)iq * N + d;
+            const float nout = cand_nout ? cand_nout[ci] : (float)expected_out_len[iq];
             const float c = fmaf(cand_tpot[ci], nout, cand_ttft[ci]);
             const int feas = (c <= slo);
             const float u = utility(quality[(size_t)iq * M + dep_model[d]], alpha, c, slo);

@@ -27,6 +27,7 @@ typedef struct {
     int32_t M, G, N, D, F, H;          /* models, GPU types, pairs, embed, feat, hidden */
     int32_t arch_width, gpu_width;     /* one-hot widths                                 */
     int32_t bf16;                      /* 1: round x, h1, h2 to bf16 before next layer  */
+    int32_t n_heads;                   /* 2 (or 0): N_out given; 3: predicted (Eq. 1)    */
     float   alpha;                     /* u = Q - alpha * C / SLO                        */
     const int32_t *dep_model, *dep_gpu;     /* [N]                                   */
     const int32_t *model_arch;              /* [M]                                   */
@@ -34,7 +35,7 @@ typedef struct {
     const float   *wq, *bq;                 /* [D*M] row-major [D][M], [M]           */
     const float   *w1, *b1;                 /* [F*H] row-major [F][H], [H]           */
     const float   *w2, *b2;                 /* [H*H] row-major [H_in][H_out], [H]    */
-    const float   *w3, *b3;                 /* [H*2] row-major [H][2], [2]           */
+    const float   *w3, *b3;                 /* [H*NH] row-major [H][NH], [NH]        */
 } orc_problem;
 
 typedef struct {                            /* per pair, Table 2 + GPU utilisation  */
@@ -54,7 +55,9 @@ typedef struct {                            /* any pointer may be NULL (not writ
     int32_t *choice;                        /* [n]                                   */
     uint8_t *feasible;                      /* [n]                                   */
     float   *utility, *e2e_s, *ttft_s, *tpot_s;   /* [n], of the chosen pair         */
-    float   *cand_z;                        /* [n*N*2] predictor outputs before softplus */
+    float   *nout;                          /* [n] N_out used for the chosen pair    */
+    float   *cand_z;                        /* [n*N*NH] predictor outputs before softplus */
+    float   *cand_nout;                     /* [n*N] N_out used per candidate        */
     float   *cand_ttft, *cand_tpot, *cand_e2e, *cand_u;   /* [n*N]                   */
     uint8_t *cand_feasible;                 /* [n*N]                                 */
     float   *quality;                       /* [n*M]                                 */
@@ -70,16 +73,16 @@ void  orc_features(const orc_problem *p, const orc_state *s, int32_t d,
                    int32_t input_len, float *x);
 /* quality of model m for one embedding row. */
 float orc_quality(const orc_problem *p, const float *emb_row, int32_t m);
-/* predictor on one feature vector: z[2] before softplus. */
+/* predictor on one feature vector: z[NH] before softplus (NH = 2 or 3). */
 void  orc_mlp(const orc_problem *p, const float *x, float *z);
 /* Eq. 2 and Eq. 3 alone, on given predictions: for each of n queries, the
- * candidates' TTFT and TPOT ([n*N]) and the per-model quality ([n*M], mapped
- * to pairs through dep_model) -> the choice and its feasibility, utility and
- * cost, with the same arithmetic and tie rule as orc_route.  Returns 0, or -1
- * on bad sizes. */
+ * candidates' TTFT and TPOT ([n*N]), their N_out ([n*N]; NULL: the query's
+ * expected_out_len) and the per-model quality ([n*M], mapped to pairs through
+ * dep_model) -> the choice and its feasibility, utility and cost, with the
+ * same arithmetic and tie rule as orc_route.  Returns 0, or -1 on bad sizes. */
 int   orc_decide(int32_t n, int32_t N, int32_t M, const int32_t *dep_model,
-                 const float *cand_ttft, const float *cand_tpot, const float *quality,
-                 const int32_t *expected_out_len, const float *slo_s, float alpha,
+                 const float *cand_ttft, const float *cand_tpot, const float *cand_nout,
+                 const float *quality, const int32_t *expected_out_len, const float *slo_s, float alpha,
                  int32_t *choice, uint8_t *feasible, float *utility_out, float *e2e_out);
 /* the whole path over a batch of queries.  Returns 0, or -1 on bad sizes. */
 int   orc_route(const orc_problem *p, const orc_state *s, const orc_queries *q,

@@ -24,9 +24,19 @@ _SRC = os.path.join(_HERE, "hwr_oracle.c")
 CFLAGS = ["-O2", "-std=c11", "-fPIC", "-shared", "-ffp-contract=off", "-fno-fast-math"]
 
 
+def _stale() -> bool:
+    if not os.path.exists(LIB_PATH):
+        return True
+    if os.environ.get("ORACLE_LIB_OVERRIDE"):
+        return False
+    t = os.path.getmtime(LIB_PATH)
+    return any(os.path.getmtime(os.path.join(_HERE, f)) > t for f in ("hwr_oracle.c", "hwr_oracle.h"))
+
+
 def build(force: bool = True) -> str:
-    """Compile liboracle.so with gcc (plain C, contraction off)."""
-    if force or not os.path.exists(LIB_PATH):
+    """Compile liboracle.so with gcc (plain C, contraction off); without
+    ``force``, only when it is missing or older than its sources."""
+    if force or _stale():
         tmp = LIB_PATH + ".tmp"
         subprocess.check_call(["gcc", *CFLAGS, "-o", tmp, _SRC, "-lm"])
         os.replace(tmp, LIB_PATH)
@@ -41,7 +51,8 @@ _u8p = C.POINTER(C.c_uint8)
 class _Problem(C.Structure):
     _fields_ = [("M", C.c_int32), ("G", C.c_int32), ("N", C.c_int32), ("D", C.c_int32),
                 ("F", C.c_int32), ("H", C.c_int32), ("arch_width", C.c_int32),
-                ("gpu_width", C.c_int32), ("bf16", C.c_int32), ("alpha", C.c_float),
+                ("gpu_width", C.c_int32), ("bf16", C.c_int32), ("n_heads", C.c_int32),
+                ("alpha", C.c_float),
                 ("dep_model", _i32p), ("dep_gpu", _i32p), ("model_arch", _i32p),
                 ("model_params_b", _f32p), ("wq", _f32p), ("bq", _f32p),
                 ("w1", _f32p), ("b1", _f32p), ("w2", _f32p), ("b2", _f32p),
@@ -60,8 +71,8 @@ class _Queries(C.Structure):
 
 class _Result(C.Structure):
     _fields_ = [("choice", _i32p), ("feasible", _u8p), ("utility", _f32p),
-                ("e2e_s", _f32p), ("ttft_s", _f32p), ("tpot_s", _f32p),
-                ("cand_z", _f32p), ("cand_ttft", _f32p), ("cand_tpot", _f32p),
+                ("e2e_s", _f32p), ("ttft_s", _f32p), ("tpot_s", _f32p), ("nout", _f32p),
+                ("cand_z", _f32p), ("cand_nout", _f32p), ("cand_ttft", _f32p), ("cand_tpot", _f32p),
                 ("cand_e2e", _f32p), ("cand_u", _f32p), ("cand_feasible", _u8p),
                 ("quality", _f32p)]
 
@@ -72,7 +83,7 @@ _lib = None
 def lib():
     global _lib
     if _lib is None:
-        if not os.path.exists(LIB_PATH):
+        if _stale():
             build(force=False)
         L = C.CDLL(LIB_PATH)
         L.orc_bf16.restype = C.c_float
@@ -88,8 +99,8 @@ def lib():
         L.orc_mlp.restype = None
         L.orc_mlp.argtypes = [C.POINTER(_Problem), _f32p, _f32p]
         L.orc_decide.restype = C.c_int
-        L.orc_decide.argtypes = [C.c_int32, C.c_int32, C.c_int32, _i32p, _f32p, _f32p, _f32p, _i32p,
-                                 _f32p, C.c_float, _i32p, _u8p, _f32p, _f32p]
+        L.orc_decide.argtypes = [C.c_int32, C.c_int32, C.c_int32, _i32p, _f32p, _f32p, _f32p, _f32p,
+                                 _i32p, _f32p, C.c_float, _i32p, _u8p, _f32p, _f32p]
         L.orc_route.restype = C.c_int
         L.orc_route.argtypes = [C.POINTER(_Problem), C.POINTER(_State), C.POINTER(_Queries),
                                 C.POINTER(_Result)]
@@ -131,6 +142,7 @@ class OracleProblem:
     n_gpu_types: int
     bf16: bool
     alpha: float = 0.5
+    n_heads: int = 2
 
     @classmethod
     def from_synth(cls, pb, alpha: Optional[float] = None) -> "OracleProblem":
@@ -138,7 +150,7 @@ class OracleProblem:
         return cls(pb.dep_model, pb.dep_gpu, pb.model_arch, pb.model_params_b,
                    pb.wq, pb.bq, pb.w1, pb.b1, pb.w2, pb.b2, pb.w3, pb.b3,
                    sp.arch_width, sp.gpu_width, sp.n_gpu_types, sp.dtype == "bf16",
-                   sp.cost_weight if alpha is None else alpha)
+                   sp.cost_weight if alpha is None else alpha, sp.n_heads)
 
     def _struct(self, keep: list) -> _Problem:
         arrs = dict(dep_model=_i32(self.dep_model), dep_gpu=_i32(self.dep_gpu),
@@ -148,10 +160,11 @@ class OracleProblem:
         keep.append(arrs)
         D, M = arrs["wq"].shape
         F, H = arrs["w1"].shape
-        assert arrs["w2"].shape == (H, H) and arrs["w3"].shape == (H, 2)
+        NH = int(self.n_heads)
+        assert arrs["w2"].shape == (H, H) and arrs["w3"].shape == (H, NH) and arrs["b3"].shape == (NH,)
         N = arrs["dep_model"].shape[0]
         s = _Problem(M, int(self.n_gpu_types), N, D, F, H, int(self.arch_width),
-                     int(self.gpu_width), int(bool(self.bf16)), float(self.alpha))
+                     int(self.gpu_width), int(bool(self.bf16)), NH, float(self.alpha))
         for k in ("dep_model", "dep_gpu", "model_arch"):
             setattr(s, k, _ptr(arrs[k], C.c_int32))
         for k in ("model_params_b", "wq", "bq", "w1", "b1", "w2", "b2", "w3", "b3"):
@@ -207,7 +220,7 @@ def mlp(prob: OracleProblem, x: np.ndarray) -> np.ndarray:
     keep: list = []
     p = prob._struct(keep)
     xx = _f32(x)
-    z = np.zeros(2, np.float32)
+    z = np.zeros(int(prob.n_heads), np.float32)
     lib().orc_mlp(C.byref(p), _ptr(xx, C.c_float), _ptr(z, C.c_float))
     return z
 
@@ -220,7 +233,9 @@ class OracleResult:
     e2e_s: np.ndarray
     ttft_s: np.ndarray
     tpot_s: np.ndarray
-    cand_z: Optional[np.ndarray] = None      # [n, N, 2]
+    nout: Optional[np.ndarray] = None        # [n] N_out used for the chosen pair
+    cand_z: Optional[np.ndarray] = None      # [n, N, n_heads]
+    cand_nout: Optional[np.ndarray] = None   # [n, N] N_out used per candidate
     cand_ttft: Optional[np.ndarray] = None   # [n, N]
     cand_tpot: Optional[np.ndarray] = None
     cand_e2e: Optional[np.ndarray] = None
@@ -247,18 +262,19 @@ def route(prob: OracleProblem, state: np.ndarray, emb: np.ndarray, input_len, ex
                  _ptr(slo, C.c_float))
     out = OracleResult(np.zeros(n, np.int32), np.zeros(n, np.uint8), np.zeros(n, np.float32),
                        np.zeros(n, np.float32), np.zeros(n, np.float32), np.zeros(n, np.float32))
+    out.nout = np.zeros(n, np.float32)
     r = _Result()
     r.choice = _ptr(out.choice, C.c_int32)
     r.feasible = _ptr(out.feasible, C.c_uint8)
-    for k in ("utility", "e2e_s", "ttft_s", "tpot_s"):
+    for k in ("utility", "e2e_s", "ttft_s", "tpot_s", "nout"):
         setattr(r, k, _ptr(getattr(out, k), C.c_float))
     if candidates:
-        out.cand_z = np.zeros((n, N, 2), np.float32)
-        for k in ("cand_ttft", "cand_tpot", "cand_e2e", "cand_u"):
+        out.cand_z = np.zeros((n, N, int(prob.n_heads)), np.float32)
+        for k in ("cand_nout", "cand_ttft", "cand_tpot", "cand_e2e", "cand_u"):
             setattr(out, k, np.zeros((n, N), np.float32))
         out.cand_feasible = np.zeros((n, N), np.uint8)
         out.quality = np.zeros((n, M), np.float32)
-        for k in ("cand_z", "cand_ttft", "cand_tpot", "cand_e2e", "cand_u", "quality"):
+        for k in ("cand_z", "cand_nout", "cand_ttft", "cand_tpot", "cand_e2e", "cand_u", "quality"):
             setattr(r, k, _ptr(getattr(out, k), C.c_float))
         r.cand_feasible = _ptr(out.cand_feasible, C.c_uint8)
     rc = lib().orc_route(C.byref(p), C.byref(s), C.byref(q), C.byref(r))
@@ -267,20 +283,23 @@ def route(prob: OracleProblem, state: np.ndarray, emb: np.ndarray, input_len, ex
     return out
 
 
-def decide(dep_model, cand_ttft, cand_tpot, quality, expected_out_len, slo_s, alpha: float) -> dict:
+def decide(dep_model, cand_ttft, cand_tpot, quality, expected_out_len, slo_s, alpha: float,
+           cand_nout=None) -> dict:
     """Eq. 2 and Eq. 3 on given predictions (the decision step alone, same
     arithmetic and tie rule as ``route``): per query the choice, feasibility,
-    utility and cost.  Inputs: TTFT / TPOT [n, N], quality [n, M]."""
+    utility and cost.  Inputs: TTFT / TPOT [n, N], quality [n, M]; N_out per
+    candidate [n, N] (three heads) or None (the queries' expected_out_len)."""
     tt, tp, qual = _f32(cand_ttft), _f32(cand_tpot), _f32(quality)
+    cn = None if cand_nout is None else _f32(cand_nout)
     n, N = tt.shape
     M = qual.shape[1]
     dm, no, slo = _i32(dep_model), _i32(expected_out_len), _f32(slo_s)
     assert tp.shape == (n, N) and qual.shape[0] == n and dm.shape == (N,)
-    assert no.shape == (n,) and slo.shape == (n,)
+    assert no.shape == (n,) and slo.shape == (n,) and (cn is None or cn.shape == (n, N))
     out = {"choice": np.zeros(n, np.int32), "feasible": np.zeros(n, np.uint8),
            "utility": np.zeros(n, np.float32), "e2e_s": np.zeros(n, np.float32)}
     rc = lib().orc_decide(n, N, M, _ptr(dm, C.c_int32), _ptr(tt, C.c_float), _ptr(tp, C.c_float),
-                          _ptr(qual, C.c_float), _ptr(no, C.c_int32), _ptr(slo, C.c_float),
+                          _ptr(cn, C.c_float), _ptr(qual, C.c_float), _ptr(no, C.c_int32), _ptr(slo, C.c_float),
                           float(alpha), _ptr(out["choice"], C.c_int32), _ptr(out["feasible"], C.c_uint8),
                           _ptr(out["utility"], C.c_float), _ptr(out["e2e_s"], C.c_float))
     if rc != 0:

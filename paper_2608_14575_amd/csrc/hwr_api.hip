@@ -35,7 +35,8 @@ struct hwr_ctx {
     hipStream_t stream = nullptr;
     int M = 0, G = 0, N = 0, A = 0, Gw = 0, D = 0, F = 0, H = 0, len_slot = 0;
     int bf16 = 0, pipeline = 0, max_chunk = 0, flags = 0, cus = 0;
-    float alpha = 0.5f, default_slo = 1.0f, b3[2] = {0, 0};
+    int NH = 2;                   // predictor heads (3: N_out predicted)
+    float alpha = 0.5f, default_slo = 1.0f, b3[kMaxHeads] = {0, 0, 0};
     // per-pair tables and state
     int32_t *d_dep_model = nullptr, *d_dep_gpu = nullptr, *d_model_arch = nullptr;
     float *d_params = nullptr;
@@ -61,7 +62,7 @@ struct hwr_ctx {
     float *d_wq = nullptr, *d_w1 = nullptr, *d_w2 = nullptr, *d_w3 = nullptr, *d_b1 = nullptr,
           *d_b2 = nullptr;
     // work space
-    float *d_qmat = nullptr, *d_ctt = nullptr, *d_ctp = nullptr;
+    float *d_qmat = nullptr, *d_ctt = nullptr, *d_ctp = nullptr, *d_cno = nullptr;
     uint16_t *d_X = nullptr;
     uint64_t *d_pkey = nullptr;
     float *d_pval = nullptr;
@@ -148,7 +149,8 @@ std::vector<uint16_t> pack_quality(const uint16_t *wq, int D, int M) {
 // (W2^T, tile mo, k-block kb = 2 t + b): the k order follows the layer-1
 // accumulator: element j of lane half h multiplies hidden unit
 // 32 t + crow(8 b + j, h).  Bias tiles hold b[32 mt + crow(r, h)] for
-// r = 0..15; head pairs hold (W3[row(2p)][o], W3[row(2p+1)][o]) as bf16x2.
+// r = 0..15; head pairs hold (W3[row(2p)][o], W3[row(2p+1)][o]) as bf16x2,
+// [tile][half][head o][8 pairs].  W3 is [H][NH] (NH = 2 or 3 heads).
 struct PackedPredictor {
     std::vector<uint16_t> w1, w2, w3frag;
     std::vector<float> b1, b2;
@@ -156,25 +158,26 @@ struct PackedPredictor {
 };
 
 PackedPredictor pack_predictor(const uint16_t *w1, const uint16_t *w2, const uint16_t *w3,
-                               const float *b1, const float *b2, int F, int H) {
+                               const float *b1, const float *b2, int F, int H, int NH) {
     const int MT = H / 32, KB2 = H / 16;
     PackedPredictor p;
     p.w1.assign(static_cast<size_t>(MT) * 2 * 64 * 8, 0);
     p.w2.assign(static_cast<size_t>(MT) * KB2 * 64 * 8, 0);
     p.b1.assign(static_cast<size_t>(MT) * 2 * 16, 0.0f);
     p.b2.assign(static_cast<size_t>(MT) * 2 * 16, 0.0f);
-    p.w3.assign(static_cast<size_t>(MT) * 2 * 16, 0u);
-    // Head layer on MFMA (z^T = W3^T h2^T): A operand rows are the two heads,
+    p.w3.assign(static_cast<size_t>(MT) * 2 * NH * 8, 0u);
+    // Head layer on MFMA (z^T = W3^T h2^T): A operand rows are the NH heads,
     // k follows the layer-2 accumulator order like W2's.  Only lanes of rows
-    // 0 and 1 hold data: [k-block][row m < 2][half h][8], then one zero
+    // 0..NH-1 hold data: [k-block][row m < NH][half h][8], then one zero
     // fragment that every other lane reads.
-    p.w3frag.assign(static_cast<size_t>(KB2) * 4 * 8 + 8, 0);
+    p.w3frag.assign(static_cast<size_t>(KB2) * NH * 2 * 8 + 8, 0);
     for (int kb = 0; kb < KB2; ++kb)
-        for (int m = 0; m < 2; ++m)
+        for (int m = 0; m < NH; ++m)
             for (int h = 0; h < 2; ++h)
                 for (int j = 0; j < 8; ++j) {
                     const int hin = 32 * (kb >> 1) + crow(8 * (kb & 1) + j, h);
-                    p.w3frag[((static_cast<size_t>(kb) * 2 + m) * 2 + h) * 8 + j] = w3[static_cast<size_t>(hin) * 2 + m];
+                    p.w3frag[((static_cast<size_t>(kb) * NH + m) * 2 + h) * 8 + j] =
+                        w3[static_cast<size_t>(hin) * NH + m];
                 }
     for (int mt = 0; mt < MT; ++mt)
         for (int lane = 0; lane < 64; ++lane) {
@@ -198,11 +201,11 @@ PackedPredictor pack_predictor(const uint16_t *w1, const uint16_t *w2, const uin
                 p.b1[(mt * 2 + h) * 16 + r] = b1[32 * mt + crow(r, h)];
                 p.b2[(mt * 2 + h) * 16 + r] = b2[32 * mt + crow(r, h)];
             }
-            for (int o = 0; o < 2; ++o)
+            for (int o = 0; o < NH; ++o)
                 for (int pp = 0; pp < 8; ++pp) {
-                    const uint32_t lo = w3[static_cast<size_t>(32 * mt + crow(2 * pp, h)) * 2 + o];
-                    const uint32_t hi = w3[static_cast<size_t>(32 * mt + crow(2 * pp + 1, h)) * 2 + o];
-                    p.w3[(mt * 2 + h) * 16 + o * 8 + pp] = lo | (hi << 16);
+                    const uint32_t lo = w3[static_cast<size_t>(32 * mt + crow(2 * pp, h)) * NH + o];
+                    const uint32_t hi = w3[static_cast<size_t>(32 * mt + crow(2 * pp + 1, h)) * NH + o];
+                    p.w3[((mt * 2 + h) * NH + o) * 8 + pp] = lo | (hi << 16);
                 }
         }
     return p;
@@ -278,6 +281,7 @@ hwr_status check_config(const hwr_config *cfg) {
     if (cfg->max_chunk < 0 || cfg->max_chunk > (1 << 22)) return bad("max_chunk must be in [0, 2^22]");
     if (!finite(cfg->cost_weight) || cfg->cost_weight < 0.0f) return bad("cost_weight must be finite and >= 0");
     if (!finite(cfg->default_slo_s) || cfg->default_slo_s <= 0.0f) return bad("default_slo_s must be finite and > 0");
+    if (cfg->n_heads != 0 && cfg->n_heads != 2 && cfg->n_heads != 3) return bad("n_heads must be 2 or 3 (0 means 2)");
     if (!cfg->dep_model || !cfg->dep_gpu || !cfg->model_arch || !cfg->model_params_b || !cfg->wq ||
         !cfg->bq || !cfg->w1 || !cfg->b1 || !cfg->w2 || !cfg->b2 || !cfg->w3 || !cfg->b3)
         return bad("a table or weight pointer is NULL");
@@ -292,7 +296,8 @@ hwr_status check_config(const hwr_config *cfg) {
     }
     for (int j = 0; j < cfg->hidden; ++j)
         if (!finite(cfg->b1[j]) || !finite(cfg->b2[j])) return bad("b1/b2 not finite");
-    if (!finite(cfg->b3[0]) || !finite(cfg->b3[1])) return bad("b3 not finite");
+    for (int k = 0; k < (cfg->n_heads == 3 ? 3 : 2); ++k)
+        if (!finite(cfg->b3[k])) return bad("b3 not finite");
     return HWR_OK;
 }
 
@@ -314,7 +319,7 @@ void release(hwr_ctx *c) {
                         c->d_pair_params, c->d_dep_f32,
                         c->d_dep_bf16, c->d_bq, c->d_wq_pk, c->d_wqT, c->d_w1_pk, c->d_w2_pk,
                         c->d_b1_pk, c->d_b2_pk, c->d_w3_pk, c->d_w3_frag, c->d_wq, c->d_w1, c->d_w2, c->d_w3,
-                        c->d_b1, c->d_b2, c->d_qmat, c->d_ctt, c->d_ctp, c->d_X, c->d_pkey,
+                        c->d_b1, c->d_b2, c->d_qmat, c->d_ctt, c->d_ctp, c->d_cno, c->d_X, c->d_pkey,
                         c->d_pval, c->d_hemb, c->d_hlen, c->d_hnout, c->d_hchoice, c->d_hslo,
                         c->d_hval, c->d_hcand, c->d_hqual, c->d_hfeas};
     for (void *p : dev_ptrs)
@@ -358,8 +363,8 @@ hwr_status init_impl(const hwr_config *cfg, hwr_ctx **out) {
     c->flags = cfg->flags;
     c->alpha = cfg->cost_weight;
     c->default_slo = cfg->default_slo_s;
-    c->b3[0] = cfg->b3[0];
-    c->b3[1] = cfg->b3[1];
+    c->NH = cfg->n_heads == 3 ? 3 : 2;
+    for (int k = 0; k < c->NH; ++k) c->b3[k] = cfg->b3[k];
     c->cus = prop.multiProcessorCount;
 
     auto bail = [&](hipError_t err, const char *what) {
@@ -402,7 +407,8 @@ hwr_status init_impl(const hwr_config *cfg, hwr_ctx **out) {
         INIT_HIP(upload(&c->d_wqT, wqT.data(), wqT.size()));
         PackedPredictor p = pack_predictor(static_cast<const uint16_t *>(cfg->w1),
                                            static_cast<const uint16_t *>(cfg->w2),
-                                           static_cast<const uint16_t *>(cfg->w3), cfg->b1, cfg->b2, F, H);
+                                           static_cast<const uint16_t *>(cfg->w3), cfg->b1, cfg->b2, F, H,
+                                           c->NH);
         INIT_HIP(upload(&c->d_w1_pk, p.w1.data(), p.w1.size()));
         INIT_HIP(upload(&c->d_w2_pk, p.w2.data(), p.w2.size()));
         INIT_HIP(upload(&c->d_b1_pk, p.b1.data(), p.b1.size()));
@@ -413,7 +419,7 @@ hwr_status init_impl(const hwr_config *cfg, hwr_ctx **out) {
         INIT_HIP(upload(&c->d_wq, static_cast<const float *>(cfg->wq), static_cast<size_t>(D) * M));
         INIT_HIP(upload(&c->d_w1, static_cast<const float *>(cfg->w1), static_cast<size_t>(F) * H));
         INIT_HIP(upload(&c->d_w2, static_cast<const float *>(cfg->w2), static_cast<size_t>(H) * H));
-        INIT_HIP(upload(&c->d_w3, static_cast<const float *>(cfg->w3), static_cast<size_t>(H) * 2));
+        INIT_HIP(upload(&c->d_w3, static_cast<const float *>(cfg->w3), static_cast<size_t>(H) * c->NH));
         INIT_HIP(upload(&c->d_b1, cfg->b1, H));
         INIT_HIP(upload(&c->d_b2, cfg->b2, H));
     }
@@ -422,12 +428,13 @@ hwr_status init_impl(const hwr_config *cfg, hwr_ctx **out) {
     if (!c->bf16 || c->pipeline == HWR_PIPE_STAGED) {
         INIT_HIP(dev_alloc(&c->d_ctt, chunk * N));
         INIT_HIP(dev_alloc(&c->d_ctp, chunk * N));
+        if (c->NH == 3) INIT_HIP(dev_alloc(&c->d_cno, chunk * N));
     }
     if (c->bf16 && c->pipeline == HWR_PIPE_STAGED) INIT_HIP(dev_alloc(&c->d_X, chunk * N * kFeatPad));
     if (c->bf16 && c->pipeline == HWR_PIPE_FUSED) {
         c->part_cap = static_cast<size_t>(2 * c->cus) * kQPerBlock;
         INIT_HIP(dev_alloc(&c->d_pkey, c->part_cap));
-        INIT_HIP(dev_alloc(&c->d_pval, c->part_cap * 4));
+        INIT_HIP(dev_alloc(&c->d_pval, c->part_cap * kPartVals));
     }
     INIT_HIP(hipHostMalloc(reinterpret_cast<void **>(&c->h_ring),
                            sizeof(hwr_hw_state) * N * kStateSlots, hipHostMallocMapped));
@@ -459,7 +466,7 @@ struct DevBatch {
     const int32_t *len, *nout;
     const float *slo;
     OutArgs out;
-    float *cand_ttft, *cand_tpot, *cand_quality;
+    float *cand_ttft, *cand_tpot, *cand_nout, *cand_quality;
 };
 
 // Turn the newest state snapshot into the device pair rows, once, ordered on
@@ -489,7 +496,7 @@ hwr_status route_device(hwr_ctx *c, const DevBatch &b) {
         QueryArgs qa;
         qa.nq = cn;
         qa.input_len = b.len + off;
-        qa.nout = b.nout + off;
+        qa.nout = c->NH == 3 ? nullptr : b.nout + off;   // three heads predict N_out
         qa.slo = b.slo ? b.slo + off : nullptr;
         qa.default_slo = c->default_slo;
         OutArgs oa = b.out;
@@ -499,9 +506,11 @@ hwr_status route_device(hwr_ctx *c, const DevBatch &b) {
         if (oa.e2e) oa.e2e += off;
         if (oa.ttft) oa.ttft += off;
         if (oa.tpot) oa.tpot += off;
+        if (oa.nout) oa.nout += off;
         float *qmat = b.cand_quality ? b.cand_quality + static_cast<size_t>(off) * M : c->d_qmat;
         float *ctt = b.cand_ttft ? b.cand_ttft + static_cast<size_t>(off) * N : nullptr;
         float *ctp = b.cand_tpot ? b.cand_tpot + static_cast<size_t>(off) * N : nullptr;
+        float *cno = (c->NH == 3 && b.cand_nout) ? b.cand_nout + static_cast<size_t>(off) * N : nullptr;
 
         QualityArgs qu;
         qu.nq = cn;
@@ -524,6 +533,8 @@ hwr_status route_device(hwr_ctx *c, const DevBatch &b) {
             ma.alpha = c->alpha;
             ma.b3_0 = c->b3[0];
             ma.b3_1 = c->b3[1];
+            ma.b3_2 = c->b3[2];
+            ma.nheads = c->NH;
             ma.q = qa;
             ma.dep_bf16 = c->d_dep_bf16;
             ma.dep_model = c->d_dep_model;
@@ -538,6 +549,7 @@ hwr_status route_device(hwr_ctx *c, const DevBatch &b) {
             if (c->pipeline == HWR_PIPE_FUSED) {
                 ma.cand_ttft = ctt;
                 ma.cand_tpot = ctp;
+                ma.cand_nout = cno;
                 const int blocks = (cn + kQPerBlock - 1) / kQPerBlock;
                 int nsplit = 1;
                 if (blocks < c->cus) nsplit = std::min(N, (c->cus + blocks - 1) / blocks);
@@ -557,6 +569,7 @@ hwr_status route_device(hwr_ctx *c, const DevBatch &b) {
             ma.X = c->d_X;
             ma.cand_ttft = ctt ? ctt : c->d_ctt;
             ma.cand_tpot = ctp ? ctp : c->d_ctp;
+            ma.cand_nout = cno ? cno : c->d_cno;
             HWR_HIP(c, timed(c, HWR_K_MLP, [&] { return launch_mlp_bf16(c->H, true, ma, c->stream); }));
         } else {
             MlpF32Args fa{};
@@ -565,6 +578,8 @@ hwr_status route_device(hwr_ctx *c, const DevBatch &b) {
             fa.len_slot = c->len_slot;
             fa.b3_0 = c->b3[0];
             fa.b3_1 = c->b3[1];
+            fa.b3_2 = c->b3[2];
+            fa.nheads = c->NH;
             fa.q = qa;
             fa.dep_f32 = c->d_dep_f32;
             fa.w1 = c->d_w1;
@@ -574,6 +589,7 @@ hwr_status route_device(hwr_ctx *c, const DevBatch &b) {
             fa.w3 = c->d_w3;
             fa.cand_ttft = ctt ? ctt : c->d_ctt;
             fa.cand_tpot = ctp ? ctp : c->d_ctp;
+            fa.cand_nout = cno ? cno : c->d_cno;
             HWR_HIP(c, timed(c, HWR_K_MLP, [&] { return launch_mlp_f32(c->H, fa, c->stream); }));
         }
         EpilogueArgs ea{};
@@ -585,8 +601,10 @@ hwr_status route_device(hwr_ctx *c, const DevBatch &b) {
         ea.qmat = qmat;
         ea.cand_ttft = ctt ? ctt : c->d_ctt;
         ea.cand_tpot = ctp ? ctp : c->d_ctp;
+        ea.cand_nout = c->NH == 3 ? (cno ? cno : c->d_cno) : nullptr;
         ea.vec4 = N % 4 == 0 && reinterpret_cast<uintptr_t>(ea.cand_ttft) % 16 == 0 &&
-                  reinterpret_cast<uintptr_t>(ea.cand_tpot) % 16 == 0;
+                  reinterpret_cast<uintptr_t>(ea.cand_tpot) % 16 == 0 &&
+                  reinterpret_cast<uintptr_t>(ea.cand_nout) % 16 == 0;
         // lanes per query: a power of two from 8 (which bounds the LDS rows of
         // the quality matrix a workgroup stages) up to 64, with up to four
         // slices of the row per lane
@@ -614,8 +632,8 @@ hwr_status ensure_host_staging(hwr_ctx *c, size_t rows) {
     HWR_HIP(c, dev_alloc(&c->d_hnout, rows));
     HWR_HIP(c, dev_alloc(&c->d_hchoice, rows));
     HWR_HIP(c, dev_alloc(&c->d_hslo, rows));
-    HWR_HIP(c, dev_alloc(&c->d_hval, rows * 4));
-    HWR_HIP(c, dev_alloc(&c->d_hcand, rows * c->N * 2));
+    HWR_HIP(c, dev_alloc(&c->d_hval, rows * 5));
+    HWR_HIP(c, dev_alloc(&c->d_hcand, rows * c->N * 3));
     HWR_HIP(c, dev_alloc(&c->d_hqual, rows * c->M));
     HWR_HIP(c, dev_alloc(&c->d_hfeas, rows));
     c->hs_cap = rows;
@@ -634,7 +652,8 @@ hwr_status route_host(hwr_ctx *c, const hwr_query_batch *q, hwr_route_result *r)
         HWR_HIP(c, hipMemcpyAsync(c->d_hemb, static_cast<const char *>(q->emb) + static_cast<size_t>(off) * D * esz,
                                   static_cast<size_t>(cn) * D * esz, hipMemcpyHostToDevice, s));
         HWR_HIP(c, hipMemcpyAsync(c->d_hlen, q->input_len + off, cn * 4, hipMemcpyHostToDevice, s));
-        HWR_HIP(c, hipMemcpyAsync(c->d_hnout, q->expected_out_len + off, cn * 4, hipMemcpyHostToDevice, s));
+        if (c->NH == 2)
+            HWR_HIP(c, hipMemcpyAsync(c->d_hnout, q->expected_out_len + off, cn * 4, hipMemcpyHostToDevice, s));
         if (q->slo_s) HWR_HIP(c, hipMemcpyAsync(c->d_hslo, q->slo_s + off, cn * 4, hipMemcpyHostToDevice, s));
         DevBatch b{};
         b.n = cn;
@@ -643,9 +662,10 @@ hwr_status route_host(hwr_ctx *c, const hwr_query_batch *q, hwr_route_result *r)
         b.nout = c->d_hnout;
         b.slo = q->slo_s ? c->d_hslo : nullptr;
         float *v = c->d_hval;
-        b.out = OutArgs{c->d_hchoice, c->d_hfeas, v, v + rows, v + 2 * rows, v + 3 * rows};
+        b.out = OutArgs{c->d_hchoice, c->d_hfeas, v, v + rows, v + 2 * rows, v + 3 * rows, v + 4 * rows};
         b.cand_ttft = r->cand_ttft ? c->d_hcand : nullptr;
         b.cand_tpot = r->cand_tpot ? c->d_hcand + rows * N : nullptr;
+        b.cand_nout = r->cand_nout ? c->d_hcand + 2 * rows * N : nullptr;
         b.cand_quality = r->cand_quality ? c->d_hqual : nullptr;
         hwr_status rs = route_device(c, b);
         if (rs != HWR_OK) return rs;
@@ -658,8 +678,11 @@ hwr_status route_host(hwr_ctx *c, const hwr_query_batch *q, hwr_route_result *r)
         if (r->e2e_s) HWR_HIP(c, d2h(r->e2e_s + off, v + rows, cn * 4));
         if (r->ttft_s) HWR_HIP(c, d2h(r->ttft_s + off, v + 2 * rows, cn * 4));
         if (r->tpot_s) HWR_HIP(c, d2h(r->tpot_s + off, v + 3 * rows, cn * 4));
+        if (r->nout) HWR_HIP(c, d2h(r->nout + off, v + 4 * rows, cn * 4));
         if (r->cand_ttft) HWR_HIP(c, d2h(r->cand_ttft + static_cast<size_t>(off) * N, c->d_hcand, static_cast<size_t>(cn) * N * 4));
         if (r->cand_tpot) HWR_HIP(c, d2h(r->cand_tpot + static_cast<size_t>(off) * N, c->d_hcand + rows * N, static_cast<size_t>(cn) * N * 4));
+        if (r->cand_nout && c->NH == 3)
+            HWR_HIP(c, d2h(r->cand_nout + static_cast<size_t>(off) * N, c->d_hcand + 2 * rows * N, static_cast<size_t>(cn) * N * 4));
         if (r->cand_quality) HWR_HIP(c, d2h(r->cand_quality + static_cast<size_t>(off) * M, c->d_hqual, static_cast<size_t>(cn) * M * 4));
         HWR_HIP(c, hipStreamSynchronize(s));   // staging is reused by the next chunk
     }
@@ -676,6 +699,8 @@ SingleArgs single_args(const hwr_ctx *c) {
     a.alpha = c->alpha;
     a.b3_0 = c->b3[0];
     a.b3_1 = c->b3[1];
+    a.b3_2 = c->b3[2];
+    a.nheads = c->NH;
     a.arch_width = c->A;
     a.gpu_width = c->Gw;
     a.in = c->d_sin;
@@ -723,7 +748,7 @@ hwr_status route_single(hwr_ctx *c, const hwr_query_batch *q, hwr_route_result *
     SingleIn *in = c->h_sin;
     const uint32_t seq = ++c->seq == 0 ? ++c->seq : c->seq;
     in->input_len = q->input_len[0];
-    in->nout = q->expected_out_len[0];
+    in->nout = c->NH == 2 ? q->expected_out_len[0] : 0;
     in->slo = q->slo_s ? q->slo_s[0] : c->default_slo;
     std::memcpy(in + 1, q->emb, static_cast<size_t>(c->D) * 2);
     in->seq = seq;
@@ -756,6 +781,7 @@ hwr_status route_single(hwr_ctx *c, const hwr_query_batch *q, hwr_route_result *
     if (r->e2e_s) r->e2e_s[0] = o->e2e;
     if (r->ttft_s) r->ttft_s[0] = o->ttft;
     if (r->tpot_s) r->tpot_s[0] = o->tpot;
+    if (r->nout) r->nout[0] = o->nout;
     return HWR_OK;
 }
 
@@ -810,8 +836,8 @@ hwr_status hwr_route_batch(hwr_ctx *c, const hwr_query_batch *q, hwr_route_resul
     if (q->n < 0) return fail(c, HWR_ERR_INVALID_ARG, "n < 0");
     if (q->mem != HWR_MEM_DEVICE && q->mem != HWR_MEM_HOST) return fail(c, HWR_ERR_INVALID_ARG, "unknown mem");
     if (q->n == 0) return HWR_OK;
-    if (!q->emb || !q->input_len || !q->expected_out_len || !r->choice)
-        return fail(c, HWR_ERR_INVALID_ARG, "emb, input_len, expected_out_len and choice are required");
+    if (!q->emb || !q->input_len || !r->choice || (c->NH == 2 && !q->expected_out_len))
+        return fail(c, HWR_ERR_INVALID_ARG, "emb, input_len, choice and (two heads) expected_out_len are required");
     if (!c->has_state) return fail(c, HWR_ERR_STATE, "no hardware state yet: call hwr_update_hw_state first");
     HWR_HIP(c, hipSetDevice(c->dev));
     if (q->mem == HWR_MEM_DEVICE) {
@@ -821,19 +847,20 @@ hwr_status hwr_route_batch(hwr_ctx *c, const hwr_query_batch *q, hwr_route_resul
         b.len = q->input_len;
         b.nout = q->expected_out_len;
         b.slo = q->slo_s;
-        b.out = OutArgs{r->choice, r->feasible, r->utility, r->e2e_s, r->ttft_s, r->tpot_s};
+        b.out = OutArgs{r->choice, r->feasible, r->utility, r->e2e_s, r->ttft_s, r->tpot_s, r->nout};
         b.cand_ttft = r->cand_ttft;
         b.cand_tpot = r->cand_tpot;
+        b.cand_nout = r->cand_nout;
         b.cand_quality = r->cand_quality;
         return route_device(c, b);
     }
     for (int i = 0; i < q->n; ++i) {
         if (q->input_len[i] < 1) return fail(c, HWR_ERR_INVALID_ARG, "input_len < 1");
-        if (q->expected_out_len[i] < 0) return fail(c, HWR_ERR_INVALID_ARG, "expected_out_len < 0");
+        if (c->NH == 2 && q->expected_out_len[i] < 0) return fail(c, HWR_ERR_INVALID_ARG, "expected_out_len < 0");
         if (q->slo_s && (!finite(q->slo_s[i]) || q->slo_s[i] <= 0.0f))
             return fail(c, HWR_ERR_INVALID_ARG, "slo_s must be finite and > 0");
     }
-    if (q->n == 1 && c->bf16 && !r->cand_ttft && !r->cand_tpot && !r->cand_quality)
+    if (q->n == 1 && c->bf16 && !r->cand_ttft && !r->cand_tpot && !r->cand_nout && !r->cand_quality)
         return route_single(c, q, r);
     return route_host(c, q, r);
 }

@@ -133,19 +133,22 @@ __device__ inline Decision decide(float ttft, float tpot, float nout, const Boun
 // decision_key (the stored utility takes the same canonical value); the key
 // is built once, for the reduction across lanes.
 struct Best {
-    float u, e2e, tt, tp;
+    float u, e2e, tt, tp, n;      // n: the candidate's N_out
     int d;                        // -1: no candidate yet
     bool f;
 };
 __device__ inline Best best_none() {
     Best b;
     b.u = -__builtin_huge_valf();
-    b.e2e = b.tt = b.tp = 0.0f;
+    b.e2e = b.tt = b.tp = b.n = 0.0f;
     b.d = -1;
     b.f = false;
     return b;
 }
-__device__ inline void offer(Best &b, const Decision &r, int d, float tt, float tp) {
+// TrackN: keep the candidate's N_out (it varies per candidate only when a
+// third head predicts it; otherwise the caller knows it).
+template <bool TrackN = true>
+__device__ inline void offer(Best &b, const Decision &r, int d, float tt, float tp, float n) {
     const float u = fmaxf(r.u, -__builtin_huge_valf()) + 0.0f;   // NaN -> -inf, -0 -> +0
     const bool better = b.d < 0 || (r.feasible && !b.f) || (r.feasible == b.f && u > b.u);
     // selects, not a branch: one v_cndmask per field
@@ -153,6 +156,7 @@ __device__ inline void offer(Best &b, const Decision &r, int d, float tt, float 
     b.e2e = better ? r.e2e : b.e2e;
     b.tt = better ? tt : b.tt;
     b.tp = better ? tp : b.tp;
+    if constexpr (TrackN) b.n = better ? n : b.n;
     b.d = better ? d : b.d;
     b.f = better ? r.feasible : b.f;
 }
@@ -205,13 +209,14 @@ __device__ inline uint64_t group_max_u64(uint64_t k, int G) {
 }
 
 __device__ inline void write_outputs(const OutArgs &o, int q, uint64_t key, float u,
-                                     float e2e, float ttft, float tpot) {
+                                     float e2e, float ttft, float tpot, float nout) {
     o.choice[q] = key_pair(key);
     if (o.feasible) o.feasible[q] = key_feasible(key) ? 1 : 0;
     if (o.utility) o.utility[q] = u;
     if (o.e2e) o.e2e[q] = e2e;
     if (o.ttft) o.ttft[q] = ttft;
     if (o.tpot) o.tpot[q] = tpot;
+    if (o.nout) o.nout[q] = nout;
 }
 
 }  // namespace hwr

@@ -20,6 +20,8 @@ constexpr int kMlpThreads = 512;             // predictor workgroup: 8 waves, tw
 constexpr int kGatherQ = 16;     // feature gather: queries per workgroup
 constexpr int kMaxPairs = 1024;
 constexpr int kMaxModels = 32;
+constexpr int kMaxHeads = 3;     // predictor outputs: TTFT, TPOT and (optionally) N_out
+constexpr int kPartVals = 8;     // floats per split partial: u, C, TTFT, TPOT, N_out, pad
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -54,7 +56,7 @@ __device__ inline bool key_feasible(uint64_t k) { return (k >> 63) != 0; }
 struct QueryArgs {
     int nq;                       // queries in this chunk
     const int32_t *input_len;     // [nq]
-    const int32_t *nout;          // [nq]
+    const int32_t *nout;          // [nq] given N_out (two-head predictor), else unused
     const float *slo;             // [nq] or nullptr
     float default_slo;
 };
@@ -62,7 +64,7 @@ struct QueryArgs {
 struct OutArgs {                  // per query; all but choice may be null
     int32_t *choice;
     uint8_t *feasible;
-    float *utility, *e2e, *ttft, *tpot;
+    float *utility, *e2e, *ttft, *tpot, *nout;
 };
 
 struct StateArgs {
@@ -86,8 +88,9 @@ struct QualityArgs {
 
 struct MlpArgs {                  // bf16 predictor (fused or staged)
     int N, M, len_slot;
+    int nheads;                   // 2, or 3: N_out predicted by the third head
     float alpha;
-    float b3_0, b3_1;
+    float b3_0, b3_1, b3_2;
     QueryArgs q;
     const uint16_t *dep_bf16;     // [N][32]
     const int32_t *dep_model;     // [N]
@@ -97,19 +100,20 @@ struct MlpArgs {                  // bf16 predictor (fused or staged)
     const uint16_t *w3_frag;      // head layer A fragments (compact, see pack_predictor)
     const uint16_t *X;            // staged input [nq][N][32]
     float *cand_ttft, *cand_tpot; // [nq][N] (staged output or debug)
+    float *cand_nout;             // [nq][N] predicted N_out (three heads: staged output or debug)
     OutArgs out;
     int nsplit;                   // pair ranges (grid.y); >1 writes partials
     uint64_t *part_key;           // [nsplit][nq]
-    float *part_val;              // [nsplit][nq][4]
+    float *part_val;              // [nsplit][nq][kPartVals]
 };
 
 struct MlpF32Args {
-    int N, F, len_slot;
-    float b3_0, b3_1;
+    int N, F, len_slot, nheads;
+    float b3_0, b3_1, b3_2;
     QueryArgs q;
     const float *dep_f32;         // [N][32]
-    const float *w1, *b1, *w2, *b2, *w3;   // [F][H], [H], [H][H], [H], [H][2]
-    float *cand_ttft, *cand_tpot;
+    const float *w1, *b1, *w2, *b2, *w3;   // [F][H], [H], [H][H], [H], [H][nheads]
+    float *cand_ttft, *cand_tpot, *cand_nout;   // cand_nout: three heads only
 };
 
 struct GatherArgs {
@@ -127,6 +131,7 @@ struct EpilogueArgs {
     const int32_t *dep_model;
     const float *qmat;
     const float *cand_ttft, *cand_tpot;
+    const float *cand_nout;       // [nq][N] predicted N_out, or null: the query's given N_out
     OutArgs out;
 };
 
@@ -150,12 +155,12 @@ struct SingleOut {
     int32_t choice;
     uint32_t feasible;
     float utility, e2e, ttft, tpot;
-    uint32_t pad;
+    float nout;                   // N_out of the chosen pair
 };
 
 struct SingleArgs {
-    int N, M, D, len_slot, arch_width, gpu_width;
-    float alpha, b3_0, b3_1;
+    int N, M, D, len_slot, arch_width, gpu_width, nheads;
+    float alpha, b3_0, b3_1, b3_2;
     const SingleIn *in;           // device-visible pinned record
     SingleOut *out;               // device-visible pinned record
     const hwr_hw_state *state;    // device-visible pinned copy of the current signals [N]

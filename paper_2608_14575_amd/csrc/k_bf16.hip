@@ -114,7 +114,7 @@ hipError_t launch_quality_bf16(const QualityArgs &a, hipStream_t s) {
 // carries column tile h alone (one query per lane).  Fused mode then applies
 // Eq. 2, the bound test and the utility and keeps the query's best candidate
 // (Eq. 3); staged mode reads X from HBM and writes TTFT/TPOT per candidate.
-template <int H, bool STAGED>
+template <int H, bool STAGED, int NH>
 __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
     constexpr int MT = H / 32;     // 32-row tiles of a hidden layer
     constexpr int KB2 = H / 16;    // k-blocks of the second layer
@@ -123,9 +123,10 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
     __shared__ bf16x8 s_w2[MT * KB2 * 64];
     __shared__ f32x4 s_b1[MT * 2 * 4];
     __shared__ f32x4 s_b2[MT * 2 * 4];
-    __shared__ bf16x8 s_w3f[KB2 * 4 + 1];
+    __shared__ bf16x8 s_w3f[KB2 * 2 * kMaxHeads + 1];
     __shared__ uint64_t s_mkey[kQPerBlock];
     __shared__ f32x4 s_mval[kQPerBlock];
+    __shared__ float s_mnout[NH == 3 ? kQPerBlock : 1];
     const int tid = threadIdx.x;
     {
         const uint4 *g;
@@ -144,7 +145,7 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
         for (int i = tid; i < MT * 2 * 4; i += kMlpThreads) d[i] = g[i];
         g = reinterpret_cast<const uint4 *>(a.w3_frag);
         d = reinterpret_cast<uint4 *>(s_w3f);
-        for (int i = tid; i < KB2 * 4 + 1; i += kMlpThreads) d[i] = g[i];
+        for (int i = tid; i < KB2 * 2 * NH + 1; i += kMlpThreads) d[i] = g[i];
     }
     __syncthreads();
 
@@ -168,7 +169,7 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
     const int qme = qbase + 32 * h + n;
     const bool vme = qme < nq;
     const int qmc = vme ? qme : 0;
-    const int32_t nomy = a.q.nout[qmc];
+    const int32_t nomy = a.q.nout ? a.q.nout[qmc] : 0;   // given N_out (two heads)
     const float nout = static_cast<float>(nomy < 0 ? 0 : nomy);
     const Bound bound = make_bound(a.q.slo ? a.q.slo[qmc] : a.q.default_slo);
     // the input-length slot: k-block, lane half and element holding it
@@ -295,13 +296,14 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
             }
         };
         // Head layer on the matrix pipe: z^T = W3^T h2^T.  Both column tiles
-        // share one accumulator: tile 0's A fragment holds the two heads in
-        // rows 0-1, tile 1's the same values in rows 4-5 (a 4-lane shift), so
-        // lanes 0-31 end with tile 0's (z0, z1) and lanes 32-63 with tile 1's,
-        // in accumulator elements 0 and 1.  (Packed bf16 dot products would
-        // stall the matrix pipe: they do not co-issue with MFMA on gfx950.)
+        // share one accumulator: tile 0's A fragment holds the NH heads (2 or
+        // 3) in rows 0..NH-1, tile 1's the same values in rows 4..3+NH (a
+        // 4-lane shift), so lanes 0-31 end with tile 0's z and lanes 32-63
+        // with tile 1's, in accumulator elements 0..NH-1.  (Packed bf16 dot
+        // products would stall the matrix pipe: they do not co-issue with
+        // MFMA on gfx950.)
         f32x16 acc3 = {};
-        const int w3_lane = (lo & 31) < 2 ? (lo & 31) : -1;
+        const int w3_lane = (lo & 31) < NH ? (lo & 31) : -1;
         auto l2_epi = [&](int mo, const f32x16 (&c)[NT]) {
             bf16x8 h2[NT][2];
 #pragma unroll
@@ -312,7 +314,7 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
 #pragma unroll
             for (int b = 0; b < 2; ++b) {
                 const int kb = 2 * mo + b;
-                const bf16x8 f0 = s_w3f[w3_lane >= 0 ? (kb * 2 + w3_lane) * 2 + ho : KB2 * 4];
+                const bf16x8 f0 = s_w3f[w3_lane >= 0 ? (kb * NH + w3_lane) * 2 + ho : KB2 * 2 * NH];
                 const bf16x8 f1 = shift_rows4(f0);
                 acc3 = mfma32(f0, h2[0][b], acc3);
                 acc3 = mfma32(f1, h2[1][b], acc3);
@@ -350,29 +352,35 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
         // holds the other 128 hidden units of the same candidates)
         const float tt = softplus_fast(acc3[0] + a.b3_0);
         const float tp = softplus_fast(acc3[1] + a.b3_1);
+        // N_out: the third head's prediction (tokens), else the query's given value
+        const float nc = NH == 3 ? softplus_fast(acc3[2] + a.b3_2) : nout;
         const size_t ci = static_cast<size_t>(qmc) * a.N + d;
         if constexpr (STAGED) {
             if (vme) {
                 a.cand_ttft[ci] = tt;
                 a.cand_tpot[ci] = tp;
+                if (NH == 3) a.cand_nout[ci] = nc;
             }
         } else {
             if (a.cand_ttft && vme) {
                 a.cand_ttft[ci] = tt;
                 a.cand_tpot[ci] = tp;
             }
+            if (a.cand_nout && vme) a.cand_nout[ci] = nc;
             // ---- cost, bound test, utility, running argmax (Eq. 2, Eq. 3)
-            offer(best, decide(tt, tp, nout, bound, Qd, a.alpha), d, tt, tp);
+            offer<NH == 3>(best, decide(tt, tp, nc, bound, Qd, a.alpha), d, tt, tp, nc);
         }
     }
     if constexpr (!STAGED) {
         uint64_t bkey = best_key(best);
         float bu = best.u, be = best.e2e, btt = best.tt, btp = best.tp;
+        float bn = NH == 3 ? best.n : nout;
         // merge the two pair halves of each query through LDS
         const int slot = qw * kQPerWave + lane;
         if (grp == 1) {
             s_mkey[slot] = bkey;
             s_mval[slot] = (f32x4){bu, be, btt, btp};
+            if constexpr (NH == 3) s_mnout[slot] = bn;
         }
         __syncthreads();
         if (grp == 0 && vme) {
@@ -384,16 +392,19 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
                 be = v[1];
                 btt = v[2];
                 btp = v[3];
+                if constexpr (NH == 3) bn = s_mnout[slot];
             }
             if (nsplit == 1) {
-                write_outputs(a.out, qme, bkey, bu, be, btt, btp);
+                write_outputs(a.out, qme, bkey, bu, be, btt, btp, bn);
             } else {
                 const size_t pi = static_cast<size_t>(split) * nq + qme;
                 a.part_key[pi] = bkey;
-                a.part_val[pi * 4 + 0] = bu;
-                a.part_val[pi * 4 + 1] = be;
-                a.part_val[pi * 4 + 2] = btt;
-                a.part_val[pi * 4 + 3] = btp;
+                float *pv = a.part_val + pi * kPartVals;
+                pv[0] = bu;
+                pv[1] = be;
+                pv[2] = btt;
+                pv[3] = btp;
+                pv[4] = bn;
             }
         }
     }
@@ -402,8 +413,14 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
 template <int H>
 static hipError_t launch_mlp_h(bool staged, const MlpArgs &a, hipStream_t s) {
     const dim3 grid((a.q.nq + kQPerBlock - 1) / kQPerBlock, staged ? 1 : a.nsplit);
-    if (staged) hipLaunchKernelGGL((k_mlp_bf16<H, true>), grid, dim3(kMlpThreads), 0, s, a);
-    else hipLaunchKernelGGL((k_mlp_bf16<H, false>), grid, dim3(kMlpThreads), 0, s, a);
+    const dim3 block(kMlpThreads);
+    if (a.nheads == 3) {
+        if (staged) hipLaunchKernelGGL((k_mlp_bf16<H, true, 3>), grid, block, 0, s, a);
+        else hipLaunchKernelGGL((k_mlp_bf16<H, false, 3>), grid, block, 0, s, a);
+    } else {
+        if (staged) hipLaunchKernelGGL((k_mlp_bf16<H, true, 2>), grid, block, 0, s, a);
+        else hipLaunchKernelGGL((k_mlp_bf16<H, false, 2>), grid, block, 0, s, a);
+    }
     return hipGetLastError();
 }
 

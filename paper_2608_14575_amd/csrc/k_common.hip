@@ -52,19 +52,20 @@ hipError_t launch_quality_f32(const QualityArgs &a, hipStream_t s) {
 
 // ------------------------------------------------------------ fp32 predictor
 // Eq. 1 predictor in fp32, one thread per candidate (q, d): features, two
-// hidden ReLU layers, the two heads, softplus.  Weights staged in LDS; the
-// first-layer rows are zero-padded to 32 slots.
+// hidden ReLU layers, the two or three heads, softplus.  Weights staged in
+// LDS; the first-layer rows are zero-padded to 32 slots.
 template <int H>
 __global__ __launch_bounds__(256) void k_mlp_f32(MlpF32Args a) {
     __shared__ float s_w1[kFeatPad * H];
     __shared__ float s_w2[H * H];
-    __shared__ float s_w3[H * 2];
+    __shared__ float s_w3[H * kMaxHeads];
+    const int NH = a.nheads;
     __shared__ float s_b1[H];
     __shared__ float s_b2[H];
     for (int i = threadIdx.x; i < kFeatPad * H; i += blockDim.x)
         s_w1[i] = (i / H) < a.F ? a.w1[i] : 0.0f;
     for (int i = threadIdx.x; i < H * H; i += blockDim.x) s_w2[i] = a.w2[i];
-    for (int i = threadIdx.x; i < H * 2; i += blockDim.x) s_w3[i] = a.w3[i];
+    for (int i = threadIdx.x; i < H * NH; i += blockDim.x) s_w3[i] = a.w3[i];
     for (int i = threadIdx.x; i < H; i += blockDim.x) {
         s_b1[i] = a.b1[i];
         s_b2[i] = a.b2[i];
@@ -91,17 +92,19 @@ __global__ __launch_bounds__(256) void k_mlp_f32(MlpF32Args a) {
     }
 #pragma unroll
     for (int j = 0; j < H; ++j) h1[j] = fmaxf(h1[j], 0.0f);
-    float z0 = 0.0f, z1 = 0.0f;
+    float z0 = 0.0f, z1 = 0.0f, z2 = 0.0f;
     for (int j = 0; j < H; ++j) {
         float acc = s_b2[j];
 #pragma unroll
         for (int i = 0; i < H; ++i) acc = fmaf(s_w2[i * H + j], h1[i], acc);
         acc = fmaxf(acc, 0.0f);
-        z0 = fmaf(s_w3[2 * j + 0], acc, z0);
-        z1 = fmaf(s_w3[2 * j + 1], acc, z1);
+        z0 = fmaf(s_w3[NH * j + 0], acc, z0);
+        z1 = fmaf(s_w3[NH * j + 1], acc, z1);
+        if (NH == 3) z2 = fmaf(s_w3[NH * j + 2], acc, z2);
     }
     a.cand_ttft[c] = softplus_f32(z0 + a.b3_0);
     a.cand_tpot[c] = softplus_f32(z1 + a.b3_1);
+    if (NH == 3) a.cand_nout[c] = softplus_f32(z2 + a.b3_2);
 }
 
 hipError_t launch_mlp_f32(int H, const MlpF32Args &a, hipStream_t s) {
@@ -168,7 +171,7 @@ hipError_t launch_gather(const GatherArgs &a, hipStream_t s) {
 // again.
 constexpr int kEpiSlices = 4;
 
-template <bool V4>
+template <bool V4, bool PN>
 __global__ __launch_bounds__(256) void k_epilogue(EpilogueArgs a) {
     extern __shared__ float s_qm[];            // [4 waves][64 / G][M] quality rows
     const int G = a.group;
@@ -181,28 +184,34 @@ __global__ __launch_bounds__(256) void k_epilogue(EpilogueArgs a) {
     const int units = V4 ? a.N / 4 : a.N;
     const float *tt_row = a.cand_ttft + static_cast<size_t>(qc) * a.N;
     const float *tp_row = a.cand_tpot + static_cast<size_t>(qc) * a.N;
-    auto load = [&](int u, f32x4 &tv, f32x4 &pv, int4 &mv) {
+    // PN: N_out per candidate (predicted by a third head), else the query's
+    constexpr bool pn = PN;
+    const float *nn_row = pn ? a.cand_nout + static_cast<size_t>(qc) * a.N : nullptr;
+    auto load = [&](int u, f32x4 &tv, f32x4 &pv, f32x4 &nv, int4 &mv) {
         if (V4) {
             tv = reinterpret_cast<const f32x4 *>(tt_row)[u];
             pv = reinterpret_cast<const f32x4 *>(tp_row)[u];
+            if (pn) nv = reinterpret_cast<const f32x4 *>(nn_row)[u];
             mv = reinterpret_cast<const int4 *>(a.dep_model)[u];
         } else {
             tv[0] = tt_row[u];
             pv[0] = tp_row[u];
+            if (pn) nv[0] = nn_row[u];
             mv.x = a.dep_model[u];
         }
     };
-    f32x4 t4[kEpiSlices], p4[kEpiSlices];
+    f32x4 t4[kEpiSlices], p4[kEpiSlices], n4[kEpiSlices];
     int4 m4[kEpiSlices];
 #pragma unroll
     for (int j = 0; j < kEpiSlices; ++j) {
         t4[j] = f32x4{0, 0, 0, 0};
         p4[j] = f32x4{0, 0, 0, 0};
+        n4[j] = f32x4{0, 0, 0, 0};
         m4[j] = int4{0, 0, 0, 0};
         const int u = g + j * G;
-        if (valid && u < units) load(u, t4[j], p4[j], m4[j]);
+        if (valid && u < units) load(u, t4[j], p4[j], n4[j], m4[j]);
     }
-    const int32_t no = a.q.nout[qc];
+    const int32_t no = pn ? 0 : a.q.nout[qc];
     const float nout = static_cast<float>(no < 0 ? 0 : no);
     const Bound bound = make_bound(a.q.slo ? a.q.slo[qc] : a.q.default_slo);
     float *s_qw = s_qm + wave * qpw * a.M;
@@ -215,41 +224,48 @@ __global__ __launch_bounds__(256) void k_epilogue(EpilogueArgs a) {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
     const float *qrow = s_qw + (lane / G) * a.M;
     Best best = best_none();
-    auto consider = [&](int d, int model, float tt, float tp) {
-        offer(best, decide(tt, tp, nout, bound, qrow[model], a.alpha), d, tt, tp);
+    auto consider = [&](int d, int model, float tt, float tp, float nc) {
+        const float n = pn ? nc : nout;
+        offer(best, decide(tt, tp, n, bound, qrow[model], a.alpha), d, tt, tp, n);
     };
-    auto consider_slice = [&](int u, const f32x4 &tv, const f32x4 &pv, const int4 &mv) {
+    auto consider_slice = [&](int u, const f32x4 &tv, const f32x4 &pv, const f32x4 &nv, const int4 &mv) {
         if (V4) {
-            consider(4 * u + 0, mv.x, tv[0], pv[0]);
-            consider(4 * u + 1, mv.y, tv[1], pv[1]);
-            consider(4 * u + 2, mv.z, tv[2], pv[2]);
-            consider(4 * u + 3, mv.w, tv[3], pv[3]);
+            consider(4 * u + 0, mv.x, tv[0], pv[0], nv[0]);
+            consider(4 * u + 1, mv.y, tv[1], pv[1], nv[1]);
+            consider(4 * u + 2, mv.z, tv[2], pv[2], nv[2]);
+            consider(4 * u + 3, mv.w, tv[3], pv[3], nv[3]);
         } else {
-            consider(u, mv.x, tv[0], pv[0]);
+            consider(u, mv.x, tv[0], pv[0], nv[0]);
         }
     };
 #pragma unroll
     for (int j = 0; j < kEpiSlices; ++j) {
         const int u = g + j * G;
-        if (valid && u < units) consider_slice(u, t4[j], p4[j], m4[j]);
+        if (valid && u < units) consider_slice(u, t4[j], p4[j], n4[j], m4[j]);
     }
     for (int u = g + kEpiSlices * G; valid && u < units; u += G) {
-        f32x4 tv = {0, 0, 0, 0}, pv = {0, 0, 0, 0};
+        f32x4 tv = {0, 0, 0, 0}, pv = {0, 0, 0, 0}, nv = {0, 0, 0, 0};
         int4 mv = {0, 0, 0, 0};
-        load(u, tv, pv, mv);
-        consider_slice(u, tv, pv, mv);
+        load(u, tv, pv, nv, mv);
+        consider_slice(u, tv, pv, nv, mv);
     }
     const uint64_t k = best_key(best);
     const uint64_t m = group_max_u64(k, G);
-    if (valid && k == m && k != 0) write_outputs(a.out, q, k, best.u, best.e2e, best.tt, best.tp);
+    if (valid && k == m && k != 0) write_outputs(a.out, q, k, best.u, best.e2e, best.tt, best.tp, best.n);
 }
 
 hipError_t launch_epilogue(const EpilogueArgs &a, hipStream_t s) {
     const int qpb = kBlock / a.group;
     const unsigned grid = static_cast<unsigned>((a.q.nq + qpb - 1) / qpb);
     const size_t lds = static_cast<size_t>(qpb) * a.M * 4;
-    if (a.vec4) hipLaunchKernelGGL(k_epilogue<true>, dim3(grid), dim3(kBlock), lds, s, a);
-    else hipLaunchKernelGGL(k_epilogue<false>, dim3(grid), dim3(kBlock), lds, s, a);
+    const bool pn = a.cand_nout != nullptr;
+    if (a.vec4) {
+        if (pn) hipLaunchKernelGGL((k_epilogue<true, true>), dim3(grid), dim3(kBlock), lds, s, a);
+        else hipLaunchKernelGGL((k_epilogue<true, false>), dim3(grid), dim3(kBlock), lds, s, a);
+    } else {
+        if (pn) hipLaunchKernelGGL((k_epilogue<false, true>), dim3(grid), dim3(kBlock), lds, s, a);
+        else hipLaunchKernelGGL((k_epilogue<false, false>), dim3(grid), dim3(kBlock), lds, s, a);
+    }
     return hipGetLastError();
 }
 
@@ -268,8 +284,8 @@ __global__ __launch_bounds__(256) void k_merge(MergeArgs a) {
             bs = s;
         }
     }
-    const float *v = a.part_val + (static_cast<size_t>(bs) * a.nq + q) * 4;
-    write_outputs(a.out, q, best, v[0], v[1], v[2], v[3]);
+    const float *v = a.part_val + (static_cast<size_t>(bs) * a.nq + q) * kPartVals;
+    write_outputs(a.out, q, best, v[0], v[1], v[2], v[3], v[4]);
 }
 
 hipError_t launch_merge(const MergeArgs &a, hipStream_t s) {

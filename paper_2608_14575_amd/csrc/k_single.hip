@@ -81,13 +81,15 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
     constexpr int kHeldS = 4;                 // quality: embedding slices held (D <= 2048)
     constexpr int kHeldM = H <= 128 ? 2 : 1;  // quality: model pairs held per wave
     __shared__ bf16x8 s_w1[MT * 2 * 64];
-    __shared__ u32x4 s_bw[3][MT * 8];         // b1 tiles, b2 tiles, head pairs
+    __shared__ u32x4 s_bw[2][MT * 8];         // b1 tiles, b2 tiles
+    __shared__ u32x4 s_w3p[MT * 4 * kMaxHeads];   // head pairs: [tile][half][head][2]
     __shared__ __attribute__((aligned(16))) uint16_t s_emb[8192];
     __shared__ __attribute__((aligned(16))) uint16_t s_row[kMaxPairs][kFeatPad];   // bf16 rows
     __shared__ int s_model[kMaxPairs];
     __shared__ float s_bq[kMaxModels];
     __shared__ float s_q[kMaxModels];
-    __shared__ float s_z[4][32][2];
+    __shared__ float s_z[4][32][kMaxHeads];
+    const int NH = a.nheads;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, n = lane & 31, h = lane >> 5;
     const int b0 = a.arch_width + a.gpu_width;
     const int j8 = tid & 7, ks = (j8 - b0) & 7;
@@ -114,10 +116,13 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
     u32x4 rw1[kW1];
 #pragma unroll
     for (int i = 0; i < kW1; ++i) rw1[i] = reinterpret_cast<const u32x4 *>(a.w1_pk)[tid + 256 * i];
+    // b1 tiles (MT * 8 pieces), b2 tiles (MT * 8), head pairs (MT * 4 * NH)
+    const int nbw = MT * 16 + MT * 4 * NH;
     u32x4 rbw;
     {
-        const int tb = tid < MT * 24 ? tid : 0;
-        const int t = tb / (MT * 8), k = tb - t * (MT * 8);
+        const int tb = tid < nbw ? tid : 0;
+        const int t = tb < MT * 8 ? 0 : tb < MT * 16 ? 1 : 2;
+        const int k = tb - t * (MT * 8);
         const u32x4 *src = reinterpret_cast<const u32x4 *>(t == 0 ? static_cast<const void *>(a.b1_pk)
                                                            : t == 1 ? static_cast<const void *>(a.b2_pk)
                                                                     : static_cast<const void *>(a.w3_pk));
@@ -160,7 +165,8 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
     }
 #pragma unroll
     for (int i = 0; i < kW1; ++i) reinterpret_cast<u32x4 *>(s_w1)[tid + 256 * i] = rw1[i];
-    if (tid < MT * 24) s_bw[0][tid] = rbw;
+    if (tid < MT * 16) s_bw[0][tid] = rbw;
+    else if (tid < nbw) s_w3p[tid - MT * 16] = rbw;
     if (tid < a.M) s_bq[tid] = rbq;
     if (has0) {
         pair_row(s_row[p0], j8, b0, ks, ia0, ig0, raw0, prm0, len);
@@ -207,7 +213,7 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
             h1[2 * mt + 1] = relu_pack8s(acc, 8);
         }
         // ---- layer 2 row tiles of this wave, folded into the heads
-        float z0 = 0.0f, z1 = 0.0f;
+        float z0 = 0.0f, z1 = 0.0f, z2 = 0.0f;
 #pragma unroll
         for (int i = 0; i < MO; ++i) {
             if (wave + 4 * i >= MT) break;
@@ -226,22 +232,28 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
             }
 #pragma unroll
             for (int kb = 0; kb < KB2; ++kb) acc = mfma32s(fw2[i][kb], h1[kb], acc);
-            const u32x4 *w3 = &s_bw[2][(mo * 2 + h) * 4];
+            const u32x4 *w3 = &s_w3p[(mo * 2 + h) * 2 * NH];
             const u32x4 wa = w3[0], wb = w3[1], wc = w3[2], wd = w3[3];
+            const u32x4 we = NH == 3 ? w3[4] : u32x4{0, 0, 0, 0};
+            const u32x4 wf = NH == 3 ? w3[5] : u32x4{0, 0, 0, 0};
 #pragma unroll
             for (int p = 0; p < 8; ++p) {
                 const bf16x2 hp = relu_bf16x2(acc[2 * p], acc[2 * p + 1]);
                 const uint32_t u0 = p < 4 ? wa[p & 3] : wb[p & 3];
                 const uint32_t u1 = p < 4 ? wc[p & 3] : wd[p & 3];
+                const uint32_t u2 = p < 4 ? we[p & 3] : wf[p & 3];
                 z0 = __builtin_amdgcn_fdot2_f32_bf16(hp, __builtin_bit_cast(bf16x2, u0), z0, false);
                 z1 = __builtin_amdgcn_fdot2_f32_bf16(hp, __builtin_bit_cast(bf16x2, u1), z1, false);
+                z2 = __builtin_amdgcn_fdot2_f32_bf16(hp, __builtin_bit_cast(bf16x2, u2), z2, false);
             }
         }
         z0 += __shfl_xor(z0, 32);
         z1 += __shfl_xor(z1, 32);
+        z2 += __shfl_xor(z2, 32);
         if (h == 0) {
             s_z[wave][n][0] = z0;
             s_z[wave][n][1] = z1;
+            s_z[wave][n][2] = z2;
         }
         // ---- quality of every model (Sec. 3.2 item 3), once: wave w takes
         // models w, w + 4, w + 8, ...; lanes split D
@@ -302,7 +314,12 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
             const float zz1 = s_z[0][n][1] + s_z[1][n][1] + s_z[2][n][1] + s_z[3][n][1];
             const float tt = softplus_fast(zz0 + a.b3_0);
             const float tp = softplus_fast(zz1 + a.b3_1);
-            offer(best, decide(tt, tp, nout, bound, s_q[model], a.alpha), d, tt, tp);
+            float nc = nout;             // N_out: the query's, or the third head's prediction
+            if (NH == 3) {
+                const float zz2 = s_z[0][n][2] + s_z[1][n][2] + s_z[2][n][2] + s_z[3][n][2];
+                nc = softplus_fast(zz2 + a.b3_2);
+            }
+            offer(best, decide(tt, tp, nc, bound, s_q[model], a.alpha), d, tt, tp, nc);
         }
         if (ct + 1 < ntiles) __syncthreads();
     }
@@ -317,6 +334,7 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
             o->e2e = best.e2e;
             o->ttft = best.tt;
             o->tpot = best.tp;
+            o->nout = best.n;
             __threadfence_system();
             __hip_atomic_store(&o->seq, seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
         }

@@ -55,7 +55,7 @@ class hwr_config(C.Structure):
                 ("feat_dim", C.c_int32), ("hidden", C.c_int32), ("emb_dtype", C.c_int32),
                 ("weight_dtype", C.c_int32), ("pipeline", C.c_int32), ("max_chunk", C.c_int32),
                 ("cost_weight", C.c_float), ("default_slo_s", C.c_float), ("device", C.c_int32),
-                ("flags", C.c_int32),
+                ("flags", C.c_int32), ("n_heads", C.c_int32),
                 ("dep_model", _i32p), ("dep_gpu", _i32p), ("model_arch", _i32p),
                 ("model_params_b", _f32p), ("wq", _vp), ("bq", _f32p), ("w1", _vp), ("b1", _f32p),
                 ("w2", _vp), ("b2", _f32p), ("w3", _vp), ("b3", _f32p), ("stream", _vp)]
@@ -68,8 +68,8 @@ class hwr_query_batch(C.Structure):
 
 class hwr_route_result(C.Structure):
     _fields_ = [("choice", _vp), ("feasible", _vp), ("utility", _vp), ("e2e_s", _vp),
-                ("ttft_s", _vp), ("tpot_s", _vp), ("cand_ttft", _vp), ("cand_tpot", _vp),
-                ("cand_quality", _vp)]
+                ("ttft_s", _vp), ("tpot_s", _vp), ("nout", _vp), ("cand_ttft", _vp), ("cand_tpot", _vp),
+                ("cand_nout", _vp), ("cand_quality", _vp)]
 
 
 class hwr_kernel_times(C.Structure):
@@ -161,12 +161,14 @@ def _ptr(a) -> int:
 
 class Router:
     """Owns one hwr context.  Arrays follow include/hwr.h: weights row-major
-    ([D][M], [F][H], [H][H], [H][2]) as uint16 bf16 bits (bf16) or float32."""
+    ([D][M], [F][H], [H][H], [H][n_heads]) as uint16 bf16 bits (bf16) or
+    float32."""
 
     def __init__(self, *, dep_model, dep_gpu, model_arch, model_params_b, wq, bq, w1, b1, w2, b2,
                  w3, b3, arch_width: int, gpu_width: int, n_gpu_types: int, dtype: str,
                  cost_weight: float = 0.5, default_slo_s: float = 1.0, pipeline: str = "fused",
-                 max_chunk: int = 65536, stream: int = 0, flags: int = 0, device: int = 0):
+                 max_chunk: int = 65536, stream: int = 0, flags: int = 0, device: int = 0,
+                 n_heads: int = 2):
         wdt = np.uint16 if dtype == "bf16" else np.float32
         keep = dict(dep_model=np.ascontiguousarray(dep_model, np.int32),
                     dep_gpu=np.ascontiguousarray(dep_gpu, np.int32),
@@ -179,6 +181,9 @@ class Router:
         D, M = keep["wq"].shape
         F, H = keep["w1"].shape
         N = keep["dep_model"].shape[0]
+        if n_heads not in (2, 3) or keep["w3"].shape != (H, n_heads) or keep["b3"].shape != (n_heads,):
+            raise ValueError(f"w3 must be [H][n_heads] and b3 [n_heads] with n_heads 2 or 3 "
+                             f"(got {keep['w3'].shape}, {keep['b3'].shape}, n_heads={n_heads})")
         cfg = hwr_config()
         cfg.n_models, cfg.n_gpu_types, cfg.n_deployments = M, int(n_gpu_types), N
         cfg.arch_width, cfg.gpu_width = int(arch_width), int(gpu_width)
@@ -187,7 +192,7 @@ class Router:
         cfg.pipeline = HWR_PIPE_STAGED if pipeline == "staged" else HWR_PIPE_FUSED
         cfg.max_chunk = int(max_chunk)
         cfg.cost_weight, cfg.default_slo_s = float(cost_weight), float(default_slo_s)
-        cfg.device, cfg.flags = int(device), int(flags)
+        cfg.device, cfg.flags, cfg.n_heads = int(device), int(flags), int(n_heads)
         for k in ("dep_model", "dep_gpu", "model_arch"):
             setattr(cfg, k, keep[k].ctypes.data_as(_i32p))
         for k in ("model_params_b", "bq", "b1", "b2", "b3"):
@@ -195,7 +200,7 @@ class Router:
         for k in ("wq", "w1", "w2", "w3"):
             setattr(cfg, k, keep[k].ctypes.data)
         cfg.stream = int(stream)
-        self.M, self.N, self.D, self.dtype = M, N, D, dtype
+        self.M, self.N, self.D, self.dtype, self.n_heads = M, N, D, dtype, int(n_heads)
         self.ctx = hwr_init(cfg)
 
     @classmethod
@@ -204,6 +209,7 @@ class Router:
         sp = pb.spec
         kw.setdefault("cost_weight", sp.cost_weight)
         kw.setdefault("default_slo_s", sp.slo_value)
+        kw.setdefault("n_heads", sp.n_heads)
         return cls(dep_model=pb.dep_model, dep_gpu=pb.dep_gpu, model_arch=pb.model_arch,
                    model_params_b=pb.model_params_b, wq=pb.wq_bits, bq=pb.bq, w1=pb.w1_bits,
                    b1=pb.b1, w2=pb.w2_bits, b2=pb.b2, w3=pb.w3_bits, b3=pb.b3,
@@ -231,14 +237,15 @@ class Router:
         return hwr_profile_read(self.ctx, reset)
 
     def route(self, emb, input_len, expected_out_len, slo_s=None, *, mem: int,
-              choice, feasible=None, utility=None, e2e_s=None, ttft_s=None, tpot_s=None,
-              cand_ttft=None, cand_tpot=None, cand_quality=None) -> None:
+              choice, feasible=None, utility=None, e2e_s=None, ttft_s=None, tpot_s=None, nout=None,
+              cand_ttft=None, cand_tpot=None, cand_nout=None, cand_quality=None) -> None:
         """Route into caller-owned outputs (numpy for HWR_MEM_HOST, torch
         tensors on the device for HWR_MEM_DEVICE)."""
         n = int(input_len.shape[0])
         b = hwr_query_batch(n, mem, _ptr(emb), _ptr(input_len), _ptr(expected_out_len), _ptr(slo_s))
         r = hwr_route_result(_ptr(choice), _ptr(feasible), _ptr(utility), _ptr(e2e_s), _ptr(ttft_s),
-                             _ptr(tpot_s), _ptr(cand_ttft), _ptr(cand_tpot), _ptr(cand_quality))
+                             _ptr(tpot_s), _ptr(nout), _ptr(cand_ttft), _ptr(cand_tpot), _ptr(cand_nout),
+                             _ptr(cand_quality))
         hwr_route_batch(self.ctx, b, r)
 
     def route_host(self, emb, input_len, expected_out_len, slo_s=None, candidates: bool = False) -> dict:
@@ -247,14 +254,17 @@ class Router:
         wdt = np.uint16 if self.dtype == "bf16" else np.float32
         emb = np.ascontiguousarray(emb, wdt)
         il = np.ascontiguousarray(input_len, np.int32)
-        no = np.ascontiguousarray(expected_out_len, np.int32)
+        no = None if expected_out_len is None else np.ascontiguousarray(expected_out_len, np.int32)
         slo = None if slo_s is None else np.ascontiguousarray(slo_s, np.float32)
         out = dict(choice=np.full(n, -1, np.int32), feasible=np.zeros(n, np.uint8),
                    utility=np.zeros(n, np.float32), e2e_s=np.zeros(n, np.float32),
-                   ttft_s=np.zeros(n, np.float32), tpot_s=np.zeros(n, np.float32))
+                   ttft_s=np.zeros(n, np.float32), tpot_s=np.zeros(n, np.float32),
+                   nout=np.zeros(n, np.float32))
         if candidates:
             out.update(cand_ttft=np.zeros((n, self.N), np.float32),
                        cand_tpot=np.zeros((n, self.N), np.float32),
                        cand_quality=np.zeros((n, self.M), np.float32))
+            if self.n_heads == 3:
+                out["cand_nout"] = np.zeros((n, self.N), np.float32)
         self.route(emb, il, no, slo, mem=HWR_MEM_HOST, **out)
         return out

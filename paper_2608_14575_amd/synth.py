@@ -58,6 +58,8 @@ _K_MODELS, _K_WEIGHTS, _K_STATE, _K_WALK, _K_QUERIES = 0, 1, 2, 3, 4
 # distribution; a per-token latency that makes a few hundred tokens cost ~1-2 s)
 B3_TARGET_TTFT_S = 0.2
 B3_TARGET_TPOT_S = 0.005
+B3_TARGET_NOUT = 288.0          # median of U{64..512}: the given N_out's median
+NOUT_HEAD_SCALE = 100.0         # weight scale of the N_out head (tokens per unit)
 
 
 @dataclass(frozen=True)
@@ -87,6 +89,7 @@ class Spec:
     nout_hi: int = 512
     overload_frac: float = 0.0
     walk_steps: int = 0
+    n_heads: int = 2            # 3: the predictor also predicts N_out (Eq. 1)
 
     @property
     def n_deployments(self) -> int:
@@ -167,28 +170,33 @@ def softplus_inverse(y: float) -> float:
     return math.log(math.expm1(y))
 
 
-def b3_default() -> np.ndarray:
-    return np.array([softplus_inverse(B3_TARGET_TTFT_S),
-                     softplus_inverse(B3_TARGET_TPOT_S)], dtype=np.float32)
+def b3_targets(n_heads: int = 2) -> list:
+    t = [B3_TARGET_TTFT_S, B3_TARGET_TPOT_S]
+    return t + [B3_TARGET_NOUT] if n_heads == 3 else t
+
+
+def b3_default(n_heads: int = 2) -> np.ndarray:
+    return np.array([softplus_inverse(t) for t in b3_targets(n_heads)], dtype=np.float32)
 
 
 def b3_for(sp: Spec, seed: int) -> np.ndarray:
     """Output bias for (spec, seed).
 
     The stored table holds, per named workload and seed, the bias that puts the
-    median predicted TTFT / TPOT at the initial state on the targets above
-    (written by tests/golden/make_b3_table.py, which runs the CPU oracle).  Any
-    other (spec, seed) gets softplus^-1(target) with no calibration.
+    median predicted TTFT / TPOT (and N_out with three heads) at the initial
+    state on the targets above (written by tests/golden/make_b3_table.py,
+    which runs the CPU oracle).  Any other (spec, seed) gets
+    softplus^-1(target) with no calibration.
     """
-    key = f"{sp.name}:{seed}:{sp.embed_dim}:{sp.feat_dim}:{sp.hidden}:{sp.n_models}x{sp.n_gpu_types}"
-    ent = _b3_table().get(key)
+    ent = _b3_table().get(b3_key(sp, seed))
     if ent is None:
-        return b3_default()
+        return b3_default(sp.n_heads)
     return np.array(ent, dtype=np.float32)
 
 
 def b3_key(sp: Spec, seed: int) -> str:
-    return f"{sp.name}:{seed}:{sp.embed_dim}:{sp.feat_dim}:{sp.hidden}:{sp.n_models}x{sp.n_gpu_types}"
+    key = f"{sp.name}:{seed}:{sp.embed_dim}:{sp.feat_dim}:{sp.hidden}:{sp.n_models}x{sp.n_gpu_types}"
+    return key + ":h3" if sp.n_heads == 3 else key
 
 
 # ---------------------------------------------------------------- draws
@@ -209,7 +217,7 @@ class Problem:
     wq: np.ndarray              # [D, M]
     w1: np.ndarray              # [F, H]
     w2: np.ndarray              # [H, H]
-    w3: np.ndarray              # [H, 2]
+    w3: np.ndarray              # [H, n_heads]
     # ... and as the bits handed to the library (uint16 for bf16, else float32)
     wq_bits: np.ndarray
     w1_bits: np.ndarray
@@ -218,7 +226,7 @@ class Problem:
     bq: np.ndarray              # float32 [M]
     b1: np.ndarray              # float32 [H]
     b2: np.ndarray              # float32 [H]
-    b3: np.ndarray              # float32 [2]
+    b3: np.ndarray              # float32 [n_heads]
 
     @property
     def n_deployments(self) -> int:
@@ -261,6 +269,12 @@ def make_problem(sp: Spec, seed: int, b3: Optional[np.ndarray] = None) -> Proble
     w3 = rw.standard_normal((H, 2)) * math.sqrt(2.0 / H)
     wq = rw.standard_normal((D, M)) * 0.1
     bq = rw.uniform(0.4, 0.8, size=M).astype(np.float32)
+    if sp.n_heads == 3:
+        # the N_out head is drawn after everything else, so the other weights
+        # equal the two-head problem's; it works in tokens, hence the scale
+        w3 = np.hstack([w3, rw.standard_normal((H, 1)) * math.sqrt(2.0 / H) * NOUT_HEAD_SCALE])
+    elif sp.n_heads != 2:
+        raise ValueError("n_heads must be 2 or 3")
     w1v, w1b = _round_to(sp.dtype, w1)
     w2v, w2b = _round_to(sp.dtype, w2)
     w3v, w3b = _round_to(sp.dtype, w3)

@@ -88,16 +88,18 @@ def route(prob: dict, state: list, queries: list):
             for j in range(H):
                 a = _dot([prob["w2"][i][j] for i in range(H)], h1, prob["b2"][j])
                 h2.append(bf16(max(a, 0.0)) if use_bf16 else max(a, 0.0))
-            z = [_dot([prob["w3"][i][k] for i in range(H)], h2, prob["b3"][k]) for k in range(2)]
+            NH = prob.get("n_heads", 2)
+            z = [_dot([prob["w3"][i][k] for i in range(H)], h2, prob["b3"][k]) for k in range(NH)]
             sp = [f32(max(v, 0.0) + math.log1p(math.exp(-abs(v)))) for v in z]
-            ttft, tpot = sp
-            e2e = f32_exact(Fraction(tpot) * q["expected_out_len"] + Fraction(ttft))
+            ttft, tpot = sp[0], sp[1]
+            nout = sp[2] if NH == 3 else q["expected_out_len"]   # Eq. 1 third head, else given
+            e2e = f32_exact(Fraction(tpot) * Fraction(nout) + Fraction(ttft))
             slo = f32(q["slo_s"])
             feas = 1 if e2e <= slo else 0
             t = f32_exact(Fraction(e2e) / Fraction(slo))
             at = f32_exact(Fraction(f32(prob["alpha"])) * Fraction(t))
             u = f32_exact(Fraction(qual[m]) - Fraction(at))
-            cands.append((feas, u, -d, dict(d=d, ttft=ttft, tpot=tpot, e2e=e2e, u=u, z=z,
+            cands.append((feas, u, -d, dict(d=d, ttft=ttft, tpot=tpot, nout=nout, e2e=e2e, u=u, z=z,
                                               feasible=feas, quality=qual[m])))
         order = sorted(cands, key=lambda c: (c[0], c[1], c[2]), reverse=True)
         choices.append(order[0][3]["d"])
@@ -110,6 +112,7 @@ def from_synth(pb, state, qs, alpha=None):
     sp = pb.spec
     prob = dict(M=sp.n_models, N=pb.n_deployments, F=sp.feat_dim, H=sp.hidden,
                 arch_width=sp.arch_width, gpu_width=sp.gpu_width, bf16=sp.dtype == "bf16",
+                n_heads=sp.n_heads,
                 alpha=sp.cost_weight if alpha is None else alpha,
                 dep_model=[int(v) for v in pb.dep_model], dep_gpu=[int(v) for v in pb.dep_gpu],
                 model_arch=[int(v) for v in pb.model_arch],

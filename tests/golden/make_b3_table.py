@@ -4,8 +4,9 @@ bias of each named synthetic workload and seed.
 For (workload, seed) the CPU oracle runs the predictor with b3 = 0 over the
 first min(Q, 256) queries x all pairs at the initial state; then
 b3_k = softplus^-1(target_k) - median_k(z), so that the median predicted TTFT
-and TPOT sit on 0.2 s and 5 ms.  Only the oracle and the input generator are
-called.  Run from the repository root:  python tests/golden/make_b3_table.py
+and TPOT sit on 0.2 s and 5 ms (and, for the three-head variant of each
+workload, the median predicted N_out on 288 tokens).  Only the oracle and the
+input generator are called.  Run from the repository root:  python tests/golden/make_b3_table.py
 """
 import json
 import os
@@ -23,13 +24,13 @@ SEEDS = [1, 2, 3, 4, 5, 101, 102, 103, 104, 105, 201, 202, 203, 204, 205]
 
 
 def calibrate(sp, seed):
-    pb = S.make_problem(sp, seed, b3=np.zeros(2, np.float32))
+    NH = sp.n_heads
+    pb = S.make_problem(sp, seed, b3=np.zeros(NH, np.float32))
     st = S.make_state(sp, seed)
     qs = S.make_queries(sp, seed, chunk=0, n=min(sp.n_queries, 256))
     r = O.route_synth(pb, st, qs, candidates=True)
-    med = np.median(r.cand_z.reshape(-1, 2).astype(np.float64), axis=0)
-    tgt = np.array([S.softplus_inverse(S.B3_TARGET_TTFT_S),
-                    S.softplus_inverse(S.B3_TARGET_TPOT_S)])
+    med = np.median(r.cand_z.reshape(-1, NH).astype(np.float64), axis=0)
+    tgt = np.array([S.softplus_inverse(t) for t in S.b3_targets(NH)])
     return [float(np.float32(v)) for v in (tgt - med)]
 
 
@@ -37,10 +38,11 @@ def main():
     O.build(force=False)
     table = {}
     for name in ["C1", "C2", "C3", "C4", "C5"]:
-        sp = S.spec(name)
-        for seed in SEEDS:
-            table[S.b3_key(sp, seed)] = calibrate(sp, seed)
-            print(name, seed, table[S.b3_key(sp, seed)], flush=True)
+        for heads in (2, 3):
+            sp = S.spec(name, n_heads=heads)
+            for seed in SEEDS:
+                table[S.b3_key(sp, seed)] = calibrate(sp, seed)
+                print(name, heads, seed, table[S.b3_key(sp, seed)], flush=True)
     out = os.path.join(ROOT, "paper_2608_14575_amd", "b3_table.json")
     with open(out, "w") as f:
         json.dump(table, f, indent=1, sort_keys=True)

@@ -34,7 +34,7 @@ def to_dev_inputs(qs, dtype: str):
     return emb, il, no, slo
 
 
-def dev_outputs(n: int, N: int, M: int, candidates: bool):
+def dev_outputs(n: int, N: int, M: int, candidates: bool, heads: int = 2):
     import torch
     dev = torch.device("cuda")
     out = dict(choice=torch.full((n,), -1, dtype=torch.int32, device=dev),
@@ -42,18 +42,21 @@ def dev_outputs(n: int, N: int, M: int, candidates: bool):
                utility=torch.zeros(n, dtype=torch.float32, device=dev),
                e2e_s=torch.zeros(n, dtype=torch.float32, device=dev),
                ttft_s=torch.zeros(n, dtype=torch.float32, device=dev),
-               tpot_s=torch.zeros(n, dtype=torch.float32, device=dev))
+               tpot_s=torch.zeros(n, dtype=torch.float32, device=dev),
+               nout=torch.zeros(n, dtype=torch.float32, device=dev))
     if candidates:
         out.update(cand_ttft=torch.zeros((n, N), dtype=torch.float32, device=dev),
                    cand_tpot=torch.zeros((n, N), dtype=torch.float32, device=dev),
                    cand_quality=torch.zeros((n, M), dtype=torch.float32, device=dev))
+        if heads == 3:
+            out["cand_nout"] = torch.zeros((n, N), dtype=torch.float32, device=dev)
     return out
 
 
 def route_device(router: hwr.Router, qs, dtype: str, candidates: bool = True, with_slo: bool = True):
     import torch
     emb, il, no, slo = to_dev_inputs(qs, dtype)
-    out = dev_outputs(qs.n, router.N, router.M, candidates)
+    out = dev_outputs(qs.n, router.N, router.M, candidates, router.n_heads)
     router.route(emb, il, no, slo if with_slo else None, mem=hwr.HWR_MEM_DEVICE, **out)
     torch.cuda.synchronize()
     return {k: v.cpu().numpy() for k, v in out.items()}
@@ -68,4 +71,5 @@ def check(pb, state, qs, gpu: dict, rtol: float = None, query_ids=None) -> parit
     rtol = rtol_for(sp.dtype) if rtol is None else rtol
     orc = O.route_synth(pb, state, qs, candidates=True)
     return parity.compare(gpu, orc, slo=qs.slo_s, alpha=sp.cost_weight, dep_model=pb.dep_model,
-                          rtol=rtol, emb=qs.emb, wq=pb.wq, bq=pb.bq, query_ids=query_ids)
+                          rtol=rtol, emb=qs.emb, wq=pb.wq, bq=pb.bq, query_ids=query_ids,
+                          heads=sp.n_heads)

@@ -4,10 +4,14 @@ Predictions: every candidate's TTFT and TPOT within ``rtol`` relative of the
 oracle; qualities within ``rtol`` of their dot-product error scale
 sum_k |e_k Wq_km| + |bq_m|.
 
+With a third head the predicted N_out of every candidate is compared the
+same way, and the cost C = TTFT + N_out * TPOT then carries two uncertain
+factors, so its share of the uncertainty below is doubled (k = 2, else 1).
+
 Decisions: floating point decides the choice, so the choice is compared
 exactly only where the oracle's decision is robust to errors of that size:
-  tau_c = rtol * (|Q_c| + alpha * C_c / SLO)          (utility uncertainty)
-  ambiguous_c = |C_c - SLO| <= rtol * C_c             (bound test uncertain)
+  tau_c = rtol * (|Q_c| + k * alpha * C_c / SLO)      (utility uncertainty)
+  ambiguous_c = |C_c - SLO| <= k * rtol * C_c         (bound test uncertain)
 A query is *eligible* for a bit-exact choice when its winner b is not
 ambiguous, no ambiguous candidate could enter or leave the feasible set in a
 way that changes the winner, and every other competitor c has
@@ -34,6 +38,7 @@ class ParityReport:
     max_rel_ttft: float = 0.0
     max_rel_tpot: float = 0.0
     max_rel_quality: float = 0.0
+    max_rel_nout: float = 0.0
     max_rel_chosen: float = 0.0
     failures: list = field(default_factory=list)
 
@@ -45,12 +50,13 @@ class ParityReport:
         return (f"n={self.n} eligible={self.eligible / max(self.n, 1):.3f} "
                 f"exact={self.exact}/{self.eligible} eps={self.eps_ok}/{self.n - self.eligible} "
                 f"max_rel ttft={self.max_rel_ttft:.2e} tpot={self.max_rel_tpot:.2e} "
-                f"quality={self.max_rel_quality:.2e} chosen={self.max_rel_chosen:.2e}")
+                f"quality={self.max_rel_quality:.2e} nout={self.max_rel_nout:.2e} "
+                f"chosen={self.max_rel_chosen:.2e}")
 
 
 def compare(gpu: dict, orc, *, slo: np.ndarray, alpha: float, dep_model: np.ndarray, rtol: float,
             emb: np.ndarray = None, wq: np.ndarray = None, bq: np.ndarray = None,
-            query_ids=None) -> ParityReport:
+            query_ids=None, heads: int = 2) -> ParityReport:
     """gpu: dict of numpy outputs (choice, feasible, utility, e2e_s, ttft_s,
     tpot_s, optional cand_ttft / cand_tpot / cand_quality), rows aligned
     with the oracle result ``orc`` (oracle.OracleResult with candidates)."""
@@ -65,6 +71,12 @@ def compare(gpu: dict, orc, *, slo: np.ndarray, alpha: float, dep_model: np.ndar
         if rep.max_rel_ttft > rtol or rep.max_rel_tpot > rtol:
             bad = np.argwhere((e1 > rtol) | (e2 > rtol))[:5]
             rep.failures.append(f"predictions beyond rtol at (query, pair) {bad.tolist()}")
+    if heads == 3 and gpu.get("cand_nout") is not None:
+        no_o = orc.cand_nout.astype(np.float64)
+        en = np.abs(gpu["cand_nout"] - no_o) / no_o
+        rep.max_rel_nout = float(en.max())
+        if rep.max_rel_nout > rtol:
+            rep.failures.append(f"N_out predictions beyond rtol (max {rep.max_rel_nout:.3e})")
     if gpu.get("cand_quality") is not None and emb is not None:
         scale = np.abs(emb.astype(np.float64)) @ np.abs(wq.astype(np.float64)) + np.abs(bq)
         eq = np.abs(gpu["cand_quality"] - orc.quality) / scale
@@ -76,8 +88,9 @@ def compare(gpu: dict, orc, *, slo: np.ndarray, alpha: float, dep_model: np.ndar
     C = orc.cand_e2e.astype(np.float64)
     u = orc.cand_u.astype(np.float64)
     S = slo.astype(np.float64)[:, None]
-    tau = rtol * (np.abs(Q) + alpha * C / S)
-    amb = np.abs(C - S) <= rtol * C
+    k = 2.0 if heads == 3 else 1.0
+    tau = rtol * (np.abs(Q) + k * alpha * C / S)
+    amb = np.abs(C - S) <= k * rtol * C
     feas = orc.cand_feasible.astype(bool)
     sure = feas & ~amb
     g_all = np.asarray(gpu["choice"]).astype(np.int64)
@@ -119,7 +132,10 @@ def compare(gpu: dict, orc, *, slo: np.ndarray, alpha: float, dep_model: np.ndar
             rep.failures.append(f"query {qid[i]}: gpu {g} outside the epsilon-set (oracle {b})")
     # values reported for the chosen pair agree with the oracle's for that pair
     rows = np.arange(n)
-    for key, ref in (("ttft_s", tt_o), ("tpot_s", tp_o), ("e2e_s", C)):
+    refs = [("ttft_s", tt_o), ("tpot_s", tp_o), ("e2e_s", C)]
+    if heads == 3:
+        refs.append(("nout", orc.cand_nout.astype(np.float64)))
+    for key, ref in refs:
         if gpu.get(key) is not None:
             r = ref[rows, g_all]
             err = np.abs(np.asarray(gpu[key], np.float64) - r) / np.abs(r)

@@ -109,6 +109,8 @@ def _valid_cfg(keep):
     (lambda c, k: setattr(c, "embed_dim", 100), hwr.HWR_ERR_UNSUPPORTED),
     (lambda c, k: setattr(c, "feat_dim", 40), hwr.HWR_ERR_UNSUPPORTED),
     (lambda c, k: setattr(c, "emb_dtype", hwr.HWR_F32), hwr.HWR_ERR_UNSUPPORTED),
+    (lambda c, k: setattr(c, "n_heads", 4), hwr.HWR_ERR_INVALID_ARG),
+    (lambda c, k: setattr(c, "n_heads", 1), hwr.HWR_ERR_INVALID_ARG),
 ])
 def test_config_errors_are_status_codes(lib, mutate, status):
     keep = {}
@@ -144,3 +146,12 @@ def test_no_device_is_a_clean_error(lib):
 def test_binding_fails_loudly_without_library(tmp_path):
     with pytest.raises(RuntimeError, match="no fallback"):
         hwr.load(str(tmp_path / "missing.so"))
+
+
+def test_router_checks_head_shapes():
+    """The binding refuses W3 / b3 whose shapes disagree with n_heads (the
+    library reads H x n_heads weights)."""
+    from paper_2608_14575_amd import synth as S
+    pb = S.make_problem(S.spec("C2", n_queries=4), 1)
+    with pytest.raises(ValueError):
+        hwr.Router.from_problem(pb, n_heads=3)

@@ -26,7 +26,7 @@ def _device():
 
 def _exact(out, pb, qs, alpha):
     d = O.decide(pb.dep_model, out["cand_ttft"], out["cand_tpot"], out["cand_quality"],
-                 qs.expected_out_len, qs.slo_s, alpha)
+                 qs.expected_out_len, qs.slo_s, alpha, cand_nout=out.get("cand_nout"))
     assert np.array_equal(out["choice"], d["choice"])
     assert np.array_equal(out["feasible"], d["feasible"])
     assert np.array_equal(out["utility"].view(np.int32), d["utility"].view(np.int32))
@@ -35,6 +35,10 @@ def _exact(out, pb, qs, alpha):
     rows = np.arange(qs.n)
     assert np.array_equal(out["ttft_s"], out["cand_ttft"][rows, out["choice"]])
     assert np.array_equal(out["tpot_s"], out["cand_tpot"][rows, out["choice"]])
+    # and the N_out used for it: predicted (three heads) or the query's own
+    want_n = (out["cand_nout"][rows, out["choice"]] if "cand_nout" in out
+              else qs.expected_out_len.astype(np.float32))
+    assert np.array_equal(out["nout"], want_n)
 
 
 CASES = {
@@ -42,6 +46,9 @@ CASES = {
     "C3 ragged": ("C3", dict(n_queries=333), 3),
     "C5 shape": ("C5", dict(n_queries=300), 5),
     "15 pairs": ("C2", dict(n_queries=257, n_models=5, n_gpu_types=3), 8),
+    "C2 3 heads": ("C2", dict(n_queries=1000, n_heads=3), 2),
+    "C3 3 heads": ("C3", dict(n_queries=333, n_heads=3), 3),
+    "H=64 15 pairs 3 heads": ("C2", dict(n_queries=200, n_models=5, n_gpu_types=3, hidden=64, n_heads=3), 9),
 }
 
 
@@ -56,8 +63,9 @@ def test_device_decisions_are_exact(case, pipeline):
     _exact(G.route_device(r, qs, sp.dtype), pb, qs, sp.cost_weight)
 
 
-def test_fp32_host_decisions_are_exact():
-    sp = S.spec("C1")
+@pytest.mark.parametrize("heads", [2, 3])
+def test_fp32_host_decisions_are_exact(heads):
+    sp = S.spec("C1", n_heads=heads)
     pb, st, qs = S.make_problem(sp, 1), S.make_state(sp, 1), S.make_queries(sp, 1)
     r = G.make_router(pb)
     r.update(st)

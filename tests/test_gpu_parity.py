@@ -142,3 +142,41 @@ def test_c4_single_query_walk(flags):
         exact += rep.exact
     print(f"[parity] C4 single-query walk flags={flags}: eligible {elig}/200 exact {exact}", flush=True)
     assert elig > 100
+
+
+# ---------------------------------------------------------------- three heads
+@pytest.mark.parametrize("pipeline", ["fused", "staged"])
+@pytest.mark.parametrize("name,kw,seed", [
+    ("C2", dict(n_queries=2048), 2),                  # H = 128
+    ("C3", dict(n_queries=300), 3),                   # H = 256, ragged tail
+    ("C2", dict(n_queries=500, hidden=64), 6),        # H = 64
+])
+def test_three_heads_predicted_output_length(name, kw, seed, pipeline):
+    """Eq. 1 with the third head: N_out predicted per candidate and used in
+    Eq. 2; the query's given expected_out_len is not passed at all."""
+    sp = S.spec(name, n_heads=3, **kw)
+    pb, st, qs = S.make_problem(sp, seed), S.make_state(sp, seed), S.make_queries(sp, seed)
+    r = G.make_router(pb, pipeline=pipeline)
+    r.update(st)
+    import torch
+    emb, il, _, slo = G.to_dev_inputs(qs, sp.dtype)
+    out = G.dev_outputs(qs.n, r.N, r.M, True, 3)
+    r.route(emb, il, None, slo, mem=hwr.HWR_MEM_DEVICE, **out)
+    torch.cuda.synchronize()
+    out = {k: v.cpu().numpy() for k, v in out.items()}
+    rep = G.check(pb, st, qs, out)
+    _report(f"{name} 3 heads {pipeline}", rep)
+    assert rep.max_rel_nout < 2e-3
+    rows = np.arange(qs.n)
+    assert np.array_equal(out["nout"], out["cand_nout"][rows, out["choice"]])
+
+
+def test_three_heads_fp32_host():
+    sp = S.spec("C1", n_heads=3)
+    pb, st, qs = S.make_problem(sp, 1), S.make_state(sp, 1), S.make_queries(sp, 1)
+    r = G.make_router(pb)
+    r.update(st)
+    out = r.route_host(qs.emb_bits, qs.input_len, None, qs.slo_s, candidates=True)
+    rep = G.check(pb, st, qs, out)
+    _report("C1 3 heads fp32 host", rep)
+    assert rep.max_rel_nout < 1e-5

@@ -27,6 +27,8 @@ def _device():
     ("C3", dict()),                                   # H = 256, 64 pairs (2 tiles), D = 1024
     ("C5", dict()),                                   # H = 256, 256 pairs (8 tiles), D = 1536, M = 32
     ("C2", dict(n_models=5, n_gpu_types=3)),          # 15 pairs, odd model count
+    ("C4", dict(n_heads=3)),                          # predicted N_out (third head), H = 128
+    ("C3", dict(n_heads=3)),                          # predicted N_out, H = 256, 2 tiles
 ])
 @pytest.mark.parametrize("flags", [0, hwr.HWR_FLAG_GRAPH])
 def test_single_query_matches_oracle(name, kw, flags):
@@ -41,9 +43,11 @@ def test_single_query_matches_oracle(name, kw, flags):
     got = {k: np.concatenate([o[k] for o in outs]) for k in outs[0]}
     orc = O.route_synth(pb, st, qs)
     rep = parity.compare(got, orc, slo=qs.slo_s, alpha=sp.cost_weight, dep_model=pb.dep_model,
-                         rtol=1e-2)
+                         rtol=1e-2, heads=sp.n_heads)
     print(f"[parity] single {name} {kw} flags={flags}: {rep.summary()}", flush=True)
     assert rep.ok, rep.failures[:5]
     # the batch path on the same queries agrees on every eligible choice
     batch = G.route_device(r, qs, "bf16", candidates=False)
     assert (batch["choice"] == got["choice"]).mean() > 0.9
+    if sp.n_heads == 2:
+        assert np.array_equal(got["nout"], qs.expected_out_len.astype(np.float32))

@@ -21,7 +21,10 @@ MUTATIONS = {
     "w2_transposed": ("p->w2[(size_t)i * H + j]", "p->w2[(size_t)j * H + i]"),
     "dropped_b2": ("float a = (float)(acc + (double)p->b2[j]);", "float a = (float)(acc);"),
     "no_second_relu": ("h2[j] = store(p, a > 0.0f ? a : 0.0f);", "h2[j] = store(p, a);"),
-    "w3_heads_swapped": ("p->w3[(size_t)i * 2 + k]", "p->w3[(size_t)i * 2 + (1 - k)]"),
+    "w3_heads_swapped": ("p->w3[(size_t)i * NH + k]", "p->w3[(size_t)i * NH + (k < 2 ? 1 - k : k)]"),
+    "w3_row_stride_two": ("p->w3[(size_t)i * NH + k]", "p->w3[(size_t)i * 2 + k]"),
+    "nout_head_ignored": ("NH == 3 ? orc_softplus(z[2]) : nout_given", "NH == 3 ? (float)q->expected_out_len[iq] : nout_given"),
+    "nout_from_tpot_head": ("NH == 3 ? orc_softplus(z[2]) : nout_given", "NH == 3 ? orc_softplus(z[1]) : nout_given"),
     "cost_without_nout": ("fmaf(tpot, nout, ttft)", "(tpot + ttft)"),
     "strict_bound": ("(c <= slo)", "(c < slo)"),
     "utility_sign": ("float u = q - at;", "float u = q + at;"),

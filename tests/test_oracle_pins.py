@@ -39,23 +39,29 @@ def _state(**cols):
     return st
 
 
-def _p5_problem(M=2, H=64):
+def _p5_problem(M=2, H=64, n_heads=2):
     F = 24
     w1 = np.zeros((F, H), np.float32)
     w1[11, 0] = 1.0
     w1[10, 1] = 1.0
     w2 = np.zeros((H, H), np.float32)
     w2[0, 0] = w2[1, 1] = 1.0
-    w3 = np.zeros((H, 2), np.float32)
+    w3 = np.zeros((H, n_heads), np.float32)
     w3[0, 0] = w3[1, 1] = 1.0
+    b3 = [0.0, -5.0]
+    if n_heads == 3:                         # gpu_util (slot 12) -> third head
+        w1[12, 2] = 1.0
+        w2[2, 2] = 1.0
+        w3[2, 2] = 10.0
+        b3.append(100.0)
     D = 8
     return O.OracleProblem(
         dep_model=np.arange(M, dtype=np.int32), dep_gpu=np.zeros(M, np.int32),
         model_arch=np.zeros(M, np.int32), model_params_b=np.full(M, 7.0, np.float32),
         wq=np.zeros((D, M), np.float32), bq=np.array([0.6, 0.7][:M], np.float32),
         w1=w1, b1=np.zeros(H, np.float32), w2=w2, b2=np.zeros(H, np.float32),
-        w3=w3, b3=np.array([0.0, -5.0], np.float32),
-        arch_width=4, gpu_width=3, n_gpu_types=1, bf16=False, alpha=0.5)
+        w3=w3, b3=np.array(b3, np.float32),
+        arch_width=4, gpu_width=3, n_gpu_types=1, bf16=False, alpha=0.5, n_heads=n_heads)
 
 
 # ------------------------------------------------------------ rounding, softplus
@@ -176,6 +182,66 @@ def test_two_candidate_hand_case():
     # SLO = 2.0: the infeasible pair has the larger utility, and is still not chosen
     r = O.route(prob, st, emb, [100], [100], [2.0])
     assert r.cand_u[0, 1] > r.cand_u[0, 0] and r.cand_feasible[0].tolist() == [1, 0]
+
+
+def test_three_head_hand_case():
+    """Eq. 1 with the output-length head and Eq. 2 with the predicted N_out
+    (tests/golden/p5_three_head.txt); the given expected_out_len is ignored."""
+    g = _golden("p5_three_head.txt")
+    prob = _p5_problem(n_heads=3)
+    st = _state(running_q=[0, 0], waiting_q=[0, 3], kv_util=[0.5, 0.0], gpu_util=[0.5, 0.2],
+                ttft_avg_s=[1.0, 1.0], tpot_avg_s=[1.0, 1.0])
+    emb = np.zeros((1, 8), np.float32)
+    for slo, want in ((2.05, 0), (2.1, 1)):
+        r = O.route(prob, st, emb, [100], [100], [slo])
+        np.testing.assert_allclose(r.cand_ttft[0], [g["ttft0"], g["ttft1"]], rtol=2e-7)
+        np.testing.assert_allclose(r.cand_tpot[0], [g["tpot0"], g["tpot1"]], rtol=2e-7)
+        np.testing.assert_allclose(r.cand_nout[0], [g["nout0"], g["nout1"]], rtol=2e-7)
+        np.testing.assert_allclose(r.cand_e2e[0], [g["e2e0"], g["e2e1"]], rtol=2e-7)
+        np.testing.assert_allclose(r.cand_u[0], [g[f"u0_slo{slo}"], g[f"u1_slo{slo}"]], rtol=1e-6)
+        assert r.choice[0] == want == int(g[f"choice_slo{slo}"])
+        assert r.nout[0] == r.cand_nout[0, want]
+
+
+def test_three_head_mlp_linear_regime_is_affine_chain():
+    """The affine-chain pin with a third output column."""
+    rng = np.random.default_rng(4)
+    F, H = 24, 40
+    w1 = rng.uniform(0, 0.3, (F, H)).astype(np.float32)
+    w2 = rng.uniform(0, 0.1, (H, H)).astype(np.float32)
+    w3 = rng.uniform(0, 0.1, (H, 3)).astype(np.float32)
+    b1 = rng.uniform(0, 0.2, H).astype(np.float32)
+    b2 = rng.uniform(0, 0.2, H).astype(np.float32)
+    b3 = np.array([0.3, -0.4, 2.5], np.float32)
+    prob = O.OracleProblem(np.zeros(1, np.int32), np.zeros(1, np.int32), np.zeros(1, np.int32),
+                           np.ones(1, np.float32), np.zeros((4, 1), np.float32), np.zeros(1, np.float32),
+                           w1, b1, w2, b2, w3, b3, 4, 3, 1, False, n_heads=3)
+    for _ in range(5):
+        x = rng.uniform(0, 1, F).astype(np.float32)
+        zz = (x.astype(np.float64) @ w1 + b1) @ w2 + b2
+        np.testing.assert_allclose(O.mlp(prob, x), zz @ w3 + b3, rtol=3e-6)
+    assert not np.allclose(w3[:, 1], w3[:, 2])
+
+
+def test_constant_output_length_head_reduces_to_given_length():
+    """A third head with zero weights and bias 300 predicts N_out = 300
+    exactly (softplus(300) rounds to 300): the three-head path then equals the
+    two-head path with N_out = 300 given, bit for bit, whatever the queries'
+    own expected_out_len."""
+    sp3 = S.spec("C2", n_queries=120, n_heads=3)
+    sp2 = S.spec("C2", n_queries=120)
+    pb3, pb2 = S.make_problem(sp3, 6), S.make_problem(sp2, 6)
+    assert np.array_equal(pb3.w3[:, :2], pb2.w3) and np.array_equal(pb3.b3[:2], pb2.b3)
+    pb3.w3[:, 2] = 0.0
+    pb3.b3[2] = 300.0
+    st, qs = S.make_state(sp2, 6), S.make_queries(sp2, 6)
+    r3 = O.route_synth(pb3, st, qs)
+    given = np.full(qs.n, 300, np.int32)
+    r2 = O.route(O.OracleProblem.from_synth(pb2), st, qs.emb, qs.input_len, given, qs.slo_s)
+    assert (r3.cand_nout == 300.0).all()
+    for k in ("choice", "feasible", "utility", "e2e_s", "ttft_s", "tpot_s"):
+        assert np.array_equal(getattr(r3, k), getattr(r2, k)), k
+    assert not np.array_equal(qs.expected_out_len, given)
 
 
 # ------------------------------------------------------------ quality
@@ -316,10 +382,11 @@ def test_bound_equality_is_feasible():
 
 
 # ------------------------------------------------------------ brute force
-@pytest.mark.parametrize("dtype,seed", [("f32", 21), ("bf16", 22), ("bf16", 23)])
-def test_bruteforce_matches_oracle(dtype, seed):
+@pytest.mark.parametrize("dtype,seed,heads", [("f32", 21, 2), ("bf16", 22, 2), ("bf16", 23, 2),
+                                              ("f32", 24, 3), ("bf16", 25, 3)])
+def test_bruteforce_matches_oracle(dtype, seed, heads):
     sp = S.custom_spec(n_queries=6, n_models=3, n_gpu_types=2, embed_dim=8, hidden=8,
-                       dtype=dtype)
+                       dtype=dtype, n_heads=heads)
     pb, st, qs = S.make_problem(sp, seed), S.make_state(sp, seed), S.make_queries(sp, seed)
     r = O.route_synth(pb, st, qs)
     ch, ranked = BF.route(*BF.from_synth(pb, st, qs))
@@ -328,6 +395,7 @@ def test_bruteforce_matches_oracle(dtype, seed):
         np.testing.assert_allclose(r.cand_ttft[i], [c[3]["ttft"] for c in vals], rtol=1e-6)
         np.testing.assert_allclose(r.cand_tpot[i], [c[3]["tpot"] for c in vals], rtol=1e-6)
         np.testing.assert_allclose(r.cand_u[i], [c[3]["u"] for c in vals], rtol=0, atol=1e-6)
+        np.testing.assert_allclose(r.cand_nout[i], [c[3]["nout"] for c in vals], rtol=1e-6)
         top, second = ranked[i][0], ranked[i][1]
         if top[0] != second[0] or top[1] - second[1] > 1e-5:
             assert r.choice[i] == ch[i]
@@ -357,15 +425,16 @@ def _decide1(tt, tp, q_of_pair, nout, slo, alpha=0.5):
     return {k: v[0] for k, v in out.items()}
 
 
+@pytest.mark.parametrize("heads", [2, 3])
 @pytest.mark.parametrize("name,kw", [("C1", {}), ("C2", dict(n_queries=300)), ("C3", dict(n_queries=200))])
-def test_decide_reproduces_route(name, kw):
+def test_decide_reproduces_route(name, kw, heads):
     """Eq. 2 / Eq. 3 applied to the oracle's own predictions give the oracle's
     decisions bit for bit (the route itself is pinned by brute force)."""
-    sp = S.spec(name, **kw)
+    sp = S.spec(name, n_heads=heads, **kw)
     pb, st, qs = S.make_problem(sp, 7), S.make_state(sp, 7), S.make_queries(sp, 7)
     r = O.route_synth(pb, st, qs)
     d = O.decide(pb.dep_model, r.cand_ttft, r.cand_tpot, r.quality, qs.expected_out_len, qs.slo_s,
-                 sp.cost_weight)
+                 sp.cost_weight, cand_nout=r.cand_nout if heads == 3 else None)
     assert np.array_equal(d["choice"], r.choice)
     assert np.array_equal(d["feasible"], r.feasible)
     assert np.array_equal(d["utility"].view(np.int32), r.utility.view(np.int32))
