@@ -38,7 +38,7 @@ KERNEL_NAMES = {   # as the profiler names them
     "mlp": "void hwr::k_mlp_bf16<256, true, 2>(hwr::MlpArgs)",
     "quality": "hwr::k_quality_bf16(hwr::QualityArgs)",
     "gather": "hwr::k_gather(hwr::GatherArgs)",
-    "epilogue": "void hwr::k_epilogue<true, false>(hwr::EpilogueArgs)",
+    "epilogue": "void hwr::k_epilogue<true, false, false, false>(hwr::EpilogueArgs)",
 }
 
 

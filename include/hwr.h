@@ -14,18 +14,22 @@
  *      -- Sec. 3.2, Eq. 1 and Eq. 2 (with two heads N_out is given per query);
  *   3. estimates the hardware-independent quality Q of the pair's model from
  *      the query embedding (a linear head per model) -- Sec. 3.2, item 3;
- *   4. scores u = Q - alpha * C / SLO (the Sec. 3.1 trade-off score with the
- *      cost normalised by the bound) and takes, per query, the argmax over the
- *      pairs that meet the latency bound, C <= SLO -- Eq. 3.
+ *   4. scores each candidate -- by default u = Q - w * C / B (the Sec. 3.1
+ *      trade-off score with the cost normalised by the bound B), or the
+ *      paper's own u = (1 - w) * Q - w * C with w = lambda -- and takes, per
+ *      query, the argmax over the pairs that meet the latency bound, C <= B
+ *      -- Eq. 3.  B is the query's SLO, or the evaluation's SLO form
+ *      B = a + b * input_len + N_out * tpot_slo.  Several weights w can be
+ *      scored in one call (a lambda sweep), reusing the predictions.
  *
  * Feature layout (F slots; A = arch_width, Gw = gpu_width, b = A + Gw):
  *   [arch one-hot (A)] [GPU one-hot (Gw)] ln(params_B)/4, ln(input_len)/8,
  *   ln(1+running)/2, ln(1+waiting)/2, kv_util, gpu_util, ln(ttft_avg_s)/4,
  *   ln(tpot_avg_s)/4, then zeros up to F.  Requires A + Gw + 8 <= F <= 32.
  *
- * Decision rule: among candidates with C <= SLO, the largest u; if none
- * meets the bound, the largest u over all pairs (reported feasible = 0);
- * exact ties go to the lowest pair index.
+ * Decision rule: among candidates with C <= B, the largest u; if none meets
+ * the bound, the largest u over all pairs (reported feasible = 0); exact ties
+ * go to the lowest pair index.
  *
  * Predictor outputs: z = W3^T h2 + b3; TTFT = softplus(z0), TPOT = softplus(z1)
  * in seconds and, with three heads, N_out = softplus(z2) in tokens.
@@ -35,7 +39,9 @@
  * bf16 (nearest, ties to even) before each matrix product; products accumulate
  * in fp32; biases, predictions, costs and utilities are fp32.  With HWR_F32
  * everything is fp32.  The decision arithmetic rounds each operation once:
- * C = fma(TPOT, N_out, TTFT), t = C / SLO, u = Q - alpha * t.
+ * C = fma(TPOT, N_out, TTFT); B = fma(N_out, tpot_slo, fma(b, input_len, a))
+ * in the paper-bound mode; u = Q - w * (C / B), or (1 - w) * Q - w * C with
+ * 1 - w rounded once.
  *
  * Conventions
  *  - Every call returns an hwr_status; nothing throws across this boundary.
@@ -79,6 +85,11 @@ typedef enum { HWR_PIPE_FUSED = 0, HWR_PIPE_STAGED = 1 } hwr_pipeline;
 /* hwr_config.flags */
 #define HWR_FLAG_GRAPH 1          /* single host query: launch a captured graph */
 
+/* hwr_config.score_mode / bound_mode */
+typedef enum { HWR_SCORE_NORMALIZED = 0, HWR_SCORE_PAPER = 1 } hwr_score_mode;
+typedef enum { HWR_BOUND_GIVEN = 0, HWR_BOUND_PAPER = 1 } hwr_bound_mode;
+#define HWR_MAX_WEIGHTS 8         /* cost weights scored in one call           */
+
 /* Runtime signals of one pair (Table 2 of the paper plus GPU utilisation). */
 typedef struct {
     int32_t running_q;            /* requests running, >= 0                    */
@@ -102,12 +113,20 @@ typedef struct {
     int32_t weight_dtype;         /* hwr_dtype of wq, w1, w2, w3                 */
     int32_t pipeline;             /* hwr_pipeline                                */
     int32_t max_chunk;            /* queries per internal chunk (0 -> 65536)     */
-    float   cost_weight;          /* alpha in u = Q - alpha * C / SLO, >= 0      */
+    float   cost_weight;          /* w (one weight; see n_weights): >= 0, and    */
+                                  /* <= 1 with HWR_SCORE_PAPER                   */
     float   default_slo_s;        /* bound when a batch gives no per-query SLO   */
     int32_t device;               /* HIP device ordinal                          */
     int32_t flags;                /* HWR_FLAG_*                                  */
     int32_t n_heads;              /* predictor heads: 2 (or 0): N_out given per  */
                                   /* query; 3: N_out predicted (Eq. 1)           */
+    int32_t score_mode;           /* hwr_score_mode                              */
+    int32_t bound_mode;           /* hwr_bound_mode                              */
+    float   ttft_slo_a;           /* paper bound: a in s, > 0 (the paper's fit   */
+    float   ttft_slo_b;           /* times its 1.2 slack); b in s per input      */
+    float   tpot_slo;             /* token, >= 0; tpot_slo in s per output token */
+    int32_t n_weights;            /* K: 0 -> one decision with cost_weight;      */
+                                  /* 1..HWR_MAX_WEIGHTS -> cost_weights[K]       */
     const int32_t *dep_model;     /* [N] model of pair i, in [0, M)              */
     const int32_t *dep_gpu;       /* [N] GPU type of pair i, in [0, G)           */
     const int32_t *model_arch;    /* [M] architecture id, in [0, A)              */
@@ -121,6 +140,8 @@ typedef struct {
     const void    *w3;            /* [H][n_heads] row-major; column 0 TTFT,      */
                                   /* 1 TPOT, 2 N_out                             */
     const float   *b3;            /* [n_heads]                                   */
+    const float   *cost_weights;  /* [K] when n_weights > 0 (same limits as      */
+                                  /* cost_weight)                                */
     void          *stream;        /* hipStream_t the context works on, or NULL   */
 } hwr_config;                     /* all pointers are host memory                */
 
@@ -134,6 +155,9 @@ typedef struct {
     const float   *slo_s;         /* [n] latency bound in s, > 0; NULL -> default_slo_s */
 } hwr_query_batch;
 
+/* With n_weights = K > 1 every per-query output below holds K values per
+ * query, [n][K] (weight k of query q at q * K + k); the debug outputs keep
+ * their shapes. */
 typedef struct {                  /* caller-owned, in the batch's memory space   */
     int32_t *choice;              /* [n] chosen pair index (required)            */
     uint8_t *feasible;            /* [n] 1 iff the chosen pair meets the bound   */

@@ -22,11 +22,14 @@
  *    third head's prediction for the candidate, or (two heads) the output
  *    length given per query.
  *  - Quality (Sec. 3.2 item 3, hardware-independent): Q = e . Wq[:, m] + bq[m].
- *  - Decision (Sec. 3.1 score, Eq. 3): utility u = Q - alpha * C / SLO in fp32
- *    (alpha = 0.5 is the paper's score with lambda = 1/3 and C normalised by
- *    the bound, scaled by 2/3: the argmax is the same); a pair is feasible iff
- *    C <= SLO; choose the feasible pair with the largest u, ties to the lowest
- *    pair index; if no pair is feasible, the largest u over all pairs.
+ *  - Decision (Sec. 3.1 score, Eq. 3): by default u = Q - w * C / B in fp32
+ *    (w = 0.5 is the paper's score with lambda = 1/3 and C normalised by
+ *    the bound, scaled by 2/3: the argmax is the same); or the paper's own
+ *    score u = (1 - w) Q - w C (w = lambda, C in seconds).  B is the query's
+ *    SLO, or the evaluation's SLO form a + b p + N_out tpot_slo (p input
+ *    tokens).  A pair is feasible iff C <= B; choose the feasible pair with
+ *    the largest u, ties to the lowest pair index; if no pair is feasible,
+ *    the largest u over all pairs.
  */
 #include "hwr_oracle.h"
 
@@ -122,15 +125,45 @@ void orc_mlp(const orc_problem *p, const float *x, float *z) {
     free(h2);
 }
 
-/* u in fp32: t = C / SLO, then u = Q - alpha * t, each operation rounded once
- * (the file is built with contraction off); -0 -> +0, NaN -> -inf. */
-static float utility(float q, float alpha, float c, float slo) {
-    const float t = c / slo;
-    const float at = alpha * t;
-    float u = q - at;
+/* u in fp32, each operation rounded once (the file is built with contraction
+ * off): score 0: t = C / B, u = Q - w * t; score 1: u = (1 - w) * Q - w * C.
+ * -0 -> +0, NaN -> -inf. */
+static float utility(const orc_rule *r, float q, float c, float bound) {
+    float u;
+    if (r->score_mode == 1) {
+        const float w1 = 1.0f - r->w;
+        const float wq = w1 * q;
+        const float wc = r->w * c;
+        u = wq - wc;
+    } else {
+        const float t = c / bound;
+        const float at = r->w * t;
+        u = q - at;
+    }
     if (u != u) u = -INFINITY;
     if (u == 0.0f) u = 0.0f;
     return u;
+}
+
+/* The latency bound B of a candidate: the query's SLO, or a + b p + N_out
+ * tpot_slo (two fused multiply-adds, each rounded once). */
+static float bound_of(const orc_rule *r, int32_t input_len, float nout, float slo) {
+    if (r->bound_mode == 1) {
+        const float base = fmaf(r->ttft_slo_b, (float)input_len, r->ttft_slo_a);
+        return fmaf(nout, r->tpot_slo, base);
+    }
+    return slo;
+}
+
+static orc_rule rule_of(const orc_problem *p) {
+    orc_rule r;
+    r.score_mode = p->score_mode;
+    r.bound_mode = p->bound_mode;
+    r.w = p->alpha;
+    r.ttft_slo_a = p->ttft_slo_a;
+    r.ttft_slo_b = p->ttft_slo_b;
+    r.tpot_slo = p->tpot_slo;
+    return r;
 }
 
 int orc_route(const orc_problem *p, const orc_state *s, const orc_queries *q,
@@ -139,6 +172,7 @@ int orc_route(const orc_problem *p, const orc_state *s, const orc_queries *q,
     const int32_t NH = p->n_heads == 3 ? 3 : 2;
     if (N <= 0 || M <= 0 || F <= 0 || p->H <= 0 || q->n < 0) return -1;
     if (p->n_heads != 0 && p->n_heads != 2 && p->n_heads != 3) return -1;
+    const orc_rule rule = rule_of(p);
     if (p->arch_width + p->gpu_width + 8 > F) return -1;
     float *x = (float *)malloc(sizeof(float) * (size_t)F);
     float *qual = (float *)malloc(sizeof(float) * (size_t)M);
@@ -161,9 +195,11 @@ int orc_route(const orc_problem *p, const orc_state *s, const orc_queries *q,
             const float tpot = orc_softplus(z[1]);
             const float nout = NH == 3 ? orc_softplus(z[2]) : nout_given;
             const float c = fmaf(tpot, nout, ttft);
-            const int feas = (c <= slo);
-            const float u = utility(qual[p->dep_model[d]], p->alpha, c, slo);
+            const float bound = bound_of(&rule, q->input_len[iq], nout, slo);
+            const int feas = (c <= bound);
+            const float u = utility(&rule, qual[p->dep_model[d]], c, bound);
             const size_t ci = (size_t)iq * N + d;
+            if (r->cand_bound) r->cand_bound[ci] = bound;
             if (r->cand_z)
                 for (int32_t k = 0; k < NH; ++k) r->cand_z[NH * ci + k] = z[k];
             if (r->cand_nout) r->cand_nout[ci] = nout;
@@ -193,7 +229,8 @@ int orc_route(const orc_problem *p, const orc_state *s, const orc_queries *q,
 
 int orc_decide(int32_t n, int32_t N, int32_t M, const int32_t *dep_model,
                const float *cand_ttft, const float *cand_tpot, const float *cand_nout,
-               const float *quality, const int32_t *expected_out_len, const float *slo_s, float alpha,
+               const float *quality, const int32_t *input_len, const int32_t *expected_out_len,
+               const float *slo_s, const orc_rule *rule,
                int32_t *choice, uint8_t *feasible, float *utility_out, float *e2e_out) {
     if (n < 0 || N <= 0 || M <= 0) return -1;
     for (int32_t iq = 0; iq < n; ++iq) {
@@ -205,8 +242,9 @@ int orc_decide(int32_t n, int32_t N, int32_t M, const int32_t *dep_model,
             const size_t ci = (size_t)iq * N + d;
             const float nout = cand_nout ? cand_nout[ci] : (float)expected_out_len[iq];
             const float c = fmaf(cand_tpot[ci], nout, cand_ttft[ci]);
-            const int feas = (c <= slo);
-            const float u = utility(quality[(size_t)iq * M + dep_model[d]], alpha, c, slo);
+            const float bound = bound_of(rule, input_len[iq], nout, slo);
+            const int feas = (c <= bound);
+            const float u = utility(rule, quality[(size_t)iq * M + dep_model[d]], c, bound);
             if (best < 0 || feas > best_f || (feas == best_f && u > best_u)) {
                 best = d; best_f = feas; best_u = u; best_c = c;
             }

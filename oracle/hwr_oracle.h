@@ -28,7 +28,10 @@ typedef struct {
     int32_t arch_width, gpu_width;     /* one-hot widths                                 */
     int32_t bf16;                      /* 1: round x, h1, h2 to bf16 before next layer  */
     int32_t n_heads;                   /* 2 (or 0): N_out given; 3: predicted (Eq. 1)    */
-    float   alpha;                     /* u = Q - alpha * C / SLO                        */
+    float   alpha;                     /* cost weight w of the score (see orc_rule)      */
+    int32_t score_mode;                /* see orc_rule                                   */
+    int32_t bound_mode;
+    float   ttft_slo_a, ttft_slo_b, tpot_slo;
     const int32_t *dep_model, *dep_gpu;     /* [N]                                   */
     const int32_t *model_arch;              /* [M]                                   */
     const float   *model_params_b;          /* [M] (billions)                        */
@@ -51,6 +54,18 @@ typedef struct {
     const float   *slo_s;                   /* [n]                                   */
 } orc_queries;
 
+/* Decision rule (Sec. 3.1 score, Eq. 3 bound; the bound's paper form is the
+ * evaluation's SLO definition):
+ *   score_mode 0: u = Q - w * (C / B)        1: u = (1 - w) * Q - w * C
+ *   bound_mode 0: B = the query's SLO        1: B = a + b * p + N_out * tpot_slo
+ * with p the input length and N_out the candidate's (given or predicted);
+ * a pair is feasible iff C <= B.  Every fp32 operation is rounded once. */
+typedef struct {
+    int32_t score_mode, bound_mode;
+    float   w;
+    float   ttft_slo_a, ttft_slo_b, tpot_slo;
+} orc_rule;
+
 typedef struct {                            /* any pointer may be NULL (not written) */
     int32_t *choice;                        /* [n]                                   */
     uint8_t *feasible;                      /* [n]                                   */
@@ -59,6 +74,7 @@ typedef struct {                            /* any pointer may be NULL (not writ
     float   *cand_z;                        /* [n*N*NH] predictor outputs before softplus */
     float   *cand_nout;                     /* [n*N] N_out used per candidate        */
     float   *cand_ttft, *cand_tpot, *cand_e2e, *cand_u;   /* [n*N]                   */
+    float   *cand_bound;                    /* [n*N] the bound B of each candidate    */
     uint8_t *cand_feasible;                 /* [n*N]                                 */
     float   *quality;                       /* [n*M]                                 */
 } orc_result;
@@ -82,7 +98,8 @@ void  orc_mlp(const orc_problem *p, const float *x, float *z);
  * same arithmetic and tie rule as orc_route.  Returns 0, or -1 on bad sizes. */
 int   orc_decide(int32_t n, int32_t N, int32_t M, const int32_t *dep_model,
                  const float *cand_ttft, const float *cand_tpot, const float *cand_nout,
-                 const float *quality, const int32_t *expected_out_len, const float *slo_s, float alpha,
+                 const float *quality, const int32_t *input_len, const int32_t *expected_out_len,
+                 const float *slo_s, const orc_rule *rule,
                  int32_t *choice, uint8_t *feasible, float *utility_out, float *e2e_out);
 /* the whole path over a batch of queries.  Returns 0, or -1 on bad sizes. */
 int   orc_route(const orc_problem *p, const orc_state *s, const orc_queries *q,

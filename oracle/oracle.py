@@ -52,7 +52,8 @@ class _Problem(C.Structure):
     _fields_ = [("M", C.c_int32), ("G", C.c_int32), ("N", C.c_int32), ("D", C.c_int32),
                 ("F", C.c_int32), ("H", C.c_int32), ("arch_width", C.c_int32),
                 ("gpu_width", C.c_int32), ("bf16", C.c_int32), ("n_heads", C.c_int32),
-                ("alpha", C.c_float),
+                ("alpha", C.c_float), ("score_mode", C.c_int32), ("bound_mode", C.c_int32),
+                ("ttft_slo_a", C.c_float), ("ttft_slo_b", C.c_float), ("tpot_slo", C.c_float),
                 ("dep_model", _i32p), ("dep_gpu", _i32p), ("model_arch", _i32p),
                 ("model_params_b", _f32p), ("wq", _f32p), ("bq", _f32p),
                 ("w1", _f32p), ("b1", _f32p), ("w2", _f32p), ("b2", _f32p),
@@ -64,6 +65,11 @@ class _State(C.Structure):
                 ("gpu_util", _f32p), ("ttft_avg_s", _f32p), ("tpot_avg_s", _f32p)]
 
 
+class _Rule(C.Structure):
+    _fields_ = [("score_mode", C.c_int32), ("bound_mode", C.c_int32), ("w", C.c_float),
+                ("ttft_slo_a", C.c_float), ("ttft_slo_b", C.c_float), ("tpot_slo", C.c_float)]
+
+
 class _Queries(C.Structure):
     _fields_ = [("n", C.c_int32), ("emb", _f32p), ("input_len", _i32p),
                 ("expected_out_len", _i32p), ("slo_s", _f32p)]
@@ -73,7 +79,7 @@ class _Result(C.Structure):
     _fields_ = [("choice", _i32p), ("feasible", _u8p), ("utility", _f32p),
                 ("e2e_s", _f32p), ("ttft_s", _f32p), ("tpot_s", _f32p), ("nout", _f32p),
                 ("cand_z", _f32p), ("cand_nout", _f32p), ("cand_ttft", _f32p), ("cand_tpot", _f32p),
-                ("cand_e2e", _f32p), ("cand_u", _f32p), ("cand_feasible", _u8p),
+                ("cand_e2e", _f32p), ("cand_u", _f32p), ("cand_bound", _f32p), ("cand_feasible", _u8p),
                 ("quality", _f32p)]
 
 
@@ -100,7 +106,7 @@ def lib():
         L.orc_mlp.argtypes = [C.POINTER(_Problem), _f32p, _f32p]
         L.orc_decide.restype = C.c_int
         L.orc_decide.argtypes = [C.c_int32, C.c_int32, C.c_int32, _i32p, _f32p, _f32p, _f32p, _f32p,
-                                 _i32p, _f32p, C.c_float, _i32p, _u8p, _f32p, _f32p]
+                                 _i32p, _i32p, _f32p, C.POINTER(_Rule), _i32p, _u8p, _f32p, _f32p]
         L.orc_route.restype = C.c_int
         L.orc_route.argtypes = [C.POINTER(_Problem), C.POINTER(_State), C.POINTER(_Queries),
                                 C.POINTER(_Result)]
@@ -143,6 +149,11 @@ class OracleProblem:
     bf16: bool
     alpha: float = 0.5
     n_heads: int = 2
+    score_mode: int = 0          # 0: u = Q - w C / B; 1: u = (1 - w) Q - w C
+    bound_mode: int = 0          # 0: B = the query's SLO; 1: B = a + b p + N_out tpot_slo
+    ttft_slo_a: float = 0.0
+    ttft_slo_b: float = 0.0
+    tpot_slo: float = 0.0
 
     @classmethod
     def from_synth(cls, pb, alpha: Optional[float] = None) -> "OracleProblem":
@@ -150,7 +161,8 @@ class OracleProblem:
         return cls(pb.dep_model, pb.dep_gpu, pb.model_arch, pb.model_params_b,
                    pb.wq, pb.bq, pb.w1, pb.b1, pb.w2, pb.b2, pb.w3, pb.b3,
                    sp.arch_width, sp.gpu_width, sp.n_gpu_types, sp.dtype == "bf16",
-                   sp.cost_weight if alpha is None else alpha, sp.n_heads)
+                   sp.cost_weight if alpha is None else alpha, sp.n_heads, sp.score_mode,
+                   sp.bound_mode, sp.ttft_slo_a, sp.ttft_slo_b, sp.tpot_slo)
 
     def _struct(self, keep: list) -> _Problem:
         arrs = dict(dep_model=_i32(self.dep_model), dep_gpu=_i32(self.dep_gpu),
@@ -164,7 +176,9 @@ class OracleProblem:
         assert arrs["w2"].shape == (H, H) and arrs["w3"].shape == (H, NH) and arrs["b3"].shape == (NH,)
         N = arrs["dep_model"].shape[0]
         s = _Problem(M, int(self.n_gpu_types), N, D, F, H, int(self.arch_width),
-                     int(self.gpu_width), int(bool(self.bf16)), NH, float(self.alpha))
+                     int(self.gpu_width), int(bool(self.bf16)), NH, float(self.alpha),
+                     int(self.score_mode), int(self.bound_mode), float(self.ttft_slo_a),
+                     float(self.ttft_slo_b), float(self.tpot_slo))
         for k in ("dep_model", "dep_gpu", "model_arch"):
             setattr(s, k, _ptr(arrs[k], C.c_int32))
         for k in ("model_params_b", "wq", "bq", "w1", "b1", "w2", "b2", "w3", "b3"):
@@ -240,6 +254,7 @@ class OracleResult:
     cand_tpot: Optional[np.ndarray] = None
     cand_e2e: Optional[np.ndarray] = None
     cand_u: Optional[np.ndarray] = None
+    cand_bound: Optional[np.ndarray] = None   # [n, N] the bound B of each candidate
     cand_feasible: Optional[np.ndarray] = None
     quality: Optional[np.ndarray] = None     # [n, M]
 
@@ -270,11 +285,12 @@ def route(prob: OracleProblem, state: np.ndarray, emb: np.ndarray, input_len, ex
         setattr(r, k, _ptr(getattr(out, k), C.c_float))
     if candidates:
         out.cand_z = np.zeros((n, N, int(prob.n_heads)), np.float32)
-        for k in ("cand_nout", "cand_ttft", "cand_tpot", "cand_e2e", "cand_u"):
+        for k in ("cand_nout", "cand_ttft", "cand_tpot", "cand_e2e", "cand_u", "cand_bound"):
             setattr(out, k, np.zeros((n, N), np.float32))
         out.cand_feasible = np.zeros((n, N), np.uint8)
         out.quality = np.zeros((n, M), np.float32)
-        for k in ("cand_z", "cand_nout", "cand_ttft", "cand_tpot", "cand_e2e", "cand_u", "quality"):
+        for k in ("cand_z", "cand_nout", "cand_ttft", "cand_tpot", "cand_e2e", "cand_u", "cand_bound",
+                  "quality"):
             setattr(r, k, _ptr(getattr(out, k), C.c_float))
         r.cand_feasible = _ptr(out.cand_feasible, C.c_uint8)
     rc = lib().orc_route(C.byref(p), C.byref(s), C.byref(q), C.byref(r))
@@ -284,23 +300,28 @@ def route(prob: OracleProblem, state: np.ndarray, emb: np.ndarray, input_len, ex
 
 
 def decide(dep_model, cand_ttft, cand_tpot, quality, expected_out_len, slo_s, alpha: float,
-           cand_nout=None) -> dict:
+           cand_nout=None, input_len=None, score_mode: int = 0, bound_mode: int = 0,
+           ttft_slo_a: float = 0.0, ttft_slo_b: float = 0.0, tpot_slo: float = 0.0) -> dict:
     """Eq. 2 and Eq. 3 on given predictions (the decision step alone, same
     arithmetic and tie rule as ``route``): per query the choice, feasibility,
     utility and cost.  Inputs: TTFT / TPOT [n, N], quality [n, M]; N_out per
-    candidate [n, N] (three heads) or None (the queries' expected_out_len)."""
+    candidate [n, N] (three heads) or None (the queries' expected_out_len);
+    the rule (weight ``alpha``, score and bound modes) as in ``orc_rule``."""
     tt, tp, qual = _f32(cand_ttft), _f32(cand_tpot), _f32(quality)
     cn = None if cand_nout is None else _f32(cand_nout)
     n, N = tt.shape
     M = qual.shape[1]
     dm, no, slo = _i32(dep_model), _i32(expected_out_len), _f32(slo_s)
+    il = _i32(np.ones(tt.shape[0]) if input_len is None else input_len)
+    rule = _Rule(int(score_mode), int(bound_mode), float(alpha), float(ttft_slo_a), float(ttft_slo_b),
+                 float(tpot_slo))
     assert tp.shape == (n, N) and qual.shape[0] == n and dm.shape == (N,)
     assert no.shape == (n,) and slo.shape == (n,) and (cn is None or cn.shape == (n, N))
     out = {"choice": np.zeros(n, np.int32), "feasible": np.zeros(n, np.uint8),
            "utility": np.zeros(n, np.float32), "e2e_s": np.zeros(n, np.float32)}
     rc = lib().orc_decide(n, N, M, _ptr(dm, C.c_int32), _ptr(tt, C.c_float), _ptr(tp, C.c_float),
-                          _ptr(cn, C.c_float), _ptr(qual, C.c_float), _ptr(no, C.c_int32), _ptr(slo, C.c_float),
-                          float(alpha), _ptr(out["choice"], C.c_int32), _ptr(out["feasible"], C.c_uint8),
+                          _ptr(cn, C.c_float), _ptr(qual, C.c_float), _ptr(il, C.c_int32), _ptr(no, C.c_int32),
+                          _ptr(slo, C.c_float), C.byref(rule), _ptr(out["choice"], C.c_int32), _ptr(out["feasible"], C.c_uint8),
                           _ptr(out["utility"], C.c_float), _ptr(out["e2e_s"], C.c_float))
     if rc != 0:
         raise ValueError("oracle rejected the sizes")

@@ -21,8 +21,10 @@ SOURCES = ["hwr_api.hip", "k_common.hip", "k_bf16.hip", "k_single.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
-    # no packed-fp32 instructions in device code
-    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # no packed-fp32 instructions in device code; no multiply-add contraction:
+    # every fp32 operation of the decision is rounded once, as documented (fused
+    # multiply-adds are written as fmaf where they are meant)
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-ffp-contract=off",
     "-Wall", "-Wno-unused-function",
     f"-I{INCLUDE}", f"-I{CSRC}",
 ]

@@ -36,7 +36,10 @@ struct hwr_ctx {
     int M = 0, G = 0, N = 0, A = 0, Gw = 0, D = 0, F = 0, H = 0, len_slot = 0;
     int bf16 = 0, pipeline = 0, max_chunk = 0, flags = 0, cus = 0;
     int NH = 2;                   // predictor heads (3: N_out predicted)
-    float alpha = 0.5f, default_slo = 1.0f, b3[kMaxHeads] = {0, 0, 0};
+    float default_slo = 1.0f, b3[kMaxHeads] = {0, 0, 0};
+    Rule rule{};                  // score and bound modes
+    int nw = 1;                   // cost weights per query (outputs [n][nw] when > 1)
+    float w[kMaxWeights] = {};
     // per-pair tables and state
     int32_t *d_dep_model = nullptr, *d_dep_gpu = nullptr, *d_model_arch = nullptr;
     float *d_params = nullptr;
@@ -279,7 +282,19 @@ hwr_status check_config(const hwr_config *cfg) {
         return uns("fp32 hidden width must be 64 or 128");
     if (cfg->pipeline != HWR_PIPE_FUSED && cfg->pipeline != HWR_PIPE_STAGED) return bad("unknown pipeline");
     if (cfg->max_chunk < 0 || cfg->max_chunk > (1 << 22)) return bad("max_chunk must be in [0, 2^22]");
-    if (!finite(cfg->cost_weight) || cfg->cost_weight < 0.0f) return bad("cost_weight must be finite and >= 0");
+    if (cfg->score_mode != HWR_SCORE_NORMALIZED && cfg->score_mode != HWR_SCORE_PAPER) return bad("unknown score_mode");
+    if (cfg->bound_mode != HWR_BOUND_GIVEN && cfg->bound_mode != HWR_BOUND_PAPER) return bad("unknown bound_mode");
+    if (cfg->bound_mode == HWR_BOUND_PAPER &&
+        (!finite(cfg->ttft_slo_a) || !finite(cfg->ttft_slo_b) || !finite(cfg->tpot_slo) ||
+         cfg->ttft_slo_a <= 0.0f || cfg->ttft_slo_b < 0.0f || cfg->tpot_slo < 0.0f))
+        return bad("paper bound needs ttft_slo_a > 0 and ttft_slo_b, tpot_slo >= 0 (finite)");
+    if (cfg->n_weights < 0 || cfg->n_weights > HWR_MAX_WEIGHTS) return bad("n_weights must be in [0, 8]");
+    if (cfg->n_weights > 0 && !cfg->cost_weights) return bad("cost_weights is NULL");
+    for (int k = 0; k < (cfg->n_weights > 0 ? cfg->n_weights : 1); ++k) {
+        const float w = cfg->n_weights > 0 ? cfg->cost_weights[k] : cfg->cost_weight;
+        if (!finite(w) || w < 0.0f) return bad("cost weights must be finite and >= 0");
+        if (cfg->score_mode == HWR_SCORE_PAPER && w > 1.0f) return bad("paper-score weights (lambda) must be <= 1");
+    }
     if (!finite(cfg->default_slo_s) || cfg->default_slo_s <= 0.0f) return bad("default_slo_s must be finite and > 0");
     if (cfg->n_heads != 0 && cfg->n_heads != 2 && cfg->n_heads != 3) return bad("n_heads must be 2 or 3 (0 means 2)");
     if (!cfg->dep_model || !cfg->dep_gpu || !cfg->model_arch || !cfg->model_params_b || !cfg->wq ||
@@ -361,9 +376,16 @@ hwr_status init_impl(const hwr_config *cfg, hwr_ctx **out) {
     c->pipeline = cfg->pipeline;
     c->max_chunk = cfg->max_chunk > 0 ? cfg->max_chunk : 65536;
     c->flags = cfg->flags;
-    c->alpha = cfg->cost_weight;
+    c->rule.score_paper = cfg->score_mode == HWR_SCORE_PAPER;
+    c->rule.bound_paper = cfg->bound_mode == HWR_BOUND_PAPER;
+    c->rule.a = cfg->ttft_slo_a;
+    c->rule.b = cfg->ttft_slo_b;
+    c->rule.tpot_slo = cfg->tpot_slo;
+    c->nw = cfg->n_weights > 0 ? cfg->n_weights : 1;
+    for (int k = 0; k < c->nw; ++k) c->w[k] = cfg->n_weights > 0 ? cfg->cost_weights[k] : cfg->cost_weight;
     c->default_slo = cfg->default_slo_s;
     c->NH = cfg->n_heads == 3 ? 3 : 2;
+    c->rule.per_cand = c->rule.bound_paper && c->NH == 3;
     for (int k = 0; k < c->NH; ++k) c->b3[k] = cfg->b3[k];
     c->cus = prop.multiProcessorCount;
 
@@ -425,7 +447,9 @@ hwr_status init_impl(const hwr_config *cfg, hwr_ctx **out) {
     }
     const size_t chunk = static_cast<size_t>(c->max_chunk);
     INIT_HIP(dev_alloc(&c->d_qmat, chunk * M));
-    if (!c->bf16 || c->pipeline == HWR_PIPE_STAGED) {
+    // per-candidate predictions in HBM: staged and fp32 paths, and several
+    // cost weights (the decisions then run after the predictor)
+    if (!c->bf16 || c->pipeline == HWR_PIPE_STAGED || c->nw > 1) {
         INIT_HIP(dev_alloc(&c->d_ctt, chunk * N));
         INIT_HIP(dev_alloc(&c->d_ctp, chunk * N));
         if (c->NH == 3) INIT_HIP(dev_alloc(&c->d_cno, chunk * N));
@@ -500,13 +524,14 @@ hwr_status route_device(hwr_ctx *c, const DevBatch &b) {
         qa.slo = b.slo ? b.slo + off : nullptr;
         qa.default_slo = c->default_slo;
         OutArgs oa = b.out;
-        oa.choice += off;
-        if (oa.feasible) oa.feasible += off;
-        if (oa.utility) oa.utility += off;
-        if (oa.e2e) oa.e2e += off;
-        if (oa.ttft) oa.ttft += off;
-        if (oa.tpot) oa.tpot += off;
-        if (oa.nout) oa.nout += off;
+        const size_t oo = static_cast<size_t>(off) * c->nw;   // outputs are [n][nw]
+        oa.choice += oo;
+        if (oa.feasible) oa.feasible += oo;
+        if (oa.utility) oa.utility += oo;
+        if (oa.e2e) oa.e2e += oo;
+        if (oa.ttft) oa.ttft += oo;
+        if (oa.tpot) oa.tpot += oo;
+        if (oa.nout) oa.nout += oo;
         float *qmat = b.cand_quality ? b.cand_quality + static_cast<size_t>(off) * M : c->d_qmat;
         float *ctt = b.cand_ttft ? b.cand_ttft + static_cast<size_t>(off) * N : nullptr;
         float *ctp = b.cand_tpot ? b.cand_tpot + static_cast<size_t>(off) * N : nullptr;
@@ -530,7 +555,8 @@ hwr_status route_device(hwr_ctx *c, const DevBatch &b) {
             ma.N = N;
             ma.M = M;
             ma.len_slot = c->len_slot;
-            ma.alpha = c->alpha;
+            ma.rule = c->rule;
+            ma.w = c->w[0];
             ma.b3_0 = c->b3[0];
             ma.b3_1 = c->b3[1];
             ma.b3_2 = c->b3[2];
@@ -546,7 +572,7 @@ hwr_status route_device(hwr_ctx *c, const DevBatch &b) {
             ma.w3_frag = c->d_w3_frag;
             ma.out = oa;
             ma.nsplit = 1;
-            if (c->pipeline == HWR_PIPE_FUSED) {
+            if (c->pipeline == HWR_PIPE_FUSED && c->nw == 1) {
                 ma.cand_ttft = ctt;
                 ma.cand_tpot = ctp;
                 ma.cand_nout = cno;
@@ -564,13 +590,25 @@ hwr_status route_device(hwr_ctx *c, const DevBatch &b) {
                 }
                 continue;
             }
-            GatherArgs ga{N, c->len_slot, qa, c->d_dep_bf16, c->d_X};
-            HWR_HIP(c, timed(c, HWR_K_GATHER, [&] { return launch_gather(ga, c->stream); }));
-            ma.X = c->d_X;
-            ma.cand_ttft = ctt ? ctt : c->d_ctt;
-            ma.cand_tpot = ctp ? ctp : c->d_ctp;
-            ma.cand_nout = cno ? cno : c->d_cno;
-            HWR_HIP(c, timed(c, HWR_K_MLP, [&] { return launch_mlp_bf16(c->H, true, ma, c->stream); }));
+            if (c->pipeline == HWR_PIPE_FUSED) {
+                // several cost weights: the fused kernel writes every
+                // candidate's predictions and no decision; the epilogue
+                // below takes one decision per weight
+                ma.cand_ttft = ctt ? ctt : c->d_ctt;
+                ma.cand_tpot = ctp ? ctp : c->d_ctp;
+                ma.cand_nout = c->NH == 3 ? (cno ? cno : c->d_cno) : nullptr;
+                ma.out = OutArgs{};
+                ma.nsplit = 1;
+                HWR_HIP(c, timed(c, HWR_K_FUSED, [&] { return launch_mlp_bf16(c->H, false, ma, c->stream); }));
+            } else {
+                GatherArgs ga{N, c->len_slot, qa, c->d_dep_bf16, c->d_X};
+                HWR_HIP(c, timed(c, HWR_K_GATHER, [&] { return launch_gather(ga, c->stream); }));
+                ma.X = c->d_X;
+                ma.cand_ttft = ctt ? ctt : c->d_ctt;
+                ma.cand_tpot = ctp ? ctp : c->d_ctp;
+                ma.cand_nout = cno ? cno : c->d_cno;
+                HWR_HIP(c, timed(c, HWR_K_MLP, [&] { return launch_mlp_bf16(c->H, true, ma, c->stream); }));
+            }
         } else {
             MlpF32Args fa{};
             fa.N = N;
@@ -595,7 +633,9 @@ hwr_status route_device(hwr_ctx *c, const DevBatch &b) {
         EpilogueArgs ea{};
         ea.N = N;
         ea.M = M;
-        ea.alpha = c->alpha;
+        ea.rule = c->rule;
+        ea.nw = c->nw;
+        for (int k = 0; k < c->nw; ++k) ea.w[k] = c->w[k];
         ea.q = qa;
         ea.dep_model = c->d_dep_model;
         ea.qmat = qmat;
@@ -630,12 +670,12 @@ hwr_status ensure_host_staging(hwr_ctx *c, size_t rows) {
     HWR_HIP(c, hipMalloc(&c->d_hemb, rows * c->D * esz));
     HWR_HIP(c, dev_alloc(&c->d_hlen, rows));
     HWR_HIP(c, dev_alloc(&c->d_hnout, rows));
-    HWR_HIP(c, dev_alloc(&c->d_hchoice, rows));
+    HWR_HIP(c, dev_alloc(&c->d_hchoice, rows * c->nw));
     HWR_HIP(c, dev_alloc(&c->d_hslo, rows));
-    HWR_HIP(c, dev_alloc(&c->d_hval, rows * 5));
+    HWR_HIP(c, dev_alloc(&c->d_hval, rows * c->nw * 5));
     HWR_HIP(c, dev_alloc(&c->d_hcand, rows * c->N * 3));
     HWR_HIP(c, dev_alloc(&c->d_hqual, rows * c->M));
-    HWR_HIP(c, dev_alloc(&c->d_hfeas, rows));
+    HWR_HIP(c, dev_alloc(&c->d_hfeas, rows * c->nw));
     c->hs_cap = rows;
     return HWR_OK;
 }
@@ -662,7 +702,8 @@ hwr_status route_host(hwr_ctx *c, const hwr_query_batch *q, hwr_route_result *r)
         b.nout = c->d_hnout;
         b.slo = q->slo_s ? c->d_hslo : nullptr;
         float *v = c->d_hval;
-        b.out = OutArgs{c->d_hchoice, c->d_hfeas, v, v + rows, v + 2 * rows, v + 3 * rows, v + 4 * rows};
+        const size_t vr = rows * c->nw;              // one [rows][nw] block per output
+        b.out = OutArgs{c->d_hchoice, c->d_hfeas, v, v + vr, v + 2 * vr, v + 3 * vr, v + 4 * vr};
         b.cand_ttft = r->cand_ttft ? c->d_hcand : nullptr;
         b.cand_tpot = r->cand_tpot ? c->d_hcand + rows * N : nullptr;
         b.cand_nout = r->cand_nout ? c->d_hcand + 2 * rows * N : nullptr;
@@ -672,13 +713,14 @@ hwr_status route_host(hwr_ctx *c, const hwr_query_batch *q, hwr_route_result *r)
         auto d2h = [&](void *dst, const void *src, size_t bytes) {
             return hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToHost, s);
         };
-        HWR_HIP(c, d2h(r->choice + off, c->d_hchoice, cn * 4));
-        if (r->feasible) HWR_HIP(c, d2h(r->feasible + off, c->d_hfeas, cn));
-        if (r->utility) HWR_HIP(c, d2h(r->utility + off, v, cn * 4));
-        if (r->e2e_s) HWR_HIP(c, d2h(r->e2e_s + off, v + rows, cn * 4));
-        if (r->ttft_s) HWR_HIP(c, d2h(r->ttft_s + off, v + 2 * rows, cn * 4));
-        if (r->tpot_s) HWR_HIP(c, d2h(r->tpot_s + off, v + 3 * rows, cn * 4));
-        if (r->nout) HWR_HIP(c, d2h(r->nout + off, v + 4 * rows, cn * 4));
+        const size_t oo = static_cast<size_t>(off) * c->nw, on = static_cast<size_t>(cn) * c->nw;
+        HWR_HIP(c, d2h(r->choice + oo, c->d_hchoice, on * 4));
+        if (r->feasible) HWR_HIP(c, d2h(r->feasible + oo, c->d_hfeas, on));
+        if (r->utility) HWR_HIP(c, d2h(r->utility + oo, v, on * 4));
+        if (r->e2e_s) HWR_HIP(c, d2h(r->e2e_s + oo, v + vr, on * 4));
+        if (r->ttft_s) HWR_HIP(c, d2h(r->ttft_s + oo, v + 2 * vr, on * 4));
+        if (r->tpot_s) HWR_HIP(c, d2h(r->tpot_s + oo, v + 3 * vr, on * 4));
+        if (r->nout) HWR_HIP(c, d2h(r->nout + oo, v + 4 * vr, on * 4));
         if (r->cand_ttft) HWR_HIP(c, d2h(r->cand_ttft + static_cast<size_t>(off) * N, c->d_hcand, static_cast<size_t>(cn) * N * 4));
         if (r->cand_tpot) HWR_HIP(c, d2h(r->cand_tpot + static_cast<size_t>(off) * N, c->d_hcand + rows * N, static_cast<size_t>(cn) * N * 4));
         if (r->cand_nout && c->NH == 3)
@@ -696,7 +738,8 @@ SingleArgs single_args(const hwr_ctx *c) {
     a.M = c->M;
     a.D = c->D;
     a.len_slot = c->len_slot;
-    a.alpha = c->alpha;
+    a.rule = c->rule;
+    a.w = c->w[0];
     a.b3_0 = c->b3[0];
     a.b3_1 = c->b3[1];
     a.b3_2 = c->b3[2];
@@ -860,7 +903,8 @@ hwr_status hwr_route_batch(hwr_ctx *c, const hwr_query_batch *q, hwr_route_resul
         if (q->slo_s && (!finite(q->slo_s[i]) || q->slo_s[i] <= 0.0f))
             return fail(c, HWR_ERR_INVALID_ARG, "slo_s must be finite and > 0");
     }
-    if (q->n == 1 && c->bf16 && !r->cand_ttft && !r->cand_tpot && !r->cand_nout && !r->cand_quality)
+    if (q->n == 1 && c->bf16 && c->nw == 1 && !r->cand_ttft && !r->cand_tpot && !r->cand_nout &&
+        !r->cand_quality)
         return route_single(c, q, r);
     return route_host(c, q, r);
 }

@@ -110,19 +110,46 @@ __device__ inline float div_bound(float c, const Bound &b) {
     return t;
 }
 
+// Per query and cost weight: the bound (when it is the same for every
+// candidate, with its reciprocal), the paper bound's a + b * input_len, and
+// the weight w with 1 - w (rounded once).
+struct QueryRule {
+    Bound bound;
+    float base, w, w1;
+};
+__device__ inline QueryRule query_rule(const Rule &R, float slo, int32_t input_len, float nout, float w) {
+    QueryRule q;
+    q.base = R.bound_paper ? __fmaf_rn(R.b, static_cast<float>(input_len), R.a) : 0.0f;
+    q.bound = make_bound(R.bound_paper ? __fmaf_rn(nout, R.tpot_slo, q.base) : slo);
+    q.w = w;
+    q.w1 = __fsub_rn(1.0f, w);
+    return q;
+}
+
 // Candidate decision values: cost (Eq. 2), bound test (Eq. 3) and utility,
 // each fp32 operation rounded once.
 struct Decision {
     float e2e, u;
     bool feasible;
 };
-__device__ inline Decision decide(float ttft, float tpot, float nout, const Bound &bound,
-                                  float quality, float alpha) {
+__device__ inline Decision decide(float ttft, float tpot, float nout, const Rule &R, const QueryRule &q,
+                                  float quality) {
     Decision r;
     r.e2e = __fmaf_rn(tpot, nout, ttft);
-    r.feasible = r.e2e <= bound.slo;
-    const float t = div_bound(r.e2e, bound);
-    r.u = __fsub_rn(quality, __fmul_rn(alpha, t));
+    const float B = R.per_cand ? __fmaf_rn(nout, R.tpot_slo, q.base) : q.bound.slo;
+    r.feasible = r.e2e <= B;
+    if (R.score_paper) {
+        r.u = __fsub_rn(__fmul_rn(q.w1, quality), __fmul_rn(q.w, r.e2e));
+    } else {
+        float t;
+        if (R.per_cand) {
+            asm volatile("");     // a real branch: the division stays off the other paths
+            t = __fdiv_rn(r.e2e, B);
+        } else {
+            t = div_bound(r.e2e, q.bound);
+        }
+        r.u = __fsub_rn(quality, __fmul_rn(q.w, t));
+    }
     return r;
 }
 
@@ -210,6 +237,7 @@ __device__ inline uint64_t group_max_u64(uint64_t k, int G) {
 
 __device__ inline void write_outputs(const OutArgs &o, int q, uint64_t key, float u,
                                      float e2e, float ttft, float tpot, float nout) {
+    if (!o.choice) return;        // decisions taken by a later kernel
     o.choice[q] = key_pair(key);
     if (o.feasible) o.feasible[q] = key_feasible(key) ? 1 : 0;
     if (o.utility) o.utility[q] = u;

@@ -22,6 +22,7 @@ constexpr int kMaxPairs = 1024;
 constexpr int kMaxModels = 32;
 constexpr int kMaxHeads = 3;     // predictor outputs: TTFT, TPOT and (optionally) N_out
 constexpr int kPartVals = 8;     // floats per split partial: u, C, TTFT, TPOT, N_out, pad
+constexpr int kMaxWeights = 8;   // cost weights scored in one call (HWR_MAX_WEIGHTS)
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -53,6 +54,14 @@ __device__ inline int key_pair(uint64_t k) { return 0x7FFFFFFF - static_cast<int
 __device__ inline bool key_feasible(uint64_t k) { return (k >> 63) != 0; }
 
 // ---------------------------------------------------------------- arguments
+// Decision rule of a launch (Sec. 3.1 score, Eq. 3 bound).
+struct Rule {
+    int score_paper;              // 1: u = (1 - w) Q - w C; 0: u = Q - w C / B
+    int bound_paper;              // 1: B = a + b * input_len + N_out * tpot_slo; 0: the query's SLO
+    int per_cand;                 // bound_paper with N_out predicted per candidate
+    float a, b, tpot_slo;
+};
+
 struct QueryArgs {
     int nq;                       // queries in this chunk
     const int32_t *input_len;     // [nq]
@@ -89,7 +98,8 @@ struct QualityArgs {
 struct MlpArgs {                  // bf16 predictor (fused or staged)
     int N, M, len_slot;
     int nheads;                   // 2, or 3: N_out predicted by the third head
-    float alpha;
+    Rule rule;
+    float w;                      // cost weight
     float b3_0, b3_1, b3_2;
     QueryArgs q;
     const uint16_t *dep_bf16;     // [N][32]
@@ -126,7 +136,9 @@ struct GatherArgs {
 struct EpilogueArgs {
     int N, M, group;              // group: lanes per query (power of two <= 64)
     int vec4;                     // 1: N % 4 == 0 and TTFT / TPOT rows 16-byte aligned
-    float alpha;
+    Rule rule;
+    int nw;                       // cost weights (>= 1); outputs are [nq][nw] when nw > 1
+    float w[kMaxWeights];
     QueryArgs q;
     const int32_t *dep_model;
     const float *qmat;
@@ -160,7 +172,8 @@ struct SingleOut {
 
 struct SingleArgs {
     int N, M, D, len_slot, arch_width, gpu_width, nheads;
-    float alpha, b3_0, b3_1, b3_2;
+    Rule rule;
+    float w, b3_0, b3_1, b3_2;
     const SingleIn *in;           // device-visible pinned record
     SingleOut *out;               // device-visible pinned record
     const hwr_hw_state *state;    // device-visible pinned copy of the current signals [N]

@@ -171,7 +171,8 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
     const int qmc = vme ? qme : 0;
     const int32_t nomy = a.q.nout ? a.q.nout[qmc] : 0;   // given N_out (two heads)
     const float nout = static_cast<float>(nomy < 0 ? 0 : nomy);
-    const Bound bound = make_bound(a.q.slo ? a.q.slo[qmc] : a.q.default_slo);
+    const QueryRule qrule = query_rule(a.rule, a.q.slo ? a.q.slo[qmc] : a.q.default_slo,
+                                       a.q.input_len[qmc], nout, a.w);
     // the input-length slot: k-block, lane half and element holding it
     const int ls_kb = a.len_slot >> 4, ls_h = (a.len_slot >> 3) & 1, ls_e = a.len_slot & 7;
     const bool patch = (h == ls_h);
@@ -368,7 +369,7 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
             }
             if (a.cand_nout && vme) a.cand_nout[ci] = nc;
             // ---- cost, bound test, utility, running argmax (Eq. 2, Eq. 3)
-            offer<NH == 3>(best, decide(tt, tp, nc, bound, Qd, a.alpha), d, tt, tp, nc);
+            offer<NH == 3>(best, decide(tt, tp, nc, a.rule, qrule, Qd), d, tt, tp, nc);
         }
     }
     if constexpr (!STAGED) {

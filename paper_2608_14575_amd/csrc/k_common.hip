@@ -162,7 +162,8 @@ hipError_t launch_gather(const GatherArgs &a, hipStream_t s) {
 // ------------------------------------------------------------ decision epilogue
 // Per query: cost (Eq. 2), bound test and utility for every pair, then the
 // Eq. 3 argmax as a maximum of packed decision keys over the `group` lanes
-// that share the query.  A lane takes up to kEpiSlices slices of the row
+// that share the query -- once per cost weight (a lambda sweep reuses the
+// loaded predictions; outputs are then [query][weight]).  A lane takes up to kEpiSlices slices of the row
 // (4 pairs each with 16-byte loads when rows are aligned, else 1 pair); the
 // models of its pairs are the same for every query, so they are loaded
 // alongside.  Each wave stages the quality rows of its own queries in LDS
@@ -171,8 +172,13 @@ hipError_t launch_gather(const GatherArgs &a, hipStream_t s) {
 // again.
 constexpr int kEpiSlices = 4;
 
-template <bool V4, bool PN>
+// Template switches: V4 16-byte loads; PN N_out per candidate; MULTI several
+// cost weights; GEN a rule other than the default (normalised score, given
+// bound), whose branches the default kernel then leaves out.
+template <bool V4, bool PN, bool MULTI, bool GEN>
 __global__ __launch_bounds__(256) void k_epilogue(EpilogueArgs a) {
+    Rule rule = a.rule;
+    if constexpr (!GEN) rule = Rule{};
     extern __shared__ float s_qm[];            // [4 waves][64 / G][M] quality rows
     const int G = a.group;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = tid & (G - 1);
@@ -213,7 +219,8 @@ __global__ __launch_bounds__(256) void k_epilogue(EpilogueArgs a) {
     }
     const int32_t no = pn ? 0 : a.q.nout[qc];
     const float nout = static_cast<float>(no < 0 ? 0 : no);
-    const Bound bound = make_bound(a.q.slo ? a.q.slo[qc] : a.q.default_slo);
+    const float slo = a.q.slo ? a.q.slo[qc] : a.q.default_slo;
+    const int32_t len = GEN ? a.q.input_len[qc] : 0;
     float *s_qw = s_qm + wave * qpw * a.M;
     const int nqw = max(0, min(qpw, a.q.nq - qw0));
     for (int i = lane; i < nqw * a.M; i += 64) s_qw[i] = a.qmat[static_cast<size_t>(qw0) * a.M + i];
@@ -223,49 +230,72 @@ __global__ __launch_bounds__(256) void k_epilogue(EpilogueArgs a) {
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
     const float *qrow = s_qw + (lane / G) * a.M;
-    Best best = best_none();
-    auto consider = [&](int d, int model, float tt, float tp, float nc) {
-        const float n = pn ? nc : nout;
-        offer(best, decide(tt, tp, n, bound, qrow[model], a.alpha), d, tt, tp, n);
-    };
-    auto consider_slice = [&](int u, const f32x4 &tv, const f32x4 &pv, const f32x4 &nv, const int4 &mv) {
-        if (V4) {
-            consider(4 * u + 0, mv.x, tv[0], pv[0], nv[0]);
-            consider(4 * u + 1, mv.y, tv[1], pv[1], nv[1]);
-            consider(4 * u + 2, mv.z, tv[2], pv[2], nv[2]);
-            consider(4 * u + 3, mv.w, tv[3], pv[3], nv[3]);
-        } else {
-            consider(u, mv.x, tv[0], pv[0], nv[0]);
-        }
-    };
+    // one decision per cost weight, from the same loaded predictions
+    const int nw = MULTI ? a.nw : 1;
+    for (int kw = 0; kw < nw; ++kw) {
+        if constexpr (MULTI) {
+            // opaque per weight: otherwise every candidate's cost and bound
+            // are hoisted out of this loop and held in registers
 #pragma unroll
-    for (int j = 0; j < kEpiSlices; ++j) {
-        const int u = g + j * G;
-        if (valid && u < units) consider_slice(u, t4[j], p4[j], n4[j], m4[j]);
+            for (int j = 0; j < kEpiSlices; ++j) asm volatile("" : "+v"(t4[j]), "+v"(p4[j]), "+v"(n4[j]));
+        }
+        const QueryRule qrule = query_rule(rule, slo, len, nout, a.w[kw]);
+        Best best = best_none();
+        auto consider = [&](int d, int model, float tt, float tp, float nc) {
+            const float n = pn ? nc : nout;
+            offer(best, decide(tt, tp, n, rule, qrule, qrow[model]), d, tt, tp, n);
+        };
+        auto consider_slice = [&](int u, const f32x4 &tv, const f32x4 &pv, const f32x4 &nv, const int4 &mv) {
+            if (V4) {
+                consider(4 * u + 0, mv.x, tv[0], pv[0], nv[0]);
+                consider(4 * u + 1, mv.y, tv[1], pv[1], nv[1]);
+                consider(4 * u + 2, mv.z, tv[2], pv[2], nv[2]);
+                consider(4 * u + 3, mv.w, tv[3], pv[3], nv[3]);
+            } else {
+                consider(u, mv.x, tv[0], pv[0], nv[0]);
+            }
+        };
+#pragma unroll
+        for (int j = 0; j < kEpiSlices; ++j) {
+            const int u = g + j * G;
+            if (valid && u < units) consider_slice(u, t4[j], p4[j], n4[j], m4[j]);
+        }
+        for (int u = g + kEpiSlices * G; valid && u < units; u += G) {
+            f32x4 tv = {0, 0, 0, 0}, pv = {0, 0, 0, 0}, nv = {0, 0, 0, 0};
+            int4 mv = {0, 0, 0, 0};
+            load(u, tv, pv, nv, mv);
+            consider_slice(u, tv, pv, nv, mv);
+        }
+        const uint64_t k = best_key(best);
+        const uint64_t m = group_max_u64(k, G);
+        if (valid && k == m && k != 0)
+            write_outputs(a.out, q * nw + kw, k, best.u, best.e2e, best.tt, best.tp, best.n);
     }
-    for (int u = g + kEpiSlices * G; valid && u < units; u += G) {
-        f32x4 tv = {0, 0, 0, 0}, pv = {0, 0, 0, 0}, nv = {0, 0, 0, 0};
-        int4 mv = {0, 0, 0, 0};
-        load(u, tv, pv, nv, mv);
-        consider_slice(u, tv, pv, nv, mv);
-    }
-    const uint64_t k = best_key(best);
-    const uint64_t m = group_max_u64(k, G);
-    if (valid && k == m && k != 0) write_outputs(a.out, q, k, best.u, best.e2e, best.tt, best.tp, best.n);
+}
+
+template <bool V4, bool PN, bool MULTI, bool GEN>
+static void launch_epilogue_t(const EpilogueArgs &a, dim3 g, size_t lds, hipStream_t s) {
+    hipLaunchKernelGGL((k_epilogue<V4, PN, MULTI, GEN>), g, dim3(kBlock), lds, s, a);
 }
 
 hipError_t launch_epilogue(const EpilogueArgs &a, hipStream_t s) {
+    using Launch = void (*)(const EpilogueArgs &, dim3, size_t, hipStream_t);
+    static const Launch table[16] = {
+        launch_epilogue_t<false, false, false, false>, launch_epilogue_t<false, false, false, true>,
+        launch_epilogue_t<false, false, true, false>, launch_epilogue_t<false, false, true, true>,
+        launch_epilogue_t<false, true, false, false>, launch_epilogue_t<false, true, false, true>,
+        launch_epilogue_t<false, true, true, false>, launch_epilogue_t<false, true, true, true>,
+        launch_epilogue_t<true, false, false, false>, launch_epilogue_t<true, false, false, true>,
+        launch_epilogue_t<true, false, true, false>, launch_epilogue_t<true, false, true, true>,
+        launch_epilogue_t<true, true, false, false>, launch_epilogue_t<true, true, false, true>,
+        launch_epilogue_t<true, true, true, false>, launch_epilogue_t<true, true, true, true>,
+    };
     const int qpb = kBlock / a.group;
     const unsigned grid = static_cast<unsigned>((a.q.nq + qpb - 1) / qpb);
     const size_t lds = static_cast<size_t>(qpb) * a.M * 4;
-    const bool pn = a.cand_nout != nullptr;
-    if (a.vec4) {
-        if (pn) hipLaunchKernelGGL((k_epilogue<true, true>), dim3(grid), dim3(kBlock), lds, s, a);
-        else hipLaunchKernelGGL((k_epilogue<true, false>), dim3(grid), dim3(kBlock), lds, s, a);
-    } else {
-        if (pn) hipLaunchKernelGGL((k_epilogue<false, true>), dim3(grid), dim3(kBlock), lds, s, a);
-        else hipLaunchKernelGGL((k_epilogue<false, false>), dim3(grid), dim3(kBlock), lds, s, a);
-    }
+    const bool gen = a.rule.score_paper || a.rule.bound_paper;
+    const int idx = (a.vec4 ? 8 : 0) + (a.cand_nout ? 4 : 0) + (a.nw > 1 ? 2 : 0) + (gen ? 1 : 0);
+    table[idx](a, dim3(grid), lds, s);
     return hipGetLastError();
 }
 

@@ -155,7 +155,7 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
     const uint32_t seq = hdr[0];
     const int32_t len = static_cast<int32_t>(hdr[1]);
     const int32_t no = static_cast<int32_t>(hdr[2]);
-    const Bound bound = make_bound(__uint_as_float(hdr[3]));
+    const float slo = __uint_as_float(hdr[3]);
 
     // ---- phase 2: LDS stores, the feature rows, one barrier
 #pragma unroll
@@ -181,6 +181,7 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
     __syncthreads();
 
     const float nout = static_cast<float>(no < 0 ? 0 : no);
+    const QueryRule qrule = query_rule(a.rule, slo, len, nout, a.w);
     Best best = best_none();
     const int ntiles = (a.N + 31) / 32;
     for (int ct = 0; ct < ntiles; ++ct) {
@@ -319,7 +320,7 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
                 const float zz2 = s_z[0][n][2] + s_z[1][n][2] + s_z[2][n][2] + s_z[3][n][2];
                 nc = softplus_fast(zz2 + a.b3_2);
             }
-            offer(best, decide(tt, tp, nc, bound, s_q[model], a.alpha), d, tt, tp, nc);
+            offer(best, decide(tt, tp, nc, a.rule, qrule, s_q[model]), d, tt, tp, nc);
         }
         if (ct + 1 < ntiles) __syncthreads();
     }

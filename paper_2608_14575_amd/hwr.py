@@ -21,6 +21,9 @@ HWR_F32, HWR_BF16 = 0, 1
 HWR_MEM_DEVICE, HWR_MEM_HOST = 0, 1
 HWR_PIPE_FUSED, HWR_PIPE_STAGED = 0, 1
 HWR_FLAG_GRAPH = 1
+HWR_SCORE_NORMALIZED, HWR_SCORE_PAPER = 0, 1
+HWR_BOUND_GIVEN, HWR_BOUND_PAPER = 0, 1
+HWR_MAX_WEIGHTS = 8
 HWR_K_STATE, HWR_K_QUALITY, HWR_K_GATHER, HWR_K_MLP, HWR_K_EPILOGUE, HWR_K_FUSED, HWR_K_MERGE, HWR_K_SINGLE = range(8)
 HWR_K_COUNT = 8
 KERNEL_NAMES = ["state", "quality", "gather", "mlp", "epilogue", "fused", "merge", "single"]
@@ -55,10 +58,13 @@ class hwr_config(C.Structure):
                 ("feat_dim", C.c_int32), ("hidden", C.c_int32), ("emb_dtype", C.c_int32),
                 ("weight_dtype", C.c_int32), ("pipeline", C.c_int32), ("max_chunk", C.c_int32),
                 ("cost_weight", C.c_float), ("default_slo_s", C.c_float), ("device", C.c_int32),
-                ("flags", C.c_int32), ("n_heads", C.c_int32),
+                ("flags", C.c_int32), ("n_heads", C.c_int32), ("score_mode", C.c_int32),
+                ("bound_mode", C.c_int32), ("ttft_slo_a", C.c_float), ("ttft_slo_b", C.c_float),
+                ("tpot_slo", C.c_float), ("n_weights", C.c_int32),
                 ("dep_model", _i32p), ("dep_gpu", _i32p), ("model_arch", _i32p),
                 ("model_params_b", _f32p), ("wq", _vp), ("bq", _f32p), ("w1", _vp), ("b1", _f32p),
-                ("w2", _vp), ("b2", _f32p), ("w3", _vp), ("b3", _f32p), ("stream", _vp)]
+                ("w2", _vp), ("b2", _f32p), ("w3", _vp), ("b3", _f32p), ("cost_weights", _f32p),
+                ("stream", _vp)]
 
 
 class hwr_query_batch(C.Structure):
@@ -168,7 +174,8 @@ class Router:
                  w3, b3, arch_width: int, gpu_width: int, n_gpu_types: int, dtype: str,
                  cost_weight: float = 0.5, default_slo_s: float = 1.0, pipeline: str = "fused",
                  max_chunk: int = 65536, stream: int = 0, flags: int = 0, device: int = 0,
-                 n_heads: int = 2):
+                 n_heads: int = 2, score_mode: int = 0, bound_mode: int = 0, ttft_slo_a: float = 0.0,
+                 ttft_slo_b: float = 0.0, tpot_slo: float = 0.0, cost_weights=None):
         wdt = np.uint16 if dtype == "bf16" else np.float32
         keep = dict(dep_model=np.ascontiguousarray(dep_model, np.int32),
                     dep_gpu=np.ascontiguousarray(dep_gpu, np.int32),
@@ -193,6 +200,12 @@ class Router:
         cfg.max_chunk = int(max_chunk)
         cfg.cost_weight, cfg.default_slo_s = float(cost_weight), float(default_slo_s)
         cfg.device, cfg.flags, cfg.n_heads = int(device), int(flags), int(n_heads)
+        cfg.score_mode, cfg.bound_mode = int(score_mode), int(bound_mode)
+        cfg.ttft_slo_a, cfg.ttft_slo_b, cfg.tpot_slo = float(ttft_slo_a), float(ttft_slo_b), float(tpot_slo)
+        if cost_weights is not None:
+            keep["cost_weights"] = np.ascontiguousarray(cost_weights, np.float32).ravel()
+            cfg.n_weights = int(keep["cost_weights"].size)
+            cfg.cost_weights = keep["cost_weights"].ctypes.data_as(_f32p)
         for k in ("dep_model", "dep_gpu", "model_arch"):
             setattr(cfg, k, keep[k].ctypes.data_as(_i32p))
         for k in ("model_params_b", "bq", "b1", "b2", "b3"):
@@ -201,6 +214,7 @@ class Router:
             setattr(cfg, k, keep[k].ctypes.data)
         cfg.stream = int(stream)
         self.M, self.N, self.D, self.dtype, self.n_heads = M, N, D, dtype, int(n_heads)
+        self.n_weights = 1 if cost_weights is None else int(np.size(cost_weights))
         self.ctx = hwr_init(cfg)
 
     @classmethod
@@ -210,6 +224,8 @@ class Router:
         kw.setdefault("cost_weight", sp.cost_weight)
         kw.setdefault("default_slo_s", sp.slo_value)
         kw.setdefault("n_heads", sp.n_heads)
+        for k in ("score_mode", "bound_mode", "ttft_slo_a", "ttft_slo_b", "tpot_slo"):
+            kw.setdefault(k, getattr(sp, k))
         return cls(dep_model=pb.dep_model, dep_gpu=pb.dep_gpu, model_arch=pb.model_arch,
                    model_params_b=pb.model_params_b, wq=pb.wq_bits, bq=pb.bq, w1=pb.w1_bits,
                    b1=pb.b1, w2=pb.w2_bits, b2=pb.b2, w3=pb.w3_bits, b3=pb.b3,
@@ -256,10 +272,11 @@ class Router:
         il = np.ascontiguousarray(input_len, np.int32)
         no = None if expected_out_len is None else np.ascontiguousarray(expected_out_len, np.int32)
         slo = None if slo_s is None else np.ascontiguousarray(slo_s, np.float32)
-        out = dict(choice=np.full(n, -1, np.int32), feasible=np.zeros(n, np.uint8),
-                   utility=np.zeros(n, np.float32), e2e_s=np.zeros(n, np.float32),
-                   ttft_s=np.zeros(n, np.float32), tpot_s=np.zeros(n, np.float32),
-                   nout=np.zeros(n, np.float32))
+        shape = (n,) if self.n_weights == 1 else (n, self.n_weights)   # [n][K] with K weights
+        out = dict(choice=np.full(shape, -1, np.int32), feasible=np.zeros(shape, np.uint8),
+                   utility=np.zeros(shape, np.float32), e2e_s=np.zeros(shape, np.float32),
+                   ttft_s=np.zeros(shape, np.float32), tpot_s=np.zeros(shape, np.float32),
+                   nout=np.zeros(shape, np.float32))
         if candidates:
             out.update(cand_ttft=np.zeros((n, self.N), np.float32),
                        cand_tpot=np.zeros((n, self.N), np.float32),

@@ -60,6 +60,10 @@ B3_TARGET_TTFT_S = 0.2
 B3_TARGET_TPOT_S = 0.005
 B3_TARGET_NOUT = 288.0          # median of U{64..512}: the given N_out's median
 NOUT_HEAD_SCALE = 100.0         # weight scale of the N_out head (tokens per unit)
+# The paper's SLO form for the synthetic workloads: TTFT_SLO(p) = a + b p with
+# the 1.2x slack folded in (1.2 x (0.2 s + 5e-5 s/token)), TPOT_SLO = 6 ms
+# (about the 70th percentile of the calibrated TPOT predictions).
+PAPER_SLO = dict(bound_mode=1, ttft_slo_a=0.24, ttft_slo_b=6e-5, tpot_slo=0.006)
 
 
 @dataclass(frozen=True)
@@ -90,6 +94,13 @@ class Spec:
     overload_frac: float = 0.0
     walk_steps: int = 0
     n_heads: int = 2            # 3: the predictor also predicts N_out (Eq. 1)
+    # decision rule: score 0: u = Q - w C / B, 1: u = (1 - w) Q - w C (Sec. 3.1);
+    # bound 0: B = the query's SLO, 1: B = a + b p + N_out tpot_slo
+    score_mode: int = 0
+    bound_mode: int = 0
+    ttft_slo_a: float = 0.0
+    ttft_slo_b: float = 0.0
+    tpot_slo: float = 0.0
 
     @property
     def n_deployments(self) -> int:

@@ -34,16 +34,17 @@ def to_dev_inputs(qs, dtype: str):
     return emb, il, no, slo
 
 
-def dev_outputs(n: int, N: int, M: int, candidates: bool, heads: int = 2):
+def dev_outputs(n: int, N: int, M: int, candidates: bool, heads: int = 2, weights: int = 1):
     import torch
     dev = torch.device("cuda")
-    out = dict(choice=torch.full((n,), -1, dtype=torch.int32, device=dev),
-               feasible=torch.zeros(n, dtype=torch.uint8, device=dev),
-               utility=torch.zeros(n, dtype=torch.float32, device=dev),
-               e2e_s=torch.zeros(n, dtype=torch.float32, device=dev),
-               ttft_s=torch.zeros(n, dtype=torch.float32, device=dev),
-               tpot_s=torch.zeros(n, dtype=torch.float32, device=dev),
-               nout=torch.zeros(n, dtype=torch.float32, device=dev))
+    sh = (n,) if weights == 1 else (n, weights)
+    out = dict(choice=torch.full(sh, -1, dtype=torch.int32, device=dev),
+               feasible=torch.zeros(sh, dtype=torch.uint8, device=dev),
+               utility=torch.zeros(sh, dtype=torch.float32, device=dev),
+               e2e_s=torch.zeros(sh, dtype=torch.float32, device=dev),
+               ttft_s=torch.zeros(sh, dtype=torch.float32, device=dev),
+               tpot_s=torch.zeros(sh, dtype=torch.float32, device=dev),
+               nout=torch.zeros(sh, dtype=torch.float32, device=dev))
     if candidates:
         out.update(cand_ttft=torch.zeros((n, N), dtype=torch.float32, device=dev),
                    cand_tpot=torch.zeros((n, N), dtype=torch.float32, device=dev),
@@ -56,7 +57,7 @@ def dev_outputs(n: int, N: int, M: int, candidates: bool, heads: int = 2):
 def route_device(router: hwr.Router, qs, dtype: str, candidates: bool = True, with_slo: bool = True):
     import torch
     emb, il, no, slo = to_dev_inputs(qs, dtype)
-    out = dev_outputs(qs.n, router.N, router.M, candidates, router.n_heads)
+    out = dev_outputs(qs.n, router.N, router.M, candidates, router.n_heads, router.n_weights)
     router.route(emb, il, no, slo if with_slo else None, mem=hwr.HWR_MEM_DEVICE, **out)
     torch.cuda.synchronize()
     return {k: v.cpu().numpy() for k, v in out.items()}
@@ -66,10 +67,11 @@ def rtol_for(dtype: str) -> float:
     return 1e-2 if dtype == "bf16" else 1e-4
 
 
-def check(pb, state, qs, gpu: dict, rtol: float = None, query_ids=None) -> parity.ParityReport:
+def check(pb, state, qs, gpu: dict, rtol: float = None, query_ids=None, alpha=None) -> parity.ParityReport:
     sp = pb.spec
     rtol = rtol_for(sp.dtype) if rtol is None else rtol
-    orc = O.route_synth(pb, state, qs, candidates=True)
-    return parity.compare(gpu, orc, slo=qs.slo_s, alpha=sp.cost_weight, dep_model=pb.dep_model,
+    alpha = sp.cost_weight if alpha is None else alpha
+    orc = O.route_synth(pb, state, qs, candidates=True, alpha=alpha)
+    return parity.compare(gpu, orc, slo=qs.slo_s, alpha=alpha, dep_model=pb.dep_model,
                           rtol=rtol, emb=qs.emb, wq=pb.wq, bq=pb.bq, query_ids=query_ids,
-                          heads=sp.n_heads)
+                          heads=sp.n_heads, score_mode=sp.score_mode)

@@ -9,9 +9,11 @@ same way, and the cost C = TTFT + N_out * TPOT then carries two uncertain
 factors, so its share of the uncertainty below is doubled (k = 2, else 1).
 
 Decisions: floating point decides the choice, so the choice is compared
-exactly only where the oracle's decision is robust to errors of that size:
-  tau_c = rtol * (|Q_c| + k * alpha * C_c / SLO)      (utility uncertainty)
-  ambiguous_c = |C_c - SLO| <= k * rtol * C_c         (bound test uncertain)
+exactly only where the oracle's decision is robust to errors of that size
+(B_c is the candidate's bound: the query's SLO, or the paper form):
+  tau_c = rtol * (|Q_c| + k * alpha * C_c / B_c)      (utility uncertainty;
+          rtol * ((1 - alpha) |Q_c| + k * alpha * C_c) for the paper score)
+  ambiguous_c = |C_c - B_c| <= rtol * (k * C_c + B_c) (bound test uncertain)
 A query is *eligible* for a bit-exact choice when its winner b is not
 ambiguous, no ambiguous candidate could enter or leave the feasible set in a
 way that changes the winner, and every other competitor c has
@@ -56,7 +58,7 @@ class ParityReport:
 
 def compare(gpu: dict, orc, *, slo: np.ndarray, alpha: float, dep_model: np.ndarray, rtol: float,
             emb: np.ndarray = None, wq: np.ndarray = None, bq: np.ndarray = None,
-            query_ids=None, heads: int = 2) -> ParityReport:
+            query_ids=None, heads: int = 2, score_mode: int = 0) -> ParityReport:
     """gpu: dict of numpy outputs (choice, feasible, utility, e2e_s, ttft_s,
     tpot_s, optional cand_ttft / cand_tpot / cand_quality), rows aligned
     with the oracle result ``orc`` (oracle.OracleResult with candidates)."""
@@ -87,10 +89,14 @@ def compare(gpu: dict, orc, *, slo: np.ndarray, alpha: float, dep_model: np.ndar
     Q = orc.quality[:, dep_model].astype(np.float64)
     C = orc.cand_e2e.astype(np.float64)
     u = orc.cand_u.astype(np.float64)
-    S = slo.astype(np.float64)[:, None]
+    S = (orc.cand_bound.astype(np.float64) if getattr(orc, "cand_bound", None) is not None
+         else np.broadcast_to(slo.astype(np.float64)[:, None], C.shape))
     k = 2.0 if heads == 3 else 1.0
-    tau = rtol * (np.abs(Q) + k * alpha * C / S)
-    amb = np.abs(C - S) <= k * rtol * C
+    if score_mode == 1:
+        tau = rtol * ((1.0 - alpha) * np.abs(Q) + k * alpha * C)
+    else:
+        tau = rtol * (np.abs(Q) + k * alpha * C / S)
+    amb = np.abs(C - S) <= rtol * (k * C + S)
     feas = orc.cand_feasible.astype(bool)
     sure = feas & ~amb
     g_all = np.asarray(gpu["choice"]).astype(np.int64)

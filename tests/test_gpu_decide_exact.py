@@ -25,8 +25,11 @@ def _device():
 
 
 def _exact(out, pb, qs, alpha):
+    sp = pb.spec
     d = O.decide(pb.dep_model, out["cand_ttft"], out["cand_tpot"], out["cand_quality"],
-                 qs.expected_out_len, qs.slo_s, alpha, cand_nout=out.get("cand_nout"))
+                 qs.expected_out_len, qs.slo_s, alpha, cand_nout=out.get("cand_nout"),
+                 input_len=qs.input_len, score_mode=sp.score_mode, bound_mode=sp.bound_mode,
+                 ttft_slo_a=sp.ttft_slo_a, ttft_slo_b=sp.ttft_slo_b, tpot_slo=sp.tpot_slo)
     assert np.array_equal(out["choice"], d["choice"])
     assert np.array_equal(out["feasible"], d["feasible"])
     assert np.array_equal(out["utility"].view(np.int32), d["utility"].view(np.int32))

@@ -26,8 +26,8 @@ MUTATIONS = {
     "nout_head_ignored": ("NH == 3 ? orc_softplus(z[2]) : nout_given", "NH == 3 ? (float)q->expected_out_len[iq] : nout_given"),
     "nout_from_tpot_head": ("NH == 3 ? orc_softplus(z[2]) : nout_given", "NH == 3 ? orc_softplus(z[1]) : nout_given"),
     "cost_without_nout": ("fmaf(tpot, nout, ttft)", "(tpot + ttft)"),
-    "strict_bound": ("(c <= slo)", "(c < slo)"),
-    "utility_sign": ("float u = q - at;", "float u = q + at;"),
+    "strict_bound": ("(c <= bound)", "(c < bound)"),
+    "utility_sign": ("u = q - at;", "u = q + at;"),
     "ties_to_highest": ("(feas == best_f && u > best_u)", "(feas == best_f && u >= best_u)"),
     "bound_ignored": ("feas > best_f || ", ""),
     "wq_transposed": ("p->wq[(size_t)k * p->M + m]", "p->wq[(size_t)m * p->D + k]"),
@@ -37,6 +37,10 @@ MUTATIONS = {
     "softplus_sign": ("log1p(exp(-fabs(v)))", "log1p(exp(fabs(v)))"),
     "wrong_model_of_pair": ("qual[p->dep_model[d]]", "qual[d % M]"),
     "decide_cost_terms_swapped": ("fmaf(cand_tpot[ci], nout, cand_ttft[ci])", "fmaf(cand_ttft[ci], nout, cand_tpot[ci])"),
+    "paper_score_sign": ("u = wq - wc;", "u = wq + wc;"),
+    "paper_score_weights_swapped": ("const float w1 = 1.0f - r->w;", "const float w1 = r->w;"),
+    "paper_bound_drops_slope": ("fmaf(r->ttft_slo_b, (float)input_len, r->ttft_slo_a)", "r->ttft_slo_a"),
+    "paper_bound_drops_nout": ("return fmaf(nout, r->tpot_slo, base);", "return base + r->tpot_slo;"),
     "decide_model_of_pair": ("quality[(size_t)iq * M + dep_model[d]]", "quality[(size_t)iq * M + d % M]"),
 }
 

@@ -425,16 +425,27 @@ def _decide1(tt, tp, q_of_pair, nout, slo, alpha=0.5):
     return {k: v[0] for k, v in out.items()}
 
 
+RULES = {"normalised": {}, "paper score": dict(score_mode=1, cost_weight=0.3),
+         "paper bound": dict(S.PAPER_SLO), "paper both": dict(S.PAPER_SLO, score_mode=1, cost_weight=0.1)}
+
+
+def _rule_kw(sp):
+    return dict(score_mode=sp.score_mode, bound_mode=sp.bound_mode, ttft_slo_a=sp.ttft_slo_a,
+                ttft_slo_b=sp.ttft_slo_b, tpot_slo=sp.tpot_slo)
+
+
+@pytest.mark.parametrize("rule", sorted(RULES))
 @pytest.mark.parametrize("heads", [2, 3])
 @pytest.mark.parametrize("name,kw", [("C1", {}), ("C2", dict(n_queries=300)), ("C3", dict(n_queries=200))])
-def test_decide_reproduces_route(name, kw, heads):
+def test_decide_reproduces_route(name, kw, heads, rule):
     """Eq. 2 / Eq. 3 applied to the oracle's own predictions give the oracle's
     decisions bit for bit (the route itself is pinned by brute force)."""
-    sp = S.spec(name, n_heads=heads, **kw)
+    sp = S.spec(name, n_heads=heads, **kw, **RULES[rule])
     pb, st, qs = S.make_problem(sp, 7), S.make_state(sp, 7), S.make_queries(sp, 7)
     r = O.route_synth(pb, st, qs)
     d = O.decide(pb.dep_model, r.cand_ttft, r.cand_tpot, r.quality, qs.expected_out_len, qs.slo_s,
-                 sp.cost_weight, cand_nout=r.cand_nout if heads == 3 else None)
+                 sp.cost_weight, cand_nout=r.cand_nout if heads == 3 else None,
+                 input_len=qs.input_len, **_rule_kw(sp))
     assert np.array_equal(d["choice"], r.choice)
     assert np.array_equal(d["feasible"], r.feasible)
     assert np.array_equal(d["utility"].view(np.int32), r.utility.view(np.int32))
@@ -461,3 +472,65 @@ def test_decide_hand_cases():
     assert r["choice"] == 0
     r = _decide1([0.2, 0.05], [0.0, 0.0], [0.6, 0.55], 0, 1.0)  # 0.5 vs 0.525
     assert r["choice"] == 1
+
+
+# ---------------------------------------------------------------- paper score and bound
+def test_paper_score_hand_values():
+    """u = (1 - lambda) Q - lambda C (Sec. 3.1), each fp32 operation rounded
+    once: two candidates whose order flips with lambda."""
+    tt, tp, q = [0.5, 1.5], [0.0, 0.0], [0.2, 0.9]        # C = (0.5, 1.5), no N_out term
+    for lam, want in ((0.25, 1), (0.5, 0)):
+        d = O.decide(np.arange(2), np.array([tt], np.float32), np.array([tp], np.float32),
+                     np.array([q], np.float32), np.array([0]), np.array([10.0], np.float32), lam,
+                     score_mode=1)
+        w1 = np.float32(1.0) - np.float32(lam)
+        us = [np.float32(w1 * np.float32(qq)) - np.float32(np.float32(lam) * np.float32(cc))
+              for qq, cc in zip(q, [0.5, 1.5])]
+        assert d["choice"][0] == want == int(np.argmax(us))
+        assert d["utility"][0] == us[want]
+    # 0.75 * 0.2 - 0.25 * 0.5 = 0.025 < 0.75 * 0.9 - 0.25 * 1.5 = 0.3;  0.5 * 0.2 - 0.25 = -0.15 > -0.3
+
+
+@pytest.mark.parametrize("heads", [2, 3])
+def test_paper_score_end_points_are_textbook_argmax(heads):
+    """lambda = 0: the score is Q (argmax of quality among feasible pairs);
+    lambda = 1: it is -C (the fastest feasible pair).  numpy argmax/argmin
+    with the lowest-index tie rule."""
+    for lam, key in ((0.0, "q"), (1.0, "c")):
+        sp = S.spec("C2", n_queries=200, n_heads=heads, score_mode=1, cost_weight=lam)
+        pb, st, qs = S.make_problem(sp, 8), S.make_state(sp, 8), S.make_queries(sp, 8)
+        r = O.route_synth(pb, st, qs)
+        val = r.quality[:, pb.dep_model] if key == "q" else -r.cand_e2e
+        feas = r.cand_feasible.astype(bool)
+        for i in range(qs.n):
+            pool = np.where(feas[i])[0] if feas[i].any() else np.arange(pb.n_deployments)
+            assert r.choice[i] == pool[np.argmax(val[i, pool])], (lam, i)
+
+
+@pytest.mark.parametrize("heads", [2, 3])
+def test_paper_bound_closed_form(heads):
+    """B = a + b p + N_out tpot_slo (the evaluation's SLO with p input
+    tokens), two fused multiply-adds, for every candidate."""
+    sp = S.spec("C2", n_queries=100, n_heads=heads, **S.PAPER_SLO)
+    pb, st, qs = S.make_problem(sp, 9), S.make_state(sp, 9), S.make_queries(sp, 9)
+    r = O.route_synth(pb, st, qs)
+    p = qs.input_len.astype(np.float64)[:, None]
+    want = sp.ttft_slo_a + sp.ttft_slo_b * p + r.cand_nout.astype(np.float64) * sp.tpot_slo
+    np.testing.assert_allclose(r.cand_bound, want, rtol=3e-7)
+    assert np.array_equal(r.cand_feasible.astype(bool), r.cand_e2e <= r.cand_bound)
+    assert 0.2 < r.cand_feasible.mean() < 0.9
+
+
+def test_paper_bound_with_constant_terms_equals_given_slo():
+    """b = 0 and tpot_slo = 0 make the bound the constant a: the same
+    decisions, bit for bit, as the given-SLO rule with SLO = a."""
+    a = 1.7
+    sp_p = S.spec("C2", n_queries=150, bound_mode=1, ttft_slo_a=a, ttft_slo_b=0.0, tpot_slo=0.0)
+    sp_g = S.spec("C2", n_queries=150)
+    pb, st, qs = S.make_problem(sp_g, 10), S.make_state(sp_g, 10), S.make_queries(sp_g, 10)
+    rp = O.route(O.OracleProblem.from_synth(S.make_problem(sp_p, 10)), st, qs.emb, qs.input_len,
+                 qs.expected_out_len, qs.slo_s)
+    rg = O.route(O.OracleProblem.from_synth(pb), st, qs.emb, qs.input_len, qs.expected_out_len,
+                 np.full(qs.n, a, np.float32))
+    for k in ("choice", "feasible", "utility", "e2e_s"):
+        assert np.array_equal(getattr(rp, k), getattr(rg, k)), k
