@@ -169,17 +169,19 @@ PackedPredictor pack_predictor(const uint16_t *w1, const uint16_t *w2, const uin
     p.b1.assign(static_cast<size_t>(MT) * 2 * 16, 0.0f);
     p.b2.assign(static_cast<size_t>(MT) * 2 * 16, 0.0f);
     p.w3.assign(static_cast<size_t>(MT) * 2 * NH * 8, 0u);
-    // Head layer on MFMA (z^T = W3^T h2^T): A operand rows are the NH heads,
-    // k follows the layer-2 accumulator order like W2's.  Only lanes of rows
-    // 0..NH-1 hold data: [k-block][row m < NH][half h][8], then one zero
-    // fragment that every other lane reads.
-    p.w3frag.assign(static_cast<size_t>(KB2) * NH * 2 * 8 + 8, 0);
+    // Head layer on MFMA (z = W3^T h2^T, 16x16x32 tiles): an A-operand lane
+    // holds either the 8 weights of head m over the 8 hidden units that one
+    // layer-2 accumulator half h packs into a B operand, or zeros.  Per
+    // k-block: [head m][half h][8] for the 2 * NH data fragments, then one zero
+    // fragment (k_mlp_bf16 picks the fragment of each lane).
+    const int W3S = 2 * NH + 1;
+    p.w3frag.assign(static_cast<size_t>(KB2) * W3S * 8, 0);
     for (int kb = 0; kb < KB2; ++kb)
         for (int m = 0; m < NH; ++m)
             for (int h = 0; h < 2; ++h)
                 for (int j = 0; j < 8; ++j) {
                     const int hin = 32 * (kb >> 1) + crow(8 * (kb & 1) + j, h);
-                    p.w3frag[((static_cast<size_t>(kb) * NH + m) * 2 + h) * 8 + j] =
+                    p.w3frag[(static_cast<size_t>(kb) * W3S + m * 2 + h) * 8 + j] =
                         w3[static_cast<size_t>(hin) * NH + m];
                 }
     for (int mt = 0; mt < MT; ++mt)

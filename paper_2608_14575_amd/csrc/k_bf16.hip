@@ -20,6 +20,13 @@ __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
+// v_mfma_f32_16x16x32_bf16: A is 16 rows x 32 k, B 32 k x 16 columns; lane l
+// holds 8 consecutive-in-k values of row (A) / column (B) l & 15, k-group
+// l >> 4.  The accumulator holds column l & 15, rows 4 * (l >> 4) + 0..3.
+__device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
 __device__ __forceinline__ f32x16 bias_tile(const f32x4 *p) {
     const f32x4 a = p[0], b = p[1], c = p[2], d = p[3];
     return (f32x16){a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3],
@@ -34,16 +41,6 @@ __device__ __forceinline__ bf16x8 relu_pack8(const f32x16 &c, int base) {
     u[1] = __builtin_bit_cast(uint32_t, relu_bf16x2(c[base + 2], c[base + 3]));
     u[2] = __builtin_bit_cast(uint32_t, relu_bf16x2(c[base + 4], c[base + 5]));
     u[3] = __builtin_bit_cast(uint32_t, relu_bf16x2(c[base + 6], c[base + 7]));
-    return __builtin_bit_cast(bf16x8, u);
-}
-
-// Move each 32-bit element from lane i to lane i + 4 within every row of 16
-// lanes (DPP row_shr:4; lanes 0-3 of a row receive 0).
-__device__ __forceinline__ bf16x8 shift_rows4(bf16x8 v) {
-    u32x4 u = __builtin_bit_cast(u32x4, v);
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-        u[i] = static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(u[i]), 0x114, 0xF, 0xF, true));
     return __builtin_bit_cast(bf16x8, u);
 }
 
@@ -104,8 +101,8 @@ hipError_t launch_quality_bf16(const QualityArgs &a, hipStream_t s) {
 //        row (L1-resident) and each query's input-length feature;
 //   h1^T = ReLU(W1^T X^T + b1)  -> bf16, registers;
 //   h2^T = ReLU(W2^T h1^T + b2) -> bf16, per 32-row tile, each tile folded at
-//   once into the head layer z = W3^T h2^T + b3, itself an MFMA chain whose A
-//   fragments carry the two heads in rows 0-1 (tile 0) and 4-5 (tile 1);
+//   once into the head layer z = W3^T h2^T + b3, itself a chain of 16x16x32
+//   MFMAs that leaves each candidate's heads in the lane that decides it;
 //   TTFT = softplus(z0), TPOT = softplus(z1).
 // The layers are software-pipelined: a tile's MFMAs are issued before the
 // previous tile's VALU epilogue (bias, ReLU, bf16 packing), so the matrix
@@ -123,7 +120,8 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
     __shared__ bf16x8 s_w2[MT * KB2 * 64];
     __shared__ f32x4 s_b1[MT * 2 * 4];
     __shared__ f32x4 s_b2[MT * 2 * 4];
-    __shared__ bf16x8 s_w3f[KB2 * 2 * kMaxHeads + 1];
+    constexpr int W3S = 2 * NH + 1;   // head fragments per k-block (last: zeros)
+    __shared__ bf16x8 s_w3f[KB2 * W3S];
     __shared__ uint64_t s_mkey[kQPerBlock];
     __shared__ f32x4 s_mval[kQPerBlock];
     __shared__ float s_mnout[NH == 3 ? kQPerBlock : 1];
@@ -145,7 +143,7 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
         for (int i = tid; i < MT * 2 * 4; i += kMlpThreads) d[i] = g[i];
         g = reinterpret_cast<const uint4 *>(a.w3_frag);
         d = reinterpret_cast<uint4 *>(s_w3f);
-        for (int i = tid; i < KB2 * 2 * NH + 1; i += kMlpThreads) d[i] = g[i];
+        for (int i = tid; i < KB2 * W3S; i += kMlpThreads) d[i] = g[i];
     }
     __syncthreads();
 
@@ -185,6 +183,19 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
     const int d1 = static_cast<int>(span0 + (span1 - span0) * (grp + 1) / 2);
 
     Best best = best_none();
+
+    // Head-layer A fragment of this lane for column tile t (an index into a
+    // k-block's fragments): lane 16g + i holds row i, k-group g.  Row
+    // i = 8t + 4s + m is head m of sub-column s; it takes weights only from
+    // the k-groups whose B lanes carry sub-column s (g & 1 == s), namely the
+    // hidden-unit half g >> 1.  Every other lane reads the zero fragment.
+    int w3_sel[NT];
+    {
+        const int i = lane & 15, g = lane >> 4, m = i & 3, s = (i >> 2) & 1;
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+            w3_sel[t] = ((i >> 3) == t && m < NH && (g & 1) == s) ? m * 2 + (g >> 1) : 2 * NH;
+    }
 
     // Per-pair inputs are loaded one step ahead: the pair's feature row
     // (fused) or the candidates' feature rows (staged), and the quality
@@ -234,8 +245,8 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
         // LDS offsets made opaque per step: the weight fragments are
         // loop-invariant, and hoisting all of them out of the pair loop would
         // need far more registers than a lane has.
-        int lo = lane, ho = h;
-        asm volatile("" : "+v"(lo), "+v"(ho));
+        int lo = lane, ho = h, w3o0 = w3_sel[0], w3o1 = w3_sel[1];
+        asm volatile("" : "+v"(lo), "+v"(ho), "+v"(w3o0), "+v"(w3o1));
         // ---- features (Eq. 1), B operand of layer 1
         bf16x8 xf[NT][2];
         if constexpr (STAGED) {
@@ -296,15 +307,17 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
                 for (int t = 0; t < NT; ++t) c[t] = mfma32(w, h1[t][kb], c[t]);
             }
         };
-        // Head layer on the matrix pipe: z^T = W3^T h2^T.  Both column tiles
-        // share one accumulator: tile 0's A fragment holds the NH heads (2 or
-        // 3) in rows 0..NH-1, tile 1's the same values in rows 4..3+NH (a
-        // 4-lane shift), so lanes 0-31 end with tile 0's z and lanes 32-63
-        // with tile 1's, in accumulator elements 0..NH-1.  (Packed bf16 dot
-        // products would stall the matrix pipe: they do not co-issue with
-        // MFMA on gfx950.)
-        f32x16 acc3 = {};
-        const int w3_lane = (lo & 31) < NH ? (lo & 31) : -1;
+        // Head layer on the matrix pipe: z = W3^T h2^T on 16x16x32 tiles (the
+        // heads need few rows, and this shape takes the same B operand as the
+        // 32x32x16 one in half the cycles).  A 16x16x32 B operand reads lanes
+        // j, j + 16, j + 32, j + 48 as its column j: candidates j and j + 16 of
+        // the column tile, each split over two lanes (hidden-unit halves).  The
+        // A fragments (see w3_sel) keep them apart: tile t's row 8t + 4s + m is
+        // head m of candidate 32t + 16s + j, so after both tiles every lane
+        // holds its own candidate's heads in accumulator elements 0..NH-1.
+        // (Packed bf16 dot products would stall the matrix pipe: they do not
+        // co-issue with MFMA on gfx950.)
+        f32x4 acc3 = {};
         auto l2_epi = [&](int mo, const f32x16 (&c)[NT]) {
             bf16x8 h2[NT][2];
 #pragma unroll
@@ -315,10 +328,8 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
 #pragma unroll
             for (int b = 0; b < 2; ++b) {
                 const int kb = 2 * mo + b;
-                const bf16x8 f0 = s_w3f[w3_lane >= 0 ? (kb * NH + w3_lane) * 2 + ho : KB2 * 2 * NH];
-                const bf16x8 f1 = shift_rows4(f0);
-                acc3 = mfma32(f0, h2[0][b], acc3);
-                acc3 = mfma32(f1, h2[1][b], acc3);
+                acc3 = mfma16(s_w3f[kb * W3S + w3o0], h2[0][b], acc3);
+                acc3 = mfma16(s_w3f[kb * W3S + w3o1], h2[1][b], acc3);
             }
             asm volatile("" : "+v"(acc3));
         };
