@@ -249,6 +249,45 @@ def single_query(args, S, hwr, torch, flags=0):
             "timing": "host clock around hwr_route_batch (ctypes call included)"}
 
 
+def closed_loop(args, hwr, torch):
+    """The closed-loop serving simulation (include/hwr_sim.h) with the library
+    routing every step's arrivals: Table 3's pool of five models on two GPUs,
+    each arrival pattern at one rate, with the monitor's signals refreshed
+    every 250 ms (live) or held at the first snapshot (frozen).  Reports the
+    paper's Sec. 5 metrics and the host time of each routing call."""
+    from paper_2608_14575_amd import simload
+    keys = ("slo_attainment", "mean_latency_s", "p99_latency_s", "mean_ttft_s", "running_fraction",
+            "avg_load", "load_skew", "running_skew", "waiting_skew", "n_completed", "route_calls",
+            "route_us_p50", "route_us_p99")
+    out = {}
+    for pattern in simload.PATTERNS:
+        w = simload.make_sim(11, pattern, args.sim_rate, duration_s=args.sim_seconds, dtype="bf16")
+        row = {"requests": w.n_requests}
+        for mode, freeze in (("live", False), ("frozen", True)):
+            r = hwr.Router.from_problem(w.problem, stream=int(torch.cuda.current_stream().cuda_stream))
+            t0 = time.perf_counter()
+            o = hwr.simulate(r, pairs=w.pairs, n_gpus=w.n_gpus, tick_us=w.tick_us,
+                             monitor_period_us=w.monitor_period_us, max_time_us=w.max_time_us,
+                             prior_ttft_s=w.prior_ttft_s, prior_tpot_s=w.prior_tpot_s,
+                             arrival_us=w.arrival_us, input_len=w.input_len, output_len=w.output_len,
+                             slo_us=w.slo_us, emb=w.queries.emb_bits, emb_dtype=hwr.HWR_BF16,
+                             expected_out_len=w.queries.expected_out_len, freeze_state=freeze)
+            wall = time.perf_counter() - t0
+            r.close()
+            row[mode] = {k: o[k] for k in keys}
+            row[mode]["wall_s"] = wall
+        out[pattern] = row
+        log(f"closed loop {pattern} at {args.sim_rate} req/s: SLO attainment live "
+            f"{row['live']['slo_attainment']:.3f} / frozen {row['frozen']['slo_attainment']:.3f}, "
+            f"load skew {row['live']['load_skew']:.2f} / {row['frozen']['load_skew']:.2f}, "
+            f"routing call p50 {row['live']['route_us_p50']:.1f} us")
+    return {"workload": f"Table 3 pool (5 models, 2 GPUs), {args.sim_seconds:g} s of arrivals at "
+                        f"{args.sim_rate:g} req/s per pattern, 1 ms steps, monitor every 250 ms, "
+                        f"hand-set load-aware predictor 24-64-64-2 bf16, embed 384",
+            "timing": "host clock around each hwr_route_batch call of the simulation (host batches)",
+            "patterns": out}
+
+
 def cpu_baseline(pb, st, sample, sp):
     """The CPU oracle (plain C, one thread) on a bounded sample of the same
     workload: the first queries of chunk 0 against all pairs."""
@@ -291,6 +330,9 @@ def main() -> int:
     ap.add_argument("--cpu-sample", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-single", action="store_true")
+    ap.add_argument("--no-sim", action="store_true", help="skip the closed-loop simulation")
+    ap.add_argument("--sim-rate", type=float, default=21.0)
+    ap.add_argument("--sim-seconds", type=float, default=60.0)
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain device copy of known size (counter calibration)")
     args = ap.parse_args()
@@ -325,6 +367,7 @@ def main() -> int:
     if single:
         log(f"single query (kernel launch) p50 {single['p50_us']:.1f} us p99 {single['p99_us']:.1f} us; "
             f"(graph launch) p50 {single_graph['p50_us']:.1f} us p99 {single_graph['p99_us']:.1f} us")
+    sim = None if args.no_sim else closed_loop(args, hwr, torch)
     cpu = None if args.no_cpu_baseline else cpu_baseline(w["pb"], w["st"], w["sample"], w["sp"])
     line = {
         "metric": METRIC, "value": res["value"], "unit": "candidates/s", "n_gpus": 1,
@@ -334,7 +377,7 @@ def main() -> int:
         "config": res["config"], "roofline": res["roofline"], "cpu_baseline": cpu,
         "single_query": single, "single_query_graph_launch": single_graph,
         "quality_roofline": res["quality_roofline"], "stages": res["stages"],
-        "staged_pipeline": staged,
+        "staged_pipeline": staged, "closed_loop": sim,
     }
     print(json.dumps(line), flush=True)
     return 0

@@ -29,7 +29,7 @@ HWR_K_COUNT = 8
 KERNEL_NAMES = ["state", "quality", "gather", "mlp", "epilogue", "fused", "merge", "single"]
 
 EXPORTS = ["hwr_init", "hwr_update_hw_state", "hwr_route_batch", "hwr_free", "hwr_last_error",
-           "hwr_profile_enable", "hwr_profile_read"]
+           "hwr_profile_enable", "hwr_profile_read", "hwr_sim_run", "hwr_sim_last_error"]
 
 _STATUS = {0: "HWR_OK", -1: "HWR_ERR_INVALID_ARG", -2: "HWR_ERR_OOM", -3: "HWR_ERR_HIP",
            -4: "HWR_ERR_STATE", -5: "HWR_ERR_UNSUPPORTED"}
@@ -82,6 +82,44 @@ class hwr_kernel_times(C.Structure):
     _fields_ = [("ms", C.c_double * HWR_K_COUNT), ("launches", C.c_int64 * HWR_K_COUNT)]
 
 
+# ---- include/hwr_sim.h
+class hwr_sim_pair(C.Structure):
+    _fields_ = [("gpu", C.c_int32), ("max_running", C.c_int32), ("kv_capacity", C.c_int64),
+                ("prefill_base_us", C.c_int32), ("prefill_per_token_ns", C.c_int32),
+                ("tpot_base_us", C.c_int32), ("tpot_per_running_us", C.c_int32)]
+
+
+class hwr_sim_config(C.Structure):
+    _fields_ = [("n_pairs", C.c_int32), ("n_gpus", C.c_int32), ("pairs", _vp), ("tick_us", C.c_int32),
+                ("monitor_period_us", C.c_int32), ("max_time_us", C.c_int64), ("freeze_state", C.c_int32),
+                ("prior_ttft_s", _vp), ("prior_tpot_s", _vp)]
+
+
+class hwr_sim_requests(C.Structure):
+    _fields_ = [("n", C.c_int32), ("arrival_us", _vp), ("input_len", _vp), ("output_len", _vp),
+                ("slo_us", _vp), ("emb", _vp), ("embed_dim", C.c_int32), ("emb_dtype", C.c_int32),
+                ("expected_out_len", _vp), ("route_slo_s", _vp)]
+
+
+SIM_METRICS = ["n_samples", "end_us", "n_completed", "n_met_slo", "route_calls", "slo_attainment",
+               "mean_latency_s", "p50_latency_s", "p99_latency_s", "mean_ttft_s", "mean_running",
+               "mean_waiting", "running_fraction", "avg_load", "load_skew", "running_skew",
+               "waiting_skew", "mean_utility", "route_us_mean", "route_us_p50", "route_us_p99"]
+
+
+class hwr_sim_result(C.Structure):
+    _fields_ = ([("pair", _vp), ("utility", _vp), ("pred_e2e_s", _vp), ("first_token_us", _vp),
+                 ("finish_us", _vp), ("max_samples", C.c_int32), ("samples", _vp), ("n_samples", C.c_int32)]
+                + [(k, C.c_int64) for k in ("end_us", "n_completed", "n_met_slo", "route_calls")]
+                + [(k, C.c_double) for k in SIM_METRICS[5:]])
+
+
+hwr_sim_router_fn = C.CFUNCTYPE(C.c_int32, C.c_void_p, C.POINTER(hwr_hw_state), C.c_int32, C.c_int32,
+                                C.c_int32, _i32p, _f32p, _f32p)
+STATE_DTYPE = np.dtype([("running_q", "<i4"), ("waiting_q", "<i4"), ("kv_util", "<f4"),
+                        ("gpu_util", "<f4"), ("ttft_avg_s", "<f4"), ("tpot_avg_s", "<f4")])
+
+
 _lib = None
 
 
@@ -109,6 +147,11 @@ def load(path: Optional[str] = None) -> C.CDLL:
     L.hwr_profile_enable.argtypes = [_vp, C.c_int32]
     L.hwr_profile_read.restype = C.c_int
     L.hwr_profile_read.argtypes = [_vp, C.POINTER(hwr_kernel_times), C.c_int32]
+    L.hwr_sim_run.restype = C.c_int
+    L.hwr_sim_run.argtypes = [_vp, C.POINTER(hwr_sim_config), C.POINTER(hwr_sim_requests),
+                              hwr_sim_router_fn, _vp, C.POINTER(hwr_sim_result)]
+    L.hwr_sim_last_error.restype = C.c_char_p
+    L.hwr_sim_last_error.argtypes = []
     if path is None:
         _lib = L
     return L
@@ -285,3 +328,74 @@ class Router:
                 out["cand_nout"] = np.zeros((n, self.N), np.float32)
         self.route(emb, il, no, slo, mem=HWR_MEM_HOST, **out)
         return out
+
+
+# ---------------------------------------------------------------- simulator
+def simulate(ctx, *, pairs: np.ndarray, n_gpus: int, tick_us: int, monitor_period_us: int,
+             max_time_us: int, prior_ttft_s, prior_tpot_s, arrival_us, input_len, output_len, slo_us,
+             emb=None, emb_dtype: int = HWR_BF16, expected_out_len=None, route_slo_s=None,
+             freeze_state: bool = False, router=None, max_samples: int = 0) -> dict:
+    """hwr_sim_run (include/hwr_sim.h).  ``ctx``: a Router or an hwr context
+    handle routes through the library; or ``router(snapshot, r0, r1)`` -- a
+    Python callable given the cached snapshot (STATE_DTYPE [N]) that returns
+    (choice, utility, e2e_s) for requests [r0, r1) -- with ctx None.  ``pairs``
+    has the hwr_sim_pair layout (simload.PAIR_DTYPE).  Returns the per-request
+    outputs, the stored snapshots and the metrics."""
+    if isinstance(ctx, Router):
+        ctx = ctx.ctx
+    N = int(pairs.shape[0])
+    R = int(np.shape(arrival_us)[0])
+    keep = dict(pairs=np.ascontiguousarray(pairs), pt=np.ascontiguousarray(prior_ttft_s, np.float32),
+                pp=np.ascontiguousarray(prior_tpot_s, np.float32),
+                arr=np.ascontiguousarray(arrival_us, np.int64), il=np.ascontiguousarray(input_len, np.int32),
+                ol=np.ascontiguousarray(output_len, np.int32), slo=np.ascontiguousarray(slo_us, np.int64))
+    if keep["pairs"].dtype.itemsize != C.sizeof(hwr_sim_pair):
+        raise ValueError("pairs must have the hwr_sim_pair layout")
+    cfg = hwr_sim_config(N, int(n_gpus), keep["pairs"].ctypes.data, int(tick_us), int(monitor_period_us),
+                         int(max_time_us), int(bool(freeze_state)), keep["pt"].ctypes.data,
+                         keep["pp"].ctypes.data)
+    req = hwr_sim_requests()
+    req.n = R
+    req.arrival_us, req.input_len = keep["arr"].ctypes.data, keep["il"].ctypes.data
+    req.output_len, req.slo_us = keep["ol"].ctypes.data, keep["slo"].ctypes.data
+    if emb is not None:
+        keep["emb"] = np.ascontiguousarray(emb, np.uint16 if emb_dtype == HWR_BF16 else np.float32)
+        req.emb, req.embed_dim, req.emb_dtype = keep["emb"].ctypes.data, int(keep["emb"].shape[1]), int(emb_dtype)
+    if expected_out_len is not None:
+        keep["no"] = np.ascontiguousarray(expected_out_len, np.int32)
+        req.expected_out_len = keep["no"].ctypes.data
+    if route_slo_s is not None:
+        keep["rslo"] = np.ascontiguousarray(route_slo_s, np.float32)
+        req.route_slo_s = keep["rslo"].ctypes.data
+    out = dict(pair=np.full(R, -1, np.int32), utility=np.zeros(R, np.float32),
+               pred_e2e_s=np.zeros(R, np.float32), first_token_us=np.full(R, -1, np.int64),
+               finish_us=np.full(R, -1, np.int64), samples=np.zeros((max(max_samples, 0), N), STATE_DTYPE))
+    res = hwr_sim_result()
+    for k in ("pair", "utility", "pred_e2e_s", "first_token_us", "finish_us", "samples"):
+        setattr(res, k, out[k].ctypes.data)
+    res.max_samples = int(max_samples)
+    errors = []
+
+    def _cb(user, snap, n_pairs, r0, r1, choice, utility, e2e):
+        try:
+            st = np.ctypeslib.as_array(C.cast(snap, C.POINTER(C.c_uint8)), (n_pairs * 24,)).view(STATE_DTYPE).copy()
+            ch, u, c = router(st, int(r0), int(r1))
+            n = r1 - r0
+            np.ctypeslib.as_array(choice, (n,))[:] = ch
+            np.ctypeslib.as_array(utility, (n,))[:] = u
+            np.ctypeslib.as_array(e2e, (n,))[:] = c
+            return 0
+        except Exception as ex:    # reported after the call returns
+            errors.append(ex)
+            return 1
+
+    cb = hwr_sim_router_fn(_cb) if router is not None else hwr_sim_router_fn()
+    st = load().hwr_sim_run(ctx, C.byref(cfg), C.byref(req), cb, None, C.byref(res))
+    if errors:
+        raise errors[0]
+    if st != HWR_OK:
+        raise HwrError(st, load().hwr_sim_last_error().decode())
+    for k in SIM_METRICS:
+        out[k] = getattr(res, k)
+    out["samples"] = out["samples"][:min(res.n_samples, max(max_samples, 0))]
+    return out

@@ -1,7 +1,8 @@
 """C-ABI contract checks that need no GPU: the library loads and exports every
-function include/hwr.h declares, the ctypes structures match the C layout,
+function include/*.h declares, the ctypes structures match the C layout,
 and argument errors come back as status codes (no device touched)."""
 import ctypes as C
+import glob
 import os
 import re
 import subprocess
@@ -12,7 +13,7 @@ import pytest
 from paper_2608_14575_amd import hwr
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "hwr.h")
+HEADERS = sorted(glob.glob(os.path.join(ROOT, "include", "*.h")))
 
 
 @pytest.fixture(scope="module")
@@ -24,8 +25,11 @@ def lib():
 
 
 def _declared():
-    txt = open(HEADER).read()
-    return sorted(set(re.findall(r"^\s*(?:hwr_status|void|const char \*)\s*(hwr_\w+)\s*\(", txt, re.M)))
+    names = set()
+    for h in HEADERS:
+        txt = open(h).read()
+        names |= set(re.findall(r"^\s*(?:hwr_status|void|const char \*)\s*(hwr_\w+)\s*\(", txt, re.M))
+    return sorted(names)
 
 
 def test_every_declared_symbol_is_exported(lib):
@@ -47,8 +51,13 @@ def test_struct_layout_matches_header(tmp_path):
         "hwr_query_batch": [f for f, _ in hwr.hwr_query_batch._fields_],
         "hwr_route_result": [f for f, _ in hwr.hwr_route_result._fields_],
         "hwr_kernel_times": [f for f, _ in hwr.hwr_kernel_times._fields_],
+        "hwr_sim_pair": [f for f, _ in hwr.hwr_sim_pair._fields_],
+        "hwr_sim_config": [f for f, _ in hwr.hwr_sim_config._fields_],
+        "hwr_sim_requests": [f for f, _ in hwr.hwr_sim_requests._fields_],
+        "hwr_sim_result": [f for f, _ in hwr.hwr_sim_result._fields_],
     }
-    src = ['#include <stdio.h>', '#include <stddef.h>', '#include "hwr.h"', "int main(void) {"]
+    src = ['#include <stdio.h>', '#include <stddef.h>', '#include "hwr.h"', '#include "hwr_sim.h"',
+           "int main(void) {"]
     for s, fl in fields.items():
         src.append(f'printf("{s} sizeof %zu\\n", sizeof({s}));')
         for f in fl:
