@@ -224,3 +224,18 @@ def test_live_state_balances_the_pool_better_than_a_frozen_one():
     assert live["running_fraction"] > frozen["running_fraction"]
     assert live["slo_attainment"] > frozen["slo_attainment"]
     assert live["mean_latency_s"] < frozen["mean_latency_s"]
+
+
+def test_empty_request_stream_and_zero_horizon():
+    pairs = one_pair()
+    base = dict(pairs=pairs, n_gpus=1, tick_us=1000, monitor_period_us=250_000,
+                prior_ttft_s=np.full(1, 0.1, np.float32), prior_tpot_s=np.full(1, 0.01, np.float32),
+                arrival_us=np.zeros(0, np.int64), input_len=np.zeros(0, np.int32),
+                output_len=np.zeros(0, np.int32), slo_us=np.zeros(0, np.int64))
+    out = hwr.simulate(None, **base, max_time_us=10**6, router=fixed_router(0), max_samples=10)
+    assert out["n_completed"] == 0 and out["route_calls"] == 0 and out["slo_attainment"] == 0.0
+    assert out["n_samples"] == 1 and out["end_us"] == 1000
+    out = hwr.simulate(None, **dict(base, arrival_us=np.zeros(1, np.int64), input_len=np.ones(1, np.int32),
+                                    output_len=np.ones(1, np.int32), slo_us=np.zeros(1, np.int64)),
+                       max_time_us=0, router=fixed_router(0))
+    assert out["n_samples"] == 0 and out["route_calls"] == 0 and out["finish_us"][0] == -1
