@@ -260,9 +260,12 @@ def closed_loop(args, hwr, torch):
             "avg_load", "load_skew", "running_skew", "waiting_skew", "n_completed", "route_calls",
             "route_us_p50", "route_us_p99")
     out = {}
-    for pattern in simload.PATTERNS:
-        w = simload.make_sim(11, pattern, args.sim_rate, duration_s=args.sim_seconds, dtype="bf16")
-        row = {"requests": w.n_requests}
+    runs = [(p, args.sim_rate) for p in simload.PATTERNS]
+    runs += [("sustained_overload", float(x)) for x in args.sim_overload_rates.split(",") if x
+             and float(x) != args.sim_rate]
+    for pattern, rate in runs:
+        w = simload.make_sim(11, pattern, rate, duration_s=args.sim_seconds, dtype="bf16")
+        row = {"requests": w.n_requests, "rate": rate}
         for mode, freeze in (("live", False), ("frozen", True)):
             r = hwr.Router.from_problem(w.problem, stream=int(torch.cuda.current_stream().cuda_stream))
             t0 = time.perf_counter()
@@ -276,13 +279,14 @@ def closed_loop(args, hwr, torch):
             r.close()
             row[mode] = {k: o[k] for k in keys}
             row[mode]["wall_s"] = wall
-        out[pattern] = row
-        log(f"closed loop {pattern} at {args.sim_rate} req/s: SLO attainment live "
+        out[pattern if rate == args.sim_rate else f"{pattern}@{rate:g}"] = row
+        log(f"closed loop {pattern} at {rate} req/s: SLO attainment live "
             f"{row['live']['slo_attainment']:.3f} / frozen {row['frozen']['slo_attainment']:.3f}, "
             f"load skew {row['live']['load_skew']:.2f} / {row['frozen']['load_skew']:.2f}, "
             f"routing call p50 {row['live']['route_us_p50']:.1f} us")
     return {"workload": f"Table 3 pool (5 models, 2 GPUs), {args.sim_seconds:g} s of arrivals at "
-                        f"{args.sim_rate:g} req/s per pattern, 1 ms steps, monitor every 250 ms, "
+                        f"{args.sim_rate:g} req/s per pattern (sustained overload also at "
+                        f"{args.sim_overload_rates} req/s), 1 ms steps, monitor every 250 ms, "
                         f"hand-set load-aware predictor 24-64-64-2 bf16, embed 384",
             "timing": "host clock around each hwr_route_batch call of the simulation (host batches)",
             "patterns": out}
@@ -333,6 +337,8 @@ def main() -> int:
     ap.add_argument("--no-sim", action="store_true", help="skip the closed-loop simulation")
     ap.add_argument("--sim-rate", type=float, default=21.0)
     ap.add_argument("--sim-seconds", type=float, default=60.0)
+    ap.add_argument("--sim-overload-rates", default="15,18,21",
+                    help="extra sustained-overload arrival rates (the paper sweeps 15, 18, 21 req/s)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain device copy of known size (counter calibration)")
     args = ap.parse_args()

@@ -206,7 +206,9 @@ void hwr_free(hwr_ctx *ctx);
  * thread when ctx is NULL.  Never NULL; owned by the library. */
 const char *hwr_last_error(const hwr_ctx *ctx);
 
-/* Kernel timing (HIP events around every launch, on the context's stream).
+/* Kernel timing: each kernel launch carries two HIP events that its dispatch
+ * records at the kernel's start and end, on the stream it runs on (a graph
+ * launch of the single-query path is bracketed by events instead).
  * Indices of hwr_kernel_times.ms / launches: */
 enum {
     HWR_K_STATE = 0, HWR_K_QUALITY = 1, HWR_K_GATHER = 2, HWR_K_MLP = 3,

@@ -16,6 +16,14 @@
 
 using namespace hwr;
 
+namespace hwr {
+// Kernel-timing events of the next launch on this thread (see launch_kernel).
+LaunchEvents &launch_events() {
+    thread_local LaunchEvents ev;
+    return ev;
+}
+}  // namespace hwr
+
 namespace {
 
 thread_local std::string g_init_error;
@@ -228,8 +236,27 @@ hipEvent_t take_event(hwr_ctx *c) {
     return e;
 }
 
+// Time one kernel launch of the library: the two events go into its dispatch
+// (launch_kernel), so they mark the kernel's own start and end on the stream.
 template <class F>
 hipError_t timed_on(hwr_ctx *c, hipStream_t s, int kind, F &&launch) {
+    if (!c->prof) return launch();
+    hipEvent_t a = take_event(c), b = take_event(c);
+    if (!a || !b) return hipErrorOutOfMemory;
+    LaunchEvents &ev = launch_events();
+    ev = LaunchEvents{a, b, false};
+    const hipError_t e = launch();
+    const bool used = ev.used;
+    ev = LaunchEvents{};
+    if (e != hipSuccess) return e;
+    if (!used) return hipErrorInvalidValue;   // every timed launch is one library kernel
+    c->pending.push_back({kind, a, b});
+    return hipSuccess;
+}
+
+// Time a graph launch: events recorded on the stream before and after it.
+template <class F>
+hipError_t timed_bracket(hwr_ctx *c, hipStream_t s, int kind, F &&launch) {
     if (!c->prof) return launch();
     hipEvent_t a = take_event(c), b = take_event(c);
     if (!a || !b) return hipErrorOutOfMemory;
@@ -799,7 +826,7 @@ hwr_status route_single(hwr_ctx *c, const hwr_query_batch *q, hwr_route_result *
     in->seq = seq;
     std::atomic_thread_fence(std::memory_order_release);
     if (c->gexec) {
-        HWR_HIP(c, timed_on(c, c->sstream, HWR_K_SINGLE, [&] { return hipGraphLaunch(c->gexec, c->sstream); }));
+        HWR_HIP(c, timed_bracket(c, c->sstream, HWR_K_SINGLE, [&] { return hipGraphLaunch(c->gexec, c->sstream); }));
     } else {
         const SingleArgs a = single_args(c);
         HWR_HIP(c, timed_on(c, c->sstream, HWR_K_SINGLE, [&] { return launch_single(c->H, a, c->sstream); }));

@@ -2,6 +2,7 @@
 // libhwr (gfx950 only).  Nothing here is part of the public C ABI.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cstddef>
@@ -31,6 +32,29 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef short i16x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// Kernel-timing events for the next launch on this thread.  When set (the
+// host runtime sets them around each timed launch), the launch hands them to
+// the dispatch, which records the kernel's own start and end (not the gap
+// before it), and marks them used.
+struct LaunchEvents {
+    hipEvent_t start = nullptr, stop = nullptr;
+    bool used = false;
+};
+LaunchEvents &launch_events();
+
+// Every kernel of the library is launched through this.
+template <typename... Args, typename F = void (*)(Args...)>
+inline hipError_t launch_kernel(F kernel, dim3 grid, dim3 block, uint32_t shm, hipStream_t s, Args... args) {
+    LaunchEvents &ev = launch_events();
+    if (ev.start) {
+        hipExtLaunchKernelGGL(kernel, grid, block, shm, s, ev.start, ev.stop, 0u, args...);
+        ev.used = true;
+    } else {
+        hipLaunchKernelGGL(kernel, grid, block, shm, s, args...);
+    }
+    return hipGetLastError();
+}
 
 // Row of output element r (0..15) held by a lane of half h (lane >> 5) in the
 // accumulator of a 32x32 MFMA; the column is lane & 31.

@@ -86,8 +86,7 @@ __global__ __launch_bounds__(256) void k_quality_bf16(QualityArgs a) {
 }
 
 hipError_t launch_quality_bf16(const QualityArgs &a, hipStream_t s) {
-    hipLaunchKernelGGL(k_quality_bf16, dim3((a.nq + 127) / 128), dim3(256), 0, s, a);
-    return hipGetLastError();
+    return launch_kernel(k_quality_bf16, dim3((a.nq + 127) / 128), dim3(256), 0, s, a);
 }
 
 // ------------------------------------------------------------ predictor
@@ -426,14 +425,11 @@ template <int H>
 static hipError_t launch_mlp_h(bool staged, const MlpArgs &a, hipStream_t s) {
     const dim3 grid((a.q.nq + kQPerBlock - 1) / kQPerBlock, staged ? 1 : a.nsplit);
     const dim3 block(kMlpThreads);
-    if (a.nheads == 3) {
-        if (staged) hipLaunchKernelGGL((k_mlp_bf16<H, true, 3>), grid, block, 0, s, a);
-        else hipLaunchKernelGGL((k_mlp_bf16<H, false, 3>), grid, block, 0, s, a);
-    } else {
-        if (staged) hipLaunchKernelGGL((k_mlp_bf16<H, true, 2>), grid, block, 0, s, a);
-        else hipLaunchKernelGGL((k_mlp_bf16<H, false, 2>), grid, block, 0, s, a);
-    }
-    return hipGetLastError();
+    if (a.nheads == 3)
+        return staged ? launch_kernel(k_mlp_bf16<H, true, 3>, grid, block, 0, s, a)
+                      : launch_kernel(k_mlp_bf16<H, false, 3>, grid, block, 0, s, a);
+    return staged ? launch_kernel(k_mlp_bf16<H, true, 2>, grid, block, 0, s, a)
+                  : launch_kernel(k_mlp_bf16<H, false, 2>, grid, block, 0, s, a);
 }
 
 hipError_t launch_mlp_bf16(int H, bool staged, const MlpArgs &a, hipStream_t s) {

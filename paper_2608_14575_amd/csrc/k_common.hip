@@ -25,8 +25,7 @@ __global__ __launch_bounds__(256) void k_state(StateArgs a) {
 }
 
 hipError_t launch_state(const StateArgs &a, hipStream_t s) {
-    hipLaunchKernelGGL(k_state, dim3((a.N + 255) / 256), dim3(256), 0, s, a);
-    return hipGetLastError();
+    return launch_kernel(k_state, dim3((a.N + 255) / 256), dim3(256), 0, s, a);
 }
 
 // ------------------------------------------------------------ fp32 quality
@@ -45,9 +44,7 @@ __global__ __launch_bounds__(256) void k_quality_f32(QualityArgs a) {
 
 hipError_t launch_quality_f32(const QualityArgs &a, hipStream_t s) {
     const long total = static_cast<long>(a.nq) * a.M;
-    hipLaunchKernelGGL(k_quality_f32, dim3(static_cast<unsigned>((total + 255) / 256)), dim3(256), 0,
-                       s, a);
-    return hipGetLastError();
+    return launch_kernel(k_quality_f32, dim3(static_cast<unsigned>((total + 255) / 256)), dim3(256), 0, s, a);
 }
 
 // ------------------------------------------------------------ fp32 predictor
@@ -110,10 +107,9 @@ __global__ __launch_bounds__(256) void k_mlp_f32(MlpF32Args a) {
 hipError_t launch_mlp_f32(int H, const MlpF32Args &a, hipStream_t s) {
     const long total = static_cast<long>(a.q.nq) * a.N;
     const dim3 grid(static_cast<unsigned>((total + 255) / 256));
-    if (H == 64) hipLaunchKernelGGL(k_mlp_f32<64>, grid, dim3(256), 0, s, a);
-    else if (H == 128) hipLaunchKernelGGL(k_mlp_f32<128>, grid, dim3(256), 0, s, a);
-    else return hipErrorInvalidValue;
-    return hipGetLastError();
+    if (H == 64) return launch_kernel(k_mlp_f32<64>, grid, dim3(256), 0, s, a);
+    if (H == 128) return launch_kernel(k_mlp_f32<128>, grid, dim3(256), 0, s, a);
+    return hipErrorInvalidValue;
 }
 
 // ------------------------------------------------------------ feature gather
@@ -155,8 +151,7 @@ __global__ __launch_bounds__(256) void k_gather(GatherArgs a) {
 
 hipError_t launch_gather(const GatherArgs &a, hipStream_t s) {
     const unsigned grid = static_cast<unsigned>((a.q.nq + kGatherQ - 1) / kGatherQ);
-    hipLaunchKernelGGL(k_gather, dim3(grid), dim3(256), static_cast<size_t>(a.N) * 64, s, a);
-    return hipGetLastError();
+    return launch_kernel(k_gather, dim3(grid), dim3(256), static_cast<uint32_t>(a.N) * 64, s, a);
 }
 
 // ------------------------------------------------------------ decision epilogue
@@ -274,12 +269,12 @@ __global__ __launch_bounds__(256) void k_epilogue(EpilogueArgs a) {
 }
 
 template <bool V4, bool PN, bool MULTI, bool GEN>
-static void launch_epilogue_t(const EpilogueArgs &a, dim3 g, size_t lds, hipStream_t s) {
-    hipLaunchKernelGGL((k_epilogue<V4, PN, MULTI, GEN>), g, dim3(kBlock), lds, s, a);
+static hipError_t launch_epilogue_t(const EpilogueArgs &a, dim3 g, size_t lds, hipStream_t s) {
+    return launch_kernel(k_epilogue<V4, PN, MULTI, GEN>, g, dim3(kBlock), static_cast<uint32_t>(lds), s, a);
 }
 
 hipError_t launch_epilogue(const EpilogueArgs &a, hipStream_t s) {
-    using Launch = void (*)(const EpilogueArgs &, dim3, size_t, hipStream_t);
+    using Launch = hipError_t (*)(const EpilogueArgs &, dim3, size_t, hipStream_t);
     static const Launch table[16] = {
         launch_epilogue_t<false, false, false, false>, launch_epilogue_t<false, false, false, true>,
         launch_epilogue_t<false, false, true, false>, launch_epilogue_t<false, false, true, true>,
@@ -295,8 +290,7 @@ hipError_t launch_epilogue(const EpilogueArgs &a, hipStream_t s) {
     const size_t lds = static_cast<size_t>(qpb) * a.M * 4;
     const bool gen = a.rule.score_paper || a.rule.bound_paper;
     const int idx = (a.vec4 ? 8 : 0) + (a.cand_nout ? 4 : 0) + (a.nw > 1 ? 2 : 0) + (gen ? 1 : 0);
-    table[idx](a, dim3(grid), lds, s);
-    return hipGetLastError();
+    return table[idx](a, dim3(grid), lds, s);
 }
 
 // ------------------------------------------------------------ split merge
@@ -319,8 +313,7 @@ __global__ __launch_bounds__(256) void k_merge(MergeArgs a) {
 }
 
 hipError_t launch_merge(const MergeArgs &a, hipStream_t s) {
-    hipLaunchKernelGGL(k_merge, dim3((a.nq + 255) / 256), dim3(256), 0, s, a);
-    return hipGetLastError();
+    return launch_kernel(k_merge, dim3((a.nq + 255) / 256), dim3(256), 0, s, a);
 }
 
 }  // namespace hwr

@@ -344,12 +344,11 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
 
 hipError_t launch_single(int H, const SingleArgs &a, hipStream_t s) {
     switch (H) {
-        case 64: hipLaunchKernelGGL(k_single<64>, dim3(1), dim3(256), 0, s, a); break;
-        case 128: hipLaunchKernelGGL(k_single<128>, dim3(1), dim3(256), 0, s, a); break;
-        case 256: hipLaunchKernelGGL(k_single<256>, dim3(1), dim3(256), 0, s, a); break;
+        case 64: return launch_kernel(k_single<64>, dim3(1), dim3(256), 0, s, a);
+        case 128: return launch_kernel(k_single<128>, dim3(1), dim3(256), 0, s, a);
+        case 256: return launch_kernel(k_single<256>, dim3(1), dim3(256), 0, s, a);
         default: return hipErrorInvalidValue;
     }
-    return hipGetLastError();
 }
 
 }  // namespace hwr
