@@ -292,6 +292,61 @@ def closed_loop(args, hwr, torch):
             "patterns": out}
 
 
+def closed_loop_pareto(args, hwr, torch):
+    """The quality-latency trade-off of the paper's Fig. 4(a), in the closed
+    loop: sustained overload on Table 3's pool, one simulation per cost weight,
+    live and frozen monitor.  The quality of each served request is the
+    library's own Q for the chosen pair's model (one device batch with the
+    per-model quality output after the run)."""
+    from paper_2608_14575_amd import simload
+    w = simload.make_sim(12, "sustained_overload", args.pareto_rate, duration_s=args.sim_seconds, dtype="bf16")
+    dev = torch.device("cuda:0")
+    stream = int(torch.cuda.current_stream().cuda_stream)
+    q = w.queries
+    emb = torch.from_numpy(q.emb_bits.view(np.int16)).to(dev)
+    il = torch.from_numpy(q.input_len).to(dev)
+    no = torch.from_numpy(q.expected_out_len).to(dev)
+    R, M = w.n_requests, w.problem.wq.shape[1]
+    rows = []
+    for alpha in [float(x) for x in args.pareto_weights.split(",") if x]:
+        r = hwr.Router.from_problem(w.problem, cost_weight=alpha, stream=stream)
+        r.update(_idle_state(w, hwr))
+        qual = torch.empty((R, M), dtype=torch.float32, device=dev)
+        choice = torch.empty(R, dtype=torch.int32, device=dev)
+        r.route(emb, il, no, None, mem=hwr.HWR_MEM_DEVICE, choice=choice, cand_quality=qual)
+        torch.cuda.synchronize()
+        qual = qual.cpu().numpy()
+        row = {"cost_weight": alpha}
+        for mode, freeze in (("live", False), ("frozen", True)):
+            o = hwr.simulate(r, pairs=w.pairs, n_gpus=w.n_gpus, tick_us=w.tick_us,
+                             monitor_period_us=w.monitor_period_us, max_time_us=w.max_time_us,
+                             prior_ttft_s=w.prior_ttft_s, prior_tpot_s=w.prior_tpot_s,
+                             arrival_us=w.arrival_us, input_len=w.input_len, output_len=w.output_len,
+                             slo_us=w.slo_us, emb=q.emb_bits, emb_dtype=hwr.HWR_BF16,
+                             expected_out_len=q.expected_out_len, freeze_state=freeze)
+            chosen_model = w.problem.dep_model[o["pair"]]
+            row[mode] = {"mean_quality": float(qual[np.arange(R), chosen_model].mean()),
+                         "mean_latency_s": o["mean_latency_s"], "p99_latency_s": o["p99_latency_s"],
+                         "slo_attainment": o["slo_attainment"], "load_skew": o["load_skew"]}
+        r.close()
+        rows.append(row)
+        log(f"pareto weight {alpha}: live quality {row['live']['mean_quality']:.4f} latency "
+            f"{row['live']['mean_latency_s']:.2f} s / frozen {row['frozen']['mean_quality']:.4f} "
+            f"{row['frozen']['mean_latency_s']:.2f} s")
+    return {"workload": f"Table 3 pool, sustained overload at {args.pareto_rate:g} req/s for "
+                        f"{args.sim_seconds:g} s, one run per cost weight",
+            "quality": "the library's Q of the chosen pair's model (per-model quality output)",
+            "points": rows}
+
+
+def _idle_state(w, hwr):
+    """The monitor's first snapshot of an idle pool (what the simulation
+    starts from), for the quality-only batch before a run."""
+    st = np.zeros(len(w.pairs), hwr.STATE_DTYPE)
+    st["ttft_avg_s"], st["tpot_avg_s"] = w.prior_ttft_s, w.prior_tpot_s
+    return st
+
+
 def cpu_baseline(pb, st, sample, sp):
     """The CPU oracle (plain C, one thread) on a bounded sample of the same
     workload: the first queries of chunk 0 against all pairs."""
@@ -337,6 +392,9 @@ def main() -> int:
     ap.add_argument("--no-sim", action="store_true", help="skip the closed-loop simulation")
     ap.add_argument("--sim-rate", type=float, default=21.0)
     ap.add_argument("--sim-seconds", type=float, default=60.0)
+    ap.add_argument("--pareto-weights", default="0,0.25,0.5,1,2,4",
+                    help="cost weights of the closed-loop quality-latency sweep ('' skips it)")
+    ap.add_argument("--pareto-rate", type=float, default=18.0)
     ap.add_argument("--sim-overload-rates", default="15,18,21",
                     help="extra sustained-overload arrival rates (the paper sweeps 15, 18, 21 req/s)")
     ap.add_argument("--copy-probe", action="store_true",
@@ -374,6 +432,7 @@ def main() -> int:
         log(f"single query (kernel launch) p50 {single['p50_us']:.1f} us p99 {single['p99_us']:.1f} us; "
             f"(graph launch) p50 {single_graph['p50_us']:.1f} us p99 {single_graph['p99_us']:.1f} us")
     sim = None if args.no_sim else closed_loop(args, hwr, torch)
+    pareto = None if args.no_sim or not args.pareto_weights else closed_loop_pareto(args, hwr, torch)
     cpu = None if args.no_cpu_baseline else cpu_baseline(w["pb"], w["st"], w["sample"], w["sp"])
     line = {
         "metric": METRIC, "value": res["value"], "unit": "candidates/s", "n_gpus": 1,
@@ -383,7 +442,7 @@ def main() -> int:
         "config": res["config"], "roofline": res["roofline"], "cpu_baseline": cpu,
         "single_query": single, "single_query_graph_launch": single_graph,
         "quality_roofline": res["quality_roofline"], "stages": res["stages"],
-        "staged_pipeline": staged, "closed_loop": sim,
+        "staged_pipeline": staged, "closed_loop": sim, "closed_loop_pareto": pareto,
     }
     print(json.dumps(line), flush=True)
     return 0

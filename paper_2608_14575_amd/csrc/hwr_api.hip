@@ -345,20 +345,22 @@ hwr_status check_config(const hwr_config *cfg) {
     return HWR_OK;
 }
 
+// Teardown: every resource is released even if one of the calls fails, so
+// their statuses are deliberately ignored.
 void release(hwr_ctx *c) {
     if (!c) return;
-    hipSetDevice(c->dev);
-    hipStreamSynchronize(c->stream);
+    (void)hipSetDevice(c->dev);
+    (void)hipStreamSynchronize(c->stream);
     for (const Pending &p : c->pending) {
-        hipEventDestroy(p.a);
-        hipEventDestroy(p.b);
+        (void)hipEventDestroy(p.a);
+        (void)hipEventDestroy(p.b);
     }
-    for (hipEvent_t e : c->pool) hipEventDestroy(e);
+    for (hipEvent_t e : c->pool) (void)hipEventDestroy(e);
     for (int i = 0; i < kStateSlots; ++i)
-        if (c->ring_ev[i]) hipEventDestroy(c->ring_ev[i]);
-    if (c->sstream) hipStreamSynchronize(c->sstream);
-    if (c->gexec) hipGraphExecDestroy(c->gexec);
-    if (c->graph) hipGraphDestroy(c->graph);
+        if (c->ring_ev[i]) (void)hipEventDestroy(c->ring_ev[i]);
+    if (c->sstream) (void)hipStreamSynchronize(c->sstream);
+    if (c->gexec) (void)hipGraphExecDestroy(c->gexec);
+    if (c->graph) (void)hipGraphDestroy(c->graph);
     void *dev_ptrs[] = {c->d_dep_model, c->d_dep_gpu, c->d_model_arch, c->d_params, c->d_pair_arch,
                         c->d_pair_params, c->d_dep_f32,
                         c->d_dep_bf16, c->d_bq, c->d_wq_pk, c->d_wqT, c->d_w1_pk, c->d_w2_pk,
@@ -367,12 +369,12 @@ void release(hwr_ctx *c) {
                         c->d_pval, c->d_hemb, c->d_hlen, c->d_hnout, c->d_hchoice, c->d_hslo,
                         c->d_hval, c->d_hcand, c->d_hqual, c->d_hfeas};
     for (void *p : dev_ptrs)
-        if (p) hipFree(p);
-    if (c->h_ring) hipHostFree(c->h_ring);
-    if (c->h_cur) hipHostFree(c->h_cur);
-    if (c->sstream) hipStreamDestroy(c->sstream);
-    if (c->h_sin) hipHostFree(c->h_sin);
-    if (c->h_sout) hipHostFree(c->h_sout);
+        if (p) (void)hipFree(p);
+    if (c->h_ring) (void)hipHostFree(c->h_ring);
+    if (c->h_cur) (void)hipHostFree(c->h_cur);
+    if (c->sstream) (void)hipStreamDestroy(c->sstream);
+    if (c->h_sin) (void)hipHostFree(c->h_sin);
+    if (c->h_sout) (void)hipHostFree(c->h_sout);
     delete c;
 }
 
@@ -693,7 +695,7 @@ hwr_status ensure_host_staging(hwr_ctx *c, size_t rows) {
                     c->d_hval, c->d_hcand, c->d_hqual, c->d_hfeas};
     HWR_HIP(c, hipStreamSynchronize(c->stream));
     for (void *p : ptrs)
-        if (p) hipFree(p);
+        if (p) (void)hipFree(p);          // idle after the synchronisation above
     c->hs_cap = 0;
     const size_t esz = c->bf16 ? 2 : 4;
     HWR_HIP(c, hipMalloc(&c->d_hemb, rows * c->D * esz));
@@ -803,9 +805,9 @@ hwr_status single_graph(hwr_ctx *c) {
     if (e == hipSuccess) e = launch_single(c->H, a, cs);
     hipGraph_t g = nullptr;
     hipError_t e2 = hipStreamEndCapture(cs, &g);
-    hipStreamDestroy(cs);
+    (void)hipStreamDestroy(cs);
     if (e != hipSuccess) {
-        if (g) hipGraphDestroy(g);
+        if (g) (void)hipGraphDestroy(g);
         return hip_fail(c, e, "single-query graph capture");
     }
     if (e2 != hipSuccess) return hip_fail(c, e2, "hipStreamEndCapture");

@@ -63,7 +63,6 @@ __global__ __launch_bounds__(256) void k_quality_bf16(QualityArgs a) {
     f32x16 acc = {};
     const int S = a.D / 64;
     const bf16x8 zero = {};
-#pragma unroll 2
     for (int s = 0; s < S; ++s) {
         bf16x8 av[4], bv[4];
 #pragma unroll
