@@ -34,8 +34,8 @@ PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_C5_1Mx256.json")
 KERNEL_NAMES = {   # as the profiler names them
-    "fused": "void hwr::k_mlp_bf16<256, false, 2>(hwr::MlpArgs)",
-    "mlp": "void hwr::k_mlp_bf16<256, true, 2>(hwr::MlpArgs)",
+    "fused": "void hwr::k_mlp_bf16<256, false, 2, true>(hwr::MlpArgs)",
+    "mlp": "void hwr::k_mlp_bf16<256, true, 2, true>(hwr::MlpArgs)",
     "quality": "hwr::k_quality_bf16(hwr::QualityArgs)",
     "gather": "hwr::k_gather(hwr::GatherArgs)",
     "epilogue": "void hwr::k_epilogue<true, false, false, false>(hwr::EpilogueArgs)",

@@ -44,6 +44,7 @@ struct hwr_ctx {
     int M = 0, G = 0, N = 0, A = 0, Gw = 0, D = 0, F = 0, H = 0, len_slot = 0;
     int bf16 = 0, pipeline = 0, max_chunk = 0, flags = 0, cus = 0;
     int NH = 2;                   // predictor heads (3: N_out predicted)
+    int fold_b1 = 0;              // b1 carried by the first layer's MFMA (bf16)
     float default_slo = 1.0f, b3[kMaxHeads] = {0, 0, 0};
     Rule rule{};                  // score and bound modes
     int nw = 1;                   // cost weights per query (outputs [n][nw] when > 1)
@@ -168,8 +169,46 @@ struct PackedPredictor {
     std::vector<uint32_t> w3;
 };
 
+// bf16 nearest-even bits of a finite fp32 value, and back.
+uint16_t bf16_rne(float x) {
+    uint32_t u;
+    std::memcpy(&u, &x, 4);
+    return static_cast<uint16_t>((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+}
+float bf16_value(uint16_t b) {
+    const uint32_t u = static_cast<uint32_t>(b) << 16;
+    float x;
+    std::memcpy(&x, &u, 4);
+    return x;
+}
+
+// b = hi + mid + lo exactly, each part a bf16 (8 significant bits apiece; each
+// residual is exact in fp32).  False when a part would not be exact (values
+// near the bottom of the exponent range), or b is not finite.
+bool bf16_split3(float b, uint16_t parts[3]) {
+    if (!std::isfinite(b)) return false;
+    float r = b;
+    for (int i = 0; i < 3; ++i) {
+        parts[i] = bf16_rne(r);
+        r = r - bf16_value(parts[i]);
+    }
+    return r == 0.0f &&
+           static_cast<double>(bf16_value(parts[0])) + static_cast<double>(bf16_value(parts[1])) +
+                   static_cast<double>(bf16_value(parts[2])) == static_cast<double>(b);
+}
+
+// Whether the layer-1 bias can ride in the first MFMA layer: bf16 weights,
+// three feature slots free after the eight signals, and b1 split exactly.
+bool can_fold_b1(const float *b1, int A, int Gw, int H) {
+    if (A + Gw + 8 > kFoldSlot) return false;
+    uint16_t parts[3];
+    for (int i = 0; i < H; ++i)
+        if (!bf16_split3(b1[i], parts)) return false;
+    return true;
+}
+
 PackedPredictor pack_predictor(const uint16_t *w1, const uint16_t *w2, const uint16_t *w3,
-                               const float *b1, const float *b2, int F, int H, int NH) {
+                               const float *b1, const float *b2, int F, int H, int NH, bool fold_b1) {
     const int MT = H / 32, KB2 = H / 16;
     PackedPredictor p;
     p.w1.assign(static_cast<size_t>(MT) * 2 * 64 * 8, 0);
@@ -198,8 +237,13 @@ PackedPredictor pack_predictor(const uint16_t *w1, const uint16_t *w2, const uin
             for (int kb = 0; kb < 2; ++kb)
                 for (int j = 0; j < 8; ++j) {
                     const int f = 16 * kb + 8 * h + j;
-                    p.w1[((static_cast<size_t>(mt) * 2 + kb) * 64 + lane) * 8 + j] =
-                        f < F ? w1[static_cast<size_t>(f) * H + 32 * mt + m] : 0;
+                    uint16_t v = f < F ? w1[static_cast<size_t>(f) * H + 32 * mt + m] : 0;
+                    if (fold_b1 && f >= kFoldSlot) {      // feature 1.0 x bias part
+                        uint16_t parts[3];
+                        bf16_split3(b1[32 * mt + m], parts);
+                        v = parts[f - kFoldSlot];
+                    }
+                    p.w1[((static_cast<size_t>(mt) * 2 + kb) * 64 + lane) * 8 + j] = v;
                 }
             for (int kb = 0; kb < KB2; ++kb)
                 for (int j = 0; j < 8; ++j) {
@@ -211,7 +255,7 @@ PackedPredictor pack_predictor(const uint16_t *w1, const uint16_t *w2, const uin
     for (int mt = 0; mt < MT; ++mt)
         for (int h = 0; h < 2; ++h) {
             for (int r = 0; r < 16; ++r) {
-                p.b1[(mt * 2 + h) * 16 + r] = b1[32 * mt + crow(r, h)];
+                p.b1[(mt * 2 + h) * 16 + r] = fold_b1 ? 0.0f : b1[32 * mt + crow(r, h)];
                 p.b2[(mt * 2 + h) * 16 + r] = b2[32 * mt + crow(r, h)];
             }
             for (int o = 0; o < NH; ++o)
@@ -458,10 +502,11 @@ hwr_status init_impl(const hwr_config *cfg, hwr_ctx **out) {
         for (int k = 0; k < D; ++k)
             for (int m = 0; m < M; ++m) wqT[static_cast<size_t>(m) * D + k] = wq[static_cast<size_t>(k) * M + m];
         INIT_HIP(upload(&c->d_wqT, wqT.data(), wqT.size()));
+        c->fold_b1 = can_fold_b1(cfg->b1, c->A, c->Gw, H) ? 1 : 0;
         PackedPredictor p = pack_predictor(static_cast<const uint16_t *>(cfg->w1),
                                            static_cast<const uint16_t *>(cfg->w2),
                                            static_cast<const uint16_t *>(cfg->w3), cfg->b1, cfg->b2, F, H,
-                                           c->NH);
+                                           c->NH, c->fold_b1 != 0);
         INIT_HIP(upload(&c->d_w1_pk, p.w1.data(), p.w1.size()));
         INIT_HIP(upload(&c->d_w2_pk, p.w2.data(), p.w2.size()));
         INIT_HIP(upload(&c->d_b1_pk, p.b1.data(), p.b1.size()));
@@ -533,7 +578,7 @@ hwr_status sync_state(hwr_ctx *c) {
     hwr_hw_state *dsrc = nullptr;
     HWR_HIP(c, hipHostGetDevicePointer(reinterpret_cast<void **>(&dsrc), src, 0));
     StateArgs a{dsrc, c->N, c->A, c->Gw, c->d_dep_model, c->d_dep_gpu, c->d_pair_arch,
-                c->d_pair_params, c->d_dep_f32, c->d_dep_bf16};
+                c->d_pair_params, c->d_dep_f32, c->d_dep_bf16, c->fold_b1};
     HWR_HIP(c, timed(c, HWR_K_STATE, [&] { return launch_state(a, c->stream); }));
     HWR_HIP(c, hipEventRecord(c->ring_ev[slot], c->stream));
     c->ring_used[slot] = true;
@@ -600,6 +645,7 @@ hwr_status route_device(hwr_ctx *c, const DevBatch &b) {
             ma.w2_pk = c->d_w2_pk;
             ma.b1_pk = c->d_b1_pk;
             ma.b2_pk = c->d_b2_pk;
+            ma.fold_b1 = c->fold_b1;
             ma.w3_frag = c->d_w3_frag;
             ma.out = oa;
             ma.nsplit = 1;
@@ -791,6 +837,7 @@ SingleArgs single_args(const hwr_ctx *c) {
     a.b1_pk = c->d_b1_pk;
     a.b2_pk = c->d_b2_pk;
     a.w3_pk = c->d_w3_pk;
+    a.fold_b1 = c->fold_b1;
     return a;
 }
 

@@ -24,6 +24,12 @@ constexpr int kMaxModels = 32;
 constexpr int kMaxHeads = 3;     // predictor outputs: TTFT, TPOT and (optionally) N_out
 constexpr int kPartVals = 8;     // floats per split partial: u, C, TTFT, TPOT, N_out, pad
 constexpr int kMaxWeights = 8;   // cost weights scored in one call (HWR_MAX_WEIGHTS)
+// Layer-1 bias folded into the first MFMA layer (bf16 predictor): feature
+// slots kFoldSlot .. kFoldSlot + 2 of the bf16 pair rows hold 1.0 and the
+// packed W1 rows there hold b1 split into three bf16 parts.  Those slots are
+// past every feature (the layout puts zeros after the eight signals), so the
+// weights they replace never contribute.
+constexpr int kFoldSlot = kFeatPad - 3;
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -108,6 +114,7 @@ struct StateArgs {
     const float *pair_params;     // [N] parameter count (B) of the pair's model
     float *dep_f32;               // [N][32]
     uint16_t *dep_bf16;           // [N][32]
+    int fold_b1;                  // bf16 rows carry 1.0 in the folded-bias slots
 };
 
 struct QualityArgs {
@@ -139,6 +146,7 @@ struct MlpArgs {                  // bf16 predictor (fused or staged)
     int nsplit;                   // pair ranges (grid.y); >1 writes partials
     uint64_t *part_key;           // [nsplit][nq]
     float *part_val;              // [nsplit][nq][kPartVals]
+    int fold_b1;                  // b1 is inside W1 (zero accumulator start)
 };
 
 struct MlpF32Args {
@@ -209,6 +217,7 @@ struct SingleArgs {
     const uint16_t *w1_pk, *w2_pk;
     const float *b1_pk, *b2_pk;
     const uint32_t *w3_pk;
+    int fold_b1;                  // feature rows carry 1.0 in the folded-bias slots
 };
 
 // ---------------------------------------------------------------- launchers

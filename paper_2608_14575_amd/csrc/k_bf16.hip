@@ -109,7 +109,7 @@ hipError_t launch_quality_bf16(const QualityArgs &a, hipStream_t s) {
 // carries column tile h alone (one query per lane).  Fused mode then applies
 // Eq. 2, the bound test and the utility and keeps the query's best candidate
 // (Eq. 3); staged mode reads X from HBM and writes TTFT/TPOT per candidate.
-template <int H, bool STAGED, int NH>
+template <int H, bool STAGED, int NH, bool FB>
 __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
     constexpr int MT = H / 32;     // 32-row tiles of a hidden layer
     constexpr int KB2 = H / 16;    // k-blocks of the second layer
@@ -271,7 +271,8 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
         bf16x8 h1[NT][KB2];
         f32x16 acc[2][NT];
         auto l1_mfma = [&](int mt, f32x16 (&c)[NT]) {
-            const f32x16 bi = bias_tile(s_b1 + (mt * 2 + ho) * 4);
+            // FB: b1 enters through the folded-bias feature slots
+            const f32x16 bi = FB ? f32x16{} : bias_tile(s_b1 + (mt * 2 + ho) * 4);
 #pragma unroll
             for (int t = 0; t < NT; ++t) c[t] = bi;
 #pragma unroll
@@ -424,11 +425,18 @@ template <int H>
 static hipError_t launch_mlp_h(bool staged, const MlpArgs &a, hipStream_t s) {
     const dim3 grid((a.q.nq + kQPerBlock - 1) / kQPerBlock, staged ? 1 : a.nsplit);
     const dim3 block(kMlpThreads);
+    if (a.fold_b1) {
+        if (a.nheads == 3)
+            return staged ? launch_kernel(k_mlp_bf16<H, true, 3, true>, grid, block, 0, s, a)
+                          : launch_kernel(k_mlp_bf16<H, false, 3, true>, grid, block, 0, s, a);
+        return staged ? launch_kernel(k_mlp_bf16<H, true, 2, true>, grid, block, 0, s, a)
+                      : launch_kernel(k_mlp_bf16<H, false, 2, true>, grid, block, 0, s, a);
+    }
     if (a.nheads == 3)
-        return staged ? launch_kernel(k_mlp_bf16<H, true, 3>, grid, block, 0, s, a)
-                      : launch_kernel(k_mlp_bf16<H, false, 3>, grid, block, 0, s, a);
-    return staged ? launch_kernel(k_mlp_bf16<H, true, 2>, grid, block, 0, s, a)
-                  : launch_kernel(k_mlp_bf16<H, false, 2>, grid, block, 0, s, a);
+        return staged ? launch_kernel(k_mlp_bf16<H, true, 3, false>, grid, block, 0, s, a)
+                      : launch_kernel(k_mlp_bf16<H, false, 3, false>, grid, block, 0, s, a);
+    return staged ? launch_kernel(k_mlp_bf16<H, true, 2, false>, grid, block, 0, s, a)
+                  : launch_kernel(k_mlp_bf16<H, false, 2, false>, grid, block, 0, s, a);
 }
 
 hipError_t launch_mlp_bf16(int H, bool staged, const MlpArgs &a, hipStream_t s) {

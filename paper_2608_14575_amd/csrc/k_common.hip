@@ -20,7 +20,7 @@ __global__ __launch_bounds__(256) void k_state(StateArgs a) {
     for (int f = 0; f < kFeatPad; ++f) {
         const float v = p.slot(f);
         rf[f] = v;
-        rb[f] = bf16_bits(v);
+        rb[f] = (a.fold_b1 && f >= kFoldSlot) ? uint16_t{0x3F80} : bf16_bits(v);   // 1.0
     }
 }
 

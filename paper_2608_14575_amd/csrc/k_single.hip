@@ -26,7 +26,7 @@ __device__ __forceinline__ bf16x8 relu_pack8s(const f32x16 &c, int base) {
 // (j - b) mod 8 (Eq. 1 layout; the query's input length is signal 1).  Logs
 // in fp64, rounded once to fp32, then to bf16 (as the state kernel does).
 __device__ __forceinline__ void pair_row(uint16_t *row, int j, int b0, int ks, int ia, int ig,
-                                         uint32_t raw, float params, int32_t len) {
+                                         uint32_t raw, float params, int32_t len, bool fold) {
     double arg = 1.0, scale = 0.0;
     if (ks == 0) { arg = static_cast<double>(params); scale = 0.25; }
     if (ks == 1) { arg = static_cast<double>(len < 1 ? 1 : len); scale = 0.125; }
@@ -38,7 +38,7 @@ __device__ __forceinline__ void pair_row(uint16_t *row, int j, int b0, int ks, i
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int f = j + 8 * i;
-        const uint16_t hot = (f == ia || f == ig) ? 0x3F80 : 0;
+        const uint16_t hot = (f == ia || f == ig || (fold && f >= kFoldSlot)) ? 0x3F80 : 0;
         row[f] = (f >= b0 && f < b0 + 8) ? sig : hot;
     }
 }
@@ -169,13 +169,14 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
     else if (tid < nbw) s_w3p[tid - MT * 16] = rbw;
     if (tid < a.M) s_bq[tid] = rbq;
     if (has0) {
-        pair_row(s_row[p0], j8, b0, ks, ia0, ig0, raw0, prm0, len);
+        pair_row(s_row[p0], j8, b0, ks, ia0, ig0, raw0, prm0, len, a.fold_b1 != 0);
         if (j8 == 0) s_model[p0] = md0;
     }
     for (int p = p0 + 32; p < a.N; p += 32) {       // more than 32 pairs
         const uint32_t raw = ks >= 2 ? reinterpret_cast<const uint32_t *>(a.state + p)[ks - 2] : 0u;
         const float prm = ks == 0 ? a.pair_params[p] : 1.0f;
-        pair_row(s_row[p], j8, b0, ks, a.pair_arch[p], a.arch_width + a.dep_gpu[p], raw, prm, len);
+        pair_row(s_row[p], j8, b0, ks, a.pair_arch[p], a.arch_width + a.dep_gpu[p], raw, prm, len,
+                 a.fold_b1 != 0);
         if (j8 == 0) s_model[p] = a.dep_model[p];
     }
     __syncthreads();
