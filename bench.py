@@ -36,7 +36,7 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_C5_1Mx256.json")
 KERNEL_NAMES = {   # as the profiler names them
     "fused": "void hwr::k_mlp_bf16<256, false, 2, true>(hwr::MlpArgs)",
     "mlp": "void hwr::k_mlp_bf16<256, true, 2, true>(hwr::MlpArgs)",
-    "quality": "hwr::k_quality_bf16(hwr::QualityArgs)",
+    "quality": "void hwr::k_quality_bf16<1>(hwr::QualityArgs)",
     "gather": "hwr::k_gather(hwr::GatherArgs)",
     "epilogue": "void hwr::k_epilogue<true, false, false, false>(hwr::EpilogueArgs)",
 }
@@ -249,6 +249,62 @@ def single_query(args, S, hwr, torch, flags=0):
             "timing": "host clock around hwr_route_batch (ctypes call included)"}
 
 
+def batch_latency(args, S, hwr, torch):
+    """Latency of one hwr_route_batch call on device-resident inputs for the
+    smaller routing workloads (C1 fp32; C2, C3 bf16), one chunk each: the C
+    function called directly (argument structs built once, as a C caller
+    would), HIP events on the call's stream around each call; median and p99
+    over `--batch-calls` calls after 10 untimed ones."""
+    L = hwr.load()
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    res = {}
+    for name in ("C1", "C2", "C3"):
+        sp = S.spec(name)
+        pb, st, qs = S.make_problem(sp, args.seed), S.make_state(sp, args.seed), S.make_queries(sp, args.seed)
+        emb_np = qs.emb_bits.view(np.int16) if sp.dtype == "bf16" else np.ascontiguousarray(qs.emb_bits, np.float32)
+        emb = torch.from_numpy(np.ascontiguousarray(emb_np)).to(dev)
+        il = torch.from_numpy(np.ascontiguousarray(qs.input_len)).to(dev)
+        no = torch.from_numpy(np.ascontiguousarray(qs.expected_out_len)).to(dev)
+        slo = torch.from_numpy(np.ascontiguousarray(qs.slo_s)).to(dev)
+        n, N = qs.n, sp.n_deployments
+        out = dict(choice=torch.empty(n, dtype=torch.int32, device=dev),
+                   feasible=torch.empty(n, dtype=torch.uint8, device=dev),
+                   utility=torch.empty(n, dtype=torch.float32, device=dev),
+                   e2e_s=torch.empty(n, dtype=torch.float32, device=dev),
+                   ttft_s=torch.empty(n, dtype=torch.float32, device=dev),
+                   tpot_s=torch.empty(n, dtype=torch.float32, device=dev))
+        r = hwr.Router.from_problem(pb, max_chunk=n, stream=int(stream.cuda_stream))
+        r.update(st)
+        qb = hwr.hwr_query_batch(n, hwr.HWR_MEM_DEVICE, emb.data_ptr(), il.data_ptr(), no.data_ptr(),
+                                 slo.data_ptr())
+        rr = hwr.hwr_route_result(**{k: v.data_ptr() for k, v in out.items()})
+        qref, rref, ctx = C.byref(qb), C.byref(rr), r.ctx
+        calls = args.batch_calls
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(calls)]
+        for _ in range(10):
+            assert L.hwr_route_batch(ctx, qref, rref) == 0, hwr.hwr_last_error(ctx)
+        torch.cuda.synchronize()
+        for a, b in ev:
+            a.record(stream)
+            rc = L.hwr_route_batch(ctx, qref, rref)
+            b.record(stream)
+            assert rc == 0, hwr.hwr_last_error(ctx)
+        torch.cuda.synchronize()
+        choice = out["choice"].cpu().numpy()
+        assert (choice >= 0).all() and (choice < N).all(), "choice out of range"
+        r.close()
+        us = np.array([a.elapsed_time(b) * 1e3 for a, b in ev])
+        p50 = float(np.percentile(us, 50))
+        res[name] = {"queries": n, "pairs": N, "candidates": n * N, "dtype": sp.dtype,
+                     "predictor": f"{sp.feat_dim}-{sp.hidden}-{sp.hidden}-2", "embed_dim": sp.embed_dim,
+                     "calls": calls, "p50_us": p50, "p99_us": float(np.percentile(us, 99)),
+                     "candidates_per_s_at_p50": n * N / (p50 / 1e6),
+                     "timing": "HIP events on the stream around each C call (host enqueue included)"}
+        log(f"batch latency {name}: {n} x {N}, p50 {p50:.1f} us")
+    return res
+
+
 def closed_loop(args, hwr, torch):
     """The closed-loop serving simulation (include/hwr_sim.h) with the library
     routing every step's arrivals: Table 3's pool of five models on two GPUs,
@@ -387,6 +443,8 @@ def main() -> int:
                     help="steps of the staged pipeline (gather / epilogue HBM figures); 0 skips it")
     ap.add_argument("--c4-calls", type=int, default=10000)
     ap.add_argument("--cpu-sample", type=int, default=1024)
+    ap.add_argument("--batch-calls", type=int, default=200,
+                    help="timed calls per workload for the C1-C3 batch latencies (0: skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-single", action="store_true")
     ap.add_argument("--no-sim", action="store_true", help="skip the closed-loop simulation")
@@ -431,6 +489,7 @@ def main() -> int:
     if single:
         log(f"single query (kernel launch) p50 {single['p50_us']:.1f} us p99 {single['p99_us']:.1f} us; "
             f"(graph launch) p50 {single_graph['p50_us']:.1f} us p99 {single_graph['p99_us']:.1f} us")
+    batch = batch_latency(args, S, hwr, torch) if args.batch_calls > 0 else None
     sim = None if args.no_sim else closed_loop(args, hwr, torch)
     pareto = None if args.no_sim or not args.pareto_weights else closed_loop_pareto(args, hwr, torch)
     cpu = None if args.no_cpu_baseline else cpu_baseline(w["pb"], w["st"], w["sample"], w["sp"])
@@ -442,7 +501,7 @@ def main() -> int:
         "config": res["config"], "roofline": res["roofline"], "cpu_baseline": cpu,
         "single_query": single, "single_query_graph_launch": single_graph,
         "quality_roofline": res["quality_roofline"], "stages": res["stages"],
-        "staged_pipeline": staged, "closed_loop": sim, "closed_loop_pareto": pareto,
+        "staged_pipeline": staged, "batch_latency": batch, "closed_loop": sim, "closed_loop_pareto": pareto,
     }
     print(json.dumps(line), flush=True)
     return 0

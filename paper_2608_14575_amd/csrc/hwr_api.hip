@@ -623,7 +623,7 @@ hwr_status route_device(hwr_ctx *c, const DevBatch &b) {
         qu.bq = c->d_bq;
         qu.qmat = qmat;
         HWR_HIP(c, timed(c, HWR_K_QUALITY, [&] {
-            return c->bf16 ? launch_quality_bf16(qu, c->stream) : launch_quality_f32(qu, c->stream);
+            return c->bf16 ? launch_quality_bf16(qu, c->cus, c->stream) : launch_quality_f32(qu, c->stream);
         }));
 
         if (c->bf16) {

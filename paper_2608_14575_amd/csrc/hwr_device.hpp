@@ -220,6 +220,19 @@ __device__ __forceinline__ uint64_t max_dpp(uint64_t k) {
                        dpp_u32<Ctrl>(static_cast<uint32_t>(k));
     return o > k ? o : k;
 }
+// Cross-lane reductions on DPP (data-parallel primitives within a 16-lane
+// row: quad permutes, half-row and row mirrors), then one read of each row's
+// lane 0; no LDS round trips.  After the four steps every lane of a row holds
+// the row's result.
+__device__ __forceinline__ float wave_sum(float v) {
+    v += __uint_as_float(dpp_u32<0xB1>(__float_as_uint(v)));    // quad_perm [1,0,3,2]
+    v += __uint_as_float(dpp_u32<0x4E>(__float_as_uint(v)));    // quad_perm [2,3,0,1]
+    v += __uint_as_float(dpp_u32<0x141>(__float_as_uint(v)));   // row_half_mirror
+    v += __uint_as_float(dpp_u32<0x140>(__float_as_uint(v)));   // row_mirror
+    const int b = __float_as_int(v);
+    return (__int_as_float(__builtin_amdgcn_readlane(b, 0)) + __int_as_float(__builtin_amdgcn_readlane(b, 16))) +
+           (__int_as_float(__builtin_amdgcn_readlane(b, 32)) + __int_as_float(__builtin_amdgcn_readlane(b, 48)));
+}
 // Maximum of a key over aligned groups of G lanes (G a power of two <= 64,
 // the same in the whole wave); every lane of a group receives it.  Lanes
 // without a candidate hold 0.

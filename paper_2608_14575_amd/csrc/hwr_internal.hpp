@@ -223,7 +223,8 @@ struct SingleArgs {
 // ---------------------------------------------------------------- launchers
 // Each returns the launch error (hipSuccess on success).
 hipError_t launch_state(const StateArgs &a, hipStream_t s);
-hipError_t launch_quality_bf16(const QualityArgs &a, hipStream_t s);
+// cus: compute units of the device (a grid below it takes the unrolled variant)
+hipError_t launch_quality_bf16(const QualityArgs &a, int cus, hipStream_t s);
 hipError_t launch_quality_f32(const QualityArgs &a, hipStream_t s);
 hipError_t launch_mlp_bf16(int H, bool staged, const MlpArgs &a, hipStream_t s);
 hipError_t launch_mlp_f32(int H, const MlpF32Args &a, hipStream_t s);

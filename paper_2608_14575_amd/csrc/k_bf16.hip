@@ -50,11 +50,17 @@ __device__ __forceinline__ bf16x8 relu_pack8(const f32x16 &c, int base) {
 // embedding, lane half h reads 64 contiguous bytes of its query row, as four
 // k-blocks; Wq is pre-packed so that each lane's B operand for the same
 // k-block is one contiguous 16-byte load.  The embedding stream dominates
-// the traffic (HBM-bound, arithmetic intensity ~M flop/byte).
+// the traffic (HBM-bound, arithmetic intensity ~M flop/byte).  U slices are
+// loaded before their MFMAs.  Large batches: four waves per workgroup and
+// U = 1, which streams best.  Batches with fewer four-wave workgroups than
+// compute units: one wave per workgroup (four times the compute units busy)
+// and U = 4 (a quarter of the dependent memory round trips).  The MFMA chain
+// runs over the slices in the same order either way: identical results.
+template <int U>
 __global__ __launch_bounds__(256) void k_quality_bf16(QualityArgs a) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int row = lane & 31, h = lane >> 5;
-    const int q0 = blockIdx.x * 128 + wave * 32;
+    const int q0 = (blockIdx.x * (blockDim.x >> 6) + wave) * 32;
     const int qa = q0 + row;
     const bool valid = qa < a.nq;
     const uint16_t *e = static_cast<const uint16_t *>(a.emb) +
@@ -63,7 +69,22 @@ __global__ __launch_bounds__(256) void k_quality_bf16(QualityArgs a) {
     f32x16 acc = {};
     const int S = a.D / 64;
     const bf16x8 zero = {};
-    for (int s = 0; s < S; ++s) {
+    int s = 0;
+    for (; s + U <= S; s += U) {
+        bf16x8 av[U][4], bv[U][4];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                av[u][c] = *reinterpret_cast<const bf16x8 *>(e + 64 * (s + u) + 8 * c);
+                bv[u][c] = wq[((s + u) * 4 + c) * 64];
+            }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int c = 0; c < 4; ++c) acc = mfma32(valid ? av[u][c] : zero, bv[u][c], acc);
+    }
+    for (; s < S; ++s) {
         bf16x8 av[4], bv[4];
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
@@ -84,8 +105,10 @@ __global__ __launch_bounds__(256) void k_quality_bf16(QualityArgs a) {
     }
 }
 
-hipError_t launch_quality_bf16(const QualityArgs &a, hipStream_t s) {
-    return launch_kernel(k_quality_bf16, dim3((a.nq + 127) / 128), dim3(256), 0, s, a);
+hipError_t launch_quality_bf16(const QualityArgs &a, int cus, hipStream_t s) {
+    const int grid = (a.nq + 127) / 128;
+    if (grid < cus) return launch_kernel(k_quality_bf16<4>, dim3((a.nq + 31) / 32), dim3(64), 0, s, a);
+    return launch_kernel(k_quality_bf16<1>, dim3(grid), dim3(256), 0, s, a);
 }
 
 // ------------------------------------------------------------ predictor

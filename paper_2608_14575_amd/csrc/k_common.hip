@@ -30,37 +30,56 @@ hipError_t launch_state(const StateArgs &a, hipStream_t s) {
 
 // ------------------------------------------------------------ fp32 quality
 // Hardware-independent quality (Sec. 3.2 item 3): Q[q][m] = e_q . Wq[:, m] + bq[m].
-// fp32 workloads only (small); one thread per (query, model).
+// fp32 workloads; one wave per query.  Lane l accumulates every model over
+// k = l, l + 64, ... (the embedding row and Wq's rows k, M consecutive
+// floats each, are read lane-contiguous), then a DPP sum per model.
 __global__ __launch_bounds__(256) void k_quality_f32(QualityArgs a) {
-    const long idx = static_cast<long>(blockIdx.x) * blockDim.x + threadIdx.x;
-    const long q = idx / a.M;
-    const int m = static_cast<int>(idx - q * a.M);
-    if (q >= a.nq) return;
-    const float *e = static_cast<const float *>(a.emb) + q * a.D;
-    float acc = 0.0f;
-    for (int k = 0; k < a.D; ++k) acc = fmaf(e[k], a.wq[static_cast<size_t>(k) * a.M + m], acc);
-    a.qmat[q * a.M + m] = acc + a.bq[m];
+    const int lane = threadIdx.x & 63;
+    const int q = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    if (q >= a.nq) return;                       // the whole wave
+    const float *e = static_cast<const float *>(a.emb) + static_cast<size_t>(q) * a.D;
+    const int M = a.M;
+    float acc[kMaxModels];
+#pragma unroll
+    for (int m = 0; m < kMaxModels; ++m) acc[m] = 0.0f;
+    for (int k = lane; k < a.D; k += 64) {
+        const float ev = e[k];
+        const float *w = a.wq + static_cast<size_t>(k) * M;
+#pragma unroll
+        for (int m = 0; m < kMaxModels; ++m)
+            if (m < M) acc[m] = fmaf(ev, w[m], acc[m]);
+    }
+#pragma unroll
+    for (int m = 0; m < kMaxModels; ++m) {
+        if (m < M) {
+            const float v = wave_sum(acc[m]);
+            if (lane == m) a.qmat[static_cast<size_t>(q) * M + m] = v + a.bq[m];
+        }
+    }
 }
 
 hipError_t launch_quality_f32(const QualityArgs &a, hipStream_t s) {
-    const long total = static_cast<long>(a.nq) * a.M;
-    return launch_kernel(k_quality_f32, dim3(static_cast<unsigned>((total + 255) / 256)), dim3(256), 0, s, a);
+    return launch_kernel(k_quality_f32, dim3(static_cast<unsigned>((a.nq + 3) / 4)), dim3(256), 0, s, a);
 }
 
 // ------------------------------------------------------------ fp32 predictor
-// Eq. 1 predictor in fp32, one thread per candidate (q, d): features, two
-// hidden ReLU layers, the two or three heads, softplus.  Weights staged in
-// LDS; the first-layer rows are zero-padded to 32 slots.
+// Eq. 1 predictor in fp32, one wave per candidate (q, d); waves stride over
+// the candidates.  Lane l holds hidden units l and (H = 128) l + 64.  Layer 1
+// reads the pair's feature row as wave-uniform values; layer 2 broadcasts
+// each first-layer unit with readlane; the heads are DPP sums, then softplus.
+// Both hidden layers accumulate in input order from the bias, one rounding
+// per fused multiply-add.  Weights staged in LDS as [input][unit] rows, so
+// the lanes of a wave read consecutive words.
 template <int H>
 __global__ __launch_bounds__(256) void k_mlp_f32(MlpF32Args a) {
+    constexpr int U = H / 64;
     __shared__ float s_w1[kFeatPad * H];
     __shared__ float s_w2[H * H];
     __shared__ float s_w3[H * kMaxHeads];
-    const int NH = a.nheads;
     __shared__ float s_b1[H];
     __shared__ float s_b2[H];
-    for (int i = threadIdx.x; i < kFeatPad * H; i += blockDim.x)
-        s_w1[i] = (i / H) < a.F ? a.w1[i] : 0.0f;
+    const int NH = a.nheads;
+    for (int i = threadIdx.x; i < a.F * H; i += blockDim.x) s_w1[i] = a.w1[i];
     for (int i = threadIdx.x; i < H * H; i += blockDim.x) s_w2[i] = a.w2[i];
     for (int i = threadIdx.x; i < H * NH; i += blockDim.x) s_w3[i] = a.w3[i];
     for (int i = threadIdx.x; i < H; i += blockDim.x) {
@@ -68,45 +87,64 @@ __global__ __launch_bounds__(256) void k_mlp_f32(MlpF32Args a) {
         s_b2[i] = a.b2[i];
     }
     __syncthreads();
-    const long c = static_cast<long>(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (c >= static_cast<long>(a.q.nq) * a.N) return;
-    const long q = c / a.N;
-    const int d = static_cast<int>(c - q * a.N);
-    float x[kFeatPad];
-    const float xl = len_feature(a.q.input_len[q]);
+    const int lane = threadIdx.x & 63;
+    const long total = static_cast<long>(a.q.nq) * a.N;
+    const long stride = static_cast<long>(gridDim.x) * 4;
+    for (long c = static_cast<long>(blockIdx.x) * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+         c < total; c += stride) {
+        const long q = c / a.N;
+        const int d = static_cast<int>(c - q * a.N);
+        const float xl = len_feature(a.q.input_len[q]);
+        const float *row = a.dep_f32 + static_cast<size_t>(d) * kFeatPad;
+        float h1[U], h2[U];
 #pragma unroll
-    for (int f = 0; f < kFeatPad; ++f) {
-        const float v = a.dep_f32[static_cast<size_t>(d) * kFeatPad + f];
-        x[f] = (f == a.len_slot) ? xl : v;
+        for (int u = 0; u < U; ++u) h1[u] = s_b1[lane + 64 * u];
+        for (int f = 0; f < a.F; ++f) {
+            const float x = (f == a.len_slot) ? xl : row[f];
+#pragma unroll
+            for (int u = 0; u < U; ++u) h1[u] = fmaf(s_w1[f * H + lane + 64 * u], x, h1[u]);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            h1[u] = fmaxf(h1[u], 0.0f);
+            h2[u] = s_b2[lane + 64 * u];
+        }
+#pragma unroll
+        for (int v = 0; v < U; ++v) {
+            const int hv = __float_as_int(h1[v]);
+#pragma unroll
+            for (int i = 0; i < 64; ++i) {
+                const float x = __int_as_float(__builtin_amdgcn_readlane(hv, i));
+                const float *w = s_w2 + (64 * v + i) * H + lane;
+#pragma unroll
+                for (int u = 0; u < U; ++u) h2[u] = fmaf(w[64 * u], x, h2[u]);
+            }
+        }
+        float z0 = 0.0f, z1 = 0.0f, z2 = 0.0f;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const float h = fmaxf(h2[u], 0.0f);
+            const int j = lane + 64 * u;
+            z0 = fmaf(s_w3[NH * j + 0], h, z0);
+            z1 = fmaf(s_w3[NH * j + 1], h, z1);
+            if (NH == 3) z2 = fmaf(s_w3[NH * j + 2], h, z2);
+        }
+        z0 = wave_sum(z0);
+        z1 = wave_sum(z1);
+        if (NH == 3) z2 = wave_sum(z2);
+        if (lane == 0) {
+            a.cand_ttft[c] = softplus_f32(z0 + a.b3_0);
+            a.cand_tpot[c] = softplus_f32(z1 + a.b3_1);
+            if (NH == 3) a.cand_nout[c] = softplus_f32(z2 + a.b3_2);
+        }
     }
-    float h1[H];
-#pragma unroll
-    for (int j = 0; j < H; ++j) h1[j] = s_b1[j];
-#pragma unroll
-    for (int f = 0; f < kFeatPad; ++f) {
-#pragma unroll
-        for (int j = 0; j < H; ++j) h1[j] = fmaf(s_w1[f * H + j], x[f], h1[j]);
-    }
-#pragma unroll
-    for (int j = 0; j < H; ++j) h1[j] = fmaxf(h1[j], 0.0f);
-    float z0 = 0.0f, z1 = 0.0f, z2 = 0.0f;
-    for (int j = 0; j < H; ++j) {
-        float acc = s_b2[j];
-#pragma unroll
-        for (int i = 0; i < H; ++i) acc = fmaf(s_w2[i * H + j], h1[i], acc);
-        acc = fmaxf(acc, 0.0f);
-        z0 = fmaf(s_w3[NH * j + 0], acc, z0);
-        z1 = fmaf(s_w3[NH * j + 1], acc, z1);
-        if (NH == 3) z2 = fmaf(s_w3[NH * j + 2], acc, z2);
-    }
-    a.cand_ttft[c] = softplus_f32(z0 + a.b3_0);
-    a.cand_tpot[c] = softplus_f32(z1 + a.b3_1);
-    if (NH == 3) a.cand_nout[c] = softplus_f32(z2 + a.b3_2);
 }
 
 hipError_t launch_mlp_f32(int H, const MlpF32Args &a, hipStream_t s) {
     const long total = static_cast<long>(a.q.nq) * a.N;
-    const dim3 grid(static_cast<unsigned>((total + 255) / 256));
+    // one wave per candidate, at most 1024 workgroups (each stages the weights once)
+    const long wgs = (total + 3) / 4;
+    const dim3 grid(static_cast<unsigned>(wgs < 1024 ? (wgs < 1 ? 1 : wgs) : 1024));
     if (H == 64) return launch_kernel(k_mlp_f32<64>, grid, dim3(256), 0, s, a);
     if (H == 128) return launch_kernel(k_mlp_f32<128>, grid, dim3(256), 0, s, a);
     return hipErrorInvalidValue;

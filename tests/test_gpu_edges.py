@@ -82,6 +82,22 @@ def test_chunking_is_invisible(pipeline):
     _same(G.route_device(a, qs, "bf16"), G.route_device(b, qs, "bf16"))
 
 
+def test_quality_unroll_is_invisible():
+    """The quality GEMM loads four embedding slices ahead when its grid is
+    smaller than the device, one otherwise; its MFMA chain is the same, so a
+    batch routed in one large chunk and in small chunks gives bit-identical
+    outputs, Q matrix included."""
+    import torch
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    n = 128 * cus + 5                       # one chunk: grid above the CU count
+    sp, pb, st, qs = _case(n_queries=n, seed=13)
+    big = G.make_router(pb, max_chunk=n)
+    small = G.make_router(pb, max_chunk=128 * (cus // 2))
+    big.update(st)
+    small.update(st)
+    _same(G.route_device(big, qs, "bf16"), G.route_device(small, qs, "bf16"))
+
+
 def test_fused_equals_staged_and_split_equals_unsplit():
     """Same arithmetic per candidate in every mode: bit-identical outputs.
     40 queries over 64 pairs makes the fused kernel split the pairs over

@@ -36,6 +36,26 @@ def test_c1_fp32_host_full():
     assert rep.max_rel_ttft < 1e-5 and rep.max_rel_tpot < 1e-5
 
 
+@pytest.mark.parametrize("hidden,heads,nq,models,D", [
+    (64, 2, 1, 4, 384),          # one query: one workgroup, one busy wave of the quality kernel
+    (64, 2, 1027, 4, 384),       # 8,216 candidates: waves loop over candidates; ragged workgroups
+    (128, 2, 301, 32, 192),      # H = 128 (two units per lane), 32 models, D = 3 x 64
+    (128, 3, 523, 6, 448),       # three heads: N_out predicted per candidate
+])
+def test_fp32_device_shapes(hidden, heads, nq, models, D):
+    """fp32 predictor (one wave per candidate) and quality (one wave per
+    query) at shapes past C1: H = 128, three heads, 32 models, batches
+    larger than one pass of the grid, ragged query counts."""
+    sp = S.spec("C1", n_queries=nq, hidden=hidden, n_heads=heads, n_models=models, embed_dim=D)
+    pb, st, qs = S.make_problem(sp, 11), S.make_state(sp, 11), S.make_queries(sp, 11)
+    r = G.make_router(pb)
+    r.update(st)
+    out = G.route_device(r, qs, sp.dtype)
+    rep = G.check(pb, st, qs, out)
+    _report(f"fp32 H={hidden} heads={heads} nq={nq} M={models} D={D}", rep)
+    assert rep.max_rel_ttft < 1e-5 and rep.max_rel_tpot < 1e-5
+
+
 @pytest.mark.parametrize("pipeline", ["fused", "staged"])
 def test_c2_bf16_device_full(pipeline):
     sp = S.spec("C2")
