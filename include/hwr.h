@@ -45,11 +45,15 @@
  *
  * Conventions
  *  - Every call returns an hwr_status; nothing throws across this boundary.
- *    On error, outputs are not written and hwr_last_error() holds a message.
+ *    On a validation error, outputs are not written; a HIP error in the middle
+ *    of a batch of several chunks may leave earlier chunks' outputs written.
+ *    hwr_last_error() holds a message.
  *  - The context owns device copies of weights and state; the caller owns all
  *    query and result buffers.  Configuration and state are copied in.
  *  - HWR_MEM_DEVICE batches are ordered on the context's stream and return
  *    without waiting; HWR_MEM_HOST batches return with the results written.
+ *    A host batch larger than max_chunk is streamed: the next chunk's upload
+ *    (on a second stream of the context) overlaps this chunk's kernels.
  *  - A context is not thread-safe: one context per thread (or per stream).
  */
 #ifndef HWR_H

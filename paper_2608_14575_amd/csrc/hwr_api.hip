@@ -79,11 +79,21 @@ struct hwr_ctx {
     uint64_t *d_pkey = nullptr;
     float *d_pval = nullptr;
     size_t part_cap = 0;
-    // host-memory batches: device staging
+    // host-memory batches: device staging.  Inputs are double-buffered (the
+    // next chunk's upload overlaps this chunk's kernels); outputs are ordered
+    // on the context's stream and need one set.
     size_t hs_cap = 0;
-    void *d_hemb = nullptr;
-    int32_t *d_hlen = nullptr, *d_hnout = nullptr, *d_hchoice = nullptr;
-    float *d_hslo = nullptr, *d_hval = nullptr, *d_hcand = nullptr, *d_hqual = nullptr;
+    struct InStage {
+        void *emb = nullptr;
+        int32_t *len = nullptr, *nout = nullptr;
+        float *slo = nullptr;
+        hipEvent_t copied = nullptr;   // the upload into this set has finished
+        hipEvent_t read = nullptr;     // the kernels that read this set have finished
+        bool used = false;
+    } hin[2];
+    hipStream_t cstream = nullptr;   // upload stream of host-memory batches
+    int32_t *d_hchoice = nullptr;
+    float *d_hval = nullptr, *d_hcand = nullptr, *d_hqual = nullptr;
     uint8_t *d_hfeas = nullptr;
     // single-query path
     SingleIn *h_sin = nullptr;
@@ -410,10 +420,17 @@ void release(hwr_ctx *c) {
                         c->d_dep_bf16, c->d_bq, c->d_wq_pk, c->d_wqT, c->d_w1_pk, c->d_w2_pk,
                         c->d_b1_pk, c->d_b2_pk, c->d_w3_pk, c->d_w3_frag, c->d_wq, c->d_w1, c->d_w2, c->d_w3,
                         c->d_b1, c->d_b2, c->d_qmat, c->d_ctt, c->d_ctp, c->d_cno, c->d_X, c->d_pkey,
-                        c->d_pval, c->d_hemb, c->d_hlen, c->d_hnout, c->d_hchoice, c->d_hslo,
+                        c->d_pval, c->hin[0].emb, c->hin[0].len, c->hin[0].nout, c->hin[0].slo,
+                        c->hin[1].emb, c->hin[1].len, c->hin[1].nout, c->hin[1].slo, c->d_hchoice,
                         c->d_hval, c->d_hcand, c->d_hqual, c->d_hfeas};
+    if (c->cstream) (void)hipStreamSynchronize(c->cstream);
     for (void *p : dev_ptrs)
         if (p) (void)hipFree(p);
+    for (auto &h : c->hin) {
+        if (h.copied) (void)hipEventDestroy(h.copied);
+        if (h.read) (void)hipEventDestroy(h.read);
+    }
+    if (c->cstream) (void)hipStreamDestroy(c->cstream);
     if (c->h_ring) (void)hipHostFree(c->h_ring);
     if (c->h_cur) (void)hipHostFree(c->h_cur);
     if (c->sstream) (void)hipStreamDestroy(c->sstream);
@@ -736,19 +753,39 @@ hwr_status route_device(hwr_ctx *c, const DevBatch &b) {
 }
 
 hwr_status ensure_host_staging(hwr_ctx *c, size_t rows) {
+    if (!c->cstream) {
+        HWR_HIP(c, hipStreamCreateWithFlags(&c->cstream, hipStreamNonBlocking));
+        for (auto &h : c->hin) {
+            HWR_HIP(c, hipEventCreateWithFlags(&h.copied, hipEventDisableTiming));
+            HWR_HIP(c, hipEventCreateWithFlags(&h.read, hipEventDisableTiming));
+        }
+    }
     if (rows <= c->hs_cap) return HWR_OK;
-    void *ptrs[] = {c->d_hemb, c->d_hlen, c->d_hnout, c->d_hchoice, c->d_hslo,
-                    c->d_hval, c->d_hcand, c->d_hqual, c->d_hfeas};
     HWR_HIP(c, hipStreamSynchronize(c->stream));
+    HWR_HIP(c, hipStreamSynchronize(c->cstream));
+    void *ptrs[] = {c->hin[0].emb, c->hin[0].len, c->hin[0].nout, c->hin[0].slo,
+                    c->hin[1].emb, c->hin[1].len, c->hin[1].nout, c->hin[1].slo,
+                    c->d_hchoice, c->d_hval, c->d_hcand, c->d_hqual, c->d_hfeas};
     for (void *p : ptrs)
-        if (p) (void)hipFree(p);          // idle after the synchronisation above
+        if (p) (void)hipFree(p);          // idle after the synchronisations above
+    for (auto &h : c->hin) {
+        h.emb = nullptr;
+        h.len = h.nout = nullptr;
+        h.slo = nullptr;
+        h.used = false;
+    }
+    c->d_hchoice = nullptr;
+    c->d_hval = c->d_hcand = c->d_hqual = nullptr;
+    c->d_hfeas = nullptr;
     c->hs_cap = 0;
     const size_t esz = c->bf16 ? 2 : 4;
-    HWR_HIP(c, hipMalloc(&c->d_hemb, rows * c->D * esz));
-    HWR_HIP(c, dev_alloc(&c->d_hlen, rows));
-    HWR_HIP(c, dev_alloc(&c->d_hnout, rows));
+    for (auto &h : c->hin) {
+        HWR_HIP(c, hipMalloc(&h.emb, rows * c->D * esz));
+        HWR_HIP(c, dev_alloc(&h.len, rows));
+        HWR_HIP(c, dev_alloc(&h.nout, rows));
+        HWR_HIP(c, dev_alloc(&h.slo, rows));
+    }
     HWR_HIP(c, dev_alloc(&c->d_hchoice, rows * c->nw));
-    HWR_HIP(c, dev_alloc(&c->d_hslo, rows));
     HWR_HIP(c, dev_alloc(&c->d_hval, rows * c->nw * 5));
     HWR_HIP(c, dev_alloc(&c->d_hcand, rows * c->N * 3));
     HWR_HIP(c, dev_alloc(&c->d_hqual, rows * c->M));
@@ -757,27 +794,45 @@ hwr_status ensure_host_staging(hwr_ctx *c, size_t rows) {
     return HWR_OK;
 }
 
+// Host-memory batches, chunk by chunk.  Chunk i's inputs go up on the upload
+// stream into input set i % 2, once the kernels that read that set for chunk
+// i - 2 have finished; the context's stream waits for the upload, runs the
+// chunk and brings its outputs down.  The next chunk's upload is issued
+// before this chunk's download, so with pageable caller memory (whose copies
+// the host stages itself) the host stages chunk i + 1 while the device
+// computes chunk i.  Returns when every output is in host memory.
 hwr_status route_host(hwr_ctx *c, const hwr_query_batch *q, hwr_route_result *r) {
     const size_t rows = static_cast<size_t>(std::min(q->n, c->max_chunk));
     hwr_status st = ensure_host_staging(c, rows);
     if (st != HWR_OK) return st;
     const size_t esz = c->bf16 ? 2 : 4;
     const int N = c->N, M = c->M, D = c->D;
-    hipStream_t s = c->stream;
+    hipStream_t s = c->stream, cs = c->cstream;
+    auto upload = [&](int off) -> hwr_status {
+        const int cn = std::min(c->max_chunk, q->n - off);
+        hwr_ctx::InStage &h = c->hin[(off / c->max_chunk) & 1];
+        if (h.used) HWR_HIP(c, hipStreamWaitEvent(cs, h.read, 0));
+        HWR_HIP(c, hipMemcpyAsync(h.emb, static_cast<const char *>(q->emb) + static_cast<size_t>(off) * D * esz,
+                                  static_cast<size_t>(cn) * D * esz, hipMemcpyHostToDevice, cs));
+        HWR_HIP(c, hipMemcpyAsync(h.len, q->input_len + off, cn * 4, hipMemcpyHostToDevice, cs));
+        if (c->NH == 2)
+            HWR_HIP(c, hipMemcpyAsync(h.nout, q->expected_out_len + off, cn * 4, hipMemcpyHostToDevice, cs));
+        if (q->slo_s) HWR_HIP(c, hipMemcpyAsync(h.slo, q->slo_s + off, cn * 4, hipMemcpyHostToDevice, cs));
+        HWR_HIP(c, hipEventRecord(h.copied, cs));
+        return HWR_OK;
+    };
+    st = upload(0);
+    if (st != HWR_OK) return st;
     for (int off = 0; off < q->n; off += c->max_chunk) {
         const int cn = std::min(c->max_chunk, q->n - off);
-        HWR_HIP(c, hipMemcpyAsync(c->d_hemb, static_cast<const char *>(q->emb) + static_cast<size_t>(off) * D * esz,
-                                  static_cast<size_t>(cn) * D * esz, hipMemcpyHostToDevice, s));
-        HWR_HIP(c, hipMemcpyAsync(c->d_hlen, q->input_len + off, cn * 4, hipMemcpyHostToDevice, s));
-        if (c->NH == 2)
-            HWR_HIP(c, hipMemcpyAsync(c->d_hnout, q->expected_out_len + off, cn * 4, hipMemcpyHostToDevice, s));
-        if (q->slo_s) HWR_HIP(c, hipMemcpyAsync(c->d_hslo, q->slo_s + off, cn * 4, hipMemcpyHostToDevice, s));
+        hwr_ctx::InStage &h = c->hin[(off / c->max_chunk) & 1];
+        HWR_HIP(c, hipStreamWaitEvent(s, h.copied, 0));
         DevBatch b{};
         b.n = cn;
-        b.emb = c->d_hemb;
-        b.len = c->d_hlen;
-        b.nout = c->d_hnout;
-        b.slo = q->slo_s ? c->d_hslo : nullptr;
+        b.emb = h.emb;
+        b.len = h.len;
+        b.nout = h.nout;
+        b.slo = q->slo_s ? h.slo : nullptr;
         float *v = c->d_hval;
         const size_t vr = rows * c->nw;              // one [rows][nw] block per output
         b.out = OutArgs{c->d_hchoice, c->d_hfeas, v, v + vr, v + 2 * vr, v + 3 * vr, v + 4 * vr};
@@ -787,6 +842,12 @@ hwr_status route_host(hwr_ctx *c, const hwr_query_batch *q, hwr_route_result *r)
         b.cand_quality = r->cand_quality ? c->d_hqual : nullptr;
         hwr_status rs = route_device(c, b);
         if (rs != HWR_OK) return rs;
+        HWR_HIP(c, hipEventRecord(h.read, s));
+        h.used = true;
+        if (off + c->max_chunk < q->n) {
+            st = upload(off + c->max_chunk);
+            if (st != HWR_OK) return st;
+        }
         auto d2h = [&](void *dst, const void *src, size_t bytes) {
             return hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToHost, s);
         };
@@ -803,8 +864,8 @@ hwr_status route_host(hwr_ctx *c, const hwr_query_batch *q, hwr_route_result *r)
         if (r->cand_nout && c->NH == 3)
             HWR_HIP(c, d2h(r->cand_nout + static_cast<size_t>(off) * N, c->d_hcand + 2 * rows * N, static_cast<size_t>(cn) * N * 4));
         if (r->cand_quality) HWR_HIP(c, d2h(r->cand_quality + static_cast<size_t>(off) * M, c->d_hqual, static_cast<size_t>(cn) * M * 4));
-        HWR_HIP(c, hipStreamSynchronize(s));   // staging is reused by the next chunk
     }
+    HWR_HIP(c, hipStreamSynchronize(s));
     return HWR_OK;
 }
 

@@ -133,6 +133,31 @@ def test_host_equals_device():
     _same(d, h)
 
 
+@pytest.mark.parametrize("name,kw", [
+    ("C2", dict(pipeline="fused")),
+    ("C2", dict(pipeline="staged")),
+    ("C2", dict(pipeline="fused", cost_weights=[0.1, 0.5, 2.0])),
+    ("C1", dict()),
+])
+def test_host_batches_in_several_chunks(name, kw):
+    """Host-memory batches stream their chunks through two input sets (the
+    next chunk's upload overlaps this chunk's kernels): 333 queries in chunks
+    of 100, against the device path in one chunk, bit for bit, candidates
+    included; and the same router routes a second, shorter batch."""
+    heads = 3 if kw.get("cost_weights") is None and name == "C2" and kw["pipeline"] == "staged" else 2
+    sp, pb, st, qs = _case(name, n_queries=333, n_heads=heads)
+    one = G.make_router(pb, **kw)
+    many = G.make_router(pb, max_chunk=100, **kw)
+    one.update(st)
+    many.update(st)
+    d = G.route_device(one, qs, sp.dtype, candidates=True)
+    h = many.route_host(qs.emb_bits, qs.input_len, qs.expected_out_len, qs.slo_s, candidates=True)
+    _same(d, h)
+    sub = qs.slice(0, 150)
+    h2 = many.route_host(sub.emb_bits, sub.input_len, sub.expected_out_len, sub.slo_s, candidates=True)
+    _same({k: v[:150] for k, v in d.items()}, h2)
+
+
 def test_default_slo_used_when_absent():
     sp, pb, st, qs = _case(n_queries=64)
     r = G.make_router(pb, default_slo_s=1.5)
