@@ -232,6 +232,25 @@ def test_maximum_shape():
     assert rep.ok, rep.failures[:5]
 
 
+def test_maximum_shape_fp32():
+    """fp32 at its largest: 1024 pairs (32 models x 8 GPU types, listed four
+    times with their own states), 32 models, D = 8192, H = 128, three heads;
+    ragged query count."""
+    sp = S.spec("C1", n_queries=37, n_models=32, n_gpu_types=8, gpu_width=8, embed_dim=8192,
+                hidden=128, n_heads=3)
+    pb = S.make_problem(sp, 32)
+    pb.dep_model = np.tile(pb.dep_model, 4)
+    pb.dep_gpu = np.tile(pb.dep_gpu, 4)
+    st = np.concatenate([S.make_state(sp, 32 + k) for k in range(4)])
+    qs = S.make_queries(sp, 32)
+    r = G.make_router(pb)
+    r.update(st)
+    out = G.route_device(r, qs, "f32")
+    rep = G.check(pb, st, qs, out)
+    print(f"[parity] fp32 max shape: {rep.summary()}", flush=True)
+    assert rep.ok, rep.failures[:5]
+
+
 def test_unsupported_shapes_are_rejected():
     sp = S.spec("C2", n_queries=4, hidden=96)
     pb = S.make_problem(sp, 1)
