@@ -139,18 +139,19 @@ def throughput(args, hwr, torch, w, pipeline, steps, warmup):
     log(f"{pipeline}: warmup done ({warmup} steps)")
     r.profile(True)
     r.profile_read(reset=True)
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    e0.record(stream)
-    for _ in range(steps):
+    ev[0].record(stream)
+    for i in range(steps):
         step()
-    e1.record(stream)
+        ev[i + 1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     kt = r.profile_read(reset=True)
     r.profile(False)
-    gpu_ms = e0.elapsed_time(e1)
+    gpu_ms = ev[0].elapsed_time(ev[-1])
+    per_step = np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(steps)])
     log(f"{pipeline}: timed {steps} steps: {gpu_ms:.2f} ms (events), {wall * 1e3:.2f} ms (host)")
     choice = out["choice"].cpu().numpy()
     assert (choice >= 0).all() and (choice < N).all(), "choice out of range"
@@ -169,14 +170,22 @@ def throughput(args, hwr, torch, w, pipeline, steps, warmup):
     chunk_cands = nq * N
     flops = predictor_flops(sp.feat_dim, sp.hidden) * chunk_cands
     achieved = flops / (k_avg_ms / 1e3) / 1e12
+    qflops = 2 * nq * D * M
+    qk_ms = k_avg_ms + avg("quality")
+    with_q = (flops + qflops) / (qk_ms / 1e3) / 1e12 if qk_ms > 0 else 0.0
     stages = {k: {"avg_ms": (v[0] / v[1]) if v[1] else 0.0, "launches_per_step": v[1] / steps}
               for k, v in kt.items() if v[1]}
     res = dict(
         value=value, ms_per_step=ms_step, stages=stages,
+        step_ms={"median": float(np.median(per_step)), "p10": float(np.percentile(per_step, 10)),
+                 "p90": float(np.percentile(per_step, 90)), "steps": steps},
         roofline={"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                   "frac": achieved / PEAK_BF16_TFLOPS, "traffic": traffic.get(kname),
                   "kernel": f"k_mlp_bf16<{sp.hidden}> ({pipeline})",
-                  "flop_per_launch": flops, "avg_launch_ms": k_avg_ms},
+                  "flop_per_launch": flops, "avg_launch_ms": k_avg_ms,
+                  # the predictor and the quality GEMM together, per chunk
+                  "with_quality": {"achieved": with_q, "frac": with_q / PEAK_BF16_TFLOPS,
+                                   "flop_per_chunk": flops + qflops}},
         # per chunk: embeddings read, Q matrix written, heads read once
         quality_roofline=hbm_line(nq * (D * 2 + M * 4) + D * 32 * 2, avg("quality"), "k_quality_bf16",
                                   traffic.get("quality")),
@@ -412,9 +421,16 @@ def cpu_baseline(pb, st, sample, sp):
     O.route_synth(pb, st, sample, candidates=False)
     dt = time.perf_counter() - t0
     cands = sample.n * sp.n_deployments
+    cpu = "unknown"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            cpu = next(line.split(":", 1)[1].strip() for line in fh if line.startswith("model name"))
+    except (OSError, StopIteration):
+        pass
     return {"value": cands / dt, "unit": "candidates/s", "cores": 1, "kind": "oracle",
             "sample": f"first {sample.n} queries of chunk 0 x {sp.n_deployments} pairs "
-                      f"({cands} candidates, {dt:.1f} s, one thread)"}
+                      f"({cands} candidates, {dt:.1f} s, one thread)",
+            "host_cpu": cpu, "host_threads": os.cpu_count()}
 
 
 def copy_probe(torch) -> int:
@@ -500,7 +516,7 @@ def main() -> int:
         "data": "synthetic (seeded; stands in for the paper's embedded prompt sets)",
         "config": res["config"], "roofline": res["roofline"], "cpu_baseline": cpu,
         "single_query": single, "single_query_graph_launch": single_graph,
-        "quality_roofline": res["quality_roofline"], "stages": res["stages"],
+        "step_ms": res["step_ms"], "quality_roofline": res["quality_roofline"], "stages": res["stages"],
         "staged_pipeline": staged, "batch_latency": batch, "closed_loop": sim, "closed_loop_pareto": pareto,
     }
     print(json.dumps(line), flush=True)
