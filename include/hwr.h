@@ -221,10 +221,14 @@ enum {
 };
 typedef struct {
     double  ms[HWR_K_COUNT];      /* summed kernel durations, milliseconds       */
-    int64_t launches[HWR_K_COUNT];
+    int64_t launches[HWR_K_COUNT];   /* timed launches                            */
 } hwr_kernel_times;
 
-/* Turn per-launch event timing on (1) or off (0); off by default. */
+/* Per-launch event timing: 0 off (the default), 1 every launch, k > 1 one
+ * launch in k of each kernel kind (the first, then every k-th).  A timed
+ * launch waits a few microseconds longer to be dispatched, so sampling keeps
+ * the timing's cost on back-to-back launches small.  hwr_kernel_times then
+ * counts and sums the timed launches only.  k < 0 is an invalid argument. */
 hwr_status hwr_profile_enable(hwr_ctx *ctx, int32_t enable);
 /* Wait for the timed launches, add their durations into *out (zeroed first),
  * and, if reset != 0, start a new accumulation. */

@@ -106,6 +106,8 @@ struct hwr_ctx {
     hipGraphExec_t gexec = nullptr;
     // timing
     bool prof = false;
+    int prof_every = 1;               // time one launch in prof_every of each kind
+    int64_t prof_seen[HWR_K_COUNT] = {};
     std::vector<Pending> pending;
     std::vector<hipEvent_t> pool;
     double acc_ms[HWR_K_COUNT] = {};
@@ -292,9 +294,14 @@ hipEvent_t take_event(hwr_ctx *c) {
 
 // Time one kernel launch of the library: the two events go into its dispatch
 // (launch_kernel), so they mark the kernel's own start and end on the stream.
+// Whether this launch of `kind` is one of the sampled ones.
+bool sampled(hwr_ctx *c, int kind) {
+    return c->prof && c->prof_seen[kind]++ % c->prof_every == 0;
+}
+
 template <class F>
 hipError_t timed_on(hwr_ctx *c, hipStream_t s, int kind, F &&launch) {
-    if (!c->prof) return launch();
+    if (!sampled(c, kind)) return launch();
     hipEvent_t a = take_event(c), b = take_event(c);
     if (!a || !b) return hipErrorOutOfMemory;
     LaunchEvents &ev = launch_events();
@@ -311,7 +318,7 @@ hipError_t timed_on(hwr_ctx *c, hipStream_t s, int kind, F &&launch) {
 // Time a graph launch: events recorded on the stream before and after it.
 template <class F>
 hipError_t timed_bracket(hwr_ctx *c, hipStream_t s, int kind, F &&launch) {
-    if (!c->prof) return launch();
+    if (!sampled(c, kind)) return launch();
     hipEvent_t a = take_event(c), b = take_event(c);
     if (!a || !b) return hipErrorOutOfMemory;
     hipError_t e = hipEventRecord(a, s);
@@ -1057,7 +1064,10 @@ const char *hwr_last_error(const hwr_ctx *c) {
 
 hwr_status hwr_profile_enable(hwr_ctx *c, int32_t enable) {
     if (!c) return fail(nullptr, HWR_ERR_INVALID_ARG, "ctx is NULL");
+    if (enable < 0) return fail(c, HWR_ERR_INVALID_ARG, "enable must be >= 0");
     c->prof = enable != 0;
+    c->prof_every = enable > 1 ? enable : 1;
+    for (int k = 0; k < HWR_K_COUNT; ++k) c->prof_seen[k] = 0;
     return HWR_OK;
 }
 

@@ -189,8 +189,9 @@ def hwr_last_error(ctx) -> str:
     return m.decode() if m else ""
 
 
-def hwr_profile_enable(ctx, enable: bool) -> None:
-    _check(load().hwr_profile_enable(ctx, 1 if enable else 0), ctx)
+def hwr_profile_enable(ctx, enable) -> None:
+    """enable: False / 0 off, True / 1 every launch, k > 1 one launch in k of each kernel."""
+    _check(load().hwr_profile_enable(ctx, int(enable)), ctx)
 
 
 def hwr_profile_read(ctx, reset: bool = True) -> dict:
@@ -289,7 +290,8 @@ class Router:
     def update(self, state: np.ndarray) -> None:
         hwr_update_hw_state(self.ctx, state)
 
-    def profile(self, enable: bool = True) -> None:
+    def profile(self, enable=True) -> None:
+        """Kernel timing: False off, True every launch, k > 1 one launch in k of each kernel."""
         hwr_profile_enable(self.ctx, enable)
 
     def profile_read(self, reset: bool = True) -> dict:

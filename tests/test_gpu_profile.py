@@ -62,6 +62,35 @@ def test_every_launch_is_timed_and_results_do_not_change(pipeline, kinds):
     assert kt["merge"][1] in (0, 3) and kt["state"][1] <= 1
 
 
+def test_sampled_timing_counts_one_launch_in_k():
+    """hwr_profile_enable(ctx, k > 1) times the first launch of each kind and
+    every k-th after it; results are unchanged, and k < 0 is refused."""
+    import torch
+    pb, st, qs = _case()
+    r = G.make_router(pb, max_chunk=1024)         # 3 chunks: launches 0, 1, 2 of each kind
+    r.update(st)
+    ref = G.route_device(r, qs, "bf16")
+    r.profile(2)
+    r.profile_read(reset=True)
+    got = G.route_device(r, qs, "bf16")
+    kt = r.profile_read(reset=True)
+    for k in ("quality", "fused"):
+        assert kt[k][1] == 2 and kt[k][0] > 0.0, (k, kt[k])
+    r.profile(5)
+    got5 = G.route_device(r, qs, "bf16")
+    kt5 = r.profile_read(reset=True)
+    assert kt5["fused"][1] == 1 and kt5["quality"][1] == 1
+    with pytest.raises(hwr.HwrError) as e:
+        r.profile(-1)
+    assert e.value.status == hwr.HWR_ERR_INVALID_ARG
+    r.profile(False)
+    r.close()
+    torch.cuda.synchronize()
+    for k in ref:
+        assert np.array_equal(ref[k], got[k]), k
+        assert np.array_equal(ref[k], got5[k]), k
+
+
 @pytest.mark.parametrize("flags", [0, hwr.HWR_FLAG_GRAPH])
 def test_single_query_launches_are_timed(flags):
     pb, st, qs = _case(n=8)
