@@ -200,3 +200,29 @@ def test_three_heads_fp32_host():
     rep = G.check(pb, st, qs, out)
     _report("C1 3 heads fp32 host", rep)
     assert rep.max_rel_nout < 1e-5
+
+
+REPLICATES = [
+    # (config, overrides, pipeline): each run at seeds 100 + id and 200 + id
+    ("C1", dict(), "fused"),
+    ("C2", dict(n_queries=1111), "fused"),
+    ("C2", dict(n_queries=1111), "staged"),
+    ("C3", dict(n_queries=777), "fused"),
+    ("C3", dict(n_queries=777), "staged"),
+]
+
+
+@pytest.mark.parametrize("offset", [100, 200])
+@pytest.mark.parametrize("name,kw,pipeline", REPLICATES)
+def test_replicate_seeds(name, kw, pipeline, offset):
+    """Replicate draws of C1-C3 (weights, state and queries all redrawn) at
+    seeds 100 + id and 200 + id, ragged query counts, through the device path."""
+    seed = offset + int(name[1:])
+    sp = S.spec(name, **kw)
+    pb, st, qs = S.make_problem(sp, seed), S.make_state(sp, seed), S.make_queries(sp, seed)
+    r = G.make_router(pb, pipeline=pipeline)
+    r.update(st)
+    out = G.route_device(r, qs, sp.dtype)
+    r.close()
+    _report(f"{name} seed {seed} {pipeline}", G.check(pb, st, qs, out))
+
