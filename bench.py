@@ -258,7 +258,8 @@ def single_query(args, S, hwr, torch, flags=0):
             "mean_us": float(us.mean()), "update_p50_us": float(np.percentile(upd_ns / 1e3, 50)),
             "workload": "C4: 1 query x 32 pairs (16 models x 2 GPU types), embed 768 bf16, "
                         "predictor 24-128-128-2, host I/O, "
-                        + ("kernel launch" if flags == 0 else "graph launch"),
+                        + {0: "kernel launch", hwr.HWR_FLAG_GRAPH: "graph launch",
+                           hwr.HWR_FLAG_RESIDENT: "resident kernel (no launch per call)"}[flags],
             "timing": "host clock around hwr_route_batch (ctypes call included)"}
 
 
@@ -506,9 +507,11 @@ def main() -> int:
             f"epilogue {sr['epilogue_roofline']['frac']:.2f} of HBM")
     single = None if args.no_single else single_query(args, S, hwr, torch)
     single_graph = None if args.no_single else single_query(args, S, hwr, torch, hwr.HWR_FLAG_GRAPH)
+    single_res = None if args.no_single else single_query(args, S, hwr, torch, hwr.HWR_FLAG_RESIDENT)
     if single:
         log(f"single query (kernel launch) p50 {single['p50_us']:.1f} us p99 {single['p99_us']:.1f} us; "
-            f"(graph launch) p50 {single_graph['p50_us']:.1f} us p99 {single_graph['p99_us']:.1f} us")
+            f"(graph launch) p50 {single_graph['p50_us']:.1f} us p99 {single_graph['p99_us']:.1f} us; "
+            f"(resident) p50 {single_res['p50_us']:.1f} us p99 {single_res['p99_us']:.1f} us")
     batch = batch_latency(args, S, hwr, torch) if args.batch_calls > 0 else None
     sim = None if args.no_sim else closed_loop(args, hwr, torch)
     pareto = None if args.no_sim or not args.pareto_weights else closed_loop_pareto(args, hwr, torch)
@@ -520,6 +523,7 @@ def main() -> int:
         "data": "synthetic (seeded; stands in for the paper's embedded prompt sets)",
         "config": res["config"], "roofline": res["roofline"], "cpu_baseline": cpu,
         "single_query": single, "single_query_graph_launch": single_graph,
+        "single_query_resident": single_res,
         "step_ms": res["step_ms"], "quality_roofline": res["quality_roofline"], "stages": res["stages"],
         "staged_pipeline": staged, "batch_latency": batch, "closed_loop": sim, "closed_loop_pareto": pareto,
     }

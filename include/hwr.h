@@ -88,6 +88,8 @@ typedef enum { HWR_PIPE_FUSED = 0, HWR_PIPE_STAGED = 1 } hwr_pipeline;
 
 /* hwr_config.flags */
 #define HWR_FLAG_GRAPH 1          /* single host query: launch a captured graph */
+#define HWR_FLAG_RESIDENT 2       /* single host query: a resident kernel serves it  */
+                                  /* (takes precedence over HWR_FLAG_GRAPH)          */
 
 /* hwr_config.score_mode / bound_mode */
 typedef enum { HWR_SCORE_NORMALIZED = 0, HWR_SCORE_PAPER = 1 } hwr_score_mode;
@@ -197,7 +199,11 @@ hwr_status hwr_update_hw_state(hwr_ctx *ctx, const hwr_hw_state *state, int32_t 
  * HWR_FLAG_GRAPH, one launch of a graph holding that kernel, captured on the
  * first call) on a private stream of the context, reading the query and the
  * newest state from pinned host memory and writing the decision there; it
- * does not wait for batches still enqueued on the context's stream.  Host
+ * does not wait for batches still enqueued on the context's stream.  With
+ * HWR_FLAG_RESIDENT, that kernel stays on the device between calls instead
+ * (one workgroup, polling the pinned request record): a call then costs no
+ * launch.  After about 0.1 s without a request it leaves, and the next call
+ * launches it again; hwr_free stops it.  Host
  * inputs are checked (input_len >= 1, N_out >= 0, SLO > 0 and finite); device
  * inputs are not, and out-of-range values give unspecified choices (all
  * memory accesses stay in bounds). */

@@ -29,6 +29,11 @@ namespace {
 thread_local std::string g_init_error;
 
 constexpr int kStateSlots = 64;     // pinned ring of state snapshots
+// Resident single-query kernel: polls of the request record before it leaves
+// (each one a host-memory round trip plus a short sleep, >= 1 us), and the
+// host idle time after which the kernel may have left and is checked for.
+constexpr uint32_t kResidentPolls = 1u << 16;
+constexpr auto kResidentCheck = std::chrono::milliseconds(20);
 
 struct Pending {
     int kind;
@@ -102,6 +107,9 @@ struct hwr_ctx {
     SingleOut *d_sout = nullptr;
     uint32_t seq = 0;
     hipStream_t sstream = nullptr;   // private stream of the single-query path
+    bool res_launched = false;       // resident single-query kernel launched at least once
+    bool res_stopping = false;       // asked to leave by a batch (which needs every compute unit)
+    std::chrono::steady_clock::time_point res_last{};   // end of the last resident request
     hipGraph_t graph = nullptr;
     hipGraphExec_t gexec = nullptr;
     // timing
@@ -371,6 +379,7 @@ hwr_status check_config(const hwr_config *cfg) {
     if (cfg->weight_dtype == HWR_F32 && cfg->hidden != 64 && cfg->hidden != 128)
         return uns("fp32 hidden width must be 64 or 128");
     if (cfg->pipeline != HWR_PIPE_FUSED && cfg->pipeline != HWR_PIPE_STAGED) return bad("unknown pipeline");
+    if (cfg->flags & ~(HWR_FLAG_GRAPH | HWR_FLAG_RESIDENT)) return bad("unknown flags");
     if (cfg->max_chunk < 0 || cfg->max_chunk > (1 << 22)) return bad("max_chunk must be in [0, 2^22]");
     if (cfg->score_mode != HWR_SCORE_NORMALIZED && cfg->score_mode != HWR_SCORE_PAPER) return bad("unknown score_mode");
     if (cfg->bound_mode != HWR_BOUND_GIVEN && cfg->bound_mode != HWR_BOUND_PAPER) return bad("unknown bound_mode");
@@ -419,6 +428,7 @@ void release(hwr_ctx *c) {
     for (hipEvent_t e : c->pool) (void)hipEventDestroy(e);
     for (int i = 0; i < kStateSlots; ++i)
         if (c->ring_ev[i]) (void)hipEventDestroy(c->ring_ev[i]);
+    if (c->h_sin) __atomic_store_n(&c->h_sin->quit, 1u, __ATOMIC_RELEASE);   // a resident kernel leaves
     if (c->sstream) (void)hipStreamSynchronize(c->sstream);
     if (c->gexec) (void)hipGraphExecDestroy(c->gexec);
     if (c->graph) (void)hipGraphDestroy(c->graph);
@@ -613,6 +623,12 @@ hwr_status sync_state(hwr_ctx *c) {
 hwr_status route_device(hwr_ctx *c, const DevBatch &b) {
     hwr_status st = sync_state(c);
     if (st != HWR_OK) return st;
+    if (c->res_launched && !c->res_stopping) {
+        // a resident single-query workgroup would hold one compute unit that
+        // the batch kernels' last workgroups wait for: ask it to leave
+        __atomic_store_n(&c->h_sin->quit, 1u, __ATOMIC_RELEASE);
+        c->res_stopping = true;
+    }
     const int M = c->M, N = c->N, D = c->D;
     const size_t esz = c->bf16 ? 2 : 4;
     for (int off = 0; off < b.n; off += c->max_chunk) {
@@ -906,6 +922,8 @@ SingleArgs single_args(const hwr_ctx *c) {
     a.b2_pk = c->d_b2_pk;
     a.w3_pk = c->d_w3_pk;
     a.fold_b1 = c->fold_b1;
+    a.last_seq = c->seq;
+    a.max_polls = kResidentPolls;
     return a;
 }
 
@@ -917,7 +935,7 @@ hwr_status single_graph(hwr_ctx *c) {
     hipStream_t cs = nullptr;
     HWR_HIP(c, hipStreamCreateWithFlags(&cs, hipStreamNonBlocking));
     hipError_t e = hipStreamBeginCapture(cs, hipStreamCaptureModeThreadLocal);
-    if (e == hipSuccess) e = launch_single(c->H, a, cs);
+    if (e == hipSuccess) e = launch_single(c->H, false, a, cs);
     hipGraph_t g = nullptr;
     hipError_t e2 = hipStreamEndCapture(cs, &g);
     (void)hipStreamDestroy(cs);
@@ -931,7 +949,78 @@ hwr_status single_graph(hwr_ctx *c) {
     return HWR_OK;
 }
 
+void read_single_out(const hwr_ctx *c, hwr_route_result *r) {
+    const SingleOut *o = c->h_sout;
+    r->choice[0] = o->choice;
+    if (r->feasible) r->feasible[0] = static_cast<uint8_t>(o->feasible);
+    if (r->utility) r->utility[0] = o->utility;
+    if (r->e2e_s) r->e2e_s[0] = o->e2e;
+    if (r->ttft_s) r->ttft_s[0] = o->ttft;
+    if (r->tpot_s) r->tpot_s[0] = o->tpot;
+    if (r->nout) r->nout[0] = o->nout;
+}
+
+// Resident single-query path (HWR_FLAG_RESIDENT): the kernel stays on the
+// device between calls and polls the request record.  It is (re)launched
+// when it has never run or may have left after its idle polls; a kernel that
+// left while a request was being written is detected and relaunched.
+hwr_status route_resident(hwr_ctx *c, const hwr_query_batch *q, hwr_route_result *r) {
+    SingleIn *in = c->h_sin;
+    const uint32_t prev = c->seq;
+    const uint32_t seq = ++c->seq == 0 ? ++c->seq : c->seq;
+    auto launch = [&]() -> hwr_status {
+        SingleArgs a = single_args(c);
+        a.last_seq = prev;            // the pending request, if already posted, is newer
+        __atomic_store_n(&in->quit, 0u, __ATOMIC_RELAXED);
+        HWR_HIP(c, launch_single(c->H, true, a, c->sstream));
+        c->res_launched = true;
+        return HWR_OK;
+    };
+    if (c->res_stopping) {            // leaves within one poll of the quit flag
+        HWR_HIP(c, hipStreamSynchronize(c->sstream));
+        c->res_stopping = false;
+        hwr_status st = launch();
+        if (st != HWR_OK) return st;
+    }
+    const auto now = std::chrono::steady_clock::now();
+    if (!c->res_launched || now - c->res_last > kResidentCheck) {
+        const hipError_t qe = hipStreamQuery(c->sstream);
+        if (qe == hipSuccess) {
+            hwr_status st = launch();
+            if (st != HWR_OK) return st;
+        } else if (qe != hipErrorNotReady) {
+            return hip_fail(c, qe, "resident single-query kernel");
+        }
+    }
+    in->input_len = q->input_len[0];
+    in->nout = c->NH == 2 ? q->expected_out_len[0] : 0;
+    in->slo = q->slo_s ? q->slo_s[0] : c->default_slo;
+    std::memcpy(in + 1, q->emb, static_cast<size_t>(c->D) * 2);
+    std::atomic_thread_fence(std::memory_order_release);
+    __atomic_store_n(&in->seq, seq, __ATOMIC_RELEASE);
+    volatile uint32_t *flag = &c->h_sout->seq;
+    const auto t0 = std::chrono::steady_clock::now();
+    uint64_t spins = 0;
+    while (*flag != seq) {
+        if ((++spins & 0xFFF) == 0) {
+            const hipError_t qe = hipStreamQuery(c->sstream);
+            if (qe != hipSuccess && qe != hipErrorNotReady) return hip_fail(c, qe, "resident single-query kernel");
+            if (qe == hipSuccess && *flag != seq) {   // it left before seeing this request
+                hwr_status st = launch();
+                if (st != HWR_OK) return st;
+            }
+            if (std::chrono::steady_clock::now() - t0 > std::chrono::seconds(10))
+                return fail(c, HWR_ERR_HIP, "resident single-query kernel did not answer within 10 s");
+        }
+    }
+    std::atomic_thread_fence(std::memory_order_acquire);
+    c->res_last = std::chrono::steady_clock::now();
+    read_single_out(c, r);
+    return HWR_OK;
+}
+
 hwr_status route_single(hwr_ctx *c, const hwr_query_batch *q, hwr_route_result *r) {
+    if (c->flags & HWR_FLAG_RESIDENT) return route_resident(c, q, r);
     hwr_status st = single_graph(c);
     if (st != HWR_OK) return st;
     SingleIn *in = c->h_sin;
@@ -946,7 +1035,7 @@ hwr_status route_single(hwr_ctx *c, const hwr_query_batch *q, hwr_route_result *
         HWR_HIP(c, timed_bracket(c, c->sstream, HWR_K_SINGLE, [&] { return hipGraphLaunch(c->gexec, c->sstream); }));
     } else {
         const SingleArgs a = single_args(c);
-        HWR_HIP(c, timed_on(c, c->sstream, HWR_K_SINGLE, [&] { return launch_single(c->H, a, c->sstream); }));
+        HWR_HIP(c, timed_on(c, c->sstream, HWR_K_SINGLE, [&] { return launch_single(c->H, false, a, c->sstream); }));
     }
     // wait for the decision record (written last by the kernel, system scope)
     volatile uint32_t *flag = &c->h_sout->seq;
@@ -963,14 +1052,7 @@ hwr_status route_single(hwr_ctx *c, const hwr_query_batch *q, hwr_route_result *
         }
     }
     std::atomic_thread_fence(std::memory_order_acquire);
-    const SingleOut *o = c->h_sout;
-    r->choice[0] = o->choice;
-    if (r->feasible) r->feasible[0] = static_cast<uint8_t>(o->feasible);
-    if (r->utility) r->utility[0] = o->utility;
-    if (r->e2e_s) r->e2e_s[0] = o->e2e;
-    if (r->ttft_s) r->ttft_s[0] = o->ttft;
-    if (r->tpot_s) r->tpot_s[0] = o->tpot;
-    if (r->nout) r->nout[0] = o->nout;
+    read_single_out(c, r);
     return HWR_OK;
 }
 

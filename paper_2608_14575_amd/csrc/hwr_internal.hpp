@@ -188,10 +188,11 @@ struct MergeArgs {
 
 // Single query, all pairs: input and output records in pinned host memory.
 struct SingleIn {
-    uint32_t seq;
+    uint32_t seq;                 // request number, written last by the host
+    uint32_t quit;                // resident kernel: leave (set by the host at teardown)
     int32_t input_len, nout;
     float slo;
-    uint32_t pad[4];
+    uint32_t pad[3];
     // followed by D bf16 embedding values (16-byte aligned)
 };
 struct SingleOut {
@@ -218,6 +219,8 @@ struct SingleArgs {
     const float *b1_pk, *b2_pk;
     const uint32_t *w3_pk;
     int fold_b1;                  // feature rows carry 1.0 in the folded-bias slots
+    uint32_t last_seq;            // resident: the request answered last (waits for a newer one)
+    uint32_t max_polls;           // resident: polls without a request before the kernel leaves
 };
 
 // ---------------------------------------------------------------- launchers
@@ -231,6 +234,6 @@ hipError_t launch_mlp_f32(int H, const MlpF32Args &a, hipStream_t s);
 hipError_t launch_gather(const GatherArgs &a, hipStream_t s);
 hipError_t launch_epilogue(const EpilogueArgs &a, hipStream_t s);
 hipError_t launch_merge(const MergeArgs &a, hipStream_t s);
-hipError_t launch_single(int H, const SingleArgs &a, hipStream_t s);
+hipError_t launch_single(int H, bool resident, const SingleArgs &a, hipStream_t s);
 
 }  // namespace hwr

@@ -1,7 +1,8 @@
 // Single-query routing kernel of libhwr (gfx950): one query against all
 // pairs in one workgroup, reading the query and the pairs' current runtime
 // signals from pinned host memory and writing the decision there, so that
-// one launch (captured once in a graph) is the whole call.  Pairs are the MFMA columns here (32 per tile); the 4 waves
+// one launch (captured once in a graph) is the whole call -- or, in the
+// resident form, one launch serves a stream of queries.  Pairs are the MFMA columns here (32 per tile); the 4 waves
 // split the second-layer row tiles and combine their head partials in LDS.
 #include "hwr_device.hpp"
 
@@ -60,7 +61,15 @@ __device__ __forceinline__ uint64_t wave_max(uint64_t k) {
     return best;
 }
 
-template <int H>
+// RES = false: one launch per query.  RES = true: the resident form, one
+// launch serving successive queries.  Thread 0 polls the request record's
+// sequence number (pinned host memory, system scope) and the workgroup
+// serves each new request in turn.  The weights and the pairs' static
+// features are loaded for the first request only; the signals, the query
+// and the feature rows are read again for every request, after a
+// system-scope acquire.  The workgroup leaves when the host sets `quit`, or
+// after max_polls polls without a request: every wait ends.
+template <int H, bool RES>
 __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
     constexpr int MT = H / 32, KB2 = H / 16;
     constexpr int MO = (MT + 3) / 4;          // second-layer row tiles per wave
@@ -77,18 +86,52 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
     __shared__ float s_bq[kMaxModels];
     __shared__ float s_q[kMaxModels];
     __shared__ float s_z[4][32][kMaxHeads];
+    __shared__ uint32_t s_ctl[2];             // resident: request found, its sequence number
     const int NH = a.nheads;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, n = lane & 31, h = lane >> 5;
     const int b0 = a.arch_width + a.gpu_width;
     const int j8 = tid & 7, ks = (j8 - b0) & 7;
 
-    // ---- phase 1: every independent load is issued before any is waited
-    // for -- host memory first (query record, runtime signals), then the
-    // device-side weights -- so the phase costs one host round trip.
-    const u32x4 hdr = *reinterpret_cast<const u32x4 *>(a.in);   // seq, input_len, nout, slo
     const int p0 = tid >> 3;
     const bool has0 = p0 < a.N;
     const int pc0 = has0 ? p0 : 0;
+    // pair p0's static features, and the weights held in registers, live
+    // across the requests of the resident form
+    float prm0 = 0.0f;
+    int ia0 = 0, ig0 = 0, md0 = 0;
+    constexpr int MOH = MO == 1 ? 1 : 0;     // second-layer tiles held in registers
+    bf16x8 fw2[MO][KB2];
+    bf16x8 wq0[kHeldM][kHeldS], wq1[kHeldM][kHeldS];
+    uint32_t last = a.last_seq;
+    for (int iter = 0;; ++iter) {
+    if constexpr (RES) {
+        // ---- wait for a request: thread 0 polls, a bounded number of times
+        if (tid == 0) {
+            uint32_t found = 0, sq = last;
+            for (uint32_t it = 0; it < a.max_polls; ++it) {
+                const uint64_t hq = __hip_atomic_load(reinterpret_cast<const uint64_t *>(a.in), __ATOMIC_RELAXED,
+                                                      __HIP_MEMORY_SCOPE_SYSTEM);   // seq, quit
+                sq = static_cast<uint32_t>(hq);
+                if (sq != last) {
+                    found = 1;
+                    break;
+                }
+                if (static_cast<uint32_t>(hq >> 32) != 0) break;
+                __builtin_amdgcn_s_sleep(4);
+            }
+            s_ctl[0] = found;
+            s_ctl[1] = sq;
+        }
+        __syncthreads();
+        if (s_ctl[0] == 0) return;
+        last = s_ctl[1];
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");   // system scope: the request record and the signals
+    }
+    // ---- phase 1: every independent load is issued before any is waited
+    // for -- host memory first (query record, runtime signals), then the
+    // device-side weights -- so the phase costs one host round trip.
+    const u32x4 hdr = *reinterpret_cast<const u32x4 *>(a.in);   // seq, quit, input_len, nout
+    const float slo = reinterpret_cast<const float *>(a.in)[4];
     // (loads are unconditional, indices clamped into range: a load under a
     // branch makes the compiler wait for it, and for all earlier ones, there)
     const uint32_t raw0 = reinterpret_cast<const uint32_t *>(a.state + pc0)[ks >= 2 ? ks - 2 : 0];
@@ -98,12 +141,16 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
         const int idx = tid + 256 * i;
         re[i] = reinterpret_cast<const u32x4 *>(a.in + 1)[idx < a.D / 8 ? idx : 0];
     }
-    const float prm0 = a.pair_params[pc0];
-    const int ia0 = a.pair_arch[pc0], ig0 = a.arch_width + a.dep_gpu[pc0];
-    const int md0 = a.dep_model[pc0];
+    const bool first = !RES || iter == 0;
+    if (first) {
+        prm0 = a.pair_params[pc0];
+        ia0 = a.pair_arch[pc0];
+        ig0 = a.arch_width + a.dep_gpu[pc0];
+        md0 = a.dep_model[pc0];
+    }
     u32x4 rw1[kW1];
 #pragma unroll
-    for (int i = 0; i < kW1; ++i) rw1[i] = reinterpret_cast<const u32x4 *>(a.w1_pk)[tid + 256 * i];
+    for (int i = 0; i < kW1; ++i) rw1[i] = first ? reinterpret_cast<const u32x4 *>(a.w1_pk)[tid + 256 * i] : u32x4{};
     // b1 tiles (MT * 8 pieces), b2 tiles (MT * 8), head pairs (MT * 4 * NH)
     const int nbw = MT * 16 + MT * 4 * NH;
     u32x4 rbw;
@@ -114,12 +161,10 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
         const u32x4 *src = reinterpret_cast<const u32x4 *>(t == 0 ? static_cast<const void *>(a.b1_pk)
                                                            : t == 1 ? static_cast<const void *>(a.b2_pk)
                                                                     : static_cast<const void *>(a.w3_pk));
-        rbw = src[k];
+        rbw = first ? src[k] : u32x4{};
     }
-    const float rbq = a.bq[tid < a.M ? tid : 0];
-    constexpr int MOH = MO == 1 ? 1 : 0;     // second-layer tiles held in registers
-    bf16x8 fw2[MO][KB2];
-    {
+    const float rbq = first ? a.bq[tid < a.M ? tid : 0] : 0.0f;
+    if (first) {
         const bf16x8 *w2 = reinterpret_cast<const bf16x8 *>(a.w2_pk);
 #pragma unroll
         for (int i = 0; i < MOH; ++i) {
@@ -128,7 +173,7 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
             for (int kb = 0; kb < KB2; ++kb) fw2[i][kb] = w2[(mo * KB2 + kb) * 64 + lane];
         }
     }
-    bf16x8 wq0[kHeldM][kHeldS], wq1[kHeldM][kHeldS];
+    if (first) {
 #pragma unroll
     for (int jm = 0; jm < kHeldM; ++jm) {
         const int m0 = wave + 8 * jm < a.M ? wave + 8 * jm : 0;
@@ -140,10 +185,10 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
             wq1[jm][i] = *reinterpret_cast<const bf16x8 *>(a.wqT + static_cast<size_t>(m1) * a.D + k);
         }
     }
-    const uint32_t seq = hdr[0];
-    const int32_t len = static_cast<int32_t>(hdr[1]);
-    const int32_t no = static_cast<int32_t>(hdr[2]);
-    const float slo = __uint_as_float(hdr[3]);
+    }
+    const uint32_t seq = RES ? last : hdr[0];
+    const int32_t len = static_cast<int32_t>(hdr[2]);
+    const int32_t no = static_cast<int32_t>(hdr[3]);
 
     // ---- phase 2: LDS stores, the feature rows, one barrier
 #pragma unroll
@@ -151,11 +196,13 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
         const int idx = tid + 256 * i;
         if (idx < a.D / 8) reinterpret_cast<u32x4 *>(s_emb)[idx] = re[i];
     }
+    if (first) {
 #pragma unroll
-    for (int i = 0; i < kW1; ++i) reinterpret_cast<u32x4 *>(s_w1)[tid + 256 * i] = rw1[i];
-    if (tid < MT * 16) s_bw[0][tid] = rbw;
-    else if (tid < nbw) s_w3p[tid - MT * 16] = rbw;
-    if (tid < a.M) s_bq[tid] = rbq;
+        for (int i = 0; i < kW1; ++i) reinterpret_cast<u32x4 *>(s_w1)[tid + 256 * i] = rw1[i];
+        if (tid < MT * 16) s_bw[0][tid] = rbw;
+        else if (tid < nbw) s_w3p[tid - MT * 16] = rbw;
+        if (tid < a.M) s_bq[tid] = rbq;
+    }
     if (has0) {
         pair_row(s_row[p0], j8, b0, ks, ia0, ig0, raw0, prm0, len, a.fold_b1 != 0);
         if (j8 == 0) s_model[p0] = md0;
@@ -329,13 +376,23 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
             __hip_atomic_store(&o->seq, seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
         }
     }
+    if constexpr (!RES) break;
+    }   // requests
 }
 
-hipError_t launch_single(int H, const SingleArgs &a, hipStream_t s) {
+hipError_t launch_single(int H, bool resident, const SingleArgs &a, hipStream_t s) {
+    if (resident) {
+        switch (H) {
+            case 64: return launch_kernel(k_single<64, true>, dim3(1), dim3(256), 0, s, a);
+            case 128: return launch_kernel(k_single<128, true>, dim3(1), dim3(256), 0, s, a);
+            case 256: return launch_kernel(k_single<256, true>, dim3(1), dim3(256), 0, s, a);
+            default: return hipErrorInvalidValue;
+        }
+    }
     switch (H) {
-        case 64: return launch_kernel(k_single<64>, dim3(1), dim3(256), 0, s, a);
-        case 128: return launch_kernel(k_single<128>, dim3(1), dim3(256), 0, s, a);
-        case 256: return launch_kernel(k_single<256>, dim3(1), dim3(256), 0, s, a);
+        case 64: return launch_kernel(k_single<64, false>, dim3(1), dim3(256), 0, s, a);
+        case 128: return launch_kernel(k_single<128, false>, dim3(1), dim3(256), 0, s, a);
+        case 256: return launch_kernel(k_single<256, false>, dim3(1), dim3(256), 0, s, a);
         default: return hipErrorInvalidValue;
     }
 }

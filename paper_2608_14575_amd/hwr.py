@@ -21,6 +21,7 @@ HWR_F32, HWR_BF16 = 0, 1
 HWR_MEM_DEVICE, HWR_MEM_HOST = 0, 1
 HWR_PIPE_FUSED, HWR_PIPE_STAGED = 0, 1
 HWR_FLAG_GRAPH = 1
+HWR_FLAG_RESIDENT = 2
 HWR_SCORE_NORMALIZED, HWR_SCORE_PAPER = 0, 1
 HWR_BOUND_GIVEN, HWR_BOUND_PAPER = 0, 1
 HWR_MAX_WEIGHTS = 8
