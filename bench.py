@@ -102,8 +102,9 @@ def prepare(args, S, torch):
         slo[a:b] = torch.from_numpy(qs.slo_s).to(dev)
         if c == 0:
             sample = qs.slice(0, args.cpu_sample)
+            sample_wide = qs.slice(0, 4 * args.cpu_sample)
         log(f"generated chunk {c + 1}/{sp.n_chunks}")
-    return dict(sp=sp, pb=pb, st=st, emb=emb, il=il, no=no, slo=slo, sample=sample)
+    return dict(sp=sp, pb=pb, st=st, emb=emb, il=il, no=no, slo=slo, sample=sample, sample_wide=sample_wide)
 
 
 def hbm_line(nbytes: float, avg_ms: float, kernel: str, traffic=None) -> dict:
@@ -417,15 +418,33 @@ def _idle_state(w, hwr):
     return st
 
 
-def cpu_baseline(pb, st, sample, sp):
+def cpu_baseline(pb, st, sample, sp, sample_wide=None):
     """The CPU oracle (plain C, one thread) on a bounded sample of the same
-    workload: the first queries of chunk 0 against all pairs."""
+    workload: the first queries of chunk 0 against all pairs.  With
+    `sample_wide`, also the same oracle on all host threads (up to 16, the
+    CPU share of one GPU): one shard of the wider sample per thread (the C
+    call releases the interpreter lock)."""
     from oracle import oracle as O
     O.build(force=False)
+    O.lib()
     t0 = time.perf_counter()
     O.route_synth(pb, st, sample, candidates=False)
     dt = time.perf_counter() - t0
     cands = sample.n * sp.n_deployments
+    wide = None
+    if sample_wide is not None:
+        from concurrent.futures import ThreadPoolExecutor
+        threads = max(1, min(os.cpu_count() or 1, 16))
+        bounds = np.linspace(0, sample_wide.n, threads + 1).astype(int)
+        shards = [sample_wide.slice(int(a), int(b)) for a, b in zip(bounds[:-1], bounds[1:]) if b > a]
+        t1 = time.perf_counter()
+        with ThreadPoolExecutor(max_workers=len(shards)) as ex:
+            list(ex.map(lambda q: O.route_synth(pb, st, q, candidates=False), shards))
+        dtw = time.perf_counter() - t1
+        wc = sample_wide.n * sp.n_deployments
+        wide = {"value": wc / dtw, "unit": "candidates/s", "cores": len(shards),
+                "sample": f"first {sample_wide.n} queries of chunk 0 x {sp.n_deployments} pairs "
+                          f"({wc} candidates, {dtw:.1f} s, {len(shards)} threads)"}
     cpu = "unknown"
     try:
         with open("/proc/cpuinfo") as fh:
@@ -435,7 +454,7 @@ def cpu_baseline(pb, st, sample, sp):
     return {"value": cands / dt, "unit": "candidates/s", "cores": 1, "kind": "oracle",
             "sample": f"first {sample.n} queries of chunk 0 x {sp.n_deployments} pairs "
                       f"({cands} candidates, {dt:.1f} s, one thread)",
-            "host_cpu": cpu, "host_threads": os.cpu_count()}
+            "host_cpu": cpu, "host_threads": os.cpu_count(), "all_cores": wide}
 
 
 def copy_probe(torch) -> int:
@@ -515,7 +534,7 @@ def main() -> int:
     batch = batch_latency(args, S, hwr, torch) if args.batch_calls > 0 else None
     sim = None if args.no_sim else closed_loop(args, hwr, torch)
     pareto = None if args.no_sim or not args.pareto_weights else closed_loop_pareto(args, hwr, torch)
-    cpu = None if args.no_cpu_baseline else cpu_baseline(w["pb"], w["st"], w["sample"], w["sp"])
+    cpu = None if args.no_cpu_baseline else cpu_baseline(w["pb"], w["st"], w["sample"], w["sp"], w["sample_wide"])
     line = {
         "metric": METRIC, "value": res["value"], "unit": "candidates/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": res["ms_per_step"],
