@@ -823,8 +823,22 @@ hwr_status ensure_host_staging(hwr_ctx *c, size_t rows) {
 // chunk and brings its outputs down.  The next chunk's upload is issued
 // before this chunk's download, so with pageable caller memory (whose copies
 // the host stages itself) the host stages chunk i + 1 while the device
-// computes chunk i.  Returns when every output is in host memory.
+// computes chunk i.  Returns when every output is in host memory, or, on an
+// error, once both streams have drained.
+hwr_status route_host_chunks(hwr_ctx *c, const hwr_query_batch *q, hwr_route_result *r);
+
 hwr_status route_host(hwr_ctx *c, const hwr_query_batch *q, hwr_route_result *r) {
+    const hwr_status st = route_host_chunks(c, q, r);
+    if (st != HWR_OK) {
+        // copies may still read the caller's buffers or write its results:
+        // let both streams drain before the caller gets control back
+        if (c->cstream) (void)hipStreamSynchronize(c->cstream);
+        (void)hipStreamSynchronize(c->stream);
+    }
+    return st;
+}
+
+hwr_status route_host_chunks(hwr_ctx *c, const hwr_query_batch *q, hwr_route_result *r) {
     const size_t rows = static_cast<size_t>(std::min(q->n, c->max_chunk));
     hwr_status st = ensure_host_staging(c, rows);
     if (st != HWR_OK) return st;
