@@ -620,6 +620,25 @@ hwr_status sync_state(hwr_ctx *c) {
     return HWR_OK;
 }
 
+MlpF32Args f32_args(const hwr_ctx *c, const QueryArgs &qa) {
+    MlpF32Args fa{};
+    fa.N = c->N;
+    fa.F = c->F;
+    fa.len_slot = c->len_slot;
+    fa.b3_0 = c->b3[0];
+    fa.b3_1 = c->b3[1];
+    fa.b3_2 = c->b3[2];
+    fa.nheads = c->NH;
+    fa.q = qa;
+    fa.dep_f32 = c->d_dep_f32;
+    fa.w1 = c->d_w1;
+    fa.b1 = c->d_b1;
+    fa.w2 = c->d_w2;
+    fa.b2 = c->d_b2;
+    fa.w3 = c->d_w3;
+    return fa;
+}
+
 hwr_status route_device(hwr_ctx *c, const DevBatch &b) {
     hwr_status st = sync_state(c);
     if (st != HWR_OK) return st;
@@ -727,21 +746,7 @@ hwr_status route_device(hwr_ctx *c, const DevBatch &b) {
                 HWR_HIP(c, timed(c, HWR_K_MLP, [&] { return launch_mlp_bf16(c->H, true, ma, c->stream); }));
             }
         } else {
-            MlpF32Args fa{};
-            fa.N = N;
-            fa.F = c->F;
-            fa.len_slot = c->len_slot;
-            fa.b3_0 = c->b3[0];
-            fa.b3_1 = c->b3[1];
-            fa.b3_2 = c->b3[2];
-            fa.nheads = c->NH;
-            fa.q = qa;
-            fa.dep_f32 = c->d_dep_f32;
-            fa.w1 = c->d_w1;
-            fa.b1 = c->d_b1;
-            fa.w2 = c->d_w2;
-            fa.b2 = c->d_b2;
-            fa.w3 = c->d_w3;
+            MlpF32Args fa = f32_args(c, qa);
             fa.cand_ttft = ctt ? ctt : c->d_ctt;
             fa.cand_tpot = ctp ? ctp : c->d_ctp;
             fa.cand_nout = cno ? cno : c->d_cno;

@@ -32,11 +32,9 @@ hipError_t launch_state(const StateArgs &a, hipStream_t s) {
 // Hardware-independent quality (Sec. 3.2 item 3): Q[q][m] = e_q . Wq[:, m] + bq[m].
 // fp32 workloads; one wave per query.  Lane l accumulates every model over
 // k = l, l + 64, ... (the embedding row and Wq's rows k, M consecutive
-// floats each, are read lane-contiguous), then a DPP sum per model.
-__global__ __launch_bounds__(256) void k_quality_f32(QualityArgs a) {
-    const int lane = threadIdx.x & 63;
-    const int q = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    if (q >= a.nq) return;                       // the whole wave
+// floats each, are read lane-contiguously), then a DPP sum per model; lane m
+// writes model m's value to dst[m].
+__device__ __forceinline__ void quality_row_f32(const QualityArgs &a, int q, int lane, float *dst) {
     const float *e = static_cast<const float *>(a.emb) + static_cast<size_t>(q) * a.D;
     const int M = a.M;
     float acc[kMaxModels];
@@ -53,9 +51,16 @@ __global__ __launch_bounds__(256) void k_quality_f32(QualityArgs a) {
     for (int m = 0; m < kMaxModels; ++m) {
         if (m < M) {
             const float v = wave_sum(acc[m]);
-            if (lane == m) a.qmat[static_cast<size_t>(q) * M + m] = v + a.bq[m];
+            if (lane == m) dst[m] = v + a.bq[m];
         }
     }
+}
+
+__global__ __launch_bounds__(256) void k_quality_f32(QualityArgs a) {
+    const int lane = threadIdx.x & 63;
+    const int q = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    if (q >= a.nq) return;                       // the whole wave
+    quality_row_f32(a, q, lane, a.qmat + static_cast<size_t>(q) * a.M);
 }
 
 hipError_t launch_quality_f32(const QualityArgs &a, hipStream_t s) {
@@ -63,29 +68,105 @@ hipError_t launch_quality_f32(const QualityArgs &a, hipStream_t s) {
 }
 
 // ------------------------------------------------------------ fp32 predictor
-// Eq. 1 predictor in fp32, one wave per candidate (q, d); waves stride over
-// the candidates.  Lane l holds hidden units l and (H = 128) l + 64.  Layer 1
-// reads the pair's feature row as wave-uniform values; layer 2 broadcasts
-// each first-layer unit with readlane; the heads are DPP sums, then softplus.
-// Both hidden layers accumulate in input order from the bias, one rounding
-// per fused multiply-add.  Weights staged in LDS as [input][unit] rows, so
-// the lanes of a wave read consecutive words.
+// Eq. 1 predictor in fp32, one wave per candidate (q, d).  Lane l holds
+// hidden units l and (H = 128) l + 64.  Layer 1 reads the pair's feature row
+// as wave-uniform values; layer 2 broadcasts each first-layer unit with
+// readlane; the heads are DPP sums, then softplus.  Both hidden layers
+// accumulate in input order from the bias, one rounding per fused
+// multiply-add.  Weights staged in LDS as [input][unit] rows, so the lanes of
+// a wave read consecutive words.
+template <int H>
+struct alignas(16) F32Weights {
+    float w1[kFeatPad * H];
+    float w2[H * H];
+    float w3[H * kMaxHeads];
+    float b1[H];
+    float b2[H];
+};
+
+// Copy the weights into LDS (256 threads).  Trip counts are compile-time
+// bounds and the copies move 16 bytes, so every load of a thread is issued
+// before its first store: one memory round trip, not one per iteration.
+template <int T, int CAP>
+__device__ __forceinline__ void copy_f32x4(float *dst, const float *src, int count) {
+    const int n4 = count / 4;                 // counts are multiples of 4 here
+    f32x4 v[(CAP / 4 + T - 1) / T];
+#pragma unroll
+    for (int i = 0; i < (CAP / 4 + T - 1) / T; ++i) {
+        const int k = threadIdx.x + i * T;
+        if (k < n4) v[i] = reinterpret_cast<const f32x4 *>(src)[k];
+    }
+#pragma unroll
+    for (int i = 0; i < (CAP / 4 + T - 1) / T; ++i) {
+        const int k = threadIdx.x + i * T;
+        if (k < n4) reinterpret_cast<f32x4 *>(dst)[k] = v[i];
+    }
+}
+
+template <int H>
+__device__ __forceinline__ void stage_f32(const MlpF32Args &a, F32Weights<H> &s) {
+    copy_f32x4<256, kFeatPad * H>(s.w1, a.w1, a.F * H);
+    copy_f32x4<256, H * H>(s.w2, a.w2, H * H);
+    copy_f32x4<256, H * kMaxHeads>(s.w3, a.w3, H * a.nheads);
+    copy_f32x4<256, H>(s.b1, a.b1, H);
+    copy_f32x4<256, H>(s.b2, a.b2, H);
+}
+
+// Candidate (q, d) on one wave (q and d wave-uniform): TTFT, TPOT and the
+// third head's N_out, the same value in every lane.
+template <int H>
+__device__ __forceinline__ void predict_f32(const MlpF32Args &a, const F32Weights<H> &s, long q, int d, int lane,
+                                            float &tt, float &tp, float &nc) {
+    constexpr int U = H / 64;
+    const int NH = a.nheads;
+    const float xl = len_feature(a.q.input_len[q]);
+    const float *row = a.dep_f32 + static_cast<size_t>(d) * kFeatPad;
+    float h1[U], h2[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) h1[u] = s.b1[lane + 64 * u];
+    for (int f = 0; f < a.F; ++f) {
+        const float x = (f == a.len_slot) ? xl : row[f];
+#pragma unroll
+        for (int u = 0; u < U; ++u) h1[u] = fmaf(s.w1[f * H + lane + 64 * u], x, h1[u]);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        h1[u] = fmaxf(h1[u], 0.0f);
+        h2[u] = s.b2[lane + 64 * u];
+    }
+#pragma unroll
+    for (int v = 0; v < U; ++v) {
+        const int hv = __float_as_int(h1[v]);
+#pragma unroll
+        for (int i = 0; i < 64; ++i) {
+            const float x = __int_as_float(__builtin_amdgcn_readlane(hv, i));
+            const float *w = s.w2 + (64 * v + i) * H + lane;
+#pragma unroll
+            for (int u = 0; u < U; ++u) h2[u] = fmaf(w[64 * u], x, h2[u]);
+        }
+    }
+    float z0 = 0.0f, z1 = 0.0f, z2 = 0.0f;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const float h = fmaxf(h2[u], 0.0f);
+        const int j = lane + 64 * u;
+        z0 = fmaf(s.w3[NH * j + 0], h, z0);
+        z1 = fmaf(s.w3[NH * j + 1], h, z1);
+        if (NH == 3) z2 = fmaf(s.w3[NH * j + 2], h, z2);
+    }
+    z0 = wave_sum(z0);
+    z1 = wave_sum(z1);
+    if (NH == 3) z2 = wave_sum(z2);
+    tt = softplus_f32(z0 + a.b3_0);
+    tp = softplus_f32(z1 + a.b3_1);
+    nc = NH == 3 ? softplus_f32(z2 + a.b3_2) : 0.0f;
+}
+
+// Waves stride over the candidates of the chunk.
 template <int H>
 __global__ __launch_bounds__(256) void k_mlp_f32(MlpF32Args a) {
-    constexpr int U = H / 64;
-    __shared__ float s_w1[kFeatPad * H];
-    __shared__ float s_w2[H * H];
-    __shared__ float s_w3[H * kMaxHeads];
-    __shared__ float s_b1[H];
-    __shared__ float s_b2[H];
-    const int NH = a.nheads;
-    for (int i = threadIdx.x; i < a.F * H; i += blockDim.x) s_w1[i] = a.w1[i];
-    for (int i = threadIdx.x; i < H * H; i += blockDim.x) s_w2[i] = a.w2[i];
-    for (int i = threadIdx.x; i < H * NH; i += blockDim.x) s_w3[i] = a.w3[i];
-    for (int i = threadIdx.x; i < H; i += blockDim.x) {
-        s_b1[i] = a.b1[i];
-        s_b2[i] = a.b2[i];
-    }
+    __shared__ F32Weights<H> s;
+    stage_f32<H>(a, s);
     __syncthreads();
     const int lane = threadIdx.x & 63;
     const long total = static_cast<long>(a.q.nq) * a.N;
@@ -94,48 +175,12 @@ __global__ __launch_bounds__(256) void k_mlp_f32(MlpF32Args a) {
          c < total; c += stride) {
         const long q = c / a.N;
         const int d = static_cast<int>(c - q * a.N);
-        const float xl = len_feature(a.q.input_len[q]);
-        const float *row = a.dep_f32 + static_cast<size_t>(d) * kFeatPad;
-        float h1[U], h2[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) h1[u] = s_b1[lane + 64 * u];
-        for (int f = 0; f < a.F; ++f) {
-            const float x = (f == a.len_slot) ? xl : row[f];
-#pragma unroll
-            for (int u = 0; u < U; ++u) h1[u] = fmaf(s_w1[f * H + lane + 64 * u], x, h1[u]);
-        }
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            h1[u] = fmaxf(h1[u], 0.0f);
-            h2[u] = s_b2[lane + 64 * u];
-        }
-#pragma unroll
-        for (int v = 0; v < U; ++v) {
-            const int hv = __float_as_int(h1[v]);
-#pragma unroll
-            for (int i = 0; i < 64; ++i) {
-                const float x = __int_as_float(__builtin_amdgcn_readlane(hv, i));
-                const float *w = s_w2 + (64 * v + i) * H + lane;
-#pragma unroll
-                for (int u = 0; u < U; ++u) h2[u] = fmaf(w[64 * u], x, h2[u]);
-            }
-        }
-        float z0 = 0.0f, z1 = 0.0f, z2 = 0.0f;
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const float h = fmaxf(h2[u], 0.0f);
-            const int j = lane + 64 * u;
-            z0 = fmaf(s_w3[NH * j + 0], h, z0);
-            z1 = fmaf(s_w3[NH * j + 1], h, z1);
-            if (NH == 3) z2 = fmaf(s_w3[NH * j + 2], h, z2);
-        }
-        z0 = wave_sum(z0);
-        z1 = wave_sum(z1);
-        if (NH == 3) z2 = wave_sum(z2);
+        float tt, tp, nc;
+        predict_f32<H>(a, s, q, d, lane, tt, tp, nc);
         if (lane == 0) {
-            a.cand_ttft[c] = softplus_f32(z0 + a.b3_0);
-            a.cand_tpot[c] = softplus_f32(z1 + a.b3_1);
-            if (NH == 3) a.cand_nout[c] = softplus_f32(z2 + a.b3_2);
+            a.cand_ttft[c] = tt;
+            a.cand_tpot[c] = tp;
+            if (a.nheads == 3) a.cand_nout[c] = nc;
         }
     }
 }

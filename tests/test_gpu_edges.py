@@ -98,6 +98,19 @@ def test_quality_unroll_is_invisible():
     _same(G.route_device(big, qs, "bf16"), G.route_device(small, qs, "bf16"))
 
 
+@pytest.mark.parametrize("kw", [dict(), dict(n_heads=3), dict(n_heads=3, **S.PAPER_SLO, score_mode=1)])
+def test_fp32_chunking_is_invisible(kw):
+    """fp32 path (quality, predictor, decision epilogue): 1500 queries in one
+    chunk and in three chunks of 500 give the same outputs, candidates and Q
+    matrix included; two and three heads, the paper's rules."""
+    sp, pb, st, qs = _case("C1", n_queries=1500, seed=14, **kw)
+    three = G.make_router(pb, max_chunk=1500)
+    one = G.make_router(pb, max_chunk=500)
+    three.update(st)
+    one.update(st)
+    _same(G.route_device(three, qs, "f32"), G.route_device(one, qs, "f32"))
+
+
 def test_fused_equals_staged_and_split_equals_unsplit():
     """Same arithmetic per candidate in every mode: bit-identical outputs.
     40 queries over 64 pairs makes the fused kernel split the pairs over
