@@ -148,23 +148,46 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
     __shared__ float s_mnout[NH == 3 ? kQPerBlock : 1];
     const int tid = threadIdx.x;
     {
-        const uint4 *g;
-        uint4 *d;
-        g = reinterpret_cast<const uint4 *>(a.w1_pk);
-        d = reinterpret_cast<uint4 *>(s_w1);
-        for (int i = tid; i < MT * 2 * 64; i += kMlpThreads) d[i] = g[i];
-        g = reinterpret_cast<const uint4 *>(a.w2_pk);
-        d = reinterpret_cast<uint4 *>(s_w2);
-        for (int i = tid; i < MT * KB2 * 64; i += kMlpThreads) d[i] = g[i];
-        g = reinterpret_cast<const uint4 *>(a.b1_pk);
-        d = reinterpret_cast<uint4 *>(s_b1);
-        for (int i = tid; i < MT * 2 * 4; i += kMlpThreads) d[i] = g[i];
-        g = reinterpret_cast<const uint4 *>(a.b2_pk);
-        d = reinterpret_cast<uint4 *>(s_b2);
-        for (int i = tid; i < MT * 2 * 4; i += kMlpThreads) d[i] = g[i];
-        g = reinterpret_cast<const uint4 *>(a.w3_frag);
-        d = reinterpret_cast<uint4 *>(s_w3f);
-        for (int i = tid; i < KB2 * W3S; i += kMlpThreads) d[i] = g[i];
+        // Every load of the staging is issued before the first LDS store:
+        // one memory round trip for the whole prologue.  Indices past an
+        // array's end are clamped for the loads and skipped for the stores.
+        constexpr int nW1 = MT * 2 * 64, nW2 = MT * KB2 * 64, nB = MT * 2 * 4, nW3 = KB2 * W3S;
+        constexpr int pW1 = (nW1 + kMlpThreads - 1) / kMlpThreads;
+        constexpr int pW2 = (nW2 + kMlpThreads - 1) / kMlpThreads;
+        const uint4 *g1 = reinterpret_cast<const uint4 *>(a.w1_pk);
+        const uint4 *g2 = reinterpret_cast<const uint4 *>(a.w2_pk);
+        const uint4 *gb1 = reinterpret_cast<const uint4 *>(a.b1_pk);
+        const uint4 *gb2 = reinterpret_cast<const uint4 *>(a.b2_pk);
+        const uint4 *g3 = reinterpret_cast<const uint4 *>(a.w3_frag);
+        uint4 v1[pW1], v2[pW2];
+#pragma unroll
+        for (int i = 0; i < pW1; ++i) {
+            const int k = tid + i * kMlpThreads;
+            v1[i] = g1[k < nW1 ? k : 0];
+        }
+#pragma unroll
+        for (int i = 0; i < pW2; ++i) {
+            const int k = tid + i * kMlpThreads;
+            v2[i] = g2[k < nW2 ? k : 0];
+        }
+        static_assert(nB <= kMlpThreads && nW3 <= kMlpThreads, "one bias / head piece per thread");
+        const uint4 vb1 = gb1[tid < nB ? tid : 0], vb2 = gb2[tid < nB ? tid : 0];
+        const uint4 v3 = g3[tid < nW3 ? tid : 0];
+#pragma unroll
+        for (int i = 0; i < pW1; ++i) {
+            const int k = tid + i * kMlpThreads;
+            if (k < nW1) reinterpret_cast<uint4 *>(s_w1)[k] = v1[i];
+        }
+#pragma unroll
+        for (int i = 0; i < pW2; ++i) {
+            const int k = tid + i * kMlpThreads;
+            if (k < nW2) reinterpret_cast<uint4 *>(s_w2)[k] = v2[i];
+        }
+        if (tid < nB) {
+            reinterpret_cast<uint4 *>(s_b1)[tid] = vb1;
+            reinterpret_cast<uint4 *>(s_b2)[tid] = vb2;
+        }
+        if (tid < nW3) reinterpret_cast<uint4 *>(s_w3f)[tid] = v3;
     }
     __syncthreads();
 
