@@ -43,6 +43,32 @@ def test_every_declared_symbol_is_exported(lib):
         assert hasattr(lib, n)
 
 
+def test_constants_match_header(tmp_path):
+    """Every HWR_ enumerator and macro of include/*.h, as the C compiler sees
+    it, has a binding constant of the same name and value."""
+    names = set()
+    for h in HEADERS:
+        txt = open(h).read()
+        names |= set(re.findall(r"^#define (HWR_[A-Z0-9_]+)\s+\S", txt, re.M))
+        for body in re.findall(r"enum\s*(?:\w+\s*)?\{(.*?)\}", txt, re.S):
+            names |= set(re.findall(r"\b(HWR_[A-Z0-9_]+)\s*(?:=|,|$)", body, re.M))
+    names.discard("HWR_H")
+    names = {n for n in names if not n.endswith("_H")}
+    assert len(names) > 20, names
+    src = ['#include <stdio.h>', '#include "hwr.h"', '#include "hwr_sim.h"', "int main(void) {"]
+    src += [f'printf("{n} %lld\\n", (long long)({n}));' for n in sorted(names)]
+    src.append("return 0; }")
+    c = tmp_path / "consts.c"
+    c.write_text("\n".join(src))
+    exe = tmp_path / "consts"
+    subprocess.check_call(["gcc", "-std=c11", f"-I{os.path.join(ROOT, 'include')}", str(c), "-o", str(exe)])
+    got = dict(line.split() for line in subprocess.check_output([str(exe)], text=True).splitlines())
+    missing = sorted(n for n in names if not hasattr(hwr, n))
+    assert not missing, missing
+    for n, v in got.items():
+        assert getattr(hwr, n) == int(v), (n, getattr(hwr, n), v)
+
+
 def test_struct_layout_matches_header(tmp_path):
     """offsetof / sizeof from the C compiler against the ctypes mirror."""
     fields = {
