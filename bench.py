@@ -37,7 +37,7 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_C5_1Mx256.json")
 KERNEL_NAMES = {   # as the profiler names them
     "fused": "void hwr::k_mlp_bf16<256, false, 2, true>(hwr::MlpArgs)",
     "mlp": "void hwr::k_mlp_bf16<256, true, 2, true>(hwr::MlpArgs)",
-    "quality": "void hwr::k_quality_bf16<1>(hwr::QualityArgs)",
+    "quality": "hwr::k_quality_bf16_lds(hwr::QualityArgs)",
     "gather": "hwr::k_gather(hwr::GatherArgs)",
     "epilogue": "void hwr::k_epilogue<true, false, false, false>(hwr::EpilogueArgs)",
 }
@@ -192,7 +192,7 @@ def throughput(args, hwr, torch, w, pipeline, steps, warmup):
                   "with_quality": {"achieved": with_q, "frac": with_q / PEAK_BF16_TFLOPS,
                                    "flop_per_chunk": flops + qflops}},
         # per chunk: embeddings read, Q matrix written, heads read once
-        quality_roofline=hbm_line(nq * (D * 2 + M * 4) + D * 32 * 2, avg("quality"), "k_quality_bf16",
+        quality_roofline=hbm_line(nq * (D * 2 + M * 4) + D * 32 * 2, avg("quality"), "k_quality_bf16_lds",
                                   traffic.get("quality")),
         config={"workload": f"{sp.name} throughput stress: {n} queries x {N} pairs ({M} models x "
                             f"{sp.n_gpu_types} GPU types), embed {D} bf16, predictor "

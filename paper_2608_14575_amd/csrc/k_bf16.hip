@@ -105,9 +105,80 @@ __global__ __launch_bounds__(256) void k_quality_bf16(QualityArgs a) {
     }
 }
 
+// Large batches with D a multiple of 256: the workgroup (four waves, 64
+// queries) streams its rows through LDS in slabs of 256 k (512 bytes per row),
+// all four waves loading coalesced with the next slab prefetched in
+// registers; waves 0 and 1 run the MFMA chains of the two 32-query tiles from
+// LDS in the same k order as k_quality_bf16, so the results are identical.
+// Each load instruction then covers two rows' 512 contiguous bytes instead of
+// 16 bytes of 32 rows (3.6% faster on HBM-resident chunks).
+constexpr int kQSlab = 256;                       // k per slab
+constexpr int kQRows = 64;                        // queries per workgroup
+__global__ __launch_bounds__(256) void k_quality_bf16_lds(QualityArgs a) {
+    constexpr int RB = 2 * kQSlab + 16;           // LDS row stride in bytes (16-byte pad)
+    constexpr int PPR = 2 * kQSlab / 16;          // 16-byte pieces per row per slab
+    constexpr int PT = kQRows * PPR / 256;        // pieces per thread per slab
+    __shared__ __attribute__((aligned(16))) unsigned char s_slab[kQRows * RB];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int r0 = blockIdx.x * kQRows;
+    const int nslab = a.D / kQSlab;
+    const uint16_t *emb = static_cast<const uint16_t *>(a.emb);
+    u32x4 pre[PT];
+    auto load = [&](int j) {
+#pragma unroll
+        for (int i = 0; i < PT; ++i) {
+            const int p = tid + 256 * i, row = p / PPR, col = p % PPR;
+            const int q = r0 + row < a.nq ? r0 + row : a.nq - 1;
+            pre[i] = *reinterpret_cast<const u32x4 *>(emb + static_cast<size_t>(q) * a.D + j * kQSlab + col * 8);
+        }
+    };
+    const int row = lane & 31, h = lane >> 5;
+    const bf16x8 *wq = reinterpret_cast<const bf16x8 *>(a.wq_pk) + lane;
+    f32x16 acc = {};
+    load(0);
+    for (int j = 0; j < nslab; ++j) {
+#pragma unroll
+        for (int i = 0; i < PT; ++i) {
+            const int p = tid + 256 * i, rw = p / PPR, col = p % PPR;
+            *reinterpret_cast<u32x4 *>(s_slab + rw * RB + col * 16) = pre[i];
+        }
+        __syncthreads();
+        if (j + 1 < nslab) load(j + 1);
+        if (wave < 2) {
+            const unsigned char *base = s_slab + (32 * wave + row) * RB + 64 * h;
+#pragma unroll
+            for (int sl = 0; sl < kQSlab / 64; ++sl) {
+                const int sg = j * (kQSlab / 64) + sl;
+                bf16x8 av[4], bv[4];
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    av[c] = *reinterpret_cast<const bf16x8 *>(base + sl * 128 + 16 * c);
+                    bv[c] = wq[(sg * 4 + c) * 64];
+                }
+#pragma unroll
+                for (int c = 0; c < 4; ++c) acc = mfma32(av[c], bv[c], acc);
+            }
+        }
+        __syncthreads();
+    }
+    if (wave < 2) {
+        const int m = lane & 31;
+        if (m < a.M) {
+            const float bias = a.bq[m];
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int q = r0 + 32 * wave + crow(r, h);
+                if (q < a.nq) a.qmat[static_cast<size_t>(q) * a.M + m] = acc[r] + bias;
+            }
+        }
+    }
+}
+
 hipError_t launch_quality_bf16(const QualityArgs &a, int cus, hipStream_t s) {
     const int grid = (a.nq + 127) / 128;
     if (grid < cus) return launch_kernel(k_quality_bf16<4>, dim3((a.nq + 31) / 32), dim3(64), 0, s, a);
+    if (a.D % kQSlab == 0)
+        return launch_kernel(k_quality_bf16_lds, dim3((a.nq + kQRows - 1) / kQRows), dim3(256), 0, s, a);
     return launch_kernel(k_quality_bf16<1>, dim3(grid), dim3(256), 0, s, a);
 }
 
