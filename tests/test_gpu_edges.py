@@ -82,15 +82,17 @@ def test_chunking_is_invisible(pipeline):
     _same(G.route_device(a, qs, "bf16"), G.route_device(b, qs, "bf16"))
 
 
-def test_quality_unroll_is_invisible():
-    """The quality GEMM loads four embedding slices ahead when its grid is
-    smaller than the device, one otherwise; its MFMA chain is the same, so a
-    batch routed in one large chunk and in small chunks gives bit-identical
-    outputs, Q matrix included."""
+@pytest.mark.parametrize("embed_dim", [768, 576])
+def test_quality_unroll_is_invisible(embed_dim):
+    """The quality GEMM has three forms with one MFMA chain order: small
+    grids load four embedding slices ahead (one wave per workgroup); large
+    ones stream rows through LDS when D is a multiple of 256 (768), else load
+    one slice at a time (576).  A batch routed in one large chunk and in
+    small chunks gives bit-identical outputs, Q matrix included."""
     import torch
     cus = torch.cuda.get_device_properties(0).multi_processor_count
     n = 128 * cus + 5                       # one chunk: grid above the CU count
-    sp, pb, st, qs = _case(n_queries=n, seed=13)
+    sp, pb, st, qs = _case(n_queries=n, seed=13, embed_dim=embed_dim)
     big = G.make_router(pb, max_chunk=n)
     small = G.make_router(pb, max_chunk=128 * (cus // 2))
     big.update(st)
