@@ -207,12 +207,30 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
         pair_row(s_row[p0], j8, b0, ks, ia0, ig0, raw0, prm0, len, a.fold_b1 != 0);
         if (j8 == 0) s_model[p0] = md0;
     }
-    for (int p = p0 + 32; p < a.N; p += 32) {       // more than 32 pairs
-        const uint32_t raw = ks >= 2 ? reinterpret_cast<const uint32_t *>(a.state + p)[ks - 2] : 0u;
-        const float prm = ks == 0 ? a.pair_params[p] : 1.0f;
-        pair_row(s_row[p], j8, b0, ks, a.pair_arch[p], a.arch_width + a.dep_gpu[p], raw, prm, len,
-                 a.fold_b1 != 0);
-        if (j8 == 0) s_model[p] = a.dep_model[p];
+    // more than 32 pairs: eight further pairs per thread per round trip (the
+    // signals come from host memory; loads unconditional, indices clamped)
+    for (int pb = p0 + 32; pb < a.N; pb += 32 * 8) {
+        uint32_t raw[8];
+        float prm[8];
+        int ia[8], ig[8], md[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int p = pb + 32 * i < a.N ? pb + 32 * i : 0;
+            raw[i] = reinterpret_cast<const uint32_t *>(a.state + p)[ks >= 2 ? ks - 2 : 0];
+            prm[i] = a.pair_params[p];
+            ia[i] = a.pair_arch[p];
+            ig[i] = a.arch_width + a.dep_gpu[p];
+            md[i] = a.dep_model[p];
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int p = pb + 32 * i;
+            if (p < a.N) {
+                pair_row(s_row[p], j8, b0, ks, ia[i], ig[i], ks >= 2 ? raw[i] : 0u, ks == 0 ? prm[i] : 1.0f, len,
+                         a.fold_b1 != 0);
+                if (j8 == 0) s_model[p] = md[i];
+            }
+        }
     }
     __syncthreads();
 
