@@ -104,297 +104,297 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
     bf16x8 wq0[kHeldM][kHeldS], wq1[kHeldM][kHeldS];
     uint32_t last = a.last_seq;
     for (int iter = 0;; ++iter) {
-    if constexpr (RES) {
-        // ---- wait for a request: thread 0 polls, a bounded number of times
-        if (tid == 0) {
-            uint32_t found = 0, sq = last;
-            for (uint32_t it = 0; it < a.max_polls; ++it) {
-                const uint64_t hq = __hip_atomic_load(reinterpret_cast<const uint64_t *>(a.in), __ATOMIC_RELAXED,
-                                                      __HIP_MEMORY_SCOPE_SYSTEM);   // seq, quit
-                sq = static_cast<uint32_t>(hq);
-                if (sq != last) {
-                    found = 1;
-                    break;
+        if constexpr (RES) {
+            // ---- wait for a request: thread 0 polls, a bounded number of times
+            if (tid == 0) {
+                uint32_t found = 0, sq = last;
+                for (uint32_t it = 0; it < a.max_polls; ++it) {
+                    const uint64_t hq = __hip_atomic_load(reinterpret_cast<const uint64_t *>(a.in), __ATOMIC_RELAXED,
+                                                          __HIP_MEMORY_SCOPE_SYSTEM);   // seq, quit
+                    sq = static_cast<uint32_t>(hq);
+                    if (sq != last) {
+                        found = 1;
+                        break;
+                    }
+                    if (static_cast<uint32_t>(hq >> 32) != 0) break;
+                    __builtin_amdgcn_s_sleep(4);
                 }
-                if (static_cast<uint32_t>(hq >> 32) != 0) break;
-                __builtin_amdgcn_s_sleep(4);
+                s_ctl[0] = found;
+                s_ctl[1] = sq;
             }
-            s_ctl[0] = found;
-            s_ctl[1] = sq;
+            __syncthreads();
+            if (s_ctl[0] == 0) return;
+            last = s_ctl[1];
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");   // system scope: the request record and the signals
         }
-        __syncthreads();
-        if (s_ctl[0] == 0) return;
-        last = s_ctl[1];
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");   // system scope: the request record and the signals
-    }
-    // ---- phase 1: every independent load is issued before any is waited
-    // for -- host memory first (query record, runtime signals), then the
-    // device-side weights -- so the phase costs one host round trip.
-    const u32x4 hdr = *reinterpret_cast<const u32x4 *>(a.in);   // seq, quit, input_len, nout
-    const float slo = reinterpret_cast<const float *>(a.in)[4];
-    // (loads are unconditional, indices clamped into range: a load under a
-    // branch makes the compiler wait for it, and for all earlier ones, there)
-    const uint32_t raw0 = reinterpret_cast<const uint32_t *>(a.state + pc0)[ks >= 2 ? ks - 2 : 0];
-    u32x4 re[kEmb];
-#pragma unroll
-    for (int i = 0; i < kEmb; ++i) {
-        const int idx = tid + 256 * i;
-        re[i] = reinterpret_cast<const u32x4 *>(a.in + 1)[idx < a.D / 8 ? idx : 0];
-    }
-    const bool first = !RES || iter == 0;
-    if (first) {
-        prm0 = a.pair_params[pc0];
-        ia0 = a.pair_arch[pc0];
-        ig0 = a.arch_width + a.dep_gpu[pc0];
-        md0 = a.dep_model[pc0];
-    }
-    u32x4 rw1[kW1];
-#pragma unroll
-    for (int i = 0; i < kW1; ++i) rw1[i] = first ? reinterpret_cast<const u32x4 *>(a.w1_pk)[tid + 256 * i] : u32x4{};
-    // b1 tiles (MT * 8 pieces), b2 tiles (MT * 8), head pairs (MT * 4 * NH)
-    const int nbw = MT * 16 + MT * 4 * NH;
-    u32x4 rbw;
-    {
-        const int tb = tid < nbw ? tid : 0;
-        const int t = tb < MT * 8 ? 0 : tb < MT * 16 ? 1 : 2;
-        const int k = tb - t * (MT * 8);
-        const u32x4 *src = reinterpret_cast<const u32x4 *>(t == 0 ? static_cast<const void *>(a.b1_pk)
-                                                           : t == 1 ? static_cast<const void *>(a.b2_pk)
-                                                                    : static_cast<const void *>(a.w3_pk));
-        rbw = first ? src[k] : u32x4{};
-    }
-    const float rbq = first ? a.bq[tid < a.M ? tid : 0] : 0.0f;
-    if (first) {
-        const bf16x8 *w2 = reinterpret_cast<const bf16x8 *>(a.w2_pk);
-#pragma unroll
-        for (int i = 0; i < MOH; ++i) {
-            const int mo = wave + 4 * i < MT ? wave + 4 * i : 0;
-#pragma unroll
-            for (int kb = 0; kb < KB2; ++kb) fw2[i][kb] = w2[(mo * KB2 + kb) * 64 + lane];
+        // ---- phase 1: every independent load is issued before any is waited
+        // for -- host memory first (query record, runtime signals), then the
+        // device-side weights -- so the phase costs one host round trip.
+        const u32x4 hdr = *reinterpret_cast<const u32x4 *>(a.in);   // seq, quit, input_len, nout
+        const float slo = reinterpret_cast<const float *>(a.in)[4];
+        // (loads are unconditional, indices clamped into range: a load under a
+        // branch makes the compiler wait for it, and for all earlier ones, there)
+        const uint32_t raw0 = reinterpret_cast<const uint32_t *>(a.state + pc0)[ks >= 2 ? ks - 2 : 0];
+        u32x4 re[kEmb];
+    #pragma unroll
+        for (int i = 0; i < kEmb; ++i) {
+            const int idx = tid + 256 * i;
+            re[i] = reinterpret_cast<const u32x4 *>(a.in + 1)[idx < a.D / 8 ? idx : 0];
         }
-    }
-    if (first) {
-#pragma unroll
-    for (int jm = 0; jm < kHeldM; ++jm) {
-        const int m0 = wave + 8 * jm < a.M ? wave + 8 * jm : 0;
-        const int m1 = wave + 8 * jm + 4 < a.M ? wave + 8 * jm + 4 : m0;
-#pragma unroll
-        for (int i = 0; i < kHeldS; ++i) {
-            const int k = (lane + 64 * i) * 8 < a.D ? (lane + 64 * i) * 8 : 0;
-            wq0[jm][i] = *reinterpret_cast<const bf16x8 *>(a.wqT + static_cast<size_t>(m0) * a.D + k);
-            wq1[jm][i] = *reinterpret_cast<const bf16x8 *>(a.wqT + static_cast<size_t>(m1) * a.D + k);
+        const bool first = !RES || iter == 0;
+        if (first) {
+            prm0 = a.pair_params[pc0];
+            ia0 = a.pair_arch[pc0];
+            ig0 = a.arch_width + a.dep_gpu[pc0];
+            md0 = a.dep_model[pc0];
         }
-    }
-    }
-    const uint32_t seq = RES ? last : hdr[0];
-    const int32_t len = static_cast<int32_t>(hdr[2]);
-    const int32_t no = static_cast<int32_t>(hdr[3]);
-
-    // ---- phase 2: LDS stores, the feature rows, one barrier
-#pragma unroll
-    for (int i = 0; i < kEmb; ++i) {
-        const int idx = tid + 256 * i;
-        if (idx < a.D / 8) reinterpret_cast<u32x4 *>(s_emb)[idx] = re[i];
-    }
-    if (first) {
-#pragma unroll
-        for (int i = 0; i < kW1; ++i) reinterpret_cast<u32x4 *>(s_w1)[tid + 256 * i] = rw1[i];
-        if (tid < MT * 16) s_bw[0][tid] = rbw;
-        else if (tid < nbw) s_w3p[tid - MT * 16] = rbw;
-        if (tid < a.M) s_bq[tid] = rbq;
-    }
-    if (has0) {
-        pair_row(s_row[p0], j8, b0, ks, ia0, ig0, raw0, prm0, len, a.fold_b1 != 0);
-        if (j8 == 0) s_model[p0] = md0;
-    }
-    // more than 32 pairs: eight further pairs per thread per round trip (the
-    // signals come from host memory; loads unconditional, indices clamped)
-    for (int pb = p0 + 32; pb < a.N; pb += 32 * 8) {
-        uint32_t raw[8];
-        float prm[8];
-        int ia[8], ig[8], md[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int p = pb + 32 * i < a.N ? pb + 32 * i : 0;
-            raw[i] = reinterpret_cast<const uint32_t *>(a.state + p)[ks >= 2 ? ks - 2 : 0];
-            prm[i] = a.pair_params[p];
-            ia[i] = a.pair_arch[p];
-            ig[i] = a.arch_width + a.dep_gpu[p];
-            md[i] = a.dep_model[p];
-        }
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int p = pb + 32 * i;
-            if (p < a.N) {
-                pair_row(s_row[p], j8, b0, ks, ia[i], ig[i], ks >= 2 ? raw[i] : 0u, ks == 0 ? prm[i] : 1.0f, len,
-                         a.fold_b1 != 0);
-                if (j8 == 0) s_model[p] = md[i];
-            }
-        }
-    }
-    __syncthreads();
-
-    const float nout = static_cast<float>(no < 0 ? 0 : no);
-    const QueryRule qrule = query_rule(a.rule, slo, len, nout, a.w);
-    Best best = best_none();
-    const int ntiles = (a.N + 31) / 32;
-    for (int ct = 0; ct < ntiles; ++ct) {
-        const int d = ct * 32 + n;
-        const bool vd = d < a.N;
-        const int dc = vd ? d : 0;
-        // ---- features of pair d (zero columns past the last pair)
-        bf16x8 xf[2];
+        u32x4 rw1[kW1];
+    #pragma unroll
+        for (int i = 0; i < kW1; ++i) rw1[i] = first ? reinterpret_cast<const u32x4 *>(a.w1_pk)[tid + 256 * i] : u32x4{};
+        // b1 tiles (MT * 8 pieces), b2 tiles (MT * 8), head pairs (MT * 4 * NH)
+        const int nbw = MT * 16 + MT * 4 * NH;
+        u32x4 rbw;
         {
-            const u32x4 *row = reinterpret_cast<const u32x4 *>(s_row[dc]);
-            const u32x4 z = {0, 0, 0, 0};
-            xf[0] = __builtin_bit_cast(bf16x8, vd ? row[h] : z);
-            xf[1] = __builtin_bit_cast(bf16x8, vd ? row[2 + h] : z);
+            const int tb = tid < nbw ? tid : 0;
+            const int t = tb < MT * 8 ? 0 : tb < MT * 16 ? 1 : 2;
+            const int k = tb - t * (MT * 8);
+            const u32x4 *src = reinterpret_cast<const u32x4 *>(t == 0 ? static_cast<const void *>(a.b1_pk)
+                                                               : t == 1 ? static_cast<const void *>(a.b2_pk)
+                                                                        : static_cast<const void *>(a.w3_pk));
+            rbw = first ? src[k] : u32x4{};
         }
-        const int model = s_model[dc];
-        // ---- layer 1 (every wave, all row tiles; weights from LDS)
-        bf16x8 h1[KB2];
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-            f32x16 acc;
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const f32x4 bt = __builtin_bit_cast(f32x4, s_bw[0][(mt * 2 + h) * 4 + i]);
-#pragma unroll
-                for (int j = 0; j < 4; ++j) acc[4 * i + j] = bt[j];
-            }
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb) acc = mfma32s(s_w1[(mt * 2 + kb) * 64 + lane], xf[kb], acc);
-            h1[2 * mt] = relu_pack8s(acc, 0);
-            h1[2 * mt + 1] = relu_pack8s(acc, 8);
-        }
-        // ---- layer 2 row tiles of this wave, folded into the heads
-        float z0 = 0.0f, z1 = 0.0f, z2 = 0.0f;
-#pragma unroll
-        for (int i = 0; i < MO; ++i) {
-            if (wave + 4 * i >= MT) break;
-            const int mo = wave + 4 * i;
-            if (i >= MOH) {
-                const bf16x8 *w2 = reinterpret_cast<const bf16x8 *>(a.w2_pk);
-#pragma unroll
+        const float rbq = first ? a.bq[tid < a.M ? tid : 0] : 0.0f;
+        if (first) {
+            const bf16x8 *w2 = reinterpret_cast<const bf16x8 *>(a.w2_pk);
+    #pragma unroll
+            for (int i = 0; i < MOH; ++i) {
+                const int mo = wave + 4 * i < MT ? wave + 4 * i : 0;
+    #pragma unroll
                 for (int kb = 0; kb < KB2; ++kb) fw2[i][kb] = w2[(mo * KB2 + kb) * 64 + lane];
             }
-            f32x16 acc;
-#pragma unroll
-            for (int p = 0; p < 4; ++p) {
-                const f32x4 bt = __builtin_bit_cast(f32x4, s_bw[1][(mo * 2 + h) * 4 + p]);
-#pragma unroll
-                for (int j = 0; j < 4; ++j) acc[4 * p + j] = bt[j];
-            }
-#pragma unroll
-            for (int kb = 0; kb < KB2; ++kb) acc = mfma32s(fw2[i][kb], h1[kb], acc);
-            const u32x4 *w3 = &s_w3p[(mo * 2 + h) * 2 * NH];
-            const u32x4 wa = w3[0], wb = w3[1], wc = w3[2], wd = w3[3];
-            const u32x4 we = NH == 3 ? w3[4] : u32x4{0, 0, 0, 0};
-            const u32x4 wf = NH == 3 ? w3[5] : u32x4{0, 0, 0, 0};
-#pragma unroll
-            for (int p = 0; p < 8; ++p) {
-                const bf16x2 hp = relu_bf16x2(acc[2 * p], acc[2 * p + 1]);
-                const uint32_t u0 = p < 4 ? wa[p & 3] : wb[p & 3];
-                const uint32_t u1 = p < 4 ? wc[p & 3] : wd[p & 3];
-                const uint32_t u2 = p < 4 ? we[p & 3] : wf[p & 3];
-                z0 = __builtin_amdgcn_fdot2_f32_bf16(hp, __builtin_bit_cast(bf16x2, u0), z0, false);
-                z1 = __builtin_amdgcn_fdot2_f32_bf16(hp, __builtin_bit_cast(bf16x2, u1), z1, false);
-                z2 = __builtin_amdgcn_fdot2_f32_bf16(hp, __builtin_bit_cast(bf16x2, u2), z2, false);
+        }
+        if (first) {
+    #pragma unroll
+        for (int jm = 0; jm < kHeldM; ++jm) {
+            const int m0 = wave + 8 * jm < a.M ? wave + 8 * jm : 0;
+            const int m1 = wave + 8 * jm + 4 < a.M ? wave + 8 * jm + 4 : m0;
+    #pragma unroll
+            for (int i = 0; i < kHeldS; ++i) {
+                const int k = (lane + 64 * i) * 8 < a.D ? (lane + 64 * i) * 8 : 0;
+                wq0[jm][i] = *reinterpret_cast<const bf16x8 *>(a.wqT + static_cast<size_t>(m0) * a.D + k);
+                wq1[jm][i] = *reinterpret_cast<const bf16x8 *>(a.wqT + static_cast<size_t>(m1) * a.D + k);
             }
         }
-        z0 += __shfl_xor(z0, 32);
-        z1 += __shfl_xor(z1, 32);
-        z2 += __shfl_xor(z2, 32);
-        if (h == 0) {
-            s_z[wave][n][0] = z0;
-            s_z[wave][n][1] = z1;
-            s_z[wave][n][2] = z2;
         }
-        // ---- quality of every model (Sec. 3.2 item 3), once: wave w takes
-        // models w, w + 4, w + 8, ...; lanes split D
-        if (ct == 0) {
-            // models wave + 8j and wave + 8j + 4; the first kHeldM pairs use the
-            // heads already in registers for the first kHeldS slices of D
-            auto finish = [&](float acc0, float acc1, int m0, int m1) {
-                acc0 = wave_sum(acc0);
-                acc1 = wave_sum(acc1);
-                if (lane == 0) {
-                    s_q[m0] = acc0 + s_bq[m0];
-                    if (m1 < a.M) s_q[m1] = acc1 + s_bq[m1];
+        const uint32_t seq = RES ? last : hdr[0];
+        const int32_t len = static_cast<int32_t>(hdr[2]);
+        const int32_t no = static_cast<int32_t>(hdr[3]);
+
+        // ---- phase 2: LDS stores, the feature rows, one barrier
+    #pragma unroll
+        for (int i = 0; i < kEmb; ++i) {
+            const int idx = tid + 256 * i;
+            if (idx < a.D / 8) reinterpret_cast<u32x4 *>(s_emb)[idx] = re[i];
+        }
+        if (first) {
+    #pragma unroll
+            for (int i = 0; i < kW1; ++i) reinterpret_cast<u32x4 *>(s_w1)[tid + 256 * i] = rw1[i];
+            if (tid < MT * 16) s_bw[0][tid] = rbw;
+            else if (tid < nbw) s_w3p[tid - MT * 16] = rbw;
+            if (tid < a.M) s_bq[tid] = rbq;
+        }
+        if (has0) {
+            pair_row(s_row[p0], j8, b0, ks, ia0, ig0, raw0, prm0, len, a.fold_b1 != 0);
+            if (j8 == 0) s_model[p0] = md0;
+        }
+        // more than 32 pairs: eight further pairs per thread per round trip (the
+        // signals come from host memory; loads unconditional, indices clamped)
+        for (int pb = p0 + 32; pb < a.N; pb += 32 * 8) {
+            uint32_t raw[8];
+            float prm[8];
+            int ia[8], ig[8], md[8];
+    #pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int p = pb + 32 * i < a.N ? pb + 32 * i : 0;
+                raw[i] = reinterpret_cast<const uint32_t *>(a.state + p)[ks >= 2 ? ks - 2 : 0];
+                prm[i] = a.pair_params[p];
+                ia[i] = a.pair_arch[p];
+                ig[i] = a.arch_width + a.dep_gpu[p];
+                md[i] = a.dep_model[p];
+            }
+    #pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int p = pb + 32 * i;
+                if (p < a.N) {
+                    pair_row(s_row[p], j8, b0, ks, ia[i], ig[i], ks >= 2 ? raw[i] : 0u, ks == 0 ? prm[i] : 1.0f, len,
+                             a.fold_b1 != 0);
+                    if (j8 == 0) s_model[p] = md[i];
                 }
-            };
-            auto dot8 = [](const bf16x8 &e, const bf16x8 &q, float acc) {
-#pragma unroll
-                for (int t = 0; t < 8; ++t) acc = fmaf(static_cast<float>(e[t]), static_cast<float>(q[t]), acc);
-                return acc;
-            };
-#pragma unroll
-            for (int j = 0; j < kHeldM; ++j) {
-                const int m0 = wave + 8 * j, m1 = m0 + 4;
-                if (m0 < a.M) {
-                    float acc0 = 0.0f, acc1 = 0.0f;
-#pragma unroll
-                    for (int i = 0; i < kHeldS; ++i) {
-                        const int k = (lane + 64 * i) * 8;
-                        if (k < a.D) {
-                            const bf16x8 e = *reinterpret_cast<const bf16x8 *>(s_emb + k);
-                            acc0 = dot8(e, wq0[j][i], acc0);
-                            acc1 = dot8(e, wq1[j][i], acc1);
-                        }
+            }
+        }
+        __syncthreads();
+
+        const float nout = static_cast<float>(no < 0 ? 0 : no);
+        const QueryRule qrule = query_rule(a.rule, slo, len, nout, a.w);
+        Best best = best_none();
+        const int ntiles = (a.N + 31) / 32;
+        for (int ct = 0; ct < ntiles; ++ct) {
+            const int d = ct * 32 + n;
+            const bool vd = d < a.N;
+            const int dc = vd ? d : 0;
+            // ---- features of pair d (zero columns past the last pair)
+            bf16x8 xf[2];
+            {
+                const u32x4 *row = reinterpret_cast<const u32x4 *>(s_row[dc]);
+                const u32x4 z = {0, 0, 0, 0};
+                xf[0] = __builtin_bit_cast(bf16x8, vd ? row[h] : z);
+                xf[1] = __builtin_bit_cast(bf16x8, vd ? row[2 + h] : z);
+            }
+            const int model = s_model[dc];
+            // ---- layer 1 (every wave, all row tiles; weights from LDS)
+            bf16x8 h1[KB2];
+    #pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+                f32x16 acc;
+    #pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const f32x4 bt = __builtin_bit_cast(f32x4, s_bw[0][(mt * 2 + h) * 4 + i]);
+    #pragma unroll
+                    for (int j = 0; j < 4; ++j) acc[4 * i + j] = bt[j];
+                }
+    #pragma unroll
+                for (int kb = 0; kb < 2; ++kb) acc = mfma32s(s_w1[(mt * 2 + kb) * 64 + lane], xf[kb], acc);
+                h1[2 * mt] = relu_pack8s(acc, 0);
+                h1[2 * mt + 1] = relu_pack8s(acc, 8);
+            }
+            // ---- layer 2 row tiles of this wave, folded into the heads
+            float z0 = 0.0f, z1 = 0.0f, z2 = 0.0f;
+    #pragma unroll
+            for (int i = 0; i < MO; ++i) {
+                if (wave + 4 * i >= MT) break;
+                const int mo = wave + 4 * i;
+                if (i >= MOH) {
+                    const bf16x8 *w2 = reinterpret_cast<const bf16x8 *>(a.w2_pk);
+    #pragma unroll
+                    for (int kb = 0; kb < KB2; ++kb) fw2[i][kb] = w2[(mo * KB2 + kb) * 64 + lane];
+                }
+                f32x16 acc;
+    #pragma unroll
+                for (int p = 0; p < 4; ++p) {
+                    const f32x4 bt = __builtin_bit_cast(f32x4, s_bw[1][(mo * 2 + h) * 4 + p]);
+    #pragma unroll
+                    for (int j = 0; j < 4; ++j) acc[4 * p + j] = bt[j];
+                }
+    #pragma unroll
+                for (int kb = 0; kb < KB2; ++kb) acc = mfma32s(fw2[i][kb], h1[kb], acc);
+                const u32x4 *w3 = &s_w3p[(mo * 2 + h) * 2 * NH];
+                const u32x4 wa = w3[0], wb = w3[1], wc = w3[2], wd = w3[3];
+                const u32x4 we = NH == 3 ? w3[4] : u32x4{0, 0, 0, 0};
+                const u32x4 wf = NH == 3 ? w3[5] : u32x4{0, 0, 0, 0};
+    #pragma unroll
+                for (int p = 0; p < 8; ++p) {
+                    const bf16x2 hp = relu_bf16x2(acc[2 * p], acc[2 * p + 1]);
+                    const uint32_t u0 = p < 4 ? wa[p & 3] : wb[p & 3];
+                    const uint32_t u1 = p < 4 ? wc[p & 3] : wd[p & 3];
+                    const uint32_t u2 = p < 4 ? we[p & 3] : wf[p & 3];
+                    z0 = __builtin_amdgcn_fdot2_f32_bf16(hp, __builtin_bit_cast(bf16x2, u0), z0, false);
+                    z1 = __builtin_amdgcn_fdot2_f32_bf16(hp, __builtin_bit_cast(bf16x2, u1), z1, false);
+                    z2 = __builtin_amdgcn_fdot2_f32_bf16(hp, __builtin_bit_cast(bf16x2, u2), z2, false);
+                }
+            }
+            z0 += __shfl_xor(z0, 32);
+            z1 += __shfl_xor(z1, 32);
+            z2 += __shfl_xor(z2, 32);
+            if (h == 0) {
+                s_z[wave][n][0] = z0;
+                s_z[wave][n][1] = z1;
+                s_z[wave][n][2] = z2;
+            }
+            // ---- quality of every model (Sec. 3.2 item 3), once: wave w takes
+            // models w, w + 4, w + 8, ...; lanes split D
+            if (ct == 0) {
+                // models wave + 8j and wave + 8j + 4; the first kHeldM pairs use the
+                // heads already in registers for the first kHeldS slices of D
+                auto finish = [&](float acc0, float acc1, int m0, int m1) {
+                    acc0 = wave_sum(acc0);
+                    acc1 = wave_sum(acc1);
+                    if (lane == 0) {
+                        s_q[m0] = acc0 + s_bq[m0];
+                        if (m1 < a.M) s_q[m1] = acc1 + s_bq[m1];
                     }
-                    for (int k = (lane + 64 * kHeldS) * 8; k < a.D; k += 512) {
+                };
+                auto dot8 = [](const bf16x8 &e, const bf16x8 &q, float acc) {
+    #pragma unroll
+                    for (int t = 0; t < 8; ++t) acc = fmaf(static_cast<float>(e[t]), static_cast<float>(q[t]), acc);
+                    return acc;
+                };
+    #pragma unroll
+                for (int j = 0; j < kHeldM; ++j) {
+                    const int m0 = wave + 8 * j, m1 = m0 + 4;
+                    if (m0 < a.M) {
+                        float acc0 = 0.0f, acc1 = 0.0f;
+    #pragma unroll
+                        for (int i = 0; i < kHeldS; ++i) {
+                            const int k = (lane + 64 * i) * 8;
+                            if (k < a.D) {
+                                const bf16x8 e = *reinterpret_cast<const bf16x8 *>(s_emb + k);
+                                acc0 = dot8(e, wq0[j][i], acc0);
+                                acc1 = dot8(e, wq1[j][i], acc1);
+                            }
+                        }
+                        for (int k = (lane + 64 * kHeldS) * 8; k < a.D; k += 512) {
+                            const bf16x8 e = *reinterpret_cast<const bf16x8 *>(s_emb + k);
+                            const int mm1 = m1 < a.M ? m1 : m0;
+                            acc0 = dot8(e, *reinterpret_cast<const bf16x8 *>(a.wqT + static_cast<size_t>(m0) * a.D + k), acc0);
+                            acc1 = dot8(e, *reinterpret_cast<const bf16x8 *>(a.wqT + static_cast<size_t>(mm1) * a.D + k), acc1);
+                        }
+                        finish(acc0, acc1, m0, m1);
+                    }
+                }
+                for (int j = kHeldM; wave + 8 * j < a.M; ++j) {
+                    const int m0 = wave + 8 * j, m1 = m0 + 4, mm1 = m1 < a.M ? m1 : m0;
+                    float acc0 = 0.0f, acc1 = 0.0f;
+                    for (int k = lane * 8; k < a.D; k += 512) {
                         const bf16x8 e = *reinterpret_cast<const bf16x8 *>(s_emb + k);
-                        const int mm1 = m1 < a.M ? m1 : m0;
                         acc0 = dot8(e, *reinterpret_cast<const bf16x8 *>(a.wqT + static_cast<size_t>(m0) * a.D + k), acc0);
                         acc1 = dot8(e, *reinterpret_cast<const bf16x8 *>(a.wqT + static_cast<size_t>(mm1) * a.D + k), acc1);
                     }
                     finish(acc0, acc1, m0, m1);
                 }
             }
-            for (int j = kHeldM; wave + 8 * j < a.M; ++j) {
-                const int m0 = wave + 8 * j, m1 = m0 + 4, mm1 = m1 < a.M ? m1 : m0;
-                float acc0 = 0.0f, acc1 = 0.0f;
-                for (int k = lane * 8; k < a.D; k += 512) {
-                    const bf16x8 e = *reinterpret_cast<const bf16x8 *>(s_emb + k);
-                    acc0 = dot8(e, *reinterpret_cast<const bf16x8 *>(a.wqT + static_cast<size_t>(m0) * a.D + k), acc0);
-                    acc1 = dot8(e, *reinterpret_cast<const bf16x8 *>(a.wqT + static_cast<size_t>(mm1) * a.D + k), acc1);
+            __syncthreads();
+            // ---- heads, cost, decision (Eq. 2, Eq. 3)
+            if (wave == 0 && h == 0 && vd) {
+                const float zz0 = s_z[0][n][0] + s_z[1][n][0] + s_z[2][n][0] + s_z[3][n][0];
+                const float zz1 = s_z[0][n][1] + s_z[1][n][1] + s_z[2][n][1] + s_z[3][n][1];
+                const float tt = softplus_fast(zz0 + a.b3_0);
+                const float tp = softplus_fast(zz1 + a.b3_1);
+                float nc = nout;             // N_out: the query's, or the third head's prediction
+                if (NH == 3) {
+                    const float zz2 = s_z[0][n][2] + s_z[1][n][2] + s_z[2][n][2] + s_z[3][n][2];
+                    nc = softplus_fast(zz2 + a.b3_2);
                 }
-                finish(acc0, acc1, m0, m1);
+                offer(best, decide(tt, tp, nc, a.rule, qrule, s_q[model]), d, tt, tp, nc);
+            }
+            if (ct + 1 < ntiles) __syncthreads();
+        }
+        if (wave == 0) {
+            const uint64_t bkey = best_key(best);
+            const uint64_t k = wave_max(bkey);
+            if (bkey == k && k != 0) {
+                SingleOut *o = a.out;
+                o->choice = key_pair(k);
+                o->feasible = key_feasible(k) ? 1u : 0u;
+                o->utility = best.u;
+                o->e2e = best.e2e;
+                o->ttft = best.tt;
+                o->tpot = best.tp;
+                o->nout = best.n;
+                __threadfence_system();
+                __hip_atomic_store(&o->seq, seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
             }
         }
-        __syncthreads();
-        // ---- heads, cost, decision (Eq. 2, Eq. 3)
-        if (wave == 0 && h == 0 && vd) {
-            const float zz0 = s_z[0][n][0] + s_z[1][n][0] + s_z[2][n][0] + s_z[3][n][0];
-            const float zz1 = s_z[0][n][1] + s_z[1][n][1] + s_z[2][n][1] + s_z[3][n][1];
-            const float tt = softplus_fast(zz0 + a.b3_0);
-            const float tp = softplus_fast(zz1 + a.b3_1);
-            float nc = nout;             // N_out: the query's, or the third head's prediction
-            if (NH == 3) {
-                const float zz2 = s_z[0][n][2] + s_z[1][n][2] + s_z[2][n][2] + s_z[3][n][2];
-                nc = softplus_fast(zz2 + a.b3_2);
-            }
-            offer(best, decide(tt, tp, nc, a.rule, qrule, s_q[model]), d, tt, tp, nc);
-        }
-        if (ct + 1 < ntiles) __syncthreads();
-    }
-    if (wave == 0) {
-        const uint64_t bkey = best_key(best);
-        const uint64_t k = wave_max(bkey);
-        if (bkey == k && k != 0) {
-            SingleOut *o = a.out;
-            o->choice = key_pair(k);
-            o->feasible = key_feasible(k) ? 1u : 0u;
-            o->utility = best.u;
-            o->e2e = best.e2e;
-            o->ttft = best.tt;
-            o->tpot = best.tp;
-            o->nout = best.n;
-            __threadfence_system();
-            __hip_atomic_store(&o->seq, seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
-        }
-    }
-    if constexpr (!RES) break;
+        if constexpr (!RES) break;
     }   // requests
 }
 
