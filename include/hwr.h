@@ -219,6 +219,8 @@ const char *hwr_last_error(const hwr_ctx *ctx);
 /* Kernel timing: each kernel launch carries two HIP events that its dispatch
  * records at the kernel's start and end, on the stream it runs on (a graph
  * launch of the single-query path is bracketed by events instead).
+ * fp32 chunks small enough for the predictor and the quality rows to share
+ * the device run both in the predictor's launch: HWR_K_MLP, no HWR_K_QUALITY.
  * Indices of hwr_kernel_times.ms / launches: */
 enum {
     HWR_K_STATE = 0, HWR_K_QUALITY = 1, HWR_K_GATHER = 2, HWR_K_MLP = 3,

@@ -681,9 +681,16 @@ hwr_status route_device(hwr_ctx *c, const DevBatch &b) {
         qu.wq = c->d_wq;
         qu.bq = c->d_bq;
         qu.qmat = qmat;
-        HWR_HIP(c, timed(c, HWR_K_QUALITY, [&] {
-            return c->bf16 ? launch_quality_bf16(qu, c->cus, c->stream) : launch_quality_f32(qu, c->stream);
-        }));
+        // fp32: the predictor reads no quality (the epilogue decides), so a
+        // chunk small enough for both to share the device runs the quality
+        // rows inside the predictor launch, in workgroups of their own.
+        const bool quality_inside =
+            !c->bf16 && mlp_f32_blocks(static_cast<long>(cn) * N) + (cn + 3) / 4 <= c->cus;
+        if (!quality_inside) {
+            HWR_HIP(c, timed(c, HWR_K_QUALITY, [&] {
+                return c->bf16 ? launch_quality_bf16(qu, c->cus, c->stream) : launch_quality_f32(qu, c->stream);
+            }));
+        }
 
         if (c->bf16) {
             MlpArgs ma{};
@@ -750,6 +757,10 @@ hwr_status route_device(hwr_ctx *c, const DevBatch &b) {
             fa.cand_ttft = ctt ? ctt : c->d_ctt;
             fa.cand_tpot = ctp ? ctp : c->d_ctp;
             fa.cand_nout = cno ? cno : c->d_cno;
+            if (quality_inside) {
+                fa.with_quality = 1;
+                fa.quality = qu;
+            }
             HWR_HIP(c, timed(c, HWR_K_MLP, [&] { return launch_mlp_f32(c->H, fa, c->stream); }));
         }
         EpilogueArgs ea{};

@@ -156,6 +156,9 @@ struct MlpF32Args {
     const float *dep_f32;         // [N][32]
     const float *w1, *b1, *w2, *b2, *w3;   // [F][H], [H], [H][H], [H], [H][nheads]
     float *cand_ttft, *cand_tpot, *cand_nout;   // cand_nout: three heads only
+    int with_quality;             // workgroups past mlp_blocks run `quality`
+    int mlp_blocks;               // set by launch_mlp_f32
+    QualityArgs quality;
 };
 
 struct GatherArgs {
@@ -230,6 +233,7 @@ hipError_t launch_state(const StateArgs &a, hipStream_t s);
 hipError_t launch_quality_bf16(const QualityArgs &a, int cus, hipStream_t s);
 hipError_t launch_quality_f32(const QualityArgs &a, hipStream_t s);
 hipError_t launch_mlp_bf16(int H, bool staged, const MlpArgs &a, hipStream_t s);
+int mlp_f32_blocks(long candidates);   // workgroups of launch_mlp_f32's predictor
 hipError_t launch_mlp_f32(int H, const MlpF32Args &a, hipStream_t s);
 hipError_t launch_gather(const GatherArgs &a, hipStream_t s);
 hipError_t launch_epilogue(const EpilogueArgs &a, hipStream_t s);

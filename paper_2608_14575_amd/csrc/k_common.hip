@@ -162,15 +162,23 @@ __device__ __forceinline__ void predict_f32(const MlpF32Args &a, const F32Weight
     nc = NH == 3 ? softplus_f32(z2 + a.b3_2) : 0.0f;
 }
 
-// Waves stride over the candidates of the chunk.
+// Waves stride over the candidates of the chunk.  Workgroups past
+// mlp_blocks, if any, run the chunk's quality rows instead (a wave per query),
+// at the same time.
 template <int H>
 __global__ __launch_bounds__(256) void k_mlp_f32(MlpF32Args a) {
+    if (static_cast<int>(blockIdx.x) >= a.mlp_blocks) {
+        const int q = (blockIdx.x - a.mlp_blocks) * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+        if (q < a.quality.nq)
+            quality_row_f32(a.quality, q, threadIdx.x & 63, a.quality.qmat + static_cast<size_t>(q) * a.quality.M);
+        return;
+    }
     __shared__ F32Weights<H> s;
     stage_f32<H>(a, s);
     __syncthreads();
     const int lane = threadIdx.x & 63;
     const long total = static_cast<long>(a.q.nq) * a.N;
-    const long stride = static_cast<long>(gridDim.x) * 4;
+    const long stride = static_cast<long>(a.mlp_blocks) * 4;
     for (long c = static_cast<long>(blockIdx.x) * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
          c < total; c += stride) {
         const long q = c / a.N;
@@ -185,11 +193,17 @@ __global__ __launch_bounds__(256) void k_mlp_f32(MlpF32Args a) {
     }
 }
 
-hipError_t launch_mlp_f32(int H, const MlpF32Args &a, hipStream_t s) {
-    const long total = static_cast<long>(a.q.nq) * a.N;
-    // one wave per candidate, at most 1024 workgroups (each stages the weights once)
-    const long wgs = (total + 3) / 4;
-    const dim3 grid(static_cast<unsigned>(wgs < 1024 ? (wgs < 1 ? 1 : wgs) : 1024));
+// One wave per candidate, at most 1024 workgroups (each stages the weights once).
+int mlp_f32_blocks(long candidates) {
+    const long wgs = (candidates + 3) / 4;
+    return static_cast<int>(wgs < 1024 ? (wgs < 1 ? 1 : wgs) : 1024);
+}
+
+hipError_t launch_mlp_f32(int H, const MlpF32Args &args, hipStream_t s) {
+    MlpF32Args a = args;
+    a.mlp_blocks = mlp_f32_blocks(static_cast<long>(a.q.nq) * a.N);
+    const int qblocks = a.with_quality ? (a.quality.nq + 3) / 4 : 0;
+    const dim3 grid(static_cast<unsigned>(a.mlp_blocks + qblocks));
     if (H == 64) return launch_kernel(k_mlp_f32<64>, grid, dim3(256), 0, s, a);
     if (H == 128) return launch_kernel(k_mlp_f32<128>, grid, dim3(256), 0, s, a);
     return hipErrorInvalidValue;

@@ -103,14 +103,22 @@ def test_quality_unroll_is_invisible(embed_dim):
 @pytest.mark.parametrize("kw", [dict(), dict(n_heads=3), dict(n_heads=3, **S.PAPER_SLO, score_mode=1)])
 def test_fp32_chunking_is_invisible(kw):
     """fp32 path (quality, predictor, decision epilogue): 1500 queries in one
-    chunk and in three chunks of 500 give the same outputs, candidates and Q
-    matrix included; two and three heads, the paper's rules."""
+    chunk, in three chunks of 500 and in 38 chunks of at most 40 give the same
+    outputs, candidates and Q matrix included; two and three heads, the
+    paper's rules.  Chunks of 40 are small enough for the predictor launch to
+    run the quality rows as well (no quality launch of their own)."""
     sp, pb, st, qs = _case("C1", n_queries=1500, seed=14, **kw)
-    three = G.make_router(pb, max_chunk=1500)
-    one = G.make_router(pb, max_chunk=500)
-    three.update(st)
-    one.update(st)
-    _same(G.route_device(three, qs, "f32"), G.route_device(one, qs, "f32"))
+    routers = [G.make_router(pb, max_chunk=m) for m in (1500, 500, 40)]
+    for r in routers:
+        r.update(st)
+    routers[2].profile(True)
+    outs = [G.route_device(r, qs, "f32") for r in routers]
+    kt = routers[2].profile_read(reset=True)
+    for r in routers:
+        r.close()
+    assert kt["quality"][1] == 0 and kt["mlp"][1] == 38, kt
+    _same(outs[0], outs[1])
+    _same(outs[0], outs[2])
 
 
 def test_fused_equals_staged_and_split_equals_unsplit():
