@@ -30,9 +30,15 @@ FLAGS = [
 ]
 
 
+# Per-source flags.  k_bf16.hip: MFMA results in vector registers (VGPR
+# form), so that the accumulation registers stay free for the four-tile
+# predictor's first-layer activations, which its MFMAs read directly.
+EXTRA = {"k_bf16.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [HIPCC, *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [HIPCC, *FLAGS, *EXTRA.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed on {src}:\n{r.stderr}")

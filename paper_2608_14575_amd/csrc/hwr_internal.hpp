@@ -17,7 +17,7 @@ constexpr int kQualTile = 32;    // quality GEMM: models padded to one 32-wide t
 constexpr int kBlock = 256;      // threads per workgroup of the batch kernels
 constexpr int kQPerWave = 64;    // fused predictor: queries per wave (two 32-column tiles)
 constexpr int kQPerBlock = kQPerWave * 4;   // four query sub-blocks per workgroup
-constexpr int kMlpThreads = 512;             // predictor workgroup: 8 waves, two per SIMD
+constexpr int kMlpThreads = 512;             // predictor workgroup with two column tiles per wave: 8 waves
 constexpr int kGatherQ = 16;     // feature gather: queries per workgroup
 constexpr int kMaxPairs = 1024;
 constexpr int kMaxModels = 32;

@@ -12,6 +12,8 @@
 // next layer's B operand -- so activations stay in registers from layer to
 // layer; the weights (A operands) are re-laid-out on the host so that their k
 // order matches the accumulator row order (see hwr_api.hip, pack_predictor).
+#include <type_traits>
+
 #include "hwr_device.hpp"
 
 namespace hwr {
@@ -182,13 +184,19 @@ hipError_t launch_quality_bf16(const QualityArgs &a, int cus, hipStream_t s) {
     return launch_kernel(k_quality_bf16<1>, dim3(grid), dim3(256), 0, s, a);
 }
 
+
 // ------------------------------------------------------------ predictor
 // Eq. 1 cost predictor on MFMA tiles, for all (query, pair) candidates of a
-// chunk.  Workgroup: 8 waves, two per SIMD.  Waves w and w + 4 take the same
-// 64 queries and split the workgroup's pair range in two halves, so that one
-// wave's VALU epilogue overlaps the other's MFMAs; their decision keys merge
-// through LDS at the end.  Each wave steps through its pairs, evaluating
-// 2 x 32 candidates (one pair, 64 queries) per step:
+// chunk.  A workgroup covers kQPerBlock queries; its waves form query groups
+// of 32 * NT queries, two waves per group, and the two waves of a group split
+// the workgroup's pair range in halves (their decision keys merge through LDS
+// at the end).  NT = 2: 8 waves, two per SIMD, so that one wave's VALU
+// epilogue overlaps the other's MFMAs.  NT = 4: 4 waves, one per SIMD, each
+// holding twice the candidates, so that every weight fragment read from LDS
+// feeds four MFMAs instead of two (half the LDS traffic per candidate); the
+// first layer's activations then sit in the accumulation registers (AGPRs),
+// which the MFMA reads directly.  Each wave steps through its pairs,
+// evaluating NT x 32 candidates (one pair, 32 * NT queries) per step:
 //   X^T  (32 features x 32 candidates, bf16)   built from the pair's feature
 //        row (L1-resident) and each query's input-length feature;
 //   h1^T = ReLU(W1^T X^T + b1)  -> bf16, registers;
@@ -200,14 +208,28 @@ hipError_t launch_quality_bf16(const QualityArgs &a, int cus, hipStream_t s) {
 // previous tile's VALU epilogue (bias, ReLU, bf16 packing), so the matrix
 // pipe and the vector ALU overlap.  W1, W2 and W3 (A operands) and the biases
 // (accumulator initial values) live in LDS.  After the heads, lane half h
-// carries column tile h alone (one query per lane).  Fused mode then applies
-// Eq. 2, the bound test and the utility and keeps the query's best candidate
-// (Eq. 3); staged mode reads X from HBM and writes TTFT/TPOT per candidate.
-template <int H, bool STAGED, int NH, bool FB>
-__global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
+// carries column tiles h, h + 2, ... (one query per lane and tile pair).
+// Fused mode then applies Eq. 2, the bound test and the utility and keeps
+// each query's best candidate (Eq. 3); staged mode reads X from HBM and
+// writes TTFT/TPOT per candidate.
+template <int NT>
+struct MlpShape {
+    static constexpr int kWaves = NT == 4 ? 4 : 8;
+    static constexpr int kThreads = 64 * kWaves;
+    static constexpr int kQPW = 32 * NT;                 // queries per wave
+    static constexpr int kQG = kQPerBlock / kQPW;        // query groups per workgroup
+    static_assert(kWaves == 2 * kQG, "two waves (pair halves) per query group");
+};
+
+template <int H, bool STAGED, int NH, bool FB, int NT, bool LEAN = false>
+__global__ __launch_bounds__(MlpShape<NT>::kThreads, 1) void k_mlp_bf16(MlpArgs a) {
     constexpr int MT = H / 32;     // 32-row tiles of a hidden layer
     constexpr int KB2 = H / 16;    // k-blocks of the second layer
-    constexpr int NT = 2;          // 32-candidate column tiles per wave
+    constexpr int NO = NT / 2;     // queries each lane decides (tiles h, h + 2, ...)
+    constexpr int kThreads = MlpShape<NT>::kThreads;
+    constexpr int kQPW = MlpShape<NT>::kQPW;
+    constexpr int kQG = MlpShape<NT>::kQG;
+    static_assert(NT == 2 || NT == 4, "two or four column tiles per wave");
     __shared__ bf16x8 s_w1[MT * 2 * 64];
     __shared__ bf16x8 s_w2[MT * KB2 * 64];
     __shared__ f32x4 s_b1[MT * 2 * 4];
@@ -219,54 +241,86 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
     __shared__ float s_mnout[NH == 3 ? kQPerBlock : 1];
     const int tid = threadIdx.x;
     {
-        // Every load of the staging is issued before the first LDS store:
-        // one memory round trip for the whole prologue.  Indices past an
-        // array's end are clamped for the loads and skipped for the stores.
+        // Every load of a staging round is issued before its first LDS
+        // store: one memory round trip per round of up to kStageRound pieces
+        // per thread (one round for 512 threads, two for 256).  Indices past
+        // an array's end are clamped for the loads and skipped for the stores.
         constexpr int nW1 = MT * 2 * 64, nW2 = MT * KB2 * 64, nB = MT * 2 * 4, nW3 = KB2 * W3S;
-        constexpr int pW1 = (nW1 + kMlpThreads - 1) / kMlpThreads;
-        constexpr int pW2 = (nW2 + kMlpThreads - 1) / kMlpThreads;
+        constexpr int pW1 = (nW1 + kThreads - 1) / kThreads;
+        constexpr int pW2 = (nW2 + kThreads - 1) / kThreads;
+        constexpr int pB = (nB + kThreads - 1) / kThreads;
+        constexpr int pW3 = (nW3 + kThreads - 1) / kThreads;
+        constexpr int kStageRound = 16;
+        constexpr int rW2 = pW2 < kStageRound ? pW2 : kStageRound;
+        static_assert(pW2 % rW2 == 0, "whole staging rounds");
         const uint4 *g1 = reinterpret_cast<const uint4 *>(a.w1_pk);
         const uint4 *g2 = reinterpret_cast<const uint4 *>(a.w2_pk);
         const uint4 *gb1 = reinterpret_cast<const uint4 *>(a.b1_pk);
         const uint4 *gb2 = reinterpret_cast<const uint4 *>(a.b2_pk);
         const uint4 *g3 = reinterpret_cast<const uint4 *>(a.w3_frag);
-        uint4 v1[pW1], v2[pW2];
+        uint4 v1[pW1], v2[rW2], vb1[pB], vb2[pB], v3[pW3];
 #pragma unroll
         for (int i = 0; i < pW1; ++i) {
-            const int k = tid + i * kMlpThreads;
+            const int k = tid + i * kThreads;
             v1[i] = g1[k < nW1 ? k : 0];
         }
 #pragma unroll
-        for (int i = 0; i < pW2; ++i) {
-            const int k = tid + i * kMlpThreads;
-            v2[i] = g2[k < nW2 ? k : 0];
+        for (int i = 0; i < pB; ++i) {
+            const int k = tid + i * kThreads;
+            vb1[i] = gb1[k < nB ? k : 0];
+            vb2[i] = gb2[k < nB ? k : 0];
         }
-        static_assert(nB <= kMlpThreads && nW3 <= kMlpThreads, "one bias / head piece per thread");
-        const uint4 vb1 = gb1[tid < nB ? tid : 0], vb2 = gb2[tid < nB ? tid : 0];
-        const uint4 v3 = g3[tid < nW3 ? tid : 0];
+#pragma unroll
+        for (int i = 0; i < pW3; ++i) {
+            const int k = tid + i * kThreads;
+            v3[i] = g3[k < nW3 ? k : 0];
+        }
+#pragma unroll
+        for (int r = 0; r < pW2 / rW2; ++r) {
+#pragma unroll
+            for (int i = 0; i < rW2; ++i) {
+                const int k = tid + (r * rW2 + i) * kThreads;
+                v2[i] = g2[k < nW2 ? k : 0];
+            }
+#pragma unroll
+            for (int i = 0; i < rW2; ++i) {
+                const int k = tid + (r * rW2 + i) * kThreads;
+                if (k < nW2) reinterpret_cast<uint4 *>(s_w2)[k] = v2[i];
+            }
+        }
 #pragma unroll
         for (int i = 0; i < pW1; ++i) {
-            const int k = tid + i * kMlpThreads;
+            const int k = tid + i * kThreads;
             if (k < nW1) reinterpret_cast<uint4 *>(s_w1)[k] = v1[i];
         }
 #pragma unroll
-        for (int i = 0; i < pW2; ++i) {
-            const int k = tid + i * kMlpThreads;
-            if (k < nW2) reinterpret_cast<uint4 *>(s_w2)[k] = v2[i];
+        for (int i = 0; i < pB; ++i) {
+            const int k = tid + i * kThreads;
+            if (k < nB) {
+                reinterpret_cast<uint4 *>(s_b1)[k] = vb1[i];
+                reinterpret_cast<uint4 *>(s_b2)[k] = vb2[i];
+            }
         }
-        if (tid < nB) {
-            reinterpret_cast<uint4 *>(s_b1)[tid] = vb1;
-            reinterpret_cast<uint4 *>(s_b2)[tid] = vb2;
+#pragma unroll
+        for (int i = 0; i < pW3; ++i) {
+            const int k = tid + i * kThreads;
+            if (k < nW3) reinterpret_cast<uint4 *>(s_w3f)[k] = v3[i];
         }
-        if (tid < nW3) reinterpret_cast<uint4 *>(s_w3f)[tid] = v3;
     }
     __syncthreads();
 
-    const int lane = tid & 63, wave = tid >> 6, n = lane & 31, h = lane >> 5;
-    const int qw = wave & 3, grp = wave >> 2;
+    // (the wave index is uniform: kept in scalar registers, so are the
+    // pair loop and the per-pair table reads)
+    const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6), n = lane & 31, h = lane >> 5;
+    const int qw = wave % kQG, grp = wave / kQG;
     const int nq = a.q.nq;
-    const int qbase = blockIdx.x * kQPerBlock + qw * kQPerWave;
-    // every lane builds features for both column tiles ...
+    const int qbase = blockIdx.x * kQPerBlock + qw * kQPW;
+    // LEAN: the default decision rule (normalised score, the query's own
+    // bound) and no per-candidate outputs, so that the decision code is
+    // straight-line
+    Rule rule = a.rule;
+    if constexpr (LEAN) rule = Rule{};
+    // every lane builds features for all column tiles ...
     int qc[NT];
     uint32_t xl[NT];
 #pragma unroll
@@ -278,14 +332,23 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
         // recomputed inside the pair loop
         asm volatile("" : "+v"(xl[t]));
     }
-    // ... and decides for column tile h only (query qme)
-    const int qme = qbase + 32 * h + n;
-    const bool vme = qme < nq;
-    const int qmc = vme ? qme : 0;
-    const int32_t nomy = a.q.nout ? a.q.nout[qmc] : 0;   // given N_out (two heads)
-    const float nout = static_cast<float>(nomy < 0 ? 0 : nomy);
-    const QueryRule qrule = query_rule(a.rule, a.q.slo ? a.q.slo[qmc] : a.q.default_slo,
-                                       a.q.input_len[qmc], nout, a.w);
+    // ... and decides for column tiles h, h + 2, ... only (queries qme[j])
+    int qme[NO], qmc[NO];
+    bool vme[NO];
+    float nout[NO];
+    QueryRule qrule[NO];
+    const float *qrow[NO];
+#pragma unroll
+    for (int j = 0; j < NO; ++j) {
+        qme[j] = qbase + 32 * (2 * j + h) + n;
+        vme[j] = qme[j] < nq;
+        qmc[j] = vme[j] ? qme[j] : 0;
+        const int32_t nomy = a.q.nout ? a.q.nout[qmc[j]] : 0;   // given N_out (two heads)
+        nout[j] = static_cast<float>(nomy < 0 ? 0 : nomy);
+        qrule[j] = query_rule(rule, a.q.slo ? a.q.slo[qmc[j]] : a.q.default_slo,
+                              a.q.input_len[qmc[j]], nout[j], a.w);
+        qrow[j] = a.qmat + static_cast<size_t>(qmc[j]) * a.M;
+    }
     // the input-length slot: k-block, lane half and element holding it
     const int ls_kb = a.len_slot >> 4, ls_h = (a.len_slot >> 3) & 1, ls_e = a.len_slot & 7;
     const bool patch = (h == ls_h);
@@ -297,18 +360,21 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
     const int d0 = static_cast<int>(span0 + (span1 - span0) * grp / 2);
     const int d1 = static_cast<int>(span0 + (span1 - span0) * (grp + 1) / 2);
 
-    Best best = best_none();
+    Best best[NO];
+#pragma unroll
+    for (int j = 0; j < NO; ++j) best[j] = best_none();
 
     // Head-layer A fragment of this lane for column tile t (an index into a
     // k-block's fragments): lane 16g + i holds row i, k-group g.  Row
-    // i = 8t + 4s + m is head m of sub-column s; it takes weights only from
-    // the k-groups whose B lanes carry sub-column s (g & 1 == s), namely the
-    // hidden-unit half g >> 1.  Every other lane reads the zero fragment.
-    int w3_sel[NT];
+    // i = 8(t & 1) + 4s + m is head m of sub-column s; it takes weights only
+    // from the k-groups whose B lanes carry sub-column s (g & 1 == s), namely
+    // the hidden-unit half g >> 1.  Every other lane reads the zero fragment.
+    // Tiles t and t ^ 1 share one head accumulator, acc3[t >> 1].
+    int w3_sel[2];
     {
         const int i = lane & 15, g = lane >> 4, m = i & 3, s = (i >> 2) & 1;
 #pragma unroll
-        for (int t = 0; t < NT; ++t)
+        for (int t = 0; t < 2; ++t)
             w3_sel[t] = ((i >> 3) == t && m < NH && (g & 1) == s) ? m * 2 + (g >> 1) : 2 * NH;
     }
 
@@ -316,9 +382,9 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
     // (fused) or the candidates' feature rows (staged), and the quality
     // Q[query][model(pair)], whose address needs a scalar load first.
     const bf16x8 *dep = reinterpret_cast<const bf16x8 *>(a.dep_bf16);
-    const float *qrow = a.qmat + static_cast<size_t>(qmc) * a.M;
     const int dfirst = d0 < d1 ? d0 : 0;
-    bf16x8 nr[NT][2];
+    constexpr int NR = STAGED ? NT : 1;   // feature rows loaded per step
+    bf16x8 nr[NR][2];
     if constexpr (STAGED) {
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
@@ -331,16 +397,49 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
         nr[0][0] = dep[dfirst * 4 + h];
         nr[0][1] = dep[dfirst * 4 + 2 + h];
     }
-    float nq_val = STAGED ? 0.0f : qrow[a.dep_model[dfirst]];
+    float nq_val[NO];
+#pragma unroll
+    for (int j = 0; j < NO; ++j) nq_val[j] = STAGED ? 0.0f : qrow[j][a.dep_model[dfirst]];
+
+    // TTFT, TPOT and N_out (the third head's prediction in tokens, else
+    // the query's given value) from the head-layer sums of own query j
+    auto head_values = [&](int j, float z0, float z1, float z2, float &tt, float &tp, float &nc) {
+        tt = softplus_fast(z0 + a.b3_0);
+        tp = softplus_fast(z1 + a.b3_1);
+        nc = NH == 3 ? softplus_fast(z2 + a.b3_2) : nout[j];
+    };
+    // per-candidate outputs when requested, then cost, bound test,
+    // utility and the running argmax (Eq. 2, Eq. 3) of own query j
+    auto take_candidate = [&](int j, int dd, float tt, float tp, float nc, float Q) {
+        const size_t ci = static_cast<size_t>(qmc[j]) * a.N + dd;
+        if (!LEAN && a.cand_ttft && vme[j]) {
+            a.cand_ttft[ci] = tt;
+            a.cand_tpot[ci] = tp;
+        }
+        if (!LEAN && a.cand_nout && vme[j]) a.cand_nout[ci] = nc;
+        offer<NH == 3>(best[j], decide(tt, tp, nc, rule, qrule[j], Q), dd, tt, tp, nc);
+    };
+    // four-tile form: head sums and quality of the previous pair step,
+    // decided during the next step (pd < 0: none pending)
+    float pz[NO][NH], pQ[NO];
+    int pd = -1;
+#pragma unroll
+    for (int j = 0; j < NO; ++j) {
+        pQ[j] = 0.0f;
+#pragma unroll
+        for (int m = 0; m < NH; ++m) pz[j][m] = 0.0f;
+    }
 
     for (int d = d0; d < d1; ++d) {
-        bf16x8 cr[NT][2];
+        bf16x8 cr[NR][2];
 #pragma unroll
-        for (int t = 0; t < NT; ++t) {
+        for (int t = 0; t < NR; ++t) {
             cr[t][0] = nr[t][0];
             cr[t][1] = nr[t][1];
         }
-        const float Qd = nq_val;
+        float Qd[NO];
+#pragma unroll
+        for (int j = 0; j < NO; ++j) Qd[j] = nq_val[j];
         {
             const int dn = d + 1 < d1 ? d + 1 : d;
             if constexpr (STAGED) {
@@ -354,7 +453,9 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
             } else {
                 nr[0][0] = dep[dn * 4 + h];
                 nr[0][1] = dep[dn * 4 + 2 + h];
-                nq_val = qrow[a.dep_model[dn]];
+                const int mdn = a.dep_model[dn];
+#pragma unroll
+                for (int j = 0; j < NO; ++j) nq_val[j] = qrow[j][mdn];
             }
         }
         // LDS offsets made opaque per step: the weight fragments are
@@ -374,8 +475,15 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
             const bf16x8 r0 = cr[0][0], r1 = cr[0][1];
 #pragma unroll
             for (int t = 0; t < NT; ++t) {
-                xf[t][0] = (patch && ls_kb == 0) ? put_elem(r0, ls_e, xl[t]) : r0;
-                xf[t][1] = (patch && ls_kb == 1) ? put_elem(r1, ls_e, xl[t]) : r1;
+                if constexpr (NT == 4) {
+                    // the launcher takes this form only with the slot in
+                    // k-block 0: the second k-block is the same for every tile
+                    xf[t][0] = patch ? put_elem(r0, ls_e, xl[t]) : r0;
+                    xf[t][1] = r1;
+                } else {
+                    xf[t][0] = (patch && ls_kb == 0) ? put_elem(r0, ls_e, xl[t]) : r0;
+                    xf[t][1] = (patch && ls_kb == 1) ? put_elem(r1, ls_e, xl[t]) : r1;
+                }
             }
         }
         // ---- layers 1 and 2, software-pipelined: the VALU epilogue of row
@@ -401,13 +509,20 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
         };
         // (the empty asm statements pin each epilogue's results at this
         // point: otherwise IR passes sink the pure ReLU / dot-product chains
-        // to their last use, past the fences, and the registers overflow)
+        // to their last use, past the fences, and the registers overflow.
+        // With four column tiles they also place the first layer's
+        // activations in the accumulation registers, read by the MFMAs of
+        // the second layer as their B operand.)
         auto l1_epi = [&](int mt, const f32x16 (&c)[NT]) {
 #pragma unroll
             for (int t = 0; t < NT; ++t) {
                 h1[t][2 * mt] = relu_pack8(c[t], 0);
                 h1[t][2 * mt + 1] = relu_pack8(c[t], 8);
-                asm volatile("" : "+v"(h1[t][2 * mt]), "+v"(h1[t][2 * mt + 1]));
+                if constexpr (NT == 4) {
+                    asm volatile("" : "+a"(h1[t][2 * mt]), "+a"(h1[t][2 * mt + 1]));
+                } else {
+                    asm volatile("" : "+v"(h1[t][2 * mt]), "+v"(h1[t][2 * mt + 1]));
+                }
             }
         };
         auto l2_mfma = [&](int mo, int kb0, int kb1, f32x16 (&c)[NT]) {
@@ -428,12 +543,16 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
         // 32x32x16 one in half the cycles).  A 16x16x32 B operand reads lanes
         // j, j + 16, j + 32, j + 48 as its column j: candidates j and j + 16 of
         // the column tile, each split over two lanes (hidden-unit halves).  The
-        // A fragments (see w3_sel) keep them apart: tile t's row 8t + 4s + m is
-        // head m of candidate 32t + 16s + j, so after both tiles every lane
-        // holds its own candidate's heads in accumulator elements 0..NH-1.
-        // (Packed bf16 dot products would stall the matrix pipe: they do not
-        // co-issue with MFMA on gfx950.)
-        f32x4 acc3 = {};
+        // A fragments (see w3_sel) keep them apart: tile t's row
+        // 8(t & 1) + 4s + m is head m of candidate 32t + 16s + j, so after
+        // tiles t and t ^ 1 every lane holds its own candidate's heads in
+        // accumulator elements 0..NH-1 of acc3[t >> 1].  One fragment read
+        // serves the tiles of every accumulator.  (Packed bf16 dot products
+        // would stall the matrix pipe: they do not co-issue with MFMA on
+        // gfx950.)
+        f32x4 acc3[NO];
+#pragma unroll
+        for (int j = 0; j < NO; ++j) acc3[j] = f32x4{};
         auto l2_epi = [&](int mo, const f32x16 (&c)[NT]) {
             bf16x8 h2[NT][2];
 #pragma unroll
@@ -444,116 +563,344 @@ __global__ __launch_bounds__(kMlpThreads, 1) void k_mlp_bf16(MlpArgs a) {
 #pragma unroll
             for (int b = 0; b < 2; ++b) {
                 const int kb = 2 * mo + b;
-                acc3 = mfma16(s_w3f[kb * W3S + w3o0], h2[0][b], acc3);
-                acc3 = mfma16(s_w3f[kb * W3S + w3o1], h2[1][b], acc3);
+                const bf16x8 f0 = s_w3f[kb * W3S + w3o0], f1 = s_w3f[kb * W3S + w3o1];
+#pragma unroll
+                for (int j = 0; j < NO; ++j) {
+                    acc3[j] = mfma16(f0, h2[2 * j][b], acc3[j]);
+                    acc3[j] = mfma16(f1, h2[2 * j + 1][b], acc3[j]);
+                }
             }
-            asm volatile("" : "+v"(acc3));
+#pragma unroll
+            for (int j = 0; j < NO; ++j) asm volatile("" : "+v"(acc3[j]));
         };
         // MFMA k-steps of tile mo issued before the previous epilogue.  For
         // mo = 0 that epilogue produces layer-1 k-blocks KB2-2 and KB2-1, so
         // the head steps must stop short of them.
         constexpr int kHead = KB2 - 2 < 4 ? KB2 - 2 : 4;
-        // layer 1: MFMAs of tile mt, then the epilogue of tile mt - 1
+        if constexpr (NT == 4) {
+            // One wave per SIMD: the matrix pipe and the vector ALU overlap
+            // only where this wave's own instruction stream interleaves them,
+            // and LDS latency is hidden only by loading fragments ahead, so
+            // both phases below are scheduled by hand (a fence after every
+            // MFMA slot).  Phase A runs the first layer together with the
+            // second layer's row tile 0, whose k-blocks become available two
+            // at a time.  Phase B runs the second layer's other row tiles,
+            // each with the previous tile's epilogue interleaved, its weight
+            // fragments streamed through a ring of kRing fragments loaded
+            // kRing k-steps ahead.  Measured on one wave per SIMD: an MFMA
+            // 32x32x16 issues every ~34 cycles with four independent
+            // accumulators; v_cvt_pk_bf16_f32 costs ~7 issue cycles,
+            // v_pk_max_i16 ~5 and v_accvgpr_write ~6, so phase A is bound by
+            // its epilogue's vector work and phase B by the MFMA issue rate.
+            constexpr int kRing = 3;
+            constexpr int kFull = 0;             // nothing crosses
+            f32x16 a1[NT];                       // first-layer row tile in flight
+            bf16x8 w1c0[2];                      // its W1 fragments
+            auto l1_tile = [&](int mt, int t, const bf16x8 (&w)[2]) {
+                a1[t] = FB ? f32x16{} : bias_tile(s_b1 + (mt * 2 + ho) * 4);
+                a1[t] = mfma32(w[0], xf[t][0], a1[t]);
+                a1[t] = mfma32(w[1], xf[t][1], a1[t]);
+            };
+            // Phase A, scheduled by hand, one iteration per first-layer row
+            // tile mt, 16 MFMA slots each with one sixth of the epilogue of
+            // row tile mt (per tile t: four slots, two ReLU + bf16 pairs
+            // each, and the move of every finished fragment into the
+            // accumulation registers).  The MFMAs of a slot: tile 3 of row
+            // tile mt (held back from the previous iteration), tiles 0-2 of
+            // row tile mt + 1 (each after its tile's epilogue has read the
+            // accumulator), and the second layer's row tile 0 over the
+            // k-blocks of row tile mt - 1.  Weight fragments are loaded one
+            // iteration ahead; a fence after every slot keeps the order.
+            bf16x8 w1n[2], w2n[2];
+            {
+                const bf16x8 w[2] = {s_w1[0 * 64 + lo], s_w1[1 * 64 + lo]};
+                w1n[0] = s_w1[2 * 64 + lo];
+                w1n[1] = s_w1[3 * 64 + lo];
+                w2n[0] = s_w2[0 * 64 + lo];
+                w2n[1] = s_w2[1 * 64 + lo];
+                const f32x16 bi = bias_tile(s_b2 + (0 * 2 + ho) * 4);
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-            l1_mfma(mt, acc[mt & 1]);
-            if (mt > 0) {
-                __builtin_amdgcn_sched_barrier(kFence);
-                l1_epi(mt - 1, acc[(mt - 1) & 1]);
-                __builtin_amdgcn_sched_barrier(kFence);
-            }
-        }
-        // layer 2: first k-steps of tile mo, epilogue of the previous tile
-        // (layer-1 tile MT-1 for mo = 0), then the remaining k-steps
+                for (int t = 0; t < NT; ++t) acc[0][t] = bi;
+                w1c0[0] = w[0];
+                w1c0[1] = w[1];
 #pragma unroll
-        for (int mo = 0; mo < MT; ++mo) {
-            const int cur = (MT + mo) & 1, prev = (MT + mo - 1) & 1;
-            l2_mfma(mo, 0, kHead, acc[cur]);
-            __builtin_amdgcn_sched_barrier(kFence);
-            if (mo == 0) l1_epi(MT - 1, acc[prev]);
-            else l2_epi(mo - 1, acc[prev]);
-            __builtin_amdgcn_sched_barrier(kFence);
-            l2_mfma(mo, kHead, KB2, acc[cur]);
-        }
-        l2_epi(MT - 1, acc[(2 * MT - 1) & 1]);
-        // ---- heads: lane half h completes column tile h (its partner lane
-        // holds the other 128 hidden units of the same candidates)
-        const float tt = softplus_fast(acc3[0] + a.b3_0);
-        const float tp = softplus_fast(acc3[1] + a.b3_1);
-        // N_out: the third head's prediction (tokens), else the query's given value
-        const float nc = NH == 3 ? softplus_fast(acc3[2] + a.b3_2) : nout;
-        const size_t ci = static_cast<size_t>(qmc) * a.N + d;
-        if constexpr (STAGED) {
-            if (vme) {
-                a.cand_ttft[ci] = tt;
-                a.cand_tpot[ci] = tp;
-                if (NH == 3) a.cand_nout[ci] = nc;
+                for (int t = 0; t < NT - 1; ++t) l1_tile(0, t, w);
             }
+            __builtin_amdgcn_sched_barrier(kFull);
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+                const bf16x8 w1c[2] = {w1n[0], w1n[1]};      // row tile mt + 1
+                const bf16x8 w2c[2] = {w2n[0], w2n[1]};      // row tile 0, k-blocks 2mt - 2, 2mt - 1
+                const bf16x8 w1m[2] = {w1c0[0], w1c0[1]};    // row tile mt (its tile 3)
+                if (mt + 2 < MT) {
+                    w1n[0] = s_w1[((mt + 2) * 2 + 0) * 64 + lo];
+                    w1n[1] = s_w1[((mt + 2) * 2 + 1) * 64 + lo];
+                }
+                if (mt >= 1) {                   // row tile 0, k-blocks 2mt, 2mt + 1 next
+                    w2n[0] = s_w2[(2 * mt + 0) * 64 + lo];
+                    w2n[1] = s_w2[(2 * mt + 1) * 64 + lo];
+                }
+                w1c0[0] = w1c[0];
+                w1c0[1] = w1c[1];
+                u32x4 hv[2];
+#pragma unroll
+                for (int sl = 0; sl < 16; ++sl) {
+                    const int t = sl / 4, part = sl % 4;
+                    // MFMA of this slot
+                    if (sl == 0 || sl == 1) {
+                        const int kb = sl;
+                        if (kb == 0) a1[NT - 1] = FB ? f32x16{} : bias_tile(s_b1 + (mt * 2 + ho) * 4);
+                        a1[NT - 1] = mfma32(w1m[kb], xf[NT - 1][kb], a1[NT - 1]);
+                    } else if (part >= 2) {
+                        if (mt > 0) {
+                            const int b = sl >= 8 ? 1 : 0;
+                            const int tt = (sl % 8 < 4 ? 0 : 2) + (part - 2);
+                            acc[0][tt] = mfma32(w2c[b], h1[tt][2 * mt - 2 + b], acc[0][tt]);
+                        }
+                    } else if (mt + 1 < MT) {        // part 0 or 1, slots 4.. : row tile mt + 1, tile t - 1
+                        const int tt = t - 1, kb = part;
+                        if (kb == 0) a1[tt] = FB ? f32x16{} : bias_tile(s_b1 + ((mt + 1) * 2 + ho) * 4);
+                        a1[tt] = mfma32(w1c[kb], xf[tt][kb], a1[tt]);
+                    }
+                    __builtin_amdgcn_sched_barrier(kFull);
+                    // epilogue of row tile mt, tile t: fragment part / 2,
+                    // pairs 2 (part % 2) .. + 1
+                    {
+                        const int fr = part / 2, p0 = 2 * (part % 2);
+#pragma unroll
+                        for (int q = 0; q < 2; ++q) {
+                            const int e = 4 * fr + p0 + q;
+                            hv[fr][p0 + q] = __builtin_bit_cast(uint32_t, relu_bf16x2(a1[t][2 * e], a1[t][2 * e + 1]));
+                        }
+                        if (part % 2 == 1) {
+                            h1[t][2 * mt + fr] = __builtin_bit_cast(bf16x8, hv[fr]);
+                            asm volatile("" : "+a"(h1[t][2 * mt + fr]));
+                        }
+                    }
+                    __builtin_amdgcn_sched_barrier(kFull);
+                }
+            }
+            // the last two k-blocks of row tile 0; the phase-B ring and the
+            // bias of row tile 1 are loaded first
+            bf16x8 ring[kRing];
+            auto w2idx = [&](int i) { return s_w2[(KB2 + i) * 64 + lo]; };   // row tiles 1.. in order
+#pragma unroll
+            for (int i = 0; i < kRing; ++i) ring[i] = w2idx(i);
+            f32x16 bnext = bias_tile(s_b2 + (1 * 2 + ho) * 4);
+#pragma unroll
+            for (int b = 0; b < 2; ++b)
+#pragma unroll
+                for (int t = 0; t < NT; ++t) acc[0][t] = mfma32(w2n[b], h1[t][KB2 - 2 + b], acc[0][t]);
+            __builtin_amdgcn_sched_barrier(kFull);
+            // Phase B, scheduled by hand: every MFMA of row tile mo is
+            // followed by one slot of work on row tile mo - 1 (slot
+            // s = 4 kb + t): slots 0-31 take the ReLU and bf16 rounding of
+            // one element pair each (tile s / 8, pair s % 8), slots 8-11 load
+            // the head fragments, slots 32-39 run the head MFMAs (the
+            // accumulation order of each head accumulator is that of the
+            // other form).  The next row tile's bias is loaded at k-step 1.
+            // A scheduling fence after every slot keeps this order.
+            constexpr int kSteps = (MT - 1) * KB2;
+            float dtt[NO], dtp[NO], dnc[NO];
+            auto epi_pair = [&](const f32x16 &v, int e) {
+                return __builtin_bit_cast(uint32_t, relu_bf16x2(v[2 * e], v[2 * e + 1]));
+            };
+            // row tile mo of phase B; DEC: with the previous pair step's
+            // decisions in its slots 40 .. 40 + 8 NO (one own query per eight
+            // slots, in pieces: TTFT, TPOT, N_out, decision)
+            auto row_tile = [&](auto mo_c, auto dec_c) {
+                constexpr int mo = decltype(mo_c)::value;
+                constexpr bool DEC = decltype(dec_c)::value;
+                f32x16 (&c)[NT] = acc[mo & 1];
+                const f32x16 (&pv)[NT] = acc[(mo - 1) & 1];
+                const f32x16 bi = bnext;
+                u32x4 h2u[NT][2];
+                bf16x8 f3[2][2];                 // head fragments [k-block half b][tile parity]
+#pragma unroll
+                for (int kb = 0; kb < KB2; ++kb) {
+                    const int i = (mo - 1) * KB2 + kb;
+                    const bf16x8 w = ring[i % kRing];
+                    if (i + kRing < kSteps) ring[i % kRing] = w2idx(i + kRing);
+                    if (kb == 1 && mo + 1 < MT) bnext = bias_tile(s_b2 + ((mo + 1) * 2 + ho) * 4);
+#pragma unroll
+                    for (int t = 0; t < NT; ++t) {
+                        c[t] = mfma32(w, h1[t][kb], kb == 0 ? bi : c[t]);
+                        __builtin_amdgcn_sched_barrier(kFull);
+                        const int sl = 4 * kb + t;
+                        if (sl < 32) {
+                            const int tt = sl / 8, e = sl % 8;
+                            h2u[tt][e / 4][e % 4] = epi_pair(pv[tt], e);
+                        }
+                        if (sl >= 8 && sl < 12) {
+                            const int b = (sl - 8) / 2, par = (sl - 8) % 2;
+                            const int kh = 2 * (mo - 1) + b;
+                            f3[b][par] = s_w3f[kh * W3S + (par ? w3o1 : w3o0)];
+                        }
+                        if (sl >= 32 && sl < 40) {
+                            // acc3[j]: (b 0, tile 2j), (b 0, tile 2j + 1), (b 1, 2j), (b 1, 2j + 1)
+                            const int j = (sl - 32) / 4, r = (sl - 32) % 4, b = r / 2, par = r % 2;
+                            acc3[j] = mfma16(f3[b][par], __builtin_bit_cast(bf16x8, h2u[2 * j + par][b]), acc3[j]);
+                        }
+                        if constexpr (DEC) {
+                            if (sl >= 40 && sl < 40 + 8 * NO && (sl - 40) % 8 < 4) {
+                                const int j = (sl - 40) / 8, piece = (sl - 40) % 8;
+                                if (pd >= 0) {
+                                    if (piece == 0) dtt[j] = softplus_fast(pz[j][0] + a.b3_0);
+                                    if (piece == 1) dtp[j] = softplus_fast(pz[j][1] + a.b3_1);
+                                    if (piece == 2) dnc[j] = NH == 3 ? softplus_fast(pz[j][NH - 1] + a.b3_2) : nout[j];
+                                    if (piece == 3) take_candidate(j, pd, dtt[j], dtp[j], dnc[j], pQ[j]);
+                                }
+                            }
+                        }
+                        __builtin_amdgcn_sched_barrier(kFull);
+                    }
+                }
+            };
+            using T = std::true_type;
+            using F = std::false_type;
+            row_tile(std::integral_constant<int, 1>{}, T{});
+            row_tile(std::integral_constant<int, 2>{}, F{});
+            row_tile(std::integral_constant<int, 3>{}, F{});
+            row_tile(std::integral_constant<int, 4>{}, F{});
+            row_tile(std::integral_constant<int, 5>{}, F{});
+            row_tile(std::integral_constant<int, 6>{}, F{});
+            row_tile(std::integral_constant<int, 7>{}, F{});
+            static_assert(MT == 8, "the four-tile form is built for H = 256");
+            l2_epi(MT - 1, acc[(MT - 1) & 1]);
         } else {
-            if (a.cand_ttft && vme) {
-                a.cand_ttft[ci] = tt;
-                a.cand_tpot[ci] = tp;
+            // layer 1: MFMAs of tile mt, then the epilogue of tile mt - 1
+    #pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+                l1_mfma(mt, acc[mt & 1]);
+                if (mt > 0) {
+                    __builtin_amdgcn_sched_barrier(kFence);
+                    l1_epi(mt - 1, acc[(mt - 1) & 1]);
+                    __builtin_amdgcn_sched_barrier(kFence);
+                }
             }
-            if (a.cand_nout && vme) a.cand_nout[ci] = nc;
-            // ---- cost, bound test, utility, running argmax (Eq. 2, Eq. 3)
-            offer<NH == 3>(best, decide(tt, tp, nc, a.rule, qrule, Qd), d, tt, tp, nc);
+            // layer 2: first k-steps of tile mo, epilogue of the previous tile
+            // (layer-1 tile MT-1 for mo = 0), then the remaining k-steps
+    #pragma unroll
+            for (int mo = 0; mo < MT; ++mo) {
+                const int cur = (MT + mo) & 1, prev = (MT + mo - 1) & 1;
+                l2_mfma(mo, 0, kHead, acc[cur]);
+                __builtin_amdgcn_sched_barrier(kFence);
+                if (mo == 0) l1_epi(MT - 1, acc[prev]);
+                else l2_epi(mo - 1, acc[prev]);
+                __builtin_amdgcn_sched_barrier(kFence);
+                l2_mfma(mo, kHead, KB2, acc[cur]);
+            }
+            l2_epi(MT - 1, acc[(2 * MT - 1) & 1]);
+        }
+        // ---- heads: lane half h completes column tiles h, h + 2, ... (its
+        // partner lane holds the other half of the same candidates' hidden
+        // units).  The four-tile fused form defers this to the next pair
+        // step, where it runs in the second layer's MFMA shadow.
+        if constexpr (NT == 4 && !STAGED) {
+#pragma unroll
+            for (int j = 0; j < NO; ++j) {
+#pragma unroll
+                for (int m = 0; m < NH; ++m) pz[j][m] = acc3[j][m];
+                pQ[j] = Qd[j];
+            }
+            pd = d;
+        } else {
+#pragma unroll
+            for (int j = 0; j < NO; ++j) {
+                float tt, tp, nc;
+                head_values(j, acc3[j][0], acc3[j][1], NH == 3 ? acc3[j][2] : 0.0f, tt, tp, nc);
+                if constexpr (STAGED) {
+                    const size_t ci = static_cast<size_t>(qmc[j]) * a.N + d;
+                    if (vme[j]) {
+                        a.cand_ttft[ci] = tt;
+                        a.cand_tpot[ci] = tp;
+                        if (NH == 3) a.cand_nout[ci] = nc;
+                    }
+                } else {
+                    take_candidate(j, d, tt, tp, nc, Qd[j]);
+                }
+            }
+        }
+    }
+    if constexpr (NT == 4 && !STAGED) {
+        if (pd >= 0) {
+#pragma unroll
+            for (int j = 0; j < NO; ++j) {
+                float tt, tp, nc;
+                head_values(j, pz[j][0], pz[j][1], NH == 3 ? pz[j][2] : 0.0f, tt, tp, nc);
+                take_candidate(j, pd, tt, tp, nc, pQ[j]);
+            }
         }
     }
     if constexpr (!STAGED) {
-        uint64_t bkey = best_key(best);
-        float bu = best.u, be = best.e2e, btt = best.tt, btp = best.tp;
-        float bn = NH == 3 ? best.n : nout;
-        // merge the two pair halves of each query through LDS
-        const int slot = qw * kQPerWave + lane;
-        if (grp == 1) {
-            s_mkey[slot] = bkey;
-            s_mval[slot] = (f32x4){bu, be, btt, btp};
-            if constexpr (NH == 3) s_mnout[slot] = bn;
-        }
-        __syncthreads();
-        if (grp == 0 && vme) {
-            const uint64_t ok = s_mkey[slot];
-            if (ok > bkey) {
-                const f32x4 v = s_mval[slot];
-                bkey = ok;
-                bu = v[0];
-                be = v[1];
-                btt = v[2];
-                btp = v[3];
-                if constexpr (NH == 3) bn = s_mnout[slot];
+#pragma unroll
+        for (int j = 0; j < NO; ++j) {
+            uint64_t bkey = best_key(best[j]);
+            float bu = best[j].u, be = best[j].e2e, btt = best[j].tt, btp = best[j].tp;
+            float bn = NH == 3 ? best[j].n : nout[j];
+            // merge the two pair halves of each query through LDS
+            const int slot = qw * kQPW + 32 * (2 * j + h) + n;
+            if (grp == 1) {
+                s_mkey[slot] = bkey;
+                s_mval[slot] = (f32x4){bu, be, btt, btp};
+                if constexpr (NH == 3) s_mnout[slot] = bn;
             }
-            if (nsplit == 1) {
-                write_outputs(a.out, qme, bkey, bu, be, btt, btp, bn);
-            } else {
-                const size_t pi = static_cast<size_t>(split) * nq + qme;
-                a.part_key[pi] = bkey;
-                float *pv = a.part_val + pi * kPartVals;
-                pv[0] = bu;
-                pv[1] = be;
-                pv[2] = btt;
-                pv[3] = btp;
-                pv[4] = bn;
+            __syncthreads();
+            if (grp == 0 && vme[j]) {
+                const uint64_t ok = s_mkey[slot];
+                if (ok > bkey) {
+                    const f32x4 v = s_mval[slot];
+                    bkey = ok;
+                    bu = v[0];
+                    be = v[1];
+                    btt = v[2];
+                    btp = v[3];
+                    if constexpr (NH == 3) bn = s_mnout[slot];
+                }
+                if (nsplit == 1) {
+                    write_outputs(a.out, qme[j], bkey, bu, be, btt, btp, bn);
+                } else {
+                    const size_t pi = static_cast<size_t>(split) * nq + qme[j];
+                    a.part_key[pi] = bkey;
+                    float *pv = a.part_val + pi * kPartVals;
+                    pv[0] = bu;
+                    pv[1] = be;
+                    pv[2] = btt;
+                    pv[3] = btp;
+                    pv[4] = bn;
+                }
             }
         }
     }
 }
 
+// Column tiles per wave: four for the fused predictor at H = 256 (the
+// large-batch throughput shape) when the input-length slot lies in the
+// first k-block; two otherwise.
+template <int H, bool STAGED, int NH, bool FB>
+static hipError_t launch_mlp_t(const MlpArgs &a, dim3 grid, hipStream_t s) {
+    if constexpr (H == 256 && !STAGED) {
+        if (a.len_slot < 16) {          // the four-tile form patches k-block 0 only
+            const bool lean = !a.cand_ttft && !a.cand_nout && !a.rule.score_paper && !a.rule.bound_paper;
+            if (lean)
+                return launch_kernel(k_mlp_bf16<H, STAGED, NH, FB, 4, true>, grid, dim3(MlpShape<4>::kThreads), 0, s, a);
+            return launch_kernel(k_mlp_bf16<H, STAGED, NH, FB, 4, false>, grid, dim3(MlpShape<4>::kThreads), 0, s, a);
+        }
+    }
+    return launch_kernel(k_mlp_bf16<H, STAGED, NH, FB, 2>, grid, dim3(MlpShape<2>::kThreads), 0, s, a);
+}
+
 template <int H>
 static hipError_t launch_mlp_h(bool staged, const MlpArgs &a, hipStream_t s) {
     const dim3 grid((a.q.nq + kQPerBlock - 1) / kQPerBlock, staged ? 1 : a.nsplit);
-    const dim3 block(kMlpThreads);
     if (a.fold_b1) {
         if (a.nheads == 3)
-            return staged ? launch_kernel(k_mlp_bf16<H, true, 3, true>, grid, block, 0, s, a)
-                          : launch_kernel(k_mlp_bf16<H, false, 3, true>, grid, block, 0, s, a);
-        return staged ? launch_kernel(k_mlp_bf16<H, true, 2, true>, grid, block, 0, s, a)
-                      : launch_kernel(k_mlp_bf16<H, false, 2, true>, grid, block, 0, s, a);
+            return staged ? launch_mlp_t<H, true, 3, true>(a, grid, s) : launch_mlp_t<H, false, 3, true>(a, grid, s);
+        return staged ? launch_mlp_t<H, true, 2, true>(a, grid, s) : launch_mlp_t<H, false, 2, true>(a, grid, s);
     }
     if (a.nheads == 3)
-        return staged ? launch_kernel(k_mlp_bf16<H, true, 3, false>, grid, block, 0, s, a)
-                      : launch_kernel(k_mlp_bf16<H, false, 3, false>, grid, block, 0, s, a);
-    return staged ? launch_kernel(k_mlp_bf16<H, true, 2, false>, grid, block, 0, s, a)
-                  : launch_kernel(k_mlp_bf16<H, false, 2, false>, grid, block, 0, s, a);
+        return staged ? launch_mlp_t<H, true, 3, false>(a, grid, s) : launch_mlp_t<H, false, 3, false>(a, grid, s);
+    return staged ? launch_mlp_t<H, true, 2, false>(a, grid, s) : launch_mlp_t<H, false, 2, false>(a, grid, s);
 }
 
 hipError_t launch_mlp_bf16(int H, bool staged, const MlpArgs &a, hipStream_t s) {
