@@ -180,9 +180,16 @@ typedef struct {                  /* caller-owned, in the batch's memory space  
     float   *cand_quality;        /* [n][M] every (query, model) quality (debug) */
 } hwr_route_result;               /* every pointer but choice may be NULL        */
 
-/* Create a context: validate the configuration, copy and re-lay-out the
- * weights on the device, allocate work space for max_chunk queries.  Routing
- * needs one hwr_update_hw_state first.  *out is NULL on error. */
+/* Create a context for one deployed pair set (Sec. 3.1: the model-GPU pairs
+ * (M_i, g_i) the router chooses among, with each model's attributes) and one
+ * trained router: the cost predictor f_cost of Sec. 3.2 Eq. 1 (w1..w3, b1..b3)
+ * and the per-model quality heads of Sec. 3.2 item 3 (wq, bq).  Validates the
+ * configuration, copies and re-lays-out the weights on the device and
+ * allocates work space for max_chunk queries; the caller may free every
+ * buffer cfg points to when this returns.  Routing needs one
+ * hwr_update_hw_state first.  Errors: HWR_ERR_INVALID_ARG for an out-of-range
+ * field or NULL table, HWR_ERR_UNSUPPORTED for a shape the kernels do not
+ * handle, HWR_ERR_OOM / HWR_ERR_HIP from the device; *out is NULL on error. */
 hwr_status hwr_init(const hwr_config *cfg, hwr_ctx **out);
 
 /* Replace the cached runtime signals of all N pairs (the hardware monitor's

@@ -210,6 +210,76 @@ def _ptr(a) -> int:
     return int(a.data_ptr())   # torch tensor
 
 
+# element kinds of the buffers of a batch: accepted numpy dtypes / torch dtype names
+_KINDS = {
+    "i32": ({np.dtype(np.int32)}, {"torch.int32"}),
+    "f32": ({np.dtype(np.float32)}, {"torch.float32"}),
+    "u8": ({np.dtype(np.uint8)}, {"torch.uint8"}),
+    "b16": ({np.dtype(np.uint16), np.dtype(np.int16)}, {"torch.int16", "torch.uint16", "torch.bfloat16"}),
+}
+
+
+def check_buffer(name: str, a, kind: str, count: int, mem: int, device: int = 0) -> None:
+    """Raise HwrError(HWR_ERR_INVALID_ARG) unless ``a`` can hold ``count``
+    elements of ``kind`` contiguously in the memory space ``mem``: a numpy
+    array (or CPU tensor) for HWR_MEM_HOST, a tensor on GPU ``device`` for
+    HWR_MEM_DEVICE.  The library reads and writes raw pointers, so a short,
+    strided or misplaced buffer would otherwise reach the kernels."""
+    def bad(msg):
+        raise HwrError(HWR_ERR_INVALID_ARG, f"{name}: {msg}")
+    np_kinds, torch_kinds = _KINDS[kind]
+    if isinstance(a, np.ndarray):
+        if mem == HWR_MEM_DEVICE:
+            bad("a device batch needs device tensors, got a numpy array")
+        if a.dtype not in np_kinds:
+            bad(f"dtype {a.dtype} (expected {kind})")
+        if not a.flags.c_contiguous:
+            bad("not contiguous")
+        size = a.size
+    elif hasattr(a, "data_ptr") and hasattr(a, "is_contiguous"):
+        dev = a.device
+        if mem == HWR_MEM_DEVICE and (dev.type != "cuda" or (dev.index if dev.index is not None else 0) != device):
+            bad(f"on {dev}, expected cuda:{device}")
+        if mem == HWR_MEM_HOST and dev.type != "cpu":
+            bad(f"on {dev}, a host batch needs host memory")
+        if str(a.dtype) not in torch_kinds:
+            bad(f"dtype {a.dtype} (expected {kind})")
+        if not a.is_contiguous():
+            bad("not contiguous")
+        size = a.numel()
+    else:
+        bad(f"unsupported buffer type {type(a).__name__}")
+    if size < count:
+        bad(f"{size} elements, needs {count}")
+
+
+def check_batch(*, n: int, D: int, M: int, N: int, K: int, dtype: str, n_heads: int, mem: int, device: int,
+                emb, input_len, expected_out_len, slo_s, choice, feasible=None, utility=None, e2e_s=None,
+                ttft_s=None, tpot_s=None, nout=None, cand_ttft=None, cand_tpot=None, cand_nout=None,
+                cand_quality=None) -> None:
+    """Every buffer of a route call checked against the context's shapes
+    (D embedding width, M models, N pairs, K cost weights) before the call."""
+    if mem not in (HWR_MEM_DEVICE, HWR_MEM_HOST):
+        raise HwrError(HWR_ERR_INVALID_ARG, f"unknown mem {mem}")
+    if n == 0:
+        return
+    check_buffer("emb", emb, "b16" if dtype == "bf16" else "f32", n * D, mem, device)
+    check_buffer("input_len", input_len, "i32", n, mem, device)
+    if expected_out_len is not None or n_heads == 2:
+        check_buffer("expected_out_len", expected_out_len, "i32", n, mem, device)
+    if slo_s is not None:
+        check_buffer("slo_s", slo_s, "f32", n, mem, device)
+    check_buffer("choice", choice, "i32", n * K, mem, device)
+    for name, a, kind, count in (("feasible", feasible, "u8", n * K), ("utility", utility, "f32", n * K),
+                                 ("e2e_s", e2e_s, "f32", n * K), ("ttft_s", ttft_s, "f32", n * K),
+                                 ("tpot_s", tpot_s, "f32", n * K), ("nout", nout, "f32", n * K),
+                                 ("cand_ttft", cand_ttft, "f32", n * N), ("cand_tpot", cand_tpot, "f32", n * N),
+                                 ("cand_nout", cand_nout, "f32", n * N),
+                                 ("cand_quality", cand_quality, "f32", n * M)):
+        if a is not None:
+            check_buffer(name, a, kind, count, mem, device)
+
+
 class Router:
     """Owns one hwr context.  Arrays follow include/hwr.h: weights row-major
     ([D][M], [F][H], [H][H], [H][n_heads]) as uint16 bf16 bits (bf16) or
@@ -259,6 +329,7 @@ class Router:
             setattr(cfg, k, keep[k].ctypes.data)
         cfg.stream = int(stream)
         self.M, self.N, self.D, self.dtype, self.n_heads = M, N, D, dtype, int(n_heads)
+        self.device = int(device)
         self.n_weights = 1 if cost_weights is None else int(np.size(cost_weights))
         self.ctx = hwr_init(cfg)
 
@@ -302,8 +373,15 @@ class Router:
               choice, feasible=None, utility=None, e2e_s=None, ttft_s=None, tpot_s=None, nout=None,
               cand_ttft=None, cand_tpot=None, cand_nout=None, cand_quality=None) -> None:
         """Route into caller-owned outputs (numpy for HWR_MEM_HOST, torch
-        tensors on the device for HWR_MEM_DEVICE)."""
+        tensors on the device for HWR_MEM_DEVICE).  Every buffer is checked
+        (kind, contiguity, memory space, size) before the library is called;
+        a mismatch raises HwrError(HWR_ERR_INVALID_ARG)."""
         n = int(input_len.shape[0])
+        check_batch(n=n, D=self.D, M=self.M, N=self.N, K=self.n_weights, dtype=self.dtype,
+                    n_heads=self.n_heads, mem=mem, device=self.device, emb=emb, input_len=input_len,
+                    expected_out_len=expected_out_len, slo_s=slo_s, choice=choice, feasible=feasible,
+                    utility=utility, e2e_s=e2e_s, ttft_s=ttft_s, tpot_s=tpot_s, nout=nout,
+                    cand_ttft=cand_ttft, cand_tpot=cand_tpot, cand_nout=cand_nout, cand_quality=cand_quality)
         b = hwr_query_batch(n, mem, _ptr(emb), _ptr(input_len), _ptr(expected_out_len), _ptr(slo_s))
         r = hwr_route_result(_ptr(choice), _ptr(feasible), _ptr(utility), _ptr(e2e_s), _ptr(ttft_s),
                              _ptr(tpot_s), _ptr(nout), _ptr(cand_ttft), _ptr(cand_tpot), _ptr(cand_nout),
