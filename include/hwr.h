@@ -216,6 +216,26 @@ hwr_status hwr_update_hw_state(hwr_ctx *ctx, const hwr_hw_state *state, int32_t 
  * memory accesses stay in bounds). */
 hwr_status hwr_route_batch(hwr_ctx *ctx, const hwr_query_batch *q, hwr_route_result *r);
 
+/* hwr_route_batch for callers that cannot allocate device memory during a
+ * call: code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc.  Same arguments, results and ordering as hwr_route_batch
+ * for HWR_MEM_DEVICE batches, bit for bit; it calls no hipMalloc, hipFree or
+ * other allocating routine (and creates no events: kernel timing is skipped).
+ * Its work space -- the quality matrix, the split partials and, for staged,
+ * fp32 and several-weight contexts, the per-candidate predictions and
+ * features -- lives in a static 64 MiB device array of the library, one per
+ * GPU, held until the process ends (its address is taken by the first
+ * hwr_init on each device).  A batch is routed in chunks of as many queries
+ * as that space holds (at most max_chunk); HWR_ERR_UNSUPPORTED when a single
+ * query needs more than 64 MiB (about 3,600 pairs at most, staged).  Host
+ * batches: HWR_ERR_INVALID_ARG (they stage through buffers allocated on first
+ * use).  Every call on one GPU uses that GPU's one array, from any context:
+ * calls that overlap in time on one GPU (different streams, threads or
+ * contexts) race on it and give undefined results; calls ordered on one
+ * stream do not.  Each call writes every element it later reads; nothing
+ * carries over from the previous call. */
+hwr_status hwr_route_batch_static(hwr_ctx *ctx, const hwr_query_batch *q, hwr_route_result *r);
+
 /* Destroy a context (NULL is allowed); waits for its stream first. */
 void hwr_free(hwr_ctx *ctx);
 

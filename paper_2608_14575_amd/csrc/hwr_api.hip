@@ -9,6 +9,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -39,6 +40,31 @@ struct Pending {
     int kind;
     hipEvent_t a, b;
 };
+
+// Work space of one batch route: where the chunk loop keeps the quality
+// matrix, the split partials and (staged, fp32 and several-weight routes)
+// the per-candidate predictions and features; and how many queries a chunk
+// may hold.
+struct Workspace {
+    float *qmat = nullptr;
+    uint64_t *pkey = nullptr;
+    float *pval = nullptr;
+    size_t part_cap = 0;
+    float *ctt = nullptr, *ctp = nullptr, *cno = nullptr;
+    uint16_t *X = nullptr;
+    int max_chunk = 0;
+    bool timing = true;             // kernel timing allowed (it may create events)
+};
+
+// Scratch of the entry point that allocates nothing (hwr_route_batch_static):
+// one array per device, held until the process ends.  In host code its name
+// stands for no device address; its address on each device is taken once,
+// with hipGetSymbolAddress, by the first hwr_init on that device.
+constexpr size_t kScratchBytes = size_t(64) << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
 
 }  // namespace
 
@@ -84,6 +110,7 @@ struct hwr_ctx {
     uint64_t *d_pkey = nullptr;
     float *d_pval = nullptr;
     size_t part_cap = 0;
+    void *scratch = nullptr;          // this device's static scratch (hwr_route_batch_static)
     // host-memory batches: device staging.  Inputs are double-buffered (the
     // next chunk's upload overlaps this chunk's kernels); outputs are ordered
     // on the context's stream and need one set.
@@ -114,6 +141,7 @@ struct hwr_ctx {
     hipGraphExec_t gexec = nullptr;
     // timing
     bool prof = false;
+    bool no_timing = false;           // set while a route must not create events
     int prof_every = 1;               // time one launch in prof_every of each kind
     int64_t prof_seen[HWR_K_COUNT] = {};
     std::vector<Pending> pending;
@@ -304,7 +332,7 @@ hipEvent_t take_event(hwr_ctx *c) {
 // (launch_kernel), so they mark the kernel's own start and end on the stream.
 // Whether this launch of `kind` is one of the sampled ones.
 bool sampled(hwr_ctx *c, int kind) {
-    return c->prof && c->prof_seen[kind]++ % c->prof_every == 0;
+    return c->prof && !c->no_timing && c->prof_seen[kind]++ % c->prof_every == 0;
 }
 
 template <class F>
@@ -510,6 +538,17 @@ hwr_status init_impl(const hwr_config *cfg, hwr_ctx **out) {
     } while (0)
 
     INIT_HIP(hipSetDevice(c->dev));
+    if (c->dev >= kMaxDevices) return bail(hipErrorInvalidDevice, "device ordinal above the scratch table");
+    {
+        std::lock_guard<std::mutex> lock(g_scratch_mu);
+        if (!g_scratch_ptr[c->dev]) {
+            void *ptr = nullptr;
+            INIT_HIP(hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)));
+            if (!ptr) return bail(hipErrorInvalidSymbol, "hipGetSymbolAddress(scratch) gave no address");
+            g_scratch_ptr[c->dev] = ptr;
+        }
+        c->scratch = g_scratch_ptr[c->dev];
+    }
     const int M = c->M, N = c->N, D = c->D, F = c->F, H = c->H;
     INIT_HIP(upload(&c->d_dep_model, cfg->dep_model, N));
     INIT_HIP(upload(&c->d_dep_gpu, cfg->dep_gpu, N));
@@ -639,7 +678,22 @@ MlpF32Args f32_args(const hwr_ctx *c, const QueryArgs &qa) {
     return fa;
 }
 
-hwr_status route_device(hwr_ctx *c, const DevBatch &b) {
+// The context's own work space, allocated by hwr_init for max_chunk queries.
+Workspace ctx_workspace(const hwr_ctx *c) {
+    Workspace w;
+    w.qmat = c->d_qmat;
+    w.pkey = c->d_pkey;
+    w.pval = c->d_pval;
+    w.part_cap = c->part_cap;
+    w.ctt = c->d_ctt;
+    w.ctp = c->d_ctp;
+    w.cno = c->d_cno;
+    w.X = c->d_X;
+    w.max_chunk = c->max_chunk;
+    return w;
+}
+
+hwr_status route_device(hwr_ctx *c, const DevBatch &b, const Workspace &w) {
     hwr_status st = sync_state(c);
     if (st != HWR_OK) return st;
     if (c->res_launched && !c->res_stopping) {
@@ -650,8 +704,8 @@ hwr_status route_device(hwr_ctx *c, const DevBatch &b) {
     }
     const int M = c->M, N = c->N, D = c->D;
     const size_t esz = c->bf16 ? 2 : 4;
-    for (int off = 0; off < b.n; off += c->max_chunk) {
-        const int cn = std::min(c->max_chunk, b.n - off);
+    for (int off = 0; off < b.n; off += w.max_chunk) {
+        const int cn = std::min(w.max_chunk, b.n - off);
         QueryArgs qa;
         qa.nq = cn;
         qa.input_len = b.len + off;
@@ -667,7 +721,7 @@ hwr_status route_device(hwr_ctx *c, const DevBatch &b) {
         if (oa.ttft) oa.ttft += oo;
         if (oa.tpot) oa.tpot += oo;
         if (oa.nout) oa.nout += oo;
-        float *qmat = b.cand_quality ? b.cand_quality + static_cast<size_t>(off) * M : c->d_qmat;
+        float *qmat = b.cand_quality ? b.cand_quality + static_cast<size_t>(off) * M : w.qmat;
         float *ctt = b.cand_ttft ? b.cand_ttft + static_cast<size_t>(off) * N : nullptr;
         float *ctp = b.cand_tpot ? b.cand_tpot + static_cast<size_t>(off) * N : nullptr;
         float *cno = (c->NH == 3 && b.cand_nout) ? b.cand_nout + static_cast<size_t>(off) * N : nullptr;
@@ -722,13 +776,13 @@ hwr_status route_device(hwr_ctx *c, const DevBatch &b) {
                 const int blocks = (cn + kQPerBlock - 1) / kQPerBlock;
                 int nsplit = 1;
                 if (blocks < c->cus) nsplit = std::min(N, (c->cus + blocks - 1) / blocks);
-                while (nsplit > 1 && static_cast<size_t>(nsplit) * cn > c->part_cap) --nsplit;
+                while (nsplit > 1 && static_cast<size_t>(nsplit) * cn > w.part_cap) --nsplit;
                 ma.nsplit = nsplit;
-                ma.part_key = c->d_pkey;
-                ma.part_val = c->d_pval;
+                ma.part_key = w.pkey;
+                ma.part_val = w.pval;
                 HWR_HIP(c, timed(c, HWR_K_FUSED, [&] { return launch_mlp_bf16(c->H, false, ma, c->stream); }));
                 if (nsplit > 1) {
-                    MergeArgs mg{cn, nsplit, c->d_pkey, c->d_pval, oa};
+                    MergeArgs mg{cn, nsplit, w.pkey, w.pval, oa};
                     HWR_HIP(c, timed(c, HWR_K_MERGE, [&] { return launch_merge(mg, c->stream); }));
                 }
                 continue;
@@ -737,26 +791,26 @@ hwr_status route_device(hwr_ctx *c, const DevBatch &b) {
                 // several cost weights: the fused kernel writes every
                 // candidate's predictions and no decision; the epilogue
                 // below takes one decision per weight
-                ma.cand_ttft = ctt ? ctt : c->d_ctt;
-                ma.cand_tpot = ctp ? ctp : c->d_ctp;
-                ma.cand_nout = c->NH == 3 ? (cno ? cno : c->d_cno) : nullptr;
+                ma.cand_ttft = ctt ? ctt : w.ctt;
+                ma.cand_tpot = ctp ? ctp : w.ctp;
+                ma.cand_nout = c->NH == 3 ? (cno ? cno : w.cno) : nullptr;
                 ma.out = OutArgs{};
                 ma.nsplit = 1;
                 HWR_HIP(c, timed(c, HWR_K_FUSED, [&] { return launch_mlp_bf16(c->H, false, ma, c->stream); }));
             } else {
-                GatherArgs ga{N, c->len_slot, qa, c->d_dep_bf16, c->d_X};
+                GatherArgs ga{N, c->len_slot, qa, c->d_dep_bf16, w.X};
                 HWR_HIP(c, timed(c, HWR_K_GATHER, [&] { return launch_gather(ga, c->stream); }));
-                ma.X = c->d_X;
-                ma.cand_ttft = ctt ? ctt : c->d_ctt;
-                ma.cand_tpot = ctp ? ctp : c->d_ctp;
-                ma.cand_nout = cno ? cno : c->d_cno;
+                ma.X = w.X;
+                ma.cand_ttft = ctt ? ctt : w.ctt;
+                ma.cand_tpot = ctp ? ctp : w.ctp;
+                ma.cand_nout = cno ? cno : w.cno;
                 HWR_HIP(c, timed(c, HWR_K_MLP, [&] { return launch_mlp_bf16(c->H, true, ma, c->stream); }));
             }
         } else {
             MlpF32Args fa = f32_args(c, qa);
-            fa.cand_ttft = ctt ? ctt : c->d_ctt;
-            fa.cand_tpot = ctp ? ctp : c->d_ctp;
-            fa.cand_nout = cno ? cno : c->d_cno;
+            fa.cand_ttft = ctt ? ctt : w.ctt;
+            fa.cand_tpot = ctp ? ctp : w.ctp;
+            fa.cand_nout = cno ? cno : w.cno;
             if (quality_inside) {
                 fa.with_quality = 1;
                 fa.quality = qu;
@@ -772,9 +826,9 @@ hwr_status route_device(hwr_ctx *c, const DevBatch &b) {
         ea.q = qa;
         ea.dep_model = c->d_dep_model;
         ea.qmat = qmat;
-        ea.cand_ttft = ctt ? ctt : c->d_ctt;
-        ea.cand_tpot = ctp ? ctp : c->d_ctp;
-        ea.cand_nout = c->NH == 3 ? (cno ? cno : c->d_cno) : nullptr;
+        ea.cand_ttft = ctt ? ctt : w.ctt;
+        ea.cand_tpot = ctp ? ctp : w.ctp;
+        ea.cand_nout = c->NH == 3 ? (cno ? cno : w.cno) : nullptr;
         ea.vec4 = N % 4 == 0 && reinterpret_cast<uintptr_t>(ea.cand_ttft) % 16 == 0 &&
                   reinterpret_cast<uintptr_t>(ea.cand_tpot) % 16 == 0 &&
                   reinterpret_cast<uintptr_t>(ea.cand_nout) % 16 == 0;
@@ -893,7 +947,7 @@ hwr_status route_host_chunks(hwr_ctx *c, const hwr_query_batch *q, hwr_route_res
         b.cand_tpot = r->cand_tpot ? c->d_hcand + rows * N : nullptr;
         b.cand_nout = r->cand_nout ? c->d_hcand + 2 * rows * N : nullptr;
         b.cand_quality = r->cand_quality ? c->d_hqual : nullptr;
-        hwr_status rs = route_device(c, b);
+        hwr_status rs = route_device(c, b, ctx_workspace(c));
         if (rs != HWR_OK) return rs;
         HWR_HIP(c, hipEventRecord(h.read, s));
         h.used = true;
@@ -1086,6 +1140,63 @@ hwr_status route_single(hwr_ctx *c, const hwr_query_batch *q, hwr_route_result *
     return HWR_OK;
 }
 
+// Arguments common to both route entry points.  HWR_OK with n == 0 means
+// there is nothing to do.
+hwr_status check_route_args(hwr_ctx *c, const hwr_query_batch *q, const hwr_route_result *r) {
+    if (!c) return fail(nullptr, HWR_ERR_INVALID_ARG, "ctx is NULL");
+    if (!q || !r) return fail(c, HWR_ERR_INVALID_ARG, "batch or result is NULL");
+    if (q->n < 0) return fail(c, HWR_ERR_INVALID_ARG, "n < 0");
+    if (q->mem != HWR_MEM_DEVICE && q->mem != HWR_MEM_HOST) return fail(c, HWR_ERR_INVALID_ARG, "unknown mem");
+    if (q->n == 0) return HWR_OK;
+    if (!q->emb || !q->input_len || !r->choice || (c->NH == 2 && !q->expected_out_len))
+        return fail(c, HWR_ERR_INVALID_ARG, "emb, input_len, choice and (two heads) expected_out_len are required");
+    if (!c->has_state) return fail(c, HWR_ERR_STATE, "no hardware state yet: call hwr_update_hw_state first");
+    return HWR_OK;
+}
+
+// Work space carved out of this device's static scratch: the split partials
+// (fused, one weight) first, then per chunk row the quality row, the
+// per-candidate predictions (staged, fp32 and several-weight routes) and the
+// staged features, each block 256-byte aligned.  Chunks hold as many queries
+// as fit, at most max_chunk; 0 rows: one query does not fit.
+Workspace scratch_workspace(const hwr_ctx *c) {
+    Workspace w;
+    w.timing = false;
+    const size_t M = c->M, N = c->N;
+    const bool fused1 = c->bf16 && c->pipeline == HWR_PIPE_FUSED && c->nw == 1;
+    const bool per_cand = !c->bf16 || c->pipeline == HWR_PIPE_STAGED || c->nw > 1;
+    const bool staged = c->bf16 && c->pipeline == HWR_PIPE_STAGED;
+    auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
+    const size_t part_cap = fused1 ? static_cast<size_t>(2 * c->cus) * kQPerBlock : 0;
+    const size_t fixed = up(part_cap * sizeof(uint64_t)) + up(part_cap * kPartVals * sizeof(float));
+    const size_t row = M * 4 + (per_cand ? N * 4 * (c->NH == 3 ? 3 : 2) : 0) + (staged ? N * kFeatPad * 2 : 0);
+    const size_t slack = 5 * 256;                       // alignment of the per-row blocks
+    if (fixed + slack >= kScratchBytes) return w;
+    const size_t rows = std::min<size_t>((kScratchBytes - fixed - slack) / row, static_cast<size_t>(c->max_chunk));
+    if (rows < 1) return w;
+    unsigned char *base = static_cast<unsigned char *>(c->scratch);
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        unsigned char *p = base + off;
+        off += up(bytes);
+        return p;
+    };
+    if (fused1) {
+        w.pkey = reinterpret_cast<uint64_t *>(take(part_cap * sizeof(uint64_t)));
+        w.pval = reinterpret_cast<float *>(take(part_cap * kPartVals * sizeof(float)));
+        w.part_cap = part_cap;
+    }
+    w.qmat = reinterpret_cast<float *>(take(rows * M * 4));
+    if (per_cand) {
+        w.ctt = reinterpret_cast<float *>(take(rows * N * 4));
+        w.ctp = reinterpret_cast<float *>(take(rows * N * 4));
+        if (c->NH == 3) w.cno = reinterpret_cast<float *>(take(rows * N * 4));
+    }
+    if (staged) w.X = reinterpret_cast<uint16_t *>(take(rows * N * kFeatPad * 2));
+    w.max_chunk = static_cast<int>(rows);
+    return off <= kScratchBytes ? w : Workspace{};
+}
+
 }  // namespace
 
 // ==================================================================== C ABI
@@ -1132,14 +1243,8 @@ hwr_status hwr_update_hw_state(hwr_ctx *c, const hwr_hw_state *state, int32_t n)
 }
 
 hwr_status hwr_route_batch(hwr_ctx *c, const hwr_query_batch *q, hwr_route_result *r) {
-    if (!c) return fail(nullptr, HWR_ERR_INVALID_ARG, "ctx is NULL");
-    if (!q || !r) return fail(c, HWR_ERR_INVALID_ARG, "batch or result is NULL");
-    if (q->n < 0) return fail(c, HWR_ERR_INVALID_ARG, "n < 0");
-    if (q->mem != HWR_MEM_DEVICE && q->mem != HWR_MEM_HOST) return fail(c, HWR_ERR_INVALID_ARG, "unknown mem");
-    if (q->n == 0) return HWR_OK;
-    if (!q->emb || !q->input_len || !r->choice || (c->NH == 2 && !q->expected_out_len))
-        return fail(c, HWR_ERR_INVALID_ARG, "emb, input_len, choice and (two heads) expected_out_len are required");
-    if (!c->has_state) return fail(c, HWR_ERR_STATE, "no hardware state yet: call hwr_update_hw_state first");
+    hwr_status st = check_route_args(c, q, r);
+    if (st != HWR_OK || q->n == 0) return st;
     HWR_HIP(c, hipSetDevice(c->dev));
     if (q->mem == HWR_MEM_DEVICE) {
         DevBatch b{};
@@ -1153,7 +1258,7 @@ hwr_status hwr_route_batch(hwr_ctx *c, const hwr_query_batch *q, hwr_route_resul
         b.cand_tpot = r->cand_tpot;
         b.cand_nout = r->cand_nout;
         b.cand_quality = r->cand_quality;
-        return route_device(c, b);
+        return route_device(c, b, ctx_workspace(c));
     }
     for (int i = 0; i < q->n; ++i) {
         if (q->input_len[i] < 1) return fail(c, HWR_ERR_INVALID_ARG, "input_len < 1");
@@ -1165,6 +1270,34 @@ hwr_status hwr_route_batch(hwr_ctx *c, const hwr_query_batch *q, hwr_route_resul
         !r->cand_quality)
         return route_single(c, q, r);
     return route_host(c, q, r);
+}
+
+hwr_status hwr_route_batch_static(hwr_ctx *c, const hwr_query_batch *q, hwr_route_result *r) {
+    hwr_status st = check_route_args(c, q, r);
+    if (st != HWR_OK || q->n == 0) return st;
+    if (q->mem != HWR_MEM_DEVICE)
+        return fail(c, HWR_ERR_INVALID_ARG, "hwr_route_batch_static routes device-memory batches only "
+                                            "(host batches stage through buffers allocated on first use)");
+    const Workspace w = scratch_workspace(c);
+    if (w.max_chunk < 1)
+        return fail(c, HWR_ERR_UNSUPPORTED, "one query of this context needs more work space than the " +
+                                                std::to_string(kScratchBytes >> 20) + " MiB static scratch holds");
+    HWR_HIP(c, hipSetDevice(c->dev));
+    DevBatch b{};
+    b.n = q->n;
+    b.emb = q->emb;
+    b.len = q->input_len;
+    b.nout = q->expected_out_len;
+    b.slo = q->slo_s;
+    b.out = OutArgs{r->choice, r->feasible, r->utility, r->e2e_s, r->ttft_s, r->tpot_s, r->nout};
+    b.cand_ttft = r->cand_ttft;
+    b.cand_tpot = r->cand_tpot;
+    b.cand_nout = r->cand_nout;
+    b.cand_quality = r->cand_quality;
+    c->no_timing = true;              // event timing could create events
+    st = route_device(c, b, w);
+    c->no_timing = false;
+    return st;
 }
 
 void hwr_free(hwr_ctx *c) { release(c); }

@@ -29,7 +29,8 @@ HWR_K_STATE, HWR_K_QUALITY, HWR_K_GATHER, HWR_K_MLP, HWR_K_EPILOGUE, HWR_K_FUSED
 HWR_K_COUNT = 8
 KERNEL_NAMES = ["state", "quality", "gather", "mlp", "epilogue", "fused", "merge", "single"]
 
-EXPORTS = ["hwr_init", "hwr_update_hw_state", "hwr_route_batch", "hwr_free", "hwr_last_error",
+EXPORTS = ["hwr_init", "hwr_update_hw_state", "hwr_route_batch", "hwr_route_batch_static", "hwr_free",
+           "hwr_last_error",
            "hwr_profile_enable", "hwr_profile_read", "hwr_sim_run", "hwr_sim_last_error"]
 
 _STATUS = {0: "HWR_OK", -1: "HWR_ERR_INVALID_ARG", -2: "HWR_ERR_OOM", -3: "HWR_ERR_HIP",
@@ -140,6 +141,8 @@ def load(path: Optional[str] = None) -> C.CDLL:
     L.hwr_update_hw_state.argtypes = [_vp, _vp, C.c_int32]
     L.hwr_route_batch.restype = C.c_int
     L.hwr_route_batch.argtypes = [_vp, C.POINTER(hwr_query_batch), C.POINTER(hwr_route_result)]
+    L.hwr_route_batch_static.restype = C.c_int
+    L.hwr_route_batch_static.argtypes = [_vp, C.POINTER(hwr_query_batch), C.POINTER(hwr_route_result)]
     L.hwr_free.restype = None
     L.hwr_free.argtypes = [_vp]
     L.hwr_last_error.restype = C.c_char_p
@@ -179,6 +182,10 @@ def hwr_update_hw_state(ctx, state: np.ndarray) -> None:
 
 def hwr_route_batch(ctx, batch: hwr_query_batch, result: hwr_route_result) -> None:
     _check(load().hwr_route_batch(ctx, C.byref(batch), C.byref(result)), ctx)
+
+
+def hwr_route_batch_static(ctx, batch: hwr_query_batch, result: hwr_route_result) -> None:
+    _check(load().hwr_route_batch_static(ctx, C.byref(batch), C.byref(result)), ctx)
 
 
 def hwr_free(ctx) -> None:
@@ -371,11 +378,13 @@ class Router:
 
     def route(self, emb, input_len, expected_out_len, slo_s=None, *, mem: int,
               choice, feasible=None, utility=None, e2e_s=None, ttft_s=None, tpot_s=None, nout=None,
-              cand_ttft=None, cand_tpot=None, cand_nout=None, cand_quality=None) -> None:
+              cand_ttft=None, cand_tpot=None, cand_nout=None, cand_quality=None, static: bool = False) -> None:
         """Route into caller-owned outputs (numpy for HWR_MEM_HOST, torch
         tensors on the device for HWR_MEM_DEVICE).  Every buffer is checked
         (kind, contiguity, memory space, size) before the library is called;
-        a mismatch raises HwrError(HWR_ERR_INVALID_ARG)."""
+        a mismatch raises HwrError(HWR_ERR_INVALID_ARG).  ``static``: through
+        hwr_route_batch_static (no allocation during the call; device
+        batches only)."""
         n = int(input_len.shape[0])
         check_batch(n=n, D=self.D, M=self.M, N=self.N, K=self.n_weights, dtype=self.dtype,
                     n_heads=self.n_heads, mem=mem, device=self.device, emb=emb, input_len=input_len,
@@ -386,7 +395,7 @@ class Router:
         r = hwr_route_result(_ptr(choice), _ptr(feasible), _ptr(utility), _ptr(e2e_s), _ptr(ttft_s),
                              _ptr(tpot_s), _ptr(nout), _ptr(cand_ttft), _ptr(cand_tpot), _ptr(cand_nout),
                              _ptr(cand_quality))
-        hwr_route_batch(self.ctx, b, r)
+        (hwr_route_batch_static if static else hwr_route_batch)(self.ctx, b, r)
 
     def route_host(self, emb, input_len, expected_out_len, slo_s=None, candidates: bool = False) -> dict:
         """Route numpy inputs; returns numpy outputs (synchronous)."""

@@ -163,6 +163,7 @@ def test_null_arguments(lib):
     assert lib.hwr_init(None, C.byref(ctx)) == hwr.HWR_ERR_INVALID_ARG
     assert lib.hwr_update_hw_state(None, None, 0) == hwr.HWR_ERR_INVALID_ARG
     assert lib.hwr_route_batch(None, None, None) == hwr.HWR_ERR_INVALID_ARG
+    assert lib.hwr_route_batch_static(None, None, None) == hwr.HWR_ERR_INVALID_ARG
     assert lib.hwr_profile_enable(None, 1) == hwr.HWR_ERR_INVALID_ARG
     lib.hwr_free(None)
 
