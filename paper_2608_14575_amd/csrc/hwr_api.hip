@@ -770,9 +770,12 @@ hwr_status route_device(hwr_ctx *c, const DevBatch &b, const Workspace &w) {
             ma.out = oa;
             ma.nsplit = 1;
             if (c->pipeline == HWR_PIPE_FUSED && c->nw == 1) {
+                // per-candidate outputs, if the caller asked for them, go
+                // straight to its [query][pair] buffers
                 ma.cand_ttft = ctt;
                 ma.cand_tpot = ctp;
                 ma.cand_nout = cno;
+                ma.cand_pm = 0;
                 const int blocks = (cn + kQPerBlock - 1) / kQPerBlock;
                 int nsplit = 1;
                 if (blocks < c->cus) nsplit = std::min(N, (c->cus + blocks - 1) / blocks);
@@ -789,11 +792,13 @@ hwr_status route_device(hwr_ctx *c, const DevBatch &b, const Workspace &w) {
             }
             if (c->pipeline == HWR_PIPE_FUSED) {
                 // several cost weights: the fused kernel writes every
-                // candidate's predictions and no decision; the epilogue
-                // below takes one decision per weight
-                ma.cand_ttft = ctt ? ctt : w.ctt;
-                ma.cand_tpot = ctp ? ctp : w.ctp;
-                ma.cand_nout = c->NH == 3 ? (cno ? cno : w.cno) : nullptr;
+                // candidate's predictions (pair-major, into the work space)
+                // and no decision; the epilogue below takes one decision per
+                // weight
+                ma.cand_ttft = w.ctt;
+                ma.cand_tpot = w.ctp;
+                ma.cand_nout = c->NH == 3 ? w.cno : nullptr;
+                ma.cand_pm = 1;
                 ma.out = OutArgs{};
                 ma.nsplit = 1;
                 HWR_HIP(c, timed(c, HWR_K_FUSED, [&] { return launch_mlp_bf16(c->H, false, ma, c->stream); }));
@@ -801,16 +806,17 @@ hwr_status route_device(hwr_ctx *c, const DevBatch &b, const Workspace &w) {
                 GatherArgs ga{N, c->len_slot, qa, c->d_dep_bf16, w.X};
                 HWR_HIP(c, timed(c, HWR_K_GATHER, [&] { return launch_gather(ga, c->stream); }));
                 ma.X = w.X;
-                ma.cand_ttft = ctt ? ctt : w.ctt;
-                ma.cand_tpot = ctp ? ctp : w.ctp;
-                ma.cand_nout = cno ? cno : w.cno;
+                ma.cand_ttft = w.ctt;
+                ma.cand_tpot = w.ctp;
+                ma.cand_nout = w.cno;
+                ma.cand_pm = 1;
                 HWR_HIP(c, timed(c, HWR_K_MLP, [&] { return launch_mlp_bf16(c->H, true, ma, c->stream); }));
             }
         } else {
             MlpF32Args fa = f32_args(c, qa);
-            fa.cand_ttft = ctt ? ctt : w.ctt;
-            fa.cand_tpot = ctp ? ctp : w.ctp;
-            fa.cand_nout = cno ? cno : w.cno;
+            fa.cand_ttft = w.ctt;
+            fa.cand_tpot = w.ctp;
+            fa.cand_nout = w.cno;
             if (quality_inside) {
                 fa.with_quality = 1;
                 fa.quality = qu;
@@ -826,19 +832,14 @@ hwr_status route_device(hwr_ctx *c, const DevBatch &b, const Workspace &w) {
         ea.q = qa;
         ea.dep_model = c->d_dep_model;
         ea.qmat = qmat;
-        ea.cand_ttft = ctt ? ctt : w.ctt;
-        ea.cand_tpot = ctp ? ctp : w.ctp;
-        ea.cand_nout = c->NH == 3 ? (cno ? cno : w.cno) : nullptr;
-        ea.vec4 = N % 4 == 0 && reinterpret_cast<uintptr_t>(ea.cand_ttft) % 16 == 0 &&
-                  reinterpret_cast<uintptr_t>(ea.cand_tpot) % 16 == 0 &&
-                  reinterpret_cast<uintptr_t>(ea.cand_nout) % 16 == 0;
-        // lanes per query: a power of two from 8 (which bounds the LDS rows of
-        // the quality matrix a workgroup stages) up to 64, with up to four
-        // slices of the row per lane
-        const int units = ea.vec4 ? N / 4 : N;
-        int g = 8;
-        while (g * 4 < units && g < 64) g <<= 1;
-        ea.group = g;
+        // the predictions are pair-major in the work space; the caller's
+        // per-candidate buffers ([query][pair]) are written by the epilogue
+        ea.cand_ttft = w.ctt;
+        ea.cand_tpot = w.ctp;
+        ea.cand_nout = c->NH == 3 ? w.cno : nullptr;
+        ea.dbg_ttft = ctt;
+        ea.dbg_tpot = ctp;
+        ea.dbg_nout = c->NH == 3 ? cno : nullptr;
         ea.out = oa;
         HWR_HIP(c, timed(c, HWR_K_EPILOGUE, [&] { return launch_epilogue(ea, c->stream); }));
     }

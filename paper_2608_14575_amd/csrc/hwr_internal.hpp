@@ -18,7 +18,7 @@ constexpr int kBlock = 256;      // threads per workgroup of the batch kernels
 constexpr int kQPerWave = 64;    // fused predictor: queries per wave (two 32-column tiles)
 constexpr int kQPerBlock = kQPerWave * 4;   // four query sub-blocks per workgroup
 constexpr int kMlpThreads = 512;             // predictor workgroup with two column tiles per wave: 8 waves
-constexpr int kGatherQ = 16;     // feature gather: queries per workgroup
+constexpr int kGatherQ = 64;     // feature gather: queries per workgroup
 constexpr int kMaxPairs = 1024;
 constexpr int kMaxModels = 32;
 constexpr int kMaxHeads = 3;     // predictor outputs: TTFT, TPOT and (optionally) N_out
@@ -139,9 +139,10 @@ struct MlpArgs {                  // bf16 predictor (fused or staged)
     const uint16_t *w1_pk, *w2_pk;
     const float *b1_pk, *b2_pk;
     const uint16_t *w3_frag;      // head layer A fragments (compact, see pack_predictor)
-    const uint16_t *X;            // staged input [nq][N][32]
-    float *cand_ttft, *cand_tpot; // [nq][N] (staged output or debug)
-    float *cand_nout;             // [nq][N] predicted N_out (three heads: staged output or debug)
+    const uint16_t *X;            // staged input [N][nq][32] (pair-major)
+    float *cand_ttft, *cand_tpot; // per-candidate TTFT / TPOT: staged, several weights or debug
+    float *cand_nout;             // predicted N_out (three heads), same layout
+    int cand_pm;                  // 1: pair-major [N][nq] (staged always); 0: [nq][N]
     OutArgs out;
     int nsplit;                   // pair ranges (grid.y); >1 writes partials
     uint64_t *part_key;           // [nsplit][nq]
@@ -155,7 +156,7 @@ struct MlpF32Args {
     QueryArgs q;
     const float *dep_f32;         // [N][32]
     const float *w1, *b1, *w2, *b2, *w3;   // [F][H], [H], [H][H], [H], [H][nheads]
-    float *cand_ttft, *cand_tpot, *cand_nout;   // cand_nout: three heads only
+    float *cand_ttft, *cand_tpot, *cand_nout;   // [N][nq], pair-major; cand_nout: three heads only
     int with_quality;             // workgroups past mlp_blocks run `quality`
     int mlp_blocks;               // set by launch_mlp_f32
     QualityArgs quality;
@@ -165,20 +166,21 @@ struct GatherArgs {
     int N, len_slot;
     QueryArgs q;
     const uint16_t *dep_bf16;     // [N][32]
-    uint16_t *X;                  // [nq][N][32]
+    uint16_t *X;                  // [N][nq][32], pair-major
 };
 
+// Decision epilogue over pair-major predictions: candidate (q, d) at d * nq + q.
 struct EpilogueArgs {
-    int N, M, group;              // group: lanes per query (power of two <= 64)
-    int vec4;                     // 1: N % 4 == 0 and TTFT / TPOT rows 16-byte aligned
+    int N, M;
     Rule rule;
     int nw;                       // cost weights (>= 1); outputs are [nq][nw] when nw > 1
     float w[kMaxWeights];
     QueryArgs q;
     const int32_t *dep_model;
-    const float *qmat;
-    const float *cand_ttft, *cand_tpot;
-    const float *cand_nout;       // [nq][N] predicted N_out, or null: the query's given N_out
+    const float *qmat;            // [nq][M]
+    const float *cand_ttft, *cand_tpot;   // [N][nq]
+    const float *cand_nout;       // [N][nq] predicted N_out, or null: the query's given N_out
+    float *dbg_ttft, *dbg_tpot, *dbg_nout;   // caller's per-candidate outputs [nq][N], or null
     OutArgs out;
 };
 

@@ -211,7 +211,9 @@ hipError_t launch_quality_bf16(const QualityArgs &a, int cus, hipStream_t s) {
 // carries column tiles h, h + 2, ... (one query per lane and tile pair).
 // Fused mode then applies Eq. 2, the bound test and the utility and keeps
 // each query's best candidate (Eq. 3); staged mode reads X from HBM and
-// writes TTFT/TPOT per candidate.
+// writes TTFT/TPOT per candidate.  X and the staged outputs are pair-major
+// (candidate (q, d) at d * nq + q): the 64 lanes of a wave, 64 consecutive
+// queries, read whole rows and write 256 contiguous bytes.
 template <int NT>
 struct MlpShape {
     static constexpr int kWaves = NT == 4 ? 4 : 8;
@@ -389,7 +391,7 @@ __global__ __launch_bounds__(MlpShape<NT>::kThreads, 1) void k_mlp_bf16(MlpArgs 
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
             const bf16x8 *xr = reinterpret_cast<const bf16x8 *>(
-                a.X + (static_cast<size_t>(qc[t]) * a.N + dfirst) * kFeatPad);
+                a.X + (static_cast<size_t>(dfirst) * nq + qc[t]) * kFeatPad);
             nr[t][0] = xr[h];
             nr[t][1] = xr[2 + h];
         }
@@ -411,7 +413,7 @@ __global__ __launch_bounds__(MlpShape<NT>::kThreads, 1) void k_mlp_bf16(MlpArgs 
     // per-candidate outputs when requested, then cost, bound test,
     // utility and the running argmax (Eq. 2, Eq. 3) of own query j
     auto take_candidate = [&](int j, int dd, float tt, float tp, float nc, float Q) {
-        const size_t ci = static_cast<size_t>(qmc[j]) * a.N + dd;
+        const size_t ci = a.cand_pm ? static_cast<size_t>(dd) * nq + qmc[j] : static_cast<size_t>(qmc[j]) * a.N + dd;
         if (!LEAN && a.cand_ttft && vme[j]) {
             a.cand_ttft[ci] = tt;
             a.cand_tpot[ci] = tp;
@@ -446,7 +448,7 @@ __global__ __launch_bounds__(MlpShape<NT>::kThreads, 1) void k_mlp_bf16(MlpArgs 
 #pragma unroll
                 for (int t = 0; t < NT; ++t) {
                     const bf16x8 *xr = reinterpret_cast<const bf16x8 *>(
-                        a.X + (static_cast<size_t>(qc[t]) * a.N + dn) * kFeatPad);
+                        a.X + (static_cast<size_t>(dn) * nq + qc[t]) * kFeatPad);
                     nr[t][0] = xr[h];
                     nr[t][1] = xr[2 + h];
                 }
@@ -810,7 +812,7 @@ __global__ __launch_bounds__(MlpShape<NT>::kThreads, 1) void k_mlp_bf16(MlpArgs 
                 float tt, tp, nc;
                 head_values(j, acc3[j][0], acc3[j][1], NH == 3 ? acc3[j][2] : 0.0f, tt, tp, nc);
                 if constexpr (STAGED) {
-                    const size_t ci = static_cast<size_t>(qmc[j]) * a.N + d;
+                    const size_t ci = static_cast<size_t>(d) * nq + qmc[j];   // pair-major
                     if (vme[j]) {
                         a.cand_ttft[ci] = tt;
                         a.cand_tpot[ci] = tp;

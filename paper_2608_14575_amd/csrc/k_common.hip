@@ -185,10 +185,11 @@ __global__ __launch_bounds__(256) void k_mlp_f32(MlpF32Args a) {
         const int d = static_cast<int>(c - q * a.N);
         float tt, tp, nc;
         predict_f32<H>(a, s, q, d, lane, tt, tp, nc);
-        if (lane == 0) {
-            a.cand_ttft[c] = tt;
-            a.cand_tpot[c] = tp;
-            if (a.nheads == 3) a.cand_nout[c] = nc;
+        if (lane == 0) {                 // pair-major, as the epilogue reads it
+            const size_t pm = static_cast<size_t>(d) * a.q.nq + q;
+            a.cand_ttft[pm] = tt;
+            a.cand_tpot[pm] = tp;
+            if (a.nheads == 3) a.cand_nout[pm] = nc;
         }
     }
 }
@@ -210,10 +211,12 @@ hipError_t launch_mlp_f32(int H, const MlpF32Args &args, hipStream_t s) {
 }
 
 // ------------------------------------------------------------ feature gather
-// Staged pipeline: X[q][d][0:32] (bf16) = the pair's feature row with the
-// query's input-length slot filled in.  Each workgroup stages all pair rows
-// in LDS once and broadcasts them across kGatherQ queries; every thread
-// writes one 16-byte piece, consecutive threads consecutive pieces.
+// Staged pipeline: X[d][q][0:32] (bf16, pair-major: for each pair the rows of
+// consecutive queries are consecutive, which is how the staged predictor reads
+// them) = the pair's feature row with the query's input-length slot filled
+// in.  Each workgroup stages all pair rows in LDS once and broadcasts them
+// over kGatherQ queries; consecutive threads write consecutive 16-byte pieces
+// of one pair's kGatherQ-row block (4 KB contiguous per pair).
 __global__ __launch_bounds__(256) void k_gather(GatherArgs a) {
     extern __shared__ uint4 s_dep[];          // [N][4]
     __shared__ uint32_t s_xl[kGatherQ];
@@ -224,14 +227,14 @@ __global__ __launch_bounds__(256) void k_gather(GatherArgs a) {
         s_xl[threadIdx.x] = bf16_bits(len_feature(a.q.input_len[q0 + threadIdx.x]));
     __syncthreads();
     const int nqb = min(kGatherQ, a.q.nq - q0);
-    const int per_q = a.N * 4;
-    const int total = nqb * per_q;
+    const int per_d = nqb * 4;
+    const int total = a.N * per_d;
     const int lpart = a.len_slot >> 3, lword = (a.len_slot & 7) >> 1, lhi = a.len_slot & 1;
     uint4 *X = reinterpret_cast<uint4 *>(a.X);
     for (int i = threadIdx.x; i < total; i += blockDim.x) {
-        const int qi = i / per_q;
-        const int rem = i - qi * per_q;
-        const int d = rem >> 2, part = rem & 3;
+        const int d = i / per_d;
+        const int rem = i - d * per_d;
+        const int qi = rem >> 2, part = rem & 3;
         uint4 v = s_dep[d * 4 + part];
         if (part == lpart) {
             const uint32_t xl = s_xl[qi];
@@ -242,7 +245,7 @@ __global__ __launch_bounds__(256) void k_gather(GatherArgs a) {
             if (lword == 2) v.z = (v.z & keep) | put;
             if (lword == 3) v.w = (v.w & keep) | put;
         }
-        X[(static_cast<size_t>(q0 + qi) * a.N + d) * 4 + part] = v;
+        X[(static_cast<size_t>(d) * a.q.nq + q0 + qi) * 4 + part] = v;
     }
 }
 
@@ -253,121 +256,86 @@ hipError_t launch_gather(const GatherArgs &a, hipStream_t s) {
 
 // ------------------------------------------------------------ decision epilogue
 // Per query: cost (Eq. 2), bound test and utility for every pair, then the
-// Eq. 3 argmax as a maximum of packed decision keys over the `group` lanes
-// that share the query -- once per cost weight (a lambda sweep reuses the
-// loaded predictions; outputs are then [query][weight]).  A lane takes up to kEpiSlices slices of the row
-// (4 pairs each with 16-byte loads when rows are aligned, else 1 pair); the
-// models of its pairs are the same for every query, so they are loaded
-// alongside.  Each wave stages the quality rows of its own queries in LDS
-// (no workgroup barrier).  Each lane keeps its own best candidate, so the
-// lane holding the winning key writes the outputs without reading anything
-// again.
-constexpr int kEpiSlices = 4;
+// Eq. 3 argmax -- once per cost weight (a lambda sweep; outputs are then
+// [query][weight]).  Predictions are pair-major: for each pair the values of
+// consecutive queries are consecutive, so lane i of a wave takes query
+// (32 * wave + i % 32) and pair group i / 32, and each load of the wave reads
+// two whole 128-byte lines (one per pair group).  Lane group g takes the
+// pairs g, g + 2, ...; the pairs' models and the wave's quality rows are
+// staged in LDS (rows padded to an odd stride: no bank conflicts).  Each lane
+// keeps its best candidate; the two lane groups of a query then compare
+// packed decision keys, and the lane holding the larger writes the outputs.
+// DBG also writes the caller's per-candidate outputs, [query][pair].
+constexpr int kEpiQ = 32;           // queries per wave
+constexpr int kEpiG = 2;            // pair groups per query
+constexpr int kEpiUnroll = 8;       // pairs per lane loaded before any is used
 
-// Template switches: V4 16-byte loads; PN N_out per candidate; MULTI several
-// cost weights; GEN a rule other than the default (normalised score, given
-// bound), whose branches the default kernel then leaves out.
-template <bool V4, bool PN, bool MULTI, bool GEN>
+template <bool PN, bool MULTI, bool GEN, bool DBG>
 __global__ __launch_bounds__(256) void k_epilogue(EpilogueArgs a) {
     Rule rule = a.rule;
     if constexpr (!GEN) rule = Rule{};
-    extern __shared__ float s_qm[];            // [4 waves][64 / G][M] quality rows
-    const int G = a.group;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = tid & (G - 1);
-    const int qpw = 64 / G;                    // queries per wave
-    const int qw0 = blockIdx.x * (kBlock / G) + wave * qpw;
-    const int q = qw0 + lane / G;
-    const bool valid = q < a.q.nq;
-    const int qc = valid ? q : 0;
-    const int units = V4 ? a.N / 4 : a.N;
-    const float *tt_row = a.cand_ttft + static_cast<size_t>(qc) * a.N;
-    const float *tp_row = a.cand_tpot + static_cast<size_t>(qc) * a.N;
-    // PN: N_out per candidate (predicted by a third head), else the query's
-    constexpr bool pn = PN;
-    const float *nn_row = pn ? a.cand_nout + static_cast<size_t>(qc) * a.N : nullptr;
-    auto load = [&](int u, f32x4 &tv, f32x4 &pv, f32x4 &nv, int4 &mv) {
-        if (V4) {
-            tv = reinterpret_cast<const f32x4 *>(tt_row)[u];
-            pv = reinterpret_cast<const f32x4 *>(tp_row)[u];
-            if (pn) nv = reinterpret_cast<const f32x4 *>(nn_row)[u];
-            mv = reinterpret_cast<const int4 *>(a.dep_model)[u];
-        } else {
-            tv[0] = tt_row[u];
-            pv[0] = tp_row[u];
-            if (pn) nv[0] = nn_row[u];
-            mv.x = a.dep_model[u];
-        }
-    };
-    f32x4 t4[kEpiSlices], p4[kEpiSlices], n4[kEpiSlices];
-    int4 m4[kEpiSlices];
-#pragma unroll
-    for (int j = 0; j < kEpiSlices; ++j) {
-        t4[j] = f32x4{0, 0, 0, 0};
-        p4[j] = f32x4{0, 0, 0, 0};
-        n4[j] = f32x4{0, 0, 0, 0};
-        m4[j] = int4{0, 0, 0, 0};
-        const int u = g + j * G;
-        if (valid && u < units) load(u, t4[j], p4[j], n4[j], m4[j]);
+    extern __shared__ float s_ep[];            // [N] models, then [4 waves][kEpiQ][MS] quality rows
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int ql = lane & (kEpiQ - 1), g = lane / kEpiQ;
+    const int MS = a.M | 1;                    // odd row stride
+    int32_t *s_model = reinterpret_cast<int32_t *>(s_ep);
+    float *s_q = s_ep + a.N + wave * kEpiQ * MS;
+    for (int i = tid; i < a.N; i += blockDim.x) s_model[i] = a.dep_model[i];
+    const int nq = a.q.nq;
+    const int qw0 = blockIdx.x * (4 * kEpiQ) + wave * kEpiQ;
+    const int nqw = max(0, min(kEpiQ, nq - qw0));
+    for (int i = lane; i < nqw * a.M; i += 64) {
+        const int r = i / a.M;
+        s_q[r * MS + (i - r * a.M)] = a.qmat[static_cast<size_t>(qw0) * a.M + i];
     }
-    const int32_t no = pn ? 0 : a.q.nout[qc];
+    __syncthreads();
+    const int q = qw0 + ql;
+    const bool valid = q < nq;
+    const int qc = valid ? q : 0;
+    const float *qrow = s_q + ql * MS;
+    const int32_t no = PN ? 0 : a.q.nout[qc];
     const float nout = static_cast<float>(no < 0 ? 0 : no);
     const float slo = a.q.slo ? a.q.slo[qc] : a.q.default_slo;
     const int32_t len = GEN ? a.q.input_len[qc] : 0;
-    float *s_qw = s_qm + wave * qpw * a.M;
-    const int nqw = max(0, min(qpw, a.q.nq - qw0));
-    for (int i = lane; i < nqw * a.M; i += 64) s_qw[i] = a.qmat[static_cast<size_t>(qw0) * a.M + i];
-    // the rows are read by other lanes of the same wave only: wait for this
-    // wave's LDS writes, no workgroup barrier
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
-    const float *qrow = s_qw + (lane / G) * a.M;
-    // one decision per cost weight, from the same loaded predictions
     const int nw = MULTI ? a.nw : 1;
+    const size_t stride = static_cast<size_t>(nq);
     for (int kw = 0; kw < nw; ++kw) {
-        if constexpr (MULTI) {
-            // opaque per weight: otherwise every candidate's cost and bound
-            // are hoisted out of this loop and held in registers
-#pragma unroll
-            for (int j = 0; j < kEpiSlices; ++j) asm volatile("" : "+v"(t4[j]), "+v"(p4[j]), "+v"(n4[j]));
-        }
         const QueryRule qrule = query_rule(rule, slo, len, nout, a.w[kw]);
         Best best = best_none();
-        auto consider = [&](int d, int model, float tt, float tp, float nc) {
-            const float n = pn ? nc : nout;
-            offer(best, decide(tt, tp, n, rule, qrule, qrow[model]), d, tt, tp, n);
-        };
-        auto consider_slice = [&](int u, const f32x4 &tv, const f32x4 &pv, const f32x4 &nv, const int4 &mv) {
-            if (V4) {
-                consider(4 * u + 0, mv.x, tv[0], pv[0], nv[0]);
-                consider(4 * u + 1, mv.y, tv[1], pv[1], nv[1]);
-                consider(4 * u + 2, mv.z, tv[2], pv[2], nv[2]);
-                consider(4 * u + 3, mv.w, tv[3], pv[3], nv[3]);
-            } else {
-                consider(u, mv.x, tv[0], pv[0], nv[0]);
-            }
-        };
+        for (int d0 = g; d0 < a.N; d0 += kEpiG * kEpiUnroll) {
+            float tv[kEpiUnroll], pv[kEpiUnroll], nv[kEpiUnroll];
 #pragma unroll
-        for (int j = 0; j < kEpiSlices; ++j) {
-            const int u = g + j * G;
-            if (valid && u < units) consider_slice(u, t4[j], p4[j], n4[j], m4[j]);
-        }
-        for (int u = g + kEpiSlices * G; valid && u < units; u += G) {
-            f32x4 tv = {0, 0, 0, 0}, pv = {0, 0, 0, 0}, nv = {0, 0, 0, 0};
-            int4 mv = {0, 0, 0, 0};
-            load(u, tv, pv, nv, mv);
-            consider_slice(u, tv, pv, nv, mv);
+            for (int u = 0; u < kEpiUnroll; ++u) {
+                const int d = d0 + kEpiG * u;
+                const size_t ci = static_cast<size_t>(d < a.N ? d : 0) * stride + qc;
+                tv[u] = a.cand_ttft[ci];
+                pv[u] = a.cand_tpot[ci];
+                nv[u] = PN ? a.cand_nout[ci] : nout;
+            }
+#pragma unroll
+            for (int u = 0; u < kEpiUnroll; ++u) {
+                const int d = d0 + kEpiG * u;
+                if (valid && d < a.N) {
+                    if (DBG && kw == 0) {
+                        const size_t co = static_cast<size_t>(q) * a.N + d;
+                        if (a.dbg_ttft) a.dbg_ttft[co] = tv[u];
+                        if (a.dbg_tpot) a.dbg_tpot[co] = pv[u];
+                        if (PN && a.dbg_nout) a.dbg_nout[co] = nv[u];
+                    }
+                    offer(best, decide(tv[u], pv[u], nv[u], rule, qrule, qrow[s_model[d]]), d, tv[u], pv[u], nv[u]);
+                }
+            }
         }
         const uint64_t k = best_key(best);
-        const uint64_t m = group_max_u64(k, G);
-        if (valid && k == m && k != 0)
+        const uint64_t o = shfl_xor_u64(k, kEpiQ);     // the query's other pair group
+        if (valid && k > o)
             write_outputs(a.out, q * nw + kw, k, best.u, best.e2e, best.tt, best.tp, best.n);
     }
 }
 
-template <bool V4, bool PN, bool MULTI, bool GEN>
+template <bool PN, bool MULTI, bool GEN, bool DBG>
 static hipError_t launch_epilogue_t(const EpilogueArgs &a, dim3 g, size_t lds, hipStream_t s) {
-    return launch_kernel(k_epilogue<V4, PN, MULTI, GEN>, g, dim3(kBlock), static_cast<uint32_t>(lds), s, a);
+    return launch_kernel(k_epilogue<PN, MULTI, GEN, DBG>, g, dim3(kBlock), static_cast<uint32_t>(lds), s, a);
 }
 
 hipError_t launch_epilogue(const EpilogueArgs &a, hipStream_t s) {
@@ -382,11 +350,12 @@ hipError_t launch_epilogue(const EpilogueArgs &a, hipStream_t s) {
         launch_epilogue_t<true, true, false, false>, launch_epilogue_t<true, true, false, true>,
         launch_epilogue_t<true, true, true, false>, launch_epilogue_t<true, true, true, true>,
     };
-    const int qpb = kBlock / a.group;
+    constexpr int qpb = 4 * kEpiQ;             // four waves per workgroup
     const unsigned grid = static_cast<unsigned>((a.q.nq + qpb - 1) / qpb);
-    const size_t lds = static_cast<size_t>(qpb) * a.M * 4;
+    const size_t lds = (static_cast<size_t>(a.N) + static_cast<size_t>(4) * kEpiQ * (a.M | 1)) * 4;
     const bool gen = a.rule.score_paper || a.rule.bound_paper;
-    const int idx = (a.vec4 ? 8 : 0) + (a.cand_nout ? 4 : 0) + (a.nw > 1 ? 2 : 0) + (gen ? 1 : 0);
+    const bool dbg = a.dbg_ttft || a.dbg_tpot || a.dbg_nout;
+    const int idx = (a.cand_nout ? 8 : 0) + (a.nw > 1 ? 4 : 0) + (gen ? 2 : 0) + (dbg ? 1 : 0);
     return table[idx](a, dim3(grid), lds, s);
 }
 
