@@ -36,7 +36,7 @@ PROFILE_EVERY = 4              # kernel timing samples one launch in four of eac
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_C5_1Mx256.json")
 KERNEL_NAMES = {   # as the profiler names them
     "fused": "void hwr::k_mlp_bf16<256, false, 2, true, 4, true>(hwr::MlpArgs)",
-    "mlp": "void hwr::k_mlp_bf16<256, true, 2, true, 2, false>(hwr::MlpArgs)",
+    "mlp": "void hwr::k_mlp_bf16<256, true, 2, true, 4, false>(hwr::MlpArgs)",
     "quality": "hwr::k_quality_bf16_lds(hwr::QualityArgs)",
     "gather": "hwr::k_gather(hwr::GatherArgs)",
     "epilogue": "void hwr::k_epilogue<false, false, false, false>(hwr::EpilogueArgs)",

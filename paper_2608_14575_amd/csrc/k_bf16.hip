@@ -386,15 +386,22 @@ __global__ __launch_bounds__(MlpShape<NT>::kThreads, 1) void k_mlp_bf16(MlpArgs 
     const bf16x8 *dep = reinterpret_cast<const bf16x8 *>(a.dep_bf16);
     const int dfirst = d0 < d1 ? d0 : 0;
     constexpr int NR = STAGED ? NT : 1;   // feature rows loaded per step
+    // staged four-tile form: the next step's rows are loaded once the first
+    // layer has consumed this step's (they share registers), in the
+    // second layer's shadow
+    constexpr bool kLateX = STAGED && NT == 4;
     bf16x8 nr[NR][2];
-    if constexpr (STAGED) {
+    auto load_x = [&](int dn) {
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
             const bf16x8 *xr = reinterpret_cast<const bf16x8 *>(
-                a.X + (static_cast<size_t>(dfirst) * nq + qc[t]) * kFeatPad);
+                a.X + (static_cast<size_t>(dn) * nq + qc[t]) * kFeatPad);
             nr[t][0] = xr[h];
             nr[t][1] = xr[2 + h];
         }
+    };
+    if constexpr (STAGED) {
+        load_x(dfirst);
     } else {
         nr[0][0] = dep[dfirst * 4 + h];
         nr[0][1] = dep[dfirst * 4 + 2 + h];
@@ -445,13 +452,7 @@ __global__ __launch_bounds__(MlpShape<NT>::kThreads, 1) void k_mlp_bf16(MlpArgs 
         {
             const int dn = d + 1 < d1 ? d + 1 : d;
             if constexpr (STAGED) {
-#pragma unroll
-                for (int t = 0; t < NT; ++t) {
-                    const bf16x8 *xr = reinterpret_cast<const bf16x8 *>(
-                        a.X + (static_cast<size_t>(dn) * nq + qc[t]) * kFeatPad);
-                    nr[t][0] = xr[h];
-                    nr[t][1] = xr[2 + h];
-                }
+                if constexpr (!kLateX) load_x(dn);
             } else {
                 nr[0][0] = dep[dn * 4 + h];
                 nr[0][1] = dep[dn * 4 + 2 + h];
@@ -684,6 +685,7 @@ __global__ __launch_bounds__(MlpShape<NT>::kThreads, 1) void k_mlp_bf16(MlpArgs 
             }
             // the last two k-blocks of row tile 0; the phase-B ring and the
             // bias of row tile 1 are loaded first
+            if constexpr (kLateX) load_x(d + 1 < d1 ? d + 1 : d);
             bf16x8 ring[kRing];
             auto w2idx = [&](int i) { return s_w2[(KB2 + i) * 64 + lo]; };   // row tiles 1.. in order
 #pragma unroll
@@ -760,7 +762,7 @@ __global__ __launch_bounds__(MlpShape<NT>::kThreads, 1) void k_mlp_bf16(MlpArgs 
             };
             using T = std::true_type;
             using F = std::false_type;
-            row_tile(std::integral_constant<int, 1>{}, T{});
+            row_tile(std::integral_constant<int, 1>{}, std::integral_constant<bool, !STAGED>{});
             row_tile(std::integral_constant<int, 2>{}, F{});
             row_tile(std::integral_constant<int, 3>{}, F{});
             row_tile(std::integral_constant<int, 4>{}, F{});
@@ -876,11 +878,14 @@ __global__ __launch_bounds__(MlpShape<NT>::kThreads, 1) void k_mlp_bf16(MlpArgs 
     }
 }
 
-// Column tiles per wave: four for the fused predictor at H = 256 (the
-// large-batch throughput shape) when the input-length slot lies in the
-// first k-block; two otherwise.
+// Column tiles per wave: four at H = 256 (the large-batch throughput shape)
+// for the staged predictor, and for the fused one when the input-length slot
+// lies in the first k-block; two otherwise.
 template <int H, bool STAGED, int NH, bool FB>
 static hipError_t launch_mlp_t(const MlpArgs &a, dim3 grid, hipStream_t s) {
+    if constexpr (H == 256 && STAGED) {
+        return launch_kernel(k_mlp_bf16<H, STAGED, NH, FB, 4, false>, grid, dim3(MlpShape<4>::kThreads), 0, s, a);
+    }
     if constexpr (H == 256 && !STAGED) {
         if (a.len_slot < 16) {          // the four-tile form patches k-block 0 only
             const bool lean = !a.cand_ttft && !a.cand_nout && !a.rule.score_paper && !a.rule.bound_paper;
