@@ -457,6 +457,45 @@ def cpu_baseline(pb, st, sample, sp, sample_wide=None):
             "host_cpu": cpu, "host_threads": os.cpu_count(), "all_cores": wide}
 
 
+PROBE_READ_BYTES = 4 << 30     # read-ceiling buffer: 16x the last-level cache
+
+
+def peak_probes(hwr, torch) -> dict:
+    """Achievable ceilings of this device, measured now with the library's
+    probe kernels: the register-fed bf16 MFMA rate (the better of one and two
+    waves per SIMD; launches of ~4 ms, long enough for the power limit to
+    act) and the streaming read rate of a 4 GiB buffer (the best of 1, 2, 4
+    and 8 waves per SIMD).  Each figure is the median of its timed launches."""
+    mfma = {w: hwr.hwr_probe_mfma_bf16(0, w, 16384, 9) for w in (1, 2)}
+    buf = torch.ones(PROBE_READ_BYTES // 4, dtype=torch.int32, device="cuda:0")
+    read = {w: hwr.hwr_probe_hbm_read(0, buf.data_ptr(), PROBE_READ_BYTES, w, 9) for w in (1, 2, 4, 8)}
+    del buf
+    torch.cuda.synchronize()
+    res = {"mfma_bf16_tflops": max(mfma.values()),
+           "mfma_bf16_by_waves_per_simd": {str(k): v for k, v in mfma.items()},
+           "hbm_read_gbs": max(read.values()),
+           "hbm_read_by_waves_per_simd": {str(k): v for k, v in read.items()},
+           "probes": "hwr_probe_mfma_bf16 (32x32x16 bf16, register operands, 8 chains per wave), "
+                     f"hwr_probe_hbm_read ({PROBE_READ_BYTES >> 30} GiB streaming read, non-temporal 16-byte loads)"}
+    log(f"ceilings: MFMA bf16 {res['mfma_bf16_tflops']:.0f} TFLOP/s "
+        f"({res['mfma_bf16_tflops'] / PEAK_BF16_TFLOPS:.3f} of nominal), HBM read "
+        f"{res['hbm_read_gbs']:.0f} GB/s ({res['hbm_read_gbs'] / PEAK_HBM_GBS:.3f} of nominal)")
+    return res
+
+
+def with_achievable(line: dict, ceilings: dict) -> dict:
+    """Adds the fraction of the measured ceiling of the line's bound next to
+    the fraction of the published peak."""
+    if line is None or not ceilings:
+        return line
+    peak = ceilings["mfma_bf16_tflops"] if line["bound"] == "mfma" else ceilings["hbm_read_gbs"]
+    line["achievable_peak"] = peak
+    line["achievable_frac"] = line["achieved"] / peak if peak > 0 else None
+    if "with_quality" in line:
+        line["with_quality"]["achievable_frac"] = line["with_quality"]["achieved"] / peak if peak > 0 else None
+    return line
+
+
 def copy_probe(torch) -> int:
     """A plain device-to-device copy of 1 GiB, three times: the reference
     for scaling the FETCH_SIZE / WRITE_SIZE counters to bytes."""
@@ -497,6 +536,10 @@ def main() -> int:
                     help="extra sustained-overload arrival rates (the paper sweeps 15, 18, 21 req/s)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain device copy of known size (counter calibration)")
+    ap.add_argument("--peak-probe", action="store_true",
+                    help="only measure the achievable MFMA and HBM-read ceilings and print them")
+    ap.add_argument("--no-peak-probe", action="store_true",
+                    help="skip the ceiling probes (rooflines carry the nominal fraction only)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the library has no multi-GPU path "
@@ -512,6 +555,9 @@ def main() -> int:
     if args.copy_probe:
         return copy_probe(torch)
     hwr.load()
+    if args.peak_probe:
+        print(json.dumps(peak_probes(hwr, torch)), flush=True)
+        return 0
     w = prepare(args, S, torch)
     res = throughput(args, hwr, torch, w, args.pipeline, args.steps, args.warmup)
     log(f"throughput {res['value']:.3e} candidates/s, predictor {res['roofline']['achieved']:.1f} TFLOP/s")
@@ -524,6 +570,15 @@ def main() -> int:
                   "stages": sr["stages"]}
         log(f"staged: gather {sr['gather_roofline']['frac']:.2f} of HBM, "
             f"epilogue {sr['epilogue_roofline']['frac']:.2f} of HBM")
+    # ceilings measured right after the throughput steps, in the same power
+    # and thermal state
+    ceilings = None if args.no_peak_probe else peak_probes(hwr, torch)
+    if ceilings:
+        with_achievable(res["roofline"], ceilings)
+        with_achievable(res["quality_roofline"], ceilings)
+        if staged:
+            for k in ("gather_roofline", "epilogue_roofline", "mlp_roofline"):
+                with_achievable(staged[k], ceilings)
     single = None if args.no_single else single_query(args, S, hwr, torch)
     single_graph = None if args.no_single else single_query(args, S, hwr, torch, hwr.HWR_FLAG_GRAPH)
     single_res = None if args.no_single else single_query(args, S, hwr, torch, hwr.HWR_FLAG_RESIDENT)
@@ -544,7 +599,7 @@ def main() -> int:
         "single_query": single, "single_query_graph_launch": single_graph,
         "single_query_resident": single_res,
         "step_ms": res["step_ms"], "quality_roofline": res["quality_roofline"], "stages": res["stages"],
-        "staged_pipeline": staged, "batch_latency": batch, "closed_loop": sim, "closed_loop_pareto": pareto,
+        "staged_pipeline": staged, "ceilings": ceilings, "batch_latency": batch, "closed_loop": sim, "closed_loop_pareto": pareto,
     }
     print(json.dumps(line), flush=True)
     return 0

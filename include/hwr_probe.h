@@ -1,0 +1,60 @@
+/*
+ * hwr_probe.h -- measured ceilings of the device the library runs on.
+ *
+ * The routing kernels are quoted against two kinds of peak: the part's
+ * published one (dense bf16 MFMA 2.5 PFLOP/s, HBM3E 8 TB/s) and the one a
+ * plain kernel actually reaches on the same device, in the same thermal and
+ * power state.  These two entry points measure the second kind:
+ *
+ *  - hwr_probe_mfma_bf16: bf16 matrix products (32x32x16, fp32 accumulate) fed
+ *    from registers only -- no memory traffic, eight independent accumulators
+ *    per wave, operands that change from product to product (so the matrix
+ *    cores draw the power real data makes them draw).  It bounds what any
+ *    MFMA kernel can issue on this part at the clock the power limit allows.
+ *  - hwr_probe_hbm_read: a streaming read of a caller buffer much larger than
+ *    the last-level cache, non-temporal 16-byte loads by every lane, eight in
+ *    flight per lane.  It bounds what a read-dominated kernel can fetch from
+ *    HBM.
+ *
+ * Both are synchronous: they launch on a stream of their own on the given
+ * device, wait, and return the median rate over the timed launches (each
+ * launch timed on the device from its own start to its own end).  They
+ * allocate small device buffers of their own (the products' results, one
+ * word for the read) and free them before returning.  Not part of routing:
+ * nothing in hwr.h calls them.
+ */
+#ifndef HWR_PROBE_H
+#define HWR_PROBE_H
+
+#include <stdint.h>
+
+#include "hwr.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Register-fed bf16 MFMA rate in TFLOP/s (2 * 32 * 32 * 16 flops per
+ * product).  waves_per_simd (1..2): waves resident on each SIMD of every
+ * compute unit; iters (>= 1): loop trips of eight products per wave and
+ * launch; reps (1..64): timed launches after one untimed one.  *tflops is
+ * the median over the timed launches.  Errors: HWR_ERR_INVALID_ARG for a
+ * NULL tflops or an argument out of range (no device touched), HWR_ERR_HIP,
+ * HWR_ERR_OOM. */
+hwr_status hwr_probe_mfma_bf16(int32_t device, int32_t waves_per_simd, int32_t iters, int32_t reps,
+                               double *tflops);
+
+/* Streaming read rate in GB/s (1e9 bytes per second) of `bytes` bytes at
+ * `buf`, device memory of `device` owned by the caller and only read.  buf
+ * 16-byte aligned, bytes a non-zero multiple of 16; waves_per_simd (1..8)
+ * as above; reps (1..64) timed launches after one untimed one.  *gbps is the
+ * median.  Errors: HWR_ERR_INVALID_ARG (NULL pointer, misaligned buffer,
+ * size or count out of range; no device touched), HWR_ERR_HIP, HWR_ERR_OOM. */
+hwr_status hwr_probe_hbm_read(int32_t device, const void *buf, uint64_t bytes, int32_t waves_per_simd,
+                              int32_t reps, double *gbps);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HWR_PROBE_H */

@@ -16,7 +16,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libhwr.so")
 BUILD = os.path.join(PKG, "_build")
 
-SOURCES = ["hwr_api.hip", "k_common.hip", "k_bf16.hip", "k_single.hip", "hwr_sim.cpp"]
+SOURCES = ["hwr_api.hip", "k_common.hip", "k_bf16.hip", "k_single.hip", "k_probe.hip", "hwr_sim.cpp"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

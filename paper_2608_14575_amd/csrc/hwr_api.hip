@@ -595,15 +595,16 @@ hwr_status init_impl(const hwr_config *cfg, hwr_ctx **out) {
         INIT_HIP(upload(&c->d_b2, cfg->b2, H));
     }
     const size_t chunk = static_cast<size_t>(c->max_chunk);
+    const size_t ldq = static_cast<size_t>(pair_stride(c->max_chunk));   // pair-major row stride
     INIT_HIP(dev_alloc(&c->d_qmat, chunk * M));
     // per-candidate predictions in HBM: staged and fp32 paths, and several
     // cost weights (the decisions then run after the predictor)
     if (!c->bf16 || c->pipeline == HWR_PIPE_STAGED || c->nw > 1) {
-        INIT_HIP(dev_alloc(&c->d_ctt, chunk * N));
-        INIT_HIP(dev_alloc(&c->d_ctp, chunk * N));
-        if (c->NH == 3) INIT_HIP(dev_alloc(&c->d_cno, chunk * N));
+        INIT_HIP(dev_alloc(&c->d_ctt, ldq * N));
+        INIT_HIP(dev_alloc(&c->d_ctp, ldq * N));
+        if (c->NH == 3) INIT_HIP(dev_alloc(&c->d_cno, ldq * N));
     }
-    if (c->bf16 && c->pipeline == HWR_PIPE_STAGED) INIT_HIP(dev_alloc(&c->d_X, chunk * N * kFeatPad));
+    if (c->bf16 && c->pipeline == HWR_PIPE_STAGED) INIT_HIP(dev_alloc(&c->d_X, ldq * N * kFeatPad));
     if (c->bf16 && c->pipeline == HWR_PIPE_FUSED) {
         c->part_cap = static_cast<size_t>(2 * c->cus) * kQPerBlock;
         INIT_HIP(dev_alloc(&c->d_pkey, c->part_cap));
@@ -706,6 +707,7 @@ hwr_status route_device(hwr_ctx *c, const DevBatch &b, const Workspace &w) {
     const size_t esz = c->bf16 ? 2 : 4;
     for (int off = 0; off < b.n; off += w.max_chunk) {
         const int cn = std::min(w.max_chunk, b.n - off);
+        const int ldq = pair_stride(cn);       // pair-major row stride of this chunk
         QueryArgs qa;
         qa.nq = cn;
         qa.input_len = b.len + off;
@@ -769,6 +771,7 @@ hwr_status route_device(hwr_ctx *c, const DevBatch &b, const Workspace &w) {
             ma.w3_frag = c->d_w3_frag;
             ma.out = oa;
             ma.nsplit = 1;
+            ma.ldq = ldq;
             if (c->pipeline == HWR_PIPE_FUSED && c->nw == 1) {
                 // per-candidate outputs, if the caller asked for them, go
                 // straight to its [query][pair] buffers
@@ -803,7 +806,7 @@ hwr_status route_device(hwr_ctx *c, const DevBatch &b, const Workspace &w) {
                 ma.nsplit = 1;
                 HWR_HIP(c, timed(c, HWR_K_FUSED, [&] { return launch_mlp_bf16(c->H, false, ma, c->stream); }));
             } else {
-                GatherArgs ga{N, c->len_slot, qa, c->d_dep_bf16, w.X};
+                GatherArgs ga{N, c->len_slot, qa, c->d_dep_bf16, w.X, ldq};
                 HWR_HIP(c, timed(c, HWR_K_GATHER, [&] { return launch_gather(ga, c->stream); }));
                 ma.X = w.X;
                 ma.cand_ttft = w.ctt;
@@ -814,6 +817,7 @@ hwr_status route_device(hwr_ctx *c, const DevBatch &b, const Workspace &w) {
             }
         } else {
             MlpF32Args fa = f32_args(c, qa);
+            fa.ldq = ldq;
             fa.cand_ttft = w.ctt;
             fa.cand_tpot = w.ctp;
             fa.cand_nout = w.cno;
@@ -826,6 +830,7 @@ hwr_status route_device(hwr_ctx *c, const DevBatch &b, const Workspace &w) {
         EpilogueArgs ea{};
         ea.N = N;
         ea.M = M;
+        ea.ldq = ldq;
         ea.rule = c->rule;
         ea.nw = c->nw;
         for (int k = 0; k < c->nw; ++k) ea.w[k] = c->w[k];
@@ -1171,10 +1176,13 @@ Workspace scratch_workspace(const hwr_ctx *c) {
     const size_t part_cap = fused1 ? static_cast<size_t>(2 * c->cus) * kQPerBlock : 0;
     const size_t fixed = up(part_cap * sizeof(uint64_t)) + up(part_cap * kPartVals * sizeof(float));
     const size_t row = M * 4 + (per_cand ? N * 4 * (c->NH == 3 ? 3 : 2) : 0) + (staged ? N * kFeatPad * 2 : 0);
-    const size_t slack = 5 * 256;                       // alignment of the per-row blocks
+    // alignment of the per-row blocks, and the pair-major rows padded to
+    // pair_stride(rows) (at most kPairAlign - 1 more rows)
+    const size_t slack = 5 * 256 + (kPairAlign - 1) * row;
     if (fixed + slack >= kScratchBytes) return w;
     const size_t rows = std::min<size_t>((kScratchBytes - fixed - slack) / row, static_cast<size_t>(c->max_chunk));
     if (rows < 1) return w;
+    const size_t ldq = static_cast<size_t>(pair_stride(static_cast<int>(rows)));
     unsigned char *base = static_cast<unsigned char *>(c->scratch);
     size_t off = 0;
     auto take = [&](size_t bytes) {
@@ -1189,11 +1197,11 @@ Workspace scratch_workspace(const hwr_ctx *c) {
     }
     w.qmat = reinterpret_cast<float *>(take(rows * M * 4));
     if (per_cand) {
-        w.ctt = reinterpret_cast<float *>(take(rows * N * 4));
-        w.ctp = reinterpret_cast<float *>(take(rows * N * 4));
-        if (c->NH == 3) w.cno = reinterpret_cast<float *>(take(rows * N * 4));
+        w.ctt = reinterpret_cast<float *>(take(ldq * N * 4));
+        w.ctp = reinterpret_cast<float *>(take(ldq * N * 4));
+        if (c->NH == 3) w.cno = reinterpret_cast<float *>(take(ldq * N * 4));
     }
-    if (staged) w.X = reinterpret_cast<uint16_t *>(take(rows * N * kFeatPad * 2));
+    if (staged) w.X = reinterpret_cast<uint16_t *>(take(ldq * N * kFeatPad * 2));
     w.max_chunk = static_cast<int>(rows);
     return off <= kScratchBytes ? w : Workspace{};
 }

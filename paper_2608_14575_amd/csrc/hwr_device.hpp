@@ -179,7 +179,8 @@ __device__ inline Best best_none() {
 template <bool TrackN = true>
 __device__ inline void offer(Best &b, const Decision &r, int d, float tt, float tp, float n) {
     const float u = fmaxf(r.u, -__builtin_huge_valf()) + 0.0f;   // NaN -> -inf, -0 -> +0
-    const bool better = b.d < 0 || (r.feasible && !b.f) || (r.feasible == b.f && u > b.u);
+    // (bitwise, not short-circuit: no branches)
+    const bool better = (b.d < 0) | (r.feasible & !b.f) | ((r.feasible == b.f) & (u > b.u));
     // selects, not a branch: one v_cndmask per field
     b.u = better ? u : b.u;
     b.e2e = better ? r.e2e : b.e2e;

@@ -30,6 +30,12 @@ constexpr int kMaxWeights = 8;   // cost weights scored in one call (HWR_MAX_WEI
 // past every feature (the layout puts zeros after the eight signals), so the
 // weights they replace never contribute.
 constexpr int kFoldSlot = kFeatPad - 3;
+// Pair-major per-candidate buffers ([pair][query]: predictions, staged
+// features) space consecutive pairs by the chunk's query count rounded up to
+// whole 16-byte groups of fp32 values, so that every pair's row starts
+// 16-byte aligned.
+constexpr int kPairAlign = 4;
+__host__ __device__ constexpr int pair_stride(int nq) { return (nq + kPairAlign - 1) / kPairAlign * kPairAlign; }
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -139,10 +145,11 @@ struct MlpArgs {                  // bf16 predictor (fused or staged)
     const uint16_t *w1_pk, *w2_pk;
     const float *b1_pk, *b2_pk;
     const uint16_t *w3_frag;      // head layer A fragments (compact, see pack_predictor)
-    const uint16_t *X;            // staged input [N][nq][32] (pair-major)
+    const uint16_t *X;            // staged input [N][ldq][32] (pair-major)
     float *cand_ttft, *cand_tpot; // per-candidate TTFT / TPOT: staged, several weights or debug
     float *cand_nout;             // predicted N_out (three heads), same layout
-    int cand_pm;                  // 1: pair-major [N][nq] (staged always); 0: [nq][N]
+    int cand_pm;                  // 1: pair-major [N][ldq] (staged always); 0: [nq][N]
+    int ldq;                      // pair stride of the pair-major buffers: pair_stride(nq)
     OutArgs out;
     int nsplit;                   // pair ranges (grid.y); >1 writes partials
     uint64_t *part_key;           // [nsplit][nq]
@@ -156,7 +163,8 @@ struct MlpF32Args {
     QueryArgs q;
     const float *dep_f32;         // [N][32]
     const float *w1, *b1, *w2, *b2, *w3;   // [F][H], [H], [H][H], [H], [H][nheads]
-    float *cand_ttft, *cand_tpot, *cand_nout;   // [N][nq], pair-major; cand_nout: three heads only
+    float *cand_ttft, *cand_tpot, *cand_nout;   // [N][ldq], pair-major; cand_nout: three heads only
+    int ldq;                      // pair_stride(nq)
     int with_quality;             // workgroups past mlp_blocks run `quality`
     int mlp_blocks;               // set by launch_mlp_f32
     QualityArgs quality;
@@ -166,20 +174,22 @@ struct GatherArgs {
     int N, len_slot;
     QueryArgs q;
     const uint16_t *dep_bf16;     // [N][32]
-    uint16_t *X;                  // [N][nq][32], pair-major
+    uint16_t *X;                  // [N][ldq][32], pair-major
+    int ldq;                      // pair_stride(nq)
 };
 
-// Decision epilogue over pair-major predictions: candidate (q, d) at d * nq + q.
+// Decision epilogue over pair-major predictions: candidate (q, d) at d * ldq + q.
 struct EpilogueArgs {
     int N, M;
+    int ldq;                      // pair_stride(nq)
     Rule rule;
     int nw;                       // cost weights (>= 1); outputs are [nq][nw] when nw > 1
     float w[kMaxWeights];
     QueryArgs q;
     const int32_t *dep_model;
     const float *qmat;            // [nq][M]
-    const float *cand_ttft, *cand_tpot;   // [N][nq]
-    const float *cand_nout;       // [N][nq] predicted N_out, or null: the query's given N_out
+    const float *cand_ttft, *cand_tpot;   // [N][ldq], 16-byte aligned
+    const float *cand_nout;       // [N][ldq] predicted N_out, or null: the query's given N_out
     float *dbg_ttft, *dbg_tpot, *dbg_nout;   // caller's per-candidate outputs [nq][N], or null
     OutArgs out;
 };

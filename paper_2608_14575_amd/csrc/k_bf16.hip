@@ -395,7 +395,7 @@ __global__ __launch_bounds__(MlpShape<NT>::kThreads, 1) void k_mlp_bf16(MlpArgs 
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
             const bf16x8 *xr = reinterpret_cast<const bf16x8 *>(
-                a.X + (static_cast<size_t>(dn) * nq + qc[t]) * kFeatPad);
+                a.X + (static_cast<size_t>(dn) * a.ldq + qc[t]) * kFeatPad);
             nr[t][0] = xr[h];
             nr[t][1] = xr[2 + h];
         }
@@ -420,7 +420,7 @@ __global__ __launch_bounds__(MlpShape<NT>::kThreads, 1) void k_mlp_bf16(MlpArgs 
     // per-candidate outputs when requested, then cost, bound test,
     // utility and the running argmax (Eq. 2, Eq. 3) of own query j
     auto take_candidate = [&](int j, int dd, float tt, float tp, float nc, float Q) {
-        const size_t ci = a.cand_pm ? static_cast<size_t>(dd) * nq + qmc[j] : static_cast<size_t>(qmc[j]) * a.N + dd;
+        const size_t ci = a.cand_pm ? static_cast<size_t>(dd) * a.ldq + qmc[j] : static_cast<size_t>(qmc[j]) * a.N + dd;
         if (!LEAN && a.cand_ttft && vme[j]) {
             a.cand_ttft[ci] = tt;
             a.cand_tpot[ci] = tp;
@@ -814,7 +814,7 @@ __global__ __launch_bounds__(MlpShape<NT>::kThreads, 1) void k_mlp_bf16(MlpArgs 
                 float tt, tp, nc;
                 head_values(j, acc3[j][0], acc3[j][1], NH == 3 ? acc3[j][2] : 0.0f, tt, tp, nc);
                 if constexpr (STAGED) {
-                    const size_t ci = static_cast<size_t>(d) * nq + qmc[j];   // pair-major
+                    const size_t ci = static_cast<size_t>(d) * a.ldq + qmc[j];   // pair-major
                     if (vme[j]) {
                         a.cand_ttft[ci] = tt;
                         a.cand_tpot[ci] = tp;

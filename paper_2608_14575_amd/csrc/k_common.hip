@@ -186,7 +186,7 @@ __global__ __launch_bounds__(256) void k_mlp_f32(MlpF32Args a) {
         float tt, tp, nc;
         predict_f32<H>(a, s, q, d, lane, tt, tp, nc);
         if (lane == 0) {                 // pair-major, as the epilogue reads it
-            const size_t pm = static_cast<size_t>(d) * a.q.nq + q;
+            const size_t pm = static_cast<size_t>(d) * a.ldq + q;
             a.cand_ttft[pm] = tt;
             a.cand_tpot[pm] = tp;
             if (a.nheads == 3) a.cand_nout[pm] = nc;
@@ -245,7 +245,7 @@ __global__ __launch_bounds__(256) void k_gather(GatherArgs a) {
             if (lword == 2) v.z = (v.z & keep) | put;
             if (lword == 3) v.w = (v.w & keep) | put;
         }
-        X[(static_cast<size_t>(d) * a.q.nq + q0 + qi) * 4 + part] = v;
+        X[(static_cast<size_t>(d) * a.ldq + q0 + qi) * 4 + part] = v;
     }
 }
 
@@ -257,85 +257,126 @@ hipError_t launch_gather(const GatherArgs &a, hipStream_t s) {
 // ------------------------------------------------------------ decision epilogue
 // Per query: cost (Eq. 2), bound test and utility for every pair, then the
 // Eq. 3 argmax -- once per cost weight (a lambda sweep; outputs are then
-// [query][weight]).  Predictions are pair-major: for each pair the values of
-// consecutive queries are consecutive, so lane i of a wave takes query
-// (32 * wave + i % 32) and pair group i / 32, and each load of the wave reads
-// two whole 128-byte lines (one per pair group).  Lane group g takes the
-// pairs g, g + 2, ...; the pairs' models and the wave's quality rows are
-// staged in LDS (rows padded to an odd stride: no bank conflicts).  Each lane
-// keeps its best candidate; the two lane groups of a query then compare
-// packed decision keys, and the lane holding the larger writes the outputs.
-// DBG also writes the caller's per-candidate outputs, [query][pair].
-constexpr int kEpiQ = 32;           // queries per wave
-constexpr int kEpiG = 2;            // pair groups per query
-constexpr int kEpiUnroll = 8;       // pairs per lane loaded before any is used
+// [query][weight]).  Predictions are pair-major with 16-byte aligned pair
+// rows: a workgroup takes kEpiQB consecutive queries, lane i of every wave
+// the four queries 4i .. 4i + 3 of them (one 16-byte load per pair and
+// array, so each load of a wave reads 1 KB of one pair's row), and wave w
+// the pairs w, w + 4, ... in increasing order.  The quality rows of the
+// workgroup's queries are staged in LDS transposed ([model][query]), so the
+// lane's four values of one model are one 16-byte read; the pairs' models
+// are staged too.  Each lane keeps the best candidate of each of its
+// queries; the four waves then compare packed decision keys through LDS
+// (unique: they hold the pair index), and the wave holding the largest
+// writes the outputs.  DBG also writes the caller's per-candidate outputs,
+// [query][pair].
+constexpr int kEpiQL = 4;                  // queries per lane
+constexpr int kEpiQB = 64 * kEpiQL;        // queries per workgroup
+constexpr int kEpiW = 16;                  // waves per workgroup: pair classes mod kEpiW
+constexpr int kEpiThreads = 64 * kEpiW;
+constexpr int kEpiQS = kEpiQB + 4;         // LDS quality row stride (16-byte multiple, offset banks)
+constexpr int kEpiUnroll = 2;              // pairs per wave loaded before any is used
 
 template <bool PN, bool MULTI, bool GEN, bool DBG>
-__global__ __launch_bounds__(256) void k_epilogue(EpilogueArgs a) {
+__global__ __launch_bounds__(kEpiThreads) void k_epilogue(EpilogueArgs a) {
     Rule rule = a.rule;
     if constexpr (!GEN) rule = Rule{};
-    extern __shared__ float s_ep[];            // [N] models, then [4 waves][kEpiQ][MS] quality rows
+    // [pair_stride(N)] models | [M][kEpiQS] quality | [kEpiW][kEpiQB] keys
+    extern __shared__ __attribute__((aligned(16))) float s_ep[];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int ql = lane & (kEpiQ - 1), g = lane / kEpiQ;
-    const int MS = a.M | 1;                    // odd row stride
     int32_t *s_model = reinterpret_cast<int32_t *>(s_ep);
-    float *s_q = s_ep + a.N + wave * kEpiQ * MS;
-    for (int i = tid; i < a.N; i += blockDim.x) s_model[i] = a.dep_model[i];
+    float *s_qt = s_ep + pair_stride(a.N);
+    uint64_t *s_key = reinterpret_cast<uint64_t *>(s_qt + static_cast<size_t>(a.M) * kEpiQS);
+    for (int i = tid; i < a.N; i += kEpiThreads) s_model[i] = a.dep_model[i];
     const int nq = a.q.nq;
-    const int qw0 = blockIdx.x * (4 * kEpiQ) + wave * kEpiQ;
-    const int nqw = max(0, min(kEpiQ, nq - qw0));
-    for (int i = lane; i < nqw * a.M; i += 64) {
-        const int r = i / a.M;
-        s_q[r * MS + (i - r * a.M)] = a.qmat[static_cast<size_t>(qw0) * a.M + i];
+    const int q0 = blockIdx.x * kEpiQB;
+    const int nqb = min(kEpiQB, nq - q0);
+    for (int i = tid; i < nqb * a.M; i += kEpiThreads) {
+        const int r = i / a.M, m = i - r * a.M;
+        s_qt[m * kEpiQS + r] = a.qmat[static_cast<size_t>(q0) * a.M + i];
     }
     __syncthreads();
-    const int q = qw0 + ql;
-    const bool valid = q < nq;
-    const int qc = valid ? q : 0;
-    const float *qrow = s_q + ql * MS;
-    const int32_t no = PN ? 0 : a.q.nout[qc];
-    const float nout = static_cast<float>(no < 0 ? 0 : no);
-    const float slo = a.q.slo ? a.q.slo[qc] : a.q.default_slo;
-    const int32_t len = GEN ? a.q.input_len[qc] : 0;
+    const int ql = kEpiQL * lane;              // the lane's first query, in the workgroup
+    bool valid[kEpiQL];
+    float nout[kEpiQL], slo[kEpiQL];
+    int32_t len[kEpiQL];
+#pragma unroll
+    for (int j = 0; j < kEpiQL; ++j) {
+        valid[j] = ql + j < nqb;
+        const int qc = valid[j] ? q0 + ql + j : 0;
+        const int32_t no = PN ? 0 : a.q.nout[qc];
+        nout[j] = static_cast<float>(no < 0 ? 0 : no);
+        slo[j] = a.q.slo ? a.q.slo[qc] : a.q.default_slo;
+        len[j] = GEN ? a.q.input_len[qc] : 0;
+    }
+    // lanes past the chunk's padded end read pair rows from their start
+    const size_t col = q0 + ql < a.ldq ? static_cast<size_t>(q0 + ql) : 0;
+    const size_t ld = static_cast<size_t>(a.ldq);
     const int nw = MULTI ? a.nw : 1;
-    const size_t stride = static_cast<size_t>(nq);
     for (int kw = 0; kw < nw; ++kw) {
-        const QueryRule qrule = query_rule(rule, slo, len, nout, a.w[kw]);
-        Best best = best_none();
-        for (int d0 = g; d0 < a.N; d0 += kEpiG * kEpiUnroll) {
-            float tv[kEpiUnroll], pv[kEpiUnroll], nv[kEpiUnroll];
+        QueryRule qrule[kEpiQL];
+        Best best[kEpiQL];
+#pragma unroll
+        for (int j = 0; j < kEpiQL; ++j) {
+            qrule[j] = query_rule(rule, slo[j], len[j], nout[j], a.w[kw]);
+            best[j] = best_none();
+        }
+        for (int d0 = wave; d0 < a.N; d0 += kEpiW * kEpiUnroll) {
+            f32x4 tv[kEpiUnroll], pv[kEpiUnroll], nv[kEpiUnroll];
 #pragma unroll
             for (int u = 0; u < kEpiUnroll; ++u) {
-                const int d = d0 + kEpiG * u;
-                const size_t ci = static_cast<size_t>(d < a.N ? d : 0) * stride + qc;
-                tv[u] = a.cand_ttft[ci];
-                pv[u] = a.cand_tpot[ci];
-                nv[u] = PN ? a.cand_nout[ci] : nout;
+                const int d = d0 + kEpiW * u;
+                const size_t ci = static_cast<size_t>(d < a.N ? d : 0) * ld + col;
+                tv[u] = *reinterpret_cast<const f32x4 *>(a.cand_ttft + ci);
+                pv[u] = *reinterpret_cast<const f32x4 *>(a.cand_tpot + ci);
+                if constexpr (PN) nv[u] = *reinterpret_cast<const f32x4 *>(a.cand_nout + ci);
             }
 #pragma unroll
             for (int u = 0; u < kEpiUnroll; ++u) {
-                const int d = d0 + kEpiG * u;
-                if (valid && d < a.N) {
-                    if (DBG && kw == 0) {
-                        const size_t co = static_cast<size_t>(q) * a.N + d;
-                        if (a.dbg_ttft) a.dbg_ttft[co] = tv[u];
-                        if (a.dbg_tpot) a.dbg_tpot[co] = pv[u];
-                        if (PN && a.dbg_nout) a.dbg_nout[co] = nv[u];
+                const int d = d0 + kEpiW * u;
+                if (d < a.N) {
+                    const f32x4 qv = *reinterpret_cast<const f32x4 *>(s_qt + s_model[d] * kEpiQS + ql);
+                    // every query of the lane is decided (a query past the
+                    // chunk's end only reads padding, and is never written)
+#pragma unroll
+                    for (int j = 0; j < kEpiQL; ++j) {
+                        const float nc = PN ? nv[u][j] : nout[j];
+                        if (DBG && kw == 0 && valid[j]) {
+                            const size_t co = static_cast<size_t>(q0 + ql + j) * a.N + d;
+                            if (a.dbg_ttft) a.dbg_ttft[co] = tv[u][j];
+                            if (a.dbg_tpot) a.dbg_tpot[co] = pv[u][j];
+                            if (PN && a.dbg_nout) a.dbg_nout[co] = nc;
+                        }
+                        offer(best[j], decide(tv[u][j], pv[u][j], nc, rule, qrule[j], qv[j]), d, tv[u][j], pv[u][j], nc);
                     }
-                    offer(best, decide(tv[u], pv[u], nv[u], rule, qrule, qrow[s_model[d]]), d, tv[u], pv[u], nv[u]);
                 }
             }
         }
-        const uint64_t k = best_key(best);
-        const uint64_t o = shfl_xor_u64(k, kEpiQ);     // the query's other pair group
-        if (valid && k > o)
-            write_outputs(a.out, q * nw + kw, k, best.u, best.e2e, best.tt, best.tp, best.n);
+        uint64_t key[kEpiQL];
+#pragma unroll
+        for (int j = 0; j < kEpiQL; ++j) {
+            key[j] = best_key(best[j]);
+            s_key[wave * kEpiQB + ql + j] = key[j];
+        }
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < kEpiQL; ++j) {
+            uint64_t top = 0;
+#pragma unroll
+            for (int v = 0; v < kEpiW; ++v) {
+                const uint64_t o = s_key[v * kEpiQB + ql + j];
+                top = o > top ? o : top;
+            }
+            if (valid[j] && key[j] == top)
+                write_outputs(a.out, (q0 + ql + j) * nw + kw, key[j], best[j].u, best[j].e2e, best[j].tt, best[j].tp,
+                              best[j].n);
+        }
+        __syncthreads();                       // the next weight reuses the keys
     }
 }
 
 template <bool PN, bool MULTI, bool GEN, bool DBG>
 static hipError_t launch_epilogue_t(const EpilogueArgs &a, dim3 g, size_t lds, hipStream_t s) {
-    return launch_kernel(k_epilogue<PN, MULTI, GEN, DBG>, g, dim3(kBlock), static_cast<uint32_t>(lds), s, a);
+    return launch_kernel(k_epilogue<PN, MULTI, GEN, DBG>, g, dim3(kEpiThreads), static_cast<uint32_t>(lds), s, a);
 }
 
 hipError_t launch_epilogue(const EpilogueArgs &a, hipStream_t s) {
@@ -350,9 +391,9 @@ hipError_t launch_epilogue(const EpilogueArgs &a, hipStream_t s) {
         launch_epilogue_t<true, true, false, false>, launch_epilogue_t<true, true, false, true>,
         launch_epilogue_t<true, true, true, false>, launch_epilogue_t<true, true, true, true>,
     };
-    constexpr int qpb = 4 * kEpiQ;             // four waves per workgroup
-    const unsigned grid = static_cast<unsigned>((a.q.nq + qpb - 1) / qpb);
-    const size_t lds = (static_cast<size_t>(a.N) + static_cast<size_t>(4) * kEpiQ * (a.M | 1)) * 4;
+    const unsigned grid = static_cast<unsigned>((a.q.nq + kEpiQB - 1) / kEpiQB);
+    const size_t lds = (static_cast<size_t>(pair_stride(a.N)) + static_cast<size_t>(a.M) * kEpiQS) * 4 +
+                       static_cast<size_t>(kEpiW) * kEpiQB * 8;
     const bool gen = a.rule.score_paper || a.rule.bound_paper;
     const bool dbg = a.dbg_ttft || a.dbg_tpot || a.dbg_nout;
     const int idx = (a.cand_nout ? 8 : 0) + (a.nw > 1 ? 4 : 0) + (gen ? 2 : 0) + (dbg ? 1 : 0);

@@ -1,0 +1,181 @@
+// Ceiling probes of the device (gfx950): register-fed bf16 MFMA and a
+// streaming HBM read.  They give the achievable peaks next to the published
+// ones; nothing on the routing path calls them.
+#include <hip/hip_ext.h>
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdint>
+
+#include "hwr_probe.h"
+
+namespace {
+
+typedef __bf16 pbf16x8 __attribute__((ext_vector_type(8)));
+typedef float pf32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int kProbeThreads = 256;    // four waves: one per SIMD of a compute unit
+constexpr int kChains = 8;            // independent accumulators per wave
+constexpr int kFrags = 4;             // distinct A and B operands, cycled
+
+// bf16 of a uniform value in [-1, 1) drawn from a 32-bit LCG state
+__device__ inline __bf16 probe_value(uint32_t &s) {
+    s = s * 1664525u + 1013904223u;
+    const float f = __uint_as_float(0x3F800000u | (s >> 9)) * 2.0f - 3.0f;   // [1,2) -> [-1,1)
+    return static_cast<__bf16>(f);
+}
+
+__global__ __launch_bounds__(kProbeThreads) void k_probe_mfma(int iters, float *out) {
+    uint32_t s = (blockIdx.x * kProbeThreads + threadIdx.x) * 0x9E3779B9u + 0x7F4A7C15u;
+    pbf16x8 a[kFrags], b[kFrags];
+#pragma unroll
+    for (int f = 0; f < kFrags; ++f)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            a[f][e] = probe_value(s);
+            b[f][e] = probe_value(s);
+        }
+    pf32x16 c[kChains];
+#pragma unroll
+    for (int k = 0; k < kChains; ++k) c[k] = pf32x16{};
+    for (int it = 0; it < iters; ++it) {
+        // consecutive products take different operands
+#pragma unroll
+        for (int k = 0; k < kChains; ++k)
+            c[k] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[k % kFrags], b[(k + k / kFrags) % kFrags], c[k], 0, 0, 0);
+    }
+    // two elements per accumulator: enough to keep every product, and the
+    // reads stay few, so that two waves fit on a SIMD
+    float sum = 0.0f;
+#pragma unroll
+    for (int k = 0; k < kChains; ++k) sum += c[k][0] + c[k][15];
+    out[blockIdx.x * kProbeThreads + threadIdx.x] = sum;
+}
+
+typedef uint32_t pu32x4 __attribute__((ext_vector_type(4)));
+constexpr int kReadUnroll = 8;        // loads in flight per lane
+
+// Every lane reads 16 bytes per load, kReadUnroll loads in flight,
+// grid-strided, non-temporal (streamed past the caches: measured on this
+// part, plain loads of the same pattern reach about 12% less); the single
+// store happens only for one XOR value, which keeps the loads.
+__global__ __launch_bounds__(kProbeThreads) void k_probe_read(const pu32x4 *__restrict__ p, uint64_t n,
+                                                              uint32_t *out) {
+    const uint64_t stride = static_cast<uint64_t>(gridDim.x) * kProbeThreads;
+    uint64_t i = static_cast<uint64_t>(blockIdx.x) * kProbeThreads + threadIdx.x;
+    uint32_t acc = 0;
+    for (; i + (kReadUnroll - 1) * stride < n; i += kReadUnroll * stride) {
+        pu32x4 v[kReadUnroll];
+#pragma unroll
+        for (int u = 0; u < kReadUnroll; ++u) v[u] = __builtin_nontemporal_load(p + i + u * stride);
+#pragma unroll
+        for (int u = 0; u < kReadUnroll; ++u) acc += v[u][0] ^ v[u][1] ^ v[u][2] ^ v[u][3];
+    }
+    for (; i < n; i += stride) {
+        const pu32x4 v = __builtin_nontemporal_load(p + i);
+        acc ^= v[0] ^ v[1] ^ v[2] ^ v[3];
+    }
+    if (acc == 0x2545F491u) out[0] = acc;
+}
+
+hwr_status status_of(hipError_t e) {
+    if (e == hipSuccess) return HWR_OK;
+    return e == hipErrorOutOfMemory ? HWR_ERR_OOM : HWR_ERR_HIP;
+}
+
+// Makes `device` current for the probe and restores the caller's device.
+struct DeviceScope {
+    int prev = -1;
+    hipError_t err = hipSuccess;
+    explicit DeviceScope(int device) {
+        err = hipGetDevice(&prev);
+        if (err == hipSuccess) err = hipSetDevice(device);
+    }
+    ~DeviceScope() {
+        if (prev >= 0) (void)hipSetDevice(prev);
+    }
+};
+
+// One untimed launch, then `reps` launches each timed on the device from its
+// start to its end; the median duration in ms.
+template <typename Launch>
+hipError_t median_ms(Launch launch, int reps, float *ms) {
+    hipStream_t s = nullptr;
+    hipEvent_t ev[2 * 64] = {};
+    float t[64];
+    hipError_t e = hipStreamCreateWithFlags(&s, hipStreamNonBlocking);
+    for (int i = 0; e == hipSuccess && i < 2 * reps; ++i) e = hipEventCreate(&ev[i]);
+    if (e == hipSuccess) e = launch(s, nullptr, nullptr);
+    for (int i = 0; e == hipSuccess && i < reps; ++i) e = launch(s, ev[2 * i], ev[2 * i + 1]);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    for (int i = 0; e == hipSuccess && i < reps; ++i) e = hipEventElapsedTime(&t[i], ev[2 * i], ev[2 * i + 1]);
+    if (e == hipSuccess) {
+        std::sort(t, t + reps);
+        *ms = reps % 2 ? t[reps / 2] : 0.5f * (t[reps / 2 - 1] + t[reps / 2]);
+    }
+    for (int i = 0; i < 2 * reps; ++i)
+        if (ev[i]) (void)hipEventDestroy(ev[i]);
+    if (s) (void)hipStreamDestroy(s);
+    return e;
+}
+
+}  // namespace
+
+extern "C" hwr_status hwr_probe_mfma_bf16(int32_t device, int32_t waves_per_simd, int32_t iters, int32_t reps,
+                                          double *tflops) {
+    if (!tflops || device < 0 || waves_per_simd < 1 || waves_per_simd > 2 || iters < 1 || reps < 1 || reps > 64)
+        return HWR_ERR_INVALID_ARG;
+    DeviceScope scope(device);
+    if (scope.err != hipSuccess) return status_of(scope.err);
+    hipDeviceProp_t prop;
+    hipError_t e = hipGetDeviceProperties(&prop, device);
+    if (e != hipSuccess) return status_of(e);
+    const int blocks = prop.multiProcessorCount * waves_per_simd;
+    float *out = nullptr;
+    e = hipMalloc(&out, static_cast<size_t>(blocks) * kProbeThreads * sizeof(float));
+    if (e != hipSuccess) return status_of(e);
+    float ms = 0.0f;
+    e = median_ms(
+        [&](hipStream_t s, hipEvent_t a, hipEvent_t b) {
+            hipExtLaunchKernelGGL(k_probe_mfma, dim3(blocks), dim3(kProbeThreads), 0, s, a, b, 0u, iters, out);
+            return hipGetLastError();
+        },
+        reps, &ms);
+    (void)hipFree(out);
+    if (e != hipSuccess) return status_of(e);
+    if (!(ms > 0.0f)) return HWR_ERR_HIP;
+    const double flops = 2.0 * 32 * 32 * 16 * kChains * static_cast<double>(iters) * blocks * (kProbeThreads / 64);
+    *tflops = flops / (ms * 1e-3) / 1e12;
+    return HWR_OK;
+}
+
+extern "C" hwr_status hwr_probe_hbm_read(int32_t device, const void *buf, uint64_t bytes, int32_t waves_per_simd,
+                                         int32_t reps, double *gbps) {
+    if (!gbps || !buf || device < 0 || bytes == 0 || bytes % 16 != 0 ||
+        reinterpret_cast<uintptr_t>(buf) % 16 != 0 || waves_per_simd < 1 || waves_per_simd > 8 || reps < 1 ||
+        reps > 64)
+        return HWR_ERR_INVALID_ARG;
+    DeviceScope scope(device);
+    if (scope.err != hipSuccess) return status_of(scope.err);
+    hipDeviceProp_t prop;
+    hipError_t e = hipGetDeviceProperties(&prop, device);
+    if (e != hipSuccess) return status_of(e);
+    const int blocks = prop.multiProcessorCount * waves_per_simd;
+    uint32_t *out = nullptr;
+    e = hipMalloc(&out, sizeof(uint32_t));
+    if (e != hipSuccess) return status_of(e);
+    const pu32x4 *p = static_cast<const pu32x4 *>(buf);
+    const uint64_t n = bytes / 16;
+    float ms = 0.0f;
+    e = median_ms(
+        [&](hipStream_t s, hipEvent_t a, hipEvent_t b) {
+            hipExtLaunchKernelGGL(k_probe_read, dim3(blocks), dim3(kProbeThreads), 0, s, a, b, 0u, p, n, out);
+            return hipGetLastError();
+        },
+        reps, &ms);
+    (void)hipFree(out);
+    if (e != hipSuccess) return status_of(e);
+    if (!(ms > 0.0f)) return HWR_ERR_HIP;
+    *gbps = static_cast<double>(bytes) / (ms * 1e-3) / 1e9;
+    return HWR_OK;
+}

@@ -31,7 +31,8 @@ KERNEL_NAMES = ["state", "quality", "gather", "mlp", "epilogue", "fused", "merge
 
 EXPORTS = ["hwr_init", "hwr_update_hw_state", "hwr_route_batch", "hwr_route_batch_static", "hwr_free",
            "hwr_last_error",
-           "hwr_profile_enable", "hwr_profile_read", "hwr_sim_run", "hwr_sim_last_error"]
+           "hwr_profile_enable", "hwr_profile_read", "hwr_sim_run", "hwr_sim_last_error",
+           "hwr_probe_mfma_bf16", "hwr_probe_hbm_read"]
 
 _STATUS = {0: "HWR_OK", -1: "HWR_ERR_INVALID_ARG", -2: "HWR_ERR_OOM", -3: "HWR_ERR_HIP",
            -4: "HWR_ERR_STATE", -5: "HWR_ERR_UNSUPPORTED"}
@@ -134,6 +135,14 @@ def load(path: Optional[str] = None) -> C.CDLL:
     if not os.path.exists(p):
         raise RuntimeError(f"libhwr.so not found at {p}: build it first "
                            "(python -m paper_2608_14575_amd.build); there is no fallback")
+    # torch carries its own copy of the HIP runtime under the same soname as
+    # the one the library is linked against.  Loaded first, that copy is the
+    # one the library binds to; loaded after the library, it would be a
+    # second runtime in the process, and the second to start finds no GPU.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     L = C.CDLL(p)
     L.hwr_init.restype = C.c_int
     L.hwr_init.argtypes = [C.POINTER(hwr_config), C.POINTER(_vp)]
@@ -156,6 +165,10 @@ def load(path: Optional[str] = None) -> C.CDLL:
                               hwr_sim_router_fn, _vp, C.POINTER(hwr_sim_result)]
     L.hwr_sim_last_error.restype = C.c_char_p
     L.hwr_sim_last_error.argtypes = []
+    L.hwr_probe_mfma_bf16.restype = C.c_int
+    L.hwr_probe_mfma_bf16.argtypes = [C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.POINTER(C.c_double)]
+    L.hwr_probe_hbm_read.restype = C.c_int
+    L.hwr_probe_hbm_read.argtypes = [C.c_int32, _vp, C.c_uint64, C.c_int32, C.c_int32, C.POINTER(C.c_double)]
     if path is None:
         _lib = L
     return L
@@ -186,6 +199,20 @@ def hwr_route_batch(ctx, batch: hwr_query_batch, result: hwr_route_result) -> No
 
 def hwr_route_batch_static(ctx, batch: hwr_query_batch, result: hwr_route_result) -> None:
     _check(load().hwr_route_batch_static(ctx, C.byref(batch), C.byref(result)), ctx)
+
+
+def hwr_probe_mfma_bf16(device: int, waves_per_simd: int, iters: int, reps: int) -> float:
+    """Register-fed bf16 MFMA rate of the device in TFLOP/s (median launch)."""
+    out = C.c_double()
+    _check(load().hwr_probe_mfma_bf16(device, waves_per_simd, iters, reps, C.byref(out)), None)
+    return out.value
+
+
+def hwr_probe_hbm_read(device: int, buf_ptr: int, nbytes: int, waves_per_simd: int, reps: int) -> float:
+    """Streaming read rate in GB/s of nbytes of device memory at buf_ptr."""
+    out = C.c_double()
+    _check(load().hwr_probe_hbm_read(device, buf_ptr, nbytes, waves_per_simd, reps, C.byref(out)), None)
+    return out.value
 
 
 def hwr_free(ctx) -> None:

@@ -168,6 +168,25 @@ def test_null_arguments(lib):
     lib.hwr_free(None)
 
 
+def test_probe_argument_errors(lib):
+    """The ceiling probes reject bad arguments before touching a device."""
+    out = C.c_double(-1.0)
+    bad_mfma = [(0, 1, 16, 3, None), (-1, 1, 16, 3, C.byref(out)), (0, 0, 16, 3, C.byref(out)),
+                (0, 3, 16, 3, C.byref(out)), (0, 1, 0, 3, C.byref(out)), (0, 1, 16, 0, C.byref(out)),
+                (0, 1, 16, 65, C.byref(out))]
+    for args in bad_mfma:
+        assert lib.hwr_probe_mfma_bf16(*args) == hwr.HWR_ERR_INVALID_ARG, args
+    buf = 1 << 20    # never dereferenced: every call below fails its checks first
+    bad_read = [(0, None, 1 << 20, 2, 3, C.byref(out)), (0, buf, 0, 2, 3, C.byref(out)),
+                (0, buf, 1000, 2, 3, C.byref(out)), (0, buf + 8, 1 << 20, 2, 3, C.byref(out)),
+                (0, buf, 1 << 20, 0, 3, C.byref(out)), (0, buf, 1 << 20, 9, 3, C.byref(out)),
+                (0, buf, 1 << 20, 2, 0, C.byref(out)), (0, buf, 1 << 20, 2, 3, None),
+                (-1, buf, 1 << 20, 2, 3, C.byref(out))]
+    for args in bad_read:
+        assert lib.hwr_probe_hbm_read(*args) == hwr.HWR_ERR_INVALID_ARG, args
+    assert out.value == -1.0
+
+
 def test_no_device_is_a_clean_error(lib):
     import torch
     if torch.cuda.is_available():

@@ -73,10 +73,13 @@ def test_empty_batch_is_noop():
 
 
 @pytest.mark.parametrize("pipeline", ["fused", "staged"])
-def test_chunking_is_invisible(pipeline):
+@pytest.mark.parametrize("chunk", [100, 101])
+def test_chunking_is_invisible(pipeline, chunk):
+    """333 queries in one chunk and in chunks of 100 or 101 (pair-major rows
+    then padded to 104 queries, the last chunk to 36 or 32)."""
     sp, pb, st, qs = _case(n_queries=333)
     a = G.make_router(pb, pipeline=pipeline)
-    b = G.make_router(pb, pipeline=pipeline, max_chunk=100)
+    b = G.make_router(pb, pipeline=pipeline, max_chunk=chunk)
     a.update(st)
     b.update(st)
     _same(G.route_device(a, qs, "bf16"), G.route_device(b, qs, "bf16"))
