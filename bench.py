@@ -107,11 +107,11 @@ def prepare(args, S, torch):
     return dict(sp=sp, pb=pb, st=st, emb=emb, il=il, no=no, slo=slo, sample=sample, sample_wide=sample_wide)
 
 
-def hbm_line(nbytes: float, avg_ms: float, kernel: str, traffic=None) -> dict:
+def hbm_line(nbytes: float, avg_ms: float, kernel: str, traffic=None, direction: str = "read") -> dict:
     gbs = nbytes / (avg_ms / 1e3) / 1e9 if avg_ms > 0 else 0.0
     return {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
             "frac": gbs / PEAK_HBM_GBS, "traffic": traffic, "bytes_per_launch": nbytes,
-            "avg_launch_ms": avg_ms, "kernel": kernel}
+            "avg_launch_ms": avg_ms, "kernel": kernel, "hbm_dir": direction}
 
 
 def throughput(args, hwr, torch, w, pipeline, steps, warmup):
@@ -206,7 +206,7 @@ def throughput(args, hwr, torch, w, pipeline, steps, warmup):
         # (8 B per candidate), the Q matrix, N_out and the bound, writes
         # choice, feasible and four floats per query
         res["gather_roofline"] = hbm_line(chunk_cands * 64 + nq * 4 + N * 64, avg("gather"), "k_gather",
-                                          traffic.get("gather"))
+                                          traffic.get("gather"), "write")
         res["epilogue_roofline"] = hbm_line(chunk_cands * 8 + nq * (M * 4 + 8 + 21), avg("epilogue"),
                                             "k_epilogue", traffic.get("epilogue"))
     return res
@@ -469,26 +469,35 @@ def peak_probes(hwr, torch) -> dict:
     mfma = {w: hwr.hwr_probe_mfma_bf16(0, w, 16384, 9) for w in (1, 2)}
     buf = torch.ones(PROBE_READ_BYTES // 4, dtype=torch.int32, device="cuda:0")
     read = {w: hwr.hwr_probe_hbm_read(0, buf.data_ptr(), PROBE_READ_BYTES, w, 9) for w in (1, 2, 4, 8)}
+    write = {w: hwr.hwr_probe_hbm_write(0, buf.data_ptr(), PROBE_READ_BYTES, w, 9) for w in (1, 2, 4, 8)}
     del buf
     torch.cuda.synchronize()
     res = {"mfma_bf16_tflops": max(mfma.values()),
            "mfma_bf16_by_waves_per_simd": {str(k): v for k, v in mfma.items()},
            "hbm_read_gbs": max(read.values()),
            "hbm_read_by_waves_per_simd": {str(k): v for k, v in read.items()},
+           "hbm_write_gbs": max(write.values()),
+           "hbm_write_by_waves_per_simd": {str(k): v for k, v in write.items()},
            "probes": "hwr_probe_mfma_bf16 (32x32x16 bf16, register operands, 8 chains per wave), "
-                     f"hwr_probe_hbm_read ({PROBE_READ_BYTES >> 30} GiB streaming read, non-temporal 16-byte loads)"}
+                     f"hwr_probe_hbm_read ({PROBE_READ_BYTES >> 30} GiB streaming read, non-temporal 16-byte loads), "
+                     f"hwr_probe_hbm_write (the same buffer, 16-byte stores)"}
     log(f"ceilings: MFMA bf16 {res['mfma_bf16_tflops']:.0f} TFLOP/s "
         f"({res['mfma_bf16_tflops'] / PEAK_BF16_TFLOPS:.3f} of nominal), HBM read "
-        f"{res['hbm_read_gbs']:.0f} GB/s ({res['hbm_read_gbs'] / PEAK_HBM_GBS:.3f} of nominal)")
+        f"{res['hbm_read_gbs']:.0f} GB/s ({res['hbm_read_gbs'] / PEAK_HBM_GBS:.3f} of nominal), HBM write "
+        f"{res['hbm_write_gbs']:.0f} GB/s ({res['hbm_write_gbs'] / PEAK_HBM_GBS:.3f} of nominal)")
     return res
 
 
 def with_achievable(line: dict, ceilings: dict) -> dict:
     """Adds the fraction of the measured ceiling of the line's bound next to
-    the fraction of the published peak."""
+    the fraction of the published peak: the MFMA ceiling, or the HBM read or
+    write ceiling by the kernel's dominant direction (`hbm_dir`)."""
     if line is None or not ceilings:
         return line
-    peak = ceilings["mfma_bf16_tflops"] if line["bound"] == "mfma" else ceilings["hbm_read_gbs"]
+    if line["bound"] == "mfma":
+        peak = ceilings["mfma_bf16_tflops"]
+    else:
+        peak = ceilings["hbm_write_gbs" if line.get("hbm_dir") == "write" else "hbm_read_gbs"]
     line["achievable_peak"] = peak
     line["achievable_frac"] = line["achieved"] / peak if peak > 0 else None
     if "with_quality" in line:

@@ -4,7 +4,7 @@
  * The routing kernels are quoted against two kinds of peak: the part's
  * published one (dense bf16 MFMA 2.5 PFLOP/s, HBM3E 8 TB/s) and the one a
  * plain kernel actually reaches on the same device, in the same thermal and
- * power state.  These two entry points measure the second kind:
+ * power state.  These three entry points measure the second kind:
  *
  *  - hwr_probe_mfma_bf16: bf16 matrix products (32x32x16, fp32 accumulate) fed
  *    from registers only -- no memory traffic, eight independent accumulators
@@ -15,13 +15,16 @@
  *    the last-level cache, non-temporal 16-byte loads by every lane, eight in
  *    flight per lane.  It bounds what a read-dominated kernel can fetch from
  *    HBM.
+ *  - hwr_probe_hbm_write: the same for 16-byte stores of every lane into a
+ *    caller buffer (its contents are overwritten).  It bounds a
+ *    write-dominated kernel.
  *
- * Both are synchronous: they launch on a stream of their own on the given
+ * All are synchronous: they launch on a stream of their own on the given
  * device, wait, and return the median rate over the timed launches (each
- * launch timed on the device from its own start to its own end).  They
- * allocate small device buffers of their own (the products' results, one
- * word for the read) and free them before returning.  Not part of routing:
- * nothing in hwr.h calls them.
+ * launch timed on the device from its own start to its own end).  The MFMA
+ * and read probes allocate small device buffers of their own (the products'
+ * results, one word for the read) and free them before returning.  Not part
+ * of routing: nothing in hwr.h calls them.
  */
 #ifndef HWR_PROBE_H
 #define HWR_PROBE_H
@@ -52,6 +55,12 @@ hwr_status hwr_probe_mfma_bf16(int32_t device, int32_t waves_per_simd, int32_t i
  * size or count out of range; no device touched), HWR_ERR_HIP, HWR_ERR_OOM. */
 hwr_status hwr_probe_hbm_read(int32_t device, const void *buf, uint64_t bytes, int32_t waves_per_simd,
                               int32_t reps, double *gbps);
+
+/* Streaming write rate in GB/s of `bytes` bytes at `buf`, device memory of
+ * `device` owned by the caller, whose contents the probe overwrites.
+ * Arguments and errors as hwr_probe_hbm_read. */
+hwr_status hwr_probe_hbm_write(int32_t device, void *buf, uint64_t bytes, int32_t waves_per_simd,
+                               int32_t reps, double *gbps);
 
 #ifdef __cplusplus
 }

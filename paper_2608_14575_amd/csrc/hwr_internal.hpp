@@ -18,7 +18,7 @@ constexpr int kBlock = 256;      // threads per workgroup of the batch kernels
 constexpr int kQPerWave = 64;    // fused predictor: queries per wave (two 32-column tiles)
 constexpr int kQPerBlock = kQPerWave * 4;   // four query sub-blocks per workgroup
 constexpr int kMlpThreads = 512;             // predictor workgroup with two column tiles per wave: 8 waves
-constexpr int kGatherQ = 64;     // feature gather: queries per workgroup
+constexpr int kGatherQ = 256;    // feature gather: queries per workgroup (one wave per SIMD)
 constexpr int kMaxPairs = 1024;
 constexpr int kMaxModels = 32;
 constexpr int kMaxHeads = 3;     // predictor outputs: TTFT, TPOT and (optionally) N_out

@@ -1,5 +1,5 @@
-// Ceiling probes of the device (gfx950): register-fed bf16 MFMA and a
-// streaming HBM read.  They give the achievable peaks next to the published
+// Ceiling probes of the device (gfx950): register-fed bf16 MFMA, a streaming
+// HBM read and a streaming HBM write.  They give the achievable peaks next to the published
 // ones; nothing on the routing path calls them.
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
@@ -76,6 +76,15 @@ __global__ __launch_bounds__(kProbeThreads) void k_probe_read(const pu32x4 *__re
         acc ^= v[0] ^ v[1] ^ v[2] ^ v[3];
     }
     if (acc == 0x2545F491u) out[0] = acc;
+}
+
+// Every lane writes 16 bytes per store, grid-strided, plain stores (on this
+// part non-temporal and unrolled forms measured no faster).
+__global__ __launch_bounds__(kProbeThreads) void k_probe_write(pu32x4 *__restrict__ p, uint64_t n) {
+    const uint64_t stride = static_cast<uint64_t>(gridDim.x) * kProbeThreads;
+    uint64_t i = static_cast<uint64_t>(blockIdx.x) * kProbeThreads + threadIdx.x;
+    const pu32x4 v = {static_cast<uint32_t>(i), 1u, 2u, 3u};
+    for (; i < n; i += stride) p[i] = v;
 }
 
 hwr_status status_of(hipError_t e) {
@@ -174,6 +183,33 @@ extern "C" hwr_status hwr_probe_hbm_read(int32_t device, const void *buf, uint64
         },
         reps, &ms);
     (void)hipFree(out);
+    if (e != hipSuccess) return status_of(e);
+    if (!(ms > 0.0f)) return HWR_ERR_HIP;
+    *gbps = static_cast<double>(bytes) / (ms * 1e-3) / 1e9;
+    return HWR_OK;
+}
+
+extern "C" hwr_status hwr_probe_hbm_write(int32_t device, void *buf, uint64_t bytes, int32_t waves_per_simd,
+                                          int32_t reps, double *gbps) {
+    if (!gbps || !buf || device < 0 || bytes == 0 || bytes % 16 != 0 ||
+        reinterpret_cast<uintptr_t>(buf) % 16 != 0 || waves_per_simd < 1 || waves_per_simd > 8 || reps < 1 ||
+        reps > 64)
+        return HWR_ERR_INVALID_ARG;
+    DeviceScope scope(device);
+    if (scope.err != hipSuccess) return status_of(scope.err);
+    hipDeviceProp_t prop;
+    hipError_t e = hipGetDeviceProperties(&prop, device);
+    if (e != hipSuccess) return status_of(e);
+    const int blocks = prop.multiProcessorCount * waves_per_simd;
+    pu32x4 *p = static_cast<pu32x4 *>(buf);
+    const uint64_t n = bytes / 16;
+    float ms = 0.0f;
+    e = median_ms(
+        [&](hipStream_t s, hipEvent_t a, hipEvent_t b) {
+            hipExtLaunchKernelGGL(k_probe_write, dim3(blocks), dim3(kProbeThreads), 0, s, a, b, 0u, p, n);
+            return hipGetLastError();
+        },
+        reps, &ms);
     if (e != hipSuccess) return status_of(e);
     if (!(ms > 0.0f)) return HWR_ERR_HIP;
     *gbps = static_cast<double>(bytes) / (ms * 1e-3) / 1e9;

@@ -184,6 +184,7 @@ def test_probe_argument_errors(lib):
                 (-1, buf, 1 << 20, 2, 3, C.byref(out))]
     for args in bad_read:
         assert lib.hwr_probe_hbm_read(*args) == hwr.HWR_ERR_INVALID_ARG, args
+        assert lib.hwr_probe_hbm_write(*args) == hwr.HWR_ERR_INVALID_ARG, args
     assert out.value == -1.0
 
 

@@ -16,21 +16,32 @@ def test_mfma_ceiling_is_below_the_published_peak():
         assert 500.0 < t <= 2500.0
 
 
-def test_hbm_read_ceiling_is_below_the_published_peak():
+def test_hbm_ceilings_are_below_the_published_peak():
     import torch
     hwr.load()
     nbytes = 1 << 30
     buf = torch.ones(nbytes // 4, dtype=torch.int32, device="cuda:0")
+    # 1 GiB is four times the last-level cache: at most a quarter of it can
+    # be served from there
     for w in (2, 8):
         g = hwr.hwr_probe_hbm_read(0, buf.data_ptr(), nbytes, w, 3)
         print(f"[probe] hbm read 1 GiB, {w} waves per SIMD: {g:.0f} GB/s", flush=True)
-        # 1 GiB is four times the last-level cache: at most a quarter of it
-        # can be served from there
         assert 1000.0 < g < 8000.0 * 1.35
     # a length that is not a whole number of 16-byte pieces, a misaligned start
-    with pytest.raises(hwr.HwrError):
-        hwr.hwr_probe_hbm_read(0, buf.data_ptr(), 1000, 2, 3)
-    with pytest.raises(hwr.HwrError):
-        hwr.hwr_probe_hbm_read(0, buf.data_ptr() + 4, 1 << 20, 2, 3)
-    # the probe only reads
+    for probe in (hwr.hwr_probe_hbm_read, hwr.hwr_probe_hbm_write):
+        with pytest.raises(hwr.HwrError):
+            probe(0, buf.data_ptr(), 1000, 2, 3)
+        with pytest.raises(hwr.HwrError):
+            probe(0, buf.data_ptr() + 4, 1 << 20, 2, 3)
+    # the read probe only reads; rejected calls write nothing
     assert bool((buf == 1).all())
+    for w in (1, 4):
+        g = hwr.hwr_probe_hbm_write(0, buf.data_ptr(), nbytes, w, 3)
+        print(f"[probe] hbm write 1 GiB, {w} waves per SIMD: {g:.0f} GB/s", flush=True)
+        assert 1000.0 < g < 8000.0 * 1.35
+    # the write probe stays inside its buffer: a guard after it is untouched
+    torch.cuda.synchronize()
+    big = torch.zeros(nbytes // 4 + 1024, dtype=torch.int32, device="cuda:0")
+    hwr.hwr_probe_hbm_write(0, big.data_ptr(), nbytes, 2, 1)
+    assert bool((big[nbytes // 4:] == 0).all())
+    assert bool((big[:nbytes // 4] != 0).any())
