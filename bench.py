@@ -466,7 +466,8 @@ def peak_probes(hwr, torch) -> dict:
     waves per SIMD; launches of ~4 ms, long enough for the power limit to
     act) and the streaming read rate of a 4 GiB buffer (the best of 1, 2, 4
     and 8 waves per SIMD).  Each figure is the median of its timed launches."""
-    mfma = {w: hwr.hwr_probe_mfma_bf16(0, w, 16384, 9) for w in (1, 2)}
+    mfma_clk = {w: hwr.hwr_probe_mfma_bf16(0, w, 16384, 9) for w in (1, 2)}
+    mfma = {w: v[0] for w, v in mfma_clk.items()}
     buf = torch.ones(PROBE_READ_BYTES // 4, dtype=torch.int32, device="cuda:0")
     read = {w: hwr.hwr_probe_hbm_read(0, buf.data_ptr(), PROBE_READ_BYTES, w, 9) for w in (1, 2, 4, 8)}
     write = {w: hwr.hwr_probe_hbm_write(0, buf.data_ptr(), PROBE_READ_BYTES, w, 9) for w in (1, 2, 4, 8)}
@@ -474,6 +475,9 @@ def peak_probes(hwr, torch) -> dict:
     torch.cuda.synchronize()
     res = {"mfma_bf16_tflops": max(mfma.values()),
            "mfma_bf16_by_waves_per_simd": {str(k): v for k, v in mfma.items()},
+           # shader clock during the product loops (the published peak
+           # assumes 2.4 GHz)
+           "mfma_clock_mhz_by_waves_per_simd": {str(k): v[1] for k, v in mfma_clk.items()},
            "hbm_read_gbs": max(read.values()),
            "hbm_read_by_waves_per_simd": {str(k): v for k, v in read.items()},
            "hbm_write_gbs": max(write.values()),
@@ -481,7 +485,8 @@ def peak_probes(hwr, torch) -> dict:
            "probes": "hwr_probe_mfma_bf16 (32x32x16 bf16, register operands, 8 chains per wave), "
                      f"hwr_probe_hbm_read ({PROBE_READ_BYTES >> 30} GiB streaming read, non-temporal 16-byte loads), "
                      f"hwr_probe_hbm_write (the same buffer, 16-byte stores)"}
-    log(f"ceilings: MFMA bf16 {res['mfma_bf16_tflops']:.0f} TFLOP/s "
+    log(f"ceilings: MFMA bf16 {res['mfma_bf16_tflops']:.0f} TFLOP/s at "
+        f"{mfma_clk[max(mfma, key=mfma.get)][1]:.0f} MHz "
         f"({res['mfma_bf16_tflops'] / PEAK_BF16_TFLOPS:.3f} of nominal), HBM read "
         f"{res['hbm_read_gbs']:.0f} GB/s ({res['hbm_read_gbs'] / PEAK_HBM_GBS:.3f} of nominal), HBM write "
         f"{res['hbm_write_gbs']:.0f} GB/s ({res['hbm_write_gbs'] / PEAK_HBM_GBS:.3f} of nominal)")

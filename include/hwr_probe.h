@@ -23,7 +23,8 @@
  * device, wait, and return the median rate over the timed launches (each
  * launch timed on the device from its own start to its own end).  The MFMA
  * and read probes allocate small device buffers of their own (the products'
- * results, one word for the read) and free them before returning.  Not part
+ * results and clock readings, one word for the read) and free them before
+ * returning.  Not part
  * of routing: nothing in hwr.h calls them.
  */
 #ifndef HWR_PROBE_H
@@ -41,11 +42,13 @@ extern "C" {
  * product).  waves_per_simd (1..2): waves resident on each SIMD of every
  * compute unit; iters (>= 1): loop trips of eight products per wave and
  * launch; reps (1..64): timed launches after one untimed one.  *tflops is
- * the median over the timed launches.  Errors: HWR_ERR_INVALID_ARG for a
- * NULL tflops or an argument out of range (no device touched), HWR_ERR_HIP,
- * HWR_ERR_OOM. */
+ * the median over the timed launches.  clock_mhz (may be NULL): the median
+ * over the timed launches of the shader clock the product loops ran at
+ * (shader-cycle counter over the 100 MHz reference counter, summed over the
+ * workgroups).  Errors: HWR_ERR_INVALID_ARG for a NULL tflops or an argument
+ * out of range (no device touched), HWR_ERR_HIP, HWR_ERR_OOM. */
 hwr_status hwr_probe_mfma_bf16(int32_t device, int32_t waves_per_simd, int32_t iters, int32_t reps,
-                               double *tflops);
+                               double *tflops, double *clock_mhz);
 
 /* Streaming read rate in GB/s (1e9 bytes per second) of `bytes` bytes at
  * `buf`, device memory of `device` owned by the caller and only read.  buf

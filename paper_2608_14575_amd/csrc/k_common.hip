@@ -282,7 +282,7 @@ template <bool PN, bool MULTI, bool GEN, bool DBG>
 __global__ __launch_bounds__(kEpiThreads) void k_epilogue(EpilogueArgs a) {
     Rule rule = a.rule;
     if constexpr (!GEN) rule = Rule{};
-    // [pair_stride(N)] models | [M][kEpiQS] quality | [kEpiW][kEpiQB] keys
+    // [pair_stride(N)] models | [M][kEpiQS] quality | [kEpiW][kEpiQL][64 lanes] keys
     extern __shared__ __attribute__((aligned(16))) float s_ep[];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     int32_t *s_model = reinterpret_cast<int32_t *>(s_ep);
@@ -357,7 +357,7 @@ __global__ __launch_bounds__(kEpiThreads) void k_epilogue(EpilogueArgs a) {
 #pragma unroll
         for (int j = 0; j < kEpiQL; ++j) {
             key[j] = best_key(best[j]);
-            s_key[wave * kEpiQB + ql + j] = key[j];
+            s_key[(wave * kEpiQL + j) * 64 + lane] = key[j];   // lane-contiguous: no bank conflicts
         }
         __syncthreads();
 #pragma unroll
@@ -365,7 +365,7 @@ __global__ __launch_bounds__(kEpiThreads) void k_epilogue(EpilogueArgs a) {
             uint64_t top = 0;
 #pragma unroll
             for (int v = 0; v < kEpiW; ++v) {
-                const uint64_t o = s_key[v * kEpiQB + ql + j];
+                const uint64_t o = s_key[(v * kEpiQL + j) * 64 + lane];
                 top = o > top ? o : top;
             }
             if (valid[j] && key[j] == top)

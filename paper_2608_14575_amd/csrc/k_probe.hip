@@ -6,6 +6,7 @@
 
 #include <algorithm>
 #include <cstdint>
+#include <vector>
 
 #include "hwr_probe.h"
 
@@ -25,7 +26,10 @@ __device__ inline __bf16 probe_value(uint32_t &s) {
     return static_cast<__bf16>(f);
 }
 
-__global__ __launch_bounds__(kProbeThreads) void k_probe_mfma(int iters, float *out) {
+// clk (per workgroup): shader-clock cycles and 100 MHz reference ticks
+// between the start and the end of its product loop, as seen by its first
+// wave (counter reads; written with an ordinary vector store).
+__global__ __launch_bounds__(kProbeThreads) void k_probe_mfma(int iters, float *out, uint64_t *clk) {
     uint32_t s = (blockIdx.x * kProbeThreads + threadIdx.x) * 0x9E3779B9u + 0x7F4A7C15u;
     pbf16x8 a[kFrags], b[kFrags];
 #pragma unroll
@@ -38,6 +42,7 @@ __global__ __launch_bounds__(kProbeThreads) void k_probe_mfma(int iters, float *
     pf32x16 c[kChains];
 #pragma unroll
     for (int k = 0; k < kChains; ++k) c[k] = pf32x16{};
+    const uint64_t t0 = __builtin_amdgcn_s_memtime(), r0 = __builtin_amdgcn_s_memrealtime();
     for (int it = 0; it < iters; ++it) {
         // consecutive products take different operands
 #pragma unroll
@@ -50,6 +55,11 @@ __global__ __launch_bounds__(kProbeThreads) void k_probe_mfma(int iters, float *
 #pragma unroll
     for (int k = 0; k < kChains; ++k) sum += c[k][0] + c[k][15];
     out[blockIdx.x * kProbeThreads + threadIdx.x] = sum;
+    const uint64_t t1 = __builtin_amdgcn_s_memtime(), r1 = __builtin_amdgcn_s_memrealtime();
+    if (threadIdx.x == 0) {
+        clk[2 * blockIdx.x] = t1 - t0;
+        clk[2 * blockIdx.x + 1] = r1 - r0;
+    }
 }
 
 typedef uint32_t pu32x4 __attribute__((ext_vector_type(4)));
@@ -131,7 +141,7 @@ hipError_t median_ms(Launch launch, int reps, float *ms) {
 }  // namespace
 
 extern "C" hwr_status hwr_probe_mfma_bf16(int32_t device, int32_t waves_per_simd, int32_t iters, int32_t reps,
-                                          double *tflops) {
+                                          double *tflops, double *clock_mhz) {
     if (!tflops || device < 0 || waves_per_simd < 1 || waves_per_simd > 2 || iters < 1 || reps < 1 || reps > 64)
         return HWR_ERR_INVALID_ARG;
     DeviceScope scope(device);
@@ -141,18 +151,45 @@ extern "C" hwr_status hwr_probe_mfma_bf16(int32_t device, int32_t waves_per_simd
     if (e != hipSuccess) return status_of(e);
     const int blocks = prop.multiProcessorCount * waves_per_simd;
     float *out = nullptr;
+    uint64_t *clk = nullptr;                   // [reps + 1 launches][blocks][2]
+    const size_t nclk = static_cast<size_t>(reps + 1) * blocks * 2;
     e = hipMalloc(&out, static_cast<size_t>(blocks) * kProbeThreads * sizeof(float));
-    if (e != hipSuccess) return status_of(e);
+    if (e == hipSuccess) e = hipMalloc(&clk, nclk * sizeof(uint64_t));
     float ms = 0.0f;
-    e = median_ms(
-        [&](hipStream_t s, hipEvent_t a, hipEvent_t b) {
-            hipExtLaunchKernelGGL(k_probe_mfma, dim3(blocks), dim3(kProbeThreads), 0, s, a, b, 0u, iters, out);
-            return hipGetLastError();
-        },
-        reps, &ms);
+    int launch = 0;
+    if (e == hipSuccess)
+        e = median_ms(
+            [&](hipStream_t s, hipEvent_t a, hipEvent_t b) {
+                uint64_t *lc = clk + static_cast<size_t>(launch++) * blocks * 2;
+                hipExtLaunchKernelGGL(k_probe_mfma, dim3(blocks), dim3(kProbeThreads), 0, s, a, b, 0u, iters, out,
+                                      lc);
+                return hipGetLastError();
+            },
+            reps, &ms);
+    std::vector<uint64_t> h;
+    if (e == hipSuccess && clock_mhz) {
+        h.resize(nclk);
+        e = hipMemcpy(h.data(), clk, nclk * sizeof(uint64_t), hipMemcpyDeviceToHost);
+    }
     (void)hipFree(out);
+    (void)hipFree(clk);
     if (e != hipSuccess) return status_of(e);
     if (!(ms > 0.0f)) return HWR_ERR_HIP;
+    if (clock_mhz) {
+        // per timed launch: all workgroups' cycles over all their reference
+        // ticks; the median over the launches
+        std::vector<double> mhz;
+        for (int l = 1; l <= reps; ++l) {
+            double cyc = 0.0, ref = 0.0;
+            for (int b = 0; b < blocks; ++b) {
+                cyc += static_cast<double>(h[(static_cast<size_t>(l) * blocks + b) * 2]);
+                ref += static_cast<double>(h[(static_cast<size_t>(l) * blocks + b) * 2 + 1]);
+            }
+            mhz.push_back(ref > 0.0 ? cyc / ref * 100.0 : 0.0);
+        }
+        std::sort(mhz.begin(), mhz.end());
+        *clock_mhz = reps % 2 ? mhz[reps / 2] : 0.5 * (mhz[reps / 2 - 1] + mhz[reps / 2]);
+    }
     const double flops = 2.0 * 32 * 32 * 16 * kChains * static_cast<double>(iters) * blocks * (kProbeThreads / 64);
     *tflops = flops / (ms * 1e-3) / 1e12;
     return HWR_OK;

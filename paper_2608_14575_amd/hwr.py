@@ -166,7 +166,8 @@ def load(path: Optional[str] = None) -> C.CDLL:
     L.hwr_sim_last_error.restype = C.c_char_p
     L.hwr_sim_last_error.argtypes = []
     L.hwr_probe_mfma_bf16.restype = C.c_int
-    L.hwr_probe_mfma_bf16.argtypes = [C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.POINTER(C.c_double)]
+    L.hwr_probe_mfma_bf16.argtypes = [C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.POINTER(C.c_double),
+                                      C.POINTER(C.c_double)]
     L.hwr_probe_hbm_read.restype = C.c_int
     L.hwr_probe_hbm_read.argtypes = [C.c_int32, _vp, C.c_uint64, C.c_int32, C.c_int32, C.POINTER(C.c_double)]
     L.hwr_probe_hbm_write.restype = C.c_int
@@ -203,11 +204,12 @@ def hwr_route_batch_static(ctx, batch: hwr_query_batch, result: hwr_route_result
     _check(load().hwr_route_batch_static(ctx, C.byref(batch), C.byref(result)), ctx)
 
 
-def hwr_probe_mfma_bf16(device: int, waves_per_simd: int, iters: int, reps: int) -> float:
-    """Register-fed bf16 MFMA rate of the device in TFLOP/s (median launch)."""
-    out = C.c_double()
-    _check(load().hwr_probe_mfma_bf16(device, waves_per_simd, iters, reps, C.byref(out)), None)
-    return out.value
+def hwr_probe_mfma_bf16(device: int, waves_per_simd: int, iters: int, reps: int) -> tuple:
+    """Register-fed bf16 MFMA rate of the device in TFLOP/s and the shader
+    clock in MHz it ran at (medians over the timed launches)."""
+    out, mhz = C.c_double(), C.c_double()
+    _check(load().hwr_probe_mfma_bf16(device, waves_per_simd, iters, reps, C.byref(out), C.byref(mhz)), None)
+    return out.value, mhz.value
 
 
 def hwr_probe_hbm_read(device: int, buf_ptr: int, nbytes: int, waves_per_simd: int, reps: int) -> float:

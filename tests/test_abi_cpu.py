@@ -171,9 +171,10 @@ def test_null_arguments(lib):
 def test_probe_argument_errors(lib):
     """The ceiling probes reject bad arguments before touching a device."""
     out = C.c_double(-1.0)
-    bad_mfma = [(0, 1, 16, 3, None), (-1, 1, 16, 3, C.byref(out)), (0, 0, 16, 3, C.byref(out)),
-                (0, 3, 16, 3, C.byref(out)), (0, 1, 0, 3, C.byref(out)), (0, 1, 16, 0, C.byref(out)),
-                (0, 1, 16, 65, C.byref(out))]
+    bad_mfma = [(0, 1, 16, 3, None, None), (-1, 1, 16, 3, C.byref(out), None),
+                (0, 0, 16, 3, C.byref(out), None), (0, 3, 16, 3, C.byref(out), None),
+                (0, 1, 0, 3, C.byref(out), None), (0, 1, 16, 0, C.byref(out), None),
+                (0, 1, 16, 65, C.byref(out), None)]
     for args in bad_mfma:
         assert lib.hwr_probe_mfma_bf16(*args) == hwr.HWR_ERR_INVALID_ARG, args
     buf = 1 << 20    # never dereferenced: every call below fails its checks first

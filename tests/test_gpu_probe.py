@@ -11,9 +11,13 @@ pytestmark = pytest.mark.gpu
 def test_mfma_ceiling_is_below_the_published_peak():
     hwr.load()
     for w in (1, 2):
-        t = hwr.hwr_probe_mfma_bf16(0, w, 1024, 3)
-        print(f"[probe] mfma bf16, {w} wave(s) per SIMD: {t:.0f} TFLOP/s", flush=True)
+        t, mhz = hwr.hwr_probe_mfma_bf16(0, w, 1024, 3)
+        print(f"[probe] mfma bf16, {w} wave(s) per SIMD: {t:.0f} TFLOP/s at {mhz:.0f} MHz", flush=True)
         assert 500.0 < t <= 2500.0
+        # within the part's clock range; and at most what the clock allows
+        # (1024 SIMDs, 32768 flops per 32-cycle product)
+        assert 500.0 < mhz <= 2500.0
+        assert t <= 1024 * 1024 * mhz * 1e6 / 1e12 * 1.02
 
 
 def test_hbm_ceilings_are_below_the_published_peak():
