@@ -246,9 +246,10 @@ __global__ __launch_bounds__(MlpShape<NT>::kThreads, 1) void k_mlp_bf16(MlpArgs 
     const int tid = threadIdx.x;
     {
         // Every load of a staging round is issued before its first LDS
-        // store: one memory round trip per round of up to kStageRound pieces
-        // per thread (one round for 512 threads, two for 256).  Indices past
-        // an array's end are clamped for the loads and skipped for the stores.
+        // store: one memory round trip for W1, the biases and the head
+        // fragments, then one per round of up to kStageRound W2 pieces per
+        // thread (one round for 512 threads, two for 256).  Indices past an
+        // array's end are clamped for the loads and skipped for the stores.
         constexpr int nW1 = MT * 2 * 64, nW2 = MT * KB2 * 64, nB = MT * 2 * 4, nW3 = KB2 * W3S;
         constexpr int pW1 = (nW1 + kThreads - 1) / kThreads;
         constexpr int pW2 = (nW2 + kThreads - 1) / kThreads;
@@ -263,6 +264,9 @@ __global__ __launch_bounds__(MlpShape<NT>::kThreads, 1) void k_mlp_bf16(MlpArgs 
         const uint4 *gb2 = reinterpret_cast<const uint4 *>(a.b2_pk);
         const uint4 *g3 = reinterpret_cast<const uint4 *>(a.w3_frag);
         uint4 v1[pW1], v2[rW2], vb1[pB], vb2[pB], v3[pW3];
+        // W1, the biases and the head fragments first (one round trip), so
+        // that nothing is held across the W2 rounds: otherwise the compiler
+        // keeps W1 in scratch memory meanwhile
 #pragma unroll
         for (int i = 0; i < pW1; ++i) {
             const int k = tid + i * kThreads;
@@ -278,19 +282,6 @@ __global__ __launch_bounds__(MlpShape<NT>::kThreads, 1) void k_mlp_bf16(MlpArgs 
         for (int i = 0; i < pW3; ++i) {
             const int k = tid + i * kThreads;
             v3[i] = g3[k < nW3 ? k : 0];
-        }
-#pragma unroll
-        for (int r = 0; r < pW2 / rW2; ++r) {
-#pragma unroll
-            for (int i = 0; i < rW2; ++i) {
-                const int k = tid + (r * rW2 + i) * kThreads;
-                v2[i] = g2[k < nW2 ? k : 0];
-            }
-#pragma unroll
-            for (int i = 0; i < rW2; ++i) {
-                const int k = tid + (r * rW2 + i) * kThreads;
-                if (k < nW2) reinterpret_cast<uint4 *>(s_w2)[k] = v2[i];
-            }
         }
 #pragma unroll
         for (int i = 0; i < pW1; ++i) {
@@ -309,6 +300,19 @@ __global__ __launch_bounds__(MlpShape<NT>::kThreads, 1) void k_mlp_bf16(MlpArgs 
         for (int i = 0; i < pW3; ++i) {
             const int k = tid + i * kThreads;
             if (k < nW3) reinterpret_cast<uint4 *>(s_w3f)[k] = v3[i];
+        }
+#pragma unroll
+        for (int r = 0; r < pW2 / rW2; ++r) {
+#pragma unroll
+            for (int i = 0; i < rW2; ++i) {
+                const int k = tid + (r * rW2 + i) * kThreads;
+                v2[i] = g2[k < nW2 ? k : 0];
+            }
+#pragma unroll
+            for (int i = 0; i < rW2; ++i) {
+                const int k = tid + (r * rW2 + i) * kThreads;
+                if (k < nW2) reinterpret_cast<uint4 *>(s_w2)[k] = v2[i];
+            }
         }
     }
     __syncthreads();
