@@ -596,6 +596,15 @@ def main() -> int:
     single = None if args.no_single else single_query(args, S, hwr, torch)
     single_graph = None if args.no_single else single_query(args, S, hwr, torch, hwr.HWR_FLAG_GRAPH)
     single_res = None if args.no_single else single_query(args, S, hwr, torch, hwr.HWR_FLAG_RESIDENT)
+    floor = None
+    if not args.no_single:
+        # what a launch answered through pinned host memory costs with no work
+        # in it: the floor under the plain and the graph-launched single query
+        fp, fg = hwr.hwr_probe_launch_floor(0, False, 2000), hwr.hwr_probe_launch_floor(0, True, 2000)
+        floor = {"plain_launch": {"p50_us": fp[0], "p99_us": fp[1]},
+                 "graph_launch": {"p50_us": fg[0], "p99_us": fg[1]},
+                 "probe": "hwr_probe_launch_floor: one wave echoes a pinned request number, 2000 calls"}
+        log(f"launch floor: plain p50 {fp[0]:.1f} us, graph p50 {fg[0]:.1f} us")
     if single:
         log(f"single query (kernel launch) p50 {single['p50_us']:.1f} us p99 {single['p99_us']:.1f} us; "
             f"(graph launch) p50 {single_graph['p50_us']:.1f} us p99 {single_graph['p99_us']:.1f} us; "
@@ -611,7 +620,7 @@ def main() -> int:
         "data": "synthetic (seeded; stands in for the paper's embedded prompt sets)",
         "config": res["config"], "roofline": res["roofline"], "cpu_baseline": cpu,
         "single_query": single, "single_query_graph_launch": single_graph,
-        "single_query_resident": single_res,
+        "single_query_resident": single_res, "single_query_launch_floor": floor,
         "step_ms": res["step_ms"], "quality_roofline": res["quality_roofline"], "stages": res["stages"],
         "staged_pipeline": staged, "ceilings": ceilings, "batch_latency": batch, "closed_loop": sim, "closed_loop_pareto": pareto,
     }

@@ -4,7 +4,8 @@
  * The routing kernels are quoted against two kinds of peak: the part's
  * published one (dense bf16 MFMA 2.5 PFLOP/s, HBM3E 8 TB/s) and the one a
  * plain kernel actually reaches on the same device, in the same thermal and
- * power state.  These three entry points measure the second kind:
+ * power state.  The first three entry points below measure the second kind;
+ * the fourth measures a latency floor:
  *
  *  - hwr_probe_mfma_bf16: bf16 matrix products (32x32x16, fp32 accumulate) fed
  *    from registers only -- no memory traffic, eight independent accumulators
@@ -18,10 +19,13 @@
  *  - hwr_probe_hbm_write: the same for 16-byte stores of every lane into a
  *    caller buffer (its contents are overwritten).  It bounds a
  *    write-dominated kernel.
+ *  - hwr_probe_launch_floor: the host-clock time of a launch of one wave
+ *    that only answers through pinned host memory, plain or graph-launched:
+ *    the floor under a single-query route.
  *
  * All are synchronous: they launch on a stream of their own on the given
- * device, wait, and return the median rate over the timed launches (each
- * launch timed on the device from its own start to its own end).  The MFMA
+ * device, wait, and return the median over the timed launches (the rates
+ * timed on the device from each launch's own start to its own end).  The MFMA
  * and read probes allocate small device buffers of their own (the products'
  * results and clock readings, one word for the read) and free them before
  * returning.  Not part
@@ -58,6 +62,19 @@ hwr_status hwr_probe_mfma_bf16(int32_t device, int32_t waves_per_simd, int32_t i
  * size or count out of range; no device touched), HWR_ERR_HIP, HWR_ERR_OOM. */
 hwr_status hwr_probe_hbm_read(int32_t device, const void *buf, uint64_t bytes, int32_t waves_per_simd,
                               int32_t reps, double *gbps);
+
+/* Launch floor in microseconds, host clock: the host writes a request number
+ * into a pinned host record, launches one wave (use_graph 0: a plain kernel
+ * launch; 1: a graph holding that launch, captured once), and spins until the
+ * wave has copied the number into a pinned answer record with a system-scope
+ * store.  The single-query route does the same around its work, so this is
+ * the part of its latency no kernel can remove.  calls (1..100000) timed calls
+ * after 8 untimed ones; *p50_us and *p99_us are their median and 99th
+ * percentile.  Errors: HWR_ERR_INVALID_ARG (NULL output, use_graph not 0 or 1,
+ * calls out of range; no device touched), HWR_ERR_HIP (including no answer
+ * within 10 s), HWR_ERR_OOM. */
+hwr_status hwr_probe_launch_floor(int32_t device, int32_t use_graph, int32_t calls, double *p50_us,
+                                  double *p99_us);
 
 /* Streaming write rate in GB/s of `bytes` bytes at `buf`, device memory of
  * `device` owned by the caller, whose contents the probe overwrites.

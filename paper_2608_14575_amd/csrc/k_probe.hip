@@ -1,10 +1,12 @@
 // Ceiling probes of the device (gfx950): register-fed bf16 MFMA, a streaming
-// HBM read and a streaming HBM write.  They give the achievable peaks next to the published
+// HBM read and a streaming HBM write, and the floor of a launch answered
+// through pinned host memory.  They give the achievable peaks next to the published
 // ones; nothing on the routing path calls them.
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <chrono>
 #include <cstdint>
 #include <vector>
 
@@ -95,6 +97,16 @@ __global__ __launch_bounds__(kProbeThreads) void k_probe_write(pu32x4 *__restric
     uint64_t i = static_cast<uint64_t>(blockIdx.x) * kProbeThreads + threadIdx.x;
     const pu32x4 v = {static_cast<uint32_t>(i), 1u, 2u, 3u};
     for (; i < n; i += stride) p[i] = v;
+}
+
+// Launch floor: one wave copies the request number from a pinned host
+// record to the answer record (system scope, the answer written last), as the
+// single-query kernel does around its work.
+__global__ __launch_bounds__(64) void k_probe_echo(const uint32_t *in, uint32_t *out) {
+    if (threadIdx.x == 0) {
+        const uint32_t v = __hip_atomic_load(in, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        __hip_atomic_store(out, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+    }
 }
 
 hwr_status status_of(hipError_t e) {
@@ -250,5 +262,82 @@ extern "C" hwr_status hwr_probe_hbm_write(int32_t device, void *buf, uint64_t by
     if (e != hipSuccess) return status_of(e);
     if (!(ms > 0.0f)) return HWR_ERR_HIP;
     *gbps = static_cast<double>(bytes) / (ms * 1e-3) / 1e9;
+    return HWR_OK;
+}
+
+extern "C" hwr_status hwr_probe_launch_floor(int32_t device, int32_t use_graph, int32_t calls, double *p50_us,
+                                             double *p99_us) {
+    if (!p50_us || !p99_us || device < 0 || (use_graph != 0 && use_graph != 1) || calls < 1 || calls > 100000)
+        return HWR_ERR_INVALID_ARG;
+    DeviceScope scope(device);
+    if (scope.err != hipSuccess) return status_of(scope.err);
+    uint32_t *h = nullptr, *d = nullptr;         // [0]: request, [16]: answer (separate lines)
+    hipStream_t s = nullptr;
+    hipGraph_t g = nullptr;
+    hipGraphExec_t ge = nullptr;
+    hipError_t e = hipHostMalloc(reinterpret_cast<void **>(&h), 256, hipHostMallocMapped | hipHostMallocCoherent);
+    if (e == hipSuccess) {
+        h[0] = 0;
+        h[16] = 0;
+        e = hipHostGetDevicePointer(reinterpret_cast<void **>(&d), h, 0);
+    }
+    if (e == hipSuccess) e = hipStreamCreateWithFlags(&s, hipStreamNonBlocking);
+    auto launch = [&]() -> hipError_t {
+        if (ge) return hipGraphLaunch(ge, s);
+        hipLaunchKernelGGL(k_probe_echo, dim3(1), dim3(64), 0, s, d, d + 16);
+        return hipGetLastError();
+    };
+    if (e == hipSuccess && use_graph) {
+        hipStream_t cs = nullptr;
+        e = hipStreamCreateWithFlags(&cs, hipStreamNonBlocking);
+        if (e == hipSuccess) {
+            e = hipStreamBeginCapture(cs, hipStreamCaptureModeThreadLocal);
+            if (e == hipSuccess) {
+                hipLaunchKernelGGL(k_probe_echo, dim3(1), dim3(64), 0, cs, d, d + 16);
+                e = hipGetLastError();
+                const hipError_t e2 = hipStreamEndCapture(cs, &g);
+                if (e == hipSuccess) e = e2;
+            }
+            (void)hipStreamDestroy(cs);
+        }
+        if (e == hipSuccess) e = hipGraphInstantiate(&ge, g, nullptr, nullptr, 0);
+    }
+    // a few untimed calls, then `calls` timed ones: request number written,
+    // launch, spin until the answer carries it
+    std::vector<double> us;
+    bool late = false;
+    for (int i = 0; e == hipSuccess && i < calls + 8; ++i) {
+        const uint32_t seq = static_cast<uint32_t>(i + 1);
+        const auto t0 = std::chrono::steady_clock::now();
+        __atomic_store_n(&h[0], seq, __ATOMIC_RELEASE);
+        e = launch();
+        uint64_t spins = 0;
+        while (e == hipSuccess && __atomic_load_n(&h[16], __ATOMIC_ACQUIRE) != seq) {
+            if ((++spins & 0xFFFF) == 0) {
+                const hipError_t qe = hipStreamQuery(s);
+                if (qe != hipSuccess && qe != hipErrorNotReady) e = qe;
+                if (std::chrono::steady_clock::now() - t0 > std::chrono::seconds(10)) {
+                    late = true;
+                    break;
+                }
+            }
+        }
+        if (late) break;
+        const auto t1 = std::chrono::steady_clock::now();
+        if (i >= 8) us.push_back(std::chrono::duration<double, std::micro>(t1 - t0).count());
+    }
+    if (s) {
+        const hipError_t se = hipStreamSynchronize(s);
+        if (e == hipSuccess) e = se;
+        (void)hipStreamDestroy(s);
+    }
+    if (ge) (void)hipGraphExecDestroy(ge);
+    if (g) (void)hipGraphDestroy(g);
+    if (h) (void)hipHostFree(h);
+    if (e != hipSuccess) return status_of(e);
+    if (late || us.empty()) return HWR_ERR_HIP;
+    std::sort(us.begin(), us.end());
+    *p50_us = us[us.size() / 2];
+    *p99_us = us[std::min(us.size() - 1, static_cast<size_t>(0.99 * us.size()))];
     return HWR_OK;
 }

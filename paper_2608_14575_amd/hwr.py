@@ -32,7 +32,7 @@ KERNEL_NAMES = ["state", "quality", "gather", "mlp", "epilogue", "fused", "merge
 EXPORTS = ["hwr_init", "hwr_update_hw_state", "hwr_route_batch", "hwr_route_batch_static", "hwr_free",
            "hwr_last_error",
            "hwr_profile_enable", "hwr_profile_read", "hwr_sim_run", "hwr_sim_last_error",
-           "hwr_probe_mfma_bf16", "hwr_probe_hbm_read", "hwr_probe_hbm_write"]
+           "hwr_probe_mfma_bf16", "hwr_probe_hbm_read", "hwr_probe_hbm_write", "hwr_probe_launch_floor"]
 
 _STATUS = {0: "HWR_OK", -1: "HWR_ERR_INVALID_ARG", -2: "HWR_ERR_OOM", -3: "HWR_ERR_HIP",
            -4: "HWR_ERR_STATE", -5: "HWR_ERR_UNSUPPORTED"}
@@ -170,6 +170,9 @@ def load(path: Optional[str] = None) -> C.CDLL:
                                       C.POINTER(C.c_double)]
     L.hwr_probe_hbm_read.restype = C.c_int
     L.hwr_probe_hbm_read.argtypes = [C.c_int32, _vp, C.c_uint64, C.c_int32, C.c_int32, C.POINTER(C.c_double)]
+    L.hwr_probe_launch_floor.restype = C.c_int
+    L.hwr_probe_launch_floor.argtypes = [C.c_int32, C.c_int32, C.c_int32, C.POINTER(C.c_double),
+                                         C.POINTER(C.c_double)]
     L.hwr_probe_hbm_write.restype = C.c_int
     L.hwr_probe_hbm_write.argtypes = [C.c_int32, _vp, C.c_uint64, C.c_int32, C.c_int32, C.POINTER(C.c_double)]
     if path is None:
@@ -225,6 +228,14 @@ def hwr_probe_hbm_write(device: int, buf_ptr: int, nbytes: int, waves_per_simd: 
     out = C.c_double()
     _check(load().hwr_probe_hbm_write(device, buf_ptr, nbytes, waves_per_simd, reps, C.byref(out)), None)
     return out.value
+
+
+def hwr_probe_launch_floor(device: int, use_graph: bool, calls: int) -> tuple:
+    """Host-clock p50 and p99 in µs of a launch of one wave answered through
+    pinned host memory (plain or graph launch)."""
+    p50, p99 = C.c_double(), C.c_double()
+    _check(load().hwr_probe_launch_floor(device, int(use_graph), calls, C.byref(p50), C.byref(p99)), None)
+    return p50.value, p99.value
 
 
 def hwr_free(ctx) -> None:

@@ -186,7 +186,12 @@ def test_probe_argument_errors(lib):
     for args in bad_read:
         assert lib.hwr_probe_hbm_read(*args) == hwr.HWR_ERR_INVALID_ARG, args
         assert lib.hwr_probe_hbm_write(*args) == hwr.HWR_ERR_INVALID_ARG, args
-    assert out.value == -1.0
+    p99 = C.c_double(-1.0)
+    for args in [(0, 0, 10, None, C.byref(p99)), (0, 0, 10, C.byref(out), None), (-1, 0, 10, C.byref(out), C.byref(p99)),
+                 (0, 2, 10, C.byref(out), C.byref(p99)), (0, 0, 0, C.byref(out), C.byref(p99)),
+                 (0, 1, 100001, C.byref(out), C.byref(p99))]:
+        assert lib.hwr_probe_launch_floor(*args) == hwr.HWR_ERR_INVALID_ARG, args
+    assert out.value == -1.0 and p99.value == -1.0
 
 
 def test_no_device_is_a_clean_error(lib):

@@ -49,3 +49,12 @@ def test_hbm_ceilings_are_below_the_published_peak():
     hwr.hwr_probe_hbm_write(0, big.data_ptr(), nbytes, 2, 1)
     assert bool((big[nbytes // 4:] == 0).all())
     assert bool((big[:nbytes // 4] != 0).any())
+
+
+def test_launch_floor_plain_and_graph():
+    hwr.load()
+    for graph in (False, True):
+        p50, p99 = hwr.hwr_probe_launch_floor(0, graph, 500)
+        print(f"[probe] launch floor ({'graph' if graph else 'plain'} launch): p50 {p50:.1f} us, p99 {p99:.1f} us",
+              flush=True)
+        assert 0.5 < p50 <= p99 < 10_000.0
