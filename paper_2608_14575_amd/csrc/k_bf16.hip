@@ -131,9 +131,10 @@ __global__ __launch_bounds__(256) void k_quality_bf16_lds(QualityArgs a) {
         for (int i = 0; i < PT; ++i) {
             const int p = tid + 256 * i, row = p / PPR, col = p % PPR;
             const int q = r0 + row < a.nq ? r0 + row : a.nq - 1;
-            // read once: streamed past the caches
-            pre[i] = __builtin_nontemporal_load(
-                reinterpret_cast<const u32x4 *>(emb + static_cast<size_t>(q) * a.D + j * kQSlab + col * 8));
+            // plain loads: a chunk that is still in the last-level cache
+            // (embeddings written just before routing) is read from there;
+            // non-temporal loads would bypass it
+            pre[i] = *reinterpret_cast<const u32x4 *>(emb + static_cast<size_t>(q) * a.D + j * kQSlab + col * 8);
         }
     };
     const int row = lane & 31, h = lane >> 5;
