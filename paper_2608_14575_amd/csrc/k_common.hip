@@ -261,19 +261,22 @@ hipError_t launch_gather(const GatherArgs &a, hipStream_t s) {
 // Eq. 3 argmax -- once per cost weight (a lambda sweep; outputs are then
 // [query][weight]).  Predictions are pair-major with 16-byte aligned pair
 // rows: a workgroup takes kEpiQB consecutive queries, lane i of every wave
-// the four queries 4i .. 4i + 3 of them (one 16-byte load per pair and
-// array, so each load of a wave reads 1 KB of one pair's row), and wave w
-// the pairs w, w + 4, ... in increasing order.  The quality rows of the
-// workgroup's queries are staged in LDS transposed ([model][query]), so the
-// lane's four values of one model are one 16-byte read; the pairs' models
-// are staged too.  Each lane keeps the best candidate of each of its
-// queries; the four waves then compare packed decision keys through LDS
-// (unique: they hold the pair index), and the wave holding the largest
-// writes the outputs.  DBG also writes the caller's per-candidate outputs,
-// [query][pair].
-constexpr int kEpiQL = 4;                  // queries per lane
+// the kEpiQL queries kEpiQL i .. kEpiQL i + kEpiQL - 1 of them (one load
+// per pair and array, so each load of a wave reads 64 kEpiQL consecutive
+// values of one pair's row), and wave w the pairs w, w + kEpiW, ... in
+// increasing order.  The quality rows of the workgroup's queries are staged
+// in LDS transposed ([model][query]), so the lane's values of one model are
+// one LDS read; the pairs' models are staged too.  Each lane keeps the best
+// candidate of each of its queries; the waves then compare packed decision
+// keys through LDS (unique: they hold the pair index), and the wave holding
+// the largest writes the outputs.  DBG also writes the caller's
+// per-candidate outputs, [query][pair].  Shape measured at 65,536 x 256
+// (same box): two queries per lane and eight waves 31.6 us; four and
+// sixteen 35.2 us; four and four 58.8 us.
+constexpr int kEpiQL = 2;                  // queries per lane
+typedef f32x2 EpiVec;                      // a lane's values of one pair: kEpiQL floats
 constexpr int kEpiQB = 64 * kEpiQL;        // queries per workgroup
-constexpr int kEpiW = 16;                  // waves per workgroup: pair classes mod kEpiW
+constexpr int kEpiW = 8;                   // waves per workgroup: pair classes mod kEpiW
 constexpr int kEpiThreads = 64 * kEpiW;
 constexpr int kEpiQS = kEpiQB + 4;         // LDS quality row stride (16-byte multiple, offset banks)
 constexpr int kEpiUnroll = 2;              // pairs per wave loaded before any is used
@@ -323,20 +326,20 @@ __global__ __launch_bounds__(kEpiThreads) void k_epilogue(EpilogueArgs a) {
             best[j] = best_none();
         }
         for (int d0 = wave; d0 < a.N; d0 += kEpiW * kEpiUnroll) {
-            f32x4 tv[kEpiUnroll], pv[kEpiUnroll], nv[kEpiUnroll];
+            EpiVec tv[kEpiUnroll], pv[kEpiUnroll], nv[kEpiUnroll];
 #pragma unroll
             for (int u = 0; u < kEpiUnroll; ++u) {
                 const int d = d0 + kEpiW * u;
                 const size_t ci = static_cast<size_t>(d < a.N ? d : 0) * ld + col;
-                tv[u] = *reinterpret_cast<const f32x4 *>(a.cand_ttft + ci);
-                pv[u] = *reinterpret_cast<const f32x4 *>(a.cand_tpot + ci);
-                if constexpr (PN) nv[u] = *reinterpret_cast<const f32x4 *>(a.cand_nout + ci);
+                tv[u] = *reinterpret_cast<const EpiVec *>(a.cand_ttft + ci);
+                pv[u] = *reinterpret_cast<const EpiVec *>(a.cand_tpot + ci);
+                if constexpr (PN) nv[u] = *reinterpret_cast<const EpiVec *>(a.cand_nout + ci);
             }
 #pragma unroll
             for (int u = 0; u < kEpiUnroll; ++u) {
                 const int d = d0 + kEpiW * u;
                 if (d < a.N) {
-                    const f32x4 qv = *reinterpret_cast<const f32x4 *>(s_qt + s_model[d] * kEpiQS + ql);
+                    const EpiVec qv = *reinterpret_cast<const EpiVec *>(s_qt + s_model[d] * kEpiQS + ql);
                     // every query of the lane is decided (a query past the
                     // chunk's end only reads padding, and is never written)
 #pragma unroll
