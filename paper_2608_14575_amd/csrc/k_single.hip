@@ -86,6 +86,7 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
     __shared__ float s_bq[kMaxModels];
     __shared__ float s_q[kMaxModels];
     __shared__ float s_z[4][32][kMaxHeads];
+    __shared__ bf16x8 s_h1[KB2][64];          // first-layer activations of the tile's 32 pairs
     __shared__ uint32_t s_ctl[2];             // resident: request found, its sequence number
     const int NH = a.nheads;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, n = lane & 31, h = lane >> 5;
@@ -251,22 +252,30 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
                 xf[1] = __builtin_bit_cast(bf16x8, vd ? row[2 + h] : z);
             }
             const int model = s_model[dc];
-            // ---- layer 1 (every wave, all row tiles; weights from LDS)
-            bf16x8 h1[KB2];
+            // ---- layer 1: wave w computes row tiles w, w + 4, ... (weights
+            // from LDS) and shares them through LDS; every wave then takes all
+            // of them as its second layer's B operand (a lane holds the same
+            // pair and hidden-unit half in every wave)
     #pragma unroll
-            for (int mt = 0; mt < MT; ++mt) {
+            for (int i = 0; i < MO; ++i) {
+                const int mt = wave + 4 * i;
+                if (mt >= MT) break;
                 f32x16 acc;
     #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const f32x4 bt = __builtin_bit_cast(f32x4, s_bw[0][(mt * 2 + h) * 4 + i]);
+                for (int p = 0; p < 4; ++p) {
+                    const f32x4 bt = __builtin_bit_cast(f32x4, s_bw[0][(mt * 2 + h) * 4 + p]);
     #pragma unroll
-                    for (int j = 0; j < 4; ++j) acc[4 * i + j] = bt[j];
+                    for (int j = 0; j < 4; ++j) acc[4 * p + j] = bt[j];
                 }
     #pragma unroll
                 for (int kb = 0; kb < 2; ++kb) acc = mfma32s(s_w1[(mt * 2 + kb) * 64 + lane], xf[kb], acc);
-                h1[2 * mt] = relu_pack8s(acc, 0);
-                h1[2 * mt + 1] = relu_pack8s(acc, 8);
+                s_h1[2 * mt][lane] = relu_pack8s(acc, 0);
+                s_h1[2 * mt + 1][lane] = relu_pack8s(acc, 8);
             }
+            __syncthreads();
+            bf16x8 h1[KB2];
+    #pragma unroll
+            for (int kb = 0; kb < KB2; ++kb) h1[kb] = s_h1[kb][lane];
             // ---- layer 2 row tiles of this wave, folded into the heads
             float z0 = 0.0f, z1 = 0.0f, z2 = 0.0f;
     #pragma unroll
@@ -390,7 +399,8 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
                 o->ttft = best.tt;
                 o->tpot = best.tp;
                 o->nout = best.n;
-                __threadfence_system();
+                // the release store orders this thread's record writes before
+                // the sequence number, at system scope
                 __hip_atomic_store(&o->seq, seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
             }
         }
