@@ -893,13 +893,16 @@ static hipError_t launch_mlp_t(const MlpArgs &a, dim3 grid, hipStream_t s) {
     if constexpr (H == 256 && STAGED) {
         return launch_kernel(k_mlp_bf16<H, STAGED, NH, FB, 4, false>, grid, dim3(MlpShape<4>::kThreads), 0, s, a);
     }
+    const bool lean = !a.cand_ttft && !a.cand_nout && !a.rule.score_paper && !a.rule.bound_paper;
     if constexpr (H == 256 && !STAGED) {
         if (a.len_slot < 16) {          // the four-tile form patches k-block 0 only
-            const bool lean = !a.cand_ttft && !a.cand_nout && !a.rule.score_paper && !a.rule.bound_paper;
             if (lean)
                 return launch_kernel(k_mlp_bf16<H, STAGED, NH, FB, 4, true>, grid, dim3(MlpShape<4>::kThreads), 0, s, a);
             return launch_kernel(k_mlp_bf16<H, STAGED, NH, FB, 4, false>, grid, dim3(MlpShape<4>::kThreads), 0, s, a);
         }
+    }
+    if constexpr (!STAGED) {
+        if (lean) return launch_kernel(k_mlp_bf16<H, STAGED, NH, FB, 2, true>, grid, dim3(MlpShape<2>::kThreads), 0, s, a);
     }
     return launch_kernel(k_mlp_bf16<H, STAGED, NH, FB, 2>, grid, dim3(MlpShape<2>::kThreads), 0, s, a);
 }
