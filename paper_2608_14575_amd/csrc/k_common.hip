@@ -270,9 +270,12 @@ hipError_t launch_gather(const GatherArgs &a, hipStream_t s) {
 // candidate of each of its queries; the waves then compare packed decision
 // keys through LDS (unique: they hold the pair index), and the wave holding
 // the largest writes the outputs.  DBG also writes the caller's
-// per-candidate outputs, [query][pair].  Shape measured at 65,536 x 256
-// (same box): two queries per lane and eight waves 31.6 us; four and
-// sixteen 35.2 us; four and four 58.8 us.
+// per-candidate outputs, [query][pair].  The predictions are read with
+// non-temporal loads (each is read once), and the first pair step's loads
+// are issued before the LDS staging.  Shape measured at 65,536 x 256 (same
+// box): two queries per lane and eight waves 31.6 us; four and sixteen
+// 35.2 us; four and four 58.8 us; the two loading changes then took the
+// chosen shape to 29.0 us.
 constexpr int kEpiQL = 2;                  // queries per lane
 typedef f32x2 EpiVec;                      // a lane's values of one pair: kEpiQL floats
 constexpr int kEpiQB = 64 * kEpiQL;        // queries per workgroup
@@ -295,12 +298,28 @@ __global__ __launch_bounds__(kEpiThreads) void k_epilogue(EpilogueArgs a) {
     const int nq = a.q.nq;
     const int q0 = blockIdx.x * kEpiQB;
     const int nqb = min(kEpiQB, nq - q0);
+    const int ql = kEpiQL * lane;              // the lane's first query, in the workgroup
+    // lanes past the chunk's padded end read pair rows from their start
+    const size_t col = q0 + ql < a.ldq ? static_cast<size_t>(q0 + ql) : 0;
+    const size_t ld = static_cast<size_t>(a.ldq);
+    auto load_step = [&](int d0, EpiVec (&t)[kEpiUnroll], EpiVec (&p)[kEpiUnroll], EpiVec (&v)[kEpiUnroll]) {
+#pragma unroll
+        for (int u = 0; u < kEpiUnroll; ++u) {
+            const int d = d0 + kEpiW * u;
+            const size_t ci = static_cast<size_t>(d < a.N ? d : 0) * ld + col;
+            t[u] = __builtin_nontemporal_load(reinterpret_cast<const EpiVec *>(a.cand_ttft + ci));
+            p[u] = __builtin_nontemporal_load(reinterpret_cast<const EpiVec *>(a.cand_tpot + ci));
+            if constexpr (PN) v[u] = __builtin_nontemporal_load(reinterpret_cast<const EpiVec *>(a.cand_nout + ci));
+        }
+    };
+    // the first pair step's predictions are requested before the staging
+    EpiVec t0[kEpiUnroll], p0[kEpiUnroll], v0[kEpiUnroll];
+    load_step(wave, t0, p0, v0);
     for (int i = tid; i < nqb * a.M; i += kEpiThreads) {
         const int r = i / a.M, m = i - r * a.M;
         s_qt[m * kEpiQS + r] = a.qmat[static_cast<size_t>(q0) * a.M + i];
     }
     __syncthreads();
-    const int ql = kEpiQL * lane;              // the lane's first query, in the workgroup
     bool valid[kEpiQL];
     float nout[kEpiQL], slo[kEpiQL];
     int32_t len[kEpiQL];
@@ -313,9 +332,6 @@ __global__ __launch_bounds__(kEpiThreads) void k_epilogue(EpilogueArgs a) {
         slo[j] = a.q.slo ? a.q.slo[qc] : a.q.default_slo;
         len[j] = GEN ? a.q.input_len[qc] : 0;
     }
-    // lanes past the chunk's padded end read pair rows from their start
-    const size_t col = q0 + ql < a.ldq ? static_cast<size_t>(q0 + ql) : 0;
-    const size_t ld = static_cast<size_t>(a.ldq);
     const int nw = MULTI ? a.nw : 1;
     for (int kw = 0; kw < nw; ++kw) {
         QueryRule qrule[kEpiQL];
@@ -327,13 +343,15 @@ __global__ __launch_bounds__(kEpiThreads) void k_epilogue(EpilogueArgs a) {
         }
         for (int d0 = wave; d0 < a.N; d0 += kEpiW * kEpiUnroll) {
             EpiVec tv[kEpiUnroll], pv[kEpiUnroll], nv[kEpiUnroll];
+            if (d0 == wave && kw == 0) {
 #pragma unroll
-            for (int u = 0; u < kEpiUnroll; ++u) {
-                const int d = d0 + kEpiW * u;
-                const size_t ci = static_cast<size_t>(d < a.N ? d : 0) * ld + col;
-                tv[u] = *reinterpret_cast<const EpiVec *>(a.cand_ttft + ci);
-                pv[u] = *reinterpret_cast<const EpiVec *>(a.cand_tpot + ci);
-                if constexpr (PN) nv[u] = *reinterpret_cast<const EpiVec *>(a.cand_nout + ci);
+                for (int u = 0; u < kEpiUnroll; ++u) {
+                    tv[u] = t0[u];
+                    pv[u] = p0[u];
+                    if constexpr (PN) nv[u] = v0[u];
+                }
+            } else {
+                load_step(d0, tv, pv, nv);
             }
 #pragma unroll
             for (int u = 0; u < kEpiUnroll; ++u) {
