@@ -707,17 +707,29 @@ __global__ __launch_bounds__(MlpShape<NT>::kThreads, 1) void k_mlp_bf16(MlpArgs 
             // followed by one slot of work on row tile mo - 1 (slot
             // s = 4 kb + t): slots 0-31 take the ReLU and bf16 rounding of
             // one element pair each (tile s / 8, pair s % 8), slots 8-11 load
-            // the head fragments, slots 32-39 run the head MFMAs (the
-            // accumulation order of each head accumulator is that of the
-            // other form).  The next row tile's bias is loaded at k-step 1.
-            // A scheduling fence after every slot keeps this order.
+            // the head fragments, and the head MFMAs follow once their tiles'
+            // activations are complete.  With 64 slots per row tile (H = 256)
+            // they take slots 32-39; with 32 (H = 128) the head MFMAs of tiles
+            // 0-1 take slots 16-19 and those of tiles 2-3, whose activations
+            // complete at the row tile's last slot, slots 0-3 of the next row
+            // tile (their activations and fragments carried over).  Either
+            // way each head accumulator takes its contributions in the order
+            // of the other form.  The next row tile's bias is loaded at
+            // k-step 1.  A scheduling fence after every slot keeps this order.
             constexpr int kSteps = (MT - 1) * KB2;
+            constexpr int kSlots = KB2 * NT;
+            constexpr bool kWide = kSlots >= 40 + 8 * NO;
+            static_assert(kWide || kSlots == 32, "four-tile slot maps: H = 256 or H = 128");
+            constexpr int kDec0 = kWide ? 40 : 20;      // first decision slot
+            constexpr int kDecStride = kWide ? 8 : 4;   // slots per own query's decision
             float dtt[NO], dtp[NO], dnc[NO];
+            u32x4 h2c[2][2];                     // narrow: tiles 2-3 of the previous row tile [par][b]
+            bf16x8 f3c[2][2];                    // narrow: their head fragments [b][par]
             auto epi_pair = [&](const f32x16 &v, int e) {
                 return __builtin_bit_cast(uint32_t, relu_bf16x2(v[2 * e], v[2 * e + 1]));
             };
             // row tile mo of phase B; DEC: with the previous pair step's
-            // decisions in its slots 40 .. 40 + 8 NO (one own query per eight
+            // decisions in its slots kDec0 .. (one own query per kDecStride
             // slots, in pieces: TTFT, TPOT, N_out, decision)
             auto row_tile = [&](auto mo_c, auto dec_c) {
                 constexpr int mo = decltype(mo_c)::value;
@@ -747,14 +759,22 @@ __global__ __launch_bounds__(MlpShape<NT>::kThreads, 1) void k_mlp_bf16(MlpArgs 
                             const int kh = 2 * (mo - 1) + b;
                             f3[b][par] = s_w3f[kh * W3S + (par ? w3o1 : w3o0)];
                         }
-                        if (sl >= 32 && sl < 40) {
-                            // acc3[j]: (b 0, tile 2j), (b 0, tile 2j + 1), (b 1, 2j), (b 1, 2j + 1)
+                        // acc3[j]: (b 0, tile 2j), (b 0, tile 2j + 1), (b 1, 2j), (b 1, 2j + 1)
+                        if (kWide && sl >= 32 && sl < 40) {
                             const int j = (sl - 32) / 4, r = (sl - 32) % 4, b = r / 2, par = r % 2;
                             acc3[j] = mfma16(f3[b][par], __builtin_bit_cast(bf16x8, h2u[2 * j + par][b]), acc3[j]);
                         }
+                        if (!kWide && sl >= 16 && sl < 20) {
+                            const int r = sl - 16, b = r / 2, par = r % 2;
+                            acc3[0] = mfma16(f3[b][par], __builtin_bit_cast(bf16x8, h2u[par][b]), acc3[0]);
+                        }
+                        if (!kWide && mo >= 2 && sl < 4) {
+                            const int b = sl / 2, par = sl % 2;
+                            acc3[1] = mfma16(f3c[b][par], __builtin_bit_cast(bf16x8, h2c[par][b]), acc3[1]);
+                        }
                         if constexpr (DEC) {
-                            if (sl >= 40 && sl < 40 + 8 * NO && (sl - 40) % 8 < 4) {
-                                const int j = (sl - 40) / 8, piece = (sl - 40) % 8;
+                            if (sl >= kDec0 && sl < kDec0 + kDecStride * NO && (sl - kDec0) % kDecStride < 4) {
+                                const int j = (sl - kDec0) / kDecStride, piece = (sl - kDec0) % kDecStride;
                                 if (pd >= 0) {
                                     if (piece == 0) dtt[j] = softplus_fast(pz[j][0] + a.b3_0);
                                     if (piece == 1) dtp[j] = softplus_fast(pz[j][1] + a.b3_1);
@@ -766,17 +786,34 @@ __global__ __launch_bounds__(MlpShape<NT>::kThreads, 1) void k_mlp_bf16(MlpArgs 
                         __builtin_amdgcn_sched_barrier(kFull);
                     }
                 }
+                if constexpr (!kWide) {
+#pragma unroll
+                    for (int par = 0; par < 2; ++par)
+#pragma unroll
+                        for (int b = 0; b < 2; ++b) {
+                            h2c[par][b] = h2u[2 + par][b];
+                            f3c[b][par] = f3[b][par];
+                        }
+                }
             };
-            using T = std::true_type;
-            using F = std::false_type;
-            row_tile(std::integral_constant<int, 1>{}, std::integral_constant<bool, !STAGED>{});
-            row_tile(std::integral_constant<int, 2>{}, F{});
-            row_tile(std::integral_constant<int, 3>{}, F{});
-            row_tile(std::integral_constant<int, 4>{}, F{});
-            row_tile(std::integral_constant<int, 5>{}, F{});
-            row_tile(std::integral_constant<int, 6>{}, F{});
-            row_tile(std::integral_constant<int, 7>{}, F{});
-            static_assert(MT == 8, "the four-tile form is built for H = 256");
+            // row tiles 1 .. MT - 1 (compile-time indices); the decisions of
+            // the previous pair step ride in row tile 1
+            auto run_tiles = [&](auto self, auto mo_c) {
+                constexpr int mo = decltype(mo_c)::value;
+                if constexpr (mo < MT) {
+                    row_tile(mo_c, std::integral_constant<bool, mo == 1 && !STAGED>{});
+                    self(self, std::integral_constant<int, mo + 1>{});
+                }
+            };
+            run_tiles(run_tiles, std::integral_constant<int, 1>{});
+            if constexpr (!kWide) {
+                // tiles 2-3 of row tile MT - 2, before row tile MT - 1's heads
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int b = r / 2, par = r % 2;
+                    acc3[1] = mfma16(f3c[b][par], __builtin_bit_cast(bf16x8, h2c[par][b]), acc3[1]);
+                }
+            }
             l2_epi(MT - 1, acc[(MT - 1) & 1]);
         } else {
             // layer 1: MFMAs of tile mt, then the epilogue of tile mt - 1
@@ -885,16 +922,17 @@ __global__ __launch_bounds__(MlpShape<NT>::kThreads, 1) void k_mlp_bf16(MlpArgs 
     }
 }
 
-// Column tiles per wave: four at H = 256 (the large-batch throughput shape)
-// for the staged predictor, and for the fused one when the input-length slot
-// lies in the first k-block; two otherwise.
+// Column tiles per wave: four at H = 256 and H = 128 (one wave per SIMD, the
+// hand-scheduled form) for the staged predictor, and for the fused one when
+// the input-length slot lies in the first k-block; two otherwise (H = 64).
 template <int H, bool STAGED, int NH, bool FB>
 static hipError_t launch_mlp_t(const MlpArgs &a, dim3 grid, hipStream_t s) {
-    if constexpr (H == 256 && STAGED) {
+    constexpr bool kFour = H == 256 || H == 128;
+    if constexpr (kFour && STAGED) {
         return launch_kernel(k_mlp_bf16<H, STAGED, NH, FB, 4, false>, grid, dim3(MlpShape<4>::kThreads), 0, s, a);
     }
     const bool lean = !a.cand_ttft && !a.cand_nout && !a.rule.score_paper && !a.rule.bound_paper;
-    if constexpr (H == 256 && !STAGED) {
+    if constexpr (kFour && !STAGED) {
         if (a.len_slot < 16) {          // the four-tile form patches k-block 0 only
             if (lean)
                 return launch_kernel(k_mlp_bf16<H, STAGED, NH, FB, 4, true>, grid, dim3(MlpShape<4>::kThreads), 0, s, a);
