@@ -772,6 +772,10 @@ hwr_status route_device(hwr_ctx *c, const DevBatch &b, const Workspace &w) {
             ma.out = oa;
             ma.nsplit = 1;
             ma.ldq = ldq;
+            // one wave per SIMD with four column tiles pays where every
+            // compute unit gets a workgroup; smaller batches take the two-tile
+            // form (two waves per SIMD), which starts and drains faster
+            ma.four_tiles = (cn + kQPerBlock - 1) / kQPerBlock >= c->cus;
             if (c->pipeline == HWR_PIPE_FUSED && c->nw == 1) {
                 // per-candidate outputs, if the caller asked for them, go
                 // straight to its [query][pair] buffers

@@ -152,6 +152,8 @@ struct MlpArgs {                  // bf16 predictor (fused or staged)
     int ldq;                      // pair stride of the pair-major buffers: pair_stride(nq)
     OutArgs out;
     int nsplit;                   // pair ranges (grid.y); >1 writes partials
+    int four_tiles;               // the batch fills the device (a workgroup per compute unit or more):
+                                  // the four-tile form, where it exists for H
     uint64_t *part_key;           // [nsplit][nq]
     float *part_val;              // [nsplit][nq][kPartVals]
     int fold_b1;                  // b1 is inside W1 (zero accumulator start)

@@ -923,17 +923,20 @@ __global__ __launch_bounds__(MlpShape<NT>::kThreads, 1) void k_mlp_bf16(MlpArgs 
 }
 
 // Column tiles per wave: four at H = 256 and H = 128 (one wave per SIMD, the
-// hand-scheduled form) for the staged predictor, and for the fused one when
-// the input-length slot lies in the first k-block; two otherwise (H = 64).
+// hand-scheduled form) for batches that give every compute unit a workgroup,
+// staged, and fused when the input-length slot lies in the first k-block; two
+// otherwise (two waves per SIMD: smaller batches start and drain faster).
+// The two forms give bit-identical results.
 template <int H, bool STAGED, int NH, bool FB>
 static hipError_t launch_mlp_t(const MlpArgs &a, dim3 grid, hipStream_t s) {
     constexpr bool kFour = H == 256 || H == 128;
     if constexpr (kFour && STAGED) {
-        return launch_kernel(k_mlp_bf16<H, STAGED, NH, FB, 4, false>, grid, dim3(MlpShape<4>::kThreads), 0, s, a);
+        if (a.four_tiles)
+            return launch_kernel(k_mlp_bf16<H, STAGED, NH, FB, 4, false>, grid, dim3(MlpShape<4>::kThreads), 0, s, a);
     }
     const bool lean = !a.cand_ttft && !a.cand_nout && !a.rule.score_paper && !a.rule.bound_paper;
     if constexpr (kFour && !STAGED) {
-        if (a.len_slot < 16) {          // the four-tile form patches k-block 0 only
+        if (a.four_tiles && a.len_slot < 16) {   // the four-tile form patches k-block 0 only
             if (lean)
                 return launch_kernel(k_mlp_bf16<H, STAGED, NH, FB, 4, true>, grid, dim3(MlpShape<4>::kThreads), 0, s, a);
             return launch_kernel(k_mlp_bf16<H, STAGED, NH, FB, 4, false>, grid, dim3(MlpShape<4>::kThreads), 0, s, a);

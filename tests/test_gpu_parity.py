@@ -275,3 +275,40 @@ def test_replicate_seeds(name, kw, pipeline, offset):
     r.close()
     _report(f"{name} seed {seed} {pipeline}", G.check(pb, st, qs, out))
 
+
+
+@pytest.mark.parametrize("kw,pipeline", [
+    (dict(), "fused"),                                           # H = 128, lean and non-lean
+    (dict(n_heads=3), "staged"),                                 # H = 128, three heads
+    (dict(hidden=256), "staged"),                                # H = 256 staged
+    (dict(hidden=256, n_heads=3), "fused"),                      # H = 256, three heads
+    (dict(score_mode=1, cost_weight=0.3, **S.PAPER_SLO), "fused"),   # H = 128, the paper's rules
+])
+def test_four_tile_form_equals_two_tile_form(kw, pipeline):
+    """A chunk that gives every compute unit a workgroup (256 queries each)
+    takes the four-column-tile, one-wave-per-SIMD predictor at H = 128 and
+    256; half that chunk takes the two-tile form (the pair range split over
+    workgroups).  Both give the same bits -- decisions, per-candidate
+    predictions, the Q matrix -- and the four-tile form's decisions are the
+    same with and without per-candidate outputs (its lean and full
+    instantiations).  Every 64th query is also checked against the oracle
+    (Sec. 3.2 Eq. 1-3)."""
+    import torch
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    n = 256 * cus
+    sp = S.spec("C2", n_queries=n, **kw)
+    pb, st, qs = S.make_problem(sp, 17), S.make_state(sp, 17), S.make_queries(sp, 17)
+    four = G.make_router(pb, pipeline=pipeline, max_chunk=n)
+    two = G.make_router(pb, pipeline=pipeline, max_chunk=n // 2)
+    for r in (four, two):
+        r.update(st)
+    a = G.route_device(four, qs, "bf16")
+    b = G.route_device(two, qs, "bf16")
+    lean = G.route_device(four, qs, "bf16", candidates=False)
+    for k in a:
+        assert np.array_equal(a[k].view(np.uint8), b[k].view(np.uint8)), k
+    for k in lean:
+        assert np.array_equal(a[k].view(np.uint8), lean[k].view(np.uint8)), k
+    idx = np.arange(0, n, 64)
+    rep = G.check(pb, st, qs.take(idx), {k: v[idx] for k, v in a.items()}, query_ids=idx)
+    _report(f"four-tile form {kw} {pipeline}, every 64th of {n} queries", rep)
