@@ -44,6 +44,31 @@ __device__ __forceinline__ void pair_row(uint16_t *row, int j, int b0, int ks, i
     }
 }
 
+// Sum over each 16-lane row on DPP: every lane of the row ends with the same
+// total (each step adds a lane's value to its partner's, both orders giving
+// the same fp32 result).
+__device__ __forceinline__ float row_sum16(float v) {
+    v += __uint_as_float(dpp_u32<0xB1>(__float_as_uint(v)));    // quad_perm [1,0,3,2]
+    v += __uint_as_float(dpp_u32<0x4E>(__float_as_uint(v)));    // quad_perm [2,3,0,1]
+    v += __uint_as_float(dpp_u32<0x141>(__float_as_uint(v)));   // row_half_mirror
+    v += __uint_as_float(dpp_u32<0x140>(__float_as_uint(v)));   // row_mirror
+    return v;
+}
+
+// Dot product of eight bf16 pairs, fp32 accumulation.  (Each element goes
+// through a named scalar before its bit cast: this compiler reads element 0
+// for a bit cast taken of a vector subscript directly.)
+__device__ __forceinline__ float dot8_bf16(const bf16x8 &x, const bf16x8 &y) {
+    const u32x4 a = __builtin_bit_cast(u32x4, x), b = __builtin_bit_cast(u32x4, y);
+    float s = 0.0f;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        const uint32_t ua = a[t], ub = b[t];
+        s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, ua), __builtin_bit_cast(bf16x2, ub), s, false);
+    }
+    return s;
+}
+
 // Cross-lane maximum on DPP (see wave_sum), then one read of each row's lane 0.
 __device__ __forceinline__ uint64_t wave_max(uint64_t k) {
     k = max_dpp<0xB1>(k);
@@ -75,8 +100,7 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
     constexpr int MO = (MT + 3) / 4;          // second-layer row tiles per wave
     constexpr int kW1 = MT * 128 / 256;       // 16-byte pieces of w1 per thread
     constexpr int kEmb = 4;                   // 16-byte embedding pieces per thread (D <= 8192)
-    constexpr int kHeldS = 4;                 // quality: embedding slices held (D <= 2048)
-    constexpr int kHeldM = H <= 128 ? 2 : 1;  // quality: model pairs held per wave
+    constexpr int kQP = 8;                    // quality: 16-byte weight pieces held per lane (D <= 1024)
     __shared__ bf16x8 s_w1[MT * 2 * 64];
     __shared__ u32x4 s_bw[2][MT * 8];         // b1 tiles, b2 tiles
     __shared__ u32x4 s_w3p[MT * 4 * kMaxHeads];   // head pairs: [tile][half][head][2]
@@ -90,6 +114,9 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
     __shared__ uint32_t s_ctl[2];             // resident: request found, its sequence number
     const int NH = a.nheads;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, n = lane & 31, h = lane >> 5;
+    // quality: row r of wave w (16 lanes) takes models 4w + r, 4w + r + 16;
+    // lane l16 of the row takes the 16-byte pieces l16, l16 + 16, ... of D
+    const int l16 = lane & 15, mq = 4 * wave + (lane >> 4), D8 = a.D >> 3;
     const int b0 = a.arch_width + a.gpu_width;
     const int j8 = tid & 7, ks = (j8 - b0) & 7;
 
@@ -102,7 +129,7 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
     int ia0 = 0, ig0 = 0, md0 = 0;
     constexpr int MOH = MO == 1 ? 1 : 0;     // second-layer tiles held in registers
     bf16x8 fw2[MO][KB2];
-    bf16x8 wq0[kHeldM][kHeldS], wq1[kHeldM][kHeldS];
+    bf16x8 wqh[kQP];
     uint32_t last = a.last_seq;
     for (int iter = 0;; ++iter) {
         if constexpr (RES) {
@@ -175,17 +202,12 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
             }
         }
         if (first) {
+            const uint16_t *wm = a.wqT + static_cast<size_t>(mq < a.M ? mq : 0) * a.D;
     #pragma unroll
-        for (int jm = 0; jm < kHeldM; ++jm) {
-            const int m0 = wave + 8 * jm < a.M ? wave + 8 * jm : 0;
-            const int m1 = wave + 8 * jm + 4 < a.M ? wave + 8 * jm + 4 : m0;
-    #pragma unroll
-            for (int i = 0; i < kHeldS; ++i) {
-                const int k = (lane + 64 * i) * 8 < a.D ? (lane + 64 * i) * 8 : 0;
-                wq0[jm][i] = *reinterpret_cast<const bf16x8 *>(a.wqT + static_cast<size_t>(m0) * a.D + k);
-                wq1[jm][i] = *reinterpret_cast<const bf16x8 *>(a.wqT + static_cast<size_t>(m1) * a.D + k);
+            for (int i = 0; i < kQP; ++i) {
+                const int c = l16 + 16 * i;
+                wqh[i] = *reinterpret_cast<const bf16x8 *>(wm + 8 * (c < D8 ? c : 0));
             }
-        }
         }
         const uint32_t seq = RES ? last : hdr[0];
         const int32_t len = static_cast<int32_t>(hdr[2]);
@@ -237,6 +259,36 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
 
         const float nout = static_cast<float>(no < 0 ? 0 : no);
         const QueryRule qrule = query_rule(a.rule, slo, len, nout, a.w);
+        // ---- quality of every model (Sec. 3.2 item 3), once per request: the
+        // held pieces first (all LDS reads issued together, pieces past D
+        // masked), further pieces and the second pass of models from memory
+        {
+            bf16x8 e[kQP];
+    #pragma unroll
+            for (int i = 0; i < kQP; ++i) {
+                const int c = l16 + 16 * i;
+                e[i] = reinterpret_cast<const bf16x8 *>(s_emb)[c < D8 ? c : 0];
+            }
+            float q = 0.0f;
+    #pragma unroll
+            for (int i = 0; i < kQP; ++i) {
+                const float t = dot8_bf16(e[i], wqh[i]);
+                q += l16 + 16 * i < D8 ? t : 0.0f;
+            }
+            const uint16_t *wm = a.wqT + static_cast<size_t>(mq < a.M ? mq : 0) * a.D;
+            for (int c = l16 + 16 * kQP; c < D8; c += 16)
+                q += dot8_bf16(reinterpret_cast<const bf16x8 *>(s_emb)[c], *reinterpret_cast<const bf16x8 *>(wm + 8 * c));
+            q = row_sum16(q);
+            if (l16 == 0 && mq < a.M) s_q[mq] = q + s_bq[mq];
+            for (int m = mq + 16; m < a.M; m += 16) {     // the same for every lane of a row
+                const uint16_t *w = a.wqT + static_cast<size_t>(m) * a.D;
+                float q2 = 0.0f;
+                for (int c = l16; c < D8; c += 16)
+                    q2 += dot8_bf16(reinterpret_cast<const bf16x8 *>(s_emb)[c], *reinterpret_cast<const bf16x8 *>(w + 8 * c));
+                q2 = row_sum16(q2);
+                if (l16 == 0) s_q[m] = q2 + s_bq[m];
+            }
+        }
         Best best = best_none();
         const int ntiles = (a.N + 31) / 32;
         for (int ct = 0; ct < ntiles; ++ct) {
@@ -318,58 +370,6 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
                 s_z[wave][n][0] = z0;
                 s_z[wave][n][1] = z1;
                 s_z[wave][n][2] = z2;
-            }
-            // ---- quality of every model (Sec. 3.2 item 3), once: wave w takes
-            // models w, w + 4, w + 8, ...; lanes split D
-            if (ct == 0) {
-                // models wave + 8j and wave + 8j + 4; the first kHeldM pairs use the
-                // heads already in registers for the first kHeldS slices of D
-                auto finish = [&](float acc0, float acc1, int m0, int m1) {
-                    acc0 = wave_sum(acc0);
-                    acc1 = wave_sum(acc1);
-                    if (lane == 0) {
-                        s_q[m0] = acc0 + s_bq[m0];
-                        if (m1 < a.M) s_q[m1] = acc1 + s_bq[m1];
-                    }
-                };
-                auto dot8 = [](const bf16x8 &e, const bf16x8 &q, float acc) {
-    #pragma unroll
-                    for (int t = 0; t < 8; ++t) acc = fmaf(static_cast<float>(e[t]), static_cast<float>(q[t]), acc);
-                    return acc;
-                };
-    #pragma unroll
-                for (int j = 0; j < kHeldM; ++j) {
-                    const int m0 = wave + 8 * j, m1 = m0 + 4;
-                    if (m0 < a.M) {
-                        float acc0 = 0.0f, acc1 = 0.0f;
-    #pragma unroll
-                        for (int i = 0; i < kHeldS; ++i) {
-                            const int k = (lane + 64 * i) * 8;
-                            if (k < a.D) {
-                                const bf16x8 e = *reinterpret_cast<const bf16x8 *>(s_emb + k);
-                                acc0 = dot8(e, wq0[j][i], acc0);
-                                acc1 = dot8(e, wq1[j][i], acc1);
-                            }
-                        }
-                        for (int k = (lane + 64 * kHeldS) * 8; k < a.D; k += 512) {
-                            const bf16x8 e = *reinterpret_cast<const bf16x8 *>(s_emb + k);
-                            const int mm1 = m1 < a.M ? m1 : m0;
-                            acc0 = dot8(e, *reinterpret_cast<const bf16x8 *>(a.wqT + static_cast<size_t>(m0) * a.D + k), acc0);
-                            acc1 = dot8(e, *reinterpret_cast<const bf16x8 *>(a.wqT + static_cast<size_t>(mm1) * a.D + k), acc1);
-                        }
-                        finish(acc0, acc1, m0, m1);
-                    }
-                }
-                for (int j = kHeldM; wave + 8 * j < a.M; ++j) {
-                    const int m0 = wave + 8 * j, m1 = m0 + 4, mm1 = m1 < a.M ? m1 : m0;
-                    float acc0 = 0.0f, acc1 = 0.0f;
-                    for (int k = lane * 8; k < a.D; k += 512) {
-                        const bf16x8 e = *reinterpret_cast<const bf16x8 *>(s_emb + k);
-                        acc0 = dot8(e, *reinterpret_cast<const bf16x8 *>(a.wqT + static_cast<size_t>(m0) * a.D + k), acc0);
-                        acc1 = dot8(e, *reinterpret_cast<const bf16x8 *>(a.wqT + static_cast<size_t>(mm1) * a.D + k), acc1);
-                    }
-                    finish(acc0, acc1, m0, m1);
-                }
             }
             __syncthreads();
             // ---- heads, cost, decision (Eq. 2, Eq. 3)
