@@ -51,3 +51,28 @@ def test_single_query_matches_oracle(name, kw, flags):
     assert (batch["choice"] == got["choice"]).mean() > 0.9
     if sp.n_heads == 2:
         assert np.array_equal(got["nout"], qs.expected_out_len.astype(np.float32))
+
+
+@pytest.mark.parametrize("flags", [0, hwr.HWR_FLAG_RESIDENT])
+def test_single_query_maximum_shape(flags):
+    """The single-query kernel at the largest shape: 1024 pairs (32 models x 8
+    GPU types, each listed four times with its own state), D = 8192, H = 256.
+    Every fallback of the kernel runs: pair rows past the first 32, quality
+    weight pieces past the eight held per lane, the second pass of models."""
+    sp = S.spec("C5", n_queries=8, embed_dim=8192)
+    pb = S.make_problem(sp, 41)
+    pb.dep_model = np.tile(pb.dep_model, 4)
+    pb.dep_gpu = np.tile(pb.dep_gpu, 4)
+    st = np.concatenate([S.make_state(sp, 41 + k) for k in range(4)])
+    qs = S.make_queries(sp, 41)
+    r = G.make_router(pb, flags=flags)
+    r.update(st)
+    outs = [r.route_host(qs.emb_bits[i:i + 1], qs.input_len[i:i + 1], qs.expected_out_len[i:i + 1],
+                         qs.slo_s[i:i + 1]) for i in range(qs.n)]
+    r.close()
+    got = {k: np.concatenate([o[k] for o in outs]) for k in outs[0]}
+    orc = O.route_synth(pb, st, qs)
+    rep = parity.compare(got, orc, slo=qs.slo_s, alpha=sp.cost_weight, dep_model=pb.dep_model,
+                         rtol=1e-2, heads=sp.n_heads)
+    print(f"[parity] single max shape flags={flags}: {rep.summary()}", flush=True)
+    assert rep.ok, rep.failures[:5]
