@@ -25,7 +25,7 @@ __device__ __forceinline__ bf16x8 relu_pack8s(const f32x16 &c, int base) {
 // j + 16, j + 24 of its row.  The eight signal slots b .. b + 7 meet each
 // residue mod 8 once, so the thread evaluates exactly one signal: number
 // (j - b) mod 8 (Eq. 1 layout; the query's input length is signal 1).  Logs
-// in fp64, rounded once to fp32, then to bf16 (as the state kernel does).
+// in fp64 (ln_pos), rounded once to fp32, then to bf16 (as the state kernel does).
 __device__ __forceinline__ void pair_row(uint16_t *row, int j, int b0, int ks, int ia, int ig,
                                          uint32_t raw, float params, int32_t len, bool fold) {
     double arg = 1.0, scale = 0.0;
@@ -33,7 +33,7 @@ __device__ __forceinline__ void pair_row(uint16_t *row, int j, int b0, int ks, i
     if (ks == 1) { arg = static_cast<double>(len < 1 ? 1 : len); scale = 0.125; }
     if (ks == 2 || ks == 3) { arg = 1.0 + static_cast<double>(static_cast<int32_t>(raw)); scale = 0.5; }
     if (ks == 6 || ks == 7) { arg = static_cast<double>(__uint_as_float(raw)); scale = 0.25; }
-    float v = static_cast<float>(log(arg) * scale);
+    float v = static_cast<float>(ln_pos(arg) * scale);
     if (ks == 4 || ks == 5) v = __uint_as_float(raw);
     const uint16_t sig = bf16_bits(v);
 #pragma unroll
