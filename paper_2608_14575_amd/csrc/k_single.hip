@@ -69,6 +69,17 @@ __device__ __forceinline__ float dot8_bf16(const bf16x8 &x, const bf16x8 &y) {
     return s;
 }
 
+// The same pointer, held in vector registers: loads through it are vector
+// loads.  (A load from a pointer every lane shares becomes a scalar load,
+// which this compiler schedules after earlier vector loads have been waited
+// for; from host memory that is a second round trip.)
+template <class T>
+__device__ __forceinline__ const __attribute__((address_space(1))) T *per_lane(const T *p) {
+    uint64_t v = reinterpret_cast<uint64_t>(p);
+    asm volatile("" : "+v"(v));
+    return reinterpret_cast<const __attribute__((address_space(1))) T *>(v);
+}
+
 // Cross-lane maximum on DPP (see wave_sum), then one read of each row's lane 0.
 __device__ __forceinline__ uint64_t wave_max(uint64_t k) {
     k = max_dpp<0xB1>(k);
@@ -158,8 +169,11 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
         // ---- phase 1: every independent load is issued before any is waited
         // for -- host memory first (query record, runtime signals), then the
         // device-side weights -- so the phase costs one host round trip.
-        const u32x4 hdr = *reinterpret_cast<const u32x4 *>(a.in);   // seq, quit, input_len, nout
-        const float slo = reinterpret_cast<const float *>(a.in)[4];
+        // seq, input_len, nout, slo: one dword load each (no unused lanes of a
+        // load in flight for the compiler to give to another value)
+        const __attribute__((address_space(1))) uint32_t *hp = per_lane(reinterpret_cast<const uint32_t *>(a.in));
+        const uint32_t h_seq = hp[0], h_len = hp[2], h_nout = hp[3];
+        const float slo = __uint_as_float(hp[4]);
         // (loads are unconditional, indices clamped into range: a load under a
         // branch makes the compiler wait for it, and for all earlier ones, there)
         const uint32_t raw0 = reinterpret_cast<const uint32_t *>(a.state + pc0)[ks >= 2 ? ks - 2 : 0];
@@ -209,9 +223,9 @@ __global__ __launch_bounds__(256) void k_single(SingleArgs a) {
                 wqh[i] = *reinterpret_cast<const bf16x8 *>(wm + 8 * (c < D8 ? c : 0));
             }
         }
-        const uint32_t seq = RES ? last : hdr[0];
-        const int32_t len = static_cast<int32_t>(hdr[2]);
-        const int32_t no = static_cast<int32_t>(hdr[3]);
+        const uint32_t seq = RES ? last : h_seq;
+        const int32_t len = static_cast<int32_t>(h_len);
+        const int32_t no = static_cast<int32_t>(h_nout);
 
         // ---- phase 2: LDS stores, the feature rows, one barrier
     #pragma unroll
