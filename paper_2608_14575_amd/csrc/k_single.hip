@@ -2,8 +2,10 @@
 // pairs in one workgroup, reading the query and the pairs' current runtime
 // signals from pinned host memory and writing the decision there, so that
 // one launch (captured once in a graph) is the whole call -- or, in the
-// resident form, one launch serves a stream of queries.  Pairs are the MFMA columns here (32 per tile); the 4 waves
-// split the second-layer row tiles and combine their head partials in LDS.
+// resident form, one launch serves a stream of queries.  Pairs are the MFMA
+// columns here (32 per tile); the 4 waves split the second-layer row tiles
+// and combine their head partials in LDS.  The quality of every model is
+// computed once per query, a 16-lane row per model.
 #include "hwr_device.hpp"
 
 namespace hwr {
