@@ -23,6 +23,9 @@
  *    that only answers through pinned host memory, plain or graph-launched:
  *    the floor under a single-query route.
  *
+ * One more entry point exposes a device helper for checking rather than a
+ * ceiling: hwr_probe_feature_log, the logarithm every feature uses.
+ *
  * All are synchronous: they launch on a stream of their own on the given
  * device, wait, and return the median over the timed launches (the rates
  * timed on the device from each launch's own start to its own end).  The MFMA
@@ -81,6 +84,17 @@ hwr_status hwr_probe_launch_floor(int32_t device, int32_t use_graph, int32_t cal
  * Arguments and errors as hwr_probe_hbm_read. */
 hwr_status hwr_probe_hbm_write(int32_t device, void *buf, uint64_t bytes, int32_t waves_per_simd,
                                int32_t reps, double *gbps);
+
+/* The device's feature logarithm, for checking: y[i] = ln(x[i]) as every
+ * Eq. 1 feature log of the library computes it (fp64; the features then
+ * round ln(x) times their scale once to fp32, then to bf16).  x and y are
+ * host arrays of n (1..2^26) doubles owned by the caller; every x[i] must be
+ * positive, finite and normal, the arguments the features have (counts plus
+ * one, parameter counts, latencies).  Synchronous: it allocates two device
+ * buffers of n doubles, runs one kernel on the device's null stream and
+ * frees them.  Errors: HWR_ERR_INVALID_ARG (NULL pointer, n out of range, an
+ * x[i] outside the domain; no device touched), HWR_ERR_HIP, HWR_ERR_OOM. */
+hwr_status hwr_probe_feature_log(int32_t device, const double *x, int64_t n, double *y);
 
 #ifdef __cplusplus
 }

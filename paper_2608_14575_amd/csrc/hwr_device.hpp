@@ -11,10 +11,11 @@ namespace hwr {
 // ln m = 2 artanh(f) = 2 f (1 + f^2/3 + f^4/5 + ...), f = (m - 1) / (m + 1)
 // (the series of Abramowitz & Stegun 4.1.27), taken to f^17: |f| <= 0.172,
 // so the first term left out is below 2^-55 relative.  The quotient is the
-// hardware reciprocal refined by two Newton steps.  Relative error below
-// 2^-49 (measured against the C library's log on 16M arguments of each
-// feature's range; every fp32 and bf16 feature value the same); about a
-// third of the operations of the library's fp64 log.
+// hardware reciprocal refined by two Newton steps.  Relative error about
+// 2^-50 at most over the features' argument ranges, and every fp32 and bf16
+// feature value the same as with an exact log (hwr_probe_feature_log exposes
+// this function for that check); about a third of the operations of the
+// library's fp64 log.
 __device__ inline double ln_pos(double x) {
     double m = __builtin_amdgcn_frexp_mant(x);    // [0.5, 1)
     int e = __builtin_amdgcn_frexp_exp(x);

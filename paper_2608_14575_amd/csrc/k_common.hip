@@ -1,6 +1,10 @@
 // State ingest, feature gather, decision epilogue, split merge and the fp32
 // predictor / quality kernels of libhwr (gfx950).
+#include <cfloat>
+#include <cmath>
+
 #include "hwr_device.hpp"
+#include "hwr_probe.h"
 
 namespace hwr {
 
@@ -447,3 +451,35 @@ hipError_t launch_merge(const MergeArgs &a, hipStream_t s) {
 }
 
 }  // namespace hwr
+
+// ------------------------------------------------------------ feature log check
+namespace {
+__global__ __launch_bounds__(256) void k_feature_log(const double *x, double *y, int64_t n) {
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    if (i < n) y[i] = hwr::ln_pos(x[i]);
+}
+}  // namespace
+
+extern "C" hwr_status hwr_probe_feature_log(int32_t device, const double *x, int64_t n, double *y) {
+    if (!x || !y || device < 0 || n < 1 || n > (int64_t{1} << 26)) return HWR_ERR_INVALID_ARG;
+    for (int64_t i = 0; i < n; ++i)
+        if (!(x[i] >= DBL_MIN && x[i] <= DBL_MAX)) return HWR_ERR_INVALID_ARG;   // positive, finite, normal
+    int prev = -1;
+    hipError_t e = hipGetDevice(&prev);
+    if (e == hipSuccess) e = hipSetDevice(device);
+    double *dx = nullptr, *dy = nullptr;
+    const size_t bytes = static_cast<size_t>(n) * sizeof(double);
+    if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void **>(&dx), bytes);
+    if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void **>(&dy), bytes);
+    if (e == hipSuccess) e = hipMemcpy(dx, x, bytes, hipMemcpyHostToDevice);
+    if (e == hipSuccess) {
+        hipLaunchKernelGGL(k_feature_log, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, nullptr, dx, dy, n);
+        e = hipGetLastError();
+    }
+    if (e == hipSuccess) e = hipMemcpy(y, dy, bytes, hipMemcpyDeviceToHost);
+    if (dx) (void)hipFree(dx);
+    if (dy) (void)hipFree(dy);
+    if (prev >= 0) (void)hipSetDevice(prev);
+    if (e == hipSuccess) return HWR_OK;
+    return e == hipErrorOutOfMemory ? HWR_ERR_OOM : HWR_ERR_HIP;
+}

@@ -32,7 +32,8 @@ KERNEL_NAMES = ["state", "quality", "gather", "mlp", "epilogue", "fused", "merge
 EXPORTS = ["hwr_init", "hwr_update_hw_state", "hwr_route_batch", "hwr_route_batch_static", "hwr_free",
            "hwr_last_error",
            "hwr_profile_enable", "hwr_profile_read", "hwr_sim_run", "hwr_sim_last_error",
-           "hwr_probe_mfma_bf16", "hwr_probe_hbm_read", "hwr_probe_hbm_write", "hwr_probe_launch_floor"]
+           "hwr_probe_mfma_bf16", "hwr_probe_hbm_read", "hwr_probe_hbm_write", "hwr_probe_launch_floor",
+           "hwr_probe_feature_log"]
 
 _STATUS = {0: "HWR_OK", -1: "HWR_ERR_INVALID_ARG", -2: "HWR_ERR_OOM", -3: "HWR_ERR_HIP",
            -4: "HWR_ERR_STATE", -5: "HWR_ERR_UNSUPPORTED"}
@@ -175,6 +176,8 @@ def load(path: Optional[str] = None) -> C.CDLL:
                                          C.POINTER(C.c_double)]
     L.hwr_probe_hbm_write.restype = C.c_int
     L.hwr_probe_hbm_write.argtypes = [C.c_int32, _vp, C.c_uint64, C.c_int32, C.c_int32, C.POINTER(C.c_double)]
+    L.hwr_probe_feature_log.restype = C.c_int
+    L.hwr_probe_feature_log.argtypes = [C.c_int32, _vp, C.c_int64, _vp]
     if path is None:
         _lib = L
     return L
@@ -236,6 +239,15 @@ def hwr_probe_launch_floor(device: int, use_graph: bool, calls: int) -> tuple:
     p50, p99 = C.c_double(), C.c_double()
     _check(load().hwr_probe_launch_floor(device, int(use_graph), calls, C.byref(p50), C.byref(p99)), None)
     return p50.value, p99.value
+
+
+def hwr_probe_feature_log(device: int, x: np.ndarray) -> np.ndarray:
+    """ln(x) as the device's feature logarithm computes it (x: positive,
+    finite, normal doubles)."""
+    x = np.ascontiguousarray(x, np.float64)
+    y = np.empty_like(x)
+    _check(load().hwr_probe_feature_log(device, x.ctypes.data, x.size, y.ctypes.data), None)
+    return y
 
 
 def hwr_free(ctx) -> None:

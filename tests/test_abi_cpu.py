@@ -192,6 +192,16 @@ def test_probe_argument_errors(lib):
                  (0, 1, 100001, C.byref(out), C.byref(p99))]:
         assert lib.hwr_probe_launch_floor(*args) == hwr.HWR_ERR_INVALID_ARG, args
     assert out.value == -1.0 and p99.value == -1.0
+    # the feature logarithm: every argument checked on the host first
+    x = np.array([2.0, 3.0], np.float64)
+    y = np.full(2, -7.0)
+    for args in [(0, None, 2, y.ctypes.data), (0, x.ctypes.data, 2, None), (-1, x.ctypes.data, 2, y.ctypes.data),
+                 (0, x.ctypes.data, 0, y.ctypes.data), (0, x.ctypes.data, (1 << 26) + 1, y.ctypes.data)]:
+        assert lib.hwr_probe_feature_log(*args) == hwr.HWR_ERR_INVALID_ARG, args
+    for bad in (0.0, -1.0, np.inf, np.nan, 1e-310):     # outside: positive, finite, normal
+        xb = np.array([2.0, bad], np.float64)
+        assert lib.hwr_probe_feature_log(0, xb.ctypes.data, 2, y.ctypes.data) == hwr.HWR_ERR_INVALID_ARG, bad
+    assert (y == -7.0).all()
 
 
 def test_no_device_is_a_clean_error(lib):

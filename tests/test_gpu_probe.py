@@ -1,6 +1,7 @@
 """The ceiling probes on the device: rates that are positive and below the
 part's published peaks (dense bf16 MFMA 2.5 PFLOP/s at the 2.4 GHz peak
 clock, HBM3E 8 TB/s), and argument checks that need a real buffer."""
+import numpy as np
 import pytest
 
 from paper_2608_14575_amd import hwr
@@ -58,3 +59,38 @@ def test_launch_floor_plain_and_graph():
         print(f"[probe] launch floor ({'graph' if graph else 'plain'} launch): p50 {p50:.1f} us, p99 {p99:.1f} us",
               flush=True)
         assert 0.5 < p50 <= p99 < 10_000.0
+
+
+def _bf16_bits(f32: np.ndarray) -> np.ndarray:
+    """bf16 bits of fp32 values, nearest with ties to even (finite inputs)."""
+    u = f32.view(np.uint32).astype(np.uint64)
+    return ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+
+
+def test_feature_log_gives_the_features_of_the_exact_log():
+    """The device's feature logarithm against numpy's fp64 log on 4M
+    arguments over every feature's range (input lengths and queue counts
+    plus one, up to 2^31; parameter counts in billions; latencies in
+    seconds): relative error below 2^-48, and every feature value (ln times
+    its scale, rounded to fp32, then to bf16) the same."""
+    rng = np.random.default_rng(7)
+    n = 1 << 20
+    cases = {
+        "input length": (1.0 + rng.integers(0, 40000, n).astype(np.float64), 0.125),
+        "1 + queue": (1.0 + rng.integers(0, 1 << 31, n).astype(np.float64), 0.5),
+        "params (B)": (np.exp(rng.uniform(-1, 11, n)).astype(np.float32).astype(np.float64), 0.25),
+        "seconds": (np.exp(rng.uniform(-12, 8, n)).astype(np.float32).astype(np.float64), 0.25),
+    }
+    for name, (x, scale) in cases.items():
+        y = hwr.hwr_probe_feature_log(0, x)
+        ref = np.log(x)
+        rel = np.abs(y - ref) / np.maximum(np.abs(ref), 1e-300)
+        rel[ref == 0] = np.abs(y[ref == 0])
+        f_dev = (y * scale).astype(np.float32)
+        f_ref = (ref * scale).astype(np.float32)
+        n32 = int((f_dev != f_ref).sum())
+        n16 = int((_bf16_bits(f_dev) != _bf16_bits(f_ref)).sum())
+        print(f"[probe] feature log, {name}: max rel {rel.max():.2e}, fp32 differ {n32}, bf16 differ {n16}",
+              flush=True)
+        assert rel.max() < 2.0 ** -48, name
+        assert n16 == 0, name
