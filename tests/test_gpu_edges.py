@@ -336,3 +336,53 @@ def test_staged_epilogue_unaligned_candidate_buffers():
     got = {k: v.cpu().numpy() for k, v in out.items()}
     _same(got, ref, keys=list(got))
     assert np.array_equal(tt[1:].cpu().numpy().reshape(n, N), ref["cand_ttft"])
+
+
+def test_contexts_on_threads_are_independent():
+    """Three contexts, each created and used by its own host thread on its
+    own stream at the same time (a fused host batch, a staged host batch,
+    a run of single queries), give the same bits as each context alone."""
+    import threading
+    import torch
+    work = []
+    for name, seed, n, pipe in (("C2", 40, 3000, "fused"), ("C3", 41, 2000, "staged"), ("C4", 42, 40, "fused")):
+        sp, pb, st, qs = _case(name, seed=seed, n_queries=n)
+        work.append((pb, st, qs, pipe, name == "C4"))
+
+    def run(pb, st, qs, pipe, single, stream):
+        r = hwr.Router.from_problem(pb, pipeline=pipe, stream=stream)
+        r.update(st)
+        if single:
+            outs = [r.route_host(qs.emb_bits[i:i + 1], qs.input_len[i:i + 1], qs.expected_out_len[i:i + 1],
+                                 qs.slo_s[i:i + 1]) for i in range(qs.n)]
+            out = {k: np.concatenate([o[k] for o in outs]) for k in outs[0]}
+        else:
+            out = r.route_host(qs.emb_bits, qs.input_len, qs.expected_out_len, qs.slo_s)
+        r.close()
+        return out
+
+    ref = [run(*w, stream=G.torch_stream()) for w in work]
+    got = [[] for _ in work]
+    errors = []
+
+    def worker(i):
+        try:
+            torch.cuda.set_device(0)
+            s = torch.cuda.Stream()
+            for _ in range(4):
+                got[i].append(run(*work[i], stream=int(s.cuda_stream)))
+            s.synchronize()
+        except Exception as e:          # reported by the main thread
+            errors.append((i, repr(e)))
+
+    threads = [threading.Thread(target=worker, args=(i,)) for i in range(len(work))]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join(timeout=120)
+    assert not any(t.is_alive() for t in threads), "a routing thread did not finish"
+    assert not errors, errors
+    for i in range(len(work)):
+        assert len(got[i]) == 4
+        for out in got[i]:
+            _same(out, ref[i])
