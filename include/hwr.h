@@ -53,7 +53,10 @@
  *  - HWR_MEM_DEVICE batches are ordered on the context's stream and return
  *    without waiting; HWR_MEM_HOST batches return with the results written.
  *    A host batch larger than max_chunk is streamed: the next chunk's upload
- *    (on a second stream of the context) overlaps this chunk's kernels.
+ *    (on a second stream of the context) overlaps this chunk's kernels.  A
+ *    host batch in pageable memory with 16 MB of embeddings or more is copied
+ *    through 128 MB of pinned memory the context allocates on first use, by
+ *    up to seven host threads of its own (held until hwr_free).
  *  - A context is not thread-safe: one context per thread (or per stream).
  */
 #ifndef HWR_H

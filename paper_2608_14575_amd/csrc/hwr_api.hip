@@ -7,10 +7,13 @@
 #include <atomic>
 #include <chrono>
 #include <cmath>
+#include <condition_variable>
 #include <cstdio>
 #include <cstring>
+#include <memory>
 #include <mutex>
 #include <string>
+#include <thread>
 #include <vector>
 
 #include "hwr_internal.hpp"
@@ -65,6 +68,98 @@ static __device__ __align__(256) unsigned char scratch[kScratchBytes];
 constexpr int kMaxDevices = 64;
 std::mutex g_scratch_mu;
 void *g_scratch_ptr[kMaxDevices] = {};
+
+// Host batches in pageable memory: their embeddings pass through a ring of
+// pinned slots, each filled by a few host threads while the previous one is
+// uploaded (the runtime's own staging of a pageable copy runs on one thread,
+// at about half the rate of an upload from pinned memory).
+constexpr int kPageSlots = 4;
+constexpr size_t kPageSlotBytes = size_t(32) << 20;
+constexpr size_t kPageMinBytes = size_t(16) << 20;   // smaller batches keep the runtime's copy
+
+// A few threads that copy one host range into another together with the
+// calling thread; one copy at a time (a context is used by one thread).
+class CopyPool {
+  public:
+    explicit CopyPool(int threads) {
+        for (int i = 0; i < threads; ++i) workers_.emplace_back([this] { serve(); });
+    }
+    ~CopyPool() {
+        {
+            std::lock_guard<std::mutex> l(mu_);
+            stop_ = true;
+        }
+        wake_.notify_all();
+        for (std::thread &t : workers_) t.join();
+    }
+    void copy(void *dst, const void *src, size_t bytes) {
+        const size_t parts = workers_.size() + 1;
+        const size_t piece = std::max<size_t>(size_t(1) << 20, (bytes / parts + 4095) & ~size_t(4095));
+        {
+            std::lock_guard<std::mutex> l(mu_);
+            dst_ = static_cast<char *>(dst);
+            src_ = static_cast<const char *>(src);
+            bytes_ = bytes;
+            piece_ = piece;
+            next_ = 0;
+            left_ = (bytes + piece - 1) / piece;
+            ++gen_;
+        }
+        wake_.notify_all();
+        work();
+        std::unique_lock<std::mutex> l(mu_);
+        done_.wait(l, [&] { return left_ == 0; });
+    }
+
+  private:
+    void work() {
+        for (;;) {
+            char *d;
+            const char *s;
+            size_t n;
+            {
+                std::lock_guard<std::mutex> l(mu_);
+                const size_t off = next_ * piece_;
+                if (off >= bytes_) return;
+                ++next_;
+                d = dst_ + off;
+                s = src_ + off;
+                n = std::min(piece_, bytes_ - off);
+            }
+            std::memcpy(d, s, n);
+            std::lock_guard<std::mutex> l(mu_);
+            if (--left_ == 0) done_.notify_all();
+        }
+    }
+    void serve() {
+        uint64_t seen = 0;
+        for (;;) {
+            {
+                std::unique_lock<std::mutex> l(mu_);
+                wake_.wait(l, [&] { return stop_ || gen_ != seen; });
+                if (stop_) return;
+                seen = gen_;
+            }
+            work();
+        }
+    }
+    std::vector<std::thread> workers_;
+    std::mutex mu_;
+    std::condition_variable wake_, done_;
+    char *dst_ = nullptr;
+    const char *src_ = nullptr;
+    size_t bytes_ = 0, piece_ = 1, next_ = 0, left_ = 0;
+    uint64_t gen_ = 0;
+    bool stop_ = false;
+};
+
+// True when p is pinned (page-locked) host memory the device reads directly.
+bool host_pinned(const void *p) {
+    hipPointerAttribute_t a{};
+    const hipError_t e = hipPointerGetAttributes(&a, p);
+    (void)hipGetLastError();   // an unregistered pointer may leave its error behind
+    return e == hipSuccess && a.type == hipMemoryTypeHost;
+}
 
 }  // namespace
 
@@ -124,6 +219,14 @@ struct hwr_ctx {
         bool used = false;
     } hin[2];
     hipStream_t cstream = nullptr;   // upload stream of host-memory batches
+    struct PageSlot {
+        void *buf = nullptr;           // pinned, kPageSlotBytes
+        hipEvent_t done = nullptr;     // its last upload has finished
+        bool used = false;
+    } pslot[kPageSlots];
+    int pslot_next = 0;
+    std::unique_ptr<CopyPool> copier;  // set up by the first pageable host batch
+    bool page_failed = false;          // the pinned ring could not be set up: the runtime copies
     int32_t *d_hchoice = nullptr;
     float *d_hval = nullptr, *d_hcand = nullptr, *d_hqual = nullptr;
     uint8_t *d_hfeas = nullptr;
@@ -476,6 +579,11 @@ void release(hwr_ctx *c) {
         if (h.read) (void)hipEventDestroy(h.read);
     }
     if (c->cstream) (void)hipStreamDestroy(c->cstream);
+    c->copier.reset();
+    for (auto &sl : c->pslot) {
+        if (sl.buf) (void)hipHostFree(sl.buf);
+        if (sl.done) (void)hipEventDestroy(sl.done);
+    }
     if (c->h_ring) (void)hipHostFree(c->h_ring);
     if (c->h_cur) (void)hipHostFree(c->h_cur);
     if (c->sstream) (void)hipStreamDestroy(c->sstream);
@@ -907,6 +1015,46 @@ hwr_status ensure_host_staging(hwr_ctx *c, size_t rows) {
 // error, once both streams have drained.
 hwr_status route_host_chunks(hwr_ctx *c, const hwr_query_batch *q, hwr_route_result *r);
 
+// The pinned ring and the copy threads of pageable host batches, set up once.
+// When pinned memory cannot be had, pageable batches keep the runtime's copy.
+bool page_ring(hwr_ctx *c) {
+    if (c->copier) return true;
+    if (c->page_failed) return false;
+    for (auto &sl : c->pslot) {
+        if (hipHostMalloc(&sl.buf, kPageSlotBytes, hipHostMallocDefault) != hipSuccess ||
+            hipEventCreateWithFlags(&sl.done, hipEventDisableTiming) != hipSuccess) {
+            (void)hipGetLastError();
+            for (auto &t : c->pslot) {
+                if (t.buf) (void)hipHostFree(t.buf);
+                if (t.done) (void)hipEventDestroy(t.done);
+                t = hwr_ctx::PageSlot{};
+            }
+            c->page_failed = true;
+            return false;
+        }
+    }
+    const unsigned hw = std::thread::hardware_concurrency();
+    c->copier = std::make_unique<CopyPool>(static_cast<int>(std::min(7u, std::max(1u, hw / 2))));
+    return true;
+}
+
+// Upload of `bytes` from pageable host memory to device memory on `stream`,
+// through the pinned ring: each slot is filled (caller and copy threads) once
+// its previous upload has finished, then uploaded.
+hwr_status upload_pageable(hwr_ctx *c, void *dst, const void *src, size_t bytes, hipStream_t stream) {
+    for (size_t o = 0; o < bytes; o += kPageSlotBytes) {
+        const size_t n = std::min(kPageSlotBytes, bytes - o);
+        hwr_ctx::PageSlot &sl = c->pslot[c->pslot_next];
+        c->pslot_next = (c->pslot_next + 1) % kPageSlots;
+        if (sl.used) HWR_HIP(c, hipEventSynchronize(sl.done));
+        c->copier->copy(sl.buf, static_cast<const char *>(src) + o, n);
+        HWR_HIP(c, hipMemcpyAsync(static_cast<char *>(dst) + o, sl.buf, n, hipMemcpyHostToDevice, stream));
+        HWR_HIP(c, hipEventRecord(sl.done, stream));
+        sl.used = true;
+    }
+    return HWR_OK;
+}
+
 hwr_status route_host(hwr_ctx *c, const hwr_query_batch *q, hwr_route_result *r) {
     const hwr_status st = route_host_chunks(c, q, r);
     if (st != HWR_OK) {
@@ -925,12 +1073,20 @@ hwr_status route_host_chunks(hwr_ctx *c, const hwr_query_batch *q, hwr_route_res
     const size_t esz = c->bf16 ? 2 : 4;
     const int N = c->N, M = c->M, D = c->D;
     hipStream_t s = c->stream, cs = c->cstream;
+    const size_t emb_bytes = static_cast<size_t>(q->n) * D * esz;
+    const bool staged_copy = emb_bytes >= kPageMinBytes && !host_pinned(q->emb) && page_ring(c);
     auto upload = [&](int off) -> hwr_status {
         const int cn = std::min(c->max_chunk, q->n - off);
         hwr_ctx::InStage &h = c->hin[(off / c->max_chunk) & 1];
         if (h.used) HWR_HIP(c, hipStreamWaitEvent(cs, h.read, 0));
-        HWR_HIP(c, hipMemcpyAsync(h.emb, static_cast<const char *>(q->emb) + static_cast<size_t>(off) * D * esz,
-                                  static_cast<size_t>(cn) * D * esz, hipMemcpyHostToDevice, cs));
+        const char *e = static_cast<const char *>(q->emb) + static_cast<size_t>(off) * D * esz;
+        const size_t eb = static_cast<size_t>(cn) * D * esz;
+        if (staged_copy) {
+            const hwr_status us = upload_pageable(c, h.emb, e, eb, cs);
+            if (us != HWR_OK) return us;
+        } else {
+            HWR_HIP(c, hipMemcpyAsync(h.emb, e, eb, hipMemcpyHostToDevice, cs));
+        }
         HWR_HIP(c, hipMemcpyAsync(h.len, q->input_len + off, cn * 4, hipMemcpyHostToDevice, cs));
         if (c->NH == 2)
             HWR_HIP(c, hipMemcpyAsync(h.nout, q->expected_out_len + off, cn * 4, hipMemcpyHostToDevice, cs));

@@ -184,6 +184,29 @@ def test_host_batches_in_several_chunks(name, kw):
     _same({k: v[:150] for k, v in d.items()}, h2)
 
 
+@pytest.mark.parametrize("pinned", [False, True])
+def test_large_host_batches_through_the_pinned_ring(pinned):
+    """A pageable host batch of at least 16 MB of embeddings passes through the
+    library's pinned ring (filled by its copy threads); a pinned one is
+    uploaded directly.  20,000 C3 queries (41 MB) in chunks of 3,000, so the
+    ring of four 32 MB slots wraps, against the device path in one chunk, bit
+    for bit; then a second batch through the same router."""
+    import torch
+    sp, pb, st, qs = _case("C3", n_queries=20000)
+    one = G.make_router(pb)
+    many = G.make_router(pb, max_chunk=3000)
+    one.update(st)
+    many.update(st)
+    d = G.route_device(one, qs, sp.dtype, candidates=False)
+    emb = qs.emb_bits
+    if pinned:
+        emb = torch.from_numpy(np.ascontiguousarray(emb)).pin_memory().numpy()
+    assert emb.nbytes >= 16 << 20
+    for _ in range(2):
+        h = many.route_host(emb, qs.input_len, qs.expected_out_len, qs.slo_s)
+        _same(d, h)
+
+
 def test_default_slo_used_when_absent():
     sp, pb, st, qs = _case(n_queries=64)
     r = G.make_router(pb, default_slo_s=1.5)
