@@ -153,12 +153,18 @@ class CopyPool {
     bool stop_ = false;
 };
 
-// True when p is pinned (page-locked) host memory the device reads directly.
-bool host_pinned(const void *p) {
+// What the runtime knows of a host batch's buffer: pinned (page-locked) host
+// memory the device reads directly, device memory (not a host buffer at
+// all), or anything else (pageable).
+enum class HostMem { kPinned, kDevice, kPageable };
+HostMem host_mem(const void *p) {
     hipPointerAttribute_t a{};
     const hipError_t e = hipPointerGetAttributes(&a, p);
     (void)hipGetLastError();   // an unregistered pointer may leave its error behind
-    return e == hipSuccess && a.type == hipMemoryTypeHost;
+    if (e != hipSuccess) return HostMem::kPageable;
+    if (a.type == hipMemoryTypeHost) return HostMem::kPinned;
+    if (a.type == hipMemoryTypeDevice) return HostMem::kDevice;
+    return HostMem::kPageable;
 }
 
 }  // namespace
@@ -1074,7 +1080,9 @@ hwr_status route_host_chunks(hwr_ctx *c, const hwr_query_batch *q, hwr_route_res
     const int N = c->N, M = c->M, D = c->D;
     hipStream_t s = c->stream, cs = c->cstream;
     const size_t emb_bytes = static_cast<size_t>(q->n) * D * esz;
-    const bool staged_copy = emb_bytes >= kPageMinBytes && !host_pinned(q->emb) && page_ring(c);
+    const HostMem em = host_mem(q->emb);
+    if (em == HostMem::kDevice) return fail(c, HWR_ERR_INVALID_ARG, "HWR_MEM_HOST batch with a device pointer");
+    const bool staged_copy = emb_bytes >= kPageMinBytes && em == HostMem::kPageable && page_ring(c);
     auto upload = [&](int off) -> hwr_status {
         const int cn = std::min(c->max_chunk, q->n - off);
         hwr_ctx::InStage &h = c->hin[(off / c->max_chunk) & 1];

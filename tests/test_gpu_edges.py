@@ -62,6 +62,18 @@ def test_bad_host_queries_rejected():
     slo[1] = -1.0
     with pytest.raises(hwr.HwrError):
         r.route_host(qs.emb_bits, qs.input_len, qs.expected_out_len, slo)
+    # a device buffer passed as host memory (the C ABI, past the binding's own
+    # checks) is rejected before anything reads it
+    import ctypes as C
+    import torch
+    emb_dev = torch.from_numpy(qs.emb_bits.view(np.int16)).to("cuda:0")
+    il, no, slo = (np.ascontiguousarray(x) for x in (qs.input_len, qs.expected_out_len, qs.slo_s))
+    choice = np.zeros(qs.n, np.int32)
+    b = hwr.hwr_query_batch(qs.n, hwr.HWR_MEM_HOST, emb_dev.data_ptr(), il.ctypes.data, no.ctypes.data,
+                            slo.ctypes.data)
+    res = hwr.hwr_route_result(choice=choice.ctypes.data)
+    assert hwr.load().hwr_route_batch(r.ctx, C.byref(b), C.byref(res)) == hwr.HWR_ERR_INVALID_ARG
+    assert "device pointer" in hwr.hwr_last_error(r.ctx)
 
 
 def test_empty_batch_is_noop():
