@@ -410,6 +410,39 @@ def closed_loop_pareto(args, hwr, torch):
             "points": rows}
 
 
+def host_batches(args, hwr, torch, w):
+    """Host-memory batches (HWR_MEM_HOST) of the first `--host-chunks` C5
+    chunks, PCIe-inclusive (never `value`): the same queries routed from
+    pageable and from pinned host memory, best of three calls each; both
+    give the same bits."""
+    sp, k = w["sp"], args.host_chunks
+    n = k * sp.n_queries
+    emb = w["emb"][:n].cpu().numpy().view(np.uint16)
+    il, no, slo = (w[x][:n].cpu().numpy() for x in ("il", "no", "slo"))
+    r = hwr.Router.from_problem(w["pb"], max_chunk=sp.n_queries)
+    r.update(w["st"])
+    res, outs = {}, {}
+    pin = lambda x: torch.from_numpy(np.ascontiguousarray(x)).pin_memory().numpy()
+    for name, arrays in (("pageable", (emb, il, no, slo)),
+                         ("pinned", (pin(emb.view(np.int16)).view(np.uint16), pin(il), pin(no), pin(slo)))):
+        r.route_host(*(a[:sp.n_queries] for a in arrays))       # first use: staging set up
+        best = None
+        for _ in range(3):
+            t0 = time.perf_counter()
+            outs[name] = r.route_host(*arrays)
+            dt = time.perf_counter() - t0
+            best = dt if best is None else min(best, dt)
+        res[name] = {"ms": best * 1e3, "candidates_per_s": n * sp.n_deployments / best,
+                     "embedding_gb_per_s": emb.nbytes / best / 1e9}
+        log(f"host batch ({name}): {n} queries in {best * 1e3:.1f} ms, {res[name]['candidates_per_s']:.3e} "
+            f"candidates/s, {res[name]['embedding_gb_per_s']:.1f} GB/s of embeddings")
+    r.close()
+    assert all(np.array_equal(outs["pageable"][x], outs["pinned"][x]) for x in outs["pinned"])
+    res["workload"] = f"{k} C5 chunks ({n} queries x {sp.n_deployments} pairs, {emb.nbytes / 1e6:.0f} MB of embeddings)"
+    res["timing"] = "host clock around hwr_route_batch (HWR_MEM_HOST), upload and copy-back included"
+    return res
+
+
 def _idle_state(w, hwr):
     """The monitor's first snapshot of an idle pool (what the simulation
     starts from), for the quality-only batch before a run."""
@@ -536,6 +569,8 @@ def main() -> int:
                     help="steps of the staged pipeline (gather / epilogue HBM figures); 0 skips it")
     ap.add_argument("--c4-calls", type=int, default=10000)
     ap.add_argument("--cpu-sample", type=int, default=1024)
+    ap.add_argument("--host-chunks", type=int, default=4,
+                    help="C5 chunks routed from host memory, pageable and pinned (0: skip)")
     ap.add_argument("--batch-calls", type=int, default=200,
                     help="timed calls per workload for the C1-C3 batch latencies (0: skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -610,6 +645,7 @@ def main() -> int:
             f"(graph launch) p50 {single_graph['p50_us']:.1f} us p99 {single_graph['p99_us']:.1f} us; "
             f"(resident) p50 {single_res['p50_us']:.1f} us p99 {single_res['p99_us']:.1f} us")
     batch = batch_latency(args, S, hwr, torch) if args.batch_calls > 0 else None
+    hostb = host_batches(args, hwr, torch, w) if args.host_chunks > 0 else None
     sim = None if args.no_sim else closed_loop(args, hwr, torch)
     pareto = None if args.no_sim or not args.pareto_weights else closed_loop_pareto(args, hwr, torch)
     cpu = None if args.no_cpu_baseline else cpu_baseline(w["pb"], w["st"], w["sample"], w["sp"], w["sample_wide"])
@@ -622,7 +658,8 @@ def main() -> int:
         "single_query": single, "single_query_graph_launch": single_graph,
         "single_query_resident": single_res, "single_query_launch_floor": floor,
         "step_ms": res["step_ms"], "quality_roofline": res["quality_roofline"], "stages": res["stages"],
-        "staged_pipeline": staged, "ceilings": ceilings, "batch_latency": batch, "closed_loop": sim, "closed_loop_pareto": pareto,
+        "staged_pipeline": staged, "ceilings": ceilings, "batch_latency": batch, "host_batches": hostb,
+        "closed_loop": sim, "closed_loop_pareto": pareto,
     }
     print(json.dumps(line), flush=True)
     return 0
