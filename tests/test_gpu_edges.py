@@ -375,12 +375,14 @@ def test_staged_epilogue_unaligned_candidate_buffers():
 
 def test_contexts_on_threads_are_independent():
     """Three contexts, each created and used by its own host thread on its
-    own stream at the same time (a fused host batch, a staged host batch,
-    a run of single queries), give the same bits as each context alone."""
+    own stream at the same time (a fused and a staged host batch, each over
+    16 MB of pageable embeddings, so each context runs its own pinned ring and
+    copy threads, and a run of single queries), give the same bits as each
+    context alone."""
     import threading
     import torch
     work = []
-    for name, seed, n, pipe in (("C2", 40, 3000, "fused"), ("C3", 41, 2000, "staged"), ("C4", 42, 40, "fused")):
+    for name, seed, n, pipe in (("C2", 40, 12000, "fused"), ("C3", 41, 9000, "staged"), ("C4", 42, 40, "fused")):
         sp, pb, st, qs = _case(name, seed=seed, n_queries=n)
         work.append((pb, st, qs, pipe, name == "C4"))
 
