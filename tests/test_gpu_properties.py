@@ -9,6 +9,8 @@ bounds every candidate meets.  Every example must pass the acceptance rule
 of tests/parity.py, and the decision step must be exact: given the GPU's own
 predictions, the oracle's Eq. 2 / Eq. 3 step reproduces every decision bit
 for bit."""
+import os
+
 import numpy as np
 import pytest
 from hypothesis import HealthCheck, given, settings
@@ -98,8 +100,13 @@ def _exact(out, pb, qs, sp):
     assert np.array_equal(out["e2e_s"].view(np.int32), d["e2e_s"].view(np.int32))
 
 
-@settings(max_examples=48, derandomize=True, deadline=None, database=None,
-          suppress_health_check=[HealthCheck.too_slow, HealthCheck.data_too_large])
+# HWR_PROPERTY_EXAMPLES=n: n random examples instead of the 48 derandomized
+# ones (a longer sweep run by hand)
+_EXAMPLES = int(os.environ.get("HWR_PROPERTY_EXAMPLES", "0")) or 48
+
+
+@settings(max_examples=_EXAMPLES, derandomize="HWR_PROPERTY_EXAMPLES" not in os.environ, deadline=None,
+          database=None, suppress_health_check=[HealthCheck.too_slow, HealthCheck.data_too_large])
 @given(c=cases())
 def test_random_problems_match_the_oracle(c):
     sp, pb, st, qs = _problem(c)
