@@ -27,6 +27,13 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
+# The HIP runtime's replay of captured graphs: with its packet capture off, a
+# one-kernel graph (the single-query graph launch mode) launches about 5 us
+# sooner on this stack.  Read when the runtime starts, so set before torch is
+# imported; an explicit setting in the environment is kept.
+GRAPH_ENV = ("DEBUG_CLR_GRAPH_PACKET_CAPTURE", "0")
+os.environ.setdefault(*GRAPH_ENV)
+
 METRIC = "routing candidates scored/sec (query×deployment) at 1 MI355X; p50 1-query route µs"
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
@@ -630,6 +637,8 @@ def main() -> int:
                 with_achievable(staged[k], ceilings)
     single = None if args.no_single else single_query(args, S, hwr, torch)
     single_graph = None if args.no_single else single_query(args, S, hwr, torch, hwr.HWR_FLAG_GRAPH)
+    if single_graph:
+        single_graph["runtime_env"] = f"{GRAPH_ENV[0]}={os.environ.get(GRAPH_ENV[0])}"
     single_res = None if args.no_single else single_query(args, S, hwr, torch, hwr.HWR_FLAG_RESIDENT)
     floor = None
     if not args.no_single:
@@ -638,7 +647,8 @@ def main() -> int:
         fp, fg = hwr.hwr_probe_launch_floor(0, False, 2000), hwr.hwr_probe_launch_floor(0, True, 2000)
         floor = {"plain_launch": {"p50_us": fp[0], "p99_us": fp[1]},
                  "graph_launch": {"p50_us": fg[0], "p99_us": fg[1]},
-                 "probe": "hwr_probe_launch_floor: one wave echoes a pinned request number, 2000 calls"}
+                 "probe": "hwr_probe_launch_floor: one wave echoes a pinned request number, 2000 calls",
+                 "runtime_env": f"{GRAPH_ENV[0]}={os.environ.get(GRAPH_ENV[0])}"}
         log(f"launch floor: plain p50 {fp[0]:.1f} us, graph p50 {fg[0]:.1f} us")
     if single:
         log(f"single query (kernel launch) p50 {single['p50_us']:.1f} us p99 {single['p99_us']:.1f} us; "

@@ -207,7 +207,9 @@ hwr_status hwr_update_hw_state(hwr_ctx *ctx, const hwr_hw_state *state, int32_t 
  * than max_chunk run as successive chunks on the context's stream.  A single
  * query in host memory takes a latency path: one kernel launch (or, with
  * HWR_FLAG_GRAPH, one launch of a graph holding that kernel, captured on the
- * first call) on a private stream of the context, reading the query and the
+ * first call; on ROCm 7 such a launch is about 5 us faster with the runtime's
+ * graph packet capture off, DEBUG_CLR_GRAPH_PACKET_CAPTURE=0 in the
+ * environment before the runtime starts) on a private stream of the context, reading the query and the
  * newest state from pinned host memory and writing the decision there; it
  * does not wait for batches still enqueued on the context's stream.  With
  * HWR_FLAG_RESIDENT, that kernel stays on the device between calls instead
