@@ -275,11 +275,13 @@ hipError_t launch_gather(const GatherArgs &a, hipStream_t s) {
 // keys through LDS (unique: they hold the pair index), and the wave holding
 // the largest writes the outputs.  DBG also writes the caller's
 // per-candidate outputs, [query][pair].  The predictions are read with
-// non-temporal loads (each is read once), and the first pair step's loads
-// are issued before the LDS staging.  Shape measured at 65,536 x 256 (same
-// box): two queries per lane and eight waves 31.6 us; four and sixteen
-// 35.2 us; four and four 58.8 us; the two loading changes then took the
-// chosen shape to 29.0 us.
+// non-temporal loads (each is read once), the first pair step's loads are
+// issued before the LDS staging, and each later step's before the previous
+// one is decided.  Shape measured at 65,536 x 256 (same box): two queries
+// per lane and eight waves 31.6 us; four and sixteen 35.2 us; four and four
+// 58.8 us; the two early loads took the chosen shape to 29.0 us and the
+// step-ahead loads to 27.4 us (four pairs per step instead of two: 29.0 us
+// without them, 31.3 us with).
 constexpr int kEpiQL = 2;                  // queries per lane
 typedef f32x2 EpiVec;                      // a lane's values of one pair: kEpiQL floats
 constexpr int kEpiQB = 64 * kEpiQL;        // queries per workgroup
@@ -347,16 +349,21 @@ __global__ __launch_bounds__(kEpiThreads) void k_epilogue(EpilogueArgs a) {
         }
         for (int d0 = wave; d0 < a.N; d0 += kEpiW * kEpiUnroll) {
             EpiVec tv[kEpiUnroll], pv[kEpiUnroll], nv[kEpiUnroll];
-            if (d0 == wave && kw == 0) {
 #pragma unroll
-                for (int u = 0; u < kEpiUnroll; ++u) {
-                    tv[u] = t0[u];
-                    pv[u] = p0[u];
-                    if constexpr (PN) nv[u] = v0[u];
-                }
-            } else {
-                load_step(d0, tv, pv, nv);
+            for (int u = 0; u < kEpiUnroll; ++u) {
+                tv[u] = t0[u];
+                pv[u] = p0[u];
+                if constexpr (PN) nv[u] = v0[u];
             }
+            // request the next step before deciding this one: this weight's
+            // next pairs, else the next weight's first
+            int dn = d0 + kEpiW * kEpiUnroll;
+            bool more = dn < a.N;
+            if (!more && kw + 1 < nw) {
+                dn = wave;
+                more = true;
+            }
+            if (more) load_step(dn, t0, p0, v0);
 #pragma unroll
             for (int u = 0; u < kEpiUnroll; ++u) {
                 const int d = d0 + kEpiW * u;
