@@ -70,10 +70,13 @@ extern "C" {
 
 typedef struct hwr_ctx hwr_ctx;   /* opaque, owned by the library */
 
+/* Every function returns a status; none lets a C++ exception reach the
+ * caller (a host allocation or a host thread that fails is HWR_ERR_OOM). */
 typedef enum {
     HWR_OK = 0,
     HWR_ERR_INVALID_ARG = -1,     /* bad pointer, size, id or value           */
-    HWR_ERR_OOM = -2,             /* device or pinned host allocation failed  */
+    HWR_ERR_OOM = -2,             /* device, pinned or host memory, or a host
+                                     thread, could not be obtained           */
     HWR_ERR_HIP = -3,             /* HIP runtime error (incl. no device)      */
     HWR_ERR_STATE = -4,           /* route before the first state update      */
     HWR_ERR_UNSUPPORTED = -5      /* valid but unsupported shape / dtype      */

@@ -16,6 +16,7 @@
 #include <thread>
 #include <vector>
 
+#include "c_boundary.hpp"
 #include "hwr_internal.hpp"
 
 using namespace hwr;
@@ -82,16 +83,14 @@ constexpr size_t kPageMinBytes = size_t(16) << 20;   // smaller batches keep the
 class CopyPool {
   public:
     explicit CopyPool(int threads) {
-        for (int i = 0; i < threads; ++i) workers_.emplace_back([this] { serve(); });
-    }
-    ~CopyPool() {
-        {
-            std::lock_guard<std::mutex> l(mu_);
-            stop_ = true;
+        try {
+            for (int i = 0; i < threads; ++i) workers_.emplace_back([this] { serve(); });
+        } catch (...) {
+            stop();                   // a thread could not start: join those that did
+            throw;
         }
-        wake_.notify_all();
-        for (std::thread &t : workers_) t.join();
     }
+    ~CopyPool() { stop(); }
     void copy(void *dst, const void *src, size_t bytes) {
         const size_t parts = workers_.size() + 1;
         const size_t piece = std::max<size_t>(size_t(1) << 20, (bytes / parts + 4095) & ~size_t(4095));
@@ -112,6 +111,14 @@ class CopyPool {
     }
 
   private:
+    void stop() {
+        {
+            std::lock_guard<std::mutex> l(mu_);
+            stop_ = true;
+        }
+        wake_.notify_all();
+        for (std::thread &t : workers_) t.join();
+    }
     void work() {
         for (;;) {
             char *d;
@@ -598,6 +605,8 @@ void release(hwr_ctx *c) {
     delete c;
 }
 
+hwr_status init_ctx(hwr_ctx *c, const hwr_config *cfg, const hipDeviceProp_t &prop, hwr_ctx **out);
+
 hwr_status init_impl(const hwr_config *cfg, hwr_ctx **out) {
     hwr_status st = check_config(cfg);
     if (st != HWR_OK) return st;
@@ -612,6 +621,16 @@ hwr_status init_impl(const hwr_config *cfg, hwr_ctx **out) {
         return fail(nullptr, HWR_ERR_UNSUPPORTED, std::string("library is built for gfx950, device is ") + prop.gcnArchName);
 
     hwr_ctx *c = new hwr_ctx();
+    try {
+        return init_ctx(c, cfg, prop, out);
+    } catch (...) {
+        release(c);                   // a host allocation failed part-way: nothing is left behind
+        throw;
+    }
+}
+
+// Fills a new context; on an error it releases it (bail).
+hwr_status init_ctx(hwr_ctx *c, const hwr_config *cfg, const hipDeviceProp_t &prop, hwr_ctx **out) {
     c->dev = cfg->device;
     c->stream = static_cast<hipStream_t>(cfg->stream);
     c->M = cfg->n_models;
@@ -1040,7 +1059,18 @@ bool page_ring(hwr_ctx *c) {
         }
     }
     const unsigned hw = std::thread::hardware_concurrency();
-    c->copier = std::make_unique<CopyPool>(static_cast<int>(std::min(7u, std::max(1u, hw / 2))));
+    try {
+        c->copier = std::make_unique<CopyPool>(static_cast<int>(std::min(7u, std::max(1u, hw / 2))));
+    } catch (const std::exception &) {
+        // no copy threads: pageable batches take the direct copies
+        for (auto &t : c->pslot) {
+            (void)hipHostFree(t.buf);
+            (void)hipEventDestroy(t.done);
+            t = hwr_ctx::PageSlot{};
+        }
+        c->page_failed = true;
+        return false;
+    }
     return true;
 }
 
@@ -1374,19 +1404,16 @@ Workspace scratch_workspace(const hwr_ctx *c) {
     return off <= kScratchBytes ? w : Workspace{};
 }
 
-}  // namespace
-
-// ==================================================================== C ABI
-extern "C" {
-
-hwr_status hwr_init(const hwr_config *cfg, hwr_ctx **out) {
+// Bodies of the exported functions below, which run them through
+// c_boundary (no exception reaches the caller).
+hwr_status init_entry(const hwr_config *cfg, hwr_ctx **out) {
     if (!out) return fail(nullptr, HWR_ERR_INVALID_ARG, "out is NULL");
     *out = nullptr;
     g_init_error.clear();
     return init_impl(cfg, out);
 }
 
-hwr_status hwr_update_hw_state(hwr_ctx *c, const hwr_hw_state *state, int32_t n) {
+hwr_status update_hw_state(hwr_ctx *c, const hwr_hw_state *state, int32_t n) {
     if (!c) return fail(nullptr, HWR_ERR_INVALID_ARG, "ctx is NULL");
     if (!state) return fail(c, HWR_ERR_INVALID_ARG, "state is NULL");
     if (n != c->N) return fail(c, HWR_ERR_INVALID_ARG, "state count must equal n_deployments");
@@ -1419,7 +1446,7 @@ hwr_status hwr_update_hw_state(hwr_ctx *c, const hwr_hw_state *state, int32_t n)
     return HWR_OK;
 }
 
-hwr_status hwr_route_batch(hwr_ctx *c, const hwr_query_batch *q, hwr_route_result *r) {
+hwr_status route_batch(hwr_ctx *c, const hwr_query_batch *q, hwr_route_result *r) {
     hwr_status st = check_route_args(c, q, r);
     if (st != HWR_OK || q->n == 0) return st;
     HWR_HIP(c, hipSetDevice(c->dev));
@@ -1449,7 +1476,7 @@ hwr_status hwr_route_batch(hwr_ctx *c, const hwr_query_batch *q, hwr_route_resul
     return route_host(c, q, r);
 }
 
-hwr_status hwr_route_batch_static(hwr_ctx *c, const hwr_query_batch *q, hwr_route_result *r) {
+hwr_status route_batch_static(hwr_ctx *c, const hwr_query_batch *q, hwr_route_result *r) {
     hwr_status st = check_route_args(c, q, r);
     if (st != HWR_OK || q->n == 0) return st;
     if (q->mem != HWR_MEM_DEVICE)
@@ -1477,14 +1504,7 @@ hwr_status hwr_route_batch_static(hwr_ctx *c, const hwr_query_batch *q, hwr_rout
     return st;
 }
 
-void hwr_free(hwr_ctx *c) { release(c); }
-
-const char *hwr_last_error(const hwr_ctx *c) {
-    if (c) return c->err.c_str();
-    return g_init_error.c_str();
-}
-
-hwr_status hwr_profile_enable(hwr_ctx *c, int32_t enable) {
+hwr_status profile_enable(hwr_ctx *c, int32_t enable) {
     if (!c) return fail(nullptr, HWR_ERR_INVALID_ARG, "ctx is NULL");
     if (enable < 0) return fail(c, HWR_ERR_INVALID_ARG, "enable must be >= 0");
     c->prof = enable != 0;
@@ -1493,7 +1513,7 @@ hwr_status hwr_profile_enable(hwr_ctx *c, int32_t enable) {
     return HWR_OK;
 }
 
-hwr_status hwr_profile_read(hwr_ctx *c, hwr_kernel_times *out, int32_t reset) {
+hwr_status profile_read(hwr_ctx *c, hwr_kernel_times *out, int32_t reset) {
     if (!c || !out) return fail(c, HWR_ERR_INVALID_ARG, "ctx or out is NULL");
     hwr_status st = drain_timing(c);
     if (st != HWR_OK) return st;
@@ -1508,6 +1528,47 @@ hwr_status hwr_profile_read(hwr_ctx *c, hwr_kernel_times *out, int32_t reset) {
         }
     }
     return HWR_OK;
+}
+}  // namespace
+
+// ==================================================================== C ABI
+extern "C" {
+
+hwr_status hwr_init(const hwr_config *cfg, hwr_ctx **out) {
+    return c_boundary([&] { return init_entry(cfg, out); },
+                      [](const char *m) { fail(nullptr, HWR_ERR_OOM, m); });
+}
+
+hwr_status hwr_update_hw_state(hwr_ctx *c, const hwr_hw_state *state, int32_t n) {
+    return c_boundary([&] { return update_hw_state(c, state, n); },
+                      [&](const char *m) { fail(c, HWR_ERR_OOM, m); });
+}
+
+hwr_status hwr_route_batch(hwr_ctx *c, const hwr_query_batch *q, hwr_route_result *r) {
+    return c_boundary([&] { return route_batch(c, q, r); },
+                      [&](const char *m) { fail(c, HWR_ERR_OOM, m); });
+}
+
+hwr_status hwr_route_batch_static(hwr_ctx *c, const hwr_query_batch *q, hwr_route_result *r) {
+    return c_boundary([&] { return route_batch_static(c, q, r); },
+                      [&](const char *m) { fail(c, HWR_ERR_OOM, m); });
+}
+
+void hwr_free(hwr_ctx *c) { release(c); }
+
+const char *hwr_last_error(const hwr_ctx *c) {
+    if (c) return c->err.c_str();
+    return g_init_error.c_str();
+}
+
+hwr_status hwr_profile_enable(hwr_ctx *c, int32_t enable) {
+    return c_boundary([&] { return profile_enable(c, enable); },
+                      [&](const char *m) { fail(c, HWR_ERR_OOM, m); });
+}
+
+hwr_status hwr_profile_read(hwr_ctx *c, hwr_kernel_times *out, int32_t reset) {
+    return c_boundary([&] { return profile_read(c, out, reset); },
+                      [&](const char *m) { fail(c, HWR_ERR_OOM, m); });
 }
 
 }  // extern "C"

@@ -13,6 +13,8 @@
 #include <string>
 #include <vector>
 
+#include "c_boundary.hpp"
+
 namespace {
 
 thread_local std::string g_sim_err = "no error";
@@ -95,10 +97,8 @@ hwr_status validate(const hwr_ctx *ctx, const hwr_sim_config *cfg, const hwr_sim
     return HWR_OK;
 }
 
-}  // namespace
-
-extern "C" hwr_status hwr_sim_run(hwr_ctx *ctx, const hwr_sim_config *cfg, const hwr_sim_requests *rq,
-                                  hwr_sim_router_fn router, void *user, hwr_sim_result *res) {
+hwr_status sim_run(hwr_ctx *ctx, const hwr_sim_config *cfg, const hwr_sim_requests *rq,
+                   hwr_sim_router_fn router, void *user, hwr_sim_result *res) {
     hwr_status st = validate(ctx, cfg, rq, router, res);
     if (st != HWR_OK) return st;
     const int N = cfg->n_pairs, G = cfg->n_gpus, R = rq->n;
@@ -344,6 +344,14 @@ extern "C" hwr_status hwr_sim_run(hwr_ctx *ctx, const hwr_sim_config *cfg, const
     if (res->finish_us) std::copy(finish.begin(), finish.end(), res->finish_us);
     g_sim_err = "no error";
     return HWR_OK;
+}
+
+}  // namespace
+
+extern "C" hwr_status hwr_sim_run(hwr_ctx *ctx, const hwr_sim_config *cfg, const hwr_sim_requests *rq,
+                                  hwr_sim_router_fn router, void *user, hwr_sim_result *res) {
+    return hwr::c_boundary([&] { return sim_run(ctx, cfg, rq, router, user, res); },
+                           [](const char *m) { g_sim_err = m; });
 }
 
 extern "C" const char *hwr_sim_last_error(void) { return g_sim_err.c_str(); }

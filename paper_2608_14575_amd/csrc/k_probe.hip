@@ -10,6 +10,7 @@
 #include <cstdint>
 #include <vector>
 
+#include "c_boundary.hpp"
 #include "hwr_probe.h"
 
 namespace {
@@ -150,10 +151,8 @@ hipError_t median_ms(Launch launch, int reps, float *ms) {
     return e;
 }
 
-}  // namespace
-
-extern "C" hwr_status hwr_probe_mfma_bf16(int32_t device, int32_t waves_per_simd, int32_t iters, int32_t reps,
-                                          double *tflops, double *clock_mhz) {
+hwr_status probe_mfma_bf16(int32_t device, int32_t waves_per_simd, int32_t iters, int32_t reps,
+                           double *tflops, double *clock_mhz) {
     if (!tflops || device < 0 || waves_per_simd < 1 || waves_per_simd > 2 || iters < 1 || reps < 1 || reps > 64)
         return HWR_ERR_INVALID_ARG;
     DeviceScope scope(device);
@@ -207,8 +206,8 @@ extern "C" hwr_status hwr_probe_mfma_bf16(int32_t device, int32_t waves_per_simd
     return HWR_OK;
 }
 
-extern "C" hwr_status hwr_probe_hbm_read(int32_t device, const void *buf, uint64_t bytes, int32_t waves_per_simd,
-                                         int32_t reps, double *gbps) {
+hwr_status probe_hbm_read(int32_t device, const void *buf, uint64_t bytes, int32_t waves_per_simd,
+                          int32_t reps, double *gbps) {
     if (!gbps || !buf || device < 0 || bytes == 0 || bytes % 16 != 0 ||
         reinterpret_cast<uintptr_t>(buf) % 16 != 0 || waves_per_simd < 1 || waves_per_simd > 8 || reps < 1 ||
         reps > 64)
@@ -238,8 +237,8 @@ extern "C" hwr_status hwr_probe_hbm_read(int32_t device, const void *buf, uint64
     return HWR_OK;
 }
 
-extern "C" hwr_status hwr_probe_hbm_write(int32_t device, void *buf, uint64_t bytes, int32_t waves_per_simd,
-                                          int32_t reps, double *gbps) {
+hwr_status probe_hbm_write(int32_t device, void *buf, uint64_t bytes, int32_t waves_per_simd,
+                           int32_t reps, double *gbps) {
     if (!gbps || !buf || device < 0 || bytes == 0 || bytes % 16 != 0 ||
         reinterpret_cast<uintptr_t>(buf) % 16 != 0 || waves_per_simd < 1 || waves_per_simd > 8 || reps < 1 ||
         reps > 64)
@@ -265,8 +264,8 @@ extern "C" hwr_status hwr_probe_hbm_write(int32_t device, void *buf, uint64_t by
     return HWR_OK;
 }
 
-extern "C" hwr_status hwr_probe_launch_floor(int32_t device, int32_t use_graph, int32_t calls, double *p50_us,
-                                             double *p99_us) {
+hwr_status probe_launch_floor(int32_t device, int32_t use_graph, int32_t calls, double *p50_us,
+                              double *p99_us) {
     if (!p50_us || !p99_us || device < 0 || (use_graph != 0 && use_graph != 1) || calls < 1 || calls > 100000)
         return HWR_ERR_INVALID_ARG;
     DeviceScope scope(device);
@@ -340,4 +339,30 @@ extern "C" hwr_status hwr_probe_launch_floor(int32_t device, int32_t use_graph, 
     *p50_us = us[us.size() / 2];
     *p99_us = us[std::min(us.size() - 1, static_cast<size_t>(0.99 * us.size()))];
     return HWR_OK;
+}
+
+}  // namespace
+
+extern "C" hwr_status hwr_probe_mfma_bf16(int32_t device, int32_t waves_per_simd, int32_t iters, int32_t reps,
+                                          double *tflops, double *clock_mhz) {
+    return hwr::c_boundary([&] { return probe_mfma_bf16(device, waves_per_simd, iters, reps, tflops, clock_mhz); },
+                           [](const char *) {});
+}
+
+extern "C" hwr_status hwr_probe_hbm_read(int32_t device, const void *buf, uint64_t bytes, int32_t waves_per_simd,
+                                         int32_t reps, double *gbps) {
+    return hwr::c_boundary([&] { return probe_hbm_read(device, buf, bytes, waves_per_simd, reps, gbps); },
+                           [](const char *) {});
+}
+
+extern "C" hwr_status hwr_probe_hbm_write(int32_t device, void *buf, uint64_t bytes, int32_t waves_per_simd,
+                                          int32_t reps, double *gbps) {
+    return hwr::c_boundary([&] { return probe_hbm_write(device, buf, bytes, waves_per_simd, reps, gbps); },
+                           [](const char *) {});
+}
+
+extern "C" hwr_status hwr_probe_launch_floor(int32_t device, int32_t use_graph, int32_t calls, double *p50_us,
+                                             double *p99_us) {
+    return hwr::c_boundary([&] { return probe_launch_floor(device, use_graph, calls, p50_us, p99_us); },
+                           [](const char *) {});
 }
