@@ -91,14 +91,16 @@ def test_c3_shape_ragged_tail(pipeline):
     _report(f"C3-shape ragged {pipeline}", G.check(pb, st, qs, out))
 
 
-def test_c3_full_size_per_candidate():
-    """65,536 queries x 64 pairs in one chunk (256 workgroups: the unsplit
-    launch): every prediction and quality of every 16th query compared with
-    the oracle, and every choice of the sample under the acceptance rule."""
+@pytest.mark.parametrize("pipeline", ["fused", "staged"])
+def test_c3_full_size_per_candidate(pipeline):
+    """65,536 queries x 64 pairs in one chunk (fused: 256 workgroups, the
+    unsplit launch; staged: gather, four-tile predictor and epilogue at full
+    size): every prediction and quality of every 16th query compared with the
+    oracle, and every choice of the sample under the acceptance rule."""
     import torch
     sp = S.spec("C3")
     pb, st, qs = S.make_problem(sp, 1), S.make_state(sp, 1), S.make_queries(sp, 1)
-    r = G.make_router(pb)
+    r = G.make_router(pb, pipeline=pipeline)
     r.update(st)
     emb, il, no, slo = G.to_dev_inputs(qs, sp.dtype)
     out = G.dev_outputs(qs.n, r.N, r.M, True)
@@ -112,7 +114,7 @@ def test_c3_full_size_per_candidate():
     sub = {k: v[torch.from_numpy(idx).to(v.device)].cpu().numpy() for k, v in out.items()}
     q = qs.take(idx)
     rep = G.check_against(pb, q, sub, G.oracle_threaded(pb, st, q), query_ids=idx)
-    _report(f"C3 full, every 16th query ({idx.size} x {r.N} candidates)", rep)
+    _report(f"C3 full {pipeline}, every 16th query ({idx.size} x {r.N} candidates)", rep)
     assert rep.max_rel_ttft < 2e-3 and rep.max_rel_tpot < 2e-3
 
 
