@@ -137,18 +137,19 @@ def _c5_inputs(sp, seed, dev):
     return emb, il, no, slo, chunks
 
 
-def test_c5_full_size_per_candidate():
+@pytest.mark.parametrize("pipeline", ["fused", "staged"])
+def test_c5_full_size_per_candidate(pipeline):
     """1,048,576 queries x 256 pairs in 65,536-query chunks -- the launch
-    configuration the benchmark times (one unsplit launch per chunk).  The
-    batch is routed twice: without per-candidate outputs (the benchmark's
-    kernel form) and with them; both give identical decisions.  Every 256th
-    query across all 16 chunks (4,096 queries x 256 pairs) is compared with
-    the oracle candidate by candidate, and its choice under the acceptance
-    rule."""
+    configuration the benchmark times (fused: one unsplit launch per chunk;
+    staged: the staged pipeline's line of the benchmark).  The batch is
+    routed twice: without per-candidate outputs (the benchmark's kernel form)
+    and with them; both give identical decisions.  Every 256th query across
+    all 16 chunks (4,096 queries x 256 pairs) is compared with the oracle
+    candidate by candidate, and its choice under the acceptance rule."""
     import torch
     sp = S.spec("C5")
     pb, st = S.make_problem(sp, 5), S.make_state(sp, 5)
-    r = G.make_router(pb, max_chunk=sp.n_queries)
+    r = G.make_router(pb, max_chunk=sp.n_queries, pipeline=pipeline)
     r.update(st)
     dev = torch.device("cuda")
     emb, il, no, slo, chunks = _c5_inputs(sp, 5, dev)
@@ -171,7 +172,7 @@ def test_c5_full_size_per_candidate():
                                        for c in range(sp.n_chunks)])
                        for f in ("emb", "emb_bits", "input_len", "expected_out_len", "slo_s")))
     rep = G.check_against(pb, qsub, sub, G.oracle_threaded(pb, st, qsub), query_ids=idx)
-    _report(f"C5 full, every 256th query ({idx.size} x {r.N} candidates)", rep)
+    _report(f"C5 full {pipeline}, every 256th query ({idx.size} x {r.N} candidates)", rep)
     assert rep.max_rel_ttft < 2e-3 and rep.max_rel_tpot < 2e-3
 
 
